@@ -1,0 +1,520 @@
+/*
+ * qlstm_oracle.c -- CPU oracle for quantized LSTM acoustic-model inference.
+ *
+ * TEST INFRASTRUCTURE ONLY (see qlstm_oracle.h).  Plain loops, one function
+ * per step of the paper's method, in the paper's order and notation:
+ *
+ *   S    = 255 (8-bit scale), R = Vmax - Vmin, Q = S/R    (Section 3, "Quantizing")
+ *   V'   = round(Q V) - round(Q Vmin)                      (Section 3.1, eq. 2)
+ *   V''  = V' + round(Q Vmin)                              (Section 3.1, eq. 1)
+ *   Vc   = Va'' Vb'' / (Qa Qb)                             (Section 3.1, eq. 1)
+ *   V    = (V' + round(Q Vmin)) / Q                        (Section 3.1, eq. 3)
+ *   y    = F(R(Mult(Q(X), W')) + B)                        (Section 3.1, Fig. 1)
+ *
+ * Readings where the paper is silent (each one is listed with its reason in
+ * the project's design notes):
+ *   - Q is formed and applied in fp64; round() is round-half-up done exactly.
+ *   - A set whose range is 0, or so narrow that Q*max|V| exceeds 2^24, has its
+ *     range widened to include 0; an all-zero set gets Q = 1, zero point 0.
+ *   - Codes are clamped to [0, 255] (a guard; the clamp never fires when
+ *     rounding is exact).
+ *   - The eq. 1 numerator sum_k Va'' Vb'' is an exact int64 sum; its recovery
+ *     is ((float)sum * Qa^-1) * Qb^-1 with Q^-1 = (float)(R / S).
+ *   - Bias is added after recovery (Fig. 1), gate pre-activations are
+ *     (Wx x + b) + Wh h.
+ *   - LSTM gate order i, f, g, o; no peepholes; c = f c + i g; m = o tanh(c);
+ *     the projection (when present) is linear with no bias.
+ *   - sigmoid(x) = 1 / (1 + e^-x), tanh(x) = 2 sigmoid(2x) - 1, with e^x by
+ *     Cody-Waite reduction and a Taylor polynomial (oracle_expf), all in fp32
+ *     with IEEE division and no fused multiply-add.
+ *   - Activations are quantized per vector (one frame of one utterance).
+ *   - Softmax posteriors are computed in fp64 from the fp32 logits.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp -fPIC -shared.
+ */
+#include "qlstm_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_S 255.0 /* the 8-bit scale S of Section 3 */
+
+/* ------------------------------------------------------------------------ */
+/* Elementary functions (not given by the paper).                            */
+/* ------------------------------------------------------------------------ */
+
+/* e^x after W. J. Cody and W. Waite, "Software Manual for the Elementary
+ * Functions" (1980): x = n ln2 + r with n the nearest integer to x / ln2 and
+ * ln2 split into a short high part (n * hi is exact) and a low part, so that
+ * |r| <= ln2 / 2; e^r is the degree-7 Taylor polynomial of exp evaluated in
+ * Horner form; e^x = 2^n e^r by an exact power-of-two scaling.  The argument
+ * is clamped to [-87, 87], so every result, and 1 / (1 + e^x), is a normal
+ * float. */
+float oracle_expf(float x) {
+  const float log2e = 1.44269504088896340736f;
+  const float ln2_hi = 0.693145751953125f;        /* 15 significant bits */
+  const float ln2_lo = 1.42860682030941723212e-6f; /* ln 2 - ln2_hi      */
+  if (x != x) return x;
+  if (x > 87.0f) x = 87.0f;
+  if (x < -87.0f) x = -87.0f;
+  float n = floorf(x * log2e + 0.5f);
+  float r = x - n * ln2_hi;
+  r = r - n * ln2_lo;
+  float p = 1.0f / 5040.0f;
+  p = p * r + 1.0f / 720.0f;
+  p = p * r + 1.0f / 120.0f;
+  p = p * r + 1.0f / 24.0f;
+  p = p * r + 1.0f / 6.0f;
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  union {
+    uint32_t u;
+    float f;
+  } two_n;
+  two_n.u = (uint32_t)((int32_t)n + 127) << 23;
+  return p * two_n.f;
+}
+
+float oracle_sigmoidf(float x) { return 1.0f / (1.0f + oracle_expf(-x)); }
+
+float oracle_tanhf(float x) { return 2.0f * oracle_sigmoidf(2.0f * x) - 1.0f; }
+
+/* Elementwise over an array: fn 0 = exp, 1 = sigmoid, 2 = tanh. */
+void oracle_elementwise(int32_t fn, const float *x, float *y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i)
+    y[i] = fn == 0 ? oracle_expf(x[i]) : fn == 1 ? oracle_sigmoidf(x[i]) : oracle_tanhf(x[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Quantizer (Section 3 "Quantizing", Section 3.1 eq. 2)                     */
+/* ------------------------------------------------------------------------ */
+
+/* round(): half up, decided exactly.  floor() is exact; x - floor(x) is exact
+ * for |x| >= 1, and for -1 < x < 0 its rounding is monotone and cannot cross
+ * 0.5 (doubles just below -0.5 are 2^-53 apart), so the tie test is exact. */
+int64_t oracle_round_half_up(double x) {
+  double r = floor(x);
+  if (x - r >= 0.5) r += 1.0;
+  return (int64_t)r;
+}
+
+/* Range R, factor Q = S / R, zero point round(Q Vmin), recovery Q^-1 = R / S. */
+void oracle_qparams(float vmin_f, float vmax_f, orc_qparams *p) {
+  double vmin = (double)vmin_f, vmax = (double)vmax_f;
+  double R = vmax - vmin;
+  double amax = fabs(vmin) > fabs(vmax) ? fabs(vmin) : fabs(vmax);
+  if (R == 0.0 || ORC_S * amax > 16777216.0 * R) {
+    /* degenerate or ill-conditioned range: widen it to include 0 */
+    if (vmin > 0.0) vmin = 0.0;
+    if (vmax < 0.0) vmax = 0.0;
+    R = vmax - vmin;
+  }
+  p->vmin = vmin;
+  p->vmax = vmax;
+  p->R = R;
+  if (R == 0.0) { /* all zeros */
+    p->Q = 1.0;
+    p->z = 0;
+    p->inv_q = 1.0f;
+    return;
+  }
+  p->Q = ORC_S / R;
+  p->z = (int32_t)oracle_round_half_up(p->Q * vmin);
+  p->inv_q = (float)(R / ORC_S);
+}
+
+/* eq. 2: V' = round(Q V) - round(Q Vmin), kept within [0, S]. */
+uint8_t oracle_code(float v, const orc_qparams *p) {
+  int64_t c = oracle_round_half_up(p->Q * (double)v) - (int64_t)p->z;
+  if (c < 0) c = 0;
+  if (c > 255) c = 255;
+  return (uint8_t)c;
+}
+
+void oracle_quantize_set(const float *v, int64_t n, uint8_t *codes,
+                         orc_qparams *p, int32_t *code_sum) {
+  float vmin = 0.0f, vmax = 0.0f;
+  for (int64_t i = 0; i < n; ++i) {
+    if (i == 0 || v[i] < vmin) vmin = v[i];
+    if (i == 0 || v[i] > vmax) vmax = v[i];
+  }
+  oracle_qparams(vmin, vmax, p);
+  int64_t s = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    codes[i] = oracle_code(v[i], p);
+    s += codes[i];
+  }
+  if (code_sum) *code_sum = (int32_t)s;
+}
+
+/* Section 3.1, granularity: each of `nblocks` row blocks (e.g. the four gate
+ * matrices of an LSTM weight) is its own quantized set. */
+int oracle_quantize(const float *src, int64_t rows, int64_t cols, int32_t nblocks,
+                    uint8_t *codes, double *range, int32_t *zero, float *inv_q,
+                    int32_t *row_sums) {
+  if (rows < 0 || cols < 0 || nblocks <= 0 || rows % nblocks != 0) return -2;
+  const int64_t rpb = rows / nblocks;
+  for (int32_t blk = 0; blk < nblocks; ++blk) {
+    orc_qparams p;
+    oracle_quantize_set(src + blk * rpb * cols, rpb * cols,
+                        codes + blk * rpb * cols, &p, NULL);
+    if (range) range[blk] = p.R;
+    if (zero) zero[blk] = p.z;
+    if (inv_q) inv_q[blk] = p.inv_q;
+  }
+  if (row_sums)
+    for (int64_t r = 0; r < rows; ++r) {
+      int64_t s = 0;
+      for (int64_t k = 0; k < cols; ++k) s += codes[r * cols + k];
+      row_sums[r] = (int32_t)s;
+    }
+  return 0;
+}
+
+/* eq. 3: V = (V' + round(Q Vmin)) / Q, with 1/Q taken as the fp32 Q^-1. */
+int oracle_dequantize(const uint8_t *codes, int64_t rows, int64_t cols,
+                      int32_t nblocks, const int32_t *zero, const float *inv_q,
+                      float *dst) {
+  if (rows < 0 || cols < 0 || nblocks <= 0 || rows % nblocks != 0) return -2;
+  const int64_t rpb = rows / nblocks;
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t blk = r / rpb;
+    for (int64_t k = 0; k < cols; ++k)
+      dst[r * cols + k] =
+          (float)((int32_t)codes[r * cols + k] + zero[blk]) * inv_q[blk];
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Quantized product (Section 3.1, eq. 1) and recovery R(.)                  */
+/* ------------------------------------------------------------------------ */
+
+/* For one quantized activation vector x' (zero point zx, recovery invqx):
+ *   acc[n] = sum_k W'[n][k] x'[k]                      (8-bit products, int32)
+ *   tot    = sum_k (W'[n][k] + zW) (x'[k] + zx)        (eq. 1 numerator, V''V'')
+ *   y[n]   = ((float)tot * QW^-1) * Qx^-1               (eq. 1 denominator)   */
+static void qlinear_vec(const orc_qmat *W, const uint8_t *xc, int32_t zx,
+                        float invqx, float *y, int32_t *acc) {
+  const int64_t K = W->cols, rpb = W->rows / W->nblocks;
+  for (int64_t n = 0; n < W->rows; ++n) {
+    const uint8_t *w = W->codes + n * K;
+    const int64_t blk = n / rpb;
+    const int64_t zw = W->zero[blk];
+    int64_t a = 0, t = 0;
+    for (int64_t k = 0; k < K; ++k) {
+      a += (int64_t)w[k] * (int64_t)xc[k];
+      t += ((int64_t)w[k] + zw) * ((int64_t)xc[k] + (int64_t)zx);
+    }
+    if (acc) acc[n] = (int32_t)a;
+    y[n] = ((float)t * W->inv_q[blk]) * invqx;
+  }
+}
+
+static int qmat_ok(const orc_qmat *W) {
+  return W && W->codes && W->zero && W->inv_q && W->rows >= 0 && W->cols >= 0 &&
+         W->nblocks > 0 && W->rows % W->nblocks == 0;
+}
+
+/* Fig. 1: y = R(Mult(Q(X), W')) + B, inputs quantized on the fly. */
+int oracle_quantized_matmul(const orc_qmat *W, const float *X, int64_t m,
+                            int32_t act_gran, const float *bias, float *Y,
+                            int32_t *acc, uint8_t *x_codes, int32_t *x_zero,
+                            float *x_inv_q) {
+  if (!qmat_ok(W) || m < 0 || (act_gran != 0 && act_gran != 1)) return -2;
+  const int64_t K = W->cols, N = W->rows;
+  uint8_t *xc = (uint8_t *)malloc((size_t)(m * K > 0 ? m * K : 1));
+  int32_t *zx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(m > 0 ? m : 1));
+  float *iq = (float *)malloc(sizeof(float) * (size_t)(m > 0 ? m : 1));
+  if (act_gran == 0) { /* per tensor: the whole X is one set */
+    orc_qparams p;
+    oracle_quantize_set(X, m * K, xc, &p, NULL);
+    for (int64_t i = 0; i < m; ++i) {
+      zx[i] = p.z;
+      iq[i] = p.inv_q;
+    }
+  } else { /* per row: each activation vector is one set */
+    for (int64_t i = 0; i < m; ++i) {
+      orc_qparams p;
+      oracle_quantize_set(X + i * K, K, xc + i * K, &p, NULL);
+      zx[i] = p.z;
+      iq[i] = p.inv_q;
+    }
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < m; ++i) {
+    qlinear_vec(W, xc + i * K, zx[i], iq[i], Y + i * N, acc ? acc + i * N : NULL);
+    if (bias)
+      for (int64_t n = 0; n < N; ++n) Y[i * N + n] = Y[i * N + n] + bias[n];
+  }
+  if (x_codes) memcpy(x_codes, xc, (size_t)(m * K));
+  if (x_zero) memcpy(x_zero, zx, sizeof(int32_t) * (size_t)m);
+  if (x_inv_q) memcpy(x_inv_q, iq, sizeof(float) * (size_t)m);
+  free(xc);
+  free(zx);
+  free(iq);
+  return 0;
+}
+
+int oracle_gemm_u8(const uint8_t *A, const uint8_t *B, int32_t *C, int64_t M,
+                   int64_t N, int64_t K) {
+  if (M < 0 || N < 0 || K < 0) return -2;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < M; ++i)
+    for (int64_t j = 0; j < N; ++j) {
+      int64_t s = 0;
+      for (int64_t k = 0; k < K; ++k) s += (int64_t)A[i * K + k] * (int64_t)B[j * K + k];
+      C[i * N + j] = (int32_t)s;
+    }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Quantized LSTM layer (Section 4 architecture; Fig. 1 per matrix product)  */
+/* ------------------------------------------------------------------------ */
+
+int oracle_lstm_layer_forward(const orc_layer *L, const float *x, int64_t T,
+                              int64_t B, const float *h0, const float *c0,
+                              float *h, float *hT, float *cT,
+                              const orc_layer_taps *taps) {
+  const int64_t H = L->hidden, P = L->proj, IN = L->in;
+  const int64_t RD = P ? P : H; /* width of h */
+  if (T < 0 || B < 0 || H <= 0 || IN <= 0 || P < 0) return -2;
+  if (!qmat_ok(&L->Wx) || L->Wx.rows != 4 * H || L->Wx.cols != IN) return -2;
+  if (!qmat_ok(&L->Wh) || L->Wh.rows != 4 * H || L->Wh.cols != RD) return -2;
+  if (P && (!qmat_ok(&L->Wr) || L->Wr.rows != P || L->Wr.cols != H)) return -2;
+  if (!L->bias) return -2;
+
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t b = 0; b < B; ++b) {
+    float *hprev = (float *)calloc((size_t)RD, sizeof(float));
+    float *cprev = (float *)calloc((size_t)H, sizeof(float));
+    float *yx = (float *)malloc(sizeof(float) * (size_t)(4 * H));
+    float *yh = (float *)malloc(sizeof(float) * (size_t)(4 * H));
+    float *m = (float *)malloc(sizeof(float) * (size_t)H);
+    float *hn = (float *)malloc(sizeof(float) * (size_t)RD);
+    uint8_t *xc = (uint8_t *)malloc((size_t)IN);
+    uint8_t *hc = (uint8_t *)malloc((size_t)RD);
+    uint8_t *mc = (uint8_t *)malloc((size_t)H);
+    if (h0) memcpy(hprev, h0 + b * RD, sizeof(float) * (size_t)RD);
+    if (c0) memcpy(cprev, c0 + b * H, sizeof(float) * (size_t)H);
+
+    for (int64_t t = 0; t < T; ++t) {
+      const int64_t row = t * B + b;
+      orc_qparams px, ph;
+      /* input product: Q(x_t) on the fly, Mult, R */
+      oracle_quantize_set(x + row * IN, IN, xc, &px, NULL);
+      qlinear_vec(&L->Wx, xc, px.z, px.inv_q, yx,
+                  taps && taps->acc_x ? taps->acc_x + row * 4 * H : NULL);
+      /* recurrent product: Q(h_{t-1}), Mult, R */
+      oracle_quantize_set(hprev, RD, hc, &ph, NULL);
+      qlinear_vec(&L->Wh, hc, ph.z, ph.inv_q, yh,
+                  taps && taps->acc_h ? taps->acc_h + row * 4 * H : NULL);
+      /* biases, then the activation functions F */
+      for (int64_t j = 0; j < H; ++j) {
+        const float ai = (yx[j] + L->bias[j]) + yh[j];
+        const float af = (yx[H + j] + L->bias[H + j]) + yh[H + j];
+        const float ag = (yx[2 * H + j] + L->bias[2 * H + j]) + yh[2 * H + j];
+        const float ao = (yx[3 * H + j] + L->bias[3 * H + j]) + yh[3 * H + j];
+        const float ig = oracle_sigmoidf(ai);
+        const float fg = oracle_sigmoidf(af);
+        const float gg = oracle_tanhf(ag);
+        const float og = oracle_sigmoidf(ao);
+        const float c = (fg * cprev[j]) + (ig * gg);
+        cprev[j] = c;
+        m[j] = og * oracle_tanhf(c);
+      }
+      if (P) { /* linear projection: h = R(Mult(Q(m), Wr')) */
+        orc_qparams pm;
+        oracle_quantize_set(m, H, mc, &pm, NULL);
+        qlinear_vec(&L->Wr, mc, pm.z, pm.inv_q, hn,
+                    taps && taps->acc_r ? taps->acc_r + row * P : NULL);
+      } else {
+        memcpy(hn, m, sizeof(float) * (size_t)H);
+      }
+      memcpy(h + row * RD, hn, sizeof(float) * (size_t)RD);
+      memcpy(hprev, hn, sizeof(float) * (size_t)RD);
+      if (taps && taps->c) memcpy(taps->c + row * H, cprev, sizeof(float) * (size_t)H);
+      if (taps && (taps->h_codes || taps->h_zero || taps->h_inv_q)) {
+        orc_qparams pn;
+        oracle_quantize_set(hn, RD, hc, &pn, NULL);
+        if (taps->h_codes) memcpy(taps->h_codes + row * RD, hc, (size_t)RD);
+        if (taps->h_zero) taps->h_zero[row] = pn.z;
+        if (taps->h_inv_q) taps->h_inv_q[row] = pn.inv_q;
+      }
+    }
+    if (hT) memcpy(hT + b * RD, hprev, sizeof(float) * (size_t)RD);
+    if (cT) memcpy(cT + b * H, cprev, sizeof(float) * (size_t)H);
+    free(hprev);
+    free(cprev);
+    free(yx);
+    free(yh);
+    free(m);
+    free(hn);
+    free(xc);
+    free(hc);
+    free(mc);
+  }
+  return 0;
+}
+
+/* softmax of one row of fp32 logits, in fp64 */
+static void softmax_row(const float *l, int64_t S, float *p) {
+  double mx = (double)l[0];
+  for (int64_t s = 1; s < S; ++s)
+    if ((double)l[s] > mx) mx = (double)l[s];
+  double sum = 0.0;
+  for (int64_t s = 0; s < S; ++s) sum += exp((double)l[s] - mx);
+  for (int64_t s = 0; s < S; ++s) p[s] = (float)(exp((double)l[s] - mx) / sum);
+}
+
+/* Section 4: stacked LSTM layers, then the output layer, quantized as every
+ * other layer ('quant-all', Section 5), then softmax. */
+int oracle_acoustic_model_forward(const orc_model *M, const float *feats,
+                                  int64_t T, int64_t B, float *post,
+                                  const orc_layer_taps *layer_taps,
+                                  int32_t *acc_y, float *logits) {
+  if (!M || M->nlayers <= 0 || !M->layers || !qmat_ok(&M->Wy) || !M->by) return -2;
+  const float *x = feats;
+  float *prev = NULL;
+  int64_t width = M->layers[0].in;
+  for (int32_t l = 0; l < M->nlayers; ++l) {
+    const orc_layer *L = &M->layers[l];
+    if (L->in != width) return -2;
+    const int64_t RD = L->proj ? L->proj : L->hidden;
+    float *hl = (float *)malloc(sizeof(float) * (size_t)(T * B * RD > 0 ? T * B * RD : 1));
+    int rc = oracle_lstm_layer_forward(L, x, T, B, NULL, NULL, hl, NULL, NULL,
+                                       layer_taps ? &layer_taps[l] : NULL);
+    free(prev);
+    if (rc) {
+      free(hl);
+      return rc;
+    }
+    prev = hl;
+    x = hl;
+    width = RD;
+  }
+  if (M->Wy.cols != width) {
+    free(prev);
+    return -2;
+  }
+  const int64_t S = M->Wy.rows;
+#pragma omp parallel for schedule(static)
+  for (int64_t row = 0; row < T * B; ++row) {
+    uint8_t *xc = (uint8_t *)malloc((size_t)width);
+    float *lg = (float *)malloc(sizeof(float) * (size_t)S);
+    orc_qparams p;
+    oracle_quantize_set(x + row * width, width, xc, &p, NULL);
+    qlinear_vec(&M->Wy, xc, p.z, p.inv_q, lg, acc_y ? acc_y + row * S : NULL);
+    for (int64_t s = 0; s < S; ++s) lg[s] = lg[s] + M->by[s];
+    if (logits) memcpy(logits + row * S, lg, sizeof(float) * (size_t)S);
+    softmax_row(lg, S, post + row * S);
+    free(xc);
+    free(lg);
+  }
+  free(prev);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Unquantized fp32 model (the 'match' condition of Section 5)               */
+/* ------------------------------------------------------------------------ */
+
+static void flinear_vec(const float *W, int64_t N, int64_t K, const float *x,
+                        float *y) {
+  for (int64_t n = 0; n < N; ++n) {
+    double s = 0.0;
+    for (int64_t k = 0; k < K; ++k) s += (double)W[n * K + k] * (double)x[k];
+    y[n] = (float)s;
+  }
+}
+
+int oracle_lstm_layer_forward_f32(const orc_layer_f32 *L, const float *x,
+                                  int64_t T, int64_t B, const float *h0,
+                                  const float *c0, float *h, float *hT, float *cT) {
+  const int64_t H = L->hidden, P = L->proj, IN = L->in;
+  const int64_t RD = P ? P : H;
+  if (T < 0 || B < 0 || H <= 0 || IN <= 0 || P < 0 || !L->Wx || !L->Wh || !L->bias ||
+      (P && !L->Wr))
+    return -2;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t b = 0; b < B; ++b) {
+    float *hprev = (float *)calloc((size_t)RD, sizeof(float));
+    float *cprev = (float *)calloc((size_t)H, sizeof(float));
+    float *yx = (float *)malloc(sizeof(float) * (size_t)(4 * H));
+    float *yh = (float *)malloc(sizeof(float) * (size_t)(4 * H));
+    float *m = (float *)malloc(sizeof(float) * (size_t)H);
+    float *hn = (float *)malloc(sizeof(float) * (size_t)RD);
+    if (h0) memcpy(hprev, h0 + b * RD, sizeof(float) * (size_t)RD);
+    if (c0) memcpy(cprev, c0 + b * H, sizeof(float) * (size_t)H);
+    for (int64_t t = 0; t < T; ++t) {
+      const int64_t row = t * B + b;
+      flinear_vec(L->Wx, 4 * H, IN, x + row * IN, yx);
+      flinear_vec(L->Wh, 4 * H, RD, hprev, yh);
+      for (int64_t j = 0; j < H; ++j) {
+        const float ig = oracle_sigmoidf((yx[j] + L->bias[j]) + yh[j]);
+        const float fg = oracle_sigmoidf((yx[H + j] + L->bias[H + j]) + yh[H + j]);
+        const float gg = oracle_tanhf((yx[2 * H + j] + L->bias[2 * H + j]) + yh[2 * H + j]);
+        const float og = oracle_sigmoidf((yx[3 * H + j] + L->bias[3 * H + j]) + yh[3 * H + j]);
+        const float c = (fg * cprev[j]) + (ig * gg);
+        cprev[j] = c;
+        m[j] = og * oracle_tanhf(c);
+      }
+      if (P)
+        flinear_vec(L->Wr, P, H, m, hn);
+      else
+        memcpy(hn, m, sizeof(float) * (size_t)H);
+      memcpy(h + row * RD, hn, sizeof(float) * (size_t)RD);
+      memcpy(hprev, hn, sizeof(float) * (size_t)RD);
+    }
+    if (hT) memcpy(hT + b * RD, hprev, sizeof(float) * (size_t)RD);
+    if (cT) memcpy(cT + b * H, cprev, sizeof(float) * (size_t)H);
+    free(hprev);
+    free(cprev);
+    free(yx);
+    free(yh);
+    free(m);
+    free(hn);
+  }
+  return 0;
+}
+
+int oracle_acoustic_model_forward_f32(const orc_model_f32 *M, const float *feats,
+                                      int64_t T, int64_t B, float *post) {
+  if (!M || M->nlayers <= 0 || !M->layers || !M->Wy || !M->by) return -2;
+  const float *x = feats;
+  float *prev = NULL;
+  int64_t width = M->layers[0].in;
+  for (int32_t l = 0; l < M->nlayers; ++l) {
+    const orc_layer_f32 *L = &M->layers[l];
+    if (L->in != width) return -2;
+    const int64_t RD = L->proj ? L->proj : L->hidden;
+    float *hl = (float *)malloc(sizeof(float) * (size_t)(T * B * RD > 0 ? T * B * RD : 1));
+    int rc = oracle_lstm_layer_forward_f32(L, x, T, B, NULL, NULL, hl, NULL, NULL);
+    free(prev);
+    if (rc) {
+      free(hl);
+      return rc;
+    }
+    prev = hl;
+    x = hl;
+    width = RD;
+  }
+  const int64_t S = M->S;
+  if (S <= 0) {
+    free(prev);
+    return -2;
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t row = 0; row < T * B; ++row) {
+    float *lg = (float *)malloc(sizeof(float) * (size_t)S);
+    flinear_vec(M->Wy, S, width, x + row * width, lg);
+    for (int64_t s = 0; s < S; ++s) lg[s] = lg[s] + M->by[s];
+    softmax_row(lg, S, post + row * S);
+    free(lg);
+  }
+  free(prev);
+  return 0;
+}

@@ -1,0 +1,436 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these compares the oracle with a re-typed copy of itself: each check
+uses an exact definition (rational arithmetic, exhaustive integer products,
+fp64 BLAS on integer data), a closed form, an invariant the paper states, a
+hand-derived fixture, or an independent library (torch.nn.LSTM, scipy).
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _ulp32(x):
+    x = np.abs(np.asarray(x, np.float64)).astype(np.float32)
+    return np.spacing(x).astype(np.float64)
+
+
+# ---------------------------------------------------------------- elementary
+def test_expf_within_2ulp_of_exp(orc):
+    """Own e^x (Cody-Waite + Taylor) against fp64 exp on a dense sweep."""
+    x = np.linspace(-87.0, 87.0, 2_000_001, dtype=np.float32)
+    x = np.concatenate([x, np.float32([0.0, -0.0, 1e-30, -1e-30, 0.34657359, -0.34657359])])
+    y = orc.expf(x).astype(np.float64)
+    ref = np.exp(x.astype(np.float64))
+    err = np.abs(y - ref) / _ulp32(ref)
+    assert err.max() <= 2.0, err.max()
+
+
+def test_expf_clamps_to_normal_range(orc):
+    y = orc.expf(np.float32([-1000.0, -87.0, 87.0, 1000.0]))
+    assert np.all(np.isfinite(y)) and np.all(y >= np.finfo(np.float32).tiny)
+    assert y[0] == y[1] and y[2] == y[3]
+
+
+def test_sigmoid_tanh_close_to_fp64(orc):
+    x = np.linspace(-30.0, 30.0, 600_001, dtype=np.float32)
+    xd = x.astype(np.float64)
+    s = orc.sigmoidf(x).astype(np.float64)
+    t = orc.tanhf(x).astype(np.float64)
+    assert np.max(np.abs(s - 1.0 / (1.0 + np.exp(-xd)))) <= 1e-6
+    assert np.max(np.abs(t - np.tanh(xd))) <= 1e-6
+    # saturation stays finite and normal
+    big = orc.sigmoidf(np.float32([-200.0, 200.0]))
+    assert big[0] >= np.finfo(np.float32).tiny and big[1] == 1.0
+
+
+# ---------------------------------------------------------------- quantizer
+def test_round_half_up_matches_exact_rational(orc):
+    """round() reading: floor(x + 1/2) in exact rational arithmetic."""
+    g = json.load(open(os.path.join(GOLDEN, "quantizer_cases.json")))
+    for x, want in g["round_half_up"]:
+        assert orc.round_half_up(x) == want, x
+    rng = np.random.default_rng(1)
+    xs = np.concatenate([rng.uniform(-1e6, 1e6, 2000), rng.integers(-1000, 1000, 2000) + 0.5,
+                         np.nextafter(rng.integers(-1000, 1000, 500) + 0.5, -np.inf),
+                         np.nextafter(rng.integers(-1000, 1000, 500) + 0.5, np.inf)])
+    for x in xs:
+        assert orc.round_half_up(float(x)) == math.floor(Fraction(float(x)) + Fraction(1, 2))
+
+
+def test_hand_derived_codes(orc):
+    """Fixture codes derived by hand from eq. 2 (values chosen so Q*V is exact)."""
+    g = json.load(open(os.path.join(GOLDEN, "quantizer_cases.json")))
+    for case in g["cases"]:
+        codes, p, s = orc.quantize_set(np.float32(case["values"]))
+        assert p["Q"] == case["Q"], case
+        assert p["z"] == case["z"], case
+        assert codes.tolist() == case["codes"], case
+        assert s == sum(case["codes"])
+
+
+def _random_sets(rng, n_sets=3000):
+    for i in range(n_sets):
+        n = int(rng.integers(2, 700))
+        kind = i % 5
+        if kind == 0:
+            v = rng.standard_normal(n)
+        elif kind == 1:
+            v = rng.uniform(-0.08, 0.08, n)
+        elif kind == 2:
+            v = rng.uniform(0.2, 0.9, n)          # range not containing 0
+        elif kind == 3:
+            v = rng.normal(0, 0.02, n) * 10.0 ** rng.integers(-6, 6)
+        else:
+            v = np.tanh(rng.standard_normal(n) * 2.0)
+        yield v.astype(np.float32)
+
+
+def test_endpoints_map_to_0_and_255(orc):
+    """Section 3: V' spans [0, S]; Vmin -> 0 and Vmax -> S = 255."""
+    rng = np.random.default_rng(2)
+    for v in _random_sets(rng):
+        codes, p, _ = orc.quantize_set(v)
+        assert codes[np.argmin(v)] == 0
+        assert codes[np.argmax(v)] == 255
+
+
+def test_round_trip_within_half_step(orc):
+    """Recovery (eq. 3) of every value is within half a quantization step."""
+    rng = np.random.default_rng(3)
+    for v in _random_sets(rng, 1500):
+        codes, p, _ = orc.quantize_set(v)
+        q = orc.QMatrix(codes.reshape(1, -1), np.float64([p["R"]]), np.int32([p["z"]]),
+                        np.float32([p["inv_q"]]), np.zeros(1, np.int32), 1)
+        back = orc.dequantize(q).ravel().astype(np.float64)
+        half = 0.5 * p["R"] / 255.0
+        bound = half * (1 + 2.0 ** -20) + 2.0 ** -23 * np.max(np.abs(v))
+        assert np.max(np.abs(back - v.astype(np.float64))) <= bound
+
+
+def test_zero_recovers_exactly_when_in_range(orc):
+    """Bias-free rounding (eq. 2/3): a 0 in the set is recovered as exactly 0."""
+    rng = np.random.default_rng(4)
+    for i in range(500):
+        v = rng.standard_normal(int(rng.integers(2, 300))).astype(np.float32)
+        v[int(rng.integers(0, v.size))] = 0.0
+        codes, p, _ = orc.quantize_set(v)
+        zpos = np.flatnonzero(v == 0.0)
+        assert np.all(codes[zpos].astype(np.int64) + p["z"] == 0)
+
+
+def test_degenerate_ranges(orc):
+    codes, p, s = orc.quantize_set(np.zeros(17, np.float32))
+    assert (codes == 0).all() and p["Q"] == 1.0 and p["z"] == 0 and s == 0
+    for c in (3.25, -0.7, 1e-3):
+        codes, p, _ = orc.quantize_set(np.full(9, c, np.float32))
+        back = (codes.astype(np.int64) + p["z"]) * np.float64(p["inv_q"])
+        assert np.all(np.abs(back - c) <= 0.5 * p["R"] / 255 * (1 + 1e-6))
+    # ill-conditioned: tiny range far from 0 is widened to include 0
+    v = np.float32([1000.0, 1000.0001])
+    codes, p, _ = orc.quantize_set(v)
+    assert p["vmin"] == 0.0 and abs(p["z"]) <= 2 ** 24
+
+
+def test_matrix_blocks_are_independent(orc):
+    """Granularity (Section 3.1): each gate block is quantized on its own."""
+    rng = np.random.default_rng(5)
+    W = rng.uniform(-0.08, 0.08, (4 * 37, 53)).astype(np.float32)
+    W[37:74] *= 5.0
+    q = orc.quantize(W, 4)
+    for b in range(4):
+        blk = W[b * 37:(b + 1) * 37]
+        codes, p, _ = orc.quantize_set(blk)
+        assert np.array_equal(q.codes[b * 37:(b + 1) * 37], codes)
+        assert q.zero[b] == p["z"] and q.inv_q[b] == p["inv_q"]
+        assert q.codes[b * 37:(b + 1) * 37].min() == 0
+        assert q.codes[b * 37:(b + 1) * 37].max() == 255
+    assert np.array_equal(q.row_sums, q.codes.astype(np.int64).sum(1))
+
+
+# ---------------------------------------------------------------- products
+def test_gemm_exhaustive_k1(orc):
+    """All 256 x 256 single products of 8-bit codes."""
+    a = np.arange(256, dtype=np.uint8).reshape(256, 1)
+    c = orc.gemm_u8(a, a)
+    assert np.array_equal(c, np.outer(np.arange(256), np.arange(256)))
+
+
+def test_gemm_brute_force_small_k(orc):
+    rng = np.random.default_rng(6)
+    for K in range(1, 17):
+        A = rng.integers(0, 256, (7, K), dtype=np.uint8)
+        B = rng.integers(0, 256, (5, K), dtype=np.uint8)
+        ref = [[sum(int(A[i, k]) * int(B[j, k]) for k in range(K)) for j in range(5)]
+               for i in range(7)]
+        assert orc.gemm_u8(A, B).tolist() == ref
+
+
+def test_gemm_equals_fp64_blas_on_integers(orc):
+    """Integer data: the fp64 BLAS product is exact (partial sums < 2^53)."""
+    rng = np.random.default_rng(7)
+    A = rng.integers(0, 256, (64, 1000), dtype=np.uint8)
+    B = rng.integers(0, 256, (48, 1000), dtype=np.uint8)
+    assert np.array_equal(orc.gemm_u8(A, B), (A.astype(np.float64) @ B.T.astype(np.float64)))
+
+
+def test_qmatmul_q1_z0_special_case_is_integer_matmul(orc):
+    """Data already in [0, 255] with min 0 and max 255: Q = 1, z = 0, codes
+    equal the data, and the recovered product is the exact integer matmul."""
+    rng = np.random.default_rng(8)
+    W = rng.integers(0, 256, (40, 64)).astype(np.float32)
+    X = rng.integers(0, 256, (9, 64)).astype(np.float32)
+    W[0, 0], W[1, 1], X[0, 0], X[1, 1] = 0, 255, 0, 255
+    q = orc.quantize(W, 1)
+    assert q.zero[0] == 0 and q.inv_q[0] == 1.0
+    r = orc.quantized_matmul(q, X, act_gran=0)
+    ref = X.astype(np.float64) @ W.T.astype(np.float64)
+    assert np.array_equal(r["acc"].astype(np.float64), ref)
+    assert np.array_equal(r["Y"].astype(np.float64), ref)   # all < 2^24: exact in fp32
+
+
+def test_qmatmul_zero_point_expansion(orc):
+    """eq. 1 numerator sum (W'+zW)(x'+zx) equals its expansion
+    acc + zx sum W' + zW sum x' + K zW zx (exact integers), and the output is
+    ((float)tot * QW^-1) * Qx^-1 bit for bit; acc equals the exact integer matmul."""
+    rng = np.random.default_rng(9)
+    for gran in (0, 1):
+        W = rng.normal(0, 0.1, (4 * 24, 77)).astype(np.float32)
+        X = rng.uniform(-1, 1, (11, 77)).astype(np.float32)
+        q = orc.quantize(W, 4)
+        r = orc.quantized_matmul(q, X, act_gran=gran)
+        xc = r["x_codes"].astype(np.int64)
+        wc = q.codes.astype(np.int64)
+        acc = xc @ wc.T
+        assert np.array_equal(r["acc"], acc.astype(np.int32))
+        zW = np.repeat(q.zero.astype(np.int64), 24)
+        iW = np.repeat(q.inv_q, 24)
+        zx = r["x_zero"].astype(np.int64)
+        K = W.shape[1]
+        tot = (acc + zx[:, None] * wc.sum(1)[None, :] + zW[None, :] * xc.sum(1)[:, None]
+               + K * zW[None, :] * zx[:, None])
+        y = (tot.astype(np.float32) * iW[None, :]) * r["x_inv_q"][:, None]
+        assert np.array_equal(r["Y"], y)
+
+
+def test_qmatmul_equals_product_of_recovered_values(orc):
+    """The integer path computes sum_k W^ x^ of the recovered (eq. 3) values,
+    to within fp32 rounding of the recovery: catches dropped or mis-signed
+    zero-point terms and transposed operands."""
+    rng = np.random.default_rng(10)
+    W = rng.normal(0, 0.1, (256, 128)).astype(np.float32)
+    X = rng.uniform(-1, 1, (16, 128)).astype(np.float32)
+    q = orc.quantize(W, 1)
+    r = orc.quantized_matmul(q, X, act_gran=1)
+    What = orc.dequantize(q).astype(np.float64)
+    xq = orc.QMatrix(r["x_codes"], np.zeros(16), r["x_zero"], r["x_inv_q"],
+                     np.zeros(16, np.int32), 16)
+    Xhat = orc.dequantize(xq).astype(np.float64)
+    ref = Xhat @ What.T
+    mag = np.abs(Xhat) @ np.abs(What).T
+    assert np.all(np.abs(r["Y"] - ref) <= 4 * 2.0 ** -24 * mag + 2 * _ulp32(ref))
+
+
+@pytest.mark.parametrize("which", ["x", "w"])
+def test_qmatmul_approaches_float_product_as_range_shrinks(orc, which):
+    """Error of the dequantized product vs the float product obeys the
+    half-step bound and shrinks in proportion to the range."""
+    rng = np.random.default_rng(11)
+    W0 = rng.normal(0, 0.1, (64, 96)).astype(np.float32)
+    X0 = rng.uniform(-1, 1, (8, 96)).astype(np.float32)
+    errs = []
+    for j in range(0, 12, 2):
+        s = np.float32(2.0 ** -j)
+        W, X = (W0, X0 * s) if which == "x" else (W0 * s, X0)
+        q = orc.quantize(W, 1)
+        r = orc.quantized_matmul(q, X, act_gran=0)
+        exact = X.astype(np.float64) @ W.T.astype(np.float64)
+        eW = 0.5 * (W.max() - W.min()) / 255.0
+        eX = 0.5 * (X.max() - X.min()) / 255.0
+        bound = (np.abs(X).astype(np.float64) @ np.full((96, 64), eW) +
+                 eX * np.abs(W).astype(np.float64).sum(1)[None, :] + 96 * eW * eX)
+        err = np.abs(r["Y"] - exact)
+        assert np.all(err <= bound * 1.001 + 1e-6 * np.abs(exact) + 1e-30)
+        errs.append(err.max())
+    ratios = np.array(errs[1:]) / np.array(errs[:-1])
+    assert np.all(ratios < 0.5), ratios   # x4 smaller range -> error ~x4 smaller
+
+
+# ---------------------------------------------------------------- LSTM
+def _torch_lstm(weights_f32, x, h0=None, c0=None):
+    import torch
+    L = weights_f32
+    H = L["Wx"].shape[0] // 4
+    P = 0 if L.get("Wr") is None else L["Wr"].shape[0]
+    m = torch.nn.LSTM(L["Wx"].shape[1], H, proj_size=P, dtype=torch.float64)
+    with torch.no_grad():
+        m.weight_ih_l0.copy_(torch.from_numpy(L["Wx"].astype(np.float64)))
+        m.weight_hh_l0.copy_(torch.from_numpy(L["Wh"].astype(np.float64)))
+        m.bias_ih_l0.copy_(torch.from_numpy(L["b"].astype(np.float64)))
+        m.bias_hh_l0.zero_()
+        if P:
+            m.weight_hr_l0.copy_(torch.from_numpy(L["Wr"].astype(np.float64)))
+        B = x.shape[1]
+        R = P if P else H
+        hh = torch.zeros(1, B, R, dtype=torch.float64) if h0 is None else \
+            torch.from_numpy(h0.astype(np.float64))[None]
+        cc = torch.zeros(1, B, H, dtype=torch.float64) if c0 is None else \
+            torch.from_numpy(c0.astype(np.float64))[None]
+        out, (hT, cT) = m(torch.from_numpy(x.astype(np.float64)), (hh, cc))
+    return out.numpy(), hT[0].numpy(), cT[0].numpy()
+
+
+@pytest.mark.parametrize("proj", [0, 12])
+def test_float_lstm_matches_torch(orc, proj):
+    """The unquantized path (gate order i,f,g,o; c = f c + i g; m = o tanh c;
+    optional linear projection) against torch.nn.LSTM in fp64."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(24, 20, 1, proj=proj, seed=3)
+    L = w["layers"][0]
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((30, 3, 24)).astype(np.float32)
+    o = orc.lstm_layer_forward_f32(L, x)
+    ref, hT, cT = _torch_lstm(L, x)
+    assert np.max(np.abs(o["h"] - ref)) < 2e-6
+    assert np.max(np.abs(o["cT"] - cT)) < 2e-6
+
+
+def _recovered(orc, codes, z, iq):
+    codes = np.atleast_2d(codes)
+    q = orc.QMatrix(codes, np.zeros(codes.shape[0]), np.atleast_1d(np.int32(z)),
+                    np.atleast_1d(np.float32(iq)), np.zeros(codes.shape[0], np.int32),
+                    codes.shape[0])
+    return orc.dequantize(q)
+
+
+def test_quantized_lstm_step_equals_float_cell_on_recovered_operands(orc):
+    """Teacher-forced: one quantized step equals a float LSTM cell (torch,
+    fp64) applied to the recovered weights, input and previous h (eq. 1-3:
+    the integer product is exactly the product of recovered values)."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, 32, 1, seed=4)
+    L = w["layers"][0]
+    ql = orc.quantize_layer(L)
+    rng = np.random.default_rng(13)
+    B = 4
+    x = rng.standard_normal((1, B, 40)).astype(np.float32)
+    h0 = np.tanh(rng.standard_normal((B, 32))).astype(np.float32) * 0.7
+    c0 = rng.standard_normal((B, 32)).astype(np.float32)
+    o = orc.lstm_layer_forward(ql, x, h0=h0, c0=c0)
+    xh = np.stack([_recovered(orc, *(lambda c, p, s: (c, p["z"], p["inv_q"]))(
+        *orc.quantize_set(x[0, b])))[0] for b in range(B)])[None]
+    hh = np.stack([_recovered(orc, *(lambda c, p, s: (c, p["z"], p["inv_q"]))(
+        *orc.quantize_set(h0[b])))[0] for b in range(B)])
+    Lhat = dict(Wx=orc.dequantize(ql.Wx), Wh=orc.dequantize(ql.Wh), b=L["b"], Wr=None)
+    ref, hT, cT = _torch_lstm(Lhat, xh, hh, c0)
+    assert np.max(np.abs(o["h"][0] - ref[0])) < 5e-6
+    assert np.max(np.abs(o["cT"] - cT)) < 5e-6
+
+
+def test_quantized_lstmp_close_to_float_cell_on_recovered_operands(orc):
+    """With a projection the projected vector m is itself quantized, so the
+    match with the float cell is within the projection's quantization noise."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, 32, 1, proj=16, seed=5)
+    L = w["layers"][0]
+    ql = orc.quantize_layer(L)
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((1, 3, 40)).astype(np.float32)
+    o = orc.lstm_layer_forward(ql, x)
+    xh = np.stack([_recovered(orc, *(lambda c, p, s: (c, p["z"], p["inv_q"]))(
+        *orc.quantize_set(x[0, b])))[0] for b in range(3)])[None]
+    Lhat = dict(Wx=orc.dequantize(ql.Wx), Wh=orc.dequantize(ql.Wh), b=L["b"],
+                Wr=orc.dequantize(ql.Wr))
+    ref, _, cT = _torch_lstm(Lhat, xh)
+    assert np.max(np.abs(o["cT"] - cT)) < 5e-6        # c does not see the projection
+    assert np.max(np.abs(o["h"][0] - ref[0])) < 5e-3
+
+
+def test_quantized_lstm_tracks_float_lstm(orc):
+    """Free-running over many steps the quantized model stays within
+    quantization noise of torch's float LSTM (gross structural errors give
+    O(0.1-1) differences)."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(320, 64, 1, seed=6)
+    L = w["layers"][0]
+    rng = np.random.default_rng(15)
+    x = rng.standard_normal((50, 2, 320)).astype(np.float32)
+    o = orc.lstm_layer_forward(orc.quantize_layer(L), x)
+    ref, _, _ = _torch_lstm(L, x)
+    assert np.max(np.abs(o["h"] - ref)) < 0.03
+
+
+def test_all_zero_h0_gives_zero_recurrent_product(orc):
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(16, 8, 1, seed=7)
+    ql = orc.quantize_layer(w["layers"][0])
+    x = np.random.default_rng(16).standard_normal((3, 2, 16)).astype(np.float32)
+    o = orc.lstm_layer_forward(ql, x, taps=True)
+    assert (o["acc_h"][0] == 0).all()
+    # with h_{-1} = 0 the first step is the feed-forward quantized layer
+    r = orc.quantized_matmul(ql.Wx, x[0], act_gran=1, bias=ql.bias)
+    assert np.array_equal(o["acc_x"][0], r["acc"])
+
+
+def test_batch_invariance_and_chunked_streaming(orc):
+    """Per-vector quantization: an utterance's result does not depend on its
+    batch-mates; splitting T with (hT, cT) -> (h0, c0) is exact."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(48, 24, 1, proj=10, seed=8)
+    ql = orc.quantize_layer(w["layers"][0])
+    x = np.random.default_rng(17).standard_normal((20, 5, 48)).astype(np.float32)
+    full = orc.lstm_layer_forward(ql, x, taps=True)
+    for b in range(5):
+        one = orc.lstm_layer_forward(ql, x[:, b:b + 1], taps=True)
+        assert np.array_equal(one["h"][:, 0], full["h"][:, b])
+        assert np.array_equal(one["acc_h"][:, 0], full["acc_h"][:, b])
+    a = orc.lstm_layer_forward(ql, x[:7])
+    b2 = orc.lstm_layer_forward(ql, x[7:], h0=a["hT"], c0=a["cT"])
+    assert np.array_equal(np.concatenate([a["h"], b2["h"]]), full["h"])
+    assert np.array_equal(b2["cT"], full["cT"])
+
+
+def test_model_softmax_properties(orc):
+    import scipy.special
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(32, 16, 2, states=50, seed=9)
+    Mq = orc.quantize_model(w)
+    x = np.random.default_rng(18).standard_normal((6, 3, 32)).astype(np.float32)
+    o = orc.acoustic_model_forward(Mq, x, taps=True)
+    p = o["post"].astype(np.float64)
+    assert np.all(np.abs(p.sum(-1) - 1.0) < 1e-6)
+    ref = scipy.special.softmax(o["logits"].astype(np.float64), axis=-1)
+    assert np.max(np.abs(p - ref)) < 1e-7
+    # layer 2 consumes layer 1's h; the output layer consumes layer 2's codes
+    h1 = orc.lstm_layer_forward(Mq.layers[0], x)["h"]
+    h2 = orc.lstm_layer_forward(Mq.layers[1], h1, taps=True)
+    assert np.array_equal(h2["h_codes"], o["layers"][1]["h_codes"])
+    r = orc.quantized_matmul(Mq.Wy, h2["h"].reshape(-1, 16), act_gran=1, bias=Mq.by)
+    assert np.array_equal(r["acc"].reshape(o["acc_y"].shape), o["acc_y"])
+
+
+def test_table1_parameter_counts():
+    """Shape convention (320-dim input, no peepholes, W_r P x N) reproduces the
+    parameter counts printed in Table 1."""
+    from paper_1607_04683_amd.workloads import LSTMModelShape
+    g = json.load(open(os.path.join(GOLDEN, "table1_params.json")))
+    for m in g["models"]:
+        s = LSTMModelShape(n_in=320, hidden=m["hidden"], layers=m["layers"], proj=m["proj"])
+        n = s.param_count() / 1e6
+        assert abs(n - m["paper_millions"]) / m["paper_millions"] <= g["tolerance_rel"], m
+
+
+def test_features_stacking_structure():
+    """Stacked inputs overlap in 5 of 8 sub-frames (stack 8, present every 3rd)."""
+    from paper_1607_04683_amd.workloads import stacked_features
+    x = stacked_features(np.random.Generator(np.random.PCG64(0)), 10, 2)
+    assert x.shape == (10, 2, 320)
+    assert np.array_equal(x[1, :, :5 * 40], x[0, :, 3 * 40:])
+    sub = stacked_features(np.random.Generator(np.random.PCG64(0)), 10, 2, utterances=[1])
+    assert np.array_equal(sub[:, 0], x[:, 1])
