@@ -1,0 +1,210 @@
+/*
+ * qlstm.h -- C ABI of the MI355X (gfx950) quantized LSTM acoustic-model library.
+ *
+ * Implements the inference side of R. Alvarez, R. Prabhavalkar, A. Bakhtin,
+ * "On the efficient representation and execution of deep acoustic models"
+ * (Interspeech 2016, arXiv:1607.04683):
+ *
+ *   - the uniform linear 8-bit quantizer of Section 3 ("Quantizing":
+ *     R = Vmax - Vmin, Q = S/R with S = 255) with the bias-free integer
+ *     rounding of Section 3.1, eq. 2: V' = round(Q V) - round(Q Vmin);
+ *   - the quantized product of Section 3.1, eq. 1, Vc = Va'' Vb'' / (Qa Qb)
+ *     with V'' = V' + round(Q Vmin), computed as uint8 x uint8 products in
+ *     32-bit accumulators plus exact zero-point terms, and recovered to float
+ *     consistently with eq. 3;
+ *   - layers that take and return float (Section 3.1, Fig. 1):
+ *     y = F(R(Mult(Q(X), W')) + B), parameters quantized offline, inputs on
+ *     the fly; weight matrices quantized independently per gate block
+ *     (Section 3.1, granularity paragraph);
+ *   - the LSTM acoustic models of Section 4: stacked LSTM layers (optionally
+ *     with a linear projection after each layer) and a quantized softmax
+ *     output layer ('quant-all', Section 5).
+ *
+ * Numerical conventions shared by every entry point:
+ *   - round() is round-half-up; Q = 255 / R is formed and applied in fp64;
+ *   - a set whose range is 0, or narrower than max|V| * 255 / 2^24, has its
+ *     range widened to include 0; an all-zero set has Q = 1, zero point 0;
+ *   - the recovery factor is Q^-1 = (float)(R / 255); a product's recovered
+ *     value is ((float)T * Qw^-1) * Qx^-1 where T = sum_k W'' x'' exactly;
+ *   - gate pre-activations are (Wx x + b) + Wh h in fp32; gates are i, f, g, o;
+ *     sigmoid(x) = 1 / (1 + e^-x), tanh(x) = 2 sigmoid(2x) - 1 with an exact
+ *     fp32 e^x (Cody-Waite reduction + degree-7 Taylor polynomial), no fused
+ *     multiply-add; c = f c + i g; m = o tanh(c); projection h = W_r m (no bias);
+ *   - activations are quantized per vector (one frame of one utterance);
+ *   - softmax is fp32 with the row maximum subtracted.
+ *
+ * Memory: every pointer argument is a device pointer unless stated otherwise;
+ * the caller owns all memory.  Scratch memory comes from a caller-provided
+ * workspace of at least the size returned by the matching *_workspace query
+ * (256-byte aligned).  The library holds no device allocations.
+ *
+ * Device code layout: a matrix of codes is stored row-major with a leading
+ * dimension `ld` (a multiple of 64, >= cols) as signed bytes equal to V' - 128
+ * (the bits of V' XOR 0x80); bytes in columns [cols, ld) are 0.
+ *
+ * Execution: every call is asynchronous on `stream` (a hipStream_t; NULL is
+ * the default stream).  Argument errors return before anything is enqueued.
+ * QL_EHIP reports a failed launch (or an error left by earlier work).
+ * Sequences are time-major: x[T][B][D].
+ */
+#ifndef QLSTM_H
+#define QLSTM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QL_OK = 0,
+  QL_EINVAL = -1,       /* null pointer or invalid enum/flag                       */
+  QL_ESHAPE = -2,       /* inconsistent sizes, rows % nblocks != 0, ld too small    */
+  QL_EOVERFLOW = -3,    /* K > 33025: 255*255*K could overflow a 32-bit accumulator */
+  QL_EWORKSPACE = -4,   /* workspace null or smaller than the query returned        */
+  QL_EHIP = -5,         /* HIP runtime error                                        */
+  QL_EUNSUPPORTED = -6, /* shape outside what the kernels implement                 */
+  QL_ETIMEOUT = -7      /* a persistent kernel's bounded inter-block wait expired   */
+} ql_status;
+
+typedef enum { QL_ACT_PER_TENSOR = 0, QL_ACT_PER_ROW = 1 } ql_act_gran;
+
+/* One quantized matrix (Section 3.1): rows split into `nblocks` equal row
+ * blocks, each quantized as an independent set (nblocks = 1: per matrix;
+ * nblocks = 4: per LSTM gate i, f, g, o).  All arrays are device memory. */
+typedef struct {
+  int8_t *codes;     /* [rows][ld], V' - 128 (see "Device code layout")    */
+  int64_t rows, cols, ld;
+  int32_t nblocks;
+  double *range;     /* [nblocks] R after the degenerate-range rule          */
+  int32_t *zero;     /* [nblocks] round(Q Vmin)                              */
+  float *inv_q;      /* [nblocks] Q^-1 = (float)(R / 255)                    */
+  int32_t *row_sums; /* [rows] sum over the row of V' (0..255 domain)        */
+} ql_qmatrix;
+
+/* One LSTM layer (Section 4).  W_x [4H][in], W_h [4H][R], W_r [P][H] where
+ * R = proj ? proj : hidden; gate blocks of W_x / W_h in the order i, f, g, o. */
+typedef struct {
+  int64_t in, hidden, proj; /* proj = 0: no projection                         */
+  ql_qmatrix Wx, Wh, Wr;    /* Wr ignored when proj = 0                         */
+  const float *bias;        /* [4H] fp32, device                                */
+} ql_lstm_layer;
+
+/* LSTM acoustic model: nlayers stacked layers and a quantized softmax layer. */
+typedef struct {
+  int32_t nlayers;
+  const ql_lstm_layer *layers; /* host array of nlayers descriptors             */
+  ql_qmatrix Wy;               /* [S][R_last]                                   */
+  const float *by;             /* [S] fp32, device                              */
+} ql_model;
+
+/* Optional diagnostic outputs of one LSTM layer (every pointer nullable,
+ * device memory).  acc_* are the raw 8-bit-domain accumulators
+ * sum_k W'[n][k] x'[k] of eq. 1 before zero-point terms and recovery. */
+typedef struct {
+  int32_t *acc_x;   /* [T][B][4H] input products                              */
+  int32_t *acc_h;   /* [T][B][4H] recurrent products (h_{t-1})                */
+  int32_t *acc_r;   /* [T][B][P]  projection products                         */
+  int8_t *h_codes;  /* [T][B][R]  codes of h_t (device code layout, ld = R)   */
+  int32_t *h_zero;  /* [T][B]     zero point of h_t                           */
+  float *h_inv_q;   /* [T][B]     recovery factor of h_t                      */
+} ql_lstm_taps;
+
+typedef struct {
+  const ql_lstm_taps *layers; /* host array [nlayers] or NULL                 */
+  int32_t *acc_y;             /* [T][B][S] softmax-layer accumulators, or NULL */
+  float *logits;              /* [T][B][S] recovered logits + bias, or NULL    */
+} ql_model_taps;
+
+/* ---- quantization (Section 3; eq. 2) ---------------------------------------
+ * Quantizes src [rows][cols] (fp32, device) in nblocks row blocks into dst,
+ * whose arrays the caller allocated (codes rows*ld bytes, ld = dst->ld).
+ * dst->rows/cols/nblocks must match.  Offline step for weights. */
+size_t ql_quantize_workspace(int64_t rows, int64_t cols, int32_t nblocks);
+ql_status ql_quantize(const float *src, int64_t rows, int64_t cols, int32_t nblocks,
+                      ql_qmatrix *dst, void *ws, size_t ws_bytes, void *stream);
+
+/* Recovery (eq. 3): dst [rows][cols] fp32 = (V' + round(Q Vmin)) * Q^-1. */
+ql_status ql_dequantize(const ql_qmatrix *q, float *dst, void *stream);
+
+/* ---- quantized layer product (Fig. 1: R(Mult(Q(X), W')) + B) ---------------
+ * X [m][cols] fp32 is quantized on the fly (per tensor or per row), multiplied
+ * by W'^T and recovered: Y [m][rows] fp32 (+ bias[rows] when non-null).
+ * acc [m][rows] (nullable) receives sum_k W'[n][k] x'[i][k]. */
+size_t ql_quantized_matmul_workspace(int64_t m, int64_t rows, int64_t cols);
+ql_status ql_quantized_matmul(const ql_qmatrix *W, const float *X, int64_t m,
+                              ql_act_gran gran, const float *bias, float *Y,
+                              int32_t *acc, void *ws, size_t ws_bytes, void *stream);
+
+/* ---- raw 8-bit GEMM (eq. 1 integer core) ------------------------------------
+ * C[M][N] = sum_k A'[i][k] B'[j][k] (int32) for code matrices in the device
+ * code layout: A [M][lda], B [N][ldb] with lda, ldb multiples of 64 and
+ * padding bytes 0.  a_sums [M] / b_sums [N] (nullable) are the row sums of
+ * the 0..255 codes; when null they are computed into the workspace. */
+size_t ql_gemm_u8_workspace(int64_t M, int64_t N, int64_t K);
+ql_status ql_gemm_u8(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb,
+                     int32_t *C, int64_t M, int64_t N, int64_t K,
+                     const int32_t *a_sums, const int32_t *b_sums,
+                     void *ws, size_t ws_bytes, void *stream);
+
+/* ---- LSTM layer (Section 4) ---------------------------------------------------
+ * x [T][B][in] fp32 -> h [T][B][R] fp32.  h0 [B][R], c0 [B][H] (nullable =
+ * zeros); hT [B][R], cT [B][H] (nullable) receive the final state, so a
+ * stream split into chunks and chained through (hT, cT) -> (h0, c0) gives
+ * the same bits as one call.  taps nullable. */
+size_t ql_lstm_layer_workspace(const ql_lstm_layer *L, int64_t T, int64_t B);
+ql_status ql_lstm_layer_forward(const ql_lstm_layer *L, const float *x, int64_t T,
+                                int64_t B, const float *h0, const float *c0,
+                                float *h, float *hT, float *cT,
+                                const ql_lstm_taps *taps, void *ws, size_t ws_bytes,
+                                void *stream);
+
+/* Per-vector quantized activation rows (the codes one layer hands the next):
+ * codes [rows][ld] in the device code layout, and per row its zero point,
+ * recovery factor and the sum of its 0..255 codes.  Device memory. */
+typedef struct {
+  int8_t *codes;
+  int64_t rows, cols, ld;
+  int32_t *zero;
+  float *inv_q;
+  int32_t *sums;
+} ql_qact;
+
+/* ---- the recurrence of one layer alone (Section 4) ------------------------------
+ * Given the input pre-activations gx [T][B][4H] fp32 = R(Mult(Q(x_t), W_x')) + b
+ * for every frame (what ql_quantized_matmul with per-row quantization and the
+ * bias computes), runs the serial part: per step, Q(h_{t-1}) per vector, the
+ * W_h' product, recovery, gates, c and h (and the projection when present).
+ * Writes h [T][B][R] fp32 and hT / cT (nullable).  h_codes (nullable; rows =
+ * T*B, cols = R, ld a multiple of 64 >= R) receives the per-vector codes of
+ * every h_t, i.e. the next layer's quantized input.  taps: acc_h, acc_r and the
+ * h_* fields are honoured (acc_x is not produced here). */
+size_t ql_lstm_recurrence_workspace(const ql_lstm_layer *L, int64_t T, int64_t B);
+ql_status ql_lstm_recurrence(const ql_lstm_layer *L, const float *gx, int64_t T, int64_t B,
+                             const float *h0, const float *c0, float *h, float *hT,
+                             float *cT, const ql_qact *h_codes, const ql_lstm_taps *taps,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* ---- acoustic model (Section 4; quantized softmax, Section 5 'quant-all') ----
+ * feats [T][B][in] fp32 -> posteriors post [T][B][S] fp32.  taps nullable. */
+size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B);
+ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T,
+                                    int64_t B, float *post, const ql_model_taps *taps,
+                                    void *ws, size_t ws_bytes, void *stream);
+
+/* ---- misc -------------------------------------------------------------------- */
+/* Synchronizes `stream`, then reports QL_ETIMEOUT if a persistent kernel of the
+ * last ql_lstm_layer_forward / ql_acoustic_model_forward that used this
+ * workspace gave up waiting for the rest of its grid (its outputs are then
+ * undefined), else QL_OK. */
+ql_status ql_workspace_status(const void *ws, void *stream);
+const char *ql_status_str(ql_status s);
+/* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
+ * 2 = tanh) -- the exact functions the LSTM kernels use. */
+ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* QLSTM_H */

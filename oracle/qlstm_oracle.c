@@ -199,6 +199,9 @@ int oracle_dequantize(const uint8_t *codes, int64_t rows, int64_t cols,
 static void qlinear_vec(const orc_qmat *W, const uint8_t *xc, int32_t zx,
                         float invqx, float *y, int32_t *acc) {
   const int64_t K = W->cols, rpb = W->rows / W->nblocks;
+  /* rows are independent; this only runs in parallel when no enclosing
+   * parallel region is active (batch of one) */
+#pragma omp parallel for schedule(static) if (W->rows * K >= 65536)
   for (int64_t n = 0; n < W->rows; ++n) {
     const uint8_t *w = W->codes + n * K;
     const int64_t blk = n / rpb;
@@ -287,7 +290,7 @@ int oracle_lstm_layer_forward(const orc_layer *L, const float *x, int64_t T,
   if (P && (!qmat_ok(&L->Wr) || L->Wr.rows != P || L->Wr.cols != H)) return -2;
   if (!L->bias) return -2;
 
-#pragma omp parallel for schedule(dynamic, 1)
+#pragma omp parallel for schedule(dynamic, 1) if (B > 1)
   for (int64_t b = 0; b < B; ++b) {
     float *hprev = (float *)calloc((size_t)RD, sizeof(float));
     float *cprev = (float *)calloc((size_t)H, sizeof(float));

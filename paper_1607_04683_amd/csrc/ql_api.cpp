@@ -1,0 +1,422 @@
+// ql_api.cpp -- the C ABI of include/qlstm.h: argument checks, workspace
+// carving and stream-ordered launches of the gfx950 kernels.
+#include "../../include/qlstm.h"
+
+#include <hip/hip_runtime.h>
+
+#include "ql_launch.h"
+
+using namespace ql;
+
+namespace {
+
+constexpr int64_t kMaxK = 33025;  // 255 * 255 * K must fit a 32-bit accumulator
+constexpr size_t kHeader = 256;   // persistent-kernel barrier counter and flag
+
+hipStream_t as_stream(void *s) { return static_cast<hipStream_t>(s); }
+
+ql_status from_hip(hipError_t e) { return e == hipSuccess ? QL_OK : QL_EHIP; }
+
+// Bump allocator over a caller workspace (256-byte aligned pieces).
+struct Carve {
+  char *base;
+  size_t off = 0;
+  explicit Carve(void *p) : base(static_cast<char *>(p)) {}
+  template <class T>
+  T *take(size_t count) {
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += align_up(count * sizeof(T), 256);
+    return p;
+  }
+};
+
+ql_status check_qmatrix(const ql_qmatrix *q, bool need_sums) {
+  if (!q || !q->codes || !q->zero || !q->inv_q || (need_sums && !q->row_sums)) return QL_EINVAL;
+  if (q->rows < 0 || q->cols < 0 || q->nblocks <= 0) return QL_ESHAPE;
+  if (q->rows % q->nblocks != 0) return QL_ESHAPE;
+  if (q->ld < q->cols || q->ld % 64 != 0) return QL_ESHAPE;
+  if (q->cols > kMaxK) return QL_EOVERFLOW;
+  return QL_OK;
+}
+
+WeightMat weight(const ql_qmatrix &q) {
+  WeightMat w;
+  w.codes = q.codes;
+  w.ld = q.ld;
+  w.rows_per_block = q.rows / q.nblocks;
+  w.zero = q.zero;
+  w.inv_q = q.inv_q;
+  w.row_sums = q.row_sums;
+  return w;
+}
+
+// Activation rows quantized on the fly: [m][ld] codes + per-row params.
+struct ActBuf {
+  int8_t *codes;
+  int64_t ld;
+  int32_t *zero, *sums;
+  float *inv_q;
+  ActRows rows() const { return ActRows{codes, ld, zero, inv_q, sums}; }
+};
+ActBuf take_act(Carve &c, int64_t m, int64_t cols) {
+  ActBuf a;
+  a.ld = round_up(cols, 64);
+  a.codes = c.take<int8_t>((size_t)(m * a.ld));
+  a.zero = c.take<int32_t>((size_t)m);
+  a.inv_q = c.take<float>((size_t)m);
+  a.sums = c.take<int32_t>((size_t)m);
+  return a;
+}
+
+int64_t layer_width(const ql_lstm_layer &L) { return L.proj ? L.proj : L.hidden; }
+
+ql_status check_layer(const ql_lstm_layer *L) {
+  if (!L || !L->bias) return QL_EINVAL;
+  if (L->in <= 0 || L->hidden <= 0 || L->proj < 0) return QL_ESHAPE;
+  const int64_t H = L->hidden, R = layer_width(*L);
+  ql_status st = check_qmatrix(&L->Wx, true);
+  if (st == QL_OK) st = check_qmatrix(&L->Wh, true);
+  if (st == QL_OK && L->proj) st = check_qmatrix(&L->Wr, true);
+  if (st != QL_OK) return st;
+  if (L->Wx.rows != 4 * H || L->Wx.cols != L->in) return QL_ESHAPE;
+  if (L->Wh.rows != 4 * H || L->Wh.cols != R) return QL_ESHAPE;
+  if (L->proj && (L->Wr.rows != L->proj || L->Wr.cols != H || L->Wr.nblocks != 1)) return QL_ESHAPE;
+  if (H > kMaxK) return QL_EOVERFLOW;
+  return QL_OK;
+}
+
+// Workspace of one layer's forward pass, carved in a fixed order.
+struct LayerWs {
+  void *rec;       // recurrent header + scratch (first: holds the timeout flag)
+  ActBuf xin;      // codes of the layer input
+  float *gx;       // [T*B][4H]
+  ActBuf hout;     // codes of every h_t
+};
+LayerWs carve_layer(Carve &c, const ql_lstm_layer &L, int64_t T, int64_t B, bool quantize_input) {
+  LayerWs w;
+  w.rec = c.take<char>(recurrent_ws(B, L.hidden, L.proj));
+  if (quantize_input) w.xin = take_act(c, T * B, L.in);
+  w.gx = c.take<float>((size_t)(T * B * 4 * L.hidden));
+  w.hout = take_act(c, T * B, layer_width(L));
+  return w;
+}
+
+RecurrentArgs rec_args(const ql_lstm_layer &L, int64_t T, int64_t B, const float *gx,
+                       const float *h0, const float *c0, float *h, float *hT, float *cT,
+                       const ActBuf &hout, const ql_lstm_taps *taps, void *rec) {
+  RecurrentArgs a{};
+  a.T = T;
+  a.B = B;
+  a.H = L.hidden;
+  a.P = L.proj;
+  a.R = layer_width(L);
+  a.gx = gx;
+  a.Wh = weight(L.Wh);
+  if (L.proj) a.Wr = weight(L.Wr);
+  a.h0 = h0;
+  a.c0 = c0;
+  a.h = h;
+  a.hT = hT;
+  a.cT = cT;
+  a.out_codes = hout.codes;
+  a.ld_out = hout.ld;
+  a.out_zero = hout.zero;
+  a.out_inv_q = hout.inv_q;
+  a.out_sums = hout.sums;
+  if (taps) {
+    a.acc_h = taps->acc_h;
+    a.acc_r = taps->acc_r;
+    a.tap_codes = taps->h_codes;
+    a.tap_zero = taps->h_zero;
+    a.tap_inv_q = taps->h_inv_q;
+  }
+  a.ws = rec;
+  return a;
+}
+
+// One layer given its input codes; writes h (float) and hout (codes).
+ql_status run_layer(const ql_lstm_layer &L, const ActRows &xin, int64_t T, int64_t B,
+                    const float *h0, const float *c0, float *h, float *hT, float *cT,
+                    const LayerWs &w, const ql_lstm_taps *taps, hipStream_t s) {
+  const int64_t M = T * B, H = L.hidden;
+  hipError_t e = launch_gemm_recover(xin, weight(L.Wx), M, 4 * H, L.in, L.bias, w.gx,
+                                     taps ? taps->acc_x : nullptr, s);
+  if (e != hipSuccess) return QL_EHIP;
+  bool unsupported = false;
+  RecurrentArgs a = rec_args(L, T, B, w.gx, h0, c0, h, hT, cT, w.hout, taps, w.rec);
+  e = launch_recurrent(a, s, &unsupported);
+  if (e != hipSuccess) return QL_EHIP;
+  return unsupported ? QL_EUNSUPPORTED : QL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ql_status_str(ql_status s) {
+  switch (s) {
+    case QL_OK: return "ok";
+    case QL_EINVAL: return "invalid argument";
+    case QL_ESHAPE: return "inconsistent shapes";
+    case QL_EOVERFLOW: return "K too large for 32-bit accumulators";
+    case QL_EWORKSPACE: return "workspace too small";
+    case QL_EHIP: return "HIP runtime error";
+    case QL_EUNSUPPORTED: return "shape not supported by the kernels";
+    case QL_ETIMEOUT: return "persistent kernel wait timed out";
+  }
+  return "unknown status";
+}
+
+size_t ql_quantize_workspace(int64_t rows, int64_t cols, int32_t nblocks) {
+  (void)rows;
+  (void)cols;
+  return set_quantize_ws(nblocks > 0 ? nblocks : 1);
+}
+
+ql_status ql_quantize(const float *src, int64_t rows, int64_t cols, int32_t nblocks,
+                      ql_qmatrix *dst, void *ws, size_t ws_bytes, void *stream) {
+  if (!dst || !dst->zero || !dst->inv_q) return QL_EINVAL;
+  if (rows * cols > 0 && (!src || !dst->codes)) return QL_EINVAL;
+  if (rows < 0 || cols < 0 || nblocks <= 0 || rows % nblocks != 0) return QL_ESHAPE;
+  if (dst->rows != rows || dst->cols != cols || dst->nblocks != nblocks) return QL_ESHAPE;
+  if (dst->ld < cols || dst->ld % 64 != 0) return QL_ESHAPE;
+  if (!ws || ws_bytes < ql_quantize_workspace(rows, cols, nblocks)) return QL_EWORKSPACE;
+  return from_hip(launch_set_quantize(src, cols, rows, cols, nblocks, dst->codes, dst->ld,
+                                      dst->range, dst->zero, dst->inv_q, dst->row_sums, nullptr,
+                                      nullptr, ws, as_stream(stream)));
+}
+
+ql_status ql_dequantize(const ql_qmatrix *q, float *dst, void *stream) {
+  if (!q || !q->codes || !q->zero || !q->inv_q) return QL_EINVAL;
+  if (q->rows * q->cols > 0 && !dst) return QL_EINVAL;
+  if (q->rows < 0 || q->cols < 0 || q->nblocks <= 0 || q->rows % q->nblocks != 0 ||
+      q->ld < q->cols)
+    return QL_ESHAPE;
+  return from_hip(launch_dequantize(q->codes, q->ld, q->rows, q->cols, q->nblocks, q->zero,
+                                    q->inv_q, dst, as_stream(stream)));
+}
+
+size_t ql_quantized_matmul_workspace(int64_t m, int64_t rows, int64_t cols) {
+  (void)rows;
+  Carve c(nullptr);
+  take_act(c, m, cols);
+  c.take<char>(set_quantize_ws(1));
+  return c.off;
+}
+
+ql_status ql_quantized_matmul(const ql_qmatrix *W, const float *X, int64_t m, ql_act_gran gran,
+                              const float *bias, float *Y, int32_t *acc, void *ws,
+                              size_t ws_bytes, void *stream) {
+  ql_status st = check_qmatrix(W, true);
+  if (st != QL_OK) return st;
+  if (m > 0 && (!X || !Y)) return QL_EINVAL;
+  if (gran != QL_ACT_PER_TENSOR && gran != QL_ACT_PER_ROW) return QL_EINVAL;
+  if (m < 0) return QL_ESHAPE;
+  if (!ws || ws_bytes < ql_quantized_matmul_workspace(m, W->rows, W->cols)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  Carve c(ws);
+  ActBuf x = take_act(c, m, W->cols);
+  void *qws = c.take<char>(set_quantize_ws(1));
+  hipError_t e;
+  if (gran == QL_ACT_PER_ROW)
+    e = launch_quantize_rows(X, W->cols, m, W->cols, x.codes, x.ld, x.zero, x.inv_q, x.sums, s);
+  else
+    e = launch_set_quantize(X, W->cols, m, W->cols, 1, x.codes, x.ld, nullptr, nullptr, nullptr,
+                            x.sums, x.zero, x.inv_q, qws, s);
+  if (e != hipSuccess) return QL_EHIP;
+  return from_hip(launch_gemm_recover(x.rows(), weight(*W), m, W->rows, W->cols, bias, Y, acc, s));
+}
+
+size_t ql_gemm_u8_workspace(int64_t M, int64_t N, int64_t K) {
+  (void)K;
+  return align_up((size_t)M * 4, 256) + align_up((size_t)N * 4, 256);
+}
+
+ql_status ql_gemm_u8(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb, int32_t *C,
+                     int64_t M, int64_t N, int64_t K, const int32_t *a_sums,
+                     const int32_t *b_sums, void *ws, size_t ws_bytes, void *stream) {
+  if (M < 0 || N < 0 || K < 0) return QL_ESHAPE;
+  if ((M > 0 && !A) || (N > 0 && !B) || (M > 0 && N > 0 && !C)) return QL_EINVAL;
+  if (M < 0 || N < 0 || K < 0 || lda < K || ldb < K || lda % 64 || ldb % 64) return QL_ESHAPE;
+  if (K > kMaxK) return QL_EOVERFLOW;
+  hipStream_t s = as_stream(stream);
+  if (!a_sums || !b_sums) {
+    if (!ws || ws_bytes < ql_gemm_u8_workspace(M, N, K)) return QL_EWORKSPACE;
+    Carve c(ws);
+    int32_t *sa = c.take<int32_t>((size_t)M), *sb = c.take<int32_t>((size_t)N);
+    if (!a_sums) {
+      if (launch_code_row_sums(A, lda, M, K, sa, s) != hipSuccess) return QL_EHIP;
+      a_sums = sa;
+    }
+    if (!b_sums) {
+      if (launch_code_row_sums(B, ldb, N, K, sb, s) != hipSuccess) return QL_EHIP;
+      b_sums = sb;
+    }
+  }
+  return from_hip(launch_gemm_raw(A, lda, B, ldb, C, M, N, K, a_sums, b_sums, s));
+}
+
+size_t ql_lstm_layer_workspace(const ql_lstm_layer *L, int64_t T, int64_t B) {
+  if (!L || T < 0 || B < 0) return 0;
+  Carve c(nullptr);
+  carve_layer(c, *L, T, B, true);
+  return c.off;
+}
+
+ql_status ql_lstm_layer_forward(const ql_lstm_layer *L, const float *x, int64_t T, int64_t B,
+                                const float *h0, const float *c0, float *h, float *hT,
+                                float *cT, const ql_lstm_taps *taps, void *ws, size_t ws_bytes,
+                                void *stream) {
+  ql_status st = check_layer(L);
+  if (st != QL_OK) return st;
+  if (T < 0 || B < 0) return QL_ESHAPE;
+  if (T * B > 0 && (!x || !h)) return QL_EINVAL;
+  if (!ws || ws_bytes < ql_lstm_layer_workspace(L, T, B)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  Carve c(ws);
+  LayerWs w = carve_layer(c, *L, T, B, true);
+  if (reset_recurrent_flag(w.rec, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+  if (launch_quantize_rows(x, L->in, T * B, L->in, w.xin.codes, w.xin.ld, w.xin.zero,
+                           w.xin.inv_q, w.xin.sums, s) != hipSuccess)
+    return QL_EHIP;
+  return run_layer(*L, w.xin.rows(), T, B, h0, c0, h, hT, cT, w, taps, s);
+}
+
+size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B) {
+  if (!M || M->nlayers <= 0 || !M->layers || T < 0 || B < 0) return 0;
+  int64_t maxH = 0, maxR = 0, maxP = 0;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_lstm_layer &L = M->layers[l];
+    maxH = L.hidden > maxH ? L.hidden : maxH;
+    maxR = layer_width(L) > maxR ? layer_width(L) : maxR;
+    maxP = L.proj > maxP ? L.proj : maxP;
+  }
+  Carve c(nullptr);
+  c.take<char>(recurrent_ws(B, maxH, maxP));
+  take_act(c, T * B, M->layers[0].in);
+  c.take<float>((size_t)(T * B * 4 * maxH));
+  take_act(c, T * B, maxR);
+  take_act(c, T * B, maxR);
+  c.take<float>((size_t)(T * B * maxR));
+  c.take<char>(softmax_ws(T * B, M->Wy.rows));
+  return c.off;
+}
+
+ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T, int64_t B,
+                                    float *post, const ql_model_taps *taps, void *ws,
+                                    size_t ws_bytes, void *stream) {
+  if (!M || !M->layers || !M->by) return QL_EINVAL;
+  if (M->nlayers <= 0 || T < 0 || B < 0) return QL_ESHAPE;
+  if (T * B > 0 && (!feats || !post)) return QL_EINVAL;
+  for (int l = 0; l < M->nlayers; ++l) {
+    ql_status st = check_layer(&M->layers[l]);
+    if (st != QL_OK) return st;
+    const int64_t want_in = l == 0 ? M->layers[0].in : layer_width(M->layers[l - 1]);
+    if (M->layers[l].in != want_in) return QL_ESHAPE;
+  }
+  ql_status st = check_qmatrix(&M->Wy, true);
+  if (st != QL_OK) return st;
+  if (M->Wy.cols != layer_width(M->layers[M->nlayers - 1])) return QL_ESHAPE;
+  if (!ws || ws_bytes < ql_acoustic_model_workspace(M, T, B)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  // the timeout flag sits at the start of the workspace in every forward call
+  if (reset_recurrent_flag(ws, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+
+  int64_t maxH = 0, maxR = 0, maxP = 0;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_lstm_layer &L = M->layers[l];
+    maxH = L.hidden > maxH ? L.hidden : maxH;
+    maxR = layer_width(L) > maxR ? layer_width(L) : maxR;
+    maxP = L.proj > maxP ? L.proj : maxP;
+  }
+  const int64_t MB = T * B;
+  Carve c(ws);
+  void *rec = c.take<char>(recurrent_ws(B, maxH, maxP));
+  ActBuf xin = take_act(c, MB, M->layers[0].in);
+  float *gx = c.take<float>((size_t)(MB * 4 * maxH));
+  ActBuf buf[2] = {take_act(c, MB, maxR), take_act(c, MB, maxR)};
+  float *hf = c.take<float>((size_t)(MB * maxR));
+  void *sws = c.take<char>(softmax_ws(MB, M->Wy.rows));
+
+  if (launch_quantize_rows(feats, M->layers[0].in, MB, M->layers[0].in, xin.codes, xin.ld,
+                           xin.zero, xin.inv_q, xin.sums, s) != hipSuccess)
+    return QL_EHIP;
+  ActRows cur = xin.rows();
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_lstm_layer &L = M->layers[l];
+    LayerWs w;
+    w.rec = rec;
+    w.gx = gx;
+    w.hout = buf[l & 1];
+    w.hout.ld = round_up(layer_width(L), 64);
+    const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l] : nullptr;
+    st = run_layer(L, cur, T, B, nullptr, nullptr, hf, nullptr, nullptr, w, lt, s);
+    if (st != QL_OK) return st;
+    cur = w.hout.rows();
+  }
+  const int64_t K = layer_width(M->layers[M->nlayers - 1]);
+  return from_hip(launch_softmax_layer(cur, weight(M->Wy), MB, M->Wy.rows, K, M->by, post,
+                                       taps ? taps->acc_y : nullptr,
+                                       taps ? taps->logits : nullptr, sws, s));
+}
+
+size_t ql_lstm_recurrence_workspace(const ql_lstm_layer *L, int64_t T, int64_t B) {
+  if (!L || T < 0 || B < 0) return 0;
+  Carve c(nullptr);
+  c.take<char>(recurrent_ws(B, L->hidden, L->proj));
+  take_act(c, T * B, layer_width(*L));
+  return c.off;
+}
+
+ql_status ql_lstm_recurrence(const ql_lstm_layer *L, const float *gx, int64_t T, int64_t B,
+                             const float *h0, const float *c0, float *h, float *hT, float *cT,
+                             const ql_qact *h_codes, const ql_lstm_taps *taps, void *ws,
+                             size_t ws_bytes, void *stream) {
+  ql_status st = check_layer(L);
+  if (st != QL_OK) return st;
+  if (T < 0 || B < 0) return QL_ESHAPE;
+  if (T * B > 0 && (!gx || !h)) return QL_EINVAL;
+  const int64_t R = layer_width(*L);
+  if (h_codes) {
+    if (!h_codes->codes || !h_codes->zero || !h_codes->inv_q || !h_codes->sums) return QL_EINVAL;
+    if (h_codes->rows != T * B || h_codes->cols != R || h_codes->ld < round_up(R, 64) ||
+        h_codes->ld % 64)
+      return QL_ESHAPE;
+  }
+  if (!ws || ws_bytes < ql_lstm_recurrence_workspace(L, T, B)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  Carve c(ws);
+  void *rec = c.take<char>(recurrent_ws(B, L->hidden, L->proj));
+  if (reset_recurrent_flag(rec, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+  ActBuf out = take_act(c, T * B, R);
+  if (h_codes) {
+    out.codes = h_codes->codes;
+    out.ld = h_codes->ld;
+    out.zero = h_codes->zero;
+    out.inv_q = h_codes->inv_q;
+    out.sums = h_codes->sums;
+  }
+  bool unsupported = false;
+  RecurrentArgs a = rec_args(*L, T, B, gx, h0, c0, h, hT, cT, out, taps, rec);
+  if (launch_recurrent(a, s, &unsupported) != hipSuccess) return QL_EHIP;
+  return unsupported ? QL_EUNSUPPORTED : QL_OK;
+}
+
+ql_status ql_workspace_status(const void *ws, void *stream) {
+  if (!ws) return QL_EINVAL;
+  bool to = false;
+  if (recurrent_timed_out(ws, as_stream(stream), &to) != hipSuccess) return QL_EHIP;
+  return to ? QL_ETIMEOUT : QL_OK;
+}
+
+ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {
+  if (n > 0 && (!x || !y)) return QL_EINVAL;
+  if (fn < 0 || fn > 2) return QL_EINVAL;
+  if (n < 0) return QL_ESHAPE;
+  return from_hip(launch_gate_fn(fn, x, y, n, as_stream(stream)));
+}
+
+}  // extern "C"

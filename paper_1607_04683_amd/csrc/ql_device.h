@@ -1,0 +1,144 @@
+// ql_device.h -- device-side building blocks shared by the gfx950 kernels.
+//
+// The arithmetic here follows the numerical conventions stated in
+// include/qlstm.h.  Every float operation is an IEEE fp32/fp64 + - * / with
+// no contraction into fused multiply-adds (the library is compiled with
+// -ffp-contract=off, and the pragma below pins it for this header), so the
+// gate functions give the same bits as any other IEEE implementation of the
+// same formulas.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#pragma clang fp contract(off)
+
+namespace ql {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr double kScale = 255.0;  // S, the 8-bit scale (Section 3)
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// e^x: Cody & Waite ("Software Manual for the Elementary Functions", 1980)
+// range reduction x = n ln2 + r with ln2 split into a 15-bit head (so n * head
+// is exact for |n| <= 127) and a tail; e^r by the Taylor series of exp to
+// degree 7 in Horner form; the result scaled by 2^n through its exponent
+// field.  x is clamped to [-87, 87] so results and 1 / (1 + e^x) are normal.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float exp_cw(float x) {
+  if (x != x) return x;
+  x = x > 87.0f ? 87.0f : x;
+  x = x < -87.0f ? -87.0f : x;
+  const float n = floorf(x * 1.44269504088896340736f + 0.5f);
+  float r = x - n * 0.693145751953125f;
+  r = r - n * 1.42860682030941723212e-6f;
+  float p = 1.0f / 5040.0f;
+  p = p * r + 1.0f / 720.0f;
+  p = p * r + 1.0f / 120.0f;
+  p = p * r + 1.0f / 24.0f;
+  p = p * r + 1.0f / 6.0f;
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  const float scale = __int_as_float(((int)n + 127) << 23);
+  return p * scale;
+}
+__device__ __forceinline__ float sigmoid_cw(float x) { return 1.0f / (1.0f + exp_cw(-x)); }
+__device__ __forceinline__ float tanh_cw(float x) { return 2.0f * sigmoid_cw(2.0f * x) - 1.0f; }
+
+// ---------------------------------------------------------------------------
+// Quantizer of Section 3 with the rounding of eq. 2.
+// ---------------------------------------------------------------------------
+// round(): half up.  floor is exact and the tie test x - floor(x) >= 0.5 is
+// decided exactly for every double.
+__device__ __forceinline__ double round_half_up(double x) {
+  double r = floor(x);
+  return (x - r >= 0.5) ? r + 1.0 : r;
+}
+
+struct QParams {
+  double q;     // Q = S / R (1 for an all-zero set)
+  int32_t z;    // round(Q Vmin)
+  float inv_q;  // (float)(R / S)
+  double range; // R
+};
+
+// Range rule: R = Vmax - Vmin in fp64; a zero range, or one so narrow that
+// Q max|V| would exceed 2^24, is widened to include 0.
+__device__ __forceinline__ QParams make_qparams(float vmin_f, float vmax_f) {
+  double lo = (double)vmin_f, hi = (double)vmax_f;
+  double R = hi - lo;
+  const double alo = lo < 0.0 ? -lo : lo, ahi = hi < 0.0 ? -hi : hi;
+  const double amax = alo > ahi ? alo : ahi;
+  if (R == 0.0 || kScale * amax > 16777216.0 * R) {
+    if (lo > 0.0) lo = 0.0;
+    if (hi < 0.0) hi = 0.0;
+    R = hi - lo;
+  }
+  QParams p;
+  p.range = R;
+  if (R == 0.0) {
+    p.q = 1.0;
+    p.z = 0;
+    p.inv_q = 1.0f;
+  } else {
+    p.q = kScale / R;
+    p.z = (int32_t)round_half_up(p.q * lo);
+    p.inv_q = (float)(R / kScale);
+  }
+  return p;
+}
+
+// eq. 2: V' = round(Q V) - round(Q Vmin), kept in [0, 255].
+__device__ __forceinline__ int encode(float v, double q, int32_t z) {
+  double c = round_half_up(q * (double)v) - (double)z;
+  c = c < 0.0 ? 0.0 : c;
+  c = c > 255.0 ? 255.0 : c;
+  return (int)c;
+}
+
+// Pack four codes (0..255) into the device layout (V' - 128 per byte).
+__device__ __forceinline__ uint32_t pack4_s8(int c0, int c1, int c2, int c3) {
+  return ((uint32_t)(c0 ^ 0x80) & 0xffu) | (((uint32_t)(c1 ^ 0x80) & 0xffu) << 8) |
+         (((uint32_t)(c2 ^ 0x80) & 0xffu) << 16) | (((uint32_t)(c3 ^ 0x80) & 0xffu) << 24);
+}
+
+// ---------------------------------------------------------------------------
+// Recovery of eq. 1 / eq. 3.  With device codes s = V' - 128, shifted zero
+// points zt = z + 128 and signed sums sig = sum s, the numerator of eq. 1 is
+//   T = sum_k (sw + ztw)(sx + ztx) = S + ztx * sigw + ztw * sigx + K ztw ztx
+// where S = sum_k sw sx is what the signed 8-bit MFMA/dot products return.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float recover(int32_t S, int64_t colterm /* sigw + K ztw */,
+                                         int32_t ztw, int32_t ztx, int32_t sigx,
+                                         float iqw, float iqx) {
+  const int64_t t = (int64_t)S + (int64_t)ztx * colterm + (int64_t)ztw * (int64_t)sigx;
+  return ((float)t * iqw) * iqx;
+}
+// Raw 0..255-domain accumulator sum_k V'w V'x from the signed one.
+__device__ __forceinline__ int32_t acc_u8(int32_t S, int32_t sigw, int32_t sigx, int64_t K) {
+  return (int32_t)((int64_t)S + 128 * (int64_t)sigw + 128 * (int64_t)sigx + 16384 * K);
+}
+
+// ---------------------------------------------------------------------------
+// Wavefront (64-lane) reductions.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace ql

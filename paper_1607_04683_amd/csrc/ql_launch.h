@@ -1,0 +1,95 @@
+// ql_launch.h -- host-side launchers of the gfx950 kernels (internal).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ql {
+
+constexpr int kSetParts = 128;  // partial min/max blocks per quantized set
+
+inline size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
+inline int64_t round_up(int64_t n, int64_t a) { return (n + a - 1) / a * a; }
+
+// ---- quantizer (ql_quantize.hip)
+hipError_t launch_quantize_rows(const float *X, int64_t ldx, int64_t m, int64_t K, int8_t *codes,
+                                int64_t ld, int32_t *zero, float *inv_q, int32_t *sums,
+                                hipStream_t s);
+size_t set_quantize_ws(int nsets);
+hipError_t launch_set_quantize(const float *X, int64_t ldx, int64_t rows, int64_t cols,
+                               int nsets, int8_t *codes, int64_t ld, double *range,
+                               int32_t *zero, float *inv_q, int32_t *row_sums,
+                               int32_t *row_zero, float *row_inv_q, void *ws, hipStream_t s);
+hipError_t launch_dequantize(const int8_t *codes, int64_t ld, int64_t rows, int64_t cols,
+                             int nblocks, const int32_t *zero, const float *inv_q, float *dst,
+                             hipStream_t s);
+hipError_t launch_code_row_sums(const int8_t *codes, int64_t ld, int64_t rows, int64_t K,
+                                int32_t *sums, hipStream_t s);
+hipError_t launch_gate_fn(int fn, const float *x, float *y, int64_t n, hipStream_t s);
+
+// ---- 8-bit GEMM (ql_gemm.hip)
+// Per-row description of a quantized activation matrix X' [M][ld].
+struct ActRows {
+  const int8_t *codes;
+  int64_t ld;
+  const int32_t *zero;   // [M] round(Q Vmin) per row
+  const float *inv_q;    // [M]
+  const int32_t *sums;   // [M] sum of V' (0..255)
+};
+// Quantized weight matrix W' [N][ld] with per-block params.
+struct WeightMat {
+  const int8_t *codes;
+  int64_t ld;
+  int64_t rows_per_block;
+  const int32_t *zero;     // [nblocks]
+  const float *inv_q;      // [nblocks]
+  const int32_t *row_sums; // [N]
+};
+
+// Y[m][n] = recover(X'[m] . W'[n]) (+ bias[n]); acc (nullable) = raw sums.
+hipError_t launch_gemm_recover(const ActRows &X, const WeightMat &W, int64_t M, int64_t N,
+                               int64_t K, const float *bias, float *Y, int32_t *acc,
+                               hipStream_t s);
+// C[m][n] = sum_k A'[m][k] B'[n][k] in the 0..255 domain.
+hipError_t launch_gemm_raw(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb,
+                           int32_t *C, int64_t M, int64_t N, int64_t K, const int32_t *a_sums,
+                           const int32_t *b_sums, hipStream_t s);
+// Softmax output layer: post[m][n] = softmax_n(recover(X'[m] . W'[n]) + bias[n]).
+size_t softmax_ws(int64_t M, int64_t N);
+hipError_t launch_softmax_layer(const ActRows &X, const WeightMat &W, int64_t M, int64_t N,
+                                int64_t K, const float *bias, float *post, int32_t *acc,
+                                float *logits, void *ws, hipStream_t s);
+
+// ---- recurrence (ql_recurrent.hip)
+struct RecurrentArgs {
+  int64_t T, B, H, P, R;     // R = P ? P : H
+  const float *gx;           // [T][B][4H] (W_x x_t + b), fp32
+  WeightMat Wh;              // [4H][ldR]
+  WeightMat Wr;              // [P][ldH] (P > 0)
+  const float *h0, *c0;      // nullable
+  float *h;                  // [T][B][R] output
+  float *hT, *cT;            // nullable
+  // codes of every h_t for the next layer / output layer
+  int8_t *out_codes;         // [T*B][ld_out]
+  int64_t ld_out;
+  int32_t *out_zero;         // [T*B]
+  float *out_inv_q;          // [T*B]
+  int32_t *out_sums;         // [T*B]
+  // optional taps
+  int32_t *acc_h;            // [T][B][4H]
+  int32_t *acc_r;            // [T][B][P]
+  int8_t *tap_codes;         // [T][B][R] (ld = R)
+  int32_t *tap_zero;         // [T][B]
+  float *tap_inv_q;          // [T][B]
+  // scratch
+  void *ws;
+};
+size_t recurrent_ws(int64_t B, int64_t H, int64_t P);
+// returns hipSuccess, or an error; *unsupported set if shapes do not fit.
+hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsupported);
+// Clears the timeout flag (once per API call, before the first layer).
+hipError_t reset_recurrent_flag(void *ws, hipStream_t s);
+// Reads the timeout flag a persistent launch left in its workspace (syncs s).
+hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
+
+}  // namespace ql

@@ -1,0 +1,415 @@
+"""Thin Python binding of libqlstm.so (include/qlstm.h).
+
+Argument marshalling only: every step of quantized inference runs in the
+library's gfx950 kernels.  PyTorch supplies device memory (tensors) and the
+current HIP stream.  If the shared library is missing this module raises; it
+never falls back to another implementation.
+
+Codes on the device use the library's layout: row-major with a leading
+dimension `ld` (multiple of 64) and bytes equal to V' - 128 (int8).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libqlstm.so")
+
+QL_OK, QL_EINVAL, QL_ESHAPE, QL_EOVERFLOW, QL_EWORKSPACE, QL_EHIP, QL_EUNSUPPORTED, \
+    QL_ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
+QL_ACT_PER_TENSOR, QL_ACT_PER_ROW = 0, 1
+
+EXPORTS = [
+    "ql_quantize_workspace", "ql_quantize", "ql_dequantize", "ql_quantized_matmul_workspace",
+    "ql_quantized_matmul", "ql_gemm_u8_workspace", "ql_gemm_u8", "ql_lstm_layer_workspace",
+    "ql_lstm_layer_forward", "ql_acoustic_model_workspace", "ql_acoustic_model_forward",
+    "ql_status_str", "ql_workspace_status", "ql_gate_fn", "ql_lstm_recurrence_workspace",
+    "ql_lstm_recurrence",
+]
+
+
+class QLError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_str(status)} ({status})")
+        self.status = status
+
+
+class CQMatrix(C.Structure):
+    _fields_ = [("codes", C.c_void_p), ("rows", C.c_int64), ("cols", C.c_int64),
+                ("ld", C.c_int64), ("nblocks", C.c_int32), ("range", C.c_void_p),
+                ("zero", C.c_void_p), ("inv_q", C.c_void_p), ("row_sums", C.c_void_p)]
+
+
+class CLayer(C.Structure):
+    _fields_ = [("in_", C.c_int64), ("hidden", C.c_int64), ("proj", C.c_int64),
+                ("Wx", CQMatrix), ("Wh", CQMatrix), ("Wr", CQMatrix), ("bias", C.c_void_p)]
+
+
+class CModel(C.Structure):
+    _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(CLayer)), ("Wy", CQMatrix),
+                ("by", C.c_void_p)]
+
+
+class CTaps(C.Structure):
+    _fields_ = [("acc_x", C.c_void_p), ("acc_h", C.c_void_p), ("acc_r", C.c_void_p),
+                ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p)]
+
+
+class CQAct(C.Structure):
+    _fields_ = [("codes", C.c_void_p), ("rows", C.c_int64), ("cols", C.c_int64),
+                ("ld", C.c_int64), ("zero", C.c_void_p), ("inv_q", C.c_void_p),
+                ("sums", C.c_void_p)]
+
+
+class CModelTaps(C.Structure):
+    _fields_ = [("layers", C.POINTER(CTaps)), ("acc_y", C.c_void_p), ("logits", C.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libqlstm.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found: build it with `python -m paper_1607_04683_amd.build`")
+    L = C.CDLL(path)
+    vp, i64, i32, sz = C.c_void_p, C.c_int64, C.c_int32, C.c_size_t
+    L.ql_status_str.argtypes = [i32]
+    L.ql_status_str.restype = C.c_char_p
+    L.ql_quantize_workspace.argtypes = [i64, i64, i32]
+    L.ql_quantize_workspace.restype = sz
+    L.ql_quantize.argtypes = [vp, i64, i64, i32, C.POINTER(CQMatrix), vp, sz, vp]
+    L.ql_dequantize.argtypes = [C.POINTER(CQMatrix), vp, vp]
+    L.ql_quantized_matmul_workspace.argtypes = [i64, i64, i64]
+    L.ql_quantized_matmul_workspace.restype = sz
+    L.ql_quantized_matmul.argtypes = [C.POINTER(CQMatrix), vp, i64, i32, vp, vp, vp, vp, sz, vp]
+    L.ql_gemm_u8_workspace.argtypes = [i64, i64, i64]
+    L.ql_gemm_u8_workspace.restype = sz
+    L.ql_gemm_u8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i64, vp, vp, vp, sz, vp]
+    L.ql_lstm_layer_workspace.argtypes = [C.POINTER(CLayer), i64, i64]
+    L.ql_lstm_layer_workspace.restype = sz
+    L.ql_lstm_layer_forward.argtypes = [C.POINTER(CLayer), vp, i64, i64, vp, vp, vp, vp, vp,
+                                        C.POINTER(CTaps), vp, sz, vp]
+    L.ql_acoustic_model_workspace.argtypes = [C.POINTER(CModel), i64, i64]
+    L.ql_acoustic_model_workspace.restype = sz
+    L.ql_acoustic_model_forward.argtypes = [C.POINTER(CModel), vp, i64, i64, vp,
+                                            C.POINTER(CModelTaps), vp, sz, vp]
+    L.ql_lstm_recurrence_workspace.argtypes = [C.POINTER(CLayer), i64, i64]
+    L.ql_lstm_recurrence_workspace.restype = sz
+    L.ql_lstm_recurrence.argtypes = [C.POINTER(CLayer), vp, i64, i64, vp, vp, vp, vp, vp,
+                                     C.POINTER(CQAct), C.POINTER(CTaps), vp, sz, vp]
+    L.ql_workspace_status.argtypes = [vp, vp]
+    L.ql_gate_fn.argtypes = [i32, vp, vp, i64, vp]
+    for f in ("ql_quantize", "ql_dequantize", "ql_quantized_matmul", "ql_gemm_u8",
+              "ql_lstm_layer_forward", "ql_acoustic_model_forward", "ql_workspace_status",
+              "ql_gate_fn", "ql_lstm_recurrence"):
+        getattr(L, f).restype = i32
+    _lib = L
+    return L
+
+
+def status_str(s: int) -> str:
+    return load().ql_status_str(s).decode()
+
+
+def _check(st: int, what: str):
+    if st != QL_OK:
+        raise QLError(st, what)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ws(nbytes: int, device):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def ld_for(cols: int) -> int:
+    return (cols + 63) // 64 * 64
+
+
+# ------------------------------------------------------------------- matrices
+@dataclass
+class QMatrix:
+    """A quantized matrix on the device (see ql_qmatrix)."""
+    codes: torch.Tensor     # int8 [rows][ld]
+    rows: int
+    cols: int
+    nblocks: int
+    range: torch.Tensor     # float64 [nblocks]
+    zero: torch.Tensor      # int32 [nblocks]
+    inv_q: torch.Tensor     # float32 [nblocks]
+    row_sums: torch.Tensor  # int32 [rows]
+
+    @property
+    def ld(self) -> int:
+        return self.codes.shape[1]
+
+    def cstruct(self) -> CQMatrix:
+        return CQMatrix(self.codes.data_ptr(), self.rows, self.cols, self.ld, self.nblocks,
+                        self.range.data_ptr(), self.zero.data_ptr(), self.inv_q.data_ptr(),
+                        self.row_sums.data_ptr())
+
+    def codes_u8(self) -> torch.Tensor:
+        """The paper's V' (0..255) as uint8 [rows][cols] (device)."""
+        return (self.codes[:, :self.cols].view(torch.uint8) ^ 0x80)
+
+    @staticmethod
+    def empty(rows: int, cols: int, nblocks: int, device) -> "QMatrix":
+        return QMatrix(torch.zeros(rows, ld_for(cols), dtype=torch.int8, device=device), rows,
+                       cols, nblocks, torch.empty(nblocks, dtype=torch.float64, device=device),
+                       torch.empty(nblocks, dtype=torch.int32, device=device),
+                       torch.empty(nblocks, dtype=torch.float32, device=device),
+                       torch.empty(rows, dtype=torch.int32, device=device))
+
+
+def quantize(W: torch.Tensor, nblocks: int = 1) -> QMatrix:
+    """Section 3 quantizer: W [rows][cols] fp32 (device) -> QMatrix."""
+    W = W.contiguous()
+    assert W.dtype == torch.float32 and W.dim() == 2
+    rows, cols = W.shape
+    q = QMatrix.empty(rows, cols, nblocks, W.device)
+    lib = load()
+    nbytes = lib.ql_quantize_workspace(rows, cols, nblocks)
+    ws = _ws(nbytes, W.device)
+    cs = q.cstruct()
+    _check(lib.ql_quantize(_ptr(W), rows, cols, nblocks, C.byref(cs), _ptr(ws), ws.numel(),
+                           _stream()), "ql_quantize")
+    return q
+
+
+def dequantize(q: QMatrix) -> torch.Tensor:
+    out = torch.empty(q.rows, q.cols, dtype=torch.float32, device=q.codes.device)
+    cs = q.cstruct()
+    _check(load().ql_dequantize(C.byref(cs), _ptr(out), _stream()), "ql_dequantize")
+    return out
+
+
+def quantized_matmul(q: QMatrix, X: torch.Tensor, gran: int = QL_ACT_PER_ROW, bias=None,
+                     want_acc: bool = False):
+    """Fig. 1: R(Mult(Q(X), W')) + B -> (Y [m][rows], acc or None)."""
+    X = X.contiguous()
+    m = X.shape[0]
+    lib = load()
+    Y = torch.empty(m, q.rows, dtype=torch.float32, device=X.device)
+    acc = torch.empty(m, q.rows, dtype=torch.int32, device=X.device) if want_acc else None
+    ws = _ws(lib.ql_quantized_matmul_workspace(m, q.rows, q.cols), X.device)
+    cs = q.cstruct()
+    _check(lib.ql_quantized_matmul(C.byref(cs), _ptr(X), m, gran, _ptr(bias), _ptr(Y), _ptr(acc),
+                                   _ptr(ws), ws.numel(), _stream()), "ql_quantized_matmul")
+    return Y, acc
+
+
+def device_codes(u8, ld: int | None = None, device="cuda") -> torch.Tensor:
+    """uint8 codes [rows][cols] (numpy or tensor) -> device layout int8 [rows][ld]."""
+    t = torch.as_tensor(u8).to(device)
+    rows, cols = t.shape
+    ld = ld or ld_for(cols)
+    out = torch.zeros(rows, ld, dtype=torch.int8, device=device)
+    out[:, :cols] = (t.to(torch.uint8) ^ 0x80).view(torch.int8)
+    return out
+
+
+def gemm_u8(A: torch.Tensor, B: torch.Tensor, K: int, a_sums=None, b_sums=None, out=None,
+            ws=None):
+    """C = A' B'^T (int32) for device-layout codes A [M][lda], B [N][ldb]."""
+    M, lda = A.shape
+    N, ldb = B.shape
+    lib = load()
+    Cm = out if out is not None else torch.empty(M, N, dtype=torch.int32, device=A.device)
+    if ws is None and (a_sums is None or b_sums is None):
+        ws = _ws(lib.ql_gemm_u8_workspace(M, N, K), A.device)
+    _check(lib.ql_gemm_u8(_ptr(A), lda, _ptr(B), ldb, _ptr(Cm), M, N, K, _ptr(a_sums),
+                          _ptr(b_sums), _ptr(ws), 0 if ws is None else ws.numel(), _stream()),
+           "ql_gemm_u8")
+    return Cm
+
+
+def gate_fn(fn: int, x: torch.Tensor) -> torch.Tensor:
+    x = x.contiguous()
+    y = torch.empty_like(x)
+    _check(load().ql_gate_fn(fn, _ptr(x), _ptr(y), x.numel(), _stream()), "ql_gate_fn")
+    return y
+
+
+# ------------------------------------------------------------------- LSTM
+@dataclass
+class Layer:
+    n_in: int
+    hidden: int
+    proj: int
+    Wx: QMatrix
+    Wh: QMatrix
+    Wr: QMatrix | None
+    bias: torch.Tensor
+
+    @property
+    def width(self) -> int:
+        return self.proj if self.proj else self.hidden
+
+    def cstruct(self) -> CLayer:
+        empty = CQMatrix(None, 0, 0, 0, 1, None, None, None, None)
+        return CLayer(self.n_in, self.hidden, self.proj, self.Wx.cstruct(), self.Wh.cstruct(),
+                      self.Wr.cstruct() if self.Wr is not None else empty, self.bias.data_ptr())
+
+
+def quantize_layer(L: dict, device="cuda", gate_blocks: int = 4) -> Layer:
+    """Float layer {'Wx','Wh','b','Wr'} (numpy/tensors) -> quantized layer on the device:
+    W_x, W_h per gate block (i, f, g, o), W_r per matrix."""
+    t = lambda a: torch.as_tensor(a, dtype=torch.float32).to(device).contiguous()
+    Wx, Wh = t(L["Wx"]), t(L["Wh"])
+    Wr = None if L.get("Wr") is None else t(L["Wr"])
+    H = Wx.shape[0] // 4
+    return Layer(Wx.shape[1], H, 0 if Wr is None else Wr.shape[0], quantize(Wx, gate_blocks),
+                 quantize(Wh, gate_blocks), None if Wr is None else quantize(Wr, 1), t(L["b"]))
+
+
+@dataclass
+class Model:
+    layers: list
+    Wy: QMatrix
+    by: torch.Tensor
+
+    def cstruct(self):
+        arr = (CLayer * len(self.layers))(*[L.cstruct() for L in self.layers])
+        return CModel(len(self.layers), arr, self.Wy.cstruct(), self.by.data_ptr()), arr
+
+
+def quantize_model(weights: dict, device="cuda", gate_blocks: int = 4) -> Model:
+    return Model([quantize_layer(L, device, gate_blocks) for L in weights["layers"]],
+                 quantize(torch.as_tensor(weights["Wy"], dtype=torch.float32).to(device), 1),
+                 torch.as_tensor(weights["by"], dtype=torch.float32).to(device).contiguous())
+
+
+TAP_NAMES = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q")
+
+
+def _taps(T, B, L: Layer, device, which=True):
+    """Allocate the requested taps (True = all, or a collection of names)."""
+    H, P, R = L.hidden, L.proj, L.width
+    want = set(TAP_NAMES) if which is True else set(which)
+    z = lambda name, *s, dt: torch.empty(*s, dtype=dt, device=device) if name in want else None
+    t = dict(acc_x=z("acc_x", T, B, 4 * H, dt=torch.int32),
+             acc_h=z("acc_h", T, B, 4 * H, dt=torch.int32),
+             acc_r=z("acc_r", T, B, P, dt=torch.int32) if P else None,
+             h_codes=z("h_codes", T, B, R, dt=torch.int8), h_zero=z("h_zero", T, B, dt=torch.int32),
+             h_inv_q=z("h_inv_q", T, B, dt=torch.float32))
+    c = CTaps(*[None if t[k] is None else t[k].data_ptr()
+                for k in ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q")])
+    return t, c
+
+
+class Workspace:
+    """Reusable device workspace (grows on demand)."""
+
+    def __init__(self):
+        self.buf = None
+
+    def get(self, nbytes: int, device):
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != torch.device(device):
+            self.buf = _ws(nbytes, device)
+        return self.buf
+
+
+def lstm_layer_forward(L: Layer, x: torch.Tensor, h0=None, c0=None, taps: bool = False,
+                       workspace: Workspace | None = None, check: bool = True):
+    """x [T][B][in] fp32 (device) -> dict(h, hT, cT[, taps])."""
+    x = x.contiguous()
+    T, B, _ = x.shape
+    dev = x.device
+    lib = load()
+    cl = L.cstruct()
+    h = torch.empty(T, B, L.width, dtype=torch.float32, device=dev)
+    hT = torch.empty(B, L.width, dtype=torch.float32, device=dev)
+    cT = torch.empty(B, L.hidden, dtype=torch.float32, device=dev)
+    nbytes = lib.ql_lstm_layer_workspace(C.byref(cl), T, B)
+    ws = (workspace or Workspace()).get(nbytes, dev)
+    out = dict(h=h, hT=hT, cT=cT)
+    tp = None
+    if taps:
+        t, ct = _taps(T, B, L, dev, taps)
+        out.update(t)
+        tp = C.byref(ct)
+    _check(lib.ql_lstm_layer_forward(C.byref(cl), _ptr(x), T, B, _ptr(h0), _ptr(c0), _ptr(h),
+                                     _ptr(hT), _ptr(cT), tp, _ptr(ws), ws.numel(), _stream()),
+           "ql_lstm_layer_forward")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_lstm_layer_forward")
+    return out
+
+
+def lstm_recurrence(L: Layer, gx: torch.Tensor, h0=None, c0=None, taps=False,
+                    workspace: Workspace | None = None, out=None, check: bool = True):
+    """gx [T][B][4H] fp32 pre-activations (device) -> dict(h, hT, cT, codes...)."""
+    gx = gx.contiguous()
+    T, B, _ = gx.shape
+    dev = gx.device
+    lib = load()
+    cl = L.cstruct()
+    o = out or {}
+    h = o.get("h")
+    if h is None:
+        h = torch.empty(T, B, L.width, dtype=torch.float32, device=dev)
+    ws = (workspace or Workspace()).get(lib.ql_lstm_recurrence_workspace(C.byref(cl), T, B), dev)
+    res = dict(h=h)
+    tp = None
+    if taps:
+        t, ct = _taps(T, B, L, dev, taps)
+        res.update(t)
+        tp = C.byref(ct)
+    _check(lib.ql_lstm_recurrence(C.byref(cl), _ptr(gx), T, B, _ptr(h0), _ptr(c0), _ptr(h),
+                                  None, None, None, tp, _ptr(ws), ws.numel(), _stream()),
+           "ql_lstm_recurrence")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_lstm_recurrence")
+    return res
+
+
+def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
+                           workspace: Workspace | None = None, post: torch.Tensor | None = None,
+                           check: bool = True):
+    """feats [T][B][in] fp32 (device) -> dict(post [T][B][S][, taps])."""
+    feats = feats.contiguous()
+    T, B, _ = feats.shape
+    dev = feats.device
+    lib = load()
+    cm, keep = M.cstruct()
+    S = M.Wy.rows
+    if post is None:
+        post = torch.empty(T, B, S, dtype=torch.float32, device=dev)
+    nbytes = lib.ql_acoustic_model_workspace(C.byref(cm), T, B)
+    ws = (workspace or Workspace()).get(nbytes, dev)
+    out = dict(post=post)
+    mt = None
+    if taps:
+        lt = []
+        arr = (CTaps * len(M.layers))()
+        for i, L in enumerate(M.layers):
+            t, ct = _taps(T, B, L, dev, taps)
+            lt.append(t)
+            arr[i] = ct
+        full = taps is True or "acc_y" in taps
+        acc_y = torch.empty(T, B, S, dtype=torch.int32, device=dev) if full else None
+        logits = torch.empty(T, B, S, dtype=torch.float32, device=dev) if full else None
+        out.update(layers=lt, acc_y=acc_y, logits=logits)
+        mt = CModelTaps(arr, None if acc_y is None else acc_y.data_ptr(),
+                        None if logits is None else logits.data_ptr())
+        out["_keep"] = arr
+    _check(lib.ql_acoustic_model_forward(C.byref(cm), _ptr(feats), T, B, _ptr(post),
+                                         C.byref(mt) if mt is not None else None, _ptr(ws),
+                                         ws.numel(), _stream()), "ql_acoustic_model_forward")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward")
+    return out

@@ -1,0 +1,127 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+include/qlstm.h declares, and rejects bad arguments before enqueuing work.
+
+Every call below fails validation before the library touches memory or the
+HIP runtime (the pointers passed are never dereferenced)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlstm.h")
+
+
+@pytest.fixture(scope="module")
+def ql():
+    from paper_1607_04683_amd import qlstm
+    if not os.path.exists(qlstm.LIB_PATH):
+        from paper_1607_04683_amd import build
+        build.build(force=False)
+    return qlstm
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ql_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_paper_calls():
+    names = declared_functions()
+    for f in ("ql_quantize", "ql_quantized_matmul", "ql_lstm_layer_forward",
+              "ql_acoustic_model_forward"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(ql):
+    lib = C.CDLL(ql.LIB_PATH)
+    missing = [f for f in declared_functions() if not hasattr(lib, f)]
+    assert not missing, missing
+    assert sorted(ql.EXPORTS) == declared_functions()
+
+
+def test_status_strings(ql):
+    for s in range(0, -8, -1):
+        assert ql.status_str(s) and ql.status_str(s) != "unknown status"
+
+
+FAKE = 0x1000  # never dereferenced: each call below fails validation first
+
+
+def qm(rows=8, cols=16, ld=64, nblocks=1, null=False):
+    return ql_mod().CQMatrix(None if null else FAKE, rows, cols, ld, nblocks, FAKE, FAKE, FAKE, FAKE)
+
+
+def ql_mod():
+    from paper_1607_04683_amd import qlstm
+    return qlstm
+
+
+def test_quantized_matmul_argument_errors(ql):
+    lib = ql.load()
+    ws = lib.ql_quantized_matmul_workspace(4, 8, 16)
+    call = lambda q, X=FAKE, m=4, gran=1, Y=FAKE, wsb=ws: lib.ql_quantized_matmul(
+        C.byref(q), X, m, gran, None, Y, None, FAKE, wsb, None)
+    assert call(qm(null=True)) == ql.QL_EINVAL
+    assert call(qm(), X=None) == ql.QL_EINVAL
+    assert call(qm(), gran=7) == ql.QL_EINVAL
+    assert call(qm(rows=9, nblocks=4)) == ql.QL_ESHAPE          # rows % nblocks
+    assert call(qm(ld=8)) == ql.QL_ESHAPE                        # ld < cols
+    assert call(qm(cols=33026, ld=33088)) == ql.QL_EOVERFLOW     # int32 accumulator guard
+    assert call(qm(), wsb=ws - 1) == ql.QL_EWORKSPACE
+    assert call(qm(), m=-1) == ql.QL_ESHAPE
+
+
+def test_gemm_argument_errors(ql):
+    lib = ql.load()
+    g = lambda lda=64, ldb=64, K=64, M=4, N=4, ws=None, wsb=0: lib.ql_gemm_u8(
+        FAKE, lda, FAKE, ldb, FAKE, M, N, K, None, None, ws, wsb, None)
+    assert g(lda=32) == ql.QL_ESHAPE
+    assert g(lda=96) == ql.QL_ESHAPE       # not a multiple of 64
+    assert g(K=33026, lda=33088, ldb=33088) == ql.QL_EOVERFLOW
+    assert g() == ql.QL_EWORKSPACE         # sums not given and no workspace
+    assert lib.ql_gemm_u8(None, 64, FAKE, 64, FAKE, 4, 4, 64, None, None, None, 0, None) == ql.QL_EINVAL
+
+
+def test_layer_argument_errors(ql):
+    lib = ql.load()
+    H, IN = 8, 16
+    good = ql.CLayer(IN, H, 0, qm(4 * H, IN, 64, 4), qm(4 * H, H, 64, 4),
+                     ql.CQMatrix(None, 0, 0, 0, 1, None, None, None, None), FAKE)
+    nbytes = lib.ql_lstm_layer_workspace(C.byref(good), 5, 2)
+    assert nbytes > 0
+    f = lambda L, wsb=nbytes, x=FAKE: lib.ql_lstm_layer_forward(
+        C.byref(L), x, 5, 2, None, None, FAKE, None, None, None, FAKE, wsb, None)
+    assert f(good, x=None) == ql.QL_EINVAL
+    assert f(good, wsb=nbytes - 1) == ql.QL_EWORKSPACE
+    bad = ql.CLayer(IN, H, 0, qm(4 * H, IN + 1, 64, 4), qm(4 * H, H, 64, 4), good.Wr, FAKE)
+    assert f(bad) == ql.QL_ESHAPE
+    bad = ql.CLayer(IN, H, 0, qm(4 * H, IN, 64, 4), qm(4 * H, H + 1, 64, 4), good.Wr, FAKE)
+    assert f(bad) == ql.QL_ESHAPE
+    bad = ql.CLayer(IN, H, 3, qm(4 * H, IN, 64, 4), qm(4 * H, 3, 64, 4), qm(3, H, 64, 1), None)
+    assert f(bad) == ql.QL_EINVAL          # null bias
+    bad = ql.CLayer(IN, H, 3, qm(4 * H, IN, 64, 4), qm(4 * H, 3, 64, 4), qm(3, H, 64, 3), FAKE)
+    assert f(bad) == ql.QL_ESHAPE          # W_r must be one block
+
+
+def test_model_argument_errors(ql):
+    lib = ql.load()
+    H, IN, S = 8, 16, 10
+    empty = ql.CQMatrix(None, 0, 0, 0, 1, None, None, None, None)
+    l0 = ql.CLayer(IN, H, 0, qm(4 * H, IN, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    l1 = ql.CLayer(H + 1, H, 0, qm(4 * H, H + 1, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    arr = (ql.CLayer * 2)(l0, l1)
+    m = ql.CModel(2, arr, qm(S, H, 64, 1), FAKE)
+    assert lib.ql_acoustic_model_forward(C.byref(m), FAKE, 3, 2, FAKE, None, FAKE, 1 << 40,
+                                         None) == ql.QL_ESHAPE   # layer widths do not chain
+    arr2 = (ql.CLayer * 1)(l0)
+    m2 = ql.CModel(1, arr2, qm(S, H + 2, 64, 1), FAKE)
+    assert lib.ql_acoustic_model_forward(C.byref(m2), FAKE, 3, 2, FAKE, None, FAKE, 1 << 40,
+                                         None) == ql.QL_ESHAPE   # W_y width
+    m3 = ql.CModel(1, arr2, qm(S, H, 64, 1), FAKE)
+    need = lib.ql_acoustic_model_workspace(C.byref(m3), 3, 2)
+    assert need > 0
+    assert lib.ql_acoustic_model_forward(C.byref(m3), FAKE, 3, 2, FAKE, None, FAKE, need - 1,
+                                         None) == ql.QL_EWORKSPACE

@@ -1,0 +1,190 @@
+"""LSTM layer / acoustic model parity of the GPU path with the CPU oracle.
+
+Free-running: the GPU's h_t feeds its own next quantization, so codes and
+int32 accumulators can only stay bit-exact if every fp32 operation of the
+chain matches; float outputs are additionally held to the 1e-4 bar and
+posteriors (a different summation order in the softmax) to 1e-4 absolute."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def ql():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_1607_04683_amd import qlstm
+    qlstm.load()
+    return qlstm
+
+
+def np_(t):
+    return t.cpu().numpy()
+
+
+def u8(t):
+    return np_(t).view(np.uint8) ^ 0x80
+
+
+def _layer_case(ql, orc, n_in, H, P, T, B, seed, h0c0=False, taps=True):
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(n_in, H, 1, proj=P, seed=seed)["layers"][0]
+    rng = np.random.default_rng(seed + 100)
+    x = rng.standard_normal((T, B, n_in)).astype(np.float32)
+    R = P if P else H
+    h0 = c0 = None
+    if h0c0:
+        h0 = (np.tanh(rng.standard_normal((B, R))) * 0.5).astype(np.float32)
+        c0 = rng.standard_normal((B, H)).astype(np.float32)
+    L = ql.quantize_layer(w)
+    g = ql.lstm_layer_forward(L, torch.from_numpy(x).cuda(),
+                              None if h0 is None else torch.from_numpy(h0).cuda(),
+                              None if c0 is None else torch.from_numpy(c0).cuda(), taps=taps)
+    o = orc.lstm_layer_forward(orc.quantize_layer(w), x, h0, c0, taps=taps)
+    return g, o
+
+
+def _assert_layer(g, o, P):
+    assert np.array_equal(np_(g["acc_x"]), o["acc_x"])
+    assert np.array_equal(np_(g["acc_h"]), o["acc_h"])
+    if P:
+        assert np.array_equal(np_(g["acc_r"]), o["acc_r"])
+    assert np.array_equal(u8(g["h_codes"]), o["h_codes"])
+    assert np.array_equal(np_(g["h_zero"]), o["h_zero"])
+    assert np.array_equal(np_(g["h_inv_q"]), o["h_inv_q"])
+    for k in ("h", "hT", "cT"):
+        assert np.max(np.abs(np_(g[k]) - o[k])) <= TOL, k
+        assert np.array_equal(np_(g[k]), o[k]), k   # the fp32 chain is bit-exact
+
+
+def test_lstm_layer_500_cells_T300_B1(ql, orc):
+    """One LSTM layer of 500 cells on 320-dim stacked features, T=300, B=1,
+    W_x 2000x320 and W_h 2000x500 ~ U[-0.08, 0.08] (per-gate quantized)."""
+    from paper_1607_04683_amd.workloads import LSTM1x500_T300_B1 as W_, model_weights, features
+    w = model_weights(W_)[0]["layers"][0]
+    x = features(W_)
+    L = ql.quantize_layer(w)
+    g = ql.lstm_layer_forward(L, torch.from_numpy(x).cuda(), taps=True)
+    o = orc.lstm_layer_forward(orc.quantize_layer(w), x, taps=True)
+    _assert_layer(g, o, 0)
+
+
+@pytest.mark.parametrize("n_in,H,P,T,B", [(50, 37, 0, 13, 1), (50, 37, 0, 13, 3),
+                                          (64, 40, 0, 9, 20), (33, 64, 24, 9, 2),
+                                          (33, 64, 24, 9, 17), (130, 129, 0, 5, 64)])
+def test_lstm_layer_shapes(ql, orc, n_in, H, P, T, B):
+    g, o = _layer_case(ql, orc, n_in, H, P, T, B, seed=n_in + H + P + T + B)
+    _assert_layer(g, o, P)
+
+
+@pytest.mark.parametrize("P", [0, 16])
+def test_lstm_layer_h0_c0(ql, orc, P):
+    g, o = _layer_case(ql, orc, 24, 32, P, 6, 18, seed=5, h0c0=True)
+    _assert_layer(g, o, P)
+
+
+def test_lstm_layer_chunked_streaming(ql):
+    """(hT, cT) -> (h0, c0) across two calls equals one call, bit for bit."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, 48, 1, proj=0, seed=11)["layers"][0]
+    L = ql.quantize_layer(w)
+    x = torch.randn(20, 4, 40, device="cuda")
+    full = ql.lstm_layer_forward(L, x)
+    a = ql.lstm_layer_forward(L, x[:8])
+    b = ql.lstm_layer_forward(L, x[8:], a["hT"], a["cT"])
+    assert torch.equal(torch.cat([a["h"], b["h"]]), full["h"])
+    assert torch.equal(b["cT"], full["cT"])
+
+
+def test_lstm_layer_empty(ql):
+    from paper_1607_04683_amd.workloads import random_model
+    L = ql.quantize_layer(random_model(8, 8, 1, seed=1)["layers"][0])
+    out = ql.lstm_layer_forward(L, torch.empty(0, 3, 8, device="cuda"))
+    assert out["h"].shape == (0, 3, 8)
+
+
+def _model_case(ql, orc, weights, feats, utts=None, taps=("h_codes",)):
+    Mg = ql.quantize_model(weights)
+    g = ql.acoustic_model_forward(Mg, torch.from_numpy(feats).cuda(), taps=taps)
+    sel = slice(None) if utts is None else list(utts)
+    fo = feats if utts is None else np.ascontiguousarray(feats[:, sel])
+    o = orc.acoustic_model_forward(orc.quantize_model(weights), fo, taps=True)
+    for l, lt in enumerate(g["layers"]):
+        got = u8(lt["h_codes"])[:, sel]
+        assert np.array_equal(got, o["layers"][l]["h_codes"]), f"layer {l} codes"
+    post = np_(g["post"])[:, sel]
+    err = np.max(np.abs(post - o["post"]))
+    assert err <= TOL, err
+    return g, o
+
+
+def test_model_small_all_taps(ql, orc):
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(32, 40, 2, states=300, seed=21)
+    x = np.random.default_rng(1).standard_normal((7, 3, 32)).astype(np.float32)
+    g, o = _model_case(ql, orc, w, x, taps=True)
+    assert np.array_equal(np_(g["acc_y"]), o["acc_y"])
+    assert np.array_equal(np_(g["logits"]), o["logits"])
+    for l in range(2):
+        assert np.array_equal(np_(g["layers"][l]["acc_h"]), o["layers"][l]["acc_h"])
+    p = np_(g["post"]).astype(np.float64)
+    assert np.max(np.abs(p.sum(-1) - 1.0)) < 1e-5
+
+
+def test_model_5x500_softmax8192_T500_B1(ql, orc):
+    """Five 500-cell layers + 8192-way quantized softmax, T=500, batch 1."""
+    from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T500_B1 as W_, model_weights, features
+    _model_case(ql, orc, model_weights(W_)[0], features(W_))
+
+
+def test_model_5x500_softmax8192_T1000_B64_sampled(ql, orc):
+    """Batch 64 x T=1000 on the GPU; the oracle recomputes two utterances
+    (per-vector quantization makes utterances independent)."""
+    from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T1000_B64 as W_, model_weights, features
+    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[0, 45])
+
+
+def test_model_4xlstmp2048_softmax16384_T800_B256_sampled(ql, orc):
+    """4 x LSTMP(2048 cells, P=512), 640-dim input, 16384-way softmax, batch 256
+    x T=800 on the GPU; the oracle recomputes one utterance."""
+    from paper_1607_04683_amd.workloads import (LSTMP4x2048P512_S16384_T800_B256 as W_,
+                                                model_weights, features)
+    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[131])
+
+
+def test_model_batch_invariance_and_determinism(ql):
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, 64, 2, states=500, seed=31)
+    M = ql.quantize_model(w)
+    x = torch.randn(12, 20, 40, device="cuda")
+    full = ql.acoustic_model_forward(M, x)["post"]
+    again = ql.acoustic_model_forward(M, x)["post"]
+    assert torch.equal(full, again)
+    for b in (0, 7, 19):
+        one = ql.acoustic_model_forward(M, x[:, b:b + 1].contiguous())["post"]
+        assert torch.equal(one[:, 0], full[:, b])
+
+
+def test_lstm_recurrence_entry_equals_layer_forward(ql):
+    """ql_lstm_recurrence on gx = R(Mult(Q(x), W_x')) + b (the per-row quantized
+    product with bias) reproduces ql_lstm_layer_forward bit for bit."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(48, 40, 1, proj=16, seed=41)["layers"][0]
+    L = ql.quantize_layer(w)
+    x = torch.randn(9, 18, 48, device="cuda")
+    ref = ql.lstm_layer_forward(L, x, taps=("acc_h", "h_codes"))
+    gx, _ = ql.quantized_matmul(L.Wx, x.reshape(-1, 48), ql.QL_ACT_PER_ROW, L.bias)
+    got = ql.lstm_recurrence(L, gx.reshape(9, 18, 4 * 40), taps=("acc_h", "h_codes"))
+    assert torch.equal(got["h"], ref["h"])
+    assert torch.equal(got["acc_h"], ref["acc_h"])
+    assert torch.equal(got["h_codes"], ref["h_codes"])
+
+
+def test_model_empty(ql):
+    from paper_1607_04683_amd.workloads import random_model
+    M = ql.quantize_model(random_model(8, 8, 1, states=5, seed=2))
+    out = ql.acoustic_model_forward(M, torch.empty(0, 2, 8, device="cuda"))
+    assert out["post"].shape == (0, 2, 5)
