@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Throughput of quantized LSTM acoustic-model inference on one MI355X.
+
+One step = one full forward pass of the acoustic model (activation
+quantization, hoisted input products, the recurrence of every layer and the
+quantized softmax output layer) over one batch of synthetic frames already
+resident in HBM.  The headline value is frames/s of the 5-layer 500-cell
+model with an 8192-way softmax at batch 64 x T=1000.  Also reported: the same
+model at batch 1 (streaming latency case), the 4-layer LSTMP(2048, P=512)
+model with a 16384-way softmax at batch 256 x T=800, the raw 8-bit GEMM
+sweep (M=N=K in {4096, 8192}), the dominant kernel against its roofline, and
+the CPU oracle timed on this host's cores on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--skip-cpu] [--quick]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "quantized LSTM AM frames/sec at batch 1 and 64; int8 GEMM TOPS vs MFMA peak"
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--skip-cpu", action="store_true", help="do not time the CPU oracle")
+    ap.add_argument("--quick", action="store_true", help="headline workload only")
+    ap.add_argument("--cpu-frames", type=int, default=8000,
+                    help="frames of the batch-64 workload the CPU oracle is timed on")
+    return ap.parse_args()
+
+
+class Timer:
+    """HIP events on torch's current stream (the stream the library launches on)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def __enter__(self):
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        self.b.synchronize()
+        self.ms = self.a.elapsed_time(self.b)
+
+
+def model_on_device(ql, workload, torch):
+    from paper_1607_04683_amd import workloads as wl
+    w, _ = wl.model_weights(workload)
+    M = ql.quantize_model(w, device="cuda")
+    x = torch.from_numpy(wl.features(workload)).cuda()
+    return w, M, x
+
+
+def time_model(ql, torch, M, x, steps, warmup):
+    """ms per forward pass (events + wall clock), posteriors preallocated."""
+    T, B, _ = x.shape
+    ws = ql.Workspace()
+    post = torch.empty(T, B, M.Wy.rows, dtype=torch.float32, device="cuda")
+    for _ in range(warmup):
+        ql.acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "warmup")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with Timer(torch) as tm:
+        for _ in range(steps):
+            ql.acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "timed steps")
+    return tm.ms / steps, wall / steps
+
+
+def recurrence_kernel(ql, torch, M, x, reps):
+    """Average duration of one persistent-recurrence launch (layer 2 of the
+    model, its real input pre-activations), by HIP events around each call."""
+    T, B, _ = x.shape
+    L1, L2 = M.layers[0], M.layers[1]
+    h1 = ql.lstm_layer_forward(L1, x)["h"]
+    gx, _ = ql.quantized_matmul(L2.Wx, h1.reshape(T * B, -1), ql.QL_ACT_PER_ROW, L2.bias)
+    gx = gx.reshape(T, B, -1)
+    ws = ql.Workspace()
+    out = {"h": torch.empty(T, B, L2.width, dtype=torch.float32, device="cuda")}
+    for _ in range(2):
+        ql.lstm_recurrence(L2, gx, workspace=ws, out=out, check=False)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        with Timer(torch) as tm:
+            ql.lstm_recurrence(L2, gx, workspace=ws, out=out, check=False)
+        ms.append(tm.ms)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "recurrence")
+    H, R = L2.hidden, L2.width
+    wh_bytes = 4 * H * R                       # W_h' codes streamed once per step
+    alg = (T * wh_bytes                        # weights, per step (decode-style)
+           + T * B * 4 * H * 4                 # read W_x x + b (fp32)
+           + T * B * R * 4                     # write h (fp32)
+           + T * B * R + T * B * 12)           # write codes of h + per-row params
+    avg = sum(ms) / len(ms)
+    return dict(avg_ms=avg, min_ms=min(ms), alg_bytes=alg, per_step_us=avg * 1e3 / T,
+                wh_bytes_per_step=wh_bytes)
+
+
+def gemm_sweep(ql, torch, n, reps):
+    from paper_1607_04683_amd import workloads as wl
+    A, Bm = wl.gemm_operands(n, n, n, seed=0)
+    Ad, Bd = ql.device_codes(A), ql.device_codes(Bm)
+    sa = torch.from_numpy(A.sum(1, dtype="int64").astype("int32")).cuda()
+    sb = torch.from_numpy(Bm.sum(1, dtype="int64").astype("int32")).cuda()
+    Cm = torch.empty(n, n, dtype=torch.int32, device="cuda")
+    for _ in range(2):
+        ql.gemm_u8(Ad, Bd, n, sa, sb, out=Cm)
+    torch.cuda.synchronize()
+    with Timer(torch) as tm:
+        for _ in range(reps):
+            ql.gemm_u8(Ad, Bd, n, sa, sb, out=Cm)
+    ms = tm.ms / reps
+    tops = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    return dict(n=n, ms=ms, tops=tops, frac_of_peak=tops / INT8_PEAK_TOPS)
+
+
+def cpu_baseline(workload, frames):
+    """The oracle (untuned) on a bounded sample of the same workload: the first
+    `frames` frames of the first utterances (utterances are independent)."""
+    import numpy as np
+
+    from oracle import oracle
+    from paper_1607_04683_amd import workloads as wl
+    w, _ = wl.model_weights(workload)
+    n_utt = min(workload.B, max(1, int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))))
+    T = max(1, min(workload.T, frames // n_utt))
+    x = wl.features(workload, utterances=list(range(n_utt)))[:T]
+    Mq = oracle.quantize_model(w)
+    oracle.lib()
+    t0 = time.perf_counter()
+    oracle.acoustic_model_forward(Mq, np.ascontiguousarray(x))
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return dict(value=T * n_utt / dt, unit="frames/s", cores=cores, kind="oracle",
+                sample=f"{n_utt} utterances x {T} frames of the batch-64 workload "
+                       f"({T * n_utt} frames, {dt:.1f} s, {cpu})")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested). Utterances are independent, so a "
+              f"data-parallel run is N copies of this one.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_1607_04683_amd import qlstm as ql
+    from paper_1607_04683_amd import workloads as wl
+    ql.load()
+    torch.cuda.set_device(0)
+
+    # ---- headline: 5x500 + softmax 8192 at batch 64 x T=1000
+    W64 = wl.LSTM5x500_S8192_T1000_B64
+    log(f"setup {W64.name}")
+    _, M64, x64 = model_on_device(ql, W64, torch)
+    ms, wall_ms = time_model(ql, torch, M64, x64, args.steps, args.warmup)
+    frames = W64.T * W64.B
+    value = frames / (ms * 1e-3)
+    log(f"batch 64: {ms:.3f} ms/step (wall {wall_ms:.3f}) -> {value:.0f} frames/s")
+
+    rec = recurrence_kernel(ql, torch, M64, x64, reps=5)
+    achieved = rec["alg_bytes"] / (rec["avg_ms"] * 1e-3) / 1e9
+    log(f"recurrence kernel: {rec['avg_ms']:.3f} ms/launch, {rec['per_step_us']:.2f} us/step, "
+        f"{achieved:.1f} GB/s algorithmic")
+    roofline = dict(bound="hbm", kernel="k_recurrent (one 500-cell layer, B=64, T=1000)",
+                    achieved=round(achieved, 2), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 5), traffic=None,
+                    avg_launch_ms=round(rec["avg_ms"], 4), alg_bytes=rec["alg_bytes"])
+
+    extra = {}
+    if not args.quick:
+        W1 = wl.LSTM5x500_S8192_T500_B1
+        log(f"setup {W1.name}")
+        _, M1, x1 = model_on_device(ql, W1, torch)
+        ms1, _ = time_model(ql, torch, M1, x1, max(3, args.steps // 2), args.warmup)
+        rec1 = recurrence_kernel(ql, torch, M1, x1, reps=5)
+        extra["batch1"] = dict(workload=W1.name, ms_per_step=round(ms1, 3),
+                               frames_per_s=round(W1.T / (ms1 * 1e-3), 1),
+                               recurrence_us_per_step=round(rec1["per_step_us"], 3),
+                               wh_GBs=round(rec1["wh_bytes_per_step"] /
+                                            (rec1["per_step_us"] * 1e-6) / 1e9, 1))
+        log(f"batch 1: {extra['batch1']}")
+        del M1, x1
+        W5 = wl.LSTMP4x2048P512_S16384_T800_B256
+        log(f"setup {W5.name}")
+        _, M5, x5 = model_on_device(ql, W5, torch)
+        ms5, _ = time_model(ql, torch, M5, x5, 3, 1)
+        extra["lstmp_b256"] = dict(workload=W5.name, ms_per_step=round(ms5, 3),
+                                   frames_per_s=round(W5.T * W5.B / (ms5 * 1e-3), 1))
+        log(f"LSTMP batch 256: {extra['lstmp_b256']}")
+        del M5, x5
+        torch.cuda.empty_cache()
+        extra["gemm_sweep"] = [gemm_sweep(ql, torch, n, reps=10) for n in wl.GEMM_SWEEP]
+        for g in extra["gemm_sweep"]:
+            g.update({k: round(v, 4) for k, v in g.items() if isinstance(v, float)})
+        log(f"GEMM sweep: {extra['gemm_sweep']}")
+
+    cpu = None
+    if not args.skip_cpu:
+        log("timing the CPU oracle")
+        cpu = cpu_baseline(W64, args.cpu_frames)
+        cpu["value"] = round(cpu["value"], 2)
+        log(f"cpu baseline: {cpu}")
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": W64.name, "layers": 5, "cells": 500, "input": 320,
+                   "states": 8192, "batch": W64.B, "T": W64.T,
+                   "quantization": "uint8 weights per gate block, uint8 activations per vector"},
+        "roofline": roofline, "cpu_baseline": cpu, **extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -52,8 +52,11 @@ struct RowParam {
   int32_t z;
 };
 
+// Grid barrier.  The workgroup's own barrier orders every wave's stores before
+// thread 0's release (agent scope) on the counter; thread 0's acquire after
+// the wait orders the workgroup's later loads after every other workgroup's
+// release.  One release and one acquire per workgroup per barrier.
 __device__ __forceinline__ bool grid_sync(unsigned *ctr, int *flag, unsigned target) {
-  __threadfence();
   __syncthreads();
   __shared__ int s_to;
   if (threadIdx.x == 0) {
@@ -80,7 +83,7 @@ __device__ __forceinline__ bool grid_sync(unsigned *ctr, int *flag, unsigned tar
 }
 
 // Quantize one vector of K floats (src null = zeros) into LDS codes; one wave.
-// Returns params in every lane.
+// Two passes over src (used when a row does not fit the register path).
 __device__ __forceinline__ RowParam quantize_vec_wave(const float *src, int64_t K, int8_t *dst,
                                                       int ldpad, int lane, int32_t *sum_out) {
   float lo = INFINITY, hi = -INFINITY;
@@ -113,6 +116,99 @@ __device__ __forceinline__ RowParam quantize_vec_wave(const float *src, int64_t 
   r.sigx = sum - 128 * (int32_t)K;
   r.iqx = p.inv_q;
   return r;
+}
+
+// Quantize RB vectors of K <= 64*NV floats at once: every value is loaded
+// exactly once into registers (all RB rows' loads in flight together), then
+// min/max, params and codes come from registers.  srcs[r] null = zero vector.
+template <int NV, int RB>
+__device__ __forceinline__ void quantize_rows_regs(const float *const (&srcs)[RB], int K,
+                                                   int8_t *const (&dst)[RB], int ldpad, int lane,
+                                                   RowParam (&rp)[RB], int32_t (&sums)[RB]) {
+  float v[RB][NV];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = i * kWave + lane;
+      v[r][i] = (srcs[r] && k < K) ? srcs[r][k] : 0.0f;
+    }
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (i * kWave + lane < K) {
+        lo = fminf(lo, v[r][i]);
+        hi = fmaxf(hi, v[r][i]);
+      }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    if (!srcs[r] || K == 0) lo = hi = 0.0f;
+    const QParams p = make_qparams(lo, hi);
+    int sum = 0;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = i * kWave + lane;
+      int8_t b = 0;
+      if (k < K) {
+        const int c = encode(v[r][i], p.q, p.z);
+        sum += c;
+        b = (int8_t)(c ^ 0x80);
+      }
+      if (k < ldpad) dst[r][k] = b;
+    }
+    for (int k = NV * kWave + lane; k < ldpad; k += kWave) dst[r][k] = 0;
+    sum = wave_sum(sum);
+    sums[r] = sum;
+    rp[r].z = p.z;
+    rp[r].ztx = p.z + 128;
+    rp[r].sigx = sum - 128 * K;
+    rp[r].iqx = p.inv_q;
+  }
+}
+
+// Quantize rows [0, nrows) of a tile, rows handed round-robin to the waves;
+// row lb reads src_of(lb) (null = zeros) with K values, codes to
+// dst + lb * ldx.  Calls done(lb, param, sum) for every row (lane-uniform).
+template <class Src, class Done>
+__device__ __forceinline__ void quantize_tile_rows(int nrows, int K, int8_t *dst, int ldx,
+                                                   int ldpad, Src src_of, Done done) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
+  if (K <= 8 * kWave) {
+    constexpr int RB = 4;
+    for (int lb0 = wave * RB; lb0 < nrows; lb0 += nwave * RB) {
+      const float *srcs[RB];
+      int8_t *dsts[RB];
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const int lb = lb0 + r < nrows ? lb0 + r : nrows - 1;
+        srcs[r] = src_of(lb);
+        dsts[r] = dst + lb * ldx;
+      }
+      RowParam rp[RB];
+      int32_t sums[RB];
+      quantize_rows_regs<8, RB>(srcs, K, dsts, ldpad, lane, rp, sums);
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+        if (lb0 + r < nrows) done(lb0 + r, rp[r], sums[r]);
+    }
+  } else if (K <= 32 * kWave) {
+    for (int lb = wave; lb < nrows; lb += nwave) {
+      const float *srcs[1] = {src_of(lb)};
+      int8_t *dsts[1] = {dst + lb * ldx};
+      RowParam rp[1];
+      int32_t sums[1];
+      quantize_rows_regs<32, 1>(srcs, K, dsts, ldpad, lane, rp, sums);
+      done(lb, rp[0], sums[0]);
+    }
+  } else {
+    for (int lb = wave; lb < nrows; lb += nwave) {
+      int32_t sum;
+      const RowParam r = quantize_vec_wave(src_of(lb), K, dst + lb * ldx, ldpad, lane, &sum);
+      done(lb, r, sum);
+    }
+  }
 }
 
 // S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (multiple of 64), signed.
@@ -240,12 +336,11 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
 
     if (activeA) {
       // ---- 3. quantize h_{t-1} rows of this batch slice
-      for (int lb = wave; lb < tl.bB; lb += nwave) {
-        const float *src = nullptr;
-        if (lb < nb)
-          src = t == 0 ? (a.h0 ? a.h0 + (b0 + lb) * R : nullptr) : a.h + ((t - 1) * B + b0 + lb) * R;
-        int32_t sum;
-        const RowParam r = quantize_vec_wave(src, lb < nb ? R : 0, xc + lb * tl.ldsX, tl.ldR, lane, &sum);
+      auto src_h = [&](int lb) -> const float * {
+        if (lb >= nb) return nullptr;
+        return t == 0 ? (a.h0 ? a.h0 + (b0 + lb) * R : nullptr) : a.h + ((t - 1) * B + b0 + lb) * R;
+      };
+      auto done_h = [&](int lb, const RowParam &r, int32_t sum) {
         if (lane == 0) rp[lb] = r;
         if (t > 0 && tu == 0 && lb < nb) {  // codes of h_{t-1} for the next consumer
           const int64_t row = (t - 1) * B + b0 + lb;
@@ -261,7 +356,8 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
             if (a.tap_inv_q) a.tap_inv_q[row] = r.iqx;
           }
         }
-      }
+      };
+      quantize_tile_rows(tl.bB, (int)R, xc, tl.ldsX, tl.ldR, src_h, done_h);
       if (t < T) {
         __syncthreads();
         // ---- 4. Mult against the resident slice
@@ -315,12 +411,11 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
       const int nb2 = (int)(B - c0 < tl.bB2 ? B - c0 : tl.bB2);
       const int np2 = (int)(P - p0 < tl.p2 ? P - p0 : tl.p2);
       const int ldx2 = tl.ldH + 16;
-      for (int lb = wave; lb < tl.bB2; lb += nwave) {
-        int32_t sum;
-        const RowParam r = quantize_vec_wave(lb < nb2 ? mbuf + (c0 + lb) * H : nullptr,
-                                             lb < nb2 ? H : 0, xc + lb * ldx2, tl.ldH, lane, &sum);
+      auto src_m = [&](int lb) -> const float * { return lb < nb2 ? mbuf + (c0 + lb) * H : nullptr; };
+      auto done_m = [&](int lb, const RowParam &r, int32_t) {
         if (lane == 0) rp[lb] = r;
-      }
+      };
+      quantize_tile_rows(tl.bB2, (int)H, xc, ldx2, tl.ldH, src_m, done_m);
       __syncthreads();
       // W_r' rows p0 .. p0 + np2 - 1, read from global memory (L2 resident)
       const int8_t *wr = a.Wr.codes + p0 * a.Wr.ld;
