@@ -4,27 +4,39 @@
 // split into tiles of (bB batch rows) x (u hidden units); a workgroup owns one
 // tile for the whole sequence, keeps the 4u gate rows of W_h' it needs
 // resident in LDS, and keeps its cell state c in LDS.  Each step:
-//   1. (before waiting) prefetch its slice of the precomputed W_x x_t + b;
-//   2. grid barrier: h_{t-1} is complete;
-//   3. quantize h_{t-1} per vector for its batch rows (eq. 2) into LDS
-//      (redundantly in every unit tile: no extra barrier is needed);
-//   4. Mult: signed 8-bit products against the resident W_h' slice
+//   1. prefetch its slice of the precomputed W_x x_t + b;
+//   2. wait for h_{t-1} of its batch rows and quantize it per vector (eq. 2)
+//      into LDS (redundantly in every unit tile of the batch slice);
+//   3. Mult: signed 8-bit products against the resident W_h' slice
 //      (v_dot4 for one batch row, v_mfma_i32_16x16x64_i8 for 16+ rows);
-//   5. R(.) of eq. 1/3, + (W_x x + b), sigmoid/tanh gates, c and m update;
-//   6. with a projection: grid barrier, quantize m per vector, W_r' product,
-//      recover h_t.
+//   4. R(.) of eq. 1/3, + (W_x x + b), sigmoid/tanh gates, c and m update;
+//   5. with a projection: wait for m_t of the batch rows of a projection
+//      tile, quantize it per vector, W_r' product, recover h_t.
 // The workgroup whose unit tile is 0 also stores the codes of h_{t-1} (the
 // next layer's / output layer's input) so they are never recomputed.
 //
-// The grid barrier is a monotone counter.  Its wait is bounded: if it ever
-// expires, a flag in the workspace is raised and every workgroup returns at
-// its next barrier, so the grid always drains.
+// There is no grid barrier.  Values passed between workgroups inside the
+// launch (h_t, and m_t with a projection) are published as 64-bit words
+// (step tag << 32 | fp32 bits) with device-coherent atomic stores into a
+// double buffer indexed by step parity; a consumer polls the words it needs
+// until every tag equals the step it waits for.  One store and one poll per
+// exchange, no counters.  Small buffers are written to several replicas a few
+// KB apart and each consumer polls its own replica, so hundreds of
+// workgroups polling one short vector do not all queue on one memory channel.  Reuse of a buffer half is safe because producing
+// step t+2 requires every workgroup's step-t+1 values, which each workgroup
+// only publishes after it has finished reading step t.  Tags start from 1 and
+// the buffer is cleared before every launch.  Every wait is bounded: on expiry
+// a flag in the workspace is raised, and all workgroups leave at their next
+// wait, so the grid always drains.
 #include "ql_device.h"
 #include "ql_launch.h"
+
+#include <algorithm>
 
 namespace ql {
 
 constexpr long kSpinLimit = 1l << 22;
+constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -36,7 +48,10 @@ struct RecTiling {
   int ldR, ldH;     // padded widths of h and m codes
   int ldsW;         // LDS row stride of the W_h' slice
   int ldsX;         // LDS row stride of activation codes
-  size_t off_w, off_x, off_s, off_c, off_col, off_row, lds_bytes;
+  int reph, repm;   // replicas of the published h / m double buffers
+  int tc;           // steps of W_x x + b staged in LDS at a time (0: none)
+  int64_t strideh, stridem;  // 64-bit words between replicas
+  size_t off_w, off_x, off_s, off_c, off_col, off_row, off_gx, lds_bytes;
 };
 
 struct ColParam {
@@ -50,59 +65,75 @@ struct RowParam {
   int32_t ztx, sigx;
   float iqx;
   int32_t z;
+  int32_t sum;  // code sum (0..255 domain)
+  int32_t pad[3];
 };
 
-// Grid barrier.  The workgroup's own barrier orders every wave's stores before
-// thread 0's release (agent scope) on the counter; thread 0's acquire after
-// the wait orders the workgroup's later loads after every other workgroup's
-// release.  One release and one acquire per workgroup per barrier.
-__device__ __forceinline__ bool grid_sync(unsigned *ctr, int *flag, unsigned target) {
-  __syncthreads();
-  __shared__ int s_to;
-  if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    int to = 0;
-    long it = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-        to = 1;
-        break;
-      }
-      if (++it > kSpinLimit) {
-        __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        to = 1;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    s_to = to;
-  }
-  __syncthreads();
-  return s_to != 0;
+constexpr int kHdrFlag = 16;  // 32-bit word index of the timeout flag (byte 64)
+
+__device__ __forceinline__ uint64_t pack_tagged(uint32_t tag, float v) {
+  return ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v);
+}
+__device__ __forceinline__ void publish(uint64_t *p, uint32_t tag, float v) {
+  __hip_atomic_store(p, pack_tagged(tag, v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_tagged(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Quantize one vector of K floats (src null = zeros) into LDS codes; one wave.
-// Two passes over src (used when a row does not fit the register path).
-__device__ __forceinline__ RowParam quantize_vec_wave(const float *src, int64_t K, int8_t *dst,
-                                                      int ldpad, int lane, int32_t *sum_out) {
-  float lo = INFINITY, hi = -INFINITY;
-  if (src) {
-    for (int64_t i = lane; i < K; i += kWave) {
-      const float v = src[i];
-      lo = fminf(lo, v);
-      hi = fmaxf(hi, v);
-    }
-    lo = wave_min(lo);
-    hi = wave_max(hi);
+// Bounded-wait bookkeeping: true when the wait must be abandoned.
+__device__ __forceinline__ bool wait_expired(int *flag, long &it) {
+  if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+    return true;
+  if (it > kSpinLimit) {
+    __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
   }
-  if (!src || K == 0) lo = hi = 0.0f;
+  __builtin_amdgcn_s_sleep(1);
+  return false;
+}
+
+// Source of one vector to quantize: read directly (an input state), or poll a
+// published row until every word carries the expected tag; neither = zeros.
+struct RowSrc {
+  const float *plain;
+  const uint64_t *tagged;
+};
+
+// Quantize one vector of K floats into LDS codes; one wave.  For long rows:
+// waits until the whole row is published, then two passes over it.
+// Returns false if the wait expired.
+__device__ __forceinline__ bool quantize_vec_wave(RowSrc src, uint32_t tag, int K, int8_t *dst,
+                                                  int ldpad, int lane, int *flag, RowParam *out,
+                                                  int32_t *sum_out) {
+  if (src.tagged) {
+    long it = 0;
+    for (;;) {
+      bool ok = true;
+      for (int i = lane; i < K; i += kWave) ok = ok && (uint32_t)(ld_tagged(&src.tagged[i]) >> 32) == tag;
+      if (__all(ok)) break;
+      if (wait_expired(flag, it)) return false;
+    }
+  }
+  auto val = [&](int i) -> float {
+    if (src.tagged) return __uint_as_float((uint32_t)ld_tagged(&src.tagged[i]));
+    return src.plain ? src.plain[i] : 0.0f;
+  };
+  float lo = INFINITY, hi = -INFINITY;
+  for (int i = lane; i < K; i += kWave) {
+    const float v = val(i);
+    lo = fminf(lo, v);
+    hi = fmaxf(hi, v);
+  }
+  lo = wave_min(lo);
+  hi = wave_max(hi);
+  if ((!src.plain && !src.tagged) || K == 0) lo = hi = 0.0f;
   const QParams p = make_qparams(lo, hi);
   int sum = 0;
-  for (int64_t i = lane; i < ldpad; i += kWave) {
+  for (int i = lane; i < ldpad; i += kWave) {
     int8_t b = 0;
     if (i < K) {
-      const int c = encode(src ? src[i] : 0.0f, p.q, p.z);
+      const int c = encode(val(i), p.q, p.z);
       sum += c;
       b = (int8_t)(c ^ 0x80);
     }
@@ -110,29 +141,46 @@ __device__ __forceinline__ RowParam quantize_vec_wave(const float *src, int64_t 
   }
   sum = wave_sum(sum);
   *sum_out = sum;
-  RowParam r;
-  r.z = p.z;
-  r.ztx = p.z + 128;
-  r.sigx = sum - 128 * (int32_t)K;
-  r.iqx = p.inv_q;
-  return r;
+  out->z = p.z;
+  out->ztx = p.z + 128;
+  out->sigx = sum - 128 * K;
+  out->iqx = p.inv_q;
+  return true;
 }
 
 // Quantize RB vectors of K <= 64*NV floats at once: every value is loaded
-// exactly once into registers (all RB rows' loads in flight together), then
-// min/max, params and codes come from registers.  srcs[r] null = zero vector.
+// into registers (all RB rows' loads in flight together; tagged rows are
+// re-read until every tag matches), then min/max, params and codes come from
+// registers.  Returns false if the wait expired.
 template <int NV, int RB>
-__device__ __forceinline__ void quantize_rows_regs(const float *const (&srcs)[RB], int K,
+__device__ __forceinline__ bool quantize_rows_regs(const RowSrc (&src)[RB], uint32_t tag, int K,
                                                    int8_t *const (&dst)[RB], int ldpad, int lane,
-                                                   RowParam (&rp)[RB], int32_t (&sums)[RB]) {
+                                                   int *flag, RowParam (&rp)[RB],
+                                                   int32_t (&sums)[RB]) {
   float v[RB][NV];
+  long it = 0;
+  for (;;) {
+    bool ok = true;
 #pragma unroll
-  for (int r = 0; r < RB; ++r)
+    for (int r = 0; r < RB; ++r)
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int k = i * kWave + lane;
-      v[r][i] = (srcs[r] && k < K) ? srcs[r][k] : 0.0f;
-    }
+      for (int i = 0; i < NV; ++i) {
+        const int k = i * kWave + lane;
+        float x = 0.0f;
+        if (k < K) {
+          if (src[r].tagged) {
+            const uint64_t w = ld_tagged(&src[r].tagged[k]);
+            ok = ok && (uint32_t)(w >> 32) == tag;
+            x = __uint_as_float((uint32_t)w);
+          } else if (src[r].plain) {
+            x = src[r].plain[k];
+          }
+        }
+        v[r][i] = x;
+      }
+    if (__all(ok)) break;
+    if (wait_expired(flag, it)) return false;
+  }
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     float lo = INFINITY, hi = -INFINITY;
@@ -144,7 +192,7 @@ __device__ __forceinline__ void quantize_rows_regs(const float *const (&srcs)[RB
       }
     lo = wave_min(lo);
     hi = wave_max(hi);
-    if (!srcs[r] || K == 0) lo = hi = 0.0f;
+    if ((!src[r].plain && !src[r].tagged) || K == 0) lo = hi = 0.0f;
     const QParams p = make_qparams(lo, hi);
     int sum = 0;
 #pragma unroll
@@ -156,9 +204,10 @@ __device__ __forceinline__ void quantize_rows_regs(const float *const (&srcs)[RB
         sum += c;
         b = (int8_t)(c ^ 0x80);
       }
-      if (k < ldpad) dst[r][k] = b;
+      if (dst[r] && k < ldpad) dst[r][k] = b;
     }
-    for (int k = NV * kWave + lane; k < ldpad; k += kWave) dst[r][k] = 0;
+    if (dst[r])
+      for (int k = NV * kWave + lane; k < ldpad; k += kWave) dst[r][k] = 0;
     sum = wave_sum(sum);
     sums[r] = sum;
     rp[r].z = p.z;
@@ -166,49 +215,55 @@ __device__ __forceinline__ void quantize_rows_regs(const float *const (&srcs)[RB
     rp[r].sigx = sum - 128 * K;
     rp[r].iqx = p.inv_q;
   }
+  return true;
 }
 
 // Quantize rows [0, nrows) of a tile, rows handed round-robin to the waves;
-// row lb reads src_of(lb) (null = zeros) with K values, codes to
-// dst + lb * ldx.  Calls done(lb, param, sum) for every row (lane-uniform).
+// row lb comes from src_of(lb), codes to dst + lb * ldx.  Calls done(lb,
+// param, sum) for every row (lane-uniform).  Returns false (for this wave) if
+// a wait expired; the caller makes the whole workgroup leave together.
 template <class Src, class Done>
-__device__ __forceinline__ void quantize_tile_rows(int nrows, int K, int8_t *dst, int ldx,
-                                                   int ldpad, Src src_of, Done done) {
+__device__ __forceinline__ bool quantize_tile_rows(int nrows, int K, uint32_t tag, int8_t *dst,
+                                                   int ldx, int ldpad, int *flag, Src src_of,
+                                                   Done done) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
   if (K <= 8 * kWave) {
     constexpr int RB = 4;
     for (int lb0 = wave * RB; lb0 < nrows; lb0 += nwave * RB) {
-      const float *srcs[RB];
+      RowSrc srcs[RB];
       int8_t *dsts[RB];
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
-        const int lb = lb0 + r < nrows ? lb0 + r : nrows - 1;
-        srcs[r] = src_of(lb);
-        dsts[r] = dst + lb * ldx;
+        const bool valid = lb0 + r < nrows;
+        srcs[r] = valid ? src_of(lb0 + r) : RowSrc{nullptr, nullptr};
+        dsts[r] = valid ? dst + (lb0 + r) * ldx : nullptr;
       }
       RowParam rp[RB];
       int32_t sums[RB];
-      quantize_rows_regs<8, RB>(srcs, K, dsts, ldpad, lane, rp, sums);
+      if (!quantize_rows_regs<8, RB>(srcs, tag, K, dsts, ldpad, lane, flag, rp, sums)) return false;
 #pragma unroll
       for (int r = 0; r < RB; ++r)
         if (lb0 + r < nrows) done(lb0 + r, rp[r], sums[r]);
     }
   } else if (K <= 32 * kWave) {
     for (int lb = wave; lb < nrows; lb += nwave) {
-      const float *srcs[1] = {src_of(lb)};
-      int8_t *dsts[1] = {dst + lb * ldx};
+      const RowSrc srcs[1] = {src_of(lb)};
+      int8_t *const dsts[1] = {dst + lb * ldx};
       RowParam rp[1];
       int32_t sums[1];
-      quantize_rows_regs<32, 1>(srcs, K, dsts, ldpad, lane, rp, sums);
+      if (!quantize_rows_regs<32, 1>(srcs, tag, K, dsts, ldpad, lane, flag, rp, sums)) return false;
       done(lb, rp[0], sums[0]);
     }
   } else {
     for (int lb = wave; lb < nrows; lb += nwave) {
+      RowParam r;
       int32_t sum;
-      const RowParam r = quantize_vec_wave(src_of(lb), K, dst + lb * ldx, ldpad, lane, &sum);
+      if (!quantize_vec_wave(src_of(lb), tag, K, dst + lb * ldx, ldpad, lane, flag, &r, &sum))
+        return false;
       done(lb, r, sum);
     }
   }
+  return true;
 }
 
 // S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (multiple of 64), signed.
@@ -260,6 +315,33 @@ __device__ __forceinline__ void products_mfma(const int8_t *x, int ldx, int nb, 
   }
 }
 
+// Store the codes of h_{t-1} (held in LDS) and their params as the layer's
+// quantized output; the whole workgroup cooperates, 16 bytes per thread.
+__device__ __forceinline__ void store_codes(const RecurrentArgs &a, const RecTiling &tl,
+                                            const int8_t *xc, const RowParam *rp, int nb,
+                                            int64_t row0) {
+  const int chunks = (int)(a.ld_out / 16);
+  for (int idx = threadIdx.x; idx < nb * chunks; idx += blockDim.x) {
+    const int lb = idx / chunks, ch = idx % chunks;
+    const int64_t row = row0 + lb;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (ch * 16 < tl.ldR) v = *reinterpret_cast<const uint4 *>(xc + lb * tl.ldsX + ch * 16);
+    *reinterpret_cast<uint4 *>(a.out_codes + row * a.ld_out + ch * 16) = v;
+    if (ch == 0) {
+      a.out_zero[row] = rp[lb].z;
+      a.out_inv_q[row] = rp[lb].iqx;
+      a.out_sums[row] = rp[lb].sum;
+      if (a.tap_zero) a.tap_zero[row] = rp[lb].z;
+      if (a.tap_inv_q) a.tap_inv_q[row] = rp[lb].iqx;
+    }
+  }
+  if (a.tap_codes)
+    for (int idx = threadIdx.x; idx < nb * (int)a.R; idx += blockDim.x) {
+      const int lb = idx / (int)a.R, k = idx % (int)a.R;
+      a.tap_codes[(row0 + lb) * a.R + k] = xc[lb * tl.ldsX + k];
+    }
+}
+
 __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int8_t *wsl = reinterpret_cast<int8_t *>(smem + tl.off_w);
@@ -268,14 +350,18 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   float *cst = reinterpret_cast<float *>(smem + tl.off_c);
   ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_col);
   RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_row);
+  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);  // [tc][bB*u][4]
+  __shared__ int s_abort;
 
-  unsigned *ctr = static_cast<unsigned *>(a.ws);
-  int *flag = reinterpret_cast<int *>(static_cast<char *>(a.ws) + 64);
-  float *mbuf = reinterpret_cast<float *>(static_cast<char *>(a.ws) + 256);
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
   const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
-  const int G = gridDim.x;
+  int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
+  // replica c of the h exchange: xh + c * strideh, [2][B][R]; of m: xm + c * stridem, [2][B][H]
+  uint64_t *xh = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  uint64_t *xm = xh + tl.reph * tl.strideh;
+  const uint64_t *xh_mine = xh + (blockIdx.x % tl.reph) * tl.strideh;
+  const uint64_t *xm_mine = xm + (blockIdx.x % tl.repm) * tl.stridem;
+
+  const int tid = threadIdx.x, lane = tid & 63;
   const bool activeA = (int)blockIdx.x < tl.nbt * tl.nut;
   const int tb = activeA ? blockIdx.x / tl.nut : 0, tu = activeA ? blockIdx.x % tl.nut : 0;
   const int64_t b0 = (int64_t)tb * tl.bB, j0 = (int64_t)tu * tl.u;
@@ -283,6 +369,12 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   const int nu = activeA ? (int)(H - j0 < tl.u ? H - j0 : tl.u) : 0;
   const int nrows = 4 * tl.u;  // slice rows, gate-major: row g*u + jj
   const int ldS = nrows;
+  const bool activeB = P > 0 && (int)blockIdx.x < tl.nbt2 * tl.npt;
+  const int tb2 = activeB ? blockIdx.x / tl.npt : 0, tp = activeB ? blockIdx.x % tl.npt : 0;
+  const int64_t c0 = (int64_t)tb2 * tl.bB2, p0 = (int64_t)tp * tl.p2;
+  const int nb2 = activeB ? (int)(B - c0 < tl.bB2 ? B - c0 : tl.bB2) : 0;
+  const int np2 = activeB ? (int)(P - p0 < tl.p2 ? P - p0 : tl.p2) : 0;
+  if (tid == 0) s_abort = 0;
 
   // ---- prologue: resident W_h' slice, column params, initial c
   if (activeA) {
@@ -307,69 +399,66 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
     }
     for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) {
       const int lb = idx / tl.u, jj = idx % tl.u;
-      float c0 = 0.0f;
-      if (lb < nb && jj < nu && a.c0) c0 = a.c0[(b0 + lb) * H + j0 + jj];
-      cst[idx] = c0;
+      float cv = 0.0f;
+      if (lb < nb && jj < nu && a.c0) cv = a.c0[(b0 + lb) * H + j0 + jj];
+      cst[idx] = cv;
     }
   }
   __syncthreads();
 
-  unsigned nsync = 0;
   const int pairs = nb * nu;
-  const int ppt = (tl.bB * tl.u + blockDim.x - 1) / blockDim.x;  // pairs per thread (max)
 
   for (int64_t t = 0; t <= T; ++t) {
-    // prefetch W_x x_t + b for this thread's (b, j) pairs
-    float gxv[8][4];
-    if (t < T && activeA) {
-      for (int q = 0; q < ppt; ++q) {
-        const int idx = tid + q * blockDim.x;
-        if (idx < pairs) {
-          const int lb = idx / nu, jj = idx % nu;
-          const float *g = a.gx + ((t * B + b0 + lb) * 4 * H) + j0 + jj;
-#pragma unroll
-          for (int gg = 0; gg < 4; ++gg) gxv[q][gg] = g[gg * H];
+    const int64_t hcur = (t & 1) * B * R;                 // h_t is published here, tag t+1
+    const uint64_t *xh_prev = xh_mine + ((t + 1) & 1) * B * R;  // h_{t-1}, tag t
+    if (activeA) {
+      // ---- 1. every tc steps, stage W_x x + b of the next tc steps in LDS
+      // (one exposed memory latency per chunk instead of one per step)
+      if (tl.tc > 0 && t < T && t % tl.tc == 0) {
+        const int steps = (int)(T - t < tl.tc ? T - t : tl.tc);
+        for (int idx = tid; idx < steps * pairs * 4; idx += blockDim.x) {
+          const int s_ = idx / (pairs * 4), rem = idx % (pairs * 4);
+          const int pr = rem >> 2, gg = rem & 3;
+          const int lb = pr / nu, jj = pr % nu;
+          gxs[(s_ * pairs + pr) * 4 + gg] = a.gx[((t + s_) * B + b0 + lb) * 4 * H + gg * H + j0 + jj];
         }
       }
-    }
-    if (t > 0 && grid_sync(ctr, flag, (++nsync) * (unsigned)G)) return;
-
-    if (activeA) {
-      // ---- 3. quantize h_{t-1} rows of this batch slice
-      auto src_h = [&](int lb) -> const float * {
-        if (lb >= nb) return nullptr;
-        return t == 0 ? (a.h0 ? a.h0 + (b0 + lb) * R : nullptr) : a.h + ((t - 1) * B + b0 + lb) * R;
+      // ---- 2. h_{t-1} of this batch slice, quantized per vector
+      auto src_h = [&](int lb) -> RowSrc {
+        RowSrc r{nullptr, nullptr};
+        if (lb < nb) {
+          if (t == 0)
+            r.plain = a.h0 ? a.h0 + (b0 + lb) * R : nullptr;
+          else
+            r.tagged = xh_prev + (b0 + lb) * R;
+        }
+        return r;
       };
       auto done_h = [&](int lb, const RowParam &r, int32_t sum) {
-        if (lane == 0) rp[lb] = r;
-        if (t > 0 && tu == 0 && lb < nb) {  // codes of h_{t-1} for the next consumer
-          const int64_t row = (t - 1) * B + b0 + lb;
-          int8_t *oc = a.out_codes + row * a.ld_out;
-          for (int64_t i = lane; i < a.ld_out; i += kWave) oc[i] = i < tl.ldR ? xc[lb * tl.ldsX + i] : 0;
-          if (a.tap_codes)
-            for (int64_t i = lane; i < R; i += kWave) a.tap_codes[row * R + i] = xc[lb * tl.ldsX + i];
-          if (lane == 0) {
-            a.out_zero[row] = r.z;
-            a.out_inv_q[row] = r.iqx;
-            a.out_sums[row] = sum;
-            if (a.tap_zero) a.tap_zero[row] = r.z;
-            if (a.tap_inv_q) a.tap_inv_q[row] = r.iqx;
-          }
+        if (lane == 0) {
+          rp[lb] = r;
+          rp[lb].sum = sum;
         }
       };
-      quantize_tile_rows(tl.bB, (int)R, xc, tl.ldsX, tl.ldR, src_h, done_h);
-      if (t < T) {
-        __syncthreads();
-        // ---- 4. Mult against the resident slice
+      if (!quantize_tile_rows(tl.bB, (int)R, (uint32_t)t, xc, tl.ldsX, tl.ldR, flag, src_h, done_h))
+        s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      if (t == T) {
+        if (tu == 0) store_codes(a, tl, xc, rp, nb, (T - 1) * B + b0);
+        break;
+      }
+      {
+        // ---- 3. Mult against the resident slice
         if (tl.mfmaA)
           products_mfma(xc, tl.ldsX, tl.bB, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
         else
           products_valu(xc, tl.ldsX, nb, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
         __syncthreads();
-        // ---- 5. recover, gates, cell update
-        for (int q = 0; q < ppt; ++q) {
-          const int idx = tid + q * blockDim.x;
-          if (idx >= pairs) break;
+        // ---- 4. recover, gates, cell update; publish h_t (or m_t)
+        const int64_t mcur = (t & 1) * B * H;
+        const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
+        for (int idx = tid; idx < pairs; idx += blockDim.x) {
           const int lb = idx / nu, jj = idx % nu;
           const RowParam r = rp[lb];
           const int64_t b = b0 + lb, j = j0 + jj;
@@ -380,7 +469,8 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
             const ColParam c = cp[n];
             const int32_t sv = S[lb * ldS + n];
             const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
-            av[gg] = gxv[q][gg] + yh;
+            const float gxv = gxt ? gxt[idx * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
+            av[gg] = gxv + yh;
             if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
           }
           const float ig = sigmoid_cw(av[0]);
@@ -391,32 +481,37 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
           cst[lb * tl.u + jj] = cn;
           const float m = og * tanh_cw(cn);
           if (P == 0) {
+            for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
             a.h[(t * B + b) * R + j] = m;
             if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
           } else {
-            mbuf[b * H + j] = m;
+            for (int c = 0; c < tl.repm; ++c) publish(&xm[c * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
           }
           if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
         }
+        // the codes of h_{t-1} become the layer's quantized output
+        if (t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
       }
     }
     if (t == T) break;
-    if (P == 0) continue;
 
-    // ---- 6. projection h_t = R(Mult(Q(m_t), W_r'))
-    if (grid_sync(ctr, flag, (++nsync) * (unsigned)G)) return;
-    if ((int)blockIdx.x < tl.nbt2 * tl.npt) {
-      const int tb2 = blockIdx.x / tl.npt, tp = blockIdx.x % tl.npt;
-      const int64_t c0 = (int64_t)tb2 * tl.bB2, p0 = (int64_t)tp * tl.p2;
-      const int nb2 = (int)(B - c0 < tl.bB2 ? B - c0 : tl.bB2);
-      const int np2 = (int)(P - p0 < tl.p2 ? P - p0 : tl.p2);
+    // ---- 5. projection h_t = R(Mult(Q(m_t), W_r'))
+    if (activeB) {
       const int ldx2 = tl.ldH + 16;
-      auto src_m = [&](int lb) -> const float * { return lb < nb2 ? mbuf + (c0 + lb) * H : nullptr; };
+      const uint64_t *xm_cur = xm_mine + (t & 1) * B * H;
+      __syncthreads();  // LDS codes / params of phase 4 are no longer read
+      auto src_m = [&](int lb) -> RowSrc {
+        RowSrc r{nullptr, nullptr};
+        if (lb < nb2) r.tagged = xm_cur + (c0 + lb) * H;
+        return r;
+      };
       auto done_m = [&](int lb, const RowParam &r, int32_t) {
         if (lane == 0) rp[lb] = r;
       };
-      quantize_tile_rows(tl.bB2, (int)H, xc, ldx2, tl.ldH, src_m, done_m);
+      if (!quantize_tile_rows(tl.bB2, (int)H, (uint32_t)(t + 1), xc, ldx2, tl.ldH, flag, src_m, done_m))
+        s_abort = 1;
       __syncthreads();
+      if (s_abort) return;
       // W_r' rows p0 .. p0 + np2 - 1, read from global memory (L2 resident)
       const int8_t *wr = a.Wr.codes + p0 * a.Wr.ld;
       if (tl.mfmaB)
@@ -434,29 +529,55 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
         const int64_t colterm = (int64_t)sigw + H * (int64_t)ztw;
         const int32_t sv = S[lb * tl.p2 + pp];
         const float hv = recover(sv, colterm, ztw, r.ztx, r.sigx, iqw, r.iqx);
+        for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * P + p], (uint32_t)(t + 1), hv);
         a.h[(t * B + b) * P + p] = hv;
         if (t == T - 1 && a.hT) a.hT[b * P + p] = hv;
         if (a.acc_r) a.acc_r[(t * B + b) * P + p] = acc_u8(sv, sigw, r.sigx, H);
       }
-      __syncthreads();
     }
+    __syncthreads();  // LDS of this step is free before the next step's quantization
   }
 }
 
-// Clears the first `words` 32-bit words of the header: 16 = the barrier
-// counter only, 32 = counter and timeout flag.
-__global__ void k_zero_header(unsigned *p, int words) {
-  if ((int)threadIdx.x < words) p[threadIdx.x] = 0u;
+// Clears the exchange buffers (n64 64-bit words after the header); the
+// timeout flag only when asked (once per API call).
+__global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0 && with_flag) hdr[kHdrFlag] = 0u;
+  uint64_t *x = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(hdr) + kHeaderBytes);
+  for (int64_t k = i; k < n64; k += (int64_t)gridDim.x * blockDim.x) x[k] = 0;
 }
 
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s) {
-  hipLaunchKernelGGL(k_zero_header, dim3(1), dim3(64), 0, s, static_cast<unsigned *>(ws), 32);
+  hipLaunchKernelGGL(k_clear_exchange, dim3(1), dim3(64), 0, s, static_cast<unsigned *>(ws),
+                     (int64_t)0, 1);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ host side
+constexpr int kMaxReplicas = 4;
+constexpr int kPublishBudget = 2048;  // values x replicas a workgroup publishes per step
+
+// 64-bit words between replicas of a double buffer of `words` words: a
+// multiple of 64 KB plus 4 KB, so replicas start on different channels.
+static int64_t replica_stride(int64_t words) { return round_up(words, 8192) + 512; }
+
+static int64_t exchange_words(int64_t B, int64_t H, int64_t P) {
+  const int64_t R = P > 0 ? P : H;
+  int64_t n = kMaxReplicas * replica_stride(2 * B * R);
+  if (P > 0) n += kMaxReplicas * replica_stride(2 * B * H);
+  return n;
+}
+
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P) {
-  return 256 + align_up((size_t)(P > 0 ? B * H : 0) * sizeof(float), 256);
+  return kHeaderBytes + align_up((size_t)exchange_words(B, H, P) * sizeof(uint64_t), 256);
+}
+
+static int replicas(int values_per_block, int consumers) {
+  int r = kPublishBudget / (values_per_block > 0 ? values_per_block : 1);
+  r = r < consumers ? r : consumers;
+  r = r < kMaxReplicas ? r : kMaxReplicas;
+  return r > 0 ? r : 1;
 }
 
 static int device_cus(int *lds_max) {
@@ -525,6 +646,15 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
     // W_r rows read in 16-row groups must stay inside the matrix
     if (a.Wr.ld < tl.ldH) return false;
   }
+  // replicas of the published buffers (consumers of one batch row: the unit
+  // tiles of its slice for h, the projection tiles for m)
+  {
+    const int hvals = P > 0 ? tl.bB2 * tl.p2 : tl.bB * tl.u;
+    tl.reph = replicas(hvals, tl.nut);
+    tl.repm = P > 0 ? replicas(tl.bB * tl.u, tl.npt) : 1;
+    tl.strideh = replica_stride(2 * B * a.R);
+    tl.stridem = P > 0 ? replica_stride(2 * B * H) : 0;
+  }
   tl.grid = tl.nbt * tl.nut;
   if (P > 0 && tl.nbt2 * tl.npt > tl.grid) tl.grid = tl.nbt2 * tl.npt;
   if (tl.grid > G) return false;
@@ -555,10 +685,19 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
   const int rows_rp = tl.bB > tl.bB2 ? tl.bB : tl.bB2;
   tl.off_row = off;
   off = align_up(off + (size_t)rows_rp * sizeof(RowParam), 16);
+  // W_x x + b staging: as many steps as fit (up to 64), at least one
+  {
+    const size_t per_step = (size_t)tl.bB * tl.u * 4 * sizeof(float);
+    const size_t room = (size_t)lds_max - 64 > off ? (size_t)lds_max - 64 - off : 0;
+    int64_t tc = (int64_t)(room / per_step);
+    tc = tc > 64 ? 64 : tc;
+    tc = tc > a.T ? a.T : tc;
+    tl.tc = tc > 0 ? (int)tc : 0;  // 0: read W_x x + b straight from memory
+    tl.off_gx = off;
+    off = align_up(off + per_step * tl.tc, 16);
+  }
   tl.lds_bytes = off;
   if (tl.lds_bytes + 64 > (size_t)lds_max) return false;  // + static shared (barrier flag)
-  // the per-thread gx prefetch holds up to 8 (b, j) pairs
-  if ((tl.bB * tl.u + 255) / 256 > 8) return false;
   *out = tl;
   return true;
 }
@@ -584,7 +723,10 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
     *unsupported = true;
     return hipSuccess;
   }
-  hipLaunchKernelGGL(k_zero_header, dim3(1), dim3(64), 0, s, static_cast<unsigned *>(a.ws), 16);
+  const int64_t n64 = tl.reph * tl.strideh + tl.repm * tl.stridem;
+  const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
+  hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(a.ws),
+                     n64, 0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   RecurrentArgs args = a;
