@@ -91,12 +91,15 @@ __device__ __forceinline__ QParams make_qparams(float vmin_f, float vmax_f) {
   return p;
 }
 
-// eq. 2: V' = round(Q V) - round(Q Vmin), kept in [0, 255].
+// eq. 2: V' = round(Q V) - round(Q Vmin), kept in [0, 255].  round() is
+// floor(x) + (x - floor(x) >= 0.5); floor(x) is integral with |x| <= 2^24
+// (the range rule bounds Q max|V|), so its int conversion is exact.
 __device__ __forceinline__ int encode(float v, double q, int32_t z) {
-  double c = round_half_up(q * (double)v) - (double)z;
-  c = c < 0.0 ? 0.0 : c;
-  c = c > 255.0 ? 255.0 : c;
-  return (int)c;
+  const double x = q * (double)v;
+  const double r = floor(x);
+  int c = (int)r - z + ((x - r) >= 0.5 ? 1 : 0);
+  c = c < 0 ? 0 : c;
+  return c > 255 ? 255 : c;
 }
 
 // Pack four codes (0..255) into the device layout (V' - 128 per byte).
@@ -123,22 +126,39 @@ __device__ __forceinline__ int32_t acc_u8(int32_t S, int32_t sigw, int32_t sigx,
 }
 
 // ---------------------------------------------------------------------------
-// Wavefront (64-lane) reductions.
+// Wavefront (64-lane) reductions with DPP: shifts within 16-lane rows, then
+// row broadcasts; the result is read from lane 63 and is the same in every
+// lane.  min/max are exact in any order, integer sums too.
 // ---------------------------------------------------------------------------
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROWS, 0xf, false);
+}
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+
+template <class Op>
+__device__ __forceinline__ int wave_reduce_i(int v, int identity, Op op) {
+  v = op(v, dpp_i<kRowShr1, 0xf>(identity, v));
+  v = op(v, dpp_i<kRowShr2, 0xf>(identity, v));
+  v = op(v, dpp_i<kRowShr4, 0xf>(identity, v));
+  v = op(v, dpp_i<kRowShr8, 0xf>(identity, v));
+  v = op(v, dpp_i<kRowBcast15, 0xa>(v, v));
+  v = op(v, dpp_i<kRowBcast31, 0xc>(v, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
 __device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
-  return v;
+  return __int_as_float(wave_reduce_i(__float_as_int(v), __float_as_int(INFINITY), [](int a, int b) {
+    return __float_as_int(fminf(__int_as_float(a), __int_as_float(b)));
+  }));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  return __int_as_float(wave_reduce_i(__float_as_int(v), __float_as_int(-INFINITY), [](int a, int b) {
+    return __float_as_int(fmaxf(__int_as_float(a), __int_as_float(b)));
+  }));
 }
 __device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return wave_reduce_i(v, 0, [](int a, int b) { return a + b; });
 }
 
 }  // namespace ql

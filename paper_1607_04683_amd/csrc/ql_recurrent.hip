@@ -37,6 +37,7 @@ namespace ql {
 
 constexpr long kSpinLimit = 1l << 22;
 constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
+constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -65,22 +66,20 @@ struct RowParam {
   int32_t ztx, sigx;
   float iqx;
   int32_t z;
-  int32_t sum;  // code sum (0..255 domain)
+  int32_t sum;      // code sum (0..255 domain)
   int32_t pad[3];
 };
 
-constexpr int kHdrFlag = 16;  // 32-bit word index of the timeout flag (byte 64)
-
-__device__ __forceinline__ uint64_t pack_tagged(uint32_t tag, float v) {
-  return ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v);
-}
+// ---------------------------------------------------------------------------
+// Exchange between workgroups (see the file comment).
+// ---------------------------------------------------------------------------
 __device__ __forceinline__ void publish(uint64_t *p, uint32_t tag, float v) {
-  __hip_atomic_store(p, pack_tagged(tag, v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p, ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint64_t ld_tagged(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
 // Bounded-wait bookkeeping: true when the wait must be abandoned.
 __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
   if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
@@ -93,96 +92,56 @@ __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
   return false;
 }
 
-// Source of one vector to quantize: read directly (an input state), or poll a
-// published row until every word carries the expected tag; neither = zeros.
-struct RowSrc {
-  const float *plain;
-  const uint64_t *tagged;
-};
-
-// Quantize one vector of K floats into LDS codes; one wave.  For long rows:
-// waits until the whole row is published, then two passes over it.
-// Returns false if the wait expired.
-__device__ __forceinline__ bool quantize_vec_wave(RowSrc src, uint32_t tag, int K, int8_t *dst,
-                                                  int ldpad, int lane, int *flag, RowParam *out,
-                                                  int32_t *sum_out) {
-  if (src.tagged) {
+// ---------------------------------------------------------------------------
+// Per-vector quantization (eq. 2) of RB consecutive rows by one wave.
+// Rows [0, nvalid) are read from `src` (row stride `stride` elements): as
+// published words carrying `tag` when TAGGED (re-read until every tag
+// matches), else as plain floats (src null = zeros).  Rows [nvalid, ntotal)
+// are zero vectors.  Each lane holds values k = i*64 + lane, i < NV, so all
+// of a group's loads are in flight together; min/max, params, codes and the
+// code sum come from registers.  Codes go to dst + r*ldx (ldpad bytes), row
+// params to rp[r].  Returns false if the wait expired.
+// ---------------------------------------------------------------------------
+template <int NV, int RB, bool TAGGED>
+__device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int nvalid,
+                                           int ntotal, uint32_t tag, int K, int8_t *dst,
+                                           int ldx, int ldpad, int *flag, RowParam *rp) {
+  const int lane = threadIdx.x & 63;
+  float v[RB][NV];
+  if (TAGGED) {
+    const uint64_t *base = static_cast<const uint64_t *>(src);
     long it = 0;
     for (;;) {
-      bool ok = true;
-      for (int i = lane; i < K; i += kWave) ok = ok && (uint32_t)(ld_tagged(&src.tagged[i]) >> 32) == tag;
-      if (__all(ok)) break;
+      uint32_t bad = 0;
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+          const int k = i * kWave + lane;
+          float x = 0.0f;
+          if (r < nvalid && k < K) {
+            const uint64_t w = ld_tagged(base + r * stride + k);
+            bad |= (uint32_t)(w >> 32) ^ tag;
+            x = __uint_as_float((uint32_t)w);
+          }
+          v[r][i] = x;
+        }
+      if (!__any(bad != 0)) break;
       if (wait_expired(flag, it)) return false;
     }
-  }
-  auto val = [&](int i) -> float {
-    if (src.tagged) return __uint_as_float((uint32_t)ld_tagged(&src.tagged[i]));
-    return src.plain ? src.plain[i] : 0.0f;
-  };
-  float lo = INFINITY, hi = -INFINITY;
-  for (int i = lane; i < K; i += kWave) {
-    const float v = val(i);
-    lo = fminf(lo, v);
-    hi = fmaxf(hi, v);
-  }
-  lo = wave_min(lo);
-  hi = wave_max(hi);
-  if ((!src.plain && !src.tagged) || K == 0) lo = hi = 0.0f;
-  const QParams p = make_qparams(lo, hi);
-  int sum = 0;
-  for (int i = lane; i < ldpad; i += kWave) {
-    int8_t b = 0;
-    if (i < K) {
-      const int c = encode(val(i), p.q, p.z);
-      sum += c;
-      b = (int8_t)(c ^ 0x80);
-    }
-    dst[i] = b;
-  }
-  sum = wave_sum(sum);
-  *sum_out = sum;
-  out->z = p.z;
-  out->ztx = p.z + 128;
-  out->sigx = sum - 128 * K;
-  out->iqx = p.inv_q;
-  return true;
-}
-
-// Quantize RB vectors of K <= 64*NV floats at once: every value is loaded
-// into registers (all RB rows' loads in flight together; tagged rows are
-// re-read until every tag matches), then min/max, params and codes come from
-// registers.  Returns false if the wait expired.
-template <int NV, int RB>
-__device__ __forceinline__ bool quantize_rows_regs(const RowSrc (&src)[RB], uint32_t tag, int K,
-                                                   int8_t *const (&dst)[RB], int ldpad, int lane,
-                                                   int *flag, RowParam (&rp)[RB],
-                                                   int32_t (&sums)[RB]) {
-  float v[RB][NV];
-  long it = 0;
-  for (;;) {
-    bool ok = true;
+  } else {
+    const float *base = static_cast<const float *>(src);
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         const int k = i * kWave + lane;
-        float x = 0.0f;
-        if (k < K) {
-          if (src[r].tagged) {
-            const uint64_t w = ld_tagged(&src[r].tagged[k]);
-            ok = ok && (uint32_t)(w >> 32) == tag;
-            x = __uint_as_float((uint32_t)w);
-          } else if (src[r].plain) {
-            x = src[r].plain[k];
-          }
-        }
-        v[r][i] = x;
+        v[r][i] = (base && r < nvalid && k < K) ? base[r * stride + k] : 0.0f;
       }
-    if (__all(ok)) break;
-    if (wait_expired(flag, it)) return false;
   }
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
+    if (r >= ntotal) break;
     float lo = INFINITY, hi = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
@@ -192,9 +151,10 @@ __device__ __forceinline__ bool quantize_rows_regs(const RowSrc (&src)[RB], uint
       }
     lo = wave_min(lo);
     hi = wave_max(hi);
-    if ((!src[r].plain && !src[r].tagged) || K == 0) lo = hi = 0.0f;
+    if (r >= nvalid || (!TAGGED && !src) || K == 0) lo = hi = 0.0f;
     const QParams p = make_qparams(lo, hi);
     int sum = 0;
+    int8_t *d = dst + r * ldx;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int k = i * kWave + lane;
@@ -204,70 +164,45 @@ __device__ __forceinline__ bool quantize_rows_regs(const RowSrc (&src)[RB], uint
         sum += c;
         b = (int8_t)(c ^ 0x80);
       }
-      if (dst[r] && k < ldpad) dst[r][k] = b;
+      if (k < ldpad) d[k] = b;
     }
-    if (dst[r])
-      for (int k = NV * kWave + lane; k < ldpad; k += kWave) dst[r][k] = 0;
+    for (int k = NV * kWave + lane; k < ldpad; k += kWave) d[k] = 0;
     sum = wave_sum(sum);
-    sums[r] = sum;
-    rp[r].z = p.z;
-    rp[r].ztx = p.z + 128;
-    rp[r].sigx = sum - 128 * K;
-    rp[r].iqx = p.inv_q;
-  }
-  return true;
-}
-
-// Quantize rows [0, nrows) of a tile, rows handed round-robin to the waves;
-// row lb comes from src_of(lb), codes to dst + lb * ldx.  Calls done(lb,
-// param, sum) for every row (lane-uniform).  Returns false (for this wave) if
-// a wait expired; the caller makes the whole workgroup leave together.
-template <class Src, class Done>
-__device__ __forceinline__ bool quantize_tile_rows(int nrows, int K, uint32_t tag, int8_t *dst,
-                                                   int ldx, int ldpad, int *flag, Src src_of,
-                                                   Done done) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
-  if (K <= 8 * kWave) {
-    constexpr int RB = 4;
-    for (int lb0 = wave * RB; lb0 < nrows; lb0 += nwave * RB) {
-      RowSrc srcs[RB];
-      int8_t *dsts[RB];
-#pragma unroll
-      for (int r = 0; r < RB; ++r) {
-        const bool valid = lb0 + r < nrows;
-        srcs[r] = valid ? src_of(lb0 + r) : RowSrc{nullptr, nullptr};
-        dsts[r] = valid ? dst + (lb0 + r) * ldx : nullptr;
-      }
-      RowParam rp[RB];
-      int32_t sums[RB];
-      if (!quantize_rows_regs<8, RB>(srcs, tag, K, dsts, ldpad, lane, flag, rp, sums)) return false;
-#pragma unroll
-      for (int r = 0; r < RB; ++r)
-        if (lb0 + r < nrows) done(lb0 + r, rp[r], sums[r]);
-    }
-  } else if (K <= 32 * kWave) {
-    for (int lb = wave; lb < nrows; lb += nwave) {
-      const RowSrc srcs[1] = {src_of(lb)};
-      int8_t *const dsts[1] = {dst + lb * ldx};
-      RowParam rp[1];
-      int32_t sums[1];
-      if (!quantize_rows_regs<32, 1>(srcs, tag, K, dsts, ldpad, lane, flag, rp, sums)) return false;
-      done(lb, rp[0], sums[0]);
-    }
-  } else {
-    for (int lb = wave; lb < nrows; lb += nwave) {
-      RowParam r;
-      int32_t sum;
-      if (!quantize_vec_wave(src_of(lb), tag, K, dst + lb * ldx, ldpad, lane, flag, &r, &sum))
-        return false;
-      done(lb, r, sum);
+    if (lane == 0) {
+      RowParam q;
+      q.z = p.z;
+      q.ztx = p.z + 128;
+      q.sigx = sum - 128 * K;
+      q.iqx = p.inv_q;
+      q.sum = sum;
+      rp[r] = q;
     }
   }
   return true;
 }
 
-// S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (multiple of 64), signed.
-// VALU path: groups of 16 lanes per (row, n) task, v_dot4 on 16-byte chunks.
+// All rows [0, ntotal) of a tile, RB-row groups handed round-robin to waves;
+// rows [0, nvalid) are real.  row_src(lb) gives the source of row lb.
+template <int NV, bool TAGGED, class RowSrcFn>
+__device__ __forceinline__ bool quant_tile(int nvalid, int ntotal, int64_t stride, uint32_t tag,
+                                           int K, int8_t *dst, int ldx, int ldpad, int *flag,
+                                           RowParam *rp, RowSrcFn row_src) {
+  constexpr int RB = NV <= 8 ? 4 : 1;
+  const int wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
+  for (int lb0 = wave * RB; lb0 < ntotal; lb0 += nwave * RB) {
+    const int nv = nvalid - lb0 < 0 ? 0 : (nvalid - lb0 < RB ? nvalid - lb0 : RB);
+    const int nt = ntotal - lb0 < RB ? ntotal - lb0 : RB;
+    if (!quant_rows<NV, RB, TAGGED>(row_src(lb0), stride, nv, nt, tag, K, dst + lb0 * ldx, ldx,
+                                    ldpad, flag, rp + lb0))
+      return false;
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// Products S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (a multiple of 64).
+// ---------------------------------------------------------------------------
+// VALU: groups of 16 lanes per (row, n) task, v_dot4 on 16-byte chunks.
 __device__ __forceinline__ void products_valu(const int8_t *x, int ldx, int nb, const int8_t *w,
                                               int64_t ldw, int nrows, int wrows, int K, int32_t *S,
                                               int ldS) {
@@ -292,7 +227,7 @@ __device__ __forceinline__ void products_valu(const int8_t *x, int ldx, int nb, 
   }
 }
 
-// MFMA path: nb (multiple of 16) rows x nrows (multiple of 16) outputs.
+// MFMA: nb (multiple of 16) rows x nrows (multiple of 16) outputs.
 __device__ __forceinline__ void products_mfma(const int8_t *x, int ldx, int nb, const int8_t *w,
                                               int64_t ldw, int nrows, int wrows, int K, int32_t *S,
                                               int ldS) {
@@ -342,6 +277,12 @@ __device__ __forceinline__ void store_codes(const RecurrentArgs &a, const RecTil
     }
 }
 
+// ---------------------------------------------------------------------------
+// The persistent kernel.  NVA / NVB: values per lane of an h / m row (8 for
+// widths <= 512, 32 for <= 2048; NVB = 0 without projection); MFA / MFB: MFMA
+// (16+ batch rows per tile) or v_dot4 products.
+// ---------------------------------------------------------------------------
+template <int NVA, bool MFA, int NVB, bool MFB>
 __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int8_t *wsl = reinterpret_cast<int8_t *>(smem + tl.off_w);
@@ -350,7 +291,7 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   float *cst = reinterpret_cast<float *>(smem + tl.off_c);
   ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_col);
   RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_row);
-  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);  // [tc][bB*u][4]
+  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);  // [tc][pairs][4]
   __shared__ int s_abort;
 
   const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
@@ -361,7 +302,7 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   const uint64_t *xh_mine = xh + (blockIdx.x % tl.reph) * tl.strideh;
   const uint64_t *xm_mine = xm + (blockIdx.x % tl.repm) * tl.stridem;
 
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x;
   const bool activeA = (int)blockIdx.x < tl.nbt * tl.nut;
   const int tb = activeA ? blockIdx.x / tl.nut : 0, tu = activeA ? blockIdx.x % tl.nut : 0;
   const int64_t b0 = (int64_t)tb * tl.bB, j0 = (int64_t)tu * tl.u;
@@ -369,7 +310,8 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   const int nu = activeA ? (int)(H - j0 < tl.u ? H - j0 : tl.u) : 0;
   const int nrows = 4 * tl.u;  // slice rows, gate-major: row g*u + jj
   const int ldS = nrows;
-  const bool activeB = P > 0 && (int)blockIdx.x < tl.nbt2 * tl.npt;
+  const int rowsA = MFA ? tl.bB : nb;  // rows quantized (MFMA tiles need zero padding rows)
+  const bool activeB = NVB > 0 && (int)blockIdx.x < tl.nbt2 * tl.npt;
   const int tb2 = activeB ? blockIdx.x / tl.npt : 0, tp = activeB ? blockIdx.x % tl.npt : 0;
   const int64_t c0 = (int64_t)tb2 * tl.bB2, p0 = (int64_t)tp * tl.p2;
   const int nb2 = activeB ? (int)(B - c0 < tl.bB2 ? B - c0 : tl.bB2) : 0;
@@ -407,13 +349,10 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   __syncthreads();
 
   const int pairs = nb * nu;
-
   for (int64_t t = 0; t <= T; ++t) {
-    const int64_t hcur = (t & 1) * B * R;                 // h_t is published here, tag t+1
-    const uint64_t *xh_prev = xh_mine + ((t + 1) & 1) * B * R;  // h_{t-1}, tag t
+    const int64_t hcur = (t & 1) * B * R;  // h_t is published here with tag t+1
     if (activeA) {
       // ---- 1. every tc steps, stage W_x x + b of the next tc steps in LDS
-      // (one exposed memory latency per chunk instead of one per step)
       if (tl.tc > 0 && t < T && t % tl.tc == 0) {
         const int steps = (int)(T - t < tl.tc ? T - t : tl.tc);
         for (int idx = tid; idx < steps * pairs * 4; idx += blockDim.x) {
@@ -424,97 +363,85 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
         }
       }
       // ---- 2. h_{t-1} of this batch slice, quantized per vector
-      auto src_h = [&](int lb) -> RowSrc {
-        RowSrc r{nullptr, nullptr};
-        if (lb < nb) {
-          if (t == 0)
-            r.plain = a.h0 ? a.h0 + (b0 + lb) * R : nullptr;
-          else
-            r.tagged = xh_prev + (b0 + lb) * R;
-        }
-        return r;
-      };
-      auto done_h = [&](int lb, const RowParam &r, int32_t sum) {
-        if (lane == 0) {
-          rp[lb] = r;
-          rp[lb].sum = sum;
-        }
-      };
-      if (!quantize_tile_rows(tl.bB, (int)R, (uint32_t)t, xc, tl.ldsX, tl.ldR, flag, src_h, done_h))
-        s_abort = 1;
+      bool ok;
+      if (t == 0) {
+        ok = quant_tile<NVA, false>(nb, rowsA, R, 0u, (int)R, xc, tl.ldsX, tl.ldR, flag, rp,
+                                    [&](int lb) -> const void * {
+                                      return a.h0 ? a.h0 + (b0 + lb) * R : nullptr;
+                                    });
+      } else {
+        const uint64_t *prev = xh_mine + ((t + 1) & 1) * B * R;
+        ok = quant_tile<NVA, true>(nb, rowsA, R, (uint32_t)t, (int)R, xc, tl.ldsX, tl.ldR, flag, rp,
+                                   [&](int lb) -> const void * { return prev + (b0 + lb) * R; });
+      }
+      if (!ok) s_abort = 1;
       __syncthreads();
       if (s_abort) return;
       if (t == T) {
         if (tu == 0) store_codes(a, tl, xc, rp, nb, (T - 1) * B + b0);
         break;
       }
-      {
-        // ---- 3. Mult against the resident slice
-        if (tl.mfmaA)
-          products_mfma(xc, tl.ldsX, tl.bB, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
-        else
-          products_valu(xc, tl.ldsX, nb, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
-        __syncthreads();
-        // ---- 4. recover, gates, cell update; publish h_t (or m_t)
-        const int64_t mcur = (t & 1) * B * H;
-        const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
-        for (int idx = tid; idx < pairs; idx += blockDim.x) {
-          const int lb = idx / nu, jj = idx % nu;
-          const RowParam r = rp[lb];
-          const int64_t b = b0 + lb, j = j0 + jj;
-          float av[4];
+      // ---- 3. Mult against the resident slice
+      if (MFA)
+        products_mfma(xc, tl.ldsX, tl.bB, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
+      else
+        products_valu(xc, tl.ldsX, nb, wsl, tl.ldsW, nrows, nrows, tl.ldR, S, ldS);
+      __syncthreads();
+      // ---- 4. recover, gates, cell update; publish h_t (or m_t)
+      const int64_t mcur = (t & 1) * B * H;
+      const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
+      for (int idx = tid; idx < pairs; idx += blockDim.x) {
+        const int lb = idx / nu, jj = idx % nu;
+        const RowParam r = rp[lb];
+        const int64_t b = b0 + lb, j = j0 + jj;
+        float av[4];
 #pragma unroll
-          for (int gg = 0; gg < 4; ++gg) {
-            const int n = gg * tl.u + jj;
-            const ColParam c = cp[n];
-            const int32_t sv = S[lb * ldS + n];
-            const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
-            const float gxv = gxt ? gxt[idx * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
-            av[gg] = gxv + yh;
-            if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
-          }
-          const float ig = sigmoid_cw(av[0]);
-          const float fg = sigmoid_cw(av[1]);
-          const float gv = tanh_cw(av[2]);
-          const float og = sigmoid_cw(av[3]);
-          const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
-          cst[lb * tl.u + jj] = cn;
-          const float m = og * tanh_cw(cn);
-          if (P == 0) {
-            for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
-            a.h[(t * B + b) * R + j] = m;
-            if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
-          } else {
-            for (int c = 0; c < tl.repm; ++c) publish(&xm[c * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
-          }
-          if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
+        for (int gg = 0; gg < 4; ++gg) {
+          const int n = gg * tl.u + jj;
+          const ColParam c = cp[n];
+          const int32_t sv = S[lb * ldS + n];
+          const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
+          const float gxv = gxt ? gxt[idx * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
+          av[gg] = gxv + yh;
+          if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
         }
-        // the codes of h_{t-1} become the layer's quantized output
-        if (t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
+        const float ig = sigmoid_cw(av[0]);
+        const float fg = sigmoid_cw(av[1]);
+        const float gv = tanh_cw(av[2]);
+        const float og = sigmoid_cw(av[3]);
+        const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
+        cst[lb * tl.u + jj] = cn;
+        const float m = og * tanh_cw(cn);
+        if (NVB == 0) {
+          for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
+          a.h[(t * B + b) * R + j] = m;
+          if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
+        } else {
+          for (int c = 0; c < tl.repm; ++c) publish(&xm[c * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
+        }
+        if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
       }
+      // the codes of h_{t-1} become the layer's quantized output
+      if (t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
     }
     if (t == T) break;
 
     // ---- 5. projection h_t = R(Mult(Q(m_t), W_r'))
-    if (activeB) {
+    if (NVB > 0 && activeB) {
       const int ldx2 = tl.ldH + 16;
-      const uint64_t *xm_cur = xm_mine + (t & 1) * B * H;
+      const uint64_t *mrows = xm_mine + (t & 1) * B * H;
+      const int rowsB = MFB ? tl.bB2 : nb2;
       __syncthreads();  // LDS codes / params of phase 4 are no longer read
-      auto src_m = [&](int lb) -> RowSrc {
-        RowSrc r{nullptr, nullptr};
-        if (lb < nb2) r.tagged = xm_cur + (c0 + lb) * H;
-        return r;
-      };
-      auto done_m = [&](int lb, const RowParam &r, int32_t) {
-        if (lane == 0) rp[lb] = r;
-      };
-      if (!quantize_tile_rows(tl.bB2, (int)H, (uint32_t)(t + 1), xc, ldx2, tl.ldH, flag, src_m, done_m))
-        s_abort = 1;
+      const bool ok = quant_tile<NVB, true>(nb2, rowsB, H, (uint32_t)(t + 1), (int)H, xc, ldx2,
+                                            tl.ldH, flag, rp, [&](int lb) -> const void * {
+                                              return mrows + (c0 + lb) * H;
+                                            });
+      if (!ok) s_abort = 1;
       __syncthreads();
       if (s_abort) return;
       // W_r' rows p0 .. p0 + np2 - 1, read from global memory (L2 resident)
       const int8_t *wr = a.Wr.codes + p0 * a.Wr.ld;
-      if (tl.mfmaB)
+      if (MFB)
         products_mfma(xc, ldx2, tl.bB2, wr, a.Wr.ld, tl.p2, np2, tl.ldH, S, tl.p2);
       else
         products_valu(xc, ldx2, nb2, wr, a.Wr.ld, tl.p2, np2, tl.ldH, S, tl.p2);
@@ -702,9 +629,27 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
   return true;
 }
 
+using RecKernel = void (*)(RecurrentArgs, RecTiling);
+
+// The instantiation for a shape class: row widths up to 512 or 2048 values.
+static RecKernel pick_kernel(const RecurrentArgs &a, const RecTiling &tl) {
+  const bool wideR = a.R > 512, wideH = a.H > 512;
+  if (a.P == 0) {
+    if (tl.mfmaA) return wideR ? k_recurrent<32, true, 0, false> : k_recurrent<8, true, 0, false>;
+    return wideR ? k_recurrent<32, false, 0, false> : k_recurrent<8, false, 0, false>;
+  }
+  if (wideR) return nullptr;  // projection widths above 512 are not instantiated
+  if (tl.mfmaA) return wideH ? k_recurrent<8, true, 32, true> : k_recurrent<8, true, 8, true>;
+  return wideH ? k_recurrent<8, false, 32, false> : k_recurrent<8, false, 8, false>;
+}
+
 hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsupported) {
   *unsupported = false;
   if (a.T == 0 || a.B == 0) return hipSuccess;
+  if (a.R > 2048 || a.H > 2048) {  // one h / m row is held in 32 registers per lane
+    *unsupported = true;
+    return hipSuccess;
+  }
   int lds_max = 0;
   const int cus = device_cus(&lds_max);
   RecTiling tl;
@@ -712,12 +657,17 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
     *unsupported = true;
     return hipSuccess;
   }
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_recurrent),
+  RecKernel kern = pick_kernel(a, tl);
+  if (!kern) {
+    *unsupported = true;
+    return hipSuccess;
+  }
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)tl.lds_bytes);
   if (e != hipSuccess) return e;
   int per_cu = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_recurrent, 256, tl.lds_bytes);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, tl.lds_bytes);
   if (e != hipSuccess) return e;
   if (per_cu * cus < tl.grid) {
     *unsupported = true;
@@ -731,8 +681,8 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
   if (e != hipSuccess) return e;
   RecurrentArgs args = a;
   void *kargs[] = {&args, &tl};
-  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(k_recurrent), dim3(tl.grid),
-                                    dim3(256), kargs, (unsigned)tl.lds_bytes, s);
+  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid), dim3(256),
+                                    kargs, (unsigned)tl.lds_bytes, s);
 }
 
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out) {
