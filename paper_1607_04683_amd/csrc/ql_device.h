@@ -147,6 +147,39 @@ __device__ __forceinline__ int wave_reduce_i(int v, int identity, Op op) {
   v = op(v, dpp_i<kRowBcast31, 0xc>(v, v));
   return __builtin_amdgcn_readlane(v, 63);
 }
+// N independent reductions at once: each DPP step is applied to all N values
+// before the next, so their latencies overlap.
+template <int N, class Op>
+__device__ __forceinline__ void wave_reduce_n(int (&v)[N], int identity, Op op) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowShr1, 0xf>(identity, v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowShr2, 0xf>(identity, v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowShr4, 0xf>(identity, v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowShr8, 0xf>(identity, v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowBcast15, 0xa>(v[i], v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_i<kRowBcast31, 0xc>(v[i], v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = __builtin_amdgcn_readlane(v[i], 63);
+}
+struct OpMinF {
+  __device__ int operator()(int a, int b) const {
+    return __float_as_int(fminf(__int_as_float(a), __int_as_float(b)));
+  }
+};
+struct OpMaxF {
+  __device__ int operator()(int a, int b) const {
+    return __float_as_int(fmaxf(__int_as_float(a), __int_as_float(b)));
+  }
+};
+struct OpAddI {
+  __device__ int operator()(int a, int b) const { return a + b; }
+};
+
 __device__ __forceinline__ float wave_min(float v) {
   return __int_as_float(wave_reduce_i(__float_as_int(v), __float_as_int(INFINITY), [](int a, int b) {
     return __float_as_int(fminf(__int_as_float(a), __int_as_float(b)));

@@ -38,6 +38,8 @@ namespace ql {
 constexpr long kSpinLimit = 1l << 22;
 constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
 constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
+constexpr int kMaxSlices = 256;    // arrival counters per kind and parity
+constexpr int kCounterBytes = 2 * 2 * kMaxSlices * 64;  // one 64-byte line per counter
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -80,6 +82,12 @@ __device__ __forceinline__ void publish(uint64_t *p, uint32_t tag, float v) {
 __device__ __forceinline__ uint64_t ld_tagged(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void st_coherent(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coherent(const float *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 // Bounded-wait bookkeeping: true when the wait must be abandoned.
 __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
   if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
@@ -92,23 +100,47 @@ __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
   return false;
 }
 
+// Counter protocol (batched tiles): after its coherent stores of step t have
+// completed (every wave waits for its own memory operations, then the
+// workgroup barrier), thread 0 adds 1 to the arrival counter of the batch
+// slice the values belong to; a consumer's thread 0 waits until the counter
+// of the slot holds uses * producers.  The stores precede the increment in
+// time, and the consumer's loads follow its observation of the count.
+__device__ __forceinline__ void arrive(unsigned *cnt) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Thread 0 waits for *cnt >= target; returns false (for thread 0) on expiry.
+__device__ __forceinline__ bool wait_count(const unsigned *cnt, unsigned target, int *flag) {
+  if (threadIdx.x != 0) return true;
+  long it = 0;
+  while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target)
+    if (wait_expired(flag, it)) return false;
+  return true;
+}
+
 // ---------------------------------------------------------------------------
 // Per-vector quantization (eq. 2) of RB consecutive rows by one wave.
 // Rows [0, nvalid) are read from `src` (row stride `stride` elements): as
-// published words carrying `tag` when TAGGED (re-read until every tag
-// matches), else as plain floats (src null = zeros).  Rows [nvalid, ntotal)
+// published words carrying `tag` (kSrcTagged: re-read until every tag
+// matches), as floats through device-coherent loads (kSrcCoherent: their
+// availability was already established), or as plain floats (kSrcPlain;
+// src null = zeros).  Rows [nvalid, ntotal)
 // are zero vectors.  Each lane holds values k = i*64 + lane, i < NV, so all
 // of a group's loads are in flight together; min/max, params, codes and the
 // code sum come from registers.  Codes go to dst + r*ldx (ldpad bytes), row
 // params to rp[r].  Returns false if the wait expired.
 // ---------------------------------------------------------------------------
-template <int NV, int RB, bool TAGGED>
+enum { kSrcPlain = 0, kSrcTagged = 1, kSrcCoherent = 2 };
+
+template <int NV, int RB, int MODE>
 __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int nvalid,
                                            int ntotal, uint32_t tag, int K, int8_t *dst,
                                            int ldx, int ldpad, int *flag, RowParam *rp) {
   const int lane = threadIdx.x & 63;
   float v[RB][NV];
-  if (TAGGED) {
+  if (MODE == kSrcTagged) {
     const uint64_t *base = static_cast<const uint64_t *>(src);
     long it = 0;
     for (;;) {
@@ -136,12 +168,16 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         const int k = i * kWave + lane;
-        v[r][i] = (base && r < nvalid && k < K) ? base[r * stride + k] : 0.0f;
+        float x = 0.0f;
+        if (base && r < nvalid && k < K)
+          x = MODE == kSrcCoherent ? ld_coherent(base + r * stride + k) : base[r * stride + k];
+        v[r][i] = x;
       }
   }
+  // lane-local min / max of every row, then all 2*RB wave reductions together
+  int mm[2 * RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
-    if (r >= ntotal) break;
     float lo = INFINITY, hi = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
@@ -149,32 +185,46 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
         lo = fminf(lo, v[r][i]);
         hi = fmaxf(hi, v[r][i]);
       }
-    lo = wave_min(lo);
-    hi = wave_max(hi);
-    if (r >= nvalid || (!TAGGED && !src) || K == 0) lo = hi = 0.0f;
-    const QParams p = make_qparams(lo, hi);
+    mm[r] = __float_as_int(lo);
+    mm[RB + r] = __float_as_int(-hi);  // max(x) = -min(-x): one reduction kind
+  }
+  wave_reduce_n<2 * RB>(mm, __float_as_int(INFINITY), OpMinF());
+  int sums[RB];
+  QParams prm[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    float lo = __int_as_float(mm[r]), hi = -__int_as_float(mm[RB + r]);
+    if (r >= nvalid || !src || K == 0) lo = hi = 0.0f;
+    prm[r] = make_qparams(lo, hi);
     int sum = 0;
     int8_t *d = dst + r * ldx;
+    const bool write = r < ntotal;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int k = i * kWave + lane;
       int8_t b = 0;
       if (k < K) {
-        const int c = encode(v[r][i], p.q, p.z);
+        const int c = encode(v[r][i], prm[r].q, prm[r].z);
         sum += c;
         b = (int8_t)(c ^ 0x80);
       }
-      if (k < ldpad) d[k] = b;
+      if (write && k < ldpad) d[k] = b;
     }
-    for (int k = NV * kWave + lane; k < ldpad; k += kWave) d[k] = 0;
-    sum = wave_sum(sum);
-    if (lane == 0) {
+    if (write)
+      for (int k = NV * kWave + lane; k < ldpad; k += kWave) d[k] = 0;
+    sums[r] = sum;
+  }
+  wave_reduce_n<RB>(sums, 0, OpAddI());
+  if (lane == 0) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      if (r >= ntotal) break;
       RowParam q;
-      q.z = p.z;
-      q.ztx = p.z + 128;
-      q.sigx = sum - 128 * K;
-      q.iqx = p.inv_q;
-      q.sum = sum;
+      q.z = prm[r].z;
+      q.ztx = prm[r].z + 128;
+      q.sigx = sums[r] - 128 * K;
+      q.iqx = prm[r].inv_q;
+      q.sum = sums[r];
       rp[r] = q;
     }
   }
@@ -183,16 +233,15 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
 
 // All rows [0, ntotal) of a tile, RB-row groups handed round-robin to waves;
 // rows [0, nvalid) are real.  row_src(lb) gives the source of row lb.
-template <int NV, bool TAGGED, class RowSrcFn>
+template <int NV, int RB, int MODE, class RowSrcFn>
 __device__ __forceinline__ bool quant_tile(int nvalid, int ntotal, int64_t stride, uint32_t tag,
                                            int K, int8_t *dst, int ldx, int ldpad, int *flag,
                                            RowParam *rp, RowSrcFn row_src) {
-  constexpr int RB = NV <= 8 ? 4 : 1;
   const int wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
   for (int lb0 = wave * RB; lb0 < ntotal; lb0 += nwave * RB) {
     const int nv = nvalid - lb0 < 0 ? 0 : (nvalid - lb0 < RB ? nvalid - lb0 : RB);
     const int nt = ntotal - lb0 < RB ? ntotal - lb0 : RB;
-    if (!quant_rows<NV, RB, TAGGED>(row_src(lb0), stride, nv, nt, tag, K, dst + lb0 * ldx, ldx,
+    if (!quant_rows<NV, RB, MODE>(row_src(lb0), stride, nv, nt, tag, K, dst + lb0 * ldx, ldx,
                                     ldpad, flag, rp + lb0))
       return false;
   }
@@ -296,8 +345,18 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
 
   const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
   int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
-  // replica c of the h exchange: xh + c * strideh, [2][B][R]; of m: xm + c * stridem, [2][B][H]
-  uint64_t *xh = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  constexpr bool CNT = MFA;  // batched tiles: counters + coherent floats; else tagged words
+  // arrival counters: [kind h/m][parity][slice], 64 bytes apart
+  unsigned *cnt = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  auto counter = [&](int kind, int64_t par, int slice) {
+    return cnt + ((kind * 2 + (int)par) * kMaxSlices + slice) * 16;
+  };
+  char *xdata = static_cast<char *>(a.ws) + kHeaderBytes + kCounterBytes;
+  // counter mode: h_t in xhf [2][B][R], m_t in xmf [2][B][H] (slot t & 1)
+  float *xhf = reinterpret_cast<float *>(xdata);
+  float *xmf = xhf + 2 * B * R;
+  // tagged mode: replica c of h: xh + c * strideh, [2][B][R]; of m: xm + c * stridem
+  uint64_t *xh = reinterpret_cast<uint64_t *>(xdata);
   uint64_t *xm = xh + tl.reph * tl.strideh;
   const uint64_t *xh_mine = xh + (blockIdx.x % tl.reph) * tl.strideh;
   const uint64_t *xm_mine = xm + (blockIdx.x % tl.repm) * tl.stridem;
@@ -311,11 +370,20 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   const int nrows = 4 * tl.u;  // slice rows, gate-major: row g*u + jj
   const int ldS = nrows;
   const int rowsA = MFA ? tl.bB : nb;  // rows quantized (MFMA tiles need zero padding rows)
+  // rows per wave-level group: several rows of a batched tile share one set of
+  // reductions; a one-row tile (v_dot4 path) uses single-row groups
+  constexpr int RBA = (MFA && NVA <= 8) ? 4 : 1;
+  constexpr int RBB = (MFB && NVB <= 8) ? 4 : 1;
   const bool activeB = NVB > 0 && (int)blockIdx.x < tl.nbt2 * tl.npt;
   const int tb2 = activeB ? blockIdx.x / tl.npt : 0, tp = activeB ? blockIdx.x % tl.npt : 0;
   const int64_t c0 = (int64_t)tb2 * tl.bB2, p0 = (int64_t)tp * tl.p2;
   const int nb2 = activeB ? (int)(B - c0 < tl.bB2 ? B - c0 : tl.bB2) : 0;
   const int np2 = activeB ? (int)(P - p0 < tl.p2 ? P - p0 : tl.p2) : 0;
+  const int tbB = activeB ? (int)(c0 / tl.bB) : 0;  // phase A slice holding these rows
+  // producers per slot use: of h for this slice, of m for the projection's slice
+  const unsigned prod_h =
+      NVB == 0 ? (unsigned)tl.nut : (unsigned)(((nb + tl.bB2 - 1) / tl.bB2) * tl.npt);
+  const unsigned prod_m = (unsigned)tl.nut;
   if (tid == 0) s_abort = 0;
 
   // ---- prologue: resident W_h' slice, column params, initial c
@@ -365,14 +433,26 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
       // ---- 2. h_{t-1} of this batch slice, quantized per vector
       bool ok;
       if (t == 0) {
-        ok = quant_tile<NVA, false>(nb, rowsA, R, 0u, (int)R, xc, tl.ldsX, tl.ldR, flag, rp,
+        ok = quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, R, 0u, (int)R, xc, tl.ldsX, tl.ldR, flag, rp,
                                     [&](int lb) -> const void * {
                                       return a.h0 ? a.h0 + (b0 + lb) * R : nullptr;
                                     });
+      } else if (CNT) {
+        const int64_t par = (t - 1) & 1;
+        if (!wait_count(counter(0, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod_h, flag)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+        const float *prev = xhf + par * B * R;
+        ok = quant_tile<NVA, RBA, kSrcCoherent>(nb, rowsA, R, 0u, (int)R, xc, tl.ldsX, tl.ldR, flag,
+                                                rp, [&](int lb) -> const void * {
+                                                  return prev + (b0 + lb) * R;
+                                                });
       } else {
         const uint64_t *prev = xh_mine + ((t + 1) & 1) * B * R;
-        ok = quant_tile<NVA, true>(nb, rowsA, R, (uint32_t)t, (int)R, xc, tl.ldsX, tl.ldR, flag, rp,
-                                   [&](int lb) -> const void * { return prev + (b0 + lb) * R; });
+        ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, R, (uint32_t)t, (int)R, xc, tl.ldsX, tl.ldR,
+                                              flag, rp, [&](int lb) -> const void * {
+                                                return prev + (b0 + lb) * R;
+                                              });
       }
       if (!ok) s_abort = 1;
       __syncthreads();
@@ -390,39 +470,51 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
       // ---- 4. recover, gates, cell update; publish h_t (or m_t)
       const int64_t mcur = (t & 1) * B * H;
       const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
-      for (int idx = tid; idx < pairs; idx += blockDim.x) {
-        const int lb = idx / nu, jj = idx % nu;
+      // four adjacent lanes per (b, j): lane g computes gate g (i, f, g, o);
+      // the cell update runs in the first lane of the quad
+      for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
+        const int pr = idx >> 2, gg = idx & 3;
+        const int lb = pr / nu, jj = pr % nu;
         const RowParam r = rp[lb];
         const int64_t b = b0 + lb, j = j0 + jj;
-        float av[4];
-#pragma unroll
-        for (int gg = 0; gg < 4; ++gg) {
-          const int n = gg * tl.u + jj;
-          const ColParam c = cp[n];
-          const int32_t sv = S[lb * ldS + n];
-          const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
-          const float gxv = gxt ? gxt[idx * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
-          av[gg] = gxv + yh;
-          if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
+        const int n = gg * tl.u + jj;
+        const ColParam c = cp[n];
+        const int32_t sv = S[lb * ldS + n];
+        const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
+        const float gxv = gxt ? gxt[pr * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
+        const float av = gxv + yh;
+        if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
+        // sigmoid for i, f, o; tanh(x) = 2 sigmoid(2x) - 1 for g
+        const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
+        const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
+        const int base = (threadIdx.x & 63) & ~3;
+        const float ig = __shfl(act, base + 0, 64);
+        const float fg = __shfl(act, base + 1, 64);
+        const float gv = __shfl(act, base + 2, 64);
+        const float og = __shfl(act, base + 3, 64);
+        if (gg == 0) {
+          const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
+          cst[lb * tl.u + jj] = cn;
+          const float m = og * tanh_cw(cn);
+          if (NVB == 0) {
+            if (CNT)
+              st_coherent(&xhf[hcur + b * R + j], m);
+            else
+              for (int c2 = 0; c2 < tl.reph; ++c2) publish(&xh[c2 * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
+            a.h[(t * B + b) * R + j] = m;
+            if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
+          } else {
+            if (CNT)
+              st_coherent(&xmf[mcur + b * H + j], m);
+            else
+              for (int c2 = 0; c2 < tl.repm; ++c2) publish(&xm[c2 * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
+          }
+          if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
         }
-        const float ig = sigmoid_cw(av[0]);
-        const float fg = sigmoid_cw(av[1]);
-        const float gv = tanh_cw(av[2]);
-        const float og = sigmoid_cw(av[3]);
-        const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
-        cst[lb * tl.u + jj] = cn;
-        const float m = og * tanh_cw(cn);
-        if (NVB == 0) {
-          for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
-          a.h[(t * B + b) * R + j] = m;
-          if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
-        } else {
-          for (int c = 0; c < tl.repm; ++c) publish(&xm[c * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
-        }
-        if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
       }
       // the codes of h_{t-1} become the layer's quantized output
       if (t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
+      if (CNT) arrive(counter(NVB == 0 ? 0 : 1, t & 1, tb));
     }
     if (t == T) break;
 
@@ -432,10 +524,22 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
       const uint64_t *mrows = xm_mine + (t & 1) * B * H;
       const int rowsB = MFB ? tl.bB2 : nb2;
       __syncthreads();  // LDS codes / params of phase 4 are no longer read
-      const bool ok = quant_tile<NVB, true>(nb2, rowsB, H, (uint32_t)(t + 1), (int)H, xc, ldx2,
-                                            tl.ldH, flag, rp, [&](int lb) -> const void * {
-                                              return mrows + (c0 + lb) * H;
-                                            });
+      bool ok;
+      if (CNT) {
+        if (!wait_count(counter(1, t & 1, tbB), (unsigned)((t >> 1) + 1) * prod_m, flag)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+        const float *mf = xmf + (t & 1) * B * H;
+        ok = quant_tile<NVB, RBB, kSrcCoherent>(nb2, rowsB, H, 0u, (int)H, xc, ldx2, tl.ldH, flag, rp,
+                                                [&](int lb) -> const void * {
+                                                  return mf + (c0 + lb) * H;
+                                                });
+      } else {
+        ok = quant_tile<NVB, RBB, kSrcTagged>(nb2, rowsB, H, (uint32_t)(t + 1), (int)H, xc, ldx2,
+                                              tl.ldH, flag, rp, [&](int lb) -> const void * {
+                                                return mrows + (c0 + lb) * H;
+                                              });
+      }
       if (!ok) s_abort = 1;
       __syncthreads();
       if (s_abort) return;
@@ -456,18 +560,22 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
         const int64_t colterm = (int64_t)sigw + H * (int64_t)ztw;
         const int32_t sv = S[lb * tl.p2 + pp];
         const float hv = recover(sv, colterm, ztw, r.ztx, r.sigx, iqw, r.iqx);
-        for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * P + p], (uint32_t)(t + 1), hv);
+        if (CNT)
+          st_coherent(&xhf[hcur + b * P + p], hv);
+        else
+          for (int c = 0; c < tl.reph; ++c) publish(&xh[c * tl.strideh + hcur + b * P + p], (uint32_t)(t + 1), hv);
         a.h[(t * B + b) * P + p] = hv;
         if (t == T - 1 && a.hT) a.hT[b * P + p] = hv;
         if (a.acc_r) a.acc_r[(t * B + b) * P + p] = acc_u8(sv, sigw, r.sigx, H);
       }
+      if (CNT) arrive(counter(0, t & 1, tbB));
     }
     __syncthreads();  // LDS of this step is free before the next step's quantization
   }
 }
 
-// Clears the exchange buffers (n64 64-bit words after the header); the
-// timeout flag only when asked (once per API call).
+// Clears the arrival counters and the exchange buffers (n64 64-bit words
+// after the header); the timeout flag only when asked (once per API call).
 __global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i == 0 && with_flag) hdr[kHdrFlag] = 0u;
@@ -491,9 +599,9 @@ static int64_t replica_stride(int64_t words) { return round_up(words, 8192) + 51
 
 static int64_t exchange_words(int64_t B, int64_t H, int64_t P) {
   const int64_t R = P > 0 ? P : H;
-  int64_t n = kMaxReplicas * replica_stride(2 * B * R);
+  int64_t n = kMaxReplicas * replica_stride(2 * B * R);  // >= the float buffers of counter mode
   if (P > 0) n += kMaxReplicas * replica_stride(2 * B * H);
-  return n;
+  return kCounterBytes / 8 + n;
 }
 
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P) {
@@ -534,19 +642,25 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
     tl.nut = (int)((H + tl.u - 1) / tl.u);
     ok = true;
   } else {
+    // Fewer unit tiles per batch slice means fewer re-reads of each h row per
+    // step; aim for at most 32 tiles, as long as the W_h' slice fits LDS.
     for (int bB = 16; bB <= 256 && !ok; bB *= 2) {
       const int nbt = (int)((B + bB - 1) / bB);
       if (nbt > G) continue;
-      const int nut = G / nbt;
-      int u = (int)((H + nut - 1) / nut);
-      u = (u + 3) / 4 * 4;
-      if ((size_t)4 * u * (tl.ldR + 16) > (size_t)lds_max / 2) continue;
-      tl.bB = bB;
-      tl.nbt = nbt;
-      tl.u = u;
-      tl.nut = (int)((H + u - 1) / u);
-      tl.mfmaA = 1;
-      ok = true;
+      const int max_nut = G / nbt;
+      for (int nut_target = 32; nut_target <= max_nut * 2 && !ok; nut_target *= 2) {
+        const int nut_try = nut_target < max_nut ? nut_target : max_nut;
+        int u = (int)((H + nut_try - 1) / nut_try);
+        u = (u + 3) / 4 * 4;
+        if ((size_t)4 * u * (tl.ldR + 16) > (size_t)lds_max / 2) continue;
+        if ((int64_t)nbt * ((H + u - 1) / u) > G) continue;
+        tl.bB = bB;
+        tl.nbt = nbt;
+        tl.u = u;
+        tl.nut = (int)((H + u - 1) / u);
+        tl.mfmaA = 1;
+        ok = true;
+      }
     }
   }
   if (!ok) return false;
@@ -582,6 +696,7 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
     tl.strideh = replica_stride(2 * B * a.R);
     tl.stridem = P > 0 ? replica_stride(2 * B * H) : 0;
   }
+  if (tl.nbt > kMaxSlices) return false;
   tl.grid = tl.nbt * tl.nut;
   if (P > 0 && tl.nbt2 * tl.npt > tl.grid) tl.grid = tl.nbt2 * tl.npt;
   if (tl.grid > G) return false;
@@ -673,7 +788,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
     *unsupported = true;
     return hipSuccess;
   }
-  const int64_t n64 = tl.reph * tl.strideh + tl.repm * tl.stridem;
+  const int64_t n64 = kCounterBytes / 8 + tl.reph * tl.strideh + tl.repm * tl.stridem;
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(a.ws),
                      n64, 0);
