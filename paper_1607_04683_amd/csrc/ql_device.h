@@ -166,6 +166,47 @@ __device__ __forceinline__ void wave_reduce_n(int (&v)[N], int identity, Op op) 
 #pragma unroll
   for (int i = 0; i < N; ++i) v[i] = __builtin_amdgcn_readlane(v[i], 63);
 }
+// All-lane reductions built from rotations inside 16-lane rows (every lane
+// has a valid source, so the compiler folds the DPP into the min/add itself),
+// then the four row results combined from lanes 0, 16, 32, 48.  N
+// independent values step together so their latencies overlap.
+template <int N>
+__device__ __forceinline__ void wave_min_n(int (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = min(v[i], __builtin_amdgcn_update_dpp(0, v[i], 0x121, 0xf, 0xf, false));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = min(v[i], __builtin_amdgcn_update_dpp(0, v[i], 0x122, 0xf, 0xf, false));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = min(v[i], __builtin_amdgcn_update_dpp(0, v[i], 0x124, 0xf, 0xf, false));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = min(v[i], __builtin_amdgcn_update_dpp(0, v[i], 0x128, 0xf, 0xf, false));
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    v[i] = min(min(__builtin_amdgcn_readlane(v[i], 0), __builtin_amdgcn_readlane(v[i], 16)),
+               min(__builtin_amdgcn_readlane(v[i], 32), __builtin_amdgcn_readlane(v[i], 48)));
+}
+template <int N>
+__device__ __forceinline__ void wave_add_n(int (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += __builtin_amdgcn_update_dpp(0, v[i], 0x121, 0xf, 0xf, false);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += __builtin_amdgcn_update_dpp(0, v[i], 0x122, 0xf, 0xf, false);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += __builtin_amdgcn_update_dpp(0, v[i], 0x124, 0xf, 0xf, false);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += __builtin_amdgcn_update_dpp(0, v[i], 0x128, 0xf, 0xf, false);
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    v[i] = (__builtin_amdgcn_readlane(v[i], 0) + __builtin_amdgcn_readlane(v[i], 16)) +
+           (__builtin_amdgcn_readlane(v[i], 32) + __builtin_amdgcn_readlane(v[i], 48));
+}
+// Order-preserving map of a (non-NaN) float to int and back.
+__device__ __forceinline__ int float_key(float f) {
+  const int u = __float_as_int(f);
+  return u ^ ((u >> 31) & 0x7fffffff);
+}
+__device__ __forceinline__ float key_float(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7fffffff)); }
+
 struct OpMinF {
   __device__ int operator()(int a, int b) const {
     return __float_as_int(fminf(__int_as_float(a), __int_as_float(b)));

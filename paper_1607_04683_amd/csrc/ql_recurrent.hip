@@ -36,6 +36,9 @@
 namespace ql {
 
 constexpr long kSpinLimit = 1l << 22;
+// 8 wavefronts per workgroup (two per SIMD): more rows / gate quads in
+// flight per step, and one wave's memory wait overlaps another's work.
+constexpr int kRecThreads = 512;
 constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
 constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
 constexpr int kMaxSlices = 256;    // arrival counters per kind and parity
@@ -126,11 +129,12 @@ __device__ __forceinline__ bool wait_count(const unsigned *cnt, unsigned target,
 // published words carrying `tag` (kSrcTagged: re-read until every tag
 // matches), as floats through device-coherent loads (kSrcCoherent: their
 // availability was already established), or as plain floats (kSrcPlain;
-// src null = zeros).  Rows [nvalid, ntotal)
-// are zero vectors.  Each lane holds values k = i*64 + lane, i < NV, so all
-// of a group's loads are in flight together; min/max, params, codes and the
-// code sum come from registers.  Codes go to dst + r*ldx (ldpad bytes), row
-// params to rp[r].  Returns false if the wait expired.
+// src null = zeros).  Rows [nvalid, ntotal) are zero vectors.  Lane l holds
+// the 4-element chunks starting at k = 4 (c*64 + l), c < NV/4, so all of a
+// group's loads are in flight together and four codes pack into one LDS
+// word; min/max, params, codes and the code sum come from registers.  Codes
+// go to dst + r*ldx (ldpad bytes, ldpad a multiple of 4), row params to
+// rp[r].  Returns false if the wait expired.
 // ---------------------------------------------------------------------------
 enum { kSrcPlain = 0, kSrcTagged = 1, kSrcCoherent = 2 };
 
@@ -138,6 +142,7 @@ template <int NV, int RB, int MODE>
 __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int nvalid,
                                            int ntotal, uint32_t tag, int K, int8_t *dst,
                                            int ldx, int ldpad, int *flag, RowParam *rp) {
+  constexpr int NC = NV / 4;
   const int lane = threadIdx.x & 63;
   float v[RB][NV];
   if (MODE == kSrcTagged) {
@@ -148,16 +153,18 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
 #pragma unroll
       for (int r = 0; r < RB; ++r)
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-          const int k = i * kWave + lane;
-          float x = 0.0f;
-          if (r < nvalid && k < K) {
-            const uint64_t w = ld_tagged(base + r * stride + k);
-            bad |= (uint32_t)(w >> 32) ^ tag;
-            x = __uint_as_float((uint32_t)w);
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int k = 4 * (c * kWave + lane) + e;
+            float x = 0.0f;
+            if (r < nvalid && k < K) {
+              const uint64_t w = ld_tagged(base + r * stride + k);
+              bad |= (uint32_t)(w >> 32) ^ tag;
+              x = __uint_as_float((uint32_t)w);
+            }
+            v[r][4 * c + e] = x;
           }
-          v[r][i] = x;
-        }
       if (!__any(bad != 0)) break;
       if (wait_expired(flag, it)) return false;
     }
@@ -166,55 +173,61 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        const int k = i * kWave + lane;
-        float x = 0.0f;
-        if (base && r < nvalid && k < K)
-          x = MODE == kSrcCoherent ? ld_coherent(base + r * stride + k) : base[r * stride + k];
-        v[r][i] = x;
-      }
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int k = 4 * (c * kWave + lane) + e;
+          float x = 0.0f;
+          if (base && r < nvalid && k < K)
+            x = MODE == kSrcCoherent ? ld_coherent(base + r * stride + k) : base[r * stride + k];
+          v[r][4 * c + e] = x;
+        }
   }
-  // lane-local min / max of every row, then all 2*RB wave reductions together
+  // order-preserving keys: min over keys, max as ~min(~key); 2*RB reductions together
   int mm[2 * RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
-    float lo = INFINITY, hi = -INFINITY;
+    int lo = 0x7fffffff, hi = 0x7fffffff;
 #pragma unroll
-    for (int i = 0; i < NV; ++i)
-      if (i * kWave + lane < K) {
-        lo = fminf(lo, v[r][i]);
-        hi = fmaxf(hi, v[r][i]);
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = 4 * (c * kWave + lane) + e < K;
+        const int key = float_key(v[r][4 * c + e]);
+        lo = ok ? min(lo, key) : lo;
+        hi = ok ? min(hi, ~key) : hi;
       }
-    mm[r] = __float_as_int(lo);
-    mm[RB + r] = __float_as_int(-hi);  // max(x) = -min(-x): one reduction kind
+    mm[r] = lo;
+    mm[RB + r] = hi;
   }
-  wave_reduce_n<2 * RB>(mm, __float_as_int(INFINITY), OpMinF());
+  wave_min_n<2 * RB>(mm);
   int sums[RB];
   QParams prm[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
-    float lo = __int_as_float(mm[r]), hi = -__int_as_float(mm[RB + r]);
+    float lo = key_float(mm[r]), hi = key_float(~mm[RB + r]);
     if (r >= nvalid || !src || K == 0) lo = hi = 0.0f;
     prm[r] = make_qparams(lo, hi);
     int sum = 0;
-    int8_t *d = dst + r * ldx;
-    const bool write = r < ntotal;
+    uint32_t *d = reinterpret_cast<uint32_t *>(dst + r * ldx);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int k = i * kWave + lane;
-      int8_t b = 0;
-      if (k < K) {
-        const int c = encode(v[r][i], prm[r].q, prm[r].z);
-        sum += c;
-        b = (int8_t)(c ^ 0x80);
+    for (int c = 0; c < NC; ++c) {
+      const int k0 = 4 * (c * kWave + lane);
+      uint32_t word = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = k0 + e < K;
+        const int code = encode(v[r][4 * c + e], prm[r].q, prm[r].z);
+        sum += ok ? code : 0;
+        word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
       }
-      if (write && k < ldpad) d[k] = b;
+      if (r < ntotal && k0 < ldpad) d[k0 / 4] = word;
     }
-    if (write)
-      for (int k = NV * kWave + lane; k < ldpad; k += kWave) d[k] = 0;
+    if (r < ntotal)
+      for (int k0 = 4 * (NC * kWave + lane); k0 < ldpad; k0 += 4 * kWave) d[k0 / 4] = 0u;
     sums[r] = sum;
   }
-  wave_reduce_n<RB>(sums, 0, OpAddI());
+  wave_add_n<RB>(sums);
   if (lane == 0) {
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
@@ -332,7 +345,7 @@ __device__ __forceinline__ void store_codes(const RecurrentArgs &a, const RecTil
 // (16+ batch rows per tile) or v_dot4 products.
 // ---------------------------------------------------------------------------
 template <int NVA, bool MFA, int NVB, bool MFB>
-__global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl) {
+__global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int8_t *wsl = reinterpret_cast<int8_t *>(smem + tl.off_w);
   int8_t *xc = reinterpret_cast<int8_t *>(smem + tl.off_x);
@@ -370,10 +383,10 @@ __global__ __launch_bounds__(256) void k_recurrent(RecurrentArgs a, RecTiling tl
   const int nrows = 4 * tl.u;  // slice rows, gate-major: row g*u + jj
   const int ldS = nrows;
   const int rowsA = MFA ? tl.bB : nb;  // rows quantized (MFMA tiles need zero padding rows)
-  // rows per wave-level group: several rows of a batched tile share one set of
-  // reductions; a one-row tile (v_dot4 path) uses single-row groups
-  constexpr int RBA = (MFA && NVA <= 8) ? 4 : 1;
-  constexpr int RBB = (MFB && NVB <= 8) ? 4 : 1;
+  // rows per wave-level group: two rows of a batched tile share one set of
+  // reductions (16 rows keep all 8 waves busy); one-row tiles use single rows
+  constexpr int RBA = (MFA && NVA <= 8) ? 2 : 1;
+  constexpr int RBB = (MFB && NVB <= 8) ? 2 : 1;
   const bool activeB = NVB > 0 && (int)blockIdx.x < tl.nbt2 * tl.npt;
   const int tb2 = activeB ? blockIdx.x / tl.npt : 0, tp = activeB ? blockIdx.x % tl.npt : 0;
   const int64_t c0 = (int64_t)tb2 * tl.bB2, p0 = (int64_t)tp * tl.p2;
@@ -782,7 +795,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
                                      (int)tl.lds_bytes);
   if (e != hipSuccess) return e;
   int per_cu = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, tl.lds_bytes);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kRecThreads, tl.lds_bytes);
   if (e != hipSuccess) return e;
   if (per_cu * cus < tl.grid) {
     *unsupported = true;
@@ -796,7 +809,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
   if (e != hipSuccess) return e;
   RecurrentArgs args = a;
   void *kargs[] = {&args, &tl};
-  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid), dim3(256),
+  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid), dim3(kRecThreads),
                                     kargs, (unsigned)tl.lds_bytes, s);
 }
 
