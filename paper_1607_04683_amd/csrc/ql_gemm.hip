@@ -44,6 +44,7 @@ struct Cfg {
   static constexpr int FM = TM / 32, FN = TN / 32;
   static constexpr int LDSS = BK + 16;  // padded LDS row stride in bytes
   static constexpr int STAGE = (BM + BN) * LDSS;
+  static constexpr int LDS = 2 * STAGE;
   static constexpr int CPR = BK / 16;   // 16-byte chunks per row
   static constexpr int LA = BM * CPR / NT, LB = BN * CPR / NT;
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/threads mismatch");
@@ -136,23 +137,264 @@ __device__ __forceinline__ void gemm_tile(const int8_t *__restrict__ A, int64_t 
   }
 }
 
+// Deeper pipeline for large tiles: K advances ROW bytes (64 or 128) per step
+// through NS LDS stages filled by direct global->LDS loads (no VGPR
+// staging).  Chunk c (16 bytes) of row r of a stage sits in slot
+// c ^ swz(r), which keeps the 16-byte fragment reads of 32 consecutive rows
+// free of bank conflicts (any 8 aligned rows, and the even and the odd rows
+// of any 16 aligned rows, take distinct slots).  swz uses only bits 0..4 of
+// the row, so a fragment's swizzle follows from lane & 31 alone.
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int ROW>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (ROW == 64) return ((r >> 1) ^ (r >> 2)) & 3;
+  else return (r & 7) ^ ((r >> 3) & 1);
+}
+
+// s_waitcnt with only the vector-memory count limited (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at maximum)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+}
+
+template <int BM, int BN, int WM, int WN, int ROW, int NS>
+struct CfgDma {
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int TBM = BM, TBN = BN;
+  static constexpr int TM = BM / WM, TN = BN / WN;
+  static constexpr int FM = TM / 32, FN = TN / 32;
+  static constexpr int CPR = ROW / 16;           // 16-byte chunks per row
+  static constexpr int STAGE = (BM + BN) * ROW;
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int LA = BM * CPR / NT, LB = BN * CPR / NT;  // loads per thread
+  static_assert(ROW == 64 || ROW == 128, "row of 64 or 128 bytes");
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile/threads mismatch");
+  static_assert(NS >= 2, "pipeline needs two stages");
+};
+
+template <int BM, int BN, int WM, int WN, int ROW, int NS>
+__device__ __forceinline__ void gemm_tile_dma(
+    const int8_t *__restrict__ A, int64_t lda, const int8_t *__restrict__ B, int64_t ldb, int64_t M,
+    int64_t N, int64_t Kp, int64_t m0, int64_t n0, char *smem,
+    v16i (&acc)[CfgDma<BM, BN, WM, WN, ROW, NS>::FM][CfgDma<BM, BN, WM, WN, ROW, NS>::FN]) {
+  using C = CfgDma<BM, BN, WM, WN, ROW, NS>;
+  constexpr int CPR = C::CPR, Q = ROW / 32;  // Q sub-steps of 32 bytes of K
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) acc[i][j] = v16i{};
+
+  // Load i of this thread fills LDS slot p = i * NT + tid of the A (or B)
+  // region: row p / CPR, slot p % CPR, holding global chunk
+  // (p % CPR) ^ swz(row).  Each wave's load instruction covers 1 KB of
+  // consecutive slots.
+  const int8_t *ga[C::LA], *gb[C::LB];
+#pragma unroll
+  for (int i = 0; i < C::LA; ++i) {
+    const int p = i * C::NT + tid, r = p / CPR, c = (p % CPR) ^ swz<ROW>(r);
+    int64_t gr = m0 + r;
+    gr = gr < M ? gr : M - 1;
+    ga[i] = A + gr * lda + c * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < C::LB; ++i) {
+    const int p = i * C::NT + tid, r = p / CPR, c = (p % CPR) ^ swz<ROW>(r);
+    int64_t gr = n0 + r;
+    gr = gr < N ? gr : N - 1;
+    gb[i] = B + gr * ldb + c * 16;
+  }
+  const int nk = (int)(Kp / ROW);
+  // Load i (of LA + LB) of step `ks` into its stage; steps past the end
+  // reload the last step into a stage that is never read again, so every
+  // step has the same number of loads in flight.
+  auto load_one = [&](int ks, int i) {
+    const int64_t ko = (int64_t)(ks < nk ? ks : nk - 1) * ROW;
+    char *st = smem + (ks % NS) * C::STAGE + wave * 1024;
+    if (i < C::LA)
+      __builtin_amdgcn_global_load_lds(ga[i] + ko, (lds_void *)(st + i * C::NT * 16), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds(gb[i - C::LA] + ko,
+                                       (lds_void *)(st + BM * ROW + (i - C::LA) * C::NT * 16),
+                                       16, 0, 0);
+  };
+  if (nk == 0) return;
+
+  // Fragment q of a sub-step: A fragments 0..FM-1, then B fragments.  A
+  // fragment i of sub-step h is rows wm*TM + i*32 + (lane & 31), chunk
+  // 2*h + (lane >> 5); swz depends only on lane & 31 here.
+  const int fr = lane & 31, fsw = swz<ROW>(fr), fhi = lane >> 5;
+  const int offa = (wm * C::TM + fr) * ROW, offb = BM * ROW + (wn * C::TN + fr) * ROW;
+  constexpr int NMF = C::FM * C::FN, NRD = C::FM + C::FN, NLD = C::LA + C::LB;
+  constexpr int SLOTS = NMF - NRD;  // load slots per sub-step
+  static_assert(Q % 2 == 0, "sub-steps alternate between two fragment sets");
+  static_assert(SLOTS > 0 && NLD <= Q * SLOTS, "not enough MFMAs to cover the memory ops");
+  v4i f0[NRD], f1[NRD];
+  auto read_one = [&](int ks, int h, int q, v4i &dst) {
+    const char *st = smem + (ks % NS) * C::STAGE + ((2 * h + fhi) ^ fsw) * 16;
+    dst = *reinterpret_cast<const v4i *>(st + (q < C::FM ? offa + q * 32 * ROW
+                                                         : offb + (q - C::FM) * 32 * ROW));
+  };
+  auto mfma_one = [&](const v4i(&f)[NRD], int q) {
+    const int i = q / C::FN, j = q % C::FN;
+    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f[i], f[C::FM + j], acc[i][j], 0, 0, 0);
+  };
+  // One sub-step: the MFMAs on `cur`, with the next sub-step's fragment
+  // reads into `nxt` and loads [l0, l0 + SLOTS) of step `lks` threaded one
+  // per MFMA; the scheduling barriers hold that order so the matrix pipe
+  // never waits on a memory instruction.
+  auto substep = [&](const v4i(&cur)[NRD], v4i(&nxt)[NRD], int rks, int rh, int lks, int l0) {
+#pragma unroll
+    for (int q = 0; q < NMF; ++q) {
+      mfma_one(cur, q);
+      if (q < NRD) read_one(rks, rh, q, nxt[q]);
+      else if (lks >= 0 && l0 + q - NRD < NLD) load_one(lks, l0 + q - NRD);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  for (int ks = 0; ks < NS; ++ks)
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) load_one(ks, i);
+  wait_vmcnt<(NS - 1) * NLD>();
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NRD; ++q) read_one(0, 0, q, f0[q]);
+  wait_lgkmcnt0();
+  // Step kt+NS-1 is loaded from the last sub-step of step kt-1 on (the
+  // prologue loaded steps 0..NS-1).
+  for (int kt = 0; kt < nk; ++kt) {
+    const int lprev = kt > 0 ? kt + NS - 1 : -1;
+#pragma unroll
+    for (int h = 0; h < Q - 1; ++h) {
+      if (h % 2 == 0) substep(f0, f1, kt, h + 1, lprev, (h + 1) * SLOTS);
+      else substep(f1, f0, kt, h + 1, lprev, (h + 1) * SLOTS);
+    }
+    // Stage kt is fully read into registers and step kt+1 has landed (steps
+    // up to kt+NS-1 were issued): after the barrier stage kt's buffer takes
+    // step kt+NS.
+    wait_vmcnt<(NS - 2) * NLD>();
+    __syncthreads();
+    substep(f1, f0, kt + 1, 0, kt + NS, 0);
+    // the fragments just read landed while the MFMAs above issued; saying so
+    // keeps the LDS counter (15 at most) from forcing a full wait on the
+    // next sub-step's reads
+    wait_lgkmcnt0();
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+}
+
+// Tile of this (1-D) workgroup.  Workgroups are dealt round-robin to the 8
+// XCDs; when the tile count allows, XCD x is given the x-th contiguous eighth
+// of the tile order, and that order walks groups of 8 tile rows column by
+// column, so the workgroups sharing an L2 also share A and B panels.
+__device__ __forceinline__ void tile_of_block(int64_t M, int64_t N, int BM, int BN, int *tm, int *tn) {
+  const int ntm = (int)((M + BM - 1) / BM), ntn = (int)((N + BN - 1) / BN);
+  const int ntiles = ntm * ntn;
+  int bid = blockIdx.x;
+  if (ntiles % 8 == 0) bid = (bid % 8) * (ntiles / 8) + bid / 8;
+  constexpr int kGroup = 8;
+  const int group = bid / (kGroup * ntn);
+  const int first = group * kGroup;
+  const int gsize = ntm - first < kGroup ? ntm - first : kGroup;
+  const int in_group = bid % (kGroup * ntn);
+  *tm = first + in_group % gsize;
+  *tn = in_group / gsize;
+}
+
 // Row/column of element r of a 32x32 MFMA block held by `lane`.
 __device__ __forceinline__ int frag_row(int r, int lane) { return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3); }
 __device__ __forceinline__ int frag_col(int lane) { return lane & 31; }
 
-template <int BM, int BN, int BK, int WM, int WN, int EPI>
+// Integer accumulators through LDS: each wave turns 32 rows of its
+// accumulators at a time into V'-domain sums (eq. 1 with the code sums) and
+// parks them row-major in its own LDS slab (row stride 136 words: the two
+// half-waves of a store land on disjoint banks), then stores whole rows with
+// 16-byte writes.  The tile's row sums are staged once.  The K loop has left
+// LDS idle (its last barrier follows the final wait for loads).
+template <class C>
+__device__ __forceinline__ void raw_epilogue_lds(const EpiArgs &e, int64_t M, int64_t N, int64_t K,
+                                                 int64_t m0, int64_t n0, int wm, int wn, int lane,
+                                                 char *smem, v16i (&acc)[C::FM][C::FN]) {
+  constexpr int TM = C::TM, TN = C::TN, RS = TN + 8;  // row stride in words
+  static_assert(TN % 4 == 0 && (RS * 4) % 16 == 0, "16-byte rows");
+  static_assert(C::TBM * 4 <= 4096 && 4096 + (C::NT / 64) * 32 * RS * 4 <= C::LDS, "LDS slabs");
+  uint32_t *rterm = reinterpret_cast<uint32_t *>(smem);  // [BM]: 128 * sigma_x
+  const int wave = threadIdx.x >> 6;
+  uint32_t *slab = reinterpret_cast<uint32_t *>(smem + 4096) + wave * 32 * RS;
+  for (int r = threadIdx.x; r < C::TBM; r += C::NT) {
+    const int64_t m = m0 + r;
+    rterm[r] = m < M ? 128u * (uint32_t)(e.x_sums[m] - 128 * (int32_t)K) : 0u;
+  }
+  uint32_t cterm[C::FN];
+#pragma unroll
+  for (int j = 0; j < C::FN; ++j) {
+    int64_t n = n0 + wn * TN + j * 32 + (lane & 31);
+    n = n < N ? n : N - 1;
+    cterm[j] = 128u * (uint32_t)(e.w_sums[n] - 128 * (int32_t)K) + 16384u * (uint32_t)K;
+  }
+  __syncthreads();
+  const bool vec = (N & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = frag_row(r, lane);
+      const uint32_t rt = rterm[wm * TM + i * 32 + row];
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+        slab[row * RS + j * 32 + (lane & 31)] = (uint32_t)acc[i][j][r] + cterm[j] + rt;
+    }
+    // the slab is this wave's own: LDS keeps one wave's accesses in order
+#pragma unroll
+    for (int it = 0; it < 32 * TN / 256; ++it) {
+      const int q = it * 64 + lane, row = q / (TN / 4), c4 = (q % (TN / 4)) * 4;
+      const v4i v = *reinterpret_cast<const v4i *>(slab + row * RS + c4);
+      const int64_t m = m0 + wm * TM + i * 32 + row, n = n0 + wn * TN + c4;
+      if (m < M) {
+        int32_t *dst = e.acc + m * N + n;
+        if (vec && n + 3 < N) {
+          *reinterpret_cast<v4i *>(dst) = v;
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            if (n + t < N) dst[t] = v[t];
+        }
+      }
+    }
+  }
+}
+
+// NS = 0: register-staged two-stage tile; NS >= 2: direct-load pipeline of
+// NS stages with BK-byte rows.
+template <int BM, int BN, int BK, int WM, int WN, int NS>
+using GemmCfg = std::conditional_t<(NS >= 2), CfgDma<BM, BN, WM, WN, BK, (NS >= 2 ? NS : 2)>,
+                                   Cfg<BM, BN, BK, WM, WN>>;
+
+template <int BM, int BN, int BK, int WM, int WN, int NS, int EPI>
 __global__ __launch_bounds__(64 * WM *WN) void k_gemm(const int8_t *__restrict__ A, int64_t lda,
                                                        const int8_t *__restrict__ B, int64_t ldb,
                                                        int64_t M, int64_t N, int64_t K,
                                                        int64_t Kp, EpiArgs e) {
-  using C = Cfg<BM, BN, BK, WM, WN>;
+  using C = GemmCfg<BM, BN, BK, WM, WN, NS>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+  int tm, tn;
+  tile_of_block(M, N, BM, BN, &tm, &tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
   // softmax output pass: combine the per-tile statistics of this tile's rows
-  float *rowmax = reinterpret_cast<float *>(smem + 2 * C::STAGE);
+  float *rowmax = reinterpret_cast<float *>(smem + C::LDS);
   float *rowinv = rowmax + BM;
   if (EPI == EPI_SMAX_OUT) {
     for (int r = threadIdx.x; r < BM; r += C::NT) {
@@ -171,7 +413,15 @@ __global__ __launch_bounds__(64 * WM *WN) void k_gemm(const int8_t *__restrict__
   }
 
   v16i acc[C::FM][C::FN];
-  gemm_tile<BM, BN, BK, WM, WN>(A, lda, B, ldb, M, N, Kp, m0, n0, smem, acc);
+  if constexpr (NS >= 2)
+    gemm_tile_dma<BM, BN, WM, WN, BK, NS>(A, lda, B, ldb, M, N, Kp, m0, n0, smem, acc);
+  else
+    gemm_tile<BM, BN, BK, WM, WN>(A, lda, B, ldb, M, N, Kp, m0, n0, smem, acc);
+
+  if constexpr (NS >= 2 && EPI == EPI_RAW) {
+    raw_epilogue_lds<C>(e, M, N, K, m0, n0, wm, wn, lane, smem, acc);
+    return;
+  }
 
   // per-column terms
   int32_t ztw[C::FN], sigw[C::FN];
@@ -291,31 +541,32 @@ __global__ __launch_bounds__(64 * WM *WN) void k_gemm(const int8_t *__restrict__
       if (m >= M) continue;
       float sm = 0.0f;
       for (int w = 0; w < WN; ++w) sm += red[w * BM + r];
-      e.stats[m * e.ntn + blockIdx.x] = make_float2(tmax[r], sm);
+      e.stats[m * e.ntn + tn] = make_float2(tmax[r], sm);
     }
   }
 }
 
 // ------------------------------------------------------------------ launch
-template <int BM, int BN, int BK, int WM, int WN, int EPI>
+template <int BM, int BN, int BK, int WM, int WN, int NS, int EPI>
 static hipError_t run(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb, int64_t M,
                       int64_t N, int64_t K, const EpiArgs &e, hipStream_t s) {
-  using C = Cfg<BM, BN, BK, WM, WN>;
+  using C = GemmCfg<BM, BN, BK, WM, WN, NS>;
   const int64_t Kp = round_up(K, BK);
-  size_t lds = 2 * (size_t)C::STAGE;
+  size_t lds = (size_t)C::LDS;
   if (EPI == EPI_SMAX_OUT) lds += 2 * BM * sizeof(float);
   if (EPI == EPI_SMAX_STATS) {
     const size_t need = (size_t)(WN + 1) * BM * sizeof(float);
     lds = lds > need ? lds : need;
   }
-  auto kern = k_gemm<BM, BN, BK, WM, WN, EPI>;
+  auto kern = k_gemm<BM, BN, BK, WM, WN, NS, EPI>;
   static bool attr_set = false;  // per instantiation; idempotent
   if (!attr_set) {
-    hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
     attr_set = true;
   }
-  dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
+  dim3 grid((unsigned)(((N + BN - 1) / BN) * ((M + BM - 1) / BM)));
   hipLaunchKernelGGL(kern, grid, dim3(C::NT), lds, s, A, lda, B, ldb, M, N, K, Kp, e);
   return hipGetLastError();
 }
@@ -326,9 +577,18 @@ template <int EPI>
 static hipError_t dispatch(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb, int64_t M,
                            int64_t N, int64_t K, const EpiArgs &e, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
-  if (round_up(K, 128) <= lda && round_up(K, 128) <= ldb)
-    return run<128, 128, 128, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
-  return run<128, 128, 64, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
+  const bool k128 = round_up(K, 128) <= lda && round_up(K, 128) <= ldb;
+  // 256x256 tiles (128x128 per wave) once there are enough of them to fill
+  // the chip; otherwise 128x128 tiles (64x64 per wave)
+  const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  if constexpr (EPI == EPI_RAW) {
+    if (big_tiles >= 256) {
+      if (k128) return run<256, 256, 128, 2, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
+      return run<256, 256, 64, 2, 2, 4, EPI>(A, lda, B, ldb, M, N, K, e, s);
+    }
+  }
+  if (k128) return run<128, 128, 128, 2, 2, 0, EPI>(A, lda, B, ldb, M, N, K, e, s);
+  return run<128, 128, 64, 2, 2, 0, EPI>(A, lda, B, ldb, M, N, K, e, s);
 }
 
 static EpiArgs make_epi(const ActRows &X, const WeightMat &W, const float *bias) {

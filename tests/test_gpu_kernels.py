@@ -129,6 +129,20 @@ def test_gemm_u8_matches_oracle(ql, orc, M, N, K):
     assert np.array_equal(got, orc.gemm_u8(A, Bm))
 
 
+@pytest.mark.parametrize("M,N,K", [(4100, 4000, 1000), (4096, 4352, 64), (8192, 2048, 2000)])
+def test_gemm_u8_large_tiles_ragged(ql, orc, M, N, K):
+    """Shapes large enough for the 256x256 tiles, with ragged M, N and K:
+    sampled rows (first and last tile rows included) against the oracle."""
+    rng = np.random.default_rng(M ^ N ^ K)
+    A = rng.integers(0, 256, (M, K), dtype=np.uint8)
+    Bm = rng.integers(0, 256, (N, K), dtype=np.uint8)
+    got = ql.gemm_u8(ql.device_codes(A), ql.device_codes(Bm), K)
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, M - 257, M - 1],
+                                     rng.choice(M, 16, replace=False)]))
+    want = orc.gemm_u8(A[rows], Bm)
+    assert np.array_equal(got[torch.from_numpy(rows).cuda()].cpu().numpy(), want)
+
+
 @pytest.mark.parametrize("n", [4096, 8192])
 def test_gemm_u8_sweep_sizes_sampled_rows(ql, orc, n):
     """M = N = K = n with U{0..255} operands: sampled rows of C against the
