@@ -193,9 +193,43 @@ ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64
                                     int64_t B, float *post, const ql_model_taps *taps,
                                     void *ws, size_t ws_bytes, void *stream);
 
+/* ---- unquantized fp32 model (the float baseline of Section 5) -----------------
+ * The same layers and model with fp32 weights and no quantization: products
+ * accumulate in fp32, gate math is the same as above, the output layer is a
+ * plain fp32 softmax.  Weights are device fp32 arrays, row-major and dense:
+ * Wx [4H][in], Wh [4H][R], Wr [P][H] (P > 0), bias [4H]; the model's layers
+ * array is a host array, Wy [states][R_last], by [states].  Float results
+ * follow the summation order of the GPU kernels, so they agree with a
+ * reference evaluation to rounding, not bit for bit. */
+typedef struct {
+  int64_t in, hidden, proj;
+  const float *Wx, *Wh, *Wr, *bias;
+} ql_f32_layer;
+typedef struct {
+  int32_t nlayers;
+  const ql_f32_layer *layers;
+  int64_t states;
+  const float *Wy, *by;
+} ql_f32_model;
+
+/* Y [m][rows] = X [m][cols] W^T + bias (bias nullable); W [rows][cols]. */
+ql_status ql_f32_matmul(const float *W, int64_t rows, int64_t cols, const float *X, int64_t m,
+                        const float *bias, float *Y, void *stream);
+/* As ql_lstm_layer_forward, without taps. */
+size_t ql_f32_lstm_layer_workspace(const ql_f32_layer *L, int64_t T, int64_t B);
+ql_status ql_f32_lstm_layer_forward(const ql_f32_layer *L, const float *x, int64_t T,
+                                    int64_t B, const float *h0, const float *c0, float *h,
+                                    float *hT, float *cT, void *ws, size_t ws_bytes,
+                                    void *stream);
+/* As ql_acoustic_model_forward: feats [T][B][in] -> post [T][B][states]. */
+size_t ql_f32_acoustic_model_workspace(const ql_f32_model *M, int64_t T, int64_t B);
+ql_status ql_f32_acoustic_model_forward(const ql_f32_model *M, const float *feats, int64_t T,
+                                        int64_t B, float *post, void *ws, size_t ws_bytes,
+                                        void *stream);
+
 /* ---- misc -------------------------------------------------------------------- */
 /* Synchronizes `stream`, then reports QL_ETIMEOUT if a persistent kernel of the
- * last ql_lstm_layer_forward / ql_acoustic_model_forward that used this
+ * last layer / model forward call (8-bit or fp32) that used this
  * workspace gave up waiting for the rest of its grid (its outputs are then
  * undefined), else QL_OK. */
 ql_status ql_workspace_status(const void *ws, void *stream);

@@ -405,6 +405,136 @@ ql_status ql_lstm_recurrence(const ql_lstm_layer *L, const float *gx, int64_t T,
   return unsupported ? QL_EUNSUPPORTED : QL_OK;
 }
 
+// ---------------------------------------------------------------- fp32 model
+namespace {
+int64_t f32_width(const ql_f32_layer &L) { return L.proj ? L.proj : L.hidden; }
+
+ql_status check_f32_layer(const ql_f32_layer *L) {
+  if (!L || !L->Wx || !L->Wh || !L->bias || (L->proj && !L->Wr)) return QL_EINVAL;
+  if (L->in <= 0 || L->hidden <= 0 || L->proj < 0) return QL_ESHAPE;
+  return QL_OK;
+}
+
+// gx = x Wx^T + b over all frames, then the recurrence.
+ql_status run_f32_layer(const ql_f32_layer &L, const float *x, int64_t T, int64_t B,
+                        const float *h0, const float *c0, float *h, float *hT, float *cT,
+                        float *gx, void *rec, hipStream_t s) {
+  const int64_t H = L.hidden;
+  if (launch_sgemm(x, L.in, L.Wx, L.in, T * B, 4 * H, L.in, L.bias, gx, 4 * H, s) != hipSuccess)
+    return QL_EHIP;
+  F32RecArgs a{};
+  a.T = T;
+  a.B = B;
+  a.H = H;
+  a.P = L.proj;
+  a.R = f32_width(L);
+  a.gx = gx;
+  a.Wh = L.Wh;
+  a.Wr = L.Wr;
+  a.h0 = h0;
+  a.c0 = c0;
+  a.h = h;
+  a.hT = hT;
+  a.cT = cT;
+  a.ws = rec;
+  bool unsupported = false;
+  if (launch_recurrent_f32(a, s, &unsupported) != hipSuccess) return QL_EHIP;
+  return unsupported ? QL_EUNSUPPORTED : QL_OK;
+}
+}  // namespace
+
+ql_status ql_f32_matmul(const float *W, int64_t rows, int64_t cols, const float *X, int64_t m,
+                        const float *bias, float *Y, void *stream) {
+  if (rows < 0 || cols < 0 || m < 0) return QL_ESHAPE;
+  if (rows * m > 0 && (!W || !X || !Y)) return QL_EINVAL;
+  return from_hip(launch_sgemm(X, cols, W, cols, m, rows, cols, bias, Y, rows, as_stream(stream)));
+}
+
+size_t ql_f32_lstm_layer_workspace(const ql_f32_layer *L, int64_t T, int64_t B) {
+  if (!L || T < 0 || B < 0) return 0;
+  Carve c(nullptr);
+  c.take<char>(recurrent_f32_ws(B, L->hidden, L->proj));
+  c.take<float>((size_t)(T * B * 4 * L->hidden));
+  return c.off;
+}
+
+ql_status ql_f32_lstm_layer_forward(const ql_f32_layer *L, const float *x, int64_t T,
+                                    int64_t B, const float *h0, const float *c0, float *h,
+                                    float *hT, float *cT, void *ws, size_t ws_bytes,
+                                    void *stream) {
+  ql_status st = check_f32_layer(L);
+  if (st != QL_OK) return st;
+  if (T < 0 || B < 0) return QL_ESHAPE;
+  if (T * B > 0 && (!x || !h)) return QL_EINVAL;
+  if (!ws || ws_bytes < ql_f32_lstm_layer_workspace(L, T, B)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  Carve c(ws);
+  void *rec = c.take<char>(recurrent_f32_ws(B, L->hidden, L->proj));
+  float *gx = c.take<float>((size_t)(T * B * 4 * L->hidden));
+  if (reset_recurrent_flag(rec, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+  return run_f32_layer(*L, x, T, B, h0, c0, h, hT, cT, gx, rec, s);
+}
+
+size_t ql_f32_acoustic_model_workspace(const ql_f32_model *M, int64_t T, int64_t B) {
+  if (!M || M->nlayers <= 0 || !M->layers || T < 0 || B < 0) return 0;
+  int64_t maxH = 0, maxR = 0, maxP = 0;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_f32_layer &L = M->layers[l];
+    maxH = L.hidden > maxH ? L.hidden : maxH;
+    maxR = f32_width(L) > maxR ? f32_width(L) : maxR;
+    maxP = L.proj > maxP ? L.proj : maxP;
+  }
+  Carve c(nullptr);
+  c.take<char>(recurrent_f32_ws(B, maxH, maxP));
+  c.take<float>((size_t)(T * B * 4 * maxH));
+  c.take<float>((size_t)(T * B * maxR));
+  c.take<float>((size_t)(T * B * maxR));
+  return c.off;
+}
+
+ql_status ql_f32_acoustic_model_forward(const ql_f32_model *M, const float *feats, int64_t T,
+                                        int64_t B, float *post, void *ws, size_t ws_bytes,
+                                        void *stream) {
+  if (!M || !M->layers || !M->Wy || !M->by) return QL_EINVAL;
+  if (M->nlayers <= 0 || M->states <= 0 || T < 0 || B < 0) return QL_ESHAPE;
+  if (T * B > 0 && (!feats || !post)) return QL_EINVAL;
+  for (int l = 0; l < M->nlayers; ++l) {
+    ql_status st = check_f32_layer(&M->layers[l]);
+    if (st != QL_OK) return st;
+    const int64_t want_in = l == 0 ? M->layers[0].in : f32_width(M->layers[l - 1]);
+    if (M->layers[l].in != want_in) return QL_ESHAPE;
+  }
+  if (!ws || ws_bytes < ql_f32_acoustic_model_workspace(M, T, B)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  if (reset_recurrent_flag(ws, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+  int64_t maxH = 0, maxR = 0, maxP = 0;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_f32_layer &L = M->layers[l];
+    maxH = L.hidden > maxH ? L.hidden : maxH;
+    maxR = f32_width(L) > maxR ? f32_width(L) : maxR;
+    maxP = L.proj > maxP ? L.proj : maxP;
+  }
+  const int64_t MB = T * B;
+  Carve c(ws);
+  void *rec = c.take<char>(recurrent_f32_ws(B, maxH, maxP));
+  float *gx = c.take<float>((size_t)(MB * 4 * maxH));
+  float *hbuf[2] = {c.take<float>((size_t)(MB * maxR)), c.take<float>((size_t)(MB * maxR))};
+  const float *cur = feats;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_f32_layer &L = M->layers[l];
+    ql_status st = run_f32_layer(L, cur, T, B, nullptr, nullptr, hbuf[l & 1], nullptr, nullptr,
+                                 gx, rec, s);
+    if (st != QL_OK) return st;
+    cur = hbuf[l & 1];
+  }
+  const int64_t K = f32_width(M->layers[M->nlayers - 1]);
+  if (launch_sgemm(cur, K, M->Wy, K, MB, M->states, K, M->by, post, M->states, s) != hipSuccess)
+    return QL_EHIP;
+  return from_hip(launch_softmax_rows(post, MB, M->states, s));
+}
+
 ql_status ql_workspace_status(const void *ws, void *stream) {
   if (!ws) return QL_EINVAL;
   bool to = false;

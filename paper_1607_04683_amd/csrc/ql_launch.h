@@ -91,5 +91,27 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s);
 // Reads the timeout flag a persistent launch left in its workspace (syncs s).
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
+// Zeroes the n64 64-bit words after the workspace header (counters first).
+hipError_t clear_exchange(void *ws, int64_t n64, hipStream_t s);
+
+// ---- unquantized fp32 model (ql_f32.hip)
+// C[m][n] = sum_k A[m][k] B[n][k] (+ bias[n]); bias nullable.
+hipError_t launch_sgemm(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M,
+                        int64_t N, int64_t K, const float *bias, float *C, int64_t ldc,
+                        hipStream_t s);
+// In-place softmax of each of `rows` rows of S floats.
+hipError_t launch_softmax_rows(float *x, int64_t rows, int64_t S, hipStream_t s);
+struct F32RecArgs {
+  int64_t T, B, H, P, R;     // R = P ? P : H
+  const float *gx;           // [T][B][4H] (W_x x_t + b)
+  const float *Wh;           // [4H][R]
+  const float *Wr;           // [P][H] (P > 0)
+  const float *h0, *c0;      // nullable
+  float *h;                  // [T][B][R]
+  float *hT, *cT;            // nullable
+  void *ws;                  // recurrent_f32_ws bytes, timeout flag cleared by the caller
+};
+size_t recurrent_f32_ws(int64_t B, int64_t H, int64_t P);
+hipError_t launch_recurrent_f32(const F32RecArgs &a, hipStream_t s, bool *unsupported);
 
 }  // namespace ql

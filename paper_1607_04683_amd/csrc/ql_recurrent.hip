@@ -29,20 +29,16 @@
 // a flag in the workspace is raised, and all workgroups leave at their next
 // wait, so the grid always drains.
 #include "ql_device.h"
+#include "ql_exchange.h"
 #include "ql_launch.h"
 
 #include <algorithm>
 
 namespace ql {
 
-constexpr long kSpinLimit = 1l << 22;
 // 8 wavefronts per workgroup (two per SIMD): more rows / gate quads in
 // flight per step, and one wave's memory wait overlaps another's work.
 constexpr int kRecThreads = 512;
-constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
-constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
-constexpr int kMaxSlices = 256;    // arrival counters per kind and parity
-constexpr int kCounterBytes = 2 * 2 * kMaxSlices * 64;  // one 64-byte line per counter
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -74,54 +70,6 @@ struct RowParam {
   int32_t sum;      // code sum (0..255 domain)
   int32_t pad[3];
 };
-
-// ---------------------------------------------------------------------------
-// Exchange between workgroups (see the file comment).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void publish(uint64_t *p, uint32_t tag, float v) {
-  __hip_atomic_store(p, ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_tagged(const uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_coherent(float *p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_coherent(const float *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Bounded-wait bookkeeping: true when the wait must be abandoned.
-__device__ __forceinline__ bool wait_expired(int *flag, long &it) {
-  if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-    return true;
-  if (it > kSpinLimit) {
-    __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return true;
-  }
-  __builtin_amdgcn_s_sleep(1);
-  return false;
-}
-
-// Counter protocol (batched tiles): after its coherent stores of step t have
-// completed (every wave waits for its own memory operations, then the
-// workgroup barrier), thread 0 adds 1 to the arrival counter of the batch
-// slice the values belong to; a consumer's thread 0 waits until the counter
-// of the slot holds uses * producers.  The stores precede the increment in
-// time, and the consumer's loads follow its observation of the count.
-__device__ __forceinline__ void arrive(unsigned *cnt) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Thread 0 waits for *cnt >= target; returns false (for thread 0) on expiry.
-__device__ __forceinline__ bool wait_count(const unsigned *cnt, unsigned target, int *flag) {
-  if (threadIdx.x != 0) return true;
-  long it = 0;
-  while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target)
-    if (wait_expired(flag, it)) return false;
-  return true;
-}
 
 // ---------------------------------------------------------------------------
 // Per-vector quantization (eq. 2) of RB consecutive rows by one wave.
@@ -594,6 +542,13 @@ __global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
   if (i == 0 && with_flag) hdr[kHdrFlag] = 0u;
   uint64_t *x = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(hdr) + kHeaderBytes);
   for (int64_t k = i; k < n64; k += (int64_t)gridDim.x * blockDim.x) x[k] = 0;
+}
+
+hipError_t clear_exchange(void *ws, int64_t n64, hipStream_t s) {
+  const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
+  hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(ws), n64,
+                     0);
+  return hipGetLastError();
 }
 
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s) {

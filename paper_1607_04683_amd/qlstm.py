@@ -28,7 +28,9 @@ EXPORTS = [
     "ql_quantized_matmul", "ql_gemm_u8_workspace", "ql_gemm_u8", "ql_lstm_layer_workspace",
     "ql_lstm_layer_forward", "ql_acoustic_model_workspace", "ql_acoustic_model_forward",
     "ql_status_str", "ql_workspace_status", "ql_gate_fn", "ql_lstm_recurrence_workspace",
-    "ql_lstm_recurrence",
+    "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_workspace",
+    "ql_f32_lstm_layer_forward", "ql_f32_acoustic_model_workspace",
+    "ql_f32_acoustic_model_forward",
 ]
 
 
@@ -63,6 +65,16 @@ class CQAct(C.Structure):
     _fields_ = [("codes", C.c_void_p), ("rows", C.c_int64), ("cols", C.c_int64),
                 ("ld", C.c_int64), ("zero", C.c_void_p), ("inv_q", C.c_void_p),
                 ("sums", C.c_void_p)]
+
+
+class CF32Layer(C.Structure):
+    _fields_ = [("in_", C.c_int64), ("hidden", C.c_int64), ("proj", C.c_int64),
+                ("Wx", C.c_void_p), ("Wh", C.c_void_p), ("Wr", C.c_void_p), ("bias", C.c_void_p)]
+
+
+class CF32Model(C.Structure):
+    _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(CF32Layer)), ("states", C.c_int64),
+                ("Wy", C.c_void_p), ("by", C.c_void_p)]
 
 
 class CModelTaps(C.Structure):
@@ -107,9 +119,19 @@ def load(path: str = LIB_PATH):
                                      C.POINTER(CQAct), C.POINTER(CTaps), vp, sz, vp]
     L.ql_workspace_status.argtypes = [vp, vp]
     L.ql_gate_fn.argtypes = [i32, vp, vp, i64, vp]
+    L.ql_f32_matmul.argtypes = [vp, i64, i64, vp, i64, vp, vp, vp]
+    L.ql_f32_lstm_layer_workspace.argtypes = [C.POINTER(CF32Layer), i64, i64]
+    L.ql_f32_lstm_layer_workspace.restype = sz
+    L.ql_f32_lstm_layer_forward.argtypes = [C.POINTER(CF32Layer), vp, i64, i64, vp, vp, vp, vp,
+                                            vp, vp, sz, vp]
+    L.ql_f32_acoustic_model_workspace.argtypes = [C.POINTER(CF32Model), i64, i64]
+    L.ql_f32_acoustic_model_workspace.restype = sz
+    L.ql_f32_acoustic_model_forward.argtypes = [C.POINTER(CF32Model), vp, i64, i64, vp, vp, sz,
+                                                vp]
     for f in ("ql_quantize", "ql_dequantize", "ql_quantized_matmul", "ql_gemm_u8",
               "ql_lstm_layer_forward", "ql_acoustic_model_forward", "ql_workspace_status",
-              "ql_gate_fn", "ql_lstm_recurrence"):
+              "ql_gate_fn", "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_forward",
+              "ql_f32_acoustic_model_forward"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -413,3 +435,101 @@ def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward")
     return out
+
+
+# ------------------------------------------------------------- fp32 model
+def f32_matmul(W: torch.Tensor, X: torch.Tensor, bias=None) -> torch.Tensor:
+    """Y [m][rows] = X [m][cols] W^T (+ bias), fp32 accumulation."""
+    W, X = W.contiguous(), X.contiguous()
+    rows, cols = W.shape
+    m = X.shape[0]
+    Y = torch.empty(m, rows, dtype=torch.float32, device=X.device)
+    _check(load().ql_f32_matmul(_ptr(W), rows, cols, _ptr(X), m, _ptr(bias), _ptr(Y), _stream()),
+           "ql_f32_matmul")
+    return Y
+
+
+@dataclass
+class F32Layer:
+    n_in: int
+    hidden: int
+    proj: int
+    Wx: torch.Tensor
+    Wh: torch.Tensor
+    Wr: torch.Tensor | None
+    bias: torch.Tensor
+
+    @property
+    def width(self) -> int:
+        return self.proj if self.proj else self.hidden
+
+    def cstruct(self) -> CF32Layer:
+        return CF32Layer(self.n_in, self.hidden, self.proj, _ptr(self.Wx), _ptr(self.Wh),
+                         _ptr(self.Wr), _ptr(self.bias))
+
+
+def f32_layer(L: dict, device="cuda") -> F32Layer:
+    """Device copy of one layer's float weights (Wx, Wh, b[, Wr])."""
+    t = lambda a: torch.as_tensor(a, dtype=torch.float32).contiguous().to(device)
+    Wr = None if L.get("Wr") is None else t(L["Wr"])
+    Wx = t(L["Wx"])
+    return F32Layer(Wx.shape[1], Wx.shape[0] // 4, 0 if Wr is None else Wr.shape[0], Wx,
+                    t(L["Wh"]), Wr, t(L["b"]))
+
+
+@dataclass
+class F32Model:
+    layers: list
+    Wy: torch.Tensor
+    by: torch.Tensor
+
+    def cstruct(self):
+        arr = (CF32Layer * len(self.layers))(*[L.cstruct() for L in self.layers])
+        return CF32Model(len(self.layers), arr, self.Wy.shape[0], _ptr(self.Wy), _ptr(self.by)), arr
+
+
+def f32_model(weights: dict, device="cuda") -> F32Model:
+    t = lambda a: torch.as_tensor(a, dtype=torch.float32).contiguous().to(device)
+    return F32Model([f32_layer(L, device) for L in weights["layers"]], t(weights["Wy"]),
+                    t(weights["by"]))
+
+
+def f32_lstm_layer_forward(L: F32Layer, x: torch.Tensor, h0=None, c0=None,
+                           workspace: Workspace | None = None, check: bool = True):
+    """x [T][B][in] fp32 (device) -> dict(h [T][B][R], hT, cT)."""
+    x = x.contiguous()
+    T, B, _ = x.shape
+    dev = x.device
+    lib = load()
+    cl = L.cstruct()
+    h = torch.empty(T, B, L.width, dtype=torch.float32, device=dev)
+    hT = torch.empty(B, L.width, dtype=torch.float32, device=dev)
+    cT = torch.empty(B, L.hidden, dtype=torch.float32, device=dev)
+    ws = (workspace or Workspace()).get(lib.ql_f32_lstm_layer_workspace(C.byref(cl), T, B), dev)
+    _check(lib.ql_f32_lstm_layer_forward(C.byref(cl), _ptr(x), T, B, _ptr(h0), _ptr(c0), _ptr(h),
+                                         _ptr(hT), _ptr(cT), _ptr(ws), ws.numel(), _stream()),
+           "ql_f32_lstm_layer_forward")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_f32_lstm_layer_forward")
+    return dict(h=h, hT=hT, cT=cT)
+
+
+def f32_acoustic_model_forward(M: F32Model, feats: torch.Tensor,
+                               workspace: Workspace | None = None,
+                               post: torch.Tensor | None = None, check: bool = True):
+    """feats [T][B][in] fp32 (device) -> dict(post [T][B][states])."""
+    feats = feats.contiguous()
+    T, B, _ = feats.shape
+    dev = feats.device
+    lib = load()
+    cm, keep = M.cstruct()
+    S = M.Wy.shape[0]
+    if post is None:
+        post = torch.empty(T, B, S, dtype=torch.float32, device=dev)
+    ws = (workspace or Workspace()).get(lib.ql_f32_acoustic_model_workspace(C.byref(cm), T, B), dev)
+    _check(lib.ql_f32_acoustic_model_forward(C.byref(cm), _ptr(feats), T, B, _ptr(post), _ptr(ws),
+                                             ws.numel(), _stream()),
+           "ql_f32_acoustic_model_forward")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_f32_acoustic_model_forward")
+    return dict(post=post)

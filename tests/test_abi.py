@@ -125,3 +125,32 @@ def test_model_argument_errors(ql):
     assert need > 0
     assert lib.ql_acoustic_model_forward(C.byref(m3), FAKE, 3, 2, FAKE, None, FAKE, need - 1,
                                          None) == ql.QL_EWORKSPACE
+
+
+def test_f32_argument_errors(ql):
+    lib = ql.load()
+    H, IN, S = 8, 16, 10
+    good = ql.CF32Layer(IN, H, 0, FAKE, FAKE, None, FAKE)
+    nbytes = lib.ql_f32_lstm_layer_workspace(C.byref(good), 5, 2)
+    assert nbytes > 0
+    f = lambda L, wsb=nbytes, x=FAKE, T=5: lib.ql_f32_lstm_layer_forward(
+        C.byref(L), x, T, 2, None, None, FAKE, None, None, FAKE, wsb, None)
+    assert f(good, x=None) == ql.QL_EINVAL
+    assert f(good, wsb=nbytes - 1) == ql.QL_EWORKSPACE
+    assert f(good, T=-1) == ql.QL_ESHAPE
+    assert f(ql.CF32Layer(IN, H, 0, None, FAKE, None, FAKE)) == ql.QL_EINVAL   # no W_x
+    assert f(ql.CF32Layer(IN, H, 3, FAKE, FAKE, None, FAKE)) == ql.QL_EINVAL   # no W_r
+    assert f(ql.CF32Layer(IN, 0, 0, FAKE, FAKE, None, FAKE)) == ql.QL_ESHAPE
+    l1 = ql.CF32Layer(H + 1, H, 0, FAKE, FAKE, None, FAKE)
+    arr = (ql.CF32Layer * 2)(good, l1)
+    m = ql.CF32Model(2, arr, S, FAKE, FAKE)
+    assert lib.ql_f32_acoustic_model_forward(C.byref(m), FAKE, 3, 2, FAKE, FAKE, 1 << 40,
+                                             None) == ql.QL_ESHAPE   # widths do not chain
+    arr1 = (ql.CF32Layer * 1)(good)
+    m1 = ql.CF32Model(1, arr1, S, FAKE, FAKE)
+    need = lib.ql_f32_acoustic_model_workspace(C.byref(m1), 3, 2)
+    assert need > 0
+    assert lib.ql_f32_acoustic_model_forward(C.byref(m1), FAKE, 3, 2, FAKE, FAKE, need - 1,
+                                             None) == ql.QL_EWORKSPACE
+    assert lib.ql_f32_matmul(None, 4, 4, FAKE, 2, None, FAKE, None) == ql.QL_EINVAL
+    assert lib.ql_f32_matmul(FAKE, -4, 4, FAKE, 2, None, FAKE, None) == ql.QL_ESHAPE
