@@ -41,8 +41,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--skip-cpu", action="store_true", help="do not time the CPU oracle")
     ap.add_argument("--quick", action="store_true", help="headline workload only")
-    ap.add_argument("--cpu-frames", type=int, default=8000,
+    ap.add_argument("--cpu-frames", type=int, default=32000,
                     help="frames of the batch-64 workload the CPU oracle is timed on")
+    ap.add_argument("--profile-target", default=None,
+                    choices=["recurrence_b64", "recurrence_b1", "gemm8192", "copy"],
+                    help="run only one piece (for hardware-counter passes) and exit")
     return ap.parse_args()
 
 
@@ -121,6 +124,42 @@ def recurrence_kernel(ql, torch, M, x, reps):
                 wh_bytes_per_step=wh_bytes)
 
 
+def time_f32_model(ql, torch, workload, steps, warmup):
+    """ms per forward pass of the unquantized fp32 model on the same workload."""
+    from paper_1607_04683_amd import workloads as wl
+    w, _ = wl.model_weights(workload)
+    M = ql.f32_model(w, device="cuda")
+    x = torch.from_numpy(wl.features(workload)).cuda()
+    T, B, _ = x.shape
+    ws = ql.Workspace()
+    post = torch.empty(T, B, M.Wy.shape[0], dtype=torch.float32, device="cuda")
+    for _ in range(warmup):
+        ql.f32_acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+    torch.cuda.synchronize()
+    with Timer(torch) as tm:
+        for _ in range(steps):
+            ql.f32_acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "fp32 steps")
+    return tm.ms / steps
+
+
+def time_layer(ql, torch, workload, steps, warmup):
+    """ms per lstm_layer_forward call of a one-layer workload (no output layer)."""
+    from paper_1607_04683_amd import workloads as wl
+    w, _ = wl.model_weights(workload)
+    L = ql.quantize_layer(w["layers"][0])
+    x = torch.from_numpy(wl.features(workload)).cuda()
+    ws = ql.Workspace()
+    for _ in range(warmup):
+        ql.lstm_layer_forward(L, x, workspace=ws, check=False)
+    torch.cuda.synchronize()
+    with Timer(torch) as tm:
+        for _ in range(steps):
+            ql.lstm_layer_forward(L, x, workspace=ws, check=False)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "layer steps")
+    return tm.ms / steps
+
+
 def gemm_sweep(ql, torch, n, reps):
     from paper_1607_04683_amd import workloads as wl
     A, Bm = wl.gemm_operands(n, n, n, seed=0)
@@ -147,7 +186,8 @@ def cpu_baseline(workload, frames):
     from oracle import oracle
     from paper_1607_04683_amd import workloads as wl
     w, _ = wl.model_weights(workload)
-    n_utt = min(workload.B, max(1, int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))))
+    threads = max(1, int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)))
+    n_utt = min(workload.B, max(threads, -(-frames // workload.T)))
     T = max(1, min(workload.T, frames // n_utt))
     x = wl.features(workload, utterances=list(range(n_utt)))[:T]
     Mq = oracle.quantize_model(w)
@@ -169,6 +209,28 @@ def cpu_baseline(workload, frames):
                        f"({T * n_utt} frames, {dt:.1f} s, {cpu})")
 
 
+def profile_target(ql, torch, target, reps):
+    """One piece of the benchmark alone, so a counter pass sees only its kernels."""
+    from paper_1607_04683_amd import workloads as wl
+    if target.startswith("recurrence"):
+        W = wl.LSTM5x500_S8192_T1000_B64 if target.endswith("b64") else wl.LSTM5x500_S8192_T500_B1
+        _, M, x = model_on_device(ql, W, torch)
+        out = recurrence_kernel(ql, torch, M, x, reps)
+        out["workload"] = W.name
+    elif target == "gemm8192":
+        out = gemm_sweep(ql, torch, 8192, reps)
+    else:  # a plain device copy of 1 GiB: calibrates the byte counters
+        n = 1 << 28
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(reps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out = dict(bytes_read=4 * n, bytes_written=4 * n, copies=reps)
+    out["target"] = target
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -182,6 +244,9 @@ def main():
     from paper_1607_04683_amd import workloads as wl
     ql.load()
     torch.cuda.set_device(0)
+    if args.profile_target:
+        profile_target(ql, torch, args.profile_target, reps=3)
+        return
 
     # ---- headline: 5x500 + softmax 8192 at batch 64 x T=1000
     W64 = wl.LSTM5x500_S8192_T1000_B64
@@ -215,6 +280,20 @@ def main():
                                             (rec1["per_step_us"] * 1e-6) / 1e9, 1))
         log(f"batch 1: {extra['batch1']}")
         del M1, x1
+        W0 = wl.LSTM1x500_T300_B1
+        ms0 = time_layer(ql, torch, W0, max(3, args.steps // 2), args.warmup)
+        extra["layer_b1"] = dict(workload=W0.name, ms_per_step=round(ms0, 3),
+                                 frames_per_s=round(W0.T / (ms0 * 1e-3), 1))
+        log(f"one layer, batch 1: {extra['layer_b1']}")
+        f64 = time_f32_model(ql, torch, W64, 3, 1)
+        f1 = time_f32_model(ql, torch, W1, 3, 1)
+        extra["fp32_model"] = dict(
+            note="unquantized fp32 model, same API and kernel structure",
+            batch64=dict(ms_per_step=round(f64, 3), frames_per_s=round(frames / (f64 * 1e-3), 1),
+                         int8_speedup=round(f64 / ms, 3)),
+            batch1=dict(ms_per_step=round(f1, 3), frames_per_s=round(W1.T / (f1 * 1e-3), 1),
+                        int8_speedup=round(f1 / ms1, 3)))
+        log(f"fp32 model: {extra['fp32_model']}")
         W5 = wl.LSTMP4x2048P512_S16384_T800_B256
         log(f"setup {W5.name}")
         _, M5, x5 = model_on_device(ql, W5, torch)
