@@ -29,6 +29,24 @@ METRIC = "quantized LSTM AM frames/sec at batch 1 and 64; int8 GEMM TOPS vs MFMA
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 
+# HBM bytes per launch of the dominant kernel (the recurrence of one 500-cell
+# layer at batch 64, T = 1000), from two rocprofv3 --pmc passes (FETCH_SIZE,
+# WRITE_SIZE) scaled by the same counters on a plain 1 GiB copy; valid only
+# for the kernel sources with this digest (any edit makes it stale -> null).
+TRAFFIC = dict(bytes=2.825e9, read=2.466e9, written=0.359e9,
+               sources=("ql_recurrent.hip", "ql_device.h", "ql_exchange.h", "ql_launch.h"),
+               sha256="896052378771745a41a92370ec3b352a995dcc5eb31361baa6985b4f8e0d401b",
+               summary="profiles/k_recurrent_5x500_B64_T1000_counters.md")
+
+
+def measured_traffic():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC["sources"]:
+        with open(os.path.join(ROOT, "paper_1607_04683_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return TRAFFIC["bytes"] if h.hexdigest() == TRAFFIC["sha256"] else None
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -263,7 +281,8 @@ def main():
         f"{achieved:.1f} GB/s algorithmic")
     roofline = dict(bound="hbm", kernel="k_recurrent (one 500-cell layer, B=64, T=1000)",
                     achieved=round(achieved, 2), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 5), traffic=None,
+                    frac=round(achieved / HBM_PEAK_GBS, 5), traffic=measured_traffic(),
+                    traffic_unit="bytes per launch", traffic_source=TRAFFIC["summary"],
                     avg_launch_ms=round(rec["avg_ms"], 4), alg_bytes=rec["alg_bytes"])
 
     extra = {}
