@@ -283,24 +283,94 @@ ql_status ql_lstm_layer_forward(const ql_lstm_layer *L, const float *x, int64_t 
   return run_layer(*L, w.xin.rows(), T, B, h0, c0, h, hT, cT, w, taps, s);
 }
 
-size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B) {
-  if (!M || M->nlayers <= 0 || !M->layers || T < 0 || B < 0) return 0;
+}  // extern "C"
+
+namespace {
+// A model whose layers share one width H <= 512 and have no projection can
+// run several layers per persistent launch (a wavefront); per-layer
+// accumulator taps need the one-layer path.
+bool stackable(const ql_model &M) {
+  if (M.nlayers < 2) return false;
+  for (int l = 0; l < M.nlayers; ++l) {
+    const ql_lstm_layer &L = M.layers[l];
+    if (L.proj != 0 || L.hidden != M.layers[0].hidden || L.hidden > 512) return false;
+  }
+  return true;
+}
+bool codes_taps_only(const ql_model_taps *taps, int nlayers) {
+  if (!taps || !taps->layers) return true;
+  for (int l = 0; l < nlayers; ++l) {
+    const ql_lstm_taps &t = taps->layers[l];
+    if (t.acc_x || t.acc_h || t.acc_r) return false;
+  }
+  return true;
+}
+
+// Workspace of a model forward: exchange scratch first (it holds the timeout
+// flag), then the input codes, W_x x + b, one code buffer per layer, h.
+struct ModelWs {
+  void *rec;
+  ActBuf xin;
+  float *gx;
+  ActBuf out[kMaxStack > 16 ? kMaxStack : 16];
+  float *hf;
+  void *sws;
+};
+ModelWs carve_model(Carve &c, const ql_model &M, int64_t T, int64_t B) {
   int64_t maxH = 0, maxR = 0, maxP = 0;
-  for (int l = 0; l < M->nlayers; ++l) {
-    const ql_lstm_layer &L = M->layers[l];
+  for (int l = 0; l < M.nlayers; ++l) {
+    const ql_lstm_layer &L = M.layers[l];
     maxH = L.hidden > maxH ? L.hidden : maxH;
     maxR = layer_width(L) > maxR ? layer_width(L) : maxR;
     maxP = L.proj > maxP ? L.proj : maxP;
   }
+  const int64_t MB = T * B;
+  size_t rec = recurrent_ws(B, maxH, maxP);
+  if (stackable(M)) {
+    const size_t st = stack_ws(M.nlayers < kMaxStack ? M.nlayers : kMaxStack, T, B, maxH);
+    rec = rec > st ? rec : st;
+  }
+  ModelWs w{};
+  w.rec = c.take<char>(rec);
+  w.xin = take_act(c, MB, M.layers[0].in);
+  w.gx = c.take<float>((size_t)(MB * 4 * maxH));
+  // one output code buffer per layer (two alternate when layers run one by one)
+  const int nbuf = stackable(M) ? (M.nlayers < 16 ? M.nlayers : 16) : 2;
+  for (int i = 0; i < nbuf; ++i) w.out[i] = take_act(c, MB, maxR);
+  w.hf = c.take<float>((size_t)(MB * maxR));
+  w.sws = c.take<char>(softmax_ws(MB, M.Wy.rows));
+  return w;
+}
+
+StackLayer stack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf &out,
+                       const ql_lstm_taps *t) {
+  StackLayer s{};
+  s.Wx = weight(L.Wx);
+  s.Wh = weight(L.Wh);
+  s.bias = L.bias;
+  s.in = L.in;
+  s.xin = xin;
+  s.out = OutRows{out.codes, out.ld, out.zero, out.inv_q, out.sums};
+  s.h = nullptr;
+  if (t) {
+    s.tap_codes = t->h_codes;
+    s.tap_zero = t->h_zero;
+    s.tap_inv_q = t->h_inv_q;
+  }
+  return s;
+}
+
+size_t model_ws_bytes(const ql_model *M, int64_t T, int64_t B) {
   Carve c(nullptr);
-  c.take<char>(recurrent_ws(B, maxH, maxP));
-  take_act(c, T * B, M->layers[0].in);
-  c.take<float>((size_t)(T * B * 4 * maxH));
-  take_act(c, T * B, maxR);
-  take_act(c, T * B, maxR);
-  c.take<float>((size_t)(T * B * maxR));
-  c.take<char>(softmax_ws(T * B, M->Wy.rows));
+  carve_model(c, *M, T, B);
   return c.off;
+}
+}  // namespace
+
+extern "C" {
+size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B) {
+  if (!M || M->nlayers <= 0 || !M->layers || T < 0 || B < 0) return 0;
+  return model_ws_bytes(M, T, B);
 }
 
 ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T, int64_t B,
@@ -332,34 +402,60 @@ ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64
     maxP = L.proj > maxP ? L.proj : maxP;
   }
   const int64_t MB = T * B;
+  (void)maxP;
   Carve c(ws);
-  void *rec = c.take<char>(recurrent_ws(B, maxH, maxP));
-  ActBuf xin = take_act(c, MB, M->layers[0].in);
-  float *gx = c.take<float>((size_t)(MB * 4 * maxH));
-  ActBuf buf[2] = {take_act(c, MB, maxR), take_act(c, MB, maxR)};
-  float *hf = c.take<float>((size_t)(MB * maxR));
-  void *sws = c.take<char>(softmax_ws(MB, M->Wy.rows));
+  ModelWs mw = carve_model(c, *M, T, B);
 
-  if (launch_quantize_rows(feats, M->layers[0].in, MB, M->layers[0].in, xin.codes, xin.ld,
-                           xin.zero, xin.inv_q, xin.sums, s) != hipSuccess)
+  if (launch_quantize_rows(feats, M->layers[0].in, MB, M->layers[0].in, mw.xin.codes, mw.xin.ld,
+                           mw.xin.zero, mw.xin.inv_q, mw.xin.sums, s) != hipSuccess)
     return QL_EHIP;
-  ActRows cur = xin.rows();
-  for (int l = 0; l < M->nlayers; ++l) {
+  ActRows cur = mw.xin.rows();
+  const bool stack = stackable(*M) && codes_taps_only(taps, M->nlayers);
+  int per_launch = 1;
+  if (stack) {
+    const int64_t in1 = M->nlayers > 1 ? M->layers[1].in : M->layers[0].in;
+    per_launch = stack_layers_per_launch(M->nlayers, T, B, maxH, M->layers[0].in, in1);
+  }
+  for (int l = 0; l < M->nlayers;) {
+    const int left = M->nlayers - l;
+    // split the layers into launches of nearly equal size
+    const int launches = (left + per_launch - 1) / per_launch;
+    const int n = (left + launches - 1) / launches;
+    if (stack && n >= 2) {
+      StackArgs sa{};
+      sa.nl = n;
+      sa.T = T;
+      sa.B = B;
+      sa.H = maxH;
+      sa.ws = mw.rec;
+      for (int k = 0; k < n; ++k) {
+        const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l + k] : nullptr;
+        const ActRows xin = k == 0 ? cur : mw.out[l + k - 1].rows();
+        sa.L[k] = stack_layer(M->layers[l + k], xin, mw.out[l + k], lt);
+      }
+      bool unsupported = false;
+      if (launch_stack(sa, s, &unsupported) != hipSuccess) return QL_EHIP;
+      if (unsupported) return QL_EUNSUPPORTED;
+      cur = mw.out[l + n - 1].rows();
+      l += n;
+      continue;
+    }
     const ql_lstm_layer &L = M->layers[l];
     LayerWs w;
-    w.rec = rec;
-    w.gx = gx;
-    w.hout = buf[l & 1];
+    w.rec = mw.rec;
+    w.gx = mw.gx;
+    w.hout = mw.out[stack ? l : (l & 1)];
     w.hout.ld = round_up(layer_width(L), 64);
     const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l] : nullptr;
-    st = run_layer(L, cur, T, B, nullptr, nullptr, hf, nullptr, nullptr, w, lt, s);
+    st = run_layer(L, cur, T, B, nullptr, nullptr, mw.hf, nullptr, nullptr, w, lt, s);
     if (st != QL_OK) return st;
     cur = w.hout.rows();
+    ++l;
   }
   const int64_t K = layer_width(M->layers[M->nlayers - 1]);
   return from_hip(launch_softmax_layer(cur, weight(M->Wy), MB, M->Wy.rows, K, M->by, post,
                                        taps ? taps->acc_y : nullptr,
-                                       taps ? taps->logits : nullptr, sws, s));
+                                       taps ? taps->logits : nullptr, mw.sws, s));
 }
 
 size_t ql_lstm_recurrence_workspace(const ql_lstm_layer *L, int64_t T, int64_t B) {

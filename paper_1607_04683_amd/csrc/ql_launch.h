@@ -94,6 +94,39 @@ hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
 // Zeroes the n64 64-bit words after the workspace header (counters first).
 hipError_t clear_exchange(void *ws, int64_t n64, hipStream_t s);
 
+// ---- several stacked layers in one launch (ql_stack.hip)
+constexpr int kMaxStack = 8;
+// Codes + row params a layer writes for every frame (its output).
+struct OutRows {
+  int8_t *codes;
+  int64_t ld;
+  int32_t *zero;
+  float *inv_q;
+  int32_t *sums;
+};
+struct StackLayer {
+  WeightMat Wx, Wh;        // [4H][ld] each
+  const float *bias;       // [4H]
+  int64_t in;              // input width
+  ActRows xin;             // input codes: the launch's first layer reads finished data,
+                           // a later layer reads the previous layer's `out`
+  OutRows out;             // [T*B] rows of codes of h_t + params
+  float *h;                // [T][B][H] fp32 (nullable)
+  int8_t *tap_codes;       // optional taps: [T][B][H] codes (ld = H), zero, inv_q
+  int32_t *tap_zero;
+  float *tap_inv_q;
+};
+struct StackArgs {
+  int nl;                  // layers in this launch (2 .. kMaxStack)
+  int64_t T, B, H;         // all layers: hidden width H, no projection
+  StackLayer L[kMaxStack];
+  void *ws;                // stack_ws bytes; timeout flag cleared by the caller
+};
+size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H);
+hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported);
+// How many layers of such a stack fit one launch (1: none, use the one-layer path).
+int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0, int64_t in1);
+
 // ---- unquantized fp32 model (ql_f32.hip)
 // C[m][n] = sum_k A[m][k] B[n][k] (+ bias[n]); bias nullable.
 hipError_t launch_sgemm(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M,

@@ -31,6 +31,7 @@
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
+#include "ql_rec_common.h"
 
 #include <algorithm>
 
@@ -55,210 +56,6 @@ struct RecTiling {
   int64_t strideh, stridem;  // 64-bit words between replicas
   size_t off_w, off_x, off_s, off_c, off_col, off_row, off_gx, lds_bytes;
 };
-
-struct ColParam {
-  int64_t colterm;  // sum s_w + K (z_w + 128)
-  int32_t ztw;      // z_w + 128
-  int32_t sigw;     // sum s_w
-  float iqw;
-  int32_t pad;
-};
-struct RowParam {
-  int32_t ztx, sigx;
-  float iqx;
-  int32_t z;
-  int32_t sum;      // code sum (0..255 domain)
-  int32_t pad[3];
-};
-
-// ---------------------------------------------------------------------------
-// Per-vector quantization (eq. 2) of RB consecutive rows by one wave.
-// Rows [0, nvalid) are read from `src` (row stride `stride` elements): as
-// published words carrying `tag` (kSrcTagged: re-read until every tag
-// matches), as floats through device-coherent loads (kSrcCoherent: their
-// availability was already established), or as plain floats (kSrcPlain;
-// src null = zeros).  Rows [nvalid, ntotal) are zero vectors.  Lane l holds
-// the 4-element chunks starting at k = 4 (c*64 + l), c < NV/4, so all of a
-// group's loads are in flight together and four codes pack into one LDS
-// word; min/max, params, codes and the code sum come from registers.  Codes
-// go to dst + r*ldx (ldpad bytes, ldpad a multiple of 4), row params to
-// rp[r].  Returns false if the wait expired.
-// ---------------------------------------------------------------------------
-enum { kSrcPlain = 0, kSrcTagged = 1, kSrcCoherent = 2 };
-
-template <int NV, int RB, int MODE>
-__device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int nvalid,
-                                           int ntotal, uint32_t tag, int K, int8_t *dst,
-                                           int ldx, int ldpad, int *flag, RowParam *rp) {
-  constexpr int NC = NV / 4;
-  const int lane = threadIdx.x & 63;
-  float v[RB][NV];
-  if (MODE == kSrcTagged) {
-    const uint64_t *base = static_cast<const uint64_t *>(src);
-    long it = 0;
-    for (;;) {
-      uint32_t bad = 0;
-#pragma unroll
-      for (int r = 0; r < RB; ++r)
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int k = 4 * (c * kWave + lane) + e;
-            float x = 0.0f;
-            if (r < nvalid && k < K) {
-              const uint64_t w = ld_tagged(base + r * stride + k);
-              bad |= (uint32_t)(w >> 32) ^ tag;
-              x = __uint_as_float((uint32_t)w);
-            }
-            v[r][4 * c + e] = x;
-          }
-      if (!__any(bad != 0)) break;
-      if (wait_expired(flag, it)) return false;
-    }
-  } else {
-    const float *base = static_cast<const float *>(src);
-#pragma unroll
-    for (int r = 0; r < RB; ++r)
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int k = 4 * (c * kWave + lane) + e;
-          float x = 0.0f;
-          if (base && r < nvalid && k < K)
-            x = MODE == kSrcCoherent ? ld_coherent(base + r * stride + k) : base[r * stride + k];
-          v[r][4 * c + e] = x;
-        }
-  }
-  // order-preserving keys: min over keys, max as ~min(~key); 2*RB reductions together
-  int mm[2 * RB];
-#pragma unroll
-  for (int r = 0; r < RB; ++r) {
-    int lo = 0x7fffffff, hi = 0x7fffffff;
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool ok = 4 * (c * kWave + lane) + e < K;
-        const int key = float_key(v[r][4 * c + e]);
-        lo = ok ? min(lo, key) : lo;
-        hi = ok ? min(hi, ~key) : hi;
-      }
-    mm[r] = lo;
-    mm[RB + r] = hi;
-  }
-  wave_min_n<2 * RB>(mm);
-  int sums[RB];
-  QParams prm[RB];
-#pragma unroll
-  for (int r = 0; r < RB; ++r) {
-    float lo = key_float(mm[r]), hi = key_float(~mm[RB + r]);
-    if (r >= nvalid || !src || K == 0) lo = hi = 0.0f;
-    prm[r] = make_qparams(lo, hi);
-    int sum = 0;
-    uint32_t *d = reinterpret_cast<uint32_t *>(dst + r * ldx);
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int k0 = 4 * (c * kWave + lane);
-      uint32_t word = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool ok = k0 + e < K;
-        const int code = encode(v[r][4 * c + e], prm[r].q, prm[r].z);
-        sum += ok ? code : 0;
-        word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
-      }
-      if (r < ntotal && k0 < ldpad) d[k0 / 4] = word;
-    }
-    if (r < ntotal)
-      for (int k0 = 4 * (NC * kWave + lane); k0 < ldpad; k0 += 4 * kWave) d[k0 / 4] = 0u;
-    sums[r] = sum;
-  }
-  wave_add_n<RB>(sums);
-  if (lane == 0) {
-#pragma unroll
-    for (int r = 0; r < RB; ++r) {
-      if (r >= ntotal) break;
-      RowParam q;
-      q.z = prm[r].z;
-      q.ztx = prm[r].z + 128;
-      q.sigx = sums[r] - 128 * K;
-      q.iqx = prm[r].inv_q;
-      q.sum = sums[r];
-      rp[r] = q;
-    }
-  }
-  return true;
-}
-
-// All rows [0, ntotal) of a tile, RB-row groups handed round-robin to waves;
-// rows [0, nvalid) are real.  row_src(lb) gives the source of row lb.
-template <int NV, int RB, int MODE, class RowSrcFn>
-__device__ __forceinline__ bool quant_tile(int nvalid, int ntotal, int64_t stride, uint32_t tag,
-                                           int K, int8_t *dst, int ldx, int ldpad, int *flag,
-                                           RowParam *rp, RowSrcFn row_src) {
-  const int wave = threadIdx.x >> 6, nwave = blockDim.x >> 6;
-  for (int lb0 = wave * RB; lb0 < ntotal; lb0 += nwave * RB) {
-    const int nv = nvalid - lb0 < 0 ? 0 : (nvalid - lb0 < RB ? nvalid - lb0 : RB);
-    const int nt = ntotal - lb0 < RB ? ntotal - lb0 : RB;
-    if (!quant_rows<NV, RB, MODE>(row_src(lb0), stride, nv, nt, tag, K, dst + lb0 * ldx, ldx,
-                                    ldpad, flag, rp + lb0))
-      return false;
-  }
-  return true;
-}
-
-// ---------------------------------------------------------------------------
-// Products S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (a multiple of 64).
-// ---------------------------------------------------------------------------
-// VALU: groups of 16 lanes per (row, n) task, v_dot4 on 16-byte chunks.
-__device__ __forceinline__ void products_valu(const int8_t *x, int ldx, int nb, const int8_t *w,
-                                              int64_t ldw, int nrows, int wrows, int K, int32_t *S,
-                                              int ldS) {
-  const int tid = threadIdx.x, grp = tid >> 4, gl = tid & 15;
-  const int ntask = nb * nrows, ngrp = blockDim.x >> 4;
-  for (int task = grp; task < ntask; task += ngrp) {
-    const int lb = task / nrows, n = task % nrows;
-    const int8_t *xr = x + lb * ldx;
-    const int8_t *wr = w + (int64_t)(n < wrows ? n : wrows - 1) * ldw;
-    int acc = 0;
-    for (int k = gl * 16; k < K; k += 16 * 16) {
-      const v4i a = *reinterpret_cast<const v4i *>(xr + k);
-      const v4i b = *reinterpret_cast<const v4i *>(wr + k);
-      acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
-    }
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-    if (gl == 0) S[lb * ldS + n] = acc;
-  }
-}
-
-// MFMA: nb (multiple of 16) rows x nrows (multiple of 16) outputs.
-__device__ __forceinline__ void products_mfma(const int8_t *x, int ldx, int nb, const int8_t *w,
-                                              int64_t ldw, int nrows, int wrows, int K, int32_t *S,
-                                              int ldS) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int mt = nb / 16, nt = nrows / 16;
-  for (int tile = wave; tile < mt * nt; tile += nw) {
-    const int ti = tile / nt, tj = tile % nt;
-    const int8_t *xr = x + (ti * 16 + (lane & 15)) * ldx + (lane >> 4) * 16;
-    const int wrow = tj * 16 + (lane & 15);
-    const int8_t *wr = w + (int64_t)(wrow < wrows ? wrow : wrows - 1) * ldw + (lane >> 4) * 16;
-    v4i acc = v4i{};
-    for (int k = 0; k < K; k += 64) {
-      const v4i a = *reinterpret_cast<const v4i *>(xr + k);
-      const v4i b = *reinterpret_cast<const v4i *>(wr + k);
-      acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc, 0, 0, 0);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      S[(ti * 16 + (lane >> 4) * 4 + r) * ldS + tj * 16 + (lane & 15)] = acc[r];
-  }
-}
 
 // Store the codes of h_{t-1} (held in LDS) and their params as the layer's
 // quantized output; the whole workgroup cooperates, 16 bytes per thread.

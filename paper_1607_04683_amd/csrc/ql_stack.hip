@@ -1,0 +1,515 @@
+// ql_stack.hip -- several stacked LSTM layers (Section 4) in one persistent
+// launch, run as a wavefront: while layer l works on frame t, layer l-1 is
+// already on frame t+1 or later, so a launch of n layers takes about T + n
+// steps instead of n * T.
+//
+// Each workgroup owns a tile of (bB batch rows) x (u hidden units) of one
+// layer and keeps both of the layer's weight slices resident in LDS: the 4u
+// gate rows of W_x' and of W_h'.  Per step it
+//   1. quantizes h_{t-1} of its batch rows per vector (eq. 2), exactly as the
+//      single-layer kernel does (values exchanged inside the layer);
+//   2. takes the codes of x_t: the launch's first layer reads them from the
+//      already quantized input, a later layer reads the codes layer l-1
+//      produced for its h_t, which are the same codes layer l-1 used itself
+//      (one vector, one quantization; no re-quantization);
+//   3. forms both 8-bit products, recovers them (eq. 1 / eq. 3), adds the
+//      bias as the hoisted path does, (W_x x + b) + W_h h, and runs the gates;
+//   4. publishes h_t to its own layer and stores its share of the codes of
+//      h_{t-1} (the layer's output and the next layer's input).
+// Between layers nothing is reused: codes go to full-length [T*B] buffers,
+// so a layer may run any number of steps ahead of the next one; a layer
+// never waits on a later layer.  Readiness: with 16+ batch rows per tile the
+// arrival counter a workgroup bumps after step t+1 also certifies its share
+// of the codes of h_t (stored, with device-coherent stores, before the
+// bump); with one batch row per tile the codes travel as tagged words.
+#include "ql_device.h"
+#include "ql_exchange.h"
+#include "ql_launch.h"
+#include "ql_rec_common.h"
+
+#include <algorithm>
+
+namespace ql {
+
+constexpr int kStackThreads = 512;
+
+// Per-layer counters: [layer][parity][slice], 64 bytes apart.
+constexpr size_t kStackCounterBytes = (size_t)2 * kMaxSlices * 64;
+
+struct StackTiling {
+  int bB, u, nbt, nut, gl;  // tile shape and counts; gl workgroups per layer
+  int grid, mfma;
+  int ldH;                  // padded width of h codes (and W_h' rows)
+  int ldXmax;               // largest padded input width over the launch
+  int ldsW, ldsWx, ldsX, ldsXx;
+  int reph;                 // replicas of the tagged h buffer (one batch row per tile)
+  int64_t strideh;          // 64-bit words between replicas
+  int nw;                   // tagged code words per row: ldH / 4 codes + 3 params
+  size_t hx_bytes, cx_bytes, layer_bytes;  // exchange bytes per layer
+  size_t off_wh, off_wx, off_xh, off_xx, off_sh, off_sx, off_c, off_colh, off_colx, off_rowh,
+      off_rowx, off_bias, lds_bytes;
+};
+
+__device__ __forceinline__ void st_coherent64(uint64_t *p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_coherent64(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent_i(int32_t *p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_coherent_i(const int32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Row params of x codes as the products need them.
+__device__ __forceinline__ RowParam row_param(int32_t z, float iq, int32_t sum, int K) {
+  RowParam q;
+  q.z = z;
+  q.ztx = z + 128;
+  q.sigx = sum - 128 * K;
+  q.iqx = iq;
+  q.sum = sum;
+  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  return q;
+}
+
+template <int NVA, bool MFA>
+__global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTiling tl) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  int8_t *wh = reinterpret_cast<int8_t *>(smem + tl.off_wh);
+  int8_t *wx = reinterpret_cast<int8_t *>(smem + tl.off_wx);
+  int8_t *xh = reinterpret_cast<int8_t *>(smem + tl.off_xh);
+  int8_t *xx = reinterpret_cast<int8_t *>(smem + tl.off_xx);
+  int32_t *Sh = reinterpret_cast<int32_t *>(smem + tl.off_sh);
+  int32_t *Sx = reinterpret_cast<int32_t *>(smem + tl.off_sx);
+  float *cst = reinterpret_cast<float *>(smem + tl.off_c);
+  ColParam *cph = reinterpret_cast<ColParam *>(smem + tl.off_colh);
+  ColParam *cpx = reinterpret_cast<ColParam *>(smem + tl.off_colx);
+  RowParam *rph = reinterpret_cast<RowParam *>(smem + tl.off_rowh);
+  RowParam *rpx = reinterpret_cast<RowParam *>(smem + tl.off_rowx);
+  float *bsl = reinterpret_cast<float *>(smem + tl.off_bias);
+  __shared__ int s_abort;
+  constexpr bool CNT = MFA;  // batched tiles: counters + coherent data; else tagged words
+
+  const int64_t T = a.T, B = a.B, H = a.H;
+  int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
+  const int l = blockIdx.x / tl.gl, wgi = blockIdx.x % tl.gl;
+  const StackLayer &Ly = a.L[l];
+  const int64_t IN = Ly.in;
+  const int ldXl = (int)((IN + 63) / 64 * 64);
+  unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  auto counter = [&](int layer, int64_t par, int slice) {
+    return cnt0 + ((layer * 2 + (int)par) * kMaxSlices + slice) * 16;
+  };
+  char *xbase = static_cast<char *>(a.ws) + kHeaderBytes + (size_t)a.nl * kStackCounterBytes;
+  auto xdata = [&](int layer) { return xbase + (size_t)layer * tl.layer_bytes; };
+  // own layer's h exchange: counter mode float [2][B][H]; tagged mode replicas of [2][B][H]
+  float *xhf = reinterpret_cast<float *>(xdata(l));
+  uint64_t *xht = reinterpret_cast<uint64_t *>(xdata(l));
+  const uint64_t *xht_mine = xht + (blockIdx.x % tl.reph) * tl.strideh;
+  // tagged codes of every h_t of a layer: [T*B][nw] words after its h exchange
+  auto ctag = [&](int layer) {
+    return reinterpret_cast<uint64_t *>(xdata(layer) + tl.hx_bytes);
+  };
+
+  const int tid = threadIdx.x;
+  const int tb = wgi / tl.nut, tu = wgi % tl.nut;
+  const int64_t b0 = (int64_t)tb * tl.bB, j0 = (int64_t)tu * tl.u;
+  const int nb = (int)(B - b0 < tl.bB ? B - b0 : tl.bB);
+  const int nu = (int)(H - j0 < tl.u ? H - j0 : tl.u);
+  const int nrows = 4 * tl.u;  // gate-major: row g*u + jj
+  const int rowsA = MFA ? tl.bB : nb;
+  constexpr int RBA = (MFA && NVA <= 8) ? 2 : 1;
+  const unsigned prod = (unsigned)tl.nut;
+  if (tid == 0) s_abort = 0;
+
+  // ---- prologue: W_x' and W_h' slices, column params, bias, c = 0
+  for (int idx = tid; idx < nrows * (tl.ldH / 16); idx += blockDim.x) {
+    const int r = idx / (tl.ldH / 16), kc = idx % (tl.ldH / 16);
+    const int g = r / tl.u, jj = r % tl.u;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (jj < nu) v = *reinterpret_cast<const uint4 *>(Ly.Wh.codes + (g * H + j0 + jj) * Ly.Wh.ld + kc * 16);
+    *reinterpret_cast<uint4 *>(wh + r * tl.ldsW + kc * 16) = v;
+  }
+  for (int idx = tid; idx < nrows * (ldXl / 16); idx += blockDim.x) {
+    const int r = idx / (ldXl / 16), kc = idx % (ldXl / 16);
+    const int g = r / tl.u, jj = r % tl.u;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (jj < nu) v = *reinterpret_cast<const uint4 *>(Ly.Wx.codes + (g * H + j0 + jj) * Ly.Wx.ld + kc * 16);
+    *reinterpret_cast<uint4 *>(wx + r * tl.ldsWx + kc * 16) = v;
+  }
+  for (int r = tid; r < nrows; r += blockDim.x) {
+    const int g = r / tl.u, jj = r % tl.u;
+    const int64_t n = g * H + j0 + (jj < nu ? jj : 0);
+    {
+      const int64_t blk = n / Ly.Wh.rows_per_block;
+      ColParam c;
+      c.ztw = Ly.Wh.zero[blk] + 128;
+      c.sigw = Ly.Wh.row_sums[n] - 128 * (int32_t)H;
+      c.colterm = (int64_t)c.sigw + H * (int64_t)c.ztw;
+      c.iqw = Ly.Wh.inv_q[blk];
+      c.pad = 0;
+      cph[r] = c;
+    }
+    {
+      const int64_t blk = n / Ly.Wx.rows_per_block;
+      ColParam c;
+      c.ztw = Ly.Wx.zero[blk] + 128;
+      c.sigw = Ly.Wx.row_sums[n] - 128 * (int32_t)IN;
+      c.colterm = (int64_t)c.sigw + IN * (int64_t)c.ztw;
+      c.iqw = Ly.Wx.inv_q[blk];
+      c.pad = 0;
+      cpx[r] = c;
+    }
+    bsl[r] = Ly.bias[n];
+  }
+  for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) cst[idx] = 0.0f;
+  __syncthreads();
+
+  for (int64_t t = 0; t <= T; ++t) {
+    const int64_t hcur = (t & 1) * B * H;
+    // ---- 1. h_{t-1} of this batch slice, quantized per vector
+    bool ok;
+    if (t == 0) {
+      ok = quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
+                                           [&](int) -> const void * { return nullptr; });
+    } else if (CNT) {
+      const int64_t par = (t - 1) & 1;
+      if (!wait_count(counter(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod, flag)) s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      const float *prev = xhf + par * B * H;
+      ok = quant_tile<NVA, RBA, kSrcCoherent>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag,
+                                              rph, [&](int lb) -> const void * {
+                                                return prev + (b0 + lb) * H;
+                                              });
+    } else {
+      const uint64_t *prev = xht_mine + ((t + 1) & 1) * B * H;
+      ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)t, (int)H, xh, tl.ldsX, tl.ldH,
+                                            flag, rph, [&](int lb) -> const void * {
+                                              return prev + (b0 + lb) * H;
+                                            });
+    }
+    if (!ok) s_abort = 1;
+    __syncthreads();
+    if (s_abort) return;
+
+    // ---- share of the codes of h_{t-1}: this layer's output and, inside the
+    // launch, the next layer's input (16-byte chunk c goes to tile c % nut)
+    if (t > 0) {
+      const int64_t row0 = (t - 1) * B + b0;
+      const int chunks = (int)(Ly.out.ld / 16);
+      for (int idx = tid; idx < nb * chunks; idx += blockDim.x) {
+        const int lb = idx / chunks, ch = idx % chunks;
+        if (ch % tl.nut != tu) continue;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
+        uint64_t *dst = reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16);
+        if (CNT) {
+          st_coherent64(dst, ((uint64_t)v.y << 32) | v.x);
+          st_coherent64(dst + 1, ((uint64_t)v.w << 32) | v.z);
+        } else {
+          dst[0] = ((uint64_t)v.y << 32) | v.x;
+          dst[1] = ((uint64_t)v.w << 32) | v.z;
+        }
+      }
+      if (tu == 0)
+        for (int lb = tid; lb < nb; lb += blockDim.x) {
+          const int64_t row = row0 + lb;
+          if (CNT) {
+            st_coherent_i(&Ly.out.zero[row], rph[lb].z);
+            st_coherent(&Ly.out.inv_q[row], rph[lb].iqx);
+            st_coherent_i(&Ly.out.sums[row], rph[lb].sum);
+          } else {
+            Ly.out.zero[row] = rph[lb].z;
+            Ly.out.inv_q[row] = rph[lb].iqx;
+            Ly.out.sums[row] = rph[lb].sum;
+          }
+          if (Ly.tap_zero) Ly.tap_zero[row] = rph[lb].z;
+          if (Ly.tap_inv_q) Ly.tap_inv_q[row] = rph[lb].iqx;
+        }
+      if (Ly.tap_codes && tu == 0)
+        for (int idx = tid; idx < nb * (int)H; idx += blockDim.x) {
+          const int lb = idx / (int)H, k = idx % (int)H;
+          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
+        }
+      if (!CNT && l + 1 < a.nl) {
+        // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
+        uint64_t *ct = ctag(l);
+        for (int idx = tid; idx < nb * tl.nw; idx += blockDim.x) {
+          const int lb = idx / tl.nw, wd = idx % tl.nw;
+          if (wd % tl.nut != tu) continue;
+          uint32_t pay;
+          if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
+          else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
+          else if (wd == tl.ldH / 4 + 1) pay = __float_as_uint(rph[lb].iqx);
+          else pay = (uint32_t)rph[lb].sum;
+          __hip_atomic_store(ct + (row0 + lb) * tl.nw + wd, ((uint64_t)t << 32) | pay,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+    if (t == T) {
+      if (CNT) arrive(counter(l, T & 1, tb));  // certifies the codes of h_{T-1}
+      break;
+    }
+
+    // ---- 2. codes of x_t
+    const int64_t xrow0 = t * B + b0;
+    if (l == 0) {
+      const int chunks = ldXl / 16;
+      for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
+        const int lb = idx / chunks, ch = idx % chunks;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (lb < nb) v = *reinterpret_cast<const uint4 *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld + ch * 16);
+        *reinterpret_cast<uint4 *>(xx + lb * tl.ldsXx + ch * 16) = v;
+      }
+      for (int lb = tid; lb < rowsA; lb += blockDim.x)
+        rpx[lb] = lb < nb ? row_param(Ly.xin.zero[xrow0 + lb], Ly.xin.inv_q[xrow0 + lb],
+                                      Ly.xin.sums[xrow0 + lb], (int)IN)
+                          : row_param(0, 0.0f, 0, (int)IN);
+    } else if (CNT) {
+      // layer l-1's arrivals after its step t+1 certify the codes of its h_t
+      if (!wait_count(counter(l - 1, (t + 1) & 1, tb), (unsigned)(((t + 1) >> 1) + 1) * prod, flag))
+        s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      const int words = ldXl / 8;
+      for (int idx = tid; idx < rowsA * words; idx += blockDim.x) {
+        const int lb = idx / words, wd = idx % words;
+        uint64_t v = 0;
+        if (lb < nb)
+          v = ld_coherent64(reinterpret_cast<const uint64_t *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld) + wd);
+        *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = v;
+      }
+      for (int lb = tid; lb < rowsA; lb += blockDim.x)
+        rpx[lb] = lb < nb ? row_param(ld_coherent_i(&Ly.xin.zero[xrow0 + lb]),
+                                      ld_coherent(&Ly.xin.inv_q[xrow0 + lb]),
+                                      ld_coherent_i(&Ly.xin.sums[xrow0 + lb]), (int)IN)
+                          : row_param(0, 0.0f, 0, (int)IN);
+    } else {
+      // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
+      const uint64_t *ct = ctag(l - 1);
+      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
+      long it = 0;
+      for (;;) {
+        uint32_t bad = 0;
+        for (int idx = tid; idx < nb * nwx; idx += blockDim.x) {
+          const int lb = idx / nwx, wd = idx % nwx;
+          const uint64_t wv = ld_tagged(ct + (xrow0 + lb) * nwx + wd);
+          bad |= (uint32_t)(wv >> 32) ^ (uint32_t)(t + 1);
+          const uint32_t pay = (uint32_t)wv;
+          if (wd < ldXl / 4) *reinterpret_cast<uint32_t *>(xx + lb * tl.ldsXx + 4 * wd) = pay;
+          else if (wd == ldXl / 4) rpx[lb].z = (int32_t)pay;
+          else if (wd == ldXl / 4 + 1) rpx[lb].iqx = __uint_as_float(pay);
+          else rpx[lb].sum = (int32_t)pay;
+        }
+        if (!__syncthreads_or(bad != 0)) break;
+        if (tid == 0 && wait_expired(flag, it)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+      }
+      for (int lb = tid; lb < nb; lb += blockDim.x)
+        rpx[lb] = row_param(rpx[lb].z, rpx[lb].iqx, rpx[lb].sum, (int)IN);
+    }
+    __syncthreads();
+
+    // ---- 3. both products against the resident slices
+    if (MFA) {
+      products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+      products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+    } else {
+      products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+      products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+    }
+    __syncthreads();
+
+    // ---- 4. recover, gates, cell; publish h_t
+    const int pairs = nb * nu;
+    for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
+      const int pr = idx >> 2, gg = idx & 3;
+      const int lb = pr / nu, jj = pr % nu;
+      const int64_t b = b0 + lb, j = j0 + jj;
+      const int n = gg * tl.u + jj;
+      const RowParam rx = rpx[lb], rh = rph[lb];
+      const ColParam cx = cpx[n], ch = cph[n];
+      const float gxv = recover(Sx[lb * nrows + n], cx.colterm, cx.ztw, rx.ztx, rx.sigx, cx.iqw, rx.iqx) + bsl[n];
+      const float yh = recover(Sh[lb * nrows + n], ch.colterm, ch.ztw, rh.ztx, rh.sigx, ch.iqw, rh.iqx);
+      const float av = gxv + yh;
+      const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
+      const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
+      const int base = (threadIdx.x & 63) & ~3;
+      const float ig = __shfl(act, base + 0, 64);
+      const float fg = __shfl(act, base + 1, 64);
+      const float gv = __shfl(act, base + 2, 64);
+      const float og = __shfl(act, base + 3, 64);
+      if (gg == 0) {
+        const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
+        cst[lb * tl.u + jj] = cn;
+        const float m = og * tanh_cw(cn);
+        if (CNT)
+          st_coherent(&xhf[hcur + b * H + j], m);
+        else
+          for (int c2 = 0; c2 < tl.reph; ++c2)
+            publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+        if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
+      }
+    }
+    if (CNT) arrive(counter(l, t & 1, tb));
+    __syncthreads();  // LDS of this step is free before the next step's quantization
+  }
+}
+
+// ------------------------------------------------------------------ host side
+static bool plan_stack(const StackArgs &a, int cus, int lds_max, StackTiling *out) {
+  StackTiling tl{};
+  const int64_t B = a.B, H = a.H;
+  const int G = cus / a.nl;  // workgroups per layer
+  tl.ldH = (int)round_up(H, 64);
+  int64_t maxin = 0;
+  for (int l = 0; l < a.nl; ++l) maxin = std::max(maxin, a.L[l].in);
+  tl.ldXmax = (int)round_up(maxin, 64);
+  tl.ldsW = tl.ldH + 16;
+  tl.ldsWx = tl.ldXmax + 16;
+  tl.ldsX = tl.ldH + 16;
+  tl.ldsXx = tl.ldXmax + 16;
+  if (B < 16) {
+    tl.bB = 1;
+    tl.mfma = 0;
+    tl.nbt = (int)B;
+    const int nut = G / (int)B;
+    if (nut < 1) return false;
+    tl.u = (int)((H + nut - 1) / nut);
+  } else {
+    tl.bB = 16;
+    tl.mfma = 1;
+    tl.nbt = (int)((B + 15) / 16);
+    if (tl.nbt > G) return false;
+    const int nut = G / tl.nbt;
+    tl.u = (int)((H + nut - 1) / nut);
+  }
+  if (tl.mfma) tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16
+  tl.nut = (int)((H + tl.u - 1) / tl.u);
+  if (tl.nbt > kMaxSlices) return false;
+  tl.gl = tl.nbt * tl.nut;
+  tl.grid = a.nl * tl.gl;
+  if (tl.grid > cus) return false;
+  const int nrows = 4 * tl.u;
+  // LDS layout
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 16);
+    return o;
+  };
+  tl.off_wh = take((size_t)nrows * tl.ldsW);
+  tl.off_wx = take((size_t)nrows * tl.ldsWx);
+  tl.off_xh = take((size_t)tl.bB * tl.ldsX);
+  tl.off_xx = take((size_t)tl.bB * tl.ldsXx);
+  tl.off_sh = take((size_t)tl.bB * nrows * 4);
+  tl.off_sx = take((size_t)tl.bB * nrows * 4);
+  tl.off_c = take((size_t)tl.bB * tl.u * 4);
+  tl.off_colh = take((size_t)nrows * sizeof(ColParam));
+  tl.off_colx = take((size_t)nrows * sizeof(ColParam));
+  tl.off_rowh = take((size_t)tl.bB * sizeof(RowParam));
+  tl.off_rowx = take((size_t)tl.bB * sizeof(RowParam));
+  tl.off_bias = take((size_t)nrows * 4);
+  tl.lds_bytes = off;
+  if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
+  // exchange per layer
+  tl.nw = tl.ldH / 4 + 3;
+  if (B < 16) {
+    tl.reph = std::max(1, std::min(4, 2048 / std::max(1, tl.u)));
+    tl.strideh = round_up(2 * B * H, 8192) + 512;
+    tl.hx_bytes = (size_t)tl.reph * tl.strideh * 8;
+    tl.cx_bytes = (size_t)a.T * B * tl.nw * 8;
+  } else {
+    tl.reph = 1;
+    tl.strideh = 0;
+    tl.hx_bytes = align_up((size_t)2 * B * H * 4, 256);
+    tl.cx_bytes = 0;
+  }
+  tl.layer_bytes = align_up(tl.hx_bytes + tl.cx_bytes, 256);
+  *out = tl;
+  return true;
+}
+
+size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H) {
+  // same sizing as plan_stack's exchange, for any tiling
+  const int64_t ldH = round_up(H, 64);
+  size_t per;
+  if (B < 16) {
+    const int64_t strideh = round_up(2 * B * H, 8192) + 512;
+    per = align_up((size_t)4 * strideh * 8 + (size_t)T * B * (ldH / 4 + 3) * 8, 256);
+  } else {
+    per = align_up(align_up((size_t)2 * B * H * 4, 256), 256);
+  }
+  return kHeaderBytes + (size_t)nl * kStackCounterBytes + (size_t)nl * per;
+}
+
+using StackKernel = void (*)(StackArgs, StackTiling);
+
+hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported) {
+  *unsupported = false;
+  if (a.T == 0 || a.B == 0) return hipSuccess;
+  if (a.nl < 1 || a.nl > kMaxStack || a.H > 512) {
+    *unsupported = true;
+    return hipSuccess;
+  }
+  int dev = 0, cus = 0, lds_max = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  StackTiling tl;
+  if (!plan_stack(a, cus, lds_max, &tl)) {
+    *unsupported = true;
+    return hipSuccess;
+  }
+  StackKernel kern = tl.mfma ? k_stack<8, true> : k_stack<8, false>;
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)tl.lds_bytes);
+  if (e != hipSuccess) return e;
+  int per_cu = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kStackThreads, tl.lds_bytes);
+  if (e != hipSuccess) return e;
+  if (per_cu * cus < tl.grid) {
+    *unsupported = true;
+    return hipSuccess;
+  }
+  const int64_t n64 =
+      (int64_t)(((size_t)a.nl * kStackCounterBytes + (size_t)a.nl * tl.layer_bytes) / 8);
+  e = clear_exchange(a.ws, n64, s);
+  if (e != hipSuccess) return e;
+  StackArgs args = a;
+  void *kargs[] = {&args, &tl};
+  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid),
+                                    dim3(kStackThreads), kargs, (unsigned)tl.lds_bytes, s);
+}
+
+// Layers per launch for a stack of n layers of width H at batch B: the most
+// that fit the chip together (at least 1; 1 means "use the one-layer path").
+int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0, int64_t in1) {
+  int dev = 0, cus = 0, lds_max = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 1;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 1;
+  if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    return 1;
+  if (H > 512) return 1;
+  for (int nl = std::min(n, kMaxStack); nl >= 2; --nl) {
+    StackArgs a{};
+    a.nl = nl;
+    a.T = T;
+    a.B = B;
+    a.H = H;
+    for (int l = 0; l < nl; ++l) a.L[l].in = l == 0 ? in0 : in1;
+    StackTiling tl;
+    if (plan_stack(a, cus, lds_max, &tl)) return nl;
+  }
+  return 1;
+}
+
+}  // namespace ql

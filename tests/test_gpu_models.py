@@ -188,3 +188,22 @@ def test_model_empty(ql):
     M = ql.quantize_model(random_model(8, 8, 1, states=5, seed=2))
     out = ql.acoustic_model_forward(M, torch.empty(0, 2, 8, device="cuda"))
     assert out["post"].shape == (0, 2, 5)
+
+
+@pytest.mark.parametrize("layers,B", [(3, 5), (3, 37), (7, 1), (6, 20)])
+def test_model_layer_wavefront(ql, orc, layers, B):
+    """Layers sharing one width run several per launch (a wavefront); codes of
+    every layer stay bit-exact and posteriors within 1e-4.  One batch row per
+    tile (tagged exchange) and 16-row tiles (counters, ragged last slice);
+    more layers than fit one launch split into several launches."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, 48, layers, states=64, seed=layers * 100 + B)
+    x = np.random.default_rng(B).standard_normal((11, B, 40)).astype(np.float32)
+    g, _ = _model_case(ql, orc, w, x, taps=("h_codes", "h_zero", "h_inv_q"))
+    # the one-layer-per-launch path (forced by accumulator taps) gives the same bits
+    M = ql.quantize_model(w)
+    one = ql.acoustic_model_forward(M, torch.from_numpy(x).cuda(), taps=True)
+    assert torch.equal(one["post"], g["post"])
+    for l in range(layers):
+        assert torch.equal(one["layers"][l]["h_codes"], g["layers"][l]["h_codes"])
+        assert torch.equal(one["layers"][l]["h_zero"], g["layers"][l]["h_zero"])
