@@ -29,14 +29,16 @@ METRIC = "quantized LSTM AM frames/sec at batch 1 and 64; int8 GEMM TOPS vs MFMA
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 
-# HBM bytes per launch of the dominant kernel (the recurrence of one 500-cell
-# layer at batch 64, T = 1000), from two rocprofv3 --pmc passes (FETCH_SIZE,
-# WRITE_SIZE) scaled by the same counters on a plain 1 GiB copy; valid only
-# for the kernel sources with this digest (any edit makes it stale -> null).
-TRAFFIC = dict(bytes=2.825e9, read=2.466e9, written=0.359e9,
-               sources=("ql_recurrent.hip", "ql_device.h", "ql_exchange.h", "ql_launch.h"),
-               sha256="896052378771745a41a92370ec3b352a995dcc5eb31361baa6985b4f8e0d401b",
-               summary="profiles/k_recurrent_5x500_B64_T1000_counters.md")
+# HBM bytes per launch of the dominant kernel (the wavefront launch over the
+# first layers of the 5x500 model at batch 64, T = 1000), from two rocprofv3
+# --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
+# 1 GiB copy; valid only for the kernel sources with this digest (any edit
+# makes it stale -> null).
+TRAFFIC = dict(bytes=None, read=None, written=None,
+               sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
+                        "ql_launch.h"),
+               sha256="",
+               summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 
 def measured_traffic():
@@ -62,7 +64,8 @@ def parse():
     ap.add_argument("--cpu-frames", type=int, default=32000,
                     help="frames of the batch-64 workload the CPU oracle is timed on")
     ap.add_argument("--profile-target", default=None,
-                    choices=["recurrence_b64", "recurrence_b1", "gemm8192", "copy"],
+                    choices=["stack_b64", "stack_b1", "recurrence_b64", "recurrence_b1",
+                             "gemm8192", "copy"],
                     help="run only one piece (for hardware-counter passes) and exit")
     return ap.parse_args()
 
@@ -178,6 +181,37 @@ def time_layer(ql, torch, workload, steps, warmup):
     return tm.ms / steps
 
 
+def stack_kernel(ql, torch, M, x, n, reps):
+    """Average duration of one wavefront launch over the model's first n
+    layers (their real input codes), by HIP events around each call, and its
+    algorithmic bytes: every layer-step streams both weight matrices once
+    (decode-style), plus the codes (and per-row params) read and written."""
+    T, B, n_in = x.shape
+    layers = M.layers[:n]
+    H = layers[0].hidden
+    xq = ql.quantize_activations(x.reshape(T * B, n_in))
+    outs = [ql.QAct.empty(T * B, H, x.device) for _ in range(n)]
+    ws = ql.Workspace()
+    for _ in range(2):
+        ql.lstm_stack_forward(layers, xq, T, B, outs=outs, workspace=ws, check=False)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        with Timer(torch) as tm:
+            ql.lstm_stack_forward(layers, xq, T, B, outs=outs, workspace=ws, check=False)
+        ms.append(tm.ms)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "stack")
+    w_step = sum(4 * L.hidden * (L.n_in + L.hidden) for L in layers)
+    rows = T * B
+    alg = (T * w_step                          # W_x' and W_h' of every layer, per step
+           + rows * (n_in + 12)                # input codes + params
+           + n * rows * (H + 12)               # codes + params written by every layer
+           + (n - 1) * rows * (H + 12))        # read again by the next layer
+    avg = sum(ms) / len(ms)
+    return dict(avg_ms=avg, min_ms=min(ms), alg_bytes=alg, layers=n,
+                us_per_frame=avg * 1e3 / T, weight_bytes_per_frame=w_step)
+
+
 def gemm_sweep(ql, torch, n, reps):
     from paper_1607_04683_amd import workloads as wl
     A, Bm = wl.gemm_operands(n, n, n, seed=0)
@@ -230,7 +264,13 @@ def cpu_baseline(workload, frames):
 def profile_target(ql, torch, target, reps):
     """One piece of the benchmark alone, so a counter pass sees only its kernels."""
     from paper_1607_04683_amd import workloads as wl
-    if target.startswith("recurrence"):
+    if target.startswith("stack"):
+        W = wl.LSTM5x500_S8192_T1000_B64 if target.endswith("b64") else wl.LSTM5x500_S8192_T500_B1
+        _, M, x = model_on_device(ql, W, torch)
+        n = ql.stack_layers_per_launch(M, W.T, W.B)
+        out = stack_kernel(ql, torch, M, x, n, reps)
+        out["workload"] = W.name
+    elif target.startswith("recurrence"):
         W = wl.LSTM5x500_S8192_T1000_B64 if target.endswith("b64") else wl.LSTM5x500_S8192_T500_B1
         _, M, x = model_on_device(ql, W, torch)
         out = recurrence_kernel(ql, torch, M, x, reps)
@@ -275,11 +315,12 @@ def main():
     value = frames / (ms * 1e-3)
     log(f"batch 64: {ms:.3f} ms/step (wall {wall_ms:.3f}) -> {value:.0f} frames/s")
 
-    rec = recurrence_kernel(ql, torch, M64, x64, reps=5)
+    nst = ql.stack_layers_per_launch(M64, W64.T, W64.B)
+    rec = stack_kernel(ql, torch, M64, x64, nst, reps=5)
     achieved = rec["alg_bytes"] / (rec["avg_ms"] * 1e-3) / 1e9
-    log(f"recurrence kernel: {rec['avg_ms']:.3f} ms/launch, {rec['per_step_us']:.2f} us/step, "
-        f"{achieved:.1f} GB/s algorithmic")
-    roofline = dict(bound="hbm", kernel="k_recurrent (one 500-cell layer, B=64, T=1000)",
+    log(f"wavefront kernel ({nst} layers): {rec['avg_ms']:.3f} ms/launch, "
+        f"{rec['us_per_frame']:.2f} us/frame, {achieved:.1f} GB/s algorithmic")
+    roofline = dict(bound="hbm", kernel=f"k_stack ({nst} 500-cell layers, B=64, T=1000)",
                     achieved=round(achieved, 2), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 5), traffic=measured_traffic(),
                     traffic_unit="bytes per launch", traffic_source=TRAFFIC["summary"],
@@ -291,12 +332,17 @@ def main():
         log(f"setup {W1.name}")
         _, M1, x1 = model_on_device(ql, W1, torch)
         ms1, _ = time_model(ql, torch, M1, x1, max(3, args.steps // 2), args.warmup)
-        rec1 = recurrence_kernel(ql, torch, M1, x1, reps=5)
+        n1 = ql.stack_layers_per_launch(M1, W1.T, W1.B)
+        rec1 = stack_kernel(ql, torch, M1, x1, n1, reps=5)
         extra["batch1"] = dict(workload=W1.name, ms_per_step=round(ms1, 3),
                                frames_per_s=round(W1.T / (ms1 * 1e-3), 1),
-                               recurrence_us_per_step=round(rec1["per_step_us"], 3),
-                               wh_GBs=round(rec1["wh_bytes_per_step"] /
-                                            (rec1["per_step_us"] * 1e-6) / 1e9, 1))
+                               wavefront_layers=n1,
+                               wavefront_us_per_frame=round(rec1["us_per_frame"], 3),
+                               weight_GBs=round(rec1["weight_bytes_per_frame"] /
+                                                (rec1["us_per_frame"] * 1e-6) / 1e9, 1),
+                               weight_frac_of_hbm=round(rec1["weight_bytes_per_frame"] /
+                                                        (rec1["us_per_frame"] * 1e-6) / 1e9 /
+                                                        HBM_PEAK_GBS, 5))
         log(f"batch 1: {extra['batch1']}")
         del M1, x1
         W0 = wl.LSTM1x500_T300_B1

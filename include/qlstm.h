@@ -171,6 +171,31 @@ typedef struct {
   int32_t *sums;
 } ql_qact;
 
+/* ---- activation quantization on the fly (Section 3.1; eq. 2) ----------------------
+ * Quantizes every row of X [m][cols] fp32 as its own vector: dst->codes
+ * [m][dst->ld] (device code layout, padding 0), dst->zero / inv_q / sums per
+ * row.  dst->rows must be m, dst->cols must be cols; the caller allocates. */
+ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const ql_qact *dst,
+                                  void *stream);
+
+/* ---- several stacked layers in one launch (Section 4) ---------------------------
+ * n layers without projection and of one width H <= 512 (layer k > 0 takes
+ * layer k-1's output), run as one persistent launch in which layer k works on
+ * frame t while layer k-1 is already on a later frame.  Input: the per-vector
+ * codes of x_t (x->rows = T*B, x->cols = layers[0].in).  Output: the codes of
+ * every h_t of every layer, h_codes[k] (rows = T*B, cols = H, ld a multiple of
+ * 64), and h_last [T][B][H] fp32 of the last layer (nullable); zero initial
+ * state.  QL_EUNSUPPORTED when the n layers do not fit one launch.  Same
+ * results, bit for bit, as n calls of the one-layer path. */
+size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B);
+/* How many of the first n layers one launch holds on the current device (the
+ * grouping ql_acoustic_model_forward uses); 1 when they cannot share one. */
+int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, int64_t T,
+                                        int64_t B);
+ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,
+                                int64_t T, int64_t B, const ql_qact *h_codes, float *h_last,
+                                void *ws, size_t ws_bytes, void *stream);
+
 /* ---- the recurrence of one layer alone (Section 4) ------------------------------
  * Given the input pre-activations gx [T][B][4H] fp32 = R(Mult(Q(x_t), W_x')) + b
  * for every frame (what ql_quantized_matmul with per-row quantization and the

@@ -631,6 +631,74 @@ ql_status ql_f32_acoustic_model_forward(const ql_f32_model *M, const float *feat
   return from_hip(launch_softmax_rows(post, MB, M->states, s));
 }
 
+ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const ql_qact *dst,
+                                  void *stream) {
+  if (!dst) return QL_EINVAL;
+  if (m < 0 || cols < 0) return QL_ESHAPE;
+  if (dst->rows != m || dst->cols != cols || dst->ld < round_up(cols, 64) || dst->ld % 64)
+    return QL_ESHAPE;
+  if (m == 0) return QL_OK;
+  if (!X || !dst->codes || !dst->zero || !dst->inv_q || !dst->sums) return QL_EINVAL;
+  return from_hip(launch_quantize_rows(X, cols, m, cols, dst->codes, dst->ld, dst->zero,
+                                       dst->inv_q, dst->sums, as_stream(stream)));
+}
+
+size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B) {
+  if (!layers || n < 1 || n > kMaxStack || T < 0 || B < 0) return 0;
+  return align_up(stack_ws(n, T, B, layers[0].hidden), 256);
+}
+
+int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, int64_t T,
+                                        int64_t B) {
+  if (!layers || n < 2 || T < 0 || B < 0) return 1;
+  const int64_t H = layers[0].hidden;
+  for (int k = 0; k < n; ++k)
+    if (layers[k].proj != 0 || layers[k].hidden != H || (k > 0 && layers[k].in != H)) return 1;
+  return stack_layers_per_launch(n, T, B, H, layers[0].in, n > 1 ? layers[1].in : layers[0].in);
+}
+
+ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,
+                                int64_t T, int64_t B, const ql_qact *h_codes, float *h_last,
+                                void *ws, size_t ws_bytes, void *stream) {
+  if (!layers || !x || !h_codes) return QL_EINVAL;
+  if (n < 1 || n > kMaxStack || T < 0 || B < 0) return QL_ESHAPE;
+  const int64_t H = layers[0].hidden;
+  for (int k = 0; k < n; ++k) {
+    const ql_status st = check_layer(&layers[k]);
+    if (st != QL_OK) return st;
+    if (layers[k].proj != 0 || layers[k].hidden != H) return QL_ESHAPE;
+    if (k > 0 && layers[k].in != H) return QL_ESHAPE;
+    const ql_qact &o = h_codes[k];
+    if (o.rows != T * B || o.cols != H || o.ld < round_up(H, 64) || o.ld % 64) return QL_ESHAPE;
+    if (T * B > 0 && (!o.codes || !o.zero || !o.inv_q || !o.sums)) return QL_EINVAL;
+  }
+  if (x->rows != T * B || x->cols != layers[0].in || x->ld < round_up(x->cols, 64) || x->ld % 64)
+    return QL_ESHAPE;
+  if (T * B > 0 && (!x->codes || !x->zero || !x->inv_q || !x->sums)) return QL_EINVAL;
+  if (!ws || ws_bytes < ql_lstm_stack_workspace(layers, n, T, B)) return QL_EWORKSPACE;
+  if (n == 1) return QL_EUNSUPPORTED;  // one layer: ql_lstm_layer_forward
+  hipStream_t s = as_stream(stream);
+  if (reset_recurrent_flag(ws, s) != hipSuccess) return QL_EHIP;
+  if (T == 0 || B == 0) return QL_OK;
+  StackArgs sa{};
+  sa.nl = n;
+  sa.T = T;
+  sa.B = B;
+  sa.H = H;
+  sa.ws = ws;
+  for (int k = 0; k < n; ++k) {
+    const ActRows xin = k == 0 ? ActRows{x->codes, x->ld, x->zero, x->inv_q, x->sums}
+                               : ActRows{h_codes[k - 1].codes, h_codes[k - 1].ld, h_codes[k - 1].zero,
+                                         h_codes[k - 1].inv_q, h_codes[k - 1].sums};
+    ActBuf out{h_codes[k].codes, h_codes[k].ld, h_codes[k].zero, h_codes[k].sums, h_codes[k].inv_q};
+    sa.L[k] = stack_layer(layers[k], xin, out, nullptr);
+    if (k == n - 1) sa.L[k].h = h_last;
+  }
+  bool unsupported = false;
+  if (launch_stack(sa, s, &unsupported) != hipSuccess) return QL_EHIP;
+  return unsupported ? QL_EUNSUPPORTED : QL_OK;
+}
+
 ql_status ql_workspace_status(const void *ws, void *stream) {
   if (!ws) return QL_EINVAL;
   bool to = false;

@@ -363,7 +363,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 }
 
 // ------------------------------------------------------------------ host side
-static bool plan_stack(const StackArgs &a, int cus, int lds_max, StackTiling *out) {
+// bB: batch rows per tile (1, or a multiple of 16 for the MFMA products).
+static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, StackTiling *out) {
   StackTiling tl{};
   const int64_t B = a.B, H = a.H;
   const int G = cus / a.nl;  // workgroups per layer
@@ -375,18 +376,11 @@ static bool plan_stack(const StackArgs &a, int cus, int lds_max, StackTiling *ou
   tl.ldsWx = tl.ldXmax + 16;
   tl.ldsX = tl.ldH + 16;
   tl.ldsXx = tl.ldXmax + 16;
-  if (B < 16) {
-    tl.bB = 1;
-    tl.mfma = 0;
-    tl.nbt = (int)B;
-    const int nut = G / (int)B;
-    if (nut < 1) return false;
-    tl.u = (int)((H + nut - 1) / nut);
-  } else {
-    tl.bB = 16;
-    tl.mfma = 1;
-    tl.nbt = (int)((B + 15) / 16);
-    if (tl.nbt > G) return false;
+  tl.bB = bB;
+  tl.mfma = bB > 1;
+  tl.nbt = (int)((B + bB - 1) / bB);
+  if (tl.nbt > G) return false;
+  {
     const int nut = G / tl.nbt;
     tl.u = (int)((H + nut - 1) / nut);
   }
@@ -434,6 +428,15 @@ static bool plan_stack(const StackArgs &a, int cus, int lds_max, StackTiling *ou
   tl.layer_bytes = align_up(tl.hx_bytes + tl.cx_bytes, 256);
   *out = tl;
   return true;
+}
+
+// One batch row per tile below 16 rows; otherwise 16-row tiles, or 32-row
+// tiles when 16-row tiles of this many layers do not fit the chip's LDS (a
+// tile quantizes twice the rows per step, but all layers share one launch).
+static bool plan_stack(const StackArgs &a, int cus, int lds_max, StackTiling *out) {
+  if (a.B < 16) return plan_stack_bb(a, cus, lds_max, 1, out);
+  if (plan_stack_bb(a, cus, lds_max, 16, out)) return true;
+  return a.B >= 32 && plan_stack_bb(a, cus, lds_max, 32, out);
 }
 
 size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H) {

@@ -30,7 +30,8 @@ EXPORTS = [
     "ql_status_str", "ql_workspace_status", "ql_gate_fn", "ql_lstm_recurrence_workspace",
     "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_workspace",
     "ql_f32_lstm_layer_forward", "ql_f32_acoustic_model_workspace",
-    "ql_f32_acoustic_model_forward",
+    "ql_f32_acoustic_model_forward", "ql_quantize_activations", "ql_lstm_stack_workspace",
+    "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch",
 ]
 
 
@@ -120,6 +121,13 @@ def load(path: str = LIB_PATH):
     L.ql_workspace_status.argtypes = [vp, vp]
     L.ql_gate_fn.argtypes = [i32, vp, vp, i64, vp]
     L.ql_f32_matmul.argtypes = [vp, i64, i64, vp, i64, vp, vp, vp]
+    L.ql_quantize_activations.argtypes = [vp, i64, i64, C.POINTER(CQAct), vp]
+    L.ql_lstm_stack_workspace.argtypes = [C.POINTER(CLayer), i32, i64, i64]
+    L.ql_lstm_stack_workspace.restype = sz
+    L.ql_lstm_stack_forward.argtypes = [C.POINTER(CLayer), i32, C.POINTER(CQAct), i64, i64,
+                                        C.POINTER(CQAct), vp, vp, sz, vp]
+    L.ql_lstm_stack_layers_per_launch.argtypes = [C.POINTER(CLayer), i32, i64, i64]
+    L.ql_lstm_stack_layers_per_launch.restype = i32
     L.ql_f32_lstm_layer_workspace.argtypes = [C.POINTER(CF32Layer), i64, i64]
     L.ql_f32_lstm_layer_workspace.restype = sz
     L.ql_f32_lstm_layer_forward.argtypes = [C.POINTER(CF32Layer), vp, i64, i64, vp, vp, vp, vp,
@@ -131,7 +139,8 @@ def load(path: str = LIB_PATH):
     for f in ("ql_quantize", "ql_dequantize", "ql_quantized_matmul", "ql_gemm_u8",
               "ql_lstm_layer_forward", "ql_acoustic_model_forward", "ql_workspace_status",
               "ql_gate_fn", "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_forward",
-              "ql_f32_acoustic_model_forward"):
+              "ql_f32_acoustic_model_forward", "ql_quantize_activations",
+              "ql_lstm_stack_forward"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -533,3 +542,67 @@ def f32_acoustic_model_forward(M: F32Model, feats: torch.Tensor,
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_f32_acoustic_model_forward")
     return dict(post=post)
+
+
+# ------------------------------------------------- activation codes and stacks
+@dataclass
+class QAct:
+    """Per-vector quantized rows: codes [rows][ld] (device layout), zero,
+    inv_q, sums per row."""
+    codes: torch.Tensor
+    cols: int
+    zero: torch.Tensor
+    inv_q: torch.Tensor
+    sums: torch.Tensor
+
+    @staticmethod
+    def empty(rows: int, cols: int, device) -> "QAct":
+        return QAct(torch.zeros(rows, ld_for(cols), dtype=torch.int8, device=device), cols,
+                    torch.empty(rows, dtype=torch.int32, device=device),
+                    torch.empty(rows, dtype=torch.float32, device=device),
+                    torch.empty(rows, dtype=torch.int32, device=device))
+
+    def cstruct(self) -> CQAct:
+        return CQAct(_ptr(self.codes), self.codes.shape[0], self.cols, self.codes.shape[1],
+                     _ptr(self.zero), _ptr(self.inv_q), _ptr(self.sums))
+
+
+def quantize_activations(X: torch.Tensor, out: QAct | None = None) -> QAct:
+    """Each row of X [m][cols] quantized as its own vector (eq. 2)."""
+    X = X.contiguous()
+    m, cols = X.shape
+    q = out or QAct.empty(m, cols, X.device)
+    cq = q.cstruct()
+    _check(load().ql_quantize_activations(_ptr(X), m, cols, C.byref(cq), _stream()),
+           "ql_quantize_activations")
+    return q
+
+
+def lstm_stack_forward(layers: list, x: QAct, T: int, B: int, want_h: bool = False,
+                       outs: list | None = None, workspace: Workspace | None = None,
+                       check: bool = True):
+    """n stacked layers (no projection, one width) in one launch from input
+    codes x (T*B rows) -> dict(codes=[QAct per layer], h=[T][B][H] of the last)."""
+    lib = load()
+    n = len(layers)
+    H = layers[0].hidden
+    dev = x.codes.device
+    arr = (CLayer * n)(*[L.cstruct() for L in layers])
+    outs = outs or [QAct.empty(T * B, H, dev) for _ in range(n)]
+    oarr = (CQAct * n)(*[o.cstruct() for o in outs])
+    h = torch.empty(T, B, H, dtype=torch.float32, device=dev) if want_h else None
+    nbytes = lib.ql_lstm_stack_workspace(arr, n, T, B)
+    ws = (workspace or Workspace()).get(nbytes, dev)
+    cx = x.cstruct()
+    _check(lib.ql_lstm_stack_forward(arr, n, C.byref(cx), T, B, oarr, _ptr(h), _ptr(ws),
+                                     ws.numel(), _stream()), "ql_lstm_stack_forward")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_lstm_stack_forward")
+    return dict(codes=outs, h=h)
+
+
+def stack_layers_per_launch(M: Model, T: int, B: int) -> int:
+    """How many of M's layers one wavefront launch holds (1: none; the model
+    forward then runs one layer per launch)."""
+    arr = (CLayer * len(M.layers))(*[L.cstruct() for L in M.layers])
+    return int(load().ql_lstm_stack_layers_per_launch(arr, len(M.layers), T, B))

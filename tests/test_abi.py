@@ -154,3 +154,30 @@ def test_f32_argument_errors(ql):
                                              None) == ql.QL_EWORKSPACE
     assert lib.ql_f32_matmul(None, 4, 4, FAKE, 2, None, FAKE, None) == ql.QL_EINVAL
     assert lib.ql_f32_matmul(FAKE, -4, 4, FAKE, 2, None, FAKE, None) == ql.QL_ESHAPE
+
+
+def test_activation_and_stack_argument_errors(ql):
+    lib = ql.load()
+    q = ql.CQAct(FAKE, 4, 16, 64, FAKE, FAKE, FAKE)
+    assert lib.ql_quantize_activations(FAKE, 5, 16, C.byref(q), None) == ql.QL_ESHAPE   # rows
+    q_bad_ld = ql.CQAct(FAKE, 4, 16, 32, FAKE, FAKE, FAKE)
+    assert lib.ql_quantize_activations(FAKE, 4, 16, C.byref(q_bad_ld), None) == ql.QL_ESHAPE
+    assert lib.ql_quantize_activations(None, 4, 16, C.byref(q), None) == ql.QL_EINVAL
+    H, IN, T, B = 8, 16, 5, 2
+    empty = ql.CQMatrix(None, 0, 0, 0, 1, None, None, None, None)
+    L0 = ql.CLayer(IN, H, 0, qm(4 * H, IN, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    L1 = ql.CLayer(H, H, 0, qm(4 * H, H, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    arr = (ql.CLayer * 2)(L0, L1)
+    x = ql.CQAct(FAKE, T * B, IN, 64, FAKE, FAKE, FAKE)
+    outs = (ql.CQAct * 2)(ql.CQAct(FAKE, T * B, H, 64, FAKE, FAKE, FAKE),
+                          ql.CQAct(FAKE, T * B, H, 64, FAKE, FAKE, FAKE))
+    need = lib.ql_lstm_stack_workspace(arr, 2, T, B)
+    assert need > 0
+    f = lambda layers=arr, xx=x, wsb=need: lib.ql_lstm_stack_forward(
+        layers, 2, C.byref(xx), T, B, outs, None, FAKE, wsb, None)
+    assert f(wsb=need - 1) == ql.QL_EWORKSPACE
+    assert f(xx=ql.CQAct(FAKE, T * B + 1, IN, 64, FAKE, FAKE, FAKE)) == ql.QL_ESHAPE
+    bad = (ql.CLayer * 2)(L0, ql.CLayer(H, H + 1, 0, qm(4 * H + 4, H, 64, 4),
+                                        qm(4 * H + 4, H + 1, 64, 4), empty, FAKE))
+    assert f(layers=bad) == ql.QL_ESHAPE   # widths differ
+    assert lib.ql_lstm_stack_forward(arr, 2, None, T, B, outs, None, FAKE, need, None) == ql.QL_EINVAL

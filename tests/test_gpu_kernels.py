@@ -154,3 +154,23 @@ def test_gemm_u8_sweep_sizes_sampled_rows(ql, orc, n):
     rows = np.concatenate([[0], rows, [n - 1]])
     want = orc.gemm_u8(A[rows], Bm)
     assert np.array_equal(got[torch.from_numpy(rows).cuda()].cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("m,cols", [(1, 1), (7, 5), (300, 320), (64, 500), (33, 2048), (0, 16)])
+def test_quantize_activations_per_vector(ql, orc, m, cols):
+    """Every row quantized as its own vector (eq. 2): the oracle's per-block
+    quantizer with one block per row gives the same codes and params."""
+    rng = np.random.default_rng(m * 31 + cols)
+    X = rng.standard_normal((m, cols)).astype(np.float32)
+    if m >= 3:
+        X[1] = 0.0        # all-zero vector
+        X[2] = 0.75       # constant vector
+    q = ql.quantize_activations(torch.from_numpy(X).cuda())
+    if m == 0:
+        return
+    o = orc.quantize(X, m)
+    assert np.array_equal(u8(q.codes, cols), o.codes)
+    assert np.array_equal(q.zero.cpu().numpy(), o.zero)
+    assert np.array_equal(q.inv_q.cpu().numpy().view(np.uint32), o.inv_q.view(np.uint32))
+    assert np.array_equal(q.sums.cpu().numpy(), o.codes.astype(np.int64).sum(1))
+    assert (q.codes[:, cols:] == 0).all()

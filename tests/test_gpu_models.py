@@ -207,3 +207,24 @@ def test_model_layer_wavefront(ql, orc, layers, B):
     for l in range(layers):
         assert torch.equal(one["layers"][l]["h_codes"], g["layers"][l]["h_codes"])
         assert torch.equal(one["layers"][l]["h_zero"], g["layers"][l]["h_zero"])
+
+
+@pytest.mark.parametrize("B", [1, 20])
+def test_lstm_stack_forward_entry(ql, orc, B):
+    """ql_lstm_stack_forward on the per-vector codes of x: every layer's codes
+    and the last layer's h equal the oracle's layer-by-layer evaluation."""
+    from paper_1607_04683_amd.workloads import random_model
+    n, T = 3, 9
+    w = random_model(40, 48, n, seed=7 + B)
+    x = np.random.default_rng(B + 3).standard_normal((T, B, 40)).astype(np.float32)
+    layers = [ql.quantize_layer(L) for L in w["layers"]]
+    xq = ql.quantize_activations(torch.from_numpy(x.reshape(T * B, 40)).cuda())
+    g = ql.lstm_stack_forward(layers, xq, T, B, want_h=True)
+    cur = x
+    for k in range(n):
+        o = orc.lstm_layer_forward(orc.quantize_layer(w["layers"][k]), cur, taps=True)
+        got = u8(g["codes"][k].codes)[:, :48].reshape(T, B, 48)
+        assert np.array_equal(got, o["h_codes"]), f"layer {k}"
+        assert np.array_equal(np_(g["codes"][k].zero).reshape(T, B), o["h_zero"])
+        cur = o["h"]
+    assert np.array_equal(np_(g["h"]), cur)
