@@ -117,6 +117,14 @@ __device__ __forceinline__ uint32_t pack4_s8(int c0, int c1, int c2, int c3) {
 __device__ __forceinline__ float recover(int32_t S, int64_t colterm /* sigw + K ztw */,
                                          int32_t ztw, int32_t ztx, int32_t sigx,
                                          float iqw, float iqx) {
+  // When both zero points lie in [-255, 0] (every set whose range contains 0),
+  // V'' = V' + z lies in [-255, 255], so |T| <= K * 255^2 < 2^31 for K <= 33025
+  // and the wrapping 32-bit evaluation is T exactly (z~ = z + 128 in [-127, 128]).
+  if ((uint32_t)(ztx + 127) <= 255u && (uint32_t)(ztw + 127) <= 255u) {
+    const uint32_t t = (uint32_t)S + (uint32_t)ztx * (uint32_t)colterm +
+                       (uint32_t)ztw * (uint32_t)sigx;
+    return ((float)(int32_t)t * iqw) * iqx;
+  }
   const int64_t t = (int64_t)S + (int64_t)ztx * colterm + (int64_t)ztw * (int64_t)sigx;
   return ((float)t * iqw) * iqx;
 }
@@ -200,6 +208,13 @@ __device__ __forceinline__ void wave_add_n(int (&v)[N]) {
     v[i] = (__builtin_amdgcn_readlane(v[i], 0) + __builtin_amdgcn_readlane(v[i], 16)) +
            (__builtin_amdgcn_readlane(v[i], 32) + __builtin_amdgcn_readlane(v[i], 48));
 }
+// The value lane (lane & ~3) + K of this lane's group of four holds
+// (DPP quad_perm broadcast; all four lanes of the group must be active).
+template <int K>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), K * 0x55, 0xf, 0xf, false));
+}
+
 // Order-preserving map of a (non-NaN) float to int and back.
 __device__ __forceinline__ int float_key(float f) {
   const int u = __float_as_int(f);

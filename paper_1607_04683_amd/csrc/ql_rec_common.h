@@ -174,16 +174,35 @@ __device__ __forceinline__ void products_valu(const int8_t *x, int ldx, int nb, 
     const int8_t *xr = x + lb * ldx;
     const int8_t *wr = w + (int64_t)(n < wrows ? n : wrows - 1) * ldw;
     int acc = 0;
-    for (int k = gl * 16; k < K; k += 16 * 16) {
-      const v4i a = *reinterpret_cast<const v4i *>(xr + k);
-      const v4i b = *reinterpret_cast<const v4i *>(wr + k);
-      acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
-      acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
+    if (K == 512) {
+      // two 16-byte chunks per lane, both loaded first
+      const v4i a0 = *reinterpret_cast<const v4i *>(xr + gl * 16);
+      const v4i b0 = *reinterpret_cast<const v4i *>(wr + gl * 16);
+      const v4i a1 = *reinterpret_cast<const v4i *>(xr + gl * 16 + 256);
+      const v4i b1 = *reinterpret_cast<const v4i *>(wr + gl * 16 + 256);
+      acc = __builtin_amdgcn_sdot4(a0.x, b0.x, acc, false);
+      acc = __builtin_amdgcn_sdot4(a0.y, b0.y, acc, false);
+      acc = __builtin_amdgcn_sdot4(a0.z, b0.z, acc, false);
+      acc = __builtin_amdgcn_sdot4(a0.w, b0.w, acc, false);
+      acc = __builtin_amdgcn_sdot4(a1.x, b1.x, acc, false);
+      acc = __builtin_amdgcn_sdot4(a1.y, b1.y, acc, false);
+      acc = __builtin_amdgcn_sdot4(a1.z, b1.z, acc, false);
+      acc = __builtin_amdgcn_sdot4(a1.w, b1.w, acc, false);
+    } else {
+      for (int k = gl * 16; k < K; k += 16 * 16) {
+        const v4i a = *reinterpret_cast<const v4i *>(xr + k);
+        const v4i b = *reinterpret_cast<const v4i *>(wr + k);
+        acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
+        acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
+        acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
+        acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
+      }
     }
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    // sum over the group's 16 lanes (one DPP row): rotations by 1, 2, 4, 8
+    acc += __builtin_amdgcn_update_dpp(0, acc, 0x121, 0xf, 0xf, false);
+    acc += __builtin_amdgcn_update_dpp(0, acc, 0x122, 0xf, 0xf, false);
+    acc += __builtin_amdgcn_update_dpp(0, acc, 0x124, 0xf, 0xf, false);
+    acc += __builtin_amdgcn_update_dpp(0, acc, 0x128, 0xf, 0xf, false);
     if (gl == 0) S[lb * ldS + n] = acc;
   }
 }
@@ -200,10 +219,24 @@ __device__ __forceinline__ void products_mfma(const int8_t *x, int ldx, int nb, 
     const int wrow = tj * 16 + (lane & 15);
     const int8_t *wr = w + (int64_t)(wrow < wrows ? wrow : wrows - 1) * ldw + (lane >> 4) * 16;
     v4i acc = v4i{};
-    for (int k = 0; k < K; k += 64) {
-      const v4i a = *reinterpret_cast<const v4i *>(xr + k);
-      const v4i b = *reinterpret_cast<const v4i *>(wr + k);
-      acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc, 0, 0, 0);
+    if (K % 512 == 0) {
+      // whole 512-byte blocks of K: each block's fragments are loaded before its MFMAs
+      for (int k0 = 0; k0 < K; k0 += 512) {
+        v4i a[8], b[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          a[c] = *reinterpret_cast<const v4i *>(xr + k0 + c * 64);
+          b[c] = *reinterpret_cast<const v4i *>(wr + k0 + c * 64);
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[c], b[c], acc, 0, 0, 0);
+      }
+    } else {
+      for (int k = 0; k < K; k += 64) {
+        const v4i a = *reinterpret_cast<const v4i *>(xr + k);
+        const v4i b = *reinterpret_cast<const v4i *>(wr + k);
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc, 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r)

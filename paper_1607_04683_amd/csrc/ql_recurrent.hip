@@ -245,11 +245,12 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         // sigmoid for i, f, o; tanh(x) = 2 sigmoid(2x) - 1 for g
         const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
         const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
-        const int base = (threadIdx.x & 63) & ~3;
-        const float ig = __shfl(act, base + 0, 64);
-        const float fg = __shfl(act, base + 1, 64);
-        const float gv = __shfl(act, base + 2, 64);
-        const float og = __shfl(act, base + 3, 64);
+        // the four gates of a (b, j) pair sit in one lane quad (the loop keeps
+        // whole quads active: pairs * 4 is a multiple of 4)
+        const float ig = quad_bcast<0>(act);
+        const float fg = quad_bcast<1>(act);
+        const float gv = quad_bcast<2>(act);
+        const float og = quad_bcast<3>(act);
         if (gg == 0) {
           const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
           cst[lb * tl.u + jj] = cn;

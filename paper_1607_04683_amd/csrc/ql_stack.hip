@@ -75,7 +75,8 @@ __device__ __forceinline__ RowParam row_param(int32_t z, float iq, int32_t sum, 
   return q;
 }
 
-template <int NVA, bool MFA>
+// RBA: rows one wave quantizes together (2 for batched tiles, 1 at one row).
+template <int NVA, bool MFA, int RBA>
 __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int8_t *wh = reinterpret_cast<int8_t *>(smem + tl.off_wh);
@@ -121,7 +122,6 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   const int nu = (int)(H - j0 < tl.u ? H - j0 : tl.u);
   const int nrows = 4 * tl.u;  // gate-major: row g*u + jj
   const int rowsA = MFA ? tl.bB : nb;
-  constexpr int RBA = (MFA && NVA <= 8) ? 2 : 1;
   const unsigned prod = (unsigned)tl.nut;
   if (tid == 0) s_abort = 0;
 
@@ -168,6 +168,31 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) cst[idx] = 0.0f;
   __syncthreads();
 
+  // Counter mode: the codes of x_t (the input, or layer l-1's h_t) are loaded
+  // into registers before h_{t-1} is quantized, and parked in LDS afterwards
+  // (kXPre words per thread cover 32 rows of up to 512 codes).
+  constexpr int kXPre = 4;
+  uint64_t xpre[kXPre];
+  int32_t xpz = 0, xps = 0;
+  float xpq = 0.0f;
+  const int xwords = ldXl / 8;
+  auto prefetch_x = [&](int64_t t) {
+    const int64_t xrow0 = t * B + b0;
+#pragma unroll
+    for (int i = 0; i < kXPre; ++i) {
+      const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
+      uint64_t v = 0;
+      if (lb < nb && idx < rowsA * xwords)
+        v = ld_coherent64(reinterpret_cast<const uint64_t *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld) + wd);
+      xpre[i] = v;
+    }
+    if (tid < nb) {
+      xpz = ld_coherent_i(&Ly.xin.zero[xrow0 + tid]);
+      xpq = ld_coherent(&Ly.xin.inv_q[xrow0 + tid]);
+      xps = ld_coherent_i(&Ly.xin.sums[xrow0 + tid]);
+    }
+  };
+
   for (int64_t t = 0; t <= T; ++t) {
     const int64_t hcur = (t & 1) * B * H;
     // ---- 1. h_{t-1} of this batch slice, quantized per vector
@@ -178,8 +203,14 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     } else if (CNT) {
       const int64_t par = (t - 1) & 1;
       if (!wait_count(counter(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod, flag)) s_abort = 1;
+      // the x codes of this step (layer l-1's h_t) are usually ready by now:
+      // wait for them here so their loads overlap the quantization below
+      if (l > 0 && t < T &&
+          !wait_count(counter(l - 1, (t + 1) & 1, tb), (unsigned)(((t + 1) >> 1) + 1) * prod, flag))
+        s_abort = 1;
       __syncthreads();
       if (s_abort) return;
+      if (t < T) prefetch_x(t);
       const float *prev = xhf + par * B * H;
       ok = quant_tile<NVA, RBA, kSrcCoherent>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag,
                                               rph, [&](int lb) -> const void * {
@@ -201,9 +232,9 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     if (t > 0) {
       const int64_t row0 = (t - 1) * B + b0;
       const int chunks = (int)(Ly.out.ld / 16);
-      for (int idx = tid; idx < nb * chunks; idx += blockDim.x) {
-        const int lb = idx / chunks, ch = idx % chunks;
-        if (ch % tl.nut != tu) continue;
+      const int mych = (chunks - tu + tl.nut - 1) / tl.nut;  // chunks tu, tu + nut, ...
+      for (int idx = tid; idx < nb * mych; idx += blockDim.x) {
+        const int lb = idx / mych, ch = tu + (idx % mych) * tl.nut;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
         uint64_t *dst = reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16);
@@ -238,9 +269,9 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       if (!CNT && l + 1 < a.nl) {
         // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
         uint64_t *ct = ctag(l);
-        for (int idx = tid; idx < nb * tl.nw; idx += blockDim.x) {
-          const int lb = idx / tl.nw, wd = idx % tl.nw;
-          if (wd % tl.nut != tu) continue;
+        const int mywd = (tl.nw - tu + tl.nut - 1) / tl.nut;  // words tu, tu + nut, ...
+        for (int idx = tid; idx < nb * mywd; idx += blockDim.x) {
+          const int lb = idx / mywd, wd = tu + (idx % mywd) * tl.nut;
           uint32_t pay;
           if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
           else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
@@ -258,7 +289,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 
     // ---- 2. codes of x_t
     const int64_t xrow0 = t * B + b0;
-    if (l == 0) {
+    if (l == 0 && !CNT) {
       const int chunks = ldXl / 16;
       for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
         const int lb = idx / chunks, ch = idx % chunks;
@@ -272,23 +303,21 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
                           : row_param(0, 0.0f, 0, (int)IN);
     } else if (CNT) {
       // layer l-1's arrivals after its step t+1 certify the codes of its h_t
-      if (!wait_count(counter(l - 1, (t + 1) & 1, tb), (unsigned)(((t + 1) >> 1) + 1) * prod, flag))
-        s_abort = 1;
-      __syncthreads();
-      if (s_abort) return;
-      const int words = ldXl / 8;
-      for (int idx = tid; idx < rowsA * words; idx += blockDim.x) {
-        const int lb = idx / words, wd = idx % words;
-        uint64_t v = 0;
-        if (lb < nb)
-          v = ld_coherent64(reinterpret_cast<const uint64_t *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld) + wd);
-        *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = v;
+      // (the first layer reads finished input); at t > 0 they were awaited
+      // and loaded together with h_{t-1} above
+      if (t == 0) {
+        if (l > 0 && !wait_count(counter(l - 1, 1, tb), prod, flag)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+        prefetch_x(0);
       }
-      for (int lb = tid; lb < rowsA; lb += blockDim.x)
-        rpx[lb] = lb < nb ? row_param(ld_coherent_i(&Ly.xin.zero[xrow0 + lb]),
-                                      ld_coherent(&Ly.xin.inv_q[xrow0 + lb]),
-                                      ld_coherent_i(&Ly.xin.sums[xrow0 + lb]), (int)IN)
-                          : row_param(0, 0.0f, 0, (int)IN);
+#pragma unroll
+      for (int i = 0; i < kXPre; ++i) {
+        const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
+        if (idx < rowsA * xwords) *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = xpre[i];
+      }
+      if (tid < rowsA)
+        rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
     } else {
       // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
       const uint64_t *ct = ctag(l - 1);
@@ -328,33 +357,50 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 
     // ---- 4. recover, gates, cell; publish h_t
     const int pairs = nb * nu;
-    for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
-      const int pr = idx >> 2, gg = idx & 3;
-      const int lb = pr / nu, jj = pr % nu;
-      const int64_t b = b0 + lb, j = j0 + jj;
-      const int n = gg * tl.u + jj;
+    auto preact = [&](int lb, int n) {
       const RowParam rx = rpx[lb], rh = rph[lb];
       const ColParam cx = cpx[n], ch = cph[n];
       const float gxv = recover(Sx[lb * nrows + n], cx.colterm, cx.ztw, rx.ztx, rx.sigx, cx.iqw, rx.iqx) + bsl[n];
       const float yh = recover(Sh[lb * nrows + n], ch.colterm, ch.ztw, rh.ztx, rh.sigx, ch.iqw, rh.iqx);
-      const float av = gxv + yh;
-      const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
-      const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
-      const int base = (threadIdx.x & 63) & ~3;
-      const float ig = __shfl(act, base + 0, 64);
-      const float fg = __shfl(act, base + 1, 64);
-      const float gv = __shfl(act, base + 2, 64);
-      const float og = __shfl(act, base + 3, 64);
-      if (gg == 0) {
-        const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
-        cst[lb * tl.u + jj] = cn;
-        const float m = og * tanh_cw(cn);
-        if (CNT)
-          st_coherent(&xhf[hcur + b * H + j], m);
-        else
-          for (int c2 = 0; c2 < tl.reph; ++c2)
-            publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
-        if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
+      return gxv + yh;
+    };
+    auto finish = [&](int lb, int jj, float ig, float fg, float gv, float og) {
+      const int64_t b = b0 + lb, j = j0 + jj;
+      const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
+      cst[lb * tl.u + jj] = cn;
+      const float m = og * tanh_cw(cn);
+      if (CNT)
+        st_coherent(&xhf[hcur + b * H + j], m);
+      else
+        for (int c2 = 0; c2 < tl.reph; ++c2)
+          publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+      if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
+    };
+    if (pairs >= (int)blockDim.x) {
+      // one lane per (b, j) pair: all four gates in the lane
+      for (int pr = tid; pr < pairs; pr += blockDim.x) {
+        const int lb = pr / nu, jj = pr % nu;
+        const float ig = sigmoid_cw(preact(lb, jj));
+        const float fg = sigmoid_cw(preact(lb, tl.u + jj));
+        const float gv = 2.0f * sigmoid_cw(2.0f * preact(lb, 2 * tl.u + jj)) - 1.0f;
+        const float og = sigmoid_cw(preact(lb, 3 * tl.u + jj));
+        finish(lb, jj, ig, fg, gv, og);
+      }
+    } else {
+      // four lanes per pair (lane g of the quad computes gate g); sigmoid for
+      // i, f, o and tanh(x) = 2 sigmoid(2x) - 1 for g
+      for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
+        const int pr = idx >> 2, gg = idx & 3;
+        const int lb = pr / nu, jj = pr % nu;
+        const float av = preact(lb, gg * tl.u + jj);
+        const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
+        const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
+        // the loop keeps whole quads active (pairs * 4 is a multiple of 4)
+        const float ig = quad_bcast<0>(act);
+        const float fg = quad_bcast<1>(act);
+        const float gv = quad_bcast<2>(act);
+        const float og = quad_bcast<3>(act);
+        if (gg == 0) finish(lb, jj, ig, fg, gv, og);
       }
     }
     if (CNT) arrive(counter(l, t & 1, tb));
@@ -387,6 +433,9 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   if (tl.mfma) tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16
   tl.nut = (int)((H + tl.u - 1) / tl.u);
   if (tl.nbt > kMaxSlices) return false;
+  // the x-code prefetch holds 4 words of 8 codes per thread
+  if (tl.ldH > 512 || (size_t)(tl.mfma ? bB : 0) * (tl.ldXmax / 8) > 4 * (size_t)kStackThreads)
+    return false;
   tl.gl = tl.nbt * tl.nut;
   tl.grid = a.nl * tl.gl;
   if (tl.grid > cus) return false;
@@ -472,7 +521,7 @@ hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported) {
     *unsupported = true;
     return hipSuccess;
   }
-  StackKernel kern = tl.mfma ? k_stack<8, true> : k_stack<8, false>;
+  StackKernel kern = tl.bB == 1 ? k_stack<8, false, 1> : k_stack<8, true, 2>;
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)tl.lds_bytes);
   if (e != hipSuccess) return e;
