@@ -33,8 +33,8 @@ namespace ql {
 
 constexpr int kStackThreads = 512;
 
-// Per-layer counters: [layer][parity][slice], 64 bytes apart.
-constexpr size_t kStackCounterBytes = (size_t)2 * kMaxSlices * 64;
+// Per-layer arrival counters: [kind: h values, codes][parity][slice], 64 bytes apart.
+constexpr size_t kStackCounterBytes = (size_t)2 * 2 * kMaxSlices * 64;
 
 struct StackTiling {
   int bB, u, nbt, nut, gl;  // tile shape and counts; gl workgroups per layer
@@ -101,8 +101,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   const int64_t IN = Ly.in;
   const int ldXl = (int)((IN + 63) / 64 * 64);
   unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
-  auto counter = [&](int layer, int64_t par, int slice) {
-    return cnt0 + ((layer * 2 + (int)par) * kMaxSlices + slice) * 16;
+  auto ctr = [&](int layer, int kind, int64_t par, int slice) {
+    return cnt0 + (((layer * 2 + kind) * 2 + (int)par) * kMaxSlices + slice) * 16;
   };
   char *xbase = static_cast<char *>(a.ws) + kHeaderBytes + (size_t)a.nl * kStackCounterBytes;
   auto xdata = [&](int layer) { return xbase + (size_t)layer * tl.layer_bytes; };
@@ -193,169 +193,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
   };
 
-  for (int64_t t = 0; t <= T; ++t) {
-    const int64_t hcur = (t & 1) * B * H;
-    // ---- 1. h_{t-1} of this batch slice, quantized per vector
-    bool ok;
-    if (t == 0) {
-      ok = quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
-                                           [&](int) -> const void * { return nullptr; });
-    } else if (CNT) {
-      const int64_t par = (t - 1) & 1;
-      if (!wait_count(counter(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod, flag)) s_abort = 1;
-      // the x codes of this step (layer l-1's h_t) are usually ready by now:
-      // wait for them here so their loads overlap the quantization below
-      if (l > 0 && t < T &&
-          !wait_count(counter(l - 1, (t + 1) & 1, tb), (unsigned)(((t + 1) >> 1) + 1) * prod, flag))
-        s_abort = 1;
-      __syncthreads();
-      if (s_abort) return;
-      if (t < T) prefetch_x(t);
-      const float *prev = xhf + par * B * H;
-      ok = quant_tile<NVA, RBA, kSrcCoherent>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag,
-                                              rph, [&](int lb) -> const void * {
-                                                return prev + (b0 + lb) * H;
-                                              });
-    } else {
-      const uint64_t *prev = xht_mine + ((t + 1) & 1) * B * H;
-      ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)t, (int)H, xh, tl.ldsX, tl.ldH,
-                                            flag, rph, [&](int lb) -> const void * {
-                                              return prev + (b0 + lb) * H;
-                                            });
-    }
-    if (!ok) s_abort = 1;
-    __syncthreads();
-    if (s_abort) return;
-
-    // ---- share of the codes of h_{t-1}: this layer's output and, inside the
-    // launch, the next layer's input (16-byte chunk c goes to tile c % nut)
-    if (t > 0) {
-      const int64_t row0 = (t - 1) * B + b0;
-      const int chunks = (int)(Ly.out.ld / 16);
-      const int mych = (chunks - tu + tl.nut - 1) / tl.nut;  // chunks tu, tu + nut, ...
-      for (int idx = tid; idx < nb * mych; idx += blockDim.x) {
-        const int lb = idx / mych, ch = tu + (idx % mych) * tl.nut;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
-        uint64_t *dst = reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16);
-        if (CNT) {
-          st_coherent64(dst, ((uint64_t)v.y << 32) | v.x);
-          st_coherent64(dst + 1, ((uint64_t)v.w << 32) | v.z);
-        } else {
-          dst[0] = ((uint64_t)v.y << 32) | v.x;
-          dst[1] = ((uint64_t)v.w << 32) | v.z;
-        }
-      }
-      if (tu == 0)
-        for (int lb = tid; lb < nb; lb += blockDim.x) {
-          const int64_t row = row0 + lb;
-          if (CNT) {
-            st_coherent_i(&Ly.out.zero[row], rph[lb].z);
-            st_coherent(&Ly.out.inv_q[row], rph[lb].iqx);
-            st_coherent_i(&Ly.out.sums[row], rph[lb].sum);
-          } else {
-            Ly.out.zero[row] = rph[lb].z;
-            Ly.out.inv_q[row] = rph[lb].iqx;
-            Ly.out.sums[row] = rph[lb].sum;
-          }
-          if (Ly.tap_zero) Ly.tap_zero[row] = rph[lb].z;
-          if (Ly.tap_inv_q) Ly.tap_inv_q[row] = rph[lb].iqx;
-        }
-      if (Ly.tap_codes && tu == 0)
-        for (int idx = tid; idx < nb * (int)H; idx += blockDim.x) {
-          const int lb = idx / (int)H, k = idx % (int)H;
-          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
-        }
-      if (!CNT && l + 1 < a.nl) {
-        // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
-        uint64_t *ct = ctag(l);
-        const int mywd = (tl.nw - tu + tl.nut - 1) / tl.nut;  // words tu, tu + nut, ...
-        for (int idx = tid; idx < nb * mywd; idx += blockDim.x) {
-          const int lb = idx / mywd, wd = tu + (idx % mywd) * tl.nut;
-          uint32_t pay;
-          if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
-          else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
-          else if (wd == tl.ldH / 4 + 1) pay = __float_as_uint(rph[lb].iqx);
-          else pay = (uint32_t)rph[lb].sum;
-          __hip_atomic_store(ct + (row0 + lb) * tl.nw + wd, ((uint64_t)t << 32) | pay,
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-    }
-    if (t == T) {
-      if (CNT) arrive(counter(l, T & 1, tb));  // certifies the codes of h_{T-1}
-      break;
-    }
-
-    // ---- 2. codes of x_t
-    const int64_t xrow0 = t * B + b0;
-    if (l == 0 && !CNT) {
-      const int chunks = ldXl / 16;
-      for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
-        const int lb = idx / chunks, ch = idx % chunks;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (lb < nb) v = *reinterpret_cast<const uint4 *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld + ch * 16);
-        *reinterpret_cast<uint4 *>(xx + lb * tl.ldsXx + ch * 16) = v;
-      }
-      for (int lb = tid; lb < rowsA; lb += blockDim.x)
-        rpx[lb] = lb < nb ? row_param(Ly.xin.zero[xrow0 + lb], Ly.xin.inv_q[xrow0 + lb],
-                                      Ly.xin.sums[xrow0 + lb], (int)IN)
-                          : row_param(0, 0.0f, 0, (int)IN);
-    } else if (CNT) {
-      // layer l-1's arrivals after its step t+1 certify the codes of its h_t
-      // (the first layer reads finished input); at t > 0 they were awaited
-      // and loaded together with h_{t-1} above
-      if (t == 0) {
-        if (l > 0 && !wait_count(counter(l - 1, 1, tb), prod, flag)) s_abort = 1;
-        __syncthreads();
-        if (s_abort) return;
-        prefetch_x(0);
-      }
-#pragma unroll
-      for (int i = 0; i < kXPre; ++i) {
-        const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
-        if (idx < rowsA * xwords) *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = xpre[i];
-      }
-      if (tid < rowsA)
-        rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
-    } else {
-      // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
-      const uint64_t *ct = ctag(l - 1);
-      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
-      long it = 0;
-      for (;;) {
-        uint32_t bad = 0;
-        for (int idx = tid; idx < nb * nwx; idx += blockDim.x) {
-          const int lb = idx / nwx, wd = idx % nwx;
-          const uint64_t wv = ld_tagged(ct + (xrow0 + lb) * nwx + wd);
-          bad |= (uint32_t)(wv >> 32) ^ (uint32_t)(t + 1);
-          const uint32_t pay = (uint32_t)wv;
-          if (wd < ldXl / 4) *reinterpret_cast<uint32_t *>(xx + lb * tl.ldsXx + 4 * wd) = pay;
-          else if (wd == ldXl / 4) rpx[lb].z = (int32_t)pay;
-          else if (wd == ldXl / 4 + 1) rpx[lb].iqx = __uint_as_float(pay);
-          else rpx[lb].sum = (int32_t)pay;
-        }
-        if (!__syncthreads_or(bad != 0)) break;
-        if (tid == 0 && wait_expired(flag, it)) s_abort = 1;
-        __syncthreads();
-        if (s_abort) return;
-      }
-      for (int lb = tid; lb < nb; lb += blockDim.x)
-        rpx[lb] = row_param(rpx[lb].z, rpx[lb].iqx, rpx[lb].sum, (int)IN);
-    }
-    __syncthreads();
-
-    // ---- 3. both products against the resident slices
-    if (MFA) {
-      products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
-      products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
-    } else {
-      products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
-      products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
-    }
-    __syncthreads();
-
-    // ---- 4. recover, gates, cell; publish h_t
+  // Recover both products, gates, cell update; publish h_t (step t).
+  auto gates = [&](int64_t t, int64_t hcur) {
     const int pairs = nb * nu;
     auto preact = [&](int lb, int n) {
       const RowParam rx = rpx[lb], rh = rph[lb];
@@ -403,7 +242,236 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         if (gg == 0) finish(lb, jj, ig, fg, gv, og);
       }
     }
-    if (CNT) arrive(counter(l, t & 1, tb));
+  };
+
+  if constexpr (CNT) {
+    // Batched tiles.  The codes of h_{t-1} are made once per slice: Qn
+    // designated tiles (tu < Qn) each quantize 8 of its rows (one per wave),
+    // store them with device-coherent stores and arrive on the slice's codes
+    // counter; every tile then loads all rows' codes, as it loads x_t.
+    const int Qn = tl.bB / 8;
+    const bool quantizer = tu < Qn;
+    const int q0 = tu * 8;
+    const int nq = quantizer ? (nb - q0 < 0 ? 0 : (nb - q0 < 8 ? nb - q0 : 8)) : 0;
+    const int hwords = tl.ldH / 8;
+    uint64_t hpre[kXPre];
+    for (int64_t t = 0; t <= T; ++t) {
+      const int64_t hcur = (t & 1) * B * H;
+      const int64_t par = (t - 1) & 1;
+      // ---- 1. designated tiles: codes of h_{t-1} for 8 rows of the slice
+      if (t > 0 && quantizer) {
+        if (!wait_count(ctr(l, 0, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod, flag)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+        const float *prev = xhf + par * B * H;
+        bool ok = true;
+        if (nq > 0)
+          ok = quant_tile<NVA, 1, kSrcCoherent>(nq, nq, H, 0u, (int)H, xh + q0 * tl.ldsX, tl.ldsX,
+                                                tl.ldH, flag, rph + q0, [&](int lb) -> const void * {
+                                                  return prev + (b0 + q0 + lb) * H;
+                                                });
+        if (!ok) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+        const int64_t row0 = (t - 1) * B + b0 + q0;
+        const int owords = (int)(Ly.out.ld / 8);
+        for (int idx = tid; idx < nq * owords; idx += blockDim.x) {
+          const int lb = idx / owords, wd = idx % owords;
+          uint64_t v = 0;
+          if (wd < hwords) v = *reinterpret_cast<const uint64_t *>(xh + (q0 + lb) * tl.ldsX + wd * 8);
+          st_coherent64(reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld) + wd, v);
+        }
+        for (int lb = tid; lb < nq; lb += blockDim.x) {
+          const RowParam r = rph[q0 + lb];
+          st_coherent_i(&Ly.out.zero[row0 + lb], r.z);
+          st_coherent(&Ly.out.inv_q[row0 + lb], r.iqx);
+          st_coherent_i(&Ly.out.sums[row0 + lb], r.sum);
+          if (Ly.tap_zero) Ly.tap_zero[row0 + lb] = r.z;
+          if (Ly.tap_inv_q) Ly.tap_inv_q[row0 + lb] = r.iqx;
+        }
+        if (Ly.tap_codes)
+          for (int idx = tid; idx < nq * (int)H; idx += blockDim.x) {
+            const int lb = idx / (int)H, k = idx % (int)H;
+            Ly.tap_codes[(row0 + lb) * H + k] = xh[(q0 + lb) * tl.ldsX + k];
+          }
+        arrive(ctr(l, 1, par, tb));
+      }
+      if (t == T) break;
+
+      // ---- 2. every tile: codes of h_{t-1} and of x_t, both loads in flight together
+      if (t > 0 && !wait_count(ctr(l, 1, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
+        s_abort = 1;
+      if (l > 0 && !wait_count(ctr(l - 1, 1, t & 1, tb), (unsigned)((t >> 1) + 1) * Qn, flag))
+        s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      const int64_t hrow0 = (t - 1) * B + b0;
+      int32_t hz = 0, hs = 0;
+      float hq = 0.0f;
+      if (t > 0) {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i) {
+          const int idx = tid + i * kStackThreads, lb = idx / hwords, wd = idx % hwords;
+          uint64_t v = 0;
+          if (lb < nb && idx < rowsA * hwords)
+            v = ld_coherent64(reinterpret_cast<const uint64_t *>(Ly.out.codes + (hrow0 + lb) * Ly.out.ld) + wd);
+          hpre[i] = v;
+        }
+        if (tid < nb) {
+          hz = ld_coherent_i(&Ly.out.zero[hrow0 + tid]);
+          hq = ld_coherent(&Ly.out.inv_q[hrow0 + tid]);
+          hs = ld_coherent_i(&Ly.out.sums[hrow0 + tid]);
+        }
+      }
+      prefetch_x(t);
+      if (t == 0) {
+        // h_{-1} = 0: every tile quantizes the zero rows itself
+        quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
+                                        [&](int) -> const void * { return nullptr; });
+      } else {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i) {
+          const int idx = tid + i * kStackThreads, lb = idx / hwords, wd = idx % hwords;
+          if (idx < rowsA * hwords) *reinterpret_cast<uint64_t *>(xh + lb * tl.ldsX + wd * 8) = hpre[i];
+        }
+        if (tid < rowsA)
+          rph[tid] = tid < nb ? row_param(hz, hq, hs, (int)H) : row_param(0, 0.0f, 0, (int)H);
+      }
+#pragma unroll
+      for (int i = 0; i < kXPre; ++i) {
+        const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
+        if (idx < rowsA * xwords) *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = xpre[i];
+      }
+      if (tid < rowsA)
+        rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
+      __syncthreads();
+
+      // ---- 3. both products against the resident slices
+      products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+      products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+      __syncthreads();
+
+      // ---- 4. recover, gates, cell; publish h_t
+      gates(t, hcur);
+      arrive(ctr(l, 0, t & 1, tb));
+      __syncthreads();  // LDS of this step is free before the next step
+    }
+    return;
+  }
+
+  // One batch row per tile: every tile quantizes its row of h_{t-1} from the
+  // tagged words of its own layer, and takes x_t from the input (first layer)
+  // or from layer l-1's tagged code words.
+  for (int64_t t = 0; t <= T; ++t) {
+    const int64_t hcur = (t & 1) * B * H;
+    // ---- 1. h_{t-1} of this batch slice, quantized per vector
+    bool ok;
+    if (t == 0) {
+      ok = quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
+                                           [&](int) -> const void * { return nullptr; });
+    } else {
+      const uint64_t *prev = xht_mine + ((t + 1) & 1) * B * H;
+      ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)t, (int)H, xh, tl.ldsX, tl.ldH,
+                                            flag, rph, [&](int lb) -> const void * {
+                                              return prev + (b0 + lb) * H;
+                                            });
+    }
+    if (!ok) s_abort = 1;
+    __syncthreads();
+    if (s_abort) return;
+
+    // ---- share of the codes of h_{t-1}: this layer's output and, inside the
+    // launch, the next layer's input (16-byte chunk c goes to tile c % nut)
+    if (t > 0) {
+      const int64_t row0 = (t - 1) * B + b0;
+      const int chunks = (int)(Ly.out.ld / 16);
+      const int mych = (chunks - tu + tl.nut - 1) / tl.nut;  // chunks tu, tu + nut, ...
+      for (int idx = tid; idx < nb * mych; idx += blockDim.x) {
+        const int lb = idx / mych, ch = tu + (idx % mych) * tl.nut;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
+        *reinterpret_cast<uint4 *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16) = v;
+      }
+      if (tu == 0)
+        for (int lb = tid; lb < nb; lb += blockDim.x) {
+          const int64_t row = row0 + lb;
+          Ly.out.zero[row] = rph[lb].z;
+          Ly.out.inv_q[row] = rph[lb].iqx;
+          Ly.out.sums[row] = rph[lb].sum;
+          if (Ly.tap_zero) Ly.tap_zero[row] = rph[lb].z;
+          if (Ly.tap_inv_q) Ly.tap_inv_q[row] = rph[lb].iqx;
+        }
+      if (Ly.tap_codes && tu == 0)
+        for (int idx = tid; idx < nb * (int)H; idx += blockDim.x) {
+          const int lb = idx / (int)H, k = idx % (int)H;
+          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
+        }
+      if (l + 1 < a.nl) {
+        // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
+        uint64_t *ct = ctag(l);
+        const int mywd = (tl.nw - tu + tl.nut - 1) / tl.nut;  // words tu, tu + nut, ...
+        for (int idx = tid; idx < nb * mywd; idx += blockDim.x) {
+          const int lb = idx / mywd, wd = tu + (idx % mywd) * tl.nut;
+          uint32_t pay;
+          if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
+          else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
+          else if (wd == tl.ldH / 4 + 1) pay = __float_as_uint(rph[lb].iqx);
+          else pay = (uint32_t)rph[lb].sum;
+          __hip_atomic_store(ct + (row0 + lb) * tl.nw + wd, ((uint64_t)t << 32) | pay,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+    if (t == T) break;
+
+    // ---- 2. codes of x_t
+    const int64_t xrow0 = t * B + b0;
+    if (l == 0) {
+      const int chunks = ldXl / 16;
+      for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
+        const int lb = idx / chunks, ch = idx % chunks;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (lb < nb) v = *reinterpret_cast<const uint4 *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld + ch * 16);
+        *reinterpret_cast<uint4 *>(xx + lb * tl.ldsXx + ch * 16) = v;
+      }
+      for (int lb = tid; lb < rowsA; lb += blockDim.x)
+        rpx[lb] = lb < nb ? row_param(Ly.xin.zero[xrow0 + lb], Ly.xin.inv_q[xrow0 + lb],
+                                      Ly.xin.sums[xrow0 + lb], (int)IN)
+                          : row_param(0, 0.0f, 0, (int)IN);
+    } else {
+      // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
+      const uint64_t *ct = ctag(l - 1);
+      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
+      long it = 0;
+      for (;;) {
+        uint32_t bad = 0;
+        for (int idx = tid; idx < nb * nwx; idx += blockDim.x) {
+          const int lb = idx / nwx, wd = idx % nwx;
+          const uint64_t wv = ld_tagged(ct + (xrow0 + lb) * nwx + wd);
+          bad |= (uint32_t)(wv >> 32) ^ (uint32_t)(t + 1);
+          const uint32_t pay = (uint32_t)wv;
+          if (wd < ldXl / 4) *reinterpret_cast<uint32_t *>(xx + lb * tl.ldsXx + 4 * wd) = pay;
+          else if (wd == ldXl / 4) rpx[lb].z = (int32_t)pay;
+          else if (wd == ldXl / 4 + 1) rpx[lb].iqx = __uint_as_float(pay);
+          else rpx[lb].sum = (int32_t)pay;
+        }
+        if (!__syncthreads_or(bad != 0)) break;
+        if (tid == 0 && wait_expired(flag, it)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return;
+      }
+      for (int lb = tid; lb < nb; lb += blockDim.x)
+        rpx[lb] = row_param(rpx[lb].z, rpx[lb].iqx, rpx[lb].sum, (int)IN);
+    }
+    __syncthreads();
+
+    // ---- 3. both products against the resident slices
+    products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+    products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+    __syncthreads();
+
+    // ---- 4. recover, gates, cell; publish h_t
+    gates(t, hcur);
     __syncthreads();  // LDS of this step is free before the next step's quantization
   }
 }
@@ -433,6 +501,7 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   if (tl.mfma) tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16
   tl.nut = (int)((H + tl.u - 1) / tl.u);
   if (tl.nbt > kMaxSlices) return false;
+  if (tl.mfma && tl.nut < tl.bB / 8) return false;  // bB / 8 tiles quantize 8 rows each
   // the x-code prefetch holds 4 words of 8 codes per thread
   if (tl.ldH > 512 || (size_t)(tl.mfma ? bB : 0) * (tl.ldXmax / 8) > 4 * (size_t)kStackThreads)
     return false;
