@@ -35,6 +35,7 @@ struct EpiArgs {
   float *logits;
   float2 *stats;  // [M][ntn] (max, sum exp) per column tile
   int ntn;
+  const float2 *rowstat;  // [M] (max, 1 / sum exp) per row
 };
 
 template <int BM, int BN, int BK, int WM, int WN>
@@ -146,6 +147,13 @@ __device__ __forceinline__ void gemm_tile(const int8_t *__restrict__ A, int64_t 
 // the row, so a fragment's swizzle follows from lane & 31 alone.
 typedef __attribute__((address_space(3))) void lds_void;
 
+// One 16-byte direct global->LDS load (each lane's 16 bytes land at
+// consecutive 16-byte slots from the wave's LDS base).  A plain function so
+// that every kernel instantiation shares one declaration of the builtin call.
+__device__ __forceinline__ void load_lds16(const int8_t *g, char *l) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)l, 16, 0, 0);
+}
+
 template <int ROW>
 __device__ __forceinline__ int swz(int r) {
   if constexpr (ROW == 64) return ((r >> 1) ^ (r >> 2)) & 3;
@@ -220,11 +228,9 @@ __device__ __forceinline__ void gemm_tile_dma(
     const int64_t ko = (int64_t)(ks < nk ? ks : nk - 1) * ROW;
     char *st = smem + (ks % NS) * C::STAGE + wave * 1024;
     if (i < C::LA)
-      __builtin_amdgcn_global_load_lds(ga[i] + ko, (lds_void *)(st + i * C::NT * 16), 16, 0, 0);
+      load_lds16(ga[i] + ko, st + i * C::NT * 16);
     else
-      __builtin_amdgcn_global_load_lds(gb[i - C::LA] + ko,
-                                       (lds_void *)(st + BM * ROW + (i - C::LA) * C::NT * 16),
-                                       16, 0, 0);
+      load_lds16(gb[i - C::LA] + ko, st + BM * ROW + (i - C::LA) * C::NT * 16);
   };
   if (nk == 0) return;
 
@@ -374,6 +380,197 @@ __device__ __forceinline__ void raw_epilogue_lds(const EpiArgs &e, int64_t M, in
   }
 }
 
+// Calls f(integral_constant<int, I>) for I in [B, E).
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// 16 independent reductions (max or sum) over each 32-lane half of a wave:
+// rotations within 16-lane rows, then the exchange of the two rows.
+template <bool MAX>
+__device__ __forceinline__ void half_wave_reduce16(float (&v)[16]) {
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : a + b; };
+  auto ror = [](float x, auto ctrl) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value,
+                                                      0xf, 0xf, false));
+  };
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x128>{}));
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x124>{}));
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x122>{}));
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x121>{}));
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = op(v[k], __shfl_xor(v[k], 16, 64));
+}
+
+// Recovering epilogues (eq. 1 recovery plus bias; softmax statistics or
+// output) through LDS: each wave parks 32 rows of raw signed sums at a time in
+// its own slab (as above), then walks them row-major with every lane owning
+// the same 4 consecutive columns of each row, so the per-column terms stay in
+// registers and every store is a 16-byte write.  The tile's per-row terms are
+// staged once.  Softmax statistics are reduced per wave over its 128 columns
+// (max, then sum of exp(y - max)) and the WN partials of a row are merged
+// with the usual rescaling.
+template <class C, int EPI>
+__device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M, int64_t N,
+                                                     int64_t K, int64_t m0, int64_t n0, int tn,
+                                                     int wm, int wn, int lane, char *smem,
+                                                     const float *rowmax, const float *rowinv,
+                                                     v16i (&acc)[C::FM][C::FN]) {
+  constexpr int BM = C::TBM, TM = C::TM, TN = C::TN, RS = TN + 8, WN = C::TBN / C::TN;
+  constexpr int kSlab = 8192;
+  static_assert(TN == 128, "a half-wave covers one row: 32 lanes x 4 columns");
+  static_assert(3 * BM * 4 + WN * BM * 8 <= kSlab, "row terms and partials");
+  static_assert(kSlab + (C::NT / 64) * 32 * RS * 4 <= C::LDS, "LDS slabs");
+  int32_t *rsig = reinterpret_cast<int32_t *>(smem);  // [BM] sigma_x
+  int32_t *rzt = rsig + BM;                            // [BM] z~x
+  float *riq = reinterpret_cast<float *>(rzt + BM);    // [BM] 1/Qx
+  float2 *red = reinterpret_cast<float2 *>(smem + 3 * BM * 4);  // [WN][BM] (max, sum)
+  const int wave = threadIdx.x >> 6;
+  uint32_t *slab = reinterpret_cast<uint32_t *>(smem + kSlab) + wave * 32 * RS;
+  for (int r = threadIdx.x; r < BM; r += C::NT) {
+    int64_t m = m0 + r;
+    m = m < M ? m : M - 1;
+    rsig[r] = e.x_sums[m] - 128 * (int32_t)K;
+    rzt[r] = e.x_zero[m] + 128;
+    riq[r] = e.x_inv_q[m];
+  }
+  // this lane's columns: n0 + wn*TN + 4*(lane & 31) + t
+  const int64_t nc = n0 + wn * TN + 4 * (lane & 31);
+  int32_t ztw[4], sigw[4];
+  int64_t colterm[4];
+  float iqw[4], bn[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int64_t nn = nc + t < N ? nc + t : N - 1;
+    const int64_t blk = nn / e.w_rpb;
+    ztw[t] = e.w_zero[blk] + 128;
+    sigw[t] = e.w_sums[nn] - 128 * (int32_t)K;
+    colterm[t] = (int64_t)sigw[t] + K * (int64_t)ztw[t];
+    iqw[t] = e.w_inv_q[blk];
+    bn[t] = e.bias ? e.bias[nn] : 0.0f;
+  }
+  __syncthreads();
+  const bool vec = (N & 3) == 0 && nc + 3 < N;
+  // chunks expanded at compile time: acc is only ever indexed by constants
+  static_for<0, C::FM>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = frag_row(r, lane);
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) slab[row * RS + j * 32 + (lane & 31)] = (uint32_t)acc[i][j][r];
+    }
+    // the slab is this wave's own: LDS keeps one wave's accesses in order
+    // row `it` of this half-wave: recover, store, and hand back y
+    auto row_step = [&](int it, float (&y)[4]) {
+      const int row = 2 * it + (lane >> 5), lr = wm * TM + i * 32 + row;
+      const int64_t m = m0 + lr;
+      const v4i v = *reinterpret_cast<const v4i *>(slab + row * RS + 4 * (lane & 31));
+      const int32_t sigx = rsig[lr], ztx = rzt[lr];
+      const float iqx = riq[lr];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) y[t] = recover(v[t], colterm[t], ztw[t], ztx, sigx, iqw[t], iqx) + bn[t];
+      const int64_t off = m * N + nc;
+      if (EPI == EPI_RECOVER || EPI == EPI_SMAX_OUT) {
+        if (EPI == EPI_SMAX_OUT) {
+          const float mx = rowmax[lr], inv = rowinv[lr];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) y[t] = __expf(y[t] - mx) * inv;
+        }
+        if (m < M) {
+          if (vec) {
+            *reinterpret_cast<float4 *>(e.Y + off) = make_float4(y[0], y[1], y[2], y[3]);
+          } else {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              if (nc + t < N) e.Y[off + t] = y[t];
+          }
+        }
+      } else if (m < M && e.logits) {  // EPI_SMAX_STATS
+        if (vec) {
+          *reinterpret_cast<float4 *>(e.logits + off) = make_float4(y[0], y[1], y[2], y[3]);
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            if (nc + t < N) e.logits[off + t] = y[t];
+        }
+      }
+      if (EPI != EPI_SMAX_OUT && m < M && e.acc) {
+        int32_t a[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) a[t] = acc_u8(v[t], sigw[t], sigx, K);
+        if (vec) {
+          *reinterpret_cast<v4i *>(e.acc + off) = v4i{a[0], a[1], a[2], a[3]};
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            if (nc + t < N) e.acc[off + t] = a[t];
+        }
+      }
+    };
+    if constexpr (EPI != EPI_SMAX_STATS) {
+#pragma unroll 2
+      for (int it = 0; it < 16; ++it) {
+        float y[4];
+        row_step(it, y);
+      }
+    } else {
+      float ys[16][4];
+#pragma unroll
+      for (int it = 0; it < 16; ++it) row_step(it, ys[it]);
+      // per row (one per half-wave and iteration): max over the 128 columns,
+      // then sum exp(y - max); 16 rows reduced together so the steps overlap
+      float mx[16], sm[16];
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        mx[it] = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (nc + t < N) mx[it] = fmaxf(mx[it], ys[it][t]);
+      }
+      half_wave_reduce16<true>(mx);
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        sm[it] = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (nc + t < N) sm[it] += __expf(ys[it][t] - mx[it]);
+      }
+      half_wave_reduce16<false>(sm);
+      if ((lane & 31) == 0) {
+#pragma unroll
+        for (int it = 0; it < 16; ++it)
+          red[wn * BM + wm * TM + i * 32 + 2 * it + (lane >> 5)] = make_float2(mx[it], sm[it]);
+      }
+    }
+  });
+  if constexpr (EPI == EPI_SMAX_STATS) {
+    __syncthreads();
+    for (int r = threadIdx.x; r < BM; r += C::NT) {
+      const int64_t m = m0 + r;
+      if (m >= M) continue;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) mx = fmaxf(mx, red[w * BM + r].x);
+      float sm = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) {
+        const float2 p = red[w * BM + r];
+        if (p.y > 0.0f) sm += p.y * __expf(p.x - mx);
+      }
+      e.stats[m * e.ntn + tn] = make_float2(mx, sm);
+    }
+  }
+}
+
 // NS = 0: register-staged two-stage tile; NS >= 2: direct-load pipeline of
 // NS stages with BK-byte rows.
 template <int BM, int BN, int BK, int WM, int WN, int NS>
@@ -399,16 +596,9 @@ __global__ __launch_bounds__(64 * WM *WN) void k_gemm(const int8_t *__restrict__
   if (EPI == EPI_SMAX_OUT) {
     for (int r = threadIdx.x; r < BM; r += C::NT) {
       const int64_t m = m0 + r;
-      float mx = -INFINITY, sm = 0.0f;
-      if (m < M) {
-        for (int t = 0; t < e.ntn; ++t) mx = fmaxf(mx, e.stats[m * e.ntn + t].x);
-        for (int t = 0; t < e.ntn; ++t) {
-          const float2 st = e.stats[m * e.ntn + t];
-          sm += st.y * __expf(st.x - mx);
-        }
-      }
-      rowmax[r] = mx;
-      rowinv[r] = 1.0f / sm;
+      const float2 st = e.rowstat[m < M ? m : M - 1];
+      rowmax[r] = st.x;
+      rowinv[r] = st.y;
     }
   }
 
@@ -418,8 +608,11 @@ __global__ __launch_bounds__(64 * WM *WN) void k_gemm(const int8_t *__restrict__
   else
     gemm_tile<BM, BN, BK, WM, WN>(A, lda, B, ldb, M, N, Kp, m0, n0, smem, acc);
 
-  if constexpr (NS >= 2 && EPI == EPI_RAW) {
-    raw_epilogue_lds<C>(e, M, N, K, m0, n0, wm, wn, lane, smem, acc);
+  if constexpr (NS >= 2) {
+    if constexpr (EPI == EPI_RAW)
+      raw_epilogue_lds<C>(e, M, N, K, m0, n0, wm, wn, lane, smem, acc);
+    else
+      recover_epilogue_lds<C, EPI>(e, M, N, K, m0, n0, tn, wm, wn, lane, smem, rowmax, rowinv, acc);
     return;
   }
 
@@ -573,6 +766,12 @@ static hipError_t run(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb
 
 // Kp must stay within the padded leading dimensions: with ld a multiple of 64
 // and BK = 64 this always holds; BK = 128 is used when both ld allow it.
+// Column width of the tiles a product of M x N uses: 256 once there are
+// enough 256x256 tiles to fill the chip, else 128.
+static int big_tile_n(int64_t M, int64_t N) {
+  return ((M + 255) / 256) * ((N + 255) / 256) >= 256 ? 256 : 128;
+}
+
 template <int EPI>
 static hipError_t dispatch(const int8_t *A, int64_t lda, const int8_t *B, int64_t ldb, int64_t M,
                            int64_t N, int64_t K, const EpiArgs &e, hipStream_t s) {
@@ -580,12 +779,9 @@ static hipError_t dispatch(const int8_t *A, int64_t lda, const int8_t *B, int64_
   const bool k128 = round_up(K, 128) <= lda && round_up(K, 128) <= ldb;
   // 256x256 tiles (128x128 per wave) once there are enough of them to fill
   // the chip; otherwise 128x128 tiles (64x64 per wave)
-  const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-  if constexpr (EPI == EPI_RAW) {
-    if (big_tiles >= 256) {
-      if (k128) return run<256, 256, 128, 2, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
-      return run<256, 256, 64, 2, 2, 4, EPI>(A, lda, B, ldb, M, N, K, e, s);
-    }
+  if (big_tile_n(M, N) == 256) {
+    if (k128) return run<256, 256, 128, 2, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
+    return run<256, 256, 64, 2, 2, 4, EPI>(A, lda, B, ldb, M, N, K, e, s);
   }
   if (k128) return run<128, 128, 128, 2, 2, 0, EPI>(A, lda, B, ldb, M, N, K, e, s);
   return run<128, 128, 64, 2, 2, 0, EPI>(A, lda, B, ldb, M, N, K, e, s);
@@ -623,8 +819,30 @@ hipError_t launch_gemm_raw(const int8_t *A, int64_t lda, const int8_t *B, int64_
   return dispatch<EPI_RAW>(A, lda, B, ldb, M, N, K, e, s);
 }
 
-size_t softmax_ws(int64_t M, int64_t N) {
+// Per-tile statistics [M][ntn] (ntn of 128-column tiles is the most any
+// launch uses), then the per-row (max, 1 / sum) [M].
+static size_t smax_stats_bytes(int64_t M, int64_t N) {
   return align_up((size_t)M * (size_t)((N + 127) / 128) * sizeof(float2), 256);
+}
+size_t softmax_ws(int64_t M, int64_t N) {
+  return smax_stats_bytes(M, N) + align_up((size_t)M * sizeof(float2), 256);
+}
+
+// Softmax normaliser of each row from its column tiles' (max, sum exp):
+// max over the tiles, sum of sum_t exp(max_t - max), stored as (max, 1/sum).
+__global__ __launch_bounds__(256) void k_smax_combine(const float2 *__restrict__ stats, int ntn,
+                                                      int64_t M, float2 *__restrict__ rowstat) {
+  const int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (m >= M) return;
+  const float2 *s = stats + m * ntn;
+  float mx = -INFINITY;
+  for (int t = 0; t < ntn; ++t) mx = fmaxf(mx, s[t].x);
+  float sm = 0.0f;
+  for (int t = 0; t < ntn; ++t) {
+    const float2 st = s[t];
+    sm += st.y * __expf(st.x - mx);
+  }
+  rowstat[m] = make_float2(mx, 1.0f / sm);
 }
 
 hipError_t launch_softmax_layer(const ActRows &X, const WeightMat &W, int64_t M, int64_t N,
@@ -632,11 +850,18 @@ hipError_t launch_softmax_layer(const ActRows &X, const WeightMat &W, int64_t M,
                                 float *logits, void *ws, hipStream_t s) {
   EpiArgs e = make_epi(X, W, bias);
   e.stats = static_cast<float2 *>(ws);
-  e.ntn = (int)((N + 127) / 128);
+  const int tn = big_tile_n(M, N);
+  e.ntn = (int)((N + tn - 1) / tn);
   e.acc = acc;
   e.logits = logits;
   hipError_t err = dispatch<EPI_SMAX_STATS>(X.codes, X.ld, W.codes, W.ld, M, N, K, e, s);
+  if (err != hipSuccess || M == 0) return err;
+  float2 *rowstat = reinterpret_cast<float2 *>(static_cast<char *>(ws) + smax_stats_bytes(M, N));
+  hipLaunchKernelGGL(k_smax_combine, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s,
+                     e.stats, e.ntn, M, rowstat);
+  err = hipGetLastError();
   if (err != hipSuccess) return err;
+  e.rowstat = rowstat;
   e.acc = nullptr;
   e.logits = nullptr;
   e.Y = post;

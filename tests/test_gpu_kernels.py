@@ -99,6 +99,26 @@ def test_qmatmul_ragged_shapes(ql, orc, m, rows, cols, nblocks, gran):
     assert np.array_equal(Y.view(np.uint32), o["Y"].view(np.uint32))
 
 
+@pytest.mark.parametrize("m,rows,cols", [(2100, 8200, 333), (4096, 4100, 64)])
+def test_qmatmul_large_tiles_sampled_rows(ql, orc, m, rows, cols):
+    """Products large enough for the 256x256 tiles (K of 333 and of 64 take
+    the two pipeline depths), ragged in rows and columns: sampled rows of the
+    recovered output and of the accumulators against the oracle (per-row
+    activation quantization keeps rows independent)."""
+    rng = np.random.default_rng(m + rows + cols)
+    W = rng.normal(0, 0.05, (rows, cols)).astype(np.float32)
+    X = rng.standard_normal((m, cols)).astype(np.float32)
+    bias = rng.normal(0, 0.1, rows).astype(np.float32)
+    q = ql.quantize(torch.from_numpy(W).cuda(), 4)
+    Y, acc = ql.quantized_matmul(q, torch.from_numpy(X).cuda(), 1, torch.from_numpy(bias).cuda(),
+                                 want_acc=True)
+    sel = np.unique(np.concatenate([[0, 1, 255, 256, m - 257, m - 1], rng.choice(m, 24, replace=False)]))
+    o = orc.quantized_matmul(orc.quantize(W, 4), X[sel], act_gran=1, bias=bias)
+    idx = torch.from_numpy(sel).cuda()
+    assert np.array_equal(acc[idx].cpu().numpy(), o["acc"])
+    assert np.array_equal(Y[idx].cpu().numpy().view(np.uint32), o["Y"].view(np.uint32))
+
+
 def test_qmatmul_max_k_accumulator(ql, orc):
     """K = 33025 with nearly all codes 255: sum_k 255*255 is just below 2^31."""
     K = 33025

@@ -134,6 +134,21 @@ def test_model_small_all_taps(ql, orc):
     assert np.max(np.abs(p.sum(-1) - 1.0)) < 1e-5
 
 
+def test_model_softmax_large_tiles_ragged_states(ql, orc):
+    """2400 frames x 8200 states: enough for the 256x256 product tiles, with
+    a ragged last column tile.  Logits and accumulators bit-exact and
+    posteriors to 1e-4 on sampled utterances."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(32, 40, 1, states=8200, seed=41)
+    x = np.random.default_rng(2).standard_normal((30, 80, 32)).astype(np.float32)
+    utts = [0, 37, 79]
+    g, o = _model_case(ql, orc, w, x, utts=utts, taps=True)
+    assert np.array_equal(np_(g["acc_y"])[:, utts], o["acc_y"])
+    assert np.array_equal(np_(g["logits"])[:, utts], o["logits"])
+    p = np_(g["post"]).astype(np.float64)
+    assert np.max(np.abs(p.sum(-1) - 1.0)) < 1e-5
+
+
 def test_model_5x500_softmax8192_T500_B1(ql, orc):
     """Five 500-cell layers + 8192-way quantized softmax, T=500, batch 1."""
     from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T500_B1 as W_, model_weights, features
