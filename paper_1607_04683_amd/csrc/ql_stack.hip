@@ -13,7 +13,9 @@
 //      produced for its h_t, which are the same codes layer l-1 used itself
 //      (one vector, one quantization; no re-quantization);
 //   3. forms both 8-bit products, recovers them (eq. 1 / eq. 3), adds the
-//      bias as the hoisted path does, (W_x x + b) + W_h h, and runs the gates;
+//      bias as the hoisted path does, (W_x x + b) + W_h h, and runs the gates
+//      (the input-side product does not depend on h_{t-1}, so it is formed
+//      while h_{t-1} is still travelling between the workgroups);
 //   4. publishes h_t to its own layer and stores its share of the codes of
 //      h_{t-1} (the layer's output and the next layer's input).
 // Between layers nothing is reused: codes go to full-length [T*B] buffers,
@@ -298,10 +300,26 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       }
       if (t == T) break;
 
-      // ---- 2. every tile: codes of h_{t-1} and of x_t, both loads in flight together
-      if (t > 0 && !wait_count(ctr(l, 1, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
-        s_abort = 1;
+      // ---- 2. the input side of step t, which does not depend on h_{t-1}:
+      // codes of x_t and their product, done while the codes of h_{t-1} are
+      // still being made (a designated tile has just made its share)
       if (l > 0 && !wait_count(ctr(l - 1, 1, t & 1, tb), (unsigned)((t >> 1) + 1) * Qn, flag))
+        s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      prefetch_x(t);
+#pragma unroll
+      for (int i = 0; i < kXPre; ++i) {
+        const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
+        if (idx < rowsA * xwords) *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = xpre[i];
+      }
+      if (tid < rowsA)
+        rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
+      __syncthreads();
+      products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+
+      // ---- 3. every tile: codes of h_{t-1}
+      if (t > 0 && !wait_count(ctr(l, 1, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
         s_abort = 1;
       __syncthreads();
       if (s_abort) return;
@@ -323,7 +341,6 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
           hs = ld_coherent_i(&Ly.out.sums[hrow0 + tid]);
         }
       }
-      prefetch_x(t);
       if (t == 0) {
         // h_{-1} = 0: every tile quantizes the zero rows itself
         quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
@@ -337,21 +354,13 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         if (tid < rowsA)
           rph[tid] = tid < nb ? row_param(hz, hq, hs, (int)H) : row_param(0, 0.0f, 0, (int)H);
       }
-#pragma unroll
-      for (int i = 0; i < kXPre; ++i) {
-        const int idx = tid + i * kStackThreads, lb = idx / xwords, wd = idx % xwords;
-        if (idx < rowsA * xwords) *reinterpret_cast<uint64_t *>(xx + lb * tl.ldsXx + wd * 8) = xpre[i];
-      }
-      if (tid < rowsA)
-        rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
       __syncthreads();
 
-      // ---- 3. both products against the resident slices
+      // ---- 4. the recurrent product against the resident W_h' slice
       products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
-      products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
       __syncthreads();
 
-      // ---- 4. recover, gates, cell; publish h_t
+      // ---- 5. recover, gates, cell; publish h_t
       gates(t, hcur);
       arrive(ctr(l, 0, t & 1, tb));
       __syncthreads();  // LDS of this step is free before the next step
@@ -362,6 +371,54 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   // One batch row per tile: every tile quantizes its row of h_{t-1} from the
   // tagged words of its own layer, and takes x_t from the input (first layer)
   // or from layer l-1's tagged code words.
+  // Codes of x_t (the input, or layer l-1's tagged words) and the input-side
+  // product into Sx; false if a wait expired.
+  auto input_side = [&](int64_t t) -> bool {
+    const int64_t xrow0 = t * B + b0;
+    if (l == 0) {
+      const int chunks = ldXl / 16;
+      for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
+        const int lb = idx / chunks, ch = idx % chunks;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (lb < nb) v = *reinterpret_cast<const uint4 *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld + ch * 16);
+        *reinterpret_cast<uint4 *>(xx + lb * tl.ldsXx + ch * 16) = v;
+      }
+      for (int lb = tid; lb < rowsA; lb += blockDim.x)
+        rpx[lb] = lb < nb ? row_param(Ly.xin.zero[xrow0 + lb], Ly.xin.inv_q[xrow0 + lb],
+                                      Ly.xin.sums[xrow0 + lb], (int)IN)
+                          : row_param(0, 0.0f, 0, (int)IN);
+    } else {
+      // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
+      const uint64_t *ct = ctag(l - 1);
+      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
+      long it = 0;
+      for (;;) {
+        uint32_t bad = 0;
+        for (int idx = tid; idx < nb * nwx; idx += blockDim.x) {
+          const int lb = idx / nwx, wd = idx % nwx;
+          const uint64_t wv = ld_tagged(ct + (xrow0 + lb) * nwx + wd);
+          bad |= (uint32_t)(wv >> 32) ^ (uint32_t)(t + 1);
+          const uint32_t pay = (uint32_t)wv;
+          if (wd < ldXl / 4) *reinterpret_cast<uint32_t *>(xx + lb * tl.ldsXx + 4 * wd) = pay;
+          else if (wd == ldXl / 4) rpx[lb].z = (int32_t)pay;
+          else if (wd == ldXl / 4 + 1) rpx[lb].iqx = __uint_as_float(pay);
+          else rpx[lb].sum = (int32_t)pay;
+        }
+        if (!__syncthreads_or(bad != 0)) break;
+        if (tid == 0 && wait_expired(flag, it)) s_abort = 1;
+        __syncthreads();
+        if (s_abort) return false;
+      }
+      for (int lb = tid; lb < nb; lb += blockDim.x)
+        rpx[lb] = row_param(rpx[lb].z, rpx[lb].iqx, rpx[lb].sum, (int)IN);
+    }
+    __syncthreads();
+
+    products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+    __syncthreads();
+    return true;
+  };
+  if (T > 0 && !input_side(0)) return;
   for (int64_t t = 0; t <= T; ++t) {
     const int64_t hcur = (t & 1) * B * H;
     // ---- 1. h_{t-1} of this batch slice, quantized per vector
@@ -424,55 +481,16 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
     if (t == T) break;
 
-    // ---- 2. codes of x_t
-    const int64_t xrow0 = t * B + b0;
-    if (l == 0) {
-      const int chunks = ldXl / 16;
-      for (int idx = tid; idx < rowsA * chunks; idx += blockDim.x) {
-        const int lb = idx / chunks, ch = idx % chunks;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (lb < nb) v = *reinterpret_cast<const uint4 *>(Ly.xin.codes + (xrow0 + lb) * Ly.xin.ld + ch * 16);
-        *reinterpret_cast<uint4 *>(xx + lb * tl.ldsXx + ch * 16) = v;
-      }
-      for (int lb = tid; lb < rowsA; lb += blockDim.x)
-        rpx[lb] = lb < nb ? row_param(Ly.xin.zero[xrow0 + lb], Ly.xin.inv_q[xrow0 + lb],
-                                      Ly.xin.sums[xrow0 + lb], (int)IN)
-                          : row_param(0, 0.0f, 0, (int)IN);
-    } else {
-      // tagged words of layer l-1 for rows xrow0 .. xrow0 + nb - 1, tag t + 1
-      const uint64_t *ct = ctag(l - 1);
-      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
-      long it = 0;
-      for (;;) {
-        uint32_t bad = 0;
-        for (int idx = tid; idx < nb * nwx; idx += blockDim.x) {
-          const int lb = idx / nwx, wd = idx % nwx;
-          const uint64_t wv = ld_tagged(ct + (xrow0 + lb) * nwx + wd);
-          bad |= (uint32_t)(wv >> 32) ^ (uint32_t)(t + 1);
-          const uint32_t pay = (uint32_t)wv;
-          if (wd < ldXl / 4) *reinterpret_cast<uint32_t *>(xx + lb * tl.ldsXx + 4 * wd) = pay;
-          else if (wd == ldXl / 4) rpx[lb].z = (int32_t)pay;
-          else if (wd == ldXl / 4 + 1) rpx[lb].iqx = __uint_as_float(pay);
-          else rpx[lb].sum = (int32_t)pay;
-        }
-        if (!__syncthreads_or(bad != 0)) break;
-        if (tid == 0 && wait_expired(flag, it)) s_abort = 1;
-        __syncthreads();
-        if (s_abort) return;
-      }
-      for (int lb = tid; lb < nb; lb += blockDim.x)
-        rpx[lb] = row_param(rpx[lb].z, rpx[lb].iqx, rpx[lb].sum, (int)IN);
-    }
-    __syncthreads();
-
-    // ---- 3. both products against the resident slices
+    // ---- 3. the recurrent product (the input side's is already in Sx)
     products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
-    products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
     __syncthreads();
 
     // ---- 4. recover, gates, cell; publish h_t
     gates(t, hcur);
-    __syncthreads();  // LDS of this step is free before the next step's quantization
+    __syncthreads();  // Sx and the LDS of this step are free
+
+    // ---- 5. the input side of step t+1 while h_t travels
+    if (t + 1 < T && !input_side(t + 1)) return;
   }
 }
 
