@@ -20,10 +20,14 @@
 //      h_{t-1} (the layer's output and the next layer's input).
 // Between layers nothing is reused: codes go to full-length [T*B] buffers,
 // so a layer may run any number of steps ahead of the next one; a layer
-// never waits on a later layer.  Readiness: with 16+ batch rows per tile the
-// arrival counter a workgroup bumps after step t+1 also certifies its share
-// of the codes of h_t (stored, with device-coherent stores, before the
-// bump); with one batch row per tile the codes travel as tagged words.
+// never waits on a later layer.  Readiness: h_t always travels as tagged
+// words (step tag + value), which the workgroups that quantize it re-read
+// until every tag matches.  With 16+ batch rows per tile a few designated
+// workgroups per batch slice quantize h_t once, store the codes with
+// device-coherent stores and then bump the slice's arrival counter, which
+// every consumer of those codes waits on; with one batch row per tile every
+// workgroup quantizes its row itself and the codes for the next layer
+// travel as tagged words.
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
@@ -35,8 +39,8 @@ namespace ql {
 
 constexpr int kStackThreads = 512;
 
-// Per-layer arrival counters: [kind: h values, codes][parity][slice], 64 bytes apart.
-constexpr size_t kStackCounterBytes = (size_t)2 * 2 * kMaxSlices * 64;
+// Per-layer arrival counters of the codes of h: [parity][slice], 64 bytes apart.
+constexpr size_t kStackCounterBytes = (size_t)2 * kMaxSlices * 64;
 
 struct StackTiling {
   int bB, u, nbt, nut, gl;  // tile shape and counts; gl workgroups per layer
@@ -103,13 +107,13 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   const int64_t IN = Ly.in;
   const int ldXl = (int)((IN + 63) / 64 * 64);
   unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
-  auto ctr = [&](int layer, int kind, int64_t par, int slice) {
-    return cnt0 + (((layer * 2 + kind) * 2 + (int)par) * kMaxSlices + slice) * 16;
+  auto ctr = [&](int layer, int64_t par, int slice) {
+    return cnt0 + ((layer * 2 + (int)par) * kMaxSlices + slice) * 16;
   };
   char *xbase = static_cast<char *>(a.ws) + kHeaderBytes + (size_t)a.nl * kStackCounterBytes;
   auto xdata = [&](int layer) { return xbase + (size_t)layer * tl.layer_bytes; };
-  // own layer's h exchange: counter mode float [2][B][H]; tagged mode replicas of [2][B][H]
-  float *xhf = reinterpret_cast<float *>(xdata(l));
+  // own layer's h exchange: tagged words, replicas of [2][B][H] (one replica
+  // for batched tiles, whose h is read by the designated tiles only)
   uint64_t *xht = reinterpret_cast<uint64_t *>(xdata(l));
   const uint64_t *xht_mine = xht + (blockIdx.x % tl.reph) * tl.strideh;
   // tagged codes of every h_t of a layer: [T*B][nw] words after its h exchange
@@ -124,7 +128,6 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   const int nu = (int)(H - j0 < tl.u ? H - j0 : tl.u);
   const int nrows = 4 * tl.u;  // gate-major: row g*u + jj
   const int rowsA = MFA ? tl.bB : nb;
-  const unsigned prod = (unsigned)tl.nut;
   if (tid == 0) s_abort = 0;
 
   // ---- prologue: W_x' and W_h' slices, column params, bias, c = 0
@@ -210,11 +213,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
       cst[lb * tl.u + jj] = cn;
       const float m = og * tanh_cw(cn);
-      if (CNT)
-        st_coherent(&xhf[hcur + b * H + j], m);
-      else
-        for (int c2 = 0; c2 < tl.reph; ++c2)
-          publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+      for (int c2 = 0; c2 < tl.reph; ++c2)
+        publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
     };
     if (pairs >= (int)blockDim.x) {
@@ -248,9 +248,10 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 
   if constexpr (CNT) {
     // Batched tiles.  The codes of h_{t-1} are made once per slice: Qn
-    // designated tiles (tu < Qn) each quantize 8 of its rows (one per wave),
-    // store them with device-coherent stores and arrive on the slice's codes
-    // counter; every tile then loads all rows' codes, as it loads x_t.
+    // designated tiles (tu < Qn) each quantize 8 of its rows (one per wave,
+    // re-reading the row's tagged words until every tag matches), store them
+    // with device-coherent stores and arrive on the slice's codes counter;
+    // every tile then loads all rows' codes, as it loads x_t.
     const int Qn = tl.bB / 8;
     const bool quantizer = tu < Qn;
     const int q0 = tu * 8;
@@ -262,16 +263,14 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       const int64_t par = (t - 1) & 1;
       // ---- 1. designated tiles: codes of h_{t-1} for 8 rows of the slice
       if (t > 0 && quantizer) {
-        if (!wait_count(ctr(l, 0, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod, flag)) s_abort = 1;
-        __syncthreads();
-        if (s_abort) return;
-        const float *prev = xhf + par * B * H;
+        const uint64_t *prev = xht + par * B * H;
         bool ok = true;
         if (nq > 0)
-          ok = quant_tile<NVA, 1, kSrcCoherent>(nq, nq, H, 0u, (int)H, xh + q0 * tl.ldsX, tl.ldsX,
-                                                tl.ldH, flag, rph + q0, [&](int lb) -> const void * {
-                                                  return prev + (b0 + q0 + lb) * H;
-                                                });
+          ok = quant_tile<NVA, 1, kSrcTagged>(nq, nq, H, (uint32_t)t, (int)H, xh + q0 * tl.ldsX,
+                                              tl.ldsX, tl.ldH, flag, rph + q0,
+                                              [&](int lb) -> const void * {
+                                                return prev + (b0 + q0 + lb) * H;
+                                              });
         if (!ok) s_abort = 1;
         __syncthreads();
         if (s_abort) return;
@@ -296,14 +295,14 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
             const int lb = idx / (int)H, k = idx % (int)H;
             Ly.tap_codes[(row0 + lb) * H + k] = xh[(q0 + lb) * tl.ldsX + k];
           }
-        arrive(ctr(l, 1, par, tb));
+        arrive(ctr(l, par, tb));
       }
       if (t == T) break;
 
       // ---- 2. the input side of step t, which does not depend on h_{t-1}:
       // codes of x_t and their product, done while the codes of h_{t-1} are
       // still being made (a designated tile has just made its share)
-      if (l > 0 && !wait_count(ctr(l - 1, 1, t & 1, tb), (unsigned)((t >> 1) + 1) * Qn, flag))
+      if (l > 0 && !wait_count(ctr(l - 1, t & 1, tb), (unsigned)((t >> 1) + 1) * Qn, flag))
         s_abort = 1;
       __syncthreads();
       if (s_abort) return;
@@ -319,7 +318,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
 
       // ---- 3. every tile: codes of h_{t-1}
-      if (t > 0 && !wait_count(ctr(l, 1, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
+      if (t > 0 && !wait_count(ctr(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
         s_abort = 1;
       __syncthreads();
       if (s_abort) return;
@@ -362,7 +361,6 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 
       // ---- 5. recover, gates, cell; publish h_t
       gates(t, hcur);
-      arrive(ctr(l, 0, t & 1, tb));
       __syncthreads();  // LDS of this step is free before the next step
     }
     return;
@@ -557,8 +555,8 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
     tl.cx_bytes = (size_t)a.T * B * tl.nw * 8;
   } else {
     tl.reph = 1;
-    tl.strideh = 0;
-    tl.hx_bytes = align_up((size_t)2 * B * H * 4, 256);
+    tl.strideh = 2 * B * H;
+    tl.hx_bytes = align_up((size_t)2 * B * H * 8, 256);
     tl.cx_bytes = 0;
   }
   tl.layer_bytes = align_up(tl.hx_bytes + tl.cx_bytes, 256);
@@ -583,7 +581,7 @@ size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H) {
     const int64_t strideh = round_up(2 * B * H, 8192) + 512;
     per = align_up((size_t)4 * strideh * 8 + (size_t)T * B * (ldH / 4 + 3) * 8, 256);
   } else {
-    per = align_up(align_up((size_t)2 * B * H * 4, 256), 256);
+    per = align_up(align_up((size_t)2 * B * H * 8, 256), 256);
   }
   return kHeaderBytes + (size_t)nl * kStackCounterBytes + (size_t)nl * per;
 }
