@@ -20,14 +20,14 @@
 //      h_{t-1} (the layer's output and the next layer's input).
 // Between layers nothing is reused: codes go to full-length [T*B] buffers,
 // so a layer may run any number of steps ahead of the next one; a layer
-// never waits on a later layer.  Readiness: h_t always travels as tagged
-// words (step tag + value), which the workgroups that quantize it re-read
-// until every tag matches.  With 16+ batch rows per tile a few designated
-// workgroups per batch slice quantize h_t once, store the codes with
-// device-coherent stores and then bump the slice's arrival counter, which
-// every consumer of those codes waits on; with one batch row per tile every
-// workgroup quantizes its row itself and the codes for the next layer
-// travel as tagged words.
+// never waits on a later layer.  Readiness: h_t travels as tagged words
+// (step tag + value) that the workgroups quantizing it re-read until every
+// tag matches.  With one batch row per tile every workgroup quantizes its row
+// itself and the codes for the next layer travel as tagged words too.  With
+// 16+ batch rows a few quantizing workgroups per batch slice (they own no
+// units, so nothing else waits behind their work) quantize h_t once, store
+// the codes with device-coherent stores and then bump the slice's arrival
+// counter, which every consumer of the codes waits on.
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
@@ -44,6 +44,7 @@ constexpr size_t kStackCounterBytes = (size_t)2 * kMaxSlices * 64;
 
 struct StackTiling {
   int bB, u, nbt, nut, gl;  // tile shape and counts; gl workgroups per layer
+  int nq;                   // quantizing workgroups per batch slice (batched tiles)
   int grid, mfma;
   int ldH;                  // padded width of h codes (and W_h' rows)
   int ldXmax;               // largest padded input width over the launch
@@ -122,13 +123,66 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   };
 
   const int tid = threadIdx.x;
-  const int tb = wgi / tl.nut, tu = wgi % tl.nut;
+  // a batch slice: nut unit tiles, then (batched tiles) nq quantizing workgroups
+  const int tb = wgi / (tl.nut + tl.nq), tw = wgi % (tl.nut + tl.nq);
+  const bool quantizer = tw >= tl.nut;
+  const int tu = quantizer ? 0 : tw;
   const int64_t b0 = (int64_t)tb * tl.bB, j0 = (int64_t)tu * tl.u;
   const int nb = (int)(B - b0 < tl.bB ? B - b0 : tl.bB);
   const int nu = (int)(H - j0 < tl.u ? H - j0 : tl.u);
   const int nrows = 4 * tl.u;  // gate-major: row g*u + jj
   const int rowsA = MFA ? tl.bB : nb;
   if (tid == 0) s_abort = 0;
+  __syncthreads();
+
+  if (CNT && quantizer) {
+    // Quantizing workgroup of a batched slice: per step, the codes of
+    // h_{t-1} for 8 rows of the slice (one per wave, re-reading the row's
+    // tagged words until every tag matches), stored with device-coherent
+    // stores, then an arrival on the slice's codes counter.
+    const int q0 = (tw - tl.nut) * 8;
+    // a ragged last slice may leave a quantizing workgroup without rows: it
+    // must not arrive either (an arrival that waited for nothing could stand
+    // in for a missing one of a later step)
+    if (q0 >= nb) return;
+    const int nq = nb - q0 < 8 ? nb - q0 : 8;
+    const int hwords = tl.ldH / 8;
+    for (int64_t t = 1; t <= T; ++t) {
+      const int64_t par = (t - 1) & 1;
+      const uint64_t *prev = xht + par * B * H;
+      const bool ok = quant_tile<NVA, 1, kSrcTagged>(nq, nq, H, (uint32_t)t, (int)H, xh, tl.ldsX,
+                                                     tl.ldH, flag, rph,
+                                                     [&](int lb) -> const void * {
+                                                       return prev + (b0 + q0 + lb) * H;
+                                                     });
+      if (!ok) s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      const int64_t row0 = (t - 1) * B + b0 + q0;
+      const int owords = (int)(Ly.out.ld / 8);
+      for (int idx = tid; idx < nq * owords; idx += blockDim.x) {
+        const int lb = idx / owords, wd = idx % owords;
+        uint64_t v = 0;
+        if (wd < hwords) v = *reinterpret_cast<const uint64_t *>(xh + lb * tl.ldsX + wd * 8);
+        st_coherent64(reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld) + wd, v);
+      }
+      for (int lb = tid; lb < nq; lb += blockDim.x) {
+        const RowParam r = rph[lb];
+        st_coherent_i(&Ly.out.zero[row0 + lb], r.z);
+        st_coherent(&Ly.out.inv_q[row0 + lb], r.iqx);
+        st_coherent_i(&Ly.out.sums[row0 + lb], r.sum);
+        if (Ly.tap_zero) Ly.tap_zero[row0 + lb] = r.z;
+        if (Ly.tap_inv_q) Ly.tap_inv_q[row0 + lb] = r.iqx;
+      }
+      if (Ly.tap_codes)
+        for (int idx = tid; idx < nq * (int)H; idx += blockDim.x) {
+          const int lb = idx / (int)H, k = idx % (int)H;
+          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
+        }
+      arrive(ctr(l, par, tb));
+    }
+    return;
+  }
 
   // ---- prologue: W_x' and W_h' slices, column params, bias, c = 0
   for (int idx = tid; idx < nrows * (tl.ldH / 16); idx += blockDim.x) {
@@ -247,61 +301,19 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   };
 
   if constexpr (CNT) {
-    // Batched tiles.  The codes of h_{t-1} are made once per slice: Qn
-    // designated tiles (tu < Qn) each quantize 8 of its rows (one per wave,
-    // re-reading the row's tagged words until every tag matches), store them
-    // with device-coherent stores and arrive on the slice's codes counter;
-    // every tile then loads all rows' codes, as it loads x_t.
-    const int Qn = tl.bB / 8;
-    const bool quantizer = tu < Qn;
-    const int q0 = tu * 8;
-    const int nq = quantizer ? (nb - q0 < 0 ? 0 : (nb - q0 < 8 ? nb - q0 : 8)) : 0;
+    // Batched unit tiles: the codes of h_{t-1} are made once per slice by its
+    // quantizing workgroups that have rows (Qn of them); every tile loads all
+    // rows' codes once their arrivals are in, as it loads x_t.
+    const int Qn = (nb + 7) / 8 < tl.nq ? (nb + 7) / 8 : tl.nq;
     const int hwords = tl.ldH / 8;
     uint64_t hpre[kXPre];
-    for (int64_t t = 0; t <= T; ++t) {
+    for (int64_t t = 0; t < T; ++t) {
       const int64_t hcur = (t & 1) * B * H;
       const int64_t par = (t - 1) & 1;
-      // ---- 1. designated tiles: codes of h_{t-1} for 8 rows of the slice
-      if (t > 0 && quantizer) {
-        const uint64_t *prev = xht + par * B * H;
-        bool ok = true;
-        if (nq > 0)
-          ok = quant_tile<NVA, 1, kSrcTagged>(nq, nq, H, (uint32_t)t, (int)H, xh + q0 * tl.ldsX,
-                                              tl.ldsX, tl.ldH, flag, rph + q0,
-                                              [&](int lb) -> const void * {
-                                                return prev + (b0 + q0 + lb) * H;
-                                              });
-        if (!ok) s_abort = 1;
-        __syncthreads();
-        if (s_abort) return;
-        const int64_t row0 = (t - 1) * B + b0 + q0;
-        const int owords = (int)(Ly.out.ld / 8);
-        for (int idx = tid; idx < nq * owords; idx += blockDim.x) {
-          const int lb = idx / owords, wd = idx % owords;
-          uint64_t v = 0;
-          if (wd < hwords) v = *reinterpret_cast<const uint64_t *>(xh + (q0 + lb) * tl.ldsX + wd * 8);
-          st_coherent64(reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld) + wd, v);
-        }
-        for (int lb = tid; lb < nq; lb += blockDim.x) {
-          const RowParam r = rph[q0 + lb];
-          st_coherent_i(&Ly.out.zero[row0 + lb], r.z);
-          st_coherent(&Ly.out.inv_q[row0 + lb], r.iqx);
-          st_coherent_i(&Ly.out.sums[row0 + lb], r.sum);
-          if (Ly.tap_zero) Ly.tap_zero[row0 + lb] = r.z;
-          if (Ly.tap_inv_q) Ly.tap_inv_q[row0 + lb] = r.iqx;
-        }
-        if (Ly.tap_codes)
-          for (int idx = tid; idx < nq * (int)H; idx += blockDim.x) {
-            const int lb = idx / (int)H, k = idx % (int)H;
-            Ly.tap_codes[(row0 + lb) * H + k] = xh[(q0 + lb) * tl.ldsX + k];
-          }
-        arrive(ctr(l, par, tb));
-      }
-      if (t == T) break;
 
-      // ---- 2. the input side of step t, which does not depend on h_{t-1}:
+      // ---- 1. the input side of step t, which does not depend on h_{t-1}:
       // codes of x_t and their product, done while the codes of h_{t-1} are
-      // still being made (a designated tile has just made its share)
+      // still being made
       if (l > 0 && !wait_count(ctr(l - 1, t & 1, tb), (unsigned)((t >> 1) + 1) * Qn, flag))
         s_abort = 1;
       __syncthreads();
@@ -317,7 +329,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       __syncthreads();
       products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
 
-      // ---- 3. every tile: codes of h_{t-1}
+      // ---- 2. codes of h_{t-1}
       if (t > 0 && !wait_count(ctr(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
         s_abort = 1;
       __syncthreads();
@@ -355,11 +367,11 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       }
       __syncthreads();
 
-      // ---- 4. the recurrent product against the resident W_h' slice
+      // ---- 3. the recurrent product against the resident W_h' slice
       products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
       __syncthreads();
 
-      // ---- 5. recover, gates, cell; publish h_t
+      // ---- 4. recover, gates, cell; publish h_t
       gates(t, hcur);
       __syncthreads();  // LDS of this step is free before the next step
     }
@@ -509,19 +521,19 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.bB = bB;
   tl.mfma = bB > 1;
   tl.nbt = (int)((B + bB - 1) / bB);
-  if (tl.nbt > G) return false;
+  if (tl.nbt > G || tl.nbt > kMaxSlices) return false;
+  tl.nq = tl.mfma ? bB / 8 : 0;  // batched: quantizing workgroups of 8 rows each
   {
-    const int nut = G / tl.nbt;
+    const int nut = G / tl.nbt - tl.nq;
+    if (nut < 1) return false;
     tl.u = (int)((H + nut - 1) / nut);
   }
   if (tl.mfma) tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16
   tl.nut = (int)((H + tl.u - 1) / tl.u);
-  if (tl.nbt > kMaxSlices) return false;
-  if (tl.mfma && tl.nut < tl.bB / 8) return false;  // bB / 8 tiles quantize 8 rows each
   // the x-code prefetch holds 4 words of 8 codes per thread
   if (tl.ldH > 512 || (size_t)(tl.mfma ? bB : 0) * (tl.ldXmax / 8) > 4 * (size_t)kStackThreads)
     return false;
-  tl.gl = tl.nbt * tl.nut;
+  tl.gl = tl.nbt * (tl.nut + tl.nq);
   tl.grid = a.nl * tl.gl;
   if (tl.grid > cus) return false;
   const int nrows = 4 * tl.u;
@@ -536,7 +548,9 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.off_wx = take((size_t)nrows * tl.ldsWx);
   tl.off_xh = take((size_t)tl.bB * tl.ldsX);
   tl.off_xx = take((size_t)tl.bB * tl.ldsXx);
-  tl.off_sh = take((size_t)tl.bB * nrows * 4);
+  // the codes of x_t are consumed (their product formed) before the
+  // recurrent product is written, so Sh may share their space
+  tl.off_sh = (size_t)nrows * 4 <= (size_t)tl.ldsXx ? tl.off_xx : take((size_t)tl.bB * nrows * 4);
   tl.off_sx = take((size_t)tl.bB * nrows * 4);
   tl.off_c = take((size_t)tl.bB * tl.u * 4);
   tl.off_colh = take((size_t)nrows * sizeof(ColParam));
