@@ -34,10 +34,10 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=7.959e9, read=6.403e9, written=1.556e9,
+TRAFFIC = dict(bytes=4.483e9, read=3.034e9, written=1.449e9,
                sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
                         "ql_launch.h"),
-               sha256="1b430bf19eddd3c05240eee49e99a1b68085afce8ebe9ea74866b3a1af4380ef",
+               sha256="1cc4b0d76f6d67b12c6e3d6249cdd4e618893a3aaa7467add979d08a244d1606",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 
