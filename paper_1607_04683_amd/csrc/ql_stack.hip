@@ -252,15 +252,43 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
   };
 
-  // Recover both products, gates, cell update; publish h_t (step t).
+  // Batched tiles: input side of the pre-activations, (W_x x + b) recovered in
+  // place in Sx (float bits) for rows [0, nr), off the recurrence's critical
+  // path.  (One-row tiles recover it in the gates: there the gates are not
+  // the long pole and the extra pass would delay the next step.)
+  auto x_preact = [&](int nr) {
+    __syncthreads();  // Sx complete
+    for (int idx = tid; idx < nr * nrows; idx += blockDim.x) {
+      const int lb = idx / nrows, n = idx % nrows;
+      const RowParam rx = rpx[lb];
+      const ColParam cx = cpx[n];
+      const float g = recover(Sx[idx], cx.colterm, cx.ztw, rx.ztx, rx.sigx, cx.iqw, rx.iqx) + bsl[n];
+      Sx[idx] = __float_as_int(g);
+    }
+  };
+
+  // Gates, cell update; publish h_t (step t).  Pairs (batch row, cell) are
+  // dealt one per lane in full rounds of the workgroup; the remainder is
+  // spread over 2 or 4 lanes per pair (lane g computes gates g of the pair's
+  // gate set) when that fits, so no lane does much more than its share.
   auto gates = [&](int64_t t, int64_t hcur) {
-    const int pairs = nb * nu;
+    const int pairs = nb * nu, nt = (int)blockDim.x;
     auto preact = [&](int lb, int n) {
-      const RowParam rx = rpx[lb], rh = rph[lb];
-      const ColParam cx = cpx[n], ch = cph[n];
-      const float gxv = recover(Sx[lb * nrows + n], cx.colterm, cx.ztw, rx.ztx, rx.sigx, cx.iqw, rx.iqx) + bsl[n];
+      const RowParam rh = rph[lb];
+      const ColParam ch = cph[n];
       const float yh = recover(Sh[lb * nrows + n], ch.colterm, ch.ztw, rh.ztx, rh.sigx, ch.iqw, rh.iqx);
+      if constexpr (CNT) return __int_as_float(Sx[lb * nrows + n]) + yh;
+      const RowParam rx = rpx[lb];
+      const ColParam cx = cpx[n];
+      const float gxv = recover(Sx[lb * nrows + n], cx.colterm, cx.ztw, rx.ztx, rx.sigx, cx.iqw, rx.iqx) + bsl[n];
       return gxv + yh;
+    };
+    // activation of gate g of pair (lb, jj): sigmoid for i, f, o and
+    // tanh(x) = 2 sigmoid(2x) - 1 for g
+    auto act = [&](int lb, int jj, int g) {
+      const float av = preact(lb, g * tl.u + jj);
+      const float sg = sigmoid_cw(g == 2 ? 2.0f * av : av);
+      return g == 2 ? 2.0f * sg - 1.0f : sg;
     };
     auto finish = [&](int lb, int jj, float ig, float fg, float gv, float og) {
       const int64_t b = b0 + lb, j = j0 + jj;
@@ -271,32 +299,35 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
     };
-    if (pairs >= (int)blockDim.x) {
-      // one lane per (b, j) pair: all four gates in the lane
-      for (int pr = tid; pr < pairs; pr += blockDim.x) {
-        const int lb = pr / nu, jj = pr % nu;
-        const float ig = sigmoid_cw(preact(lb, jj));
-        const float fg = sigmoid_cw(preact(lb, tl.u + jj));
-        const float gv = 2.0f * sigmoid_cw(2.0f * preact(lb, 2 * tl.u + jj)) - 1.0f;
-        const float og = sigmoid_cw(preact(lb, 3 * tl.u + jj));
-        finish(lb, jj, ig, fg, gv, og);
+    const int full = pairs / nt, rem = pairs % nt;
+    for (int k = 0; k < full; ++k) {
+      const int pr = k * nt + tid, lb = pr / nu, jj = pr % nu;
+      finish(lb, jj, act(lb, jj, 0), act(lb, jj, 1), act(lb, jj, 2), act(lb, jj, 3));
+    }
+    if (rem == 0) return;
+    const int p0 = full * nt;
+    if (4 * rem <= nt) {
+      // four lanes per pair (whole quads active: 4 * rem lanes from lane 0)
+      if (tid < 4 * rem) {
+        const int pr = p0 + (tid >> 2), lb = pr / nu, jj = pr % nu;
+        const float a = act(lb, jj, tid & 3);
+        const float ig = quad_bcast<0>(a), fg = quad_bcast<1>(a);
+        const float gv = quad_bcast<2>(a), og = quad_bcast<3>(a);
+        if ((tid & 3) == 0) finish(lb, jj, ig, fg, gv, og);
       }
-    } else {
-      // four lanes per pair (lane g of the quad computes gate g); sigmoid for
-      // i, f, o and tanh(x) = 2 sigmoid(2x) - 1 for g
-      for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
-        const int pr = idx >> 2, gg = idx & 3;
-        const int lb = pr / nu, jj = pr % nu;
-        const float av = preact(lb, gg * tl.u + jj);
-        const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
-        const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
-        // the loop keeps whole quads active (pairs * 4 is a multiple of 4)
-        const float ig = quad_bcast<0>(act);
-        const float fg = quad_bcast<1>(act);
-        const float gv = quad_bcast<2>(act);
-        const float og = quad_bcast<3>(act);
-        if (gg == 0) finish(lb, jj, ig, fg, gv, og);
+    } else if (2 * rem <= nt) {
+      // two lanes per pair: the even lane takes i and f, the odd one g and o
+      if (tid < 2 * rem) {
+        const int pr = p0 + (tid >> 1), lb = pr / nu, jj = pr % nu, h = tid & 1;
+        const float a0 = act(lb, jj, 2 * h), a1 = act(lb, jj, 2 * h + 1);
+        // swap with the other lane of the pair (quad_perm 1,0,3,2)
+        const float b0v = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a0), 0xB1, 0xf, 0xf, false));
+        const float b1v = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a1), 0xB1, 0xf, 0xf, false));
+        if (h == 0) finish(lb, jj, a0, a1, b0v, b1v);
       }
+    } else if (tid < rem) {
+      const int pr = p0 + tid, lb = pr / nu, jj = pr % nu;
+      finish(lb, jj, act(lb, jj, 0), act(lb, jj, 1), act(lb, jj, 2), act(lb, jj, 3));
     }
   };
 
@@ -328,6 +359,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
       __syncthreads();
       products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+      x_preact(nb);
 
       // ---- 2. codes of h_{t-1}
       if (t > 0 && !wait_count(ctr(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
