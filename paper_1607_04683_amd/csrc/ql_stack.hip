@@ -53,6 +53,7 @@ struct StackTiling {
   int64_t strideh;          // 64-bit words between replicas
   int nw;                   // tagged code words per row: ldH / 4 codes + 3 params
   size_t hx_bytes, cx_bytes, layer_bytes;  // exchange bytes per layer
+  size_t off_xh2, off_rowh2;  // second buffer of the codes of h (one-row tiles)
   size_t off_wh, off_wx, off_xh, off_xx, off_sh, off_sx, off_c, off_colh, off_colx, off_rowh,
       off_rowx, off_bias, lds_bytes;
 };
@@ -460,80 +461,179 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     __syncthreads();
     return true;
   };
-  if (T > 0 && !input_side(0)) return;
-  for (int64_t t = 0; t <= T; ++t) {
-    const int64_t hcur = (t & 1) * B * H;
-    // ---- 1. h_{t-1} of this batch slice, quantized per vector
-    bool ok;
-    if (t == 0) {
-      ok = quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
-                                           [&](int) -> const void * { return nullptr; });
+  // Share of the codes of h_{t-1} (in xh / rph) by threads first, first +
+  // stride, ...: this layer's output and, inside the launch, the next
+  // layer's input (16-byte chunk c and tagged word w go to tile c % nut and
+  // w % nut).
+  const int chunks_out = (int)(Ly.out.ld / 16);
+  const int mych = (chunks_out - tu + tl.nut - 1) / tl.nut;  // chunks tu, tu + nut, ...
+  const int mywd = (tl.nw - tu + tl.nut - 1) / tl.nut;       // words tu, tu + nut, ...
+  auto share_prev = [&](int64_t t, int first, int stride) {
+    const int64_t row0 = (t - 1) * B + b0;
+    const int me = tid - first;
+    for (int idx = me; idx < nb * mych; idx += stride) {
+      const int lb = idx / mych, ch = tu + (idx % mych) * tl.nut;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
+      *reinterpret_cast<uint4 *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16) = v;
+    }
+    if (tu == 0)
+      for (int lb = me; lb < nb; lb += stride) {
+        const int64_t row = row0 + lb;
+        Ly.out.zero[row] = rph[lb].z;
+        Ly.out.inv_q[row] = rph[lb].iqx;
+        Ly.out.sums[row] = rph[lb].sum;
+        if (Ly.tap_zero) Ly.tap_zero[row] = rph[lb].z;
+        if (Ly.tap_inv_q) Ly.tap_inv_q[row] = rph[lb].iqx;
+      }
+    if (Ly.tap_codes && tu == 0)
+      for (int idx = me; idx < nb * (int)H; idx += stride) {
+        const int lb = idx / (int)H, k = idx % (int)H;
+        Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
+      }
+    if (l + 1 < a.nl) {
+      // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
+      uint64_t *ct = ctag(l);
+      for (int idx = me; idx < nb * mywd; idx += stride) {
+        const int lb = idx / mywd, wd = tu + (idx % mywd) * tl.nut;
+        uint32_t pay;
+        if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
+        else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
+        else if (wd == tl.ldH / 4 + 1) pay = __float_as_uint(rph[lb].iqx);
+        else pay = (uint32_t)rph[lb].sum;
+        __hip_atomic_store(ct + (row0 + lb) * tl.nw + wd, ((uint64_t)t << 32) | pay,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  };
+
+  // Input side of step t for waves 1..: the codes of x_t straight into
+  // registers (plain input, or layer l-1's tagged words re-read until their
+  // tags match), their products against the resident W_x' slice into Sx,
+  // and the row params into rpx; no workgroup barrier inside.  False if a
+  // wait expired.  One batch row; its ld of at most 512 codes is two 16-byte
+  // chunks per lane of a 16-lane group.
+  auto input_side_async = [&](int64_t t) -> bool {
+    const int gt = tid - kWave, grp = gt >> 4, gl = gt & 15;
+    const int ngrp = ((int)blockDim.x - kWave) >> 4;
+    const int64_t xrow = t * B + b0;
+    v4i xa[2] = {v4i{}, v4i{}};
+    bool ok = true;
+    if (l == 0) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int k = gl * 16 + c * 256;
+        if (k < ldXl) xa[c] = *reinterpret_cast<const v4i *>(Ly.xin.codes + xrow * Ly.xin.ld + k);
+      }
+      if (gt == 0)
+        rpx[0] = row_param(Ly.xin.zero[xrow], Ly.xin.inv_q[xrow], Ly.xin.sums[xrow], (int)IN);
     } else {
-      const uint64_t *prev = xht_mine + ((t + 1) & 1) * B * H;
-      ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)t, (int)H, xh, tl.ldsX, tl.ldH,
-                                            flag, rph, [&](int lb) -> const void * {
-                                              return prev + (b0 + lb) * H;
-                                            });
-    }
-    if (!ok) s_abort = 1;
-    __syncthreads();
-    if (s_abort) return;
-
-    // ---- share of the codes of h_{t-1}: this layer's output and, inside the
-    // launch, the next layer's input (16-byte chunk c goes to tile c % nut)
-    if (t > 0) {
-      const int64_t row0 = (t - 1) * B + b0;
-      const int chunks = (int)(Ly.out.ld / 16);
-      const int mych = (chunks - tu + tl.nut - 1) / tl.nut;  // chunks tu, tu + nut, ...
-      for (int idx = tid; idx < nb * mych; idx += blockDim.x) {
-        const int lb = idx / mych, ch = tu + (idx % mych) * tl.nut;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (ch * 16 < tl.ldH) v = *reinterpret_cast<const uint4 *>(xh + lb * tl.ldsX + ch * 16);
-        *reinterpret_cast<uint4 *>(Ly.out.codes + (row0 + lb) * Ly.out.ld + ch * 16) = v;
-      }
-      if (tu == 0)
-        for (int lb = tid; lb < nb; lb += blockDim.x) {
-          const int64_t row = row0 + lb;
-          Ly.out.zero[row] = rph[lb].z;
-          Ly.out.inv_q[row] = rph[lb].iqx;
-          Ly.out.sums[row] = rph[lb].sum;
-          if (Ly.tap_zero) Ly.tap_zero[row] = rph[lb].z;
-          if (Ly.tap_inv_q) Ly.tap_inv_q[row] = rph[lb].iqx;
+      const int nwx = ldXl / 4 + 3;  // layer l-1's row: its ldH == ldXl here
+      const uint64_t *ct = ctag(l - 1) + xrow * nwx;
+      const uint32_t tag = (uint32_t)(t + 1);
+      uint32_t pz = 0, pq = 0, ps = 0;
+      long it = 0;
+      for (;;) {
+        uint32_t bad = 0;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int k = gl * 16 + c * 256;
+          if (k < ldXl) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint64_t w = ld_tagged(ct + k / 4 + e);
+              bad |= (uint32_t)(w >> 32) ^ tag;
+              xa[c][e] = (int)(uint32_t)w;
+            }
+          }
         }
-      if (Ly.tap_codes && tu == 0)
-        for (int idx = tid; idx < nb * (int)H; idx += blockDim.x) {
-          const int lb = idx / (int)H, k = idx % (int)H;
-          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
+        if (gt == 0) {
+          const uint64_t w0 = ld_tagged(ct + ldXl / 4), w1 = ld_tagged(ct + ldXl / 4 + 1),
+                         w2 = ld_tagged(ct + ldXl / 4 + 2);
+          bad |= ((uint32_t)(w0 >> 32) ^ tag) | ((uint32_t)(w1 >> 32) ^ tag) |
+                 ((uint32_t)(w2 >> 32) ^ tag);
+          pz = (uint32_t)w0;
+          pq = (uint32_t)w1;
+          ps = (uint32_t)w2;
         }
-      if (l + 1 < a.nl) {
-        // tagged words for the next layer: 4 codes per word, then z, inv_q, sum
-        uint64_t *ct = ctag(l);
-        const int mywd = (tl.nw - tu + tl.nut - 1) / tl.nut;  // words tu, tu + nut, ...
-        for (int idx = tid; idx < nb * mywd; idx += blockDim.x) {
-          const int lb = idx / mywd, wd = tu + (idx % mywd) * tl.nut;
-          uint32_t pay;
-          if (wd < tl.ldH / 4) pay = *reinterpret_cast<const uint32_t *>(xh + lb * tl.ldsX + 4 * wd);
-          else if (wd == tl.ldH / 4) pay = (uint32_t)rph[lb].z;
-          else if (wd == tl.ldH / 4 + 1) pay = __float_as_uint(rph[lb].iqx);
-          else pay = (uint32_t)rph[lb].sum;
-          __hip_atomic_store(ct + (row0 + lb) * tl.nw + wd, ((uint64_t)t << 32) | pay,
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (bad == 0) break;
+        if (wait_expired(flag, it)) {
+          ok = false;
+          break;
         }
       }
+      if (gt == 0 && ok) rpx[0] = row_param((int32_t)pz, __uint_as_float(pq), (int32_t)ps, (int)IN);
     }
-    if (t == T) break;
+    for (int n = grp; n < nrows; n += ngrp) {
+      const int8_t *wr = wx + n * tl.ldsWx;
+      int acc = 0;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int k = gl * 16 + c * 256;
+        if (k < ldXl) {
+          const v4i b = *reinterpret_cast<const v4i *>(wr + k);
+          acc = __builtin_amdgcn_sdot4(xa[c].x, b.x, acc, false);
+          acc = __builtin_amdgcn_sdot4(xa[c].y, b.y, acc, false);
+          acc = __builtin_amdgcn_sdot4(xa[c].z, b.z, acc, false);
+          acc = __builtin_amdgcn_sdot4(xa[c].w, b.w, acc, false);
+        }
+      }
+      // sum over the group's 16 lanes (one DPP row)
+      acc += __builtin_amdgcn_update_dpp(0, acc, 0x121, 0xf, 0xf, false);
+      acc += __builtin_amdgcn_update_dpp(0, acc, 0x122, 0xf, 0xf, false);
+      acc += __builtin_amdgcn_update_dpp(0, acc, 0x124, 0xf, 0xf, false);
+      acc += __builtin_amdgcn_update_dpp(0, acc, 0x128, 0xf, 0xf, false);
+      if (gl == 0) Sx[n] = acc;
+    }
+    return ok;
+  };
 
-    // ---- 3. the recurrent product (the input side's is already in Sx)
+  // Per step: the recurrent product and the gates (all waves); then, while
+  // h_t travels, wave 0 quantizes h_t into the other buffer of codes and the
+  // other waves share the codes of h_{t-1} and form the input side of step
+  // t+1.
+  int8_t *const xhb[2] = {xh, reinterpret_cast<int8_t *>(smem + tl.off_xh2)};
+  RowParam *const rphb[2] = {rph, reinterpret_cast<RowParam *>(smem + tl.off_rowh2)};
+  if (T > 0 && !input_side(0)) return;
+  if (!quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
+                                       [&](int) -> const void * { return nullptr; }))
+    return;
+  __syncthreads();
+  const int wave = tid >> 6;
+  for (int64_t t = 0; t < T; ++t) {
+    const int64_t hcur = (t & 1) * B * H;
+    xh = xhb[t & 1];
+    rph = rphb[t & 1];
+
+    // ---- 1. the recurrent product (the input side's is already in Sx)
     products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
     __syncthreads();
 
-    // ---- 4. recover, gates, cell; publish h_t
+    // ---- 2. recover, gates, cell; publish h_t
     gates(t, hcur);
-    __syncthreads();  // Sx and the LDS of this step are free
+    __syncthreads();  // Sx and Sh are free
 
-    // ---- 5. the input side of step t+1 while h_t travels
-    if (t + 1 < T && !input_side(t + 1)) return;
+    // ---- 3. while h_t travels: its codes (wave 0); the share of the codes
+    // of h_{t-1} and the input side of step t+1 (the other waves)
+    if (wave == 0) {
+      const uint64_t *cur = xht_mine + (t & 1) * B * H;
+      if (!quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)(t + 1), (int)H,
+                                            xhb[(t + 1) & 1], tl.ldsX, tl.ldH, flag,
+                                            rphb[(t + 1) & 1], [&](int lb) -> const void * {
+                                              return cur + (b0 + lb) * H;
+                                            }))
+        s_abort = 1;
+    } else {
+      if (t > 0) share_prev(t, kWave, (int)blockDim.x - kWave);
+      if (t + 1 < T && !input_side_async(t + 1)) s_abort = 1;
+    }
+    __syncthreads();
+    if (s_abort) return;
   }
+  // the codes of h_{T-1}
+  xh = xhb[T & 1];
+  rph = rphb[T & 1];
+  share_prev(T, 0, (int)blockDim.x);
 }
 
 // ------------------------------------------------------------------ host side
@@ -565,6 +665,7 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   // the x-code prefetch holds 4 words of 8 codes per thread
   if (tl.ldH > 512 || (size_t)(tl.mfma ? bB : 0) * (tl.ldXmax / 8) > 4 * (size_t)kStackThreads)
     return false;
+  if (!tl.mfma && tl.ldXmax > 512) return false;  // one-row input side: two 16-byte chunks per lane
   tl.gl = tl.nbt * (tl.nut + tl.nq);
   tl.grid = a.nl * tl.gl;
   if (tl.grid > cus) return false;
@@ -590,6 +691,9 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.off_rowh = take((size_t)tl.bB * sizeof(RowParam));
   tl.off_rowx = take((size_t)tl.bB * sizeof(RowParam));
   tl.off_bias = take((size_t)nrows * 4);
+  // one-row tiles make the codes of h_t while h_{t-1}'s are still being shared
+  tl.off_xh2 = tl.mfma ? tl.off_xh : take((size_t)tl.bB * tl.ldsX);
+  tl.off_rowh2 = tl.mfma ? tl.off_rowh : take((size_t)tl.bB * sizeof(RowParam));
   tl.lds_bytes = off;
   if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
   // exchange per layer
