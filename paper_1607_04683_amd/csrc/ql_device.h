@@ -114,15 +114,43 @@ __device__ __forceinline__ uint32_t pack4_s8(int c0, int c1, int c2, int c3) {
 //   T = sum_k (sw + ztw)(sx + ztx) = S + ztx * sigw + ztw * sigx + K ztw ztx
 // where S = sum_k sw sx is what the signed 8-bit MFMA/dot products return.
 // ---------------------------------------------------------------------------
+// Low 32 bits of the product of two signed 24-bit values (v_mul_i32_i24,
+// full rate; a 32-bit v_mul_lo_u32 runs at a quarter of it).  Written out
+// because the compiler, having proved the range, would fold the 24-bit
+// extension of __mul24 away and fall back to the 32-bit multiply.
+__device__ __forceinline__ int32_t mul_i24(int32_t a, int32_t b) {
+  int32_t r;
+  asm("v_mul_i32_i24 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// T in 32 bits with 24-bit multiplies; only valid where recover() below
+// takes its fast path (both shifted zero points in [-127, 128] and
+// |colterm| < 2^23): callers check that once for a whole tile.
+__device__ __forceinline__ float recover_fast(int32_t S, int32_t colterm, int32_t ztw, int32_t ztx,
+                                              int32_t sigx, float iqw, float iqx) {
+  const uint32_t t = (uint32_t)S + (uint32_t)mul_i24(ztx, colterm) + (uint32_t)mul_i24(ztw, sigx);
+  return ((float)(int32_t)t * iqw) * iqx;
+}
+// The fast-path condition for one row (ztx) or one column (ztw, colterm).
+__device__ __forceinline__ bool fast_row(int32_t ztx) { return (uint32_t)(ztx + 127) <= 255u; }
+__device__ __forceinline__ bool fast_col(int32_t ztw, int64_t colterm) {
+  return (uint32_t)(ztw + 127) <= 255u && (uint64_t)(colterm + (1 << 23)) < (uint64_t)(1 << 24);
+}
+
 __device__ __forceinline__ float recover(int32_t S, int64_t colterm /* sigw + K ztw */,
                                          int32_t ztw, int32_t ztx, int32_t sigx,
                                          float iqw, float iqx) {
   // When both zero points lie in [-255, 0] (every set whose range contains 0),
   // V'' = V' + z lies in [-255, 255], so |T| <= K * 255^2 < 2^31 for K <= 33025
   // and the wrapping 32-bit evaluation is T exactly (z~ = z + 128 in [-127, 128]).
-  if ((uint32_t)(ztx + 127) <= 255u && (uint32_t)(ztw + 127) <= 255u) {
-    const uint32_t t = (uint32_t)S + (uint32_t)ztx * (uint32_t)colterm +
-                       (uint32_t)ztw * (uint32_t)sigx;
+  // Every factor then fits 24 signed bits (|sigx| <= 128 K; colterm is checked,
+  // it does for K < 32768), so the full-rate 24-bit multiplies, which return
+  // the low 32 bits of the exact product, serve.
+  if ((uint32_t)(ztx + 127) <= 255u && (uint32_t)(ztw + 127) <= 255u &&
+      (uint64_t)(colterm + (1 << 23)) < (uint64_t)(1 << 24)) {
+    const uint32_t t = (uint32_t)S + (uint32_t)mul_i24(ztx, (int32_t)colterm) +
+                       (uint32_t)mul_i24(ztw, sigx);
     return ((float)(int32_t)t * iqw) * iqx;
   }
   const int64_t t = (int64_t)S + (int64_t)ztx * colterm + (int64_t)ztw * (int64_t)sigx;

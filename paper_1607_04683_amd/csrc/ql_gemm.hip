@@ -435,12 +435,14 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
   float2 *red = reinterpret_cast<float2 *>(smem + 3 * BM * 4);  // [WN][BM] (max, sum)
   const int wave = threadIdx.x >> 6;
   uint32_t *slab = reinterpret_cast<uint32_t *>(smem + kSlab) + wave * 32 * RS;
+  bool fast = true;  // every row and column of the tile on recover()'s fast path
   for (int r = threadIdx.x; r < BM; r += C::NT) {
     int64_t m = m0 + r;
     m = m < M ? m : M - 1;
     rsig[r] = e.x_sums[m] - 128 * (int32_t)K;
     rzt[r] = e.x_zero[m] + 128;
     riq[r] = e.x_inv_q[m];
+    fast = fast && fast_row(rzt[r]);
   }
   // this lane's columns: n0 + wn*TN + 4*(lane & 31) + t
   const int64_t nc = n0 + wn * TN + 4 * (lane & 31);
@@ -456,8 +458,12 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
     colterm[t] = (int64_t)sigw[t] + K * (int64_t)ztw[t];
     iqw[t] = e.w_inv_q[blk];
     bn[t] = e.bias ? e.bias[nn] : 0.0f;
+    fast = fast && fast_col(ztw[t], colterm[t]);
   }
-  __syncthreads();
+  fast = __syncthreads_and(fast);
+  int32_t colt32[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) colt32[t] = (int32_t)colterm[t];
   const bool vec = (N & 3) == 0 && nc + 3 < N;
   // chunks expanded at compile time: acc is only ever indexed by constants
   static_for<0, C::FM>([&](auto ic) {
@@ -476,8 +482,13 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
       const v4i v = *reinterpret_cast<const v4i *>(slab + row * RS + 4 * (lane & 31));
       const int32_t sigx = rsig[lr], ztx = rzt[lr];
       const float iqx = riq[lr];
+      if (fast) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) y[t] = recover(v[t], colterm[t], ztw[t], ztx, sigx, iqw[t], iqx) + bn[t];
+        for (int t = 0; t < 4; ++t) y[t] = recover_fast(v[t], colt32[t], ztw[t], ztx, sigx, iqw[t], iqx) + bn[t];
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) y[t] = recover(v[t], colterm[t], ztw[t], ztx, sigx, iqw[t], iqx) + bn[t];
+      }
       const int64_t off = m * N + nc;
       if (EPI == EPI_RECOVER || EPI == EPI_SMAX_OUT) {
         if (EPI == EPI_SMAX_OUT) {
