@@ -164,10 +164,11 @@ def test_model_5x500_softmax8192_T1000_B64_sampled(ql, orc):
 
 def test_model_4xlstmp2048_softmax16384_T800_B256_sampled(ql, orc):
     """4 x LSTMP(2048 cells, P=512), 640-dim input, 16384-way softmax, batch 256
-    x T=800 on the GPU; the oracle recomputes one utterance."""
+    x T=800 on the GPU; the oracle recomputes four whole utterances (the first
+    and the last among them)."""
     from paper_1607_04683_amd.workloads import (LSTMP4x2048P512_S16384_T800_B256 as W_,
                                                 model_weights, features)
-    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[131])
+    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[0, 77, 131, 255])
 
 
 def test_model_batch_invariance_and_determinism(ql):
