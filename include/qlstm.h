@@ -27,9 +27,10 @@
  *   - the recovery factor is Q^-1 = (float)(R / 255); a product's recovered
  *     value is ((float)T * Qw^-1) * Qx^-1 where T = sum_k W'' x'' exactly;
  *   - gate pre-activations are (Wx x + b) + Wh h in fp32; gates are i, f, g, o;
- *     sigmoid(x) = 1 / (1 + e^-x), tanh(x) = 2 sigmoid(2x) - 1 with an exact
- *     fp32 e^x (Cody-Waite reduction + degree-7 Taylor polynomial), no fused
- *     multiply-add; c = f c + i g; m = o tanh(c); projection h = W_r m (no bias);
+ *     sigmoid(x) = 1 / (1 + e^-x) (IEEE division), tanh(x) = 2 sigmoid(2x) - 1
+ *     with a fixed fp32 e^x (Cody-Waite reduction + degree-7 Taylor polynomial,
+ *     each of their steps one fused multiply-add, no other contraction);
+ *     c = f c + i g; m = o tanh(c); projection h = W_r m (no bias);
  *   - activations are quantized per vector (one frame of one utterance);
  *   - softmax is fp32 with the row maximum subtracted.
  *

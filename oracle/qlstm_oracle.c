@@ -26,7 +26,8 @@
  *     the projection (when present) is linear with no bias.
  *   - sigmoid(x) = 1 / (1 + e^-x), tanh(x) = 2 sigmoid(2x) - 1, with e^x by
  *     Cody-Waite reduction and a Taylor polynomial (oracle_expf), all in fp32
- *     with IEEE division and no fused multiply-add.
+ *     with IEEE division; the reduction and the polynomial use fused
+ *     multiply-add (fmaf, one rounding), nothing else is contracted.
  *   - Activations are quantized per vector (one frame of one utterance).
  *   - Softmax posteriors are computed in fp64 from the fp32 logits.
  *
@@ -47,10 +48,11 @@
 /* e^x after W. J. Cody and W. Waite, "Software Manual for the Elementary
  * Functions" (1980): x = n ln2 + r with n the nearest integer to x / ln2 and
  * ln2 split into a short high part (n * hi is exact) and a low part, so that
- * |r| <= ln2 / 2; e^r is the degree-7 Taylor polynomial of exp evaluated in
- * Horner form; e^x = 2^n e^r by an exact power-of-two scaling.  The argument
- * is clamped to [-87, 87], so every result, and 1 / (1 + e^x), is a normal
- * float. */
+ * |r| <= ln2 / 2 (about); e^r is the degree-7 Taylor polynomial of exp
+ * evaluated in Horner form; e^x = 2^n e^r by an exact power-of-two scaling.
+ * Every multiply-add of the reduction and of Horner's scheme is one fused
+ * multiply-add (fmaf), so each step rounds once.  The argument is clamped to
+ * [-87, 87], so every result, and 1 / (1 + e^x), is a normal float. */
 float oracle_expf(float x) {
   const float log2e = 1.44269504088896340736f;
   const float ln2_hi = 0.693145751953125f;        /* 15 significant bits */
@@ -58,17 +60,17 @@ float oracle_expf(float x) {
   if (x != x) return x;
   if (x > 87.0f) x = 87.0f;
   if (x < -87.0f) x = -87.0f;
-  float n = floorf(x * log2e + 0.5f);
-  float r = x - n * ln2_hi;
-  r = r - n * ln2_lo;
+  float n = floorf(fmaf(x, log2e, 0.5f));
+  float r = fmaf(-n, ln2_hi, x);
+  r = fmaf(-n, ln2_lo, r);
   float p = 1.0f / 5040.0f;
-  p = p * r + 1.0f / 720.0f;
-  p = p * r + 1.0f / 120.0f;
-  p = p * r + 1.0f / 24.0f;
-  p = p * r + 1.0f / 6.0f;
-  p = p * r + 0.5f;
-  p = p * r + 1.0f;
-  p = p * r + 1.0f;
+  p = fmaf(p, r, 1.0f / 720.0f);
+  p = fmaf(p, r, 1.0f / 120.0f);
+  p = fmaf(p, r, 1.0f / 24.0f);
+  p = fmaf(p, r, 1.0f / 6.0f);
+  p = fmaf(p, r, 0.5f);
+  p = fmaf(p, r, 1.0f);
+  p = fmaf(p, r, 1.0f);
   union {
     uint32_t u;
     float f;

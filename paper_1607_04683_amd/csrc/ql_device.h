@@ -1,11 +1,12 @@
 // ql_device.h -- device-side building blocks shared by the gfx950 kernels.
 //
 // The arithmetic here follows the numerical conventions stated in
-// include/qlstm.h.  Every float operation is an IEEE fp32/fp64 + - * / with
-// no contraction into fused multiply-adds (the library is compiled with
-// -ffp-contract=off, and the pragma below pins it for this header), so the
-// gate functions give the same bits as any other IEEE implementation of the
-// same formulas.
+// include/qlstm.h.  Every float operation is an IEEE fp32/fp64 + - * / or,
+// where written out (the reduction and polynomial of e^x), a fused
+// multiply-add; nothing is contracted implicitly (the library is compiled
+// with -ffp-contract=off, and the pragma below pins it for this header), so
+// the gate functions give the same bits as any other IEEE implementation of
+// the same formulas.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -24,24 +25,25 @@ constexpr int kWave = 64;
 // e^x: Cody & Waite ("Software Manual for the Elementary Functions", 1980)
 // range reduction x = n ln2 + r with ln2 split into a 15-bit head (so n * head
 // is exact for |n| <= 127) and a tail; e^r by the Taylor series of exp to
-// degree 7 in Horner form; the result scaled by 2^n through its exponent
+// degree 7 in Horner form, each step of the reduction and of Horner's scheme
+// one fused multiply-add; the result scaled by 2^n through its exponent
 // field.  x is clamped to [-87, 87] so results and 1 / (1 + e^x) are normal.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float exp_cw(float x) {
   if (x != x) return x;
   x = x > 87.0f ? 87.0f : x;
   x = x < -87.0f ? -87.0f : x;
-  const float n = floorf(x * 1.44269504088896340736f + 0.5f);
-  float r = x - n * 0.693145751953125f;
-  r = r - n * 1.42860682030941723212e-6f;
+  const float n = floorf(__builtin_fmaf(x, 1.44269504088896340736f, 0.5f));
+  float r = __builtin_fmaf(-n, 0.693145751953125f, x);
+  r = __builtin_fmaf(-n, 1.42860682030941723212e-6f, r);
   float p = 1.0f / 5040.0f;
-  p = p * r + 1.0f / 720.0f;
-  p = p * r + 1.0f / 120.0f;
-  p = p * r + 1.0f / 24.0f;
-  p = p * r + 1.0f / 6.0f;
-  p = p * r + 0.5f;
-  p = p * r + 1.0f;
-  p = p * r + 1.0f;
+  p = __builtin_fmaf(p, r, 1.0f / 720.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 120.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 24.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 6.0f);
+  p = __builtin_fmaf(p, r, 0.5f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
   const float scale = __int_as_float(((int)n + 127) << 23);
   return p * scale;
 }
