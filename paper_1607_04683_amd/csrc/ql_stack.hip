@@ -38,6 +38,8 @@
 namespace ql {
 
 constexpr int kStackThreads = 512;
+// Replicas of the tagged h words at one batch row (readers spread over them).
+constexpr int kMaxReph = 2;
 
 // Per-layer arrival counters of the codes of h: [parity][slice], 64 bytes apart.
 constexpr size_t kStackCounterBytes = (size_t)2 * kMaxSlices * 64;
@@ -699,7 +701,7 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   // exchange per layer
   tl.nw = tl.ldH / 4 + 3;
   if (B < 16) {
-    tl.reph = std::max(1, std::min(4, 2048 / std::max(1, tl.u)));
+    tl.reph = std::max(1, std::min(kMaxReph, 2048 / std::max(1, tl.u)));
     tl.strideh = round_up(2 * B * H, 8192) + 512;
     tl.hx_bytes = (size_t)tl.reph * tl.strideh * 8;
     tl.cx_bytes = (size_t)a.T * B * tl.nw * 8;
@@ -729,7 +731,7 @@ size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H) {
   size_t per;
   if (B < 16) {
     const int64_t strideh = round_up(2 * B * H, 8192) + 512;
-    per = align_up((size_t)4 * strideh * 8 + (size_t)T * B * (ldH / 4 + 3) * 8, 256);
+    per = align_up((size_t)kMaxReph * strideh * 8 + (size_t)T * B * (ldH / 4 + 3) * 8, 256);
   } else {
     per = align_up(align_up((size_t)2 * B * H * 8, 256), 256);
   }
