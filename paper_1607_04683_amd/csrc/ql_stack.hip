@@ -159,30 +159,33 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
                                                        return prev + (b0 + q0 + lb) * H;
                                                      });
       if (!ok) s_abort = 1;
+      // each wave stores the row it quantized (its own LDS writes are in order)
+      const int lb = tid >> 6, lane = tid & 63;
+      if (ok && lb < nq) {
+        const int64_t row = (t - 1) * B + b0 + q0 + lb;
+        const int owords = (int)(Ly.out.ld / 8);
+        for (int wd = lane; wd < owords; wd += kWave) {
+          uint64_t v = 0;
+          if (wd < hwords) v = *reinterpret_cast<const uint64_t *>(xh + lb * tl.ldsX + wd * 8);
+          st_coherent64(reinterpret_cast<uint64_t *>(Ly.out.codes + row * Ly.out.ld) + wd, v);
+        }
+        if (lane == 0) {
+          const RowParam r = rph[lb];
+          st_coherent_i(&Ly.out.zero[row], r.z);
+          st_coherent(&Ly.out.inv_q[row], r.iqx);
+          st_coherent_i(&Ly.out.sums[row], r.sum);
+          if (Ly.tap_zero) Ly.tap_zero[row] = r.z;
+          if (Ly.tap_inv_q) Ly.tap_inv_q[row] = r.iqx;
+        }
+        if (Ly.tap_codes)
+          for (int k = lane; k < (int)H; k += kWave) Ly.tap_codes[row * H + k] = xh[lb * tl.ldsX + k];
+      }
+      // arrival once every wave's stores have completed (none after a failed wait)
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       if (s_abort) return;
-      const int64_t row0 = (t - 1) * B + b0 + q0;
-      const int owords = (int)(Ly.out.ld / 8);
-      for (int idx = tid; idx < nq * owords; idx += blockDim.x) {
-        const int lb = idx / owords, wd = idx % owords;
-        uint64_t v = 0;
-        if (wd < hwords) v = *reinterpret_cast<const uint64_t *>(xh + lb * tl.ldsX + wd * 8);
-        st_coherent64(reinterpret_cast<uint64_t *>(Ly.out.codes + (row0 + lb) * Ly.out.ld) + wd, v);
-      }
-      for (int lb = tid; lb < nq; lb += blockDim.x) {
-        const RowParam r = rph[lb];
-        st_coherent_i(&Ly.out.zero[row0 + lb], r.z);
-        st_coherent(&Ly.out.inv_q[row0 + lb], r.iqx);
-        st_coherent_i(&Ly.out.sums[row0 + lb], r.sum);
-        if (Ly.tap_zero) Ly.tap_zero[row0 + lb] = r.z;
-        if (Ly.tap_inv_q) Ly.tap_inv_q[row0 + lb] = r.iqx;
-      }
-      if (Ly.tap_codes)
-        for (int idx = tid; idx < nq * (int)H; idx += blockDim.x) {
-          const int lb = idx / (int)H, k = idx % (int)H;
-          Ly.tap_codes[(row0 + lb) * H + k] = xh[lb * tl.ldsX + k];
-        }
-      arrive(ctr(l, par, tb));
+      if (tid == 0)
+        __hip_atomic_fetch_add(ctr(l, par, tb), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     return;
   }
