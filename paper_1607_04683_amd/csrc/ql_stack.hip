@@ -3,31 +3,32 @@
 // already on frame t+1 or later, so a launch of n layers takes about T + n
 // steps instead of n * T.
 //
-// Each workgroup owns a tile of (bB batch rows) x (u hidden units) of one
-// layer and keeps both of the layer's weight slices resident in LDS: the 4u
-// gate rows of W_x' and of W_h'.  Per step it
-//   1. quantizes h_{t-1} of its batch rows per vector (eq. 2), exactly as the
-//      single-layer kernel does (values exchanged inside the layer);
-//   2. takes the codes of x_t: the launch's first layer reads them from the
+// A unit tile owns (bB batch rows) x (u hidden units) of one layer and keeps
+// both of the layer's weight slices resident in LDS: the 4u gate rows of W_x'
+// and of W_h'.  Per step it
+//   1. takes the codes of x_t: the launch's first layer reads them from the
 //      already quantized input, a later layer reads the codes layer l-1
 //      produced for its h_t, which are the same codes layer l-1 used itself
-//      (one vector, one quantization; no re-quantization);
-//   3. forms both 8-bit products, recovers them (eq. 1 / eq. 3), adds the
-//      bias as the hoisted path does, (W_x x + b) + W_h h, and runs the gates
-//      (the input-side product does not depend on h_{t-1}, so it is formed
-//      while h_{t-1} is still travelling between the workgroups);
-//   4. publishes h_t to its own layer and stores its share of the codes of
-//      h_{t-1} (the layer's output and the next layer's input).
+//      (one vector, one quantization; no re-quantization), and forms the
+//      input-side product; none of this depends on h_{t-1}, so it is done
+//      while h_{t-1} is still travelling between the workgroups;
+//   2. takes the codes of h_{t-1} (quantized per vector, eq. 2);
+//   3. forms the recurrent 8-bit product, recovers both products (eq. 1 /
+//      eq. 3), adds the bias as the hoisted path does, (W_x x + b) + W_h h,
+//      and runs the gates and the cell update;
+//   4. publishes h_t as tagged words (step tag + value).
+// Who quantizes h_t: with one batch row per tile, every unit tile quantizes
+// its row itself from the tagged words (one wave does it while the others
+// store the tile's share of the previous codes and form the next input
+// side); the codes for the next layer travel as tagged words too.  With 16+
+// batch rows, a few quantizing workgroups per batch slice (8 rows each, one
+// per wave; they own no units, so no gate work waits behind them) re-read
+// the tagged h words until every tag matches, quantize, store the codes with
+// device-coherent stores and then bump the slice's arrival counter, which
+// the unit tiles and the next layer wait on.
 // Between layers nothing is reused: codes go to full-length [T*B] buffers,
 // so a layer may run any number of steps ahead of the next one; a layer
-// never waits on a later layer.  Readiness: h_t travels as tagged words
-// (step tag + value) that the workgroups quantizing it re-read until every
-// tag matches.  With one batch row per tile every workgroup quantizes its row
-// itself and the codes for the next layer travel as tagged words too.  With
-// 16+ batch rows a few quantizing workgroups per batch slice (they own no
-// units, so nothing else waits behind their work) quantize h_t once, store
-// the codes with device-coherent stores and then bump the slice's arrival
-// counter, which every consumer of the codes waits on.
+// never waits on a later layer.
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
