@@ -65,7 +65,7 @@ def parse():
                     help="frames of the batch-64 workload the CPU oracle is timed on")
     ap.add_argument("--profile-target", default=None,
                     choices=["stack_b64", "stack_b1", "recurrence_b64", "recurrence_b1",
-                             "gemm8192", "copy"],
+                             "gemm8192", "lstmp_b256", "copy"],
                     help="run only one piece (for hardware-counter passes) and exit")
     return ap.parse_args()
 
@@ -277,6 +277,11 @@ def profile_target(ql, torch, target, reps):
         out["workload"] = W.name
     elif target == "gemm8192":
         out = gemm_sweep(ql, torch, 8192, reps)
+    elif target == "lstmp_b256":
+        W = wl.LSTMP4x2048P512_S16384_T800_B256
+        _, M, x = model_on_device(ql, W, torch)
+        ms, _ = time_model(ql, torch, M, x, 2, 1)
+        out = dict(workload=W.name, ms_per_step=round(ms, 3))
     else:  # a plain device copy of 1 GiB: calibrates the byte counters
         n = 1 << 28
         src = torch.ones(n, dtype=torch.float32, device="cuda")
