@@ -47,8 +47,7 @@ __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
     __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return true;
   }
-  __builtin_amdgcn_s_sleep(1);
-  return false;
+  return false;  // no sleep: every re-read is a memory round trip already
 }
 
 // Counter protocol (batched tiles): after its coherent stores of step t have
