@@ -389,25 +389,29 @@ __device__ __forceinline__ void static_for(F &&f) {
   }
 }
 
-// 16 independent reductions (max or sum) over each 32-lane half of a wave:
-// rotations within 16-lane rows, then the exchange of the two rows.
-template <bool MAX>
-__device__ __forceinline__ void half_wave_reduce16(float (&v)[16]) {
+// N independent reductions (max or sum) over each group of L lanes (32: a
+// half-wave, 16: one DPP row): rotations within 16-lane rows, then for 32
+// the exchange of the two rows.
+template <bool MAX, int L, int N>
+__device__ __forceinline__ void row_reduce(float (&v)[N]) {
+  static_assert(L == 16 || L == 32, "16 or 32 lanes");
   auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : a + b; };
   auto ror = [](float x, auto ctrl) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value,
                                                       0xf, 0xf, false));
   };
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x128>{}));
+  for (int k = 0; k < N; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x128>{}));
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x124>{}));
+  for (int k = 0; k < N; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x124>{}));
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x122>{}));
+  for (int k = 0; k < N; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x122>{}));
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x121>{}));
+  for (int k = 0; k < N; ++k) v[k] = op(v[k], ror(v[k], std::integral_constant<int, 0x121>{}));
+  if constexpr (L == 32) {
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = op(v[k], __shfl_xor(v[k], 16, 64));
+    for (int k = 0; k < N; ++k) v[k] = op(v[k], __shfl_xor(v[k], 16, 64));
+  }
 }
 
 // Recovering epilogues (eq. 1 recovery plus bias; softmax statistics or
@@ -415,7 +419,7 @@ __device__ __forceinline__ void half_wave_reduce16(float (&v)[16]) {
 // its own slab (as above), then walks them row-major with every lane owning
 // the same 4 consecutive columns of each row, so the per-column terms stay in
 // registers and every store is a 16-byte write.  The tile's per-row terms are
-// staged once.  Softmax statistics are reduced per wave over its 128 columns
+// staged once.  Softmax statistics are reduced per wave over its TN columns
 // (max, then sum of exp(y - max)) and the WN partials of a row are merged
 // with the usual rescaling.
 template <class C, int EPI>
@@ -425,9 +429,11 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
                                                      const float *rowmax, const float *rowinv,
                                                      v16i (&acc)[C::FM][C::FN]) {
   constexpr int BM = C::TBM, TM = C::TM, TN = C::TN, RS = TN + 8, WN = C::TBN / C::TN;
-  constexpr int kSlab = 8192;
-  static_assert(TN == 128, "a half-wave covers one row: 32 lanes x 4 columns");
-  static_assert(3 * BM * 4 + WN * BM * 8 <= kSlab, "row terms and partials");
+  // LPR lanes cover one row of the wave's TN columns, 4 columns each; a wave
+  // covers RPI rows per iteration, NIT iterations per 32-row chunk
+  constexpr int LPR = TN / 4, RPI = 64 / LPR, NIT = 32 / RPI;
+  static_assert(TN == 128 || TN == 64, "32 or 16 lanes per row");
+  constexpr int kSlab = (3 * BM * 4 + WN * BM * 8 + 4095) / 4096 * 4096;
   static_assert(kSlab + (C::NT / 64) * 32 * RS * 4 <= C::LDS, "LDS slabs");
   int32_t *rsig = reinterpret_cast<int32_t *>(smem);  // [BM] sigma_x
   int32_t *rzt = rsig + BM;                            // [BM] z~x
@@ -444,8 +450,8 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
     riq[r] = e.x_inv_q[m];
     fast = fast && fast_row(rzt[r]);
   }
-  // this lane's columns: n0 + wn*TN + 4*(lane & 31) + t
-  const int64_t nc = n0 + wn * TN + 4 * (lane & 31);
+  // this lane's columns: n0 + wn*TN + 4*(lane % LPR) + t
+  const int64_t nc = n0 + wn * TN + 4 * (lane % LPR);
   int32_t ztw[4], sigw[4];
   int64_t colterm[4];
   float iqw[4], bn[4];
@@ -477,9 +483,9 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
     // the slab is this wave's own: LDS keeps one wave's accesses in order
     // row `it` of this half-wave: recover, store, and hand back y
     auto row_step = [&](int it, float (&y)[4]) {
-      const int row = 2 * it + (lane >> 5), lr = wm * TM + i * 32 + row;
+      const int row = RPI * it + lane / LPR, lr = wm * TM + i * 32 + row;
       const int64_t m = m0 + lr;
-      const v4i v = *reinterpret_cast<const v4i *>(slab + row * RS + 4 * (lane & 31));
+      const v4i v = *reinterpret_cast<const v4i *>(slab + row * RS + 4 * (lane % LPR));
       const int32_t sigx = rsig[lr], ztx = rzt[lr];
       const float iqx = riq[lr];
       if (fast) {
@@ -529,37 +535,38 @@ __device__ __forceinline__ void recover_epilogue_lds(const EpiArgs &e, int64_t M
     };
     if constexpr (EPI != EPI_SMAX_STATS) {
 #pragma unroll 2
-      for (int it = 0; it < 16; ++it) {
+      for (int it = 0; it < NIT; ++it) {
         float y[4];
         row_step(it, y);
       }
     } else {
-      float ys[16][4];
+      float ys[NIT][4];
 #pragma unroll
-      for (int it = 0; it < 16; ++it) row_step(it, ys[it]);
-      // per row (one per half-wave and iteration): max over the 128 columns,
-      // then sum exp(y - max); 16 rows reduced together so the steps overlap
-      float mx[16], sm[16];
+      for (int it = 0; it < NIT; ++it) row_step(it, ys[it]);
+      // per row (one per LPR lanes and iteration): max over the wave's TN
+      // columns, then sum exp(y - max); NIT rows reduced together so the
+      // steps overlap
+      float mx[NIT], sm[NIT];
 #pragma unroll
-      for (int it = 0; it < 16; ++it) {
+      for (int it = 0; it < NIT; ++it) {
         mx[it] = -INFINITY;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
           if (nc + t < N) mx[it] = fmaxf(mx[it], ys[it][t]);
       }
-      half_wave_reduce16<true>(mx);
+      row_reduce<true, LPR>(mx);
 #pragma unroll
-      for (int it = 0; it < 16; ++it) {
+      for (int it = 0; it < NIT; ++it) {
         sm[it] = 0.0f;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
           if (nc + t < N) sm[it] += __expf(ys[it][t] - mx[it]);
       }
-      half_wave_reduce16<false>(sm);
-      if ((lane & 31) == 0) {
+      row_reduce<false, LPR>(sm);
+      if (lane % LPR == 0) {
 #pragma unroll
-        for (int it = 0; it < 16; ++it)
-          red[wn * BM + wm * TM + i * 32 + 2 * it + (lane >> 5)] = make_float2(mx[it], sm[it]);
+        for (int it = 0; it < NIT; ++it)
+          red[wn * BM + wm * TM + i * 32 + RPI * it + lane / LPR] = make_float2(mx[it], sm[it]);
       }
     }
   });
@@ -791,6 +798,12 @@ static hipError_t dispatch(const int8_t *A, int64_t lda, const int8_t *B, int64_
   // 256x256 tiles (128x128 per wave) once there are enough of them to fill
   // the chip; otherwise 128x128 tiles (64x64 per wave)
   if (big_tile_n(M, N) == 256) {
+    if constexpr (EPI != EPI_RAW) {
+      // recovering epilogues: 8 waves of 128x64 (two per SIMD, so one wave's
+      // epilogue stalls hide behind the other's work)
+      if (k128) return run<256, 256, 128, 2, 4, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
+      return run<256, 256, 64, 2, 4, 4, EPI>(A, lda, B, ldb, M, N, K, e, s);
+    }
     if (k128) return run<256, 256, 128, 2, 2, 2, EPI>(A, lda, B, ldb, M, N, K, e, s);
     return run<256, 256, 64, 2, 2, 4, EPI>(A, lda, B, ldb, M, N, K, e, s);
   }
