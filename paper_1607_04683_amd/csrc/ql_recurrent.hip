@@ -228,10 +228,9 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       // ---- 4. recover, gates, cell update; publish h_t (or m_t)
       const int64_t mcur = (t & 1) * B * H;
       const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
-      // four adjacent lanes per (b, j): lane g computes gate g (i, f, g, o);
-      // the cell update runs in the first lane of the quad
-      for (int idx = tid; idx < pairs * 4; idx += blockDim.x) {
-        const int pr = idx >> 2, gg = idx & 3;
+      // activation of gate gg of pair pr (sigmoid for i, f, o; tanh(x) =
+      // 2 sigmoid(2x) - 1 for g), with the raw accumulator tap
+      auto act = [&](int pr, int gg) {
         const int lb = pr / nu, jj = pr % nu;
         const RowParam r = rp[lb];
         const int64_t b = b0 + lb, j = j0 + jj;
@@ -242,33 +241,52 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         const float gxv = gxt ? gxt[pr * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
         const float av = gxv + yh;
         if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
-        // sigmoid for i, f, o; tanh(x) = 2 sigmoid(2x) - 1 for g
         const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
-        const float act = gg == 2 ? 2.0f * sg - 1.0f : sg;
-        // the four gates of a (b, j) pair sit in one lane quad (the loop keeps
-        // whole quads active: pairs * 4 is a multiple of 4)
-        const float ig = quad_bcast<0>(act);
-        const float fg = quad_bcast<1>(act);
-        const float gv = quad_bcast<2>(act);
-        const float og = quad_bcast<3>(act);
-        if (gg == 0) {
-          const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
-          cst[lb * tl.u + jj] = cn;
-          const float m = og * tanh_cw(cn);
-          if (NVB == 0) {
-            if (CNT)
-              st_coherent(&xhf[hcur + b * R + j], m);
-            else
-              for (int c2 = 0; c2 < tl.reph; ++c2) publish(&xh[c2 * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
-            a.h[(t * B + b) * R + j] = m;
-            if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
-          } else {
-            if (CNT)
-              st_coherent(&xmf[mcur + b * H + j], m);
-            else
-              for (int c2 = 0; c2 < tl.repm; ++c2) publish(&xm[c2 * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
+        return gg == 2 ? 2.0f * sg - 1.0f : sg;
+      };
+      // cell update and publication of pair pr
+      auto finish = [&](int pr, float ig, float fg, float gv, float og) {
+        const int lb = pr / nu, jj = pr % nu;
+        const int64_t b = b0 + lb, j = j0 + jj;
+        const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
+        cst[lb * tl.u + jj] = cn;
+        const float m = og * tanh_cw(cn);
+        if (NVB == 0) {
+          if (CNT)
+            st_coherent(&xhf[hcur + b * R + j], m);
+          else
+            for (int c2 = 0; c2 < tl.reph; ++c2) publish(&xh[c2 * tl.strideh + hcur + b * R + j], (uint32_t)(t + 1), m);
+          a.h[(t * B + b) * R + j] = m;
+          if (t == T - 1 && a.hT) a.hT[b * R + j] = m;
+        } else {
+          if (CNT)
+            st_coherent(&xmf[mcur + b * H + j], m);
+          else
+            for (int c2 = 0; c2 < tl.repm; ++c2) publish(&xm[c2 * tl.stridem + mcur + b * H + j], (uint32_t)(t + 1), m);
+        }
+        if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
+      };
+      // pairs one per lane in full rounds of the workgroup; the remainder
+      // over four lanes per pair (lane g of a quad computes gate g) when that
+      // fits, so no lane does much more than its share
+      const int nt = (int)blockDim.x, full = pairs / nt, remp = pairs % nt;
+      for (int k = 0; k < full; ++k) {
+        const int pr = k * nt + tid;
+        finish(pr, act(pr, 0), act(pr, 1), act(pr, 2), act(pr, 3));
+      }
+      if (remp > 0) {
+        const int p0 = full * nt;
+        if (4 * remp <= nt) {
+          if (tid < 4 * remp) {  // whole quads active
+            const int pr = p0 + (tid >> 2);
+            const float av = act(pr, tid & 3);
+            const float ig = quad_bcast<0>(av), fg = quad_bcast<1>(av);
+            const float gv = quad_bcast<2>(av), og = quad_bcast<3>(av);
+            if ((tid & 3) == 0) finish(pr, ig, fg, gv, og);
           }
-          if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
+        } else if (tid < remp) {
+          const int pr = p0 + tid;
+          finish(pr, act(pr, 0), act(pr, 1), act(pr, 2), act(pr, 3));
         }
       }
       // the codes of h_{t-1} become the layer's quantized output
