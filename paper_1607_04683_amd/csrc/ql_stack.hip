@@ -345,6 +345,113 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     const int Qn = (nb + 7) / 8 < tl.nq ? (nb + 7) / 8 : tl.nq;
     const int hwords = tl.ldH / 8;
     uint64_t hpre[kXPre];
+
+    // Gate work of this lane, fixed for the launch: pair (row, cell) number
+    // tid of every full round of nt pairs, then in the remainder one pair
+    // over lpp lanes (gates g0 .. g0 + ng - 1 on this lane).  Index
+    // arithmetic and the column params of the 24-bit recovery are made once
+    // here instead of at every step.
+    struct PairRec {
+      int lb, jj, sidx, cidx;  // row and cell in the tile; Sh/Sx and c index of gate 0
+      int64_t poff;            // b * H + j
+      int32_t colt[4], ztw[4];
+      float iqw[4];
+      bool cfast, valid;       // every column of the lane fits the 24-bit recovery
+    };
+    const int nt = (int)blockDim.x, pairs = nb * nu;
+    const int full = pairs / nt, rem = pairs % nt;
+    const int lpp = 4 * rem <= nt ? 4 : 2 * rem <= nt ? 2 : 1;
+    auto make_pair = [&](int pr, bool valid, int g0, int ng) {
+      PairRec p;
+      p.valid = valid;
+      const int prc = valid ? pr : 0;
+      p.lb = prc / nu;
+      p.jj = prc % nu;
+      p.sidx = p.lb * nrows + p.jj;
+      p.cidx = p.lb * tl.u + p.jj;
+      p.poff = (b0 + p.lb) * H + j0 + p.jj;
+      p.cfast = true;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p.colt[i] = 0;
+        p.ztw[i] = 0;
+        p.iqw[i] = 0.0f;
+        if (i < ng) {
+          const ColParam c = cph[(g0 + i) * tl.u + p.jj];
+          p.colt[i] = (int32_t)c.colterm;
+          p.ztw[i] = c.ztw;
+          p.iqw[i] = c.iqw;
+          p.cfast = p.cfast && (uint32_t)(c.ztw + 127) <= 255u &&
+                    (uint64_t)(c.colterm + (1 << 23)) < (uint64_t)(1 << 24);
+        }
+      }
+      return p;
+    };
+    const PairRec pf = make_pair(tid, full > 0, 0, 4);
+    const int rg0 = lpp == 4 ? (tid & 3) : lpp == 2 ? 2 * (tid & 1) : 0;
+    const PairRec prm = make_pair(full * nt + tid / lpp, rem > 0 && tid < lpp * rem, rg0, 4 / lpp);
+    // activation of gate g (slot i of the lane's columns) of pair p: the
+    // recovered recurrent product plus the recovered input side in Sx
+    auto act_b = [&](const PairRec &p, int i, int g, const RowParam &rh, bool fast) {
+      const int n = g * tl.u;
+      const int32_t S = Sh[p.sidx + n];
+      float yh;
+      if (fast) {
+        const uint32_t tt = (uint32_t)S + (uint32_t)mul_i24(rh.ztx, p.colt[i]) +
+                            (uint32_t)mul_i24(p.ztw[i], rh.sigx);
+        yh = ((float)(int32_t)tt * p.iqw[i]) * rh.iqx;
+      } else {
+        const ColParam c = cph[n + p.jj];
+        yh = recover(S, c.colterm, c.ztw, rh.ztx, rh.sigx, c.iqw, rh.iqx);
+      }
+      const float av = __int_as_float(Sx[p.sidx + n]) + yh;
+      const float sg = sigmoid_cw(g == 2 ? 2.0f * av : av);
+      return g == 2 ? 2.0f * sg - 1.0f : sg;
+    };
+    auto finish_b = [&](const PairRec &p, int64_t t, int64_t hcur, float ig, float fg, float gv,
+                        float og) {
+      const float cn = (fg * cst[p.cidx]) + (ig * gv);
+      cst[p.cidx] = cn;
+      const float m = og * tanh_cw(cn);
+      for (int c2 = 0; c2 < tl.reph; ++c2)
+        publish(&xht[c2 * tl.strideh + hcur + p.poff], (uint32_t)(t + 1), m);
+      if (Ly.h) Ly.h[t * B * H + p.poff] = m;
+    };
+    auto row_fast = [](const RowParam &rh) { return (uint32_t)(rh.ztx + 127) <= 255u; };
+    auto gates_b = [&](int64_t t, int64_t hcur) {
+      auto one_lane = [&](const PairRec &p) {
+        const RowParam rh = rph[p.lb];
+        const bool fast = p.cfast && row_fast(rh);
+        const float ig = act_b(p, 0, 0, rh, fast), fg = act_b(p, 1, 1, rh, fast);
+        const float gv = act_b(p, 2, 2, rh, fast), og = act_b(p, 3, 3, rh, fast);
+        finish_b(p, t, hcur, ig, fg, gv, og);
+      };
+      if (full > 0) one_lane(pf);
+      for (int k = 1; k < full; ++k) one_lane(make_pair(k * nt + tid, true, 0, 4));
+      if (!prm.valid) return;
+      const RowParam rh = rph[prm.lb];
+      const bool fast = prm.cfast && row_fast(rh);
+      if (lpp == 4) {
+        // whole quads are active (4 * rem lanes from lane 0)
+        const float a = act_b(prm, 0, tid & 3, rh, fast);
+        const float ig = quad_bcast<0>(a), fg = quad_bcast<1>(a);
+        const float gv = quad_bcast<2>(a), og = quad_bcast<3>(a);
+        if ((tid & 3) == 0) finish_b(prm, t, hcur, ig, fg, gv, og);
+      } else if (lpp == 2) {
+        // the even lane takes i and f, the odd one g and o; swap within the
+        // pair of lanes (quad_perm 1,0,3,2)
+        const int h2 = 2 * (tid & 1);
+        const float a0 = act_b(prm, 0, h2, rh, fast), a1 = act_b(prm, 1, h2 + 1, rh, fast);
+        const float b0v = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a0), 0xB1, 0xf, 0xf, false));
+        const float b1v = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a1), 0xB1, 0xf, 0xf, false));
+        if (h2 == 0) finish_b(prm, t, hcur, a0, a1, b0v, b1v);
+      } else {
+        const float ig = act_b(prm, 0, 0, rh, fast), fg = act_b(prm, 1, 1, rh, fast);
+        const float gv = act_b(prm, 2, 2, rh, fast), og = act_b(prm, 3, 3, rh, fast);
+        finish_b(prm, t, hcur, ig, fg, gv, og);
+      }
+    };
+
     for (int64_t t = 0; t < T; ++t) {
       const int64_t hcur = (t & 1) * B * H;
       const int64_t par = (t - 1) & 1;
@@ -411,7 +518,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       __syncthreads();
 
       // ---- 4. recover, gates, cell; publish h_t
-      gates(t, hcur);
+      gates_b(t, hcur);
       __syncthreads();  // LDS of this step is free before the next step
     }
     return;
