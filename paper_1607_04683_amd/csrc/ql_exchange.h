@@ -30,6 +30,17 @@ __device__ __forceinline__ void publish(uint64_t *p, uint32_t tag, float v) {
   __hip_atomic_store(p, ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v), __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
 }
+// The same for consumers on the producer's own XCD only: a plain store, which
+// lands in that XCD's L2 without being written through to memory.  Their
+// device-coherent loads see it there sooner (a ping-pong between two
+// workgroups of one XCD: 0.52-0.68 us a round trip against 0.83-0.95 us);
+// a consumer on another XCD might not see it before the end of the launch.
+__device__ __forceinline__ void publish_local(uint64_t *p, uint32_t tag, float v) {
+  const uint64_t w = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v);
+  // one 8-byte store without cache-policy bits (a workgroup-scope atomic
+  // store would carry sc0)
+  asm volatile("global_store_dwordx2 %0, %1, off" ::"v"(p), "v"(w) : "memory");
+}
 __device__ __forceinline__ uint64_t ld_tagged(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

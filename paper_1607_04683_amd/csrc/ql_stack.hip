@@ -39,6 +39,7 @@
 namespace ql {
 
 constexpr int kStackThreads = 512;
+constexpr int kXcds = 8;  // accelerator complex dies (XCDs) of the MI355X, each with its own L2
 // Replicas of the tagged h words at one batch row (readers spread over them).
 constexpr int kMaxReph = 2;
 
@@ -53,6 +54,7 @@ struct StackTiling {
   int ldXmax;               // largest padded input width over the launch
   int ldsW, ldsWx, ldsX, ldsXx;
   int reph;                 // replicas of the tagged h buffer (one batch row per tile)
+  int xcd;                  // one-row tiles: every layer's tiles on one XCD of its own
   int64_t strideh;          // 64-bit words between replicas
   int nw;                   // tagged code words per row: ldH / 4 codes + 3 params
   size_t hx_bytes, cx_bytes, layer_bytes;  // exchange bytes per layer
@@ -107,11 +109,28 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 
   const int64_t T = a.T, B = a.B, H = a.H;
   int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
-  const int l = blockIdx.x / tl.gl, wgi = blockIdx.x % tl.gl;
+  unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  // XCD-local layout: the launch has a workgroup for every CU; each takes the
+  // next free slot of the XCD it runs on (XCC_ID) and plays tile `slot` of
+  // layer `xcc`, so a layer's tiles share one L2 (the per-layer counters,
+  // unused at one batch row, hand out the slots); the rest leave at once.
+  int blk = (int)blockIdx.x;
+  if (tl.xcd) {
+    __shared__ int s_role;
+    if (threadIdx.x == 0) {
+      const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
+      const unsigned k = __hip_atomic_fetch_add(cnt0 + xcc * 16, 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      s_role = xcc < a.nl && k < (unsigned)tl.gl ? xcc * tl.gl + (int)k : -1;
+    }
+    __syncthreads();
+    if (s_role < 0) return;
+    blk = s_role;
+  }
+  const int l = blk / tl.gl, wgi = blk % tl.gl;
   const StackLayer &Ly = a.L[l];
   const int64_t IN = Ly.in;
   const int ldXl = (int)((IN + 63) / 64 * 64);
-  unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
   auto ctr = [&](int layer, int64_t par, int slice) {
     return cnt0 + ((layer * 2 + (int)par) * kMaxSlices + slice) * 16;
   };
@@ -120,7 +139,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   // own layer's h exchange: tagged words, replicas of [2][B][H] (one replica
   // for batched tiles, whose h is read by the designated tiles only)
   uint64_t *xht = reinterpret_cast<uint64_t *>(xdata(l));
-  const uint64_t *xht_mine = xht + (blockIdx.x % tl.reph) * tl.strideh;
+  const uint64_t *xht_mine = xht + (blk % tl.reph) * tl.strideh;
   // tagged codes of every h_t of a layer: [T*B][nw] words after its h exchange
   auto ctag = [&](int layer) {
     return reinterpret_cast<uint64_t *>(xdata(layer) + tl.hx_bytes);
@@ -302,8 +321,10 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
       cst[lb * tl.u + jj] = cn;
       const float m = og * tanh_cw(cn);
-      for (int c2 = 0; c2 < tl.reph; ++c2)
-        publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+      for (int c2 = 0; c2 < tl.reph; ++c2) {
+        if (tl.xcd) publish_local(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+        else publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
+      }
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
     };
     const int full = pairs / nt, rem = pairs % nt;
@@ -756,8 +777,10 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   const int64_t B = a.B, H = a.H;
   // workgroups per layer: at one batch row, half of the CUs' share (25 tiles
   // of 20 cells for five 500-cell layers): the per-step exchange costs less
-  // with fewer readers than the extra cells per tile cost (measured: 40%,
-  // 50%, 60% and 100% of the share give 5.80, 5.59, 5.68, 6.54 us per frame)
+  // with fewer readers than the extra cells per tile cost (measured with every
+  // layer on an XCD of its own: 20, 25, 28 and 32 tiles give 5.05, 4.88,
+  // 4.97 and 4.97 us per frame; spread over all XCDs, 40%, 50%, 60% and 100%
+  // of the share gave 5.80, 5.59, 5.68 and 6.54)
   const int G = bB == 1 ? cus / a.nl / 2 : cus / a.nl;
   tl.ldH = (int)round_up(H, 64);
   int64_t maxin = 0;
@@ -786,6 +809,13 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.gl = tl.nbt * (tl.nut + tl.nq);
   tl.grid = a.nl * tl.gl;
   if (tl.grid > cus) return false;
+  // one-row tiles: each layer on an XCD of its own when its tiles fit one
+  // (the h exchange then stays in that XCD's L2); the grid covers every CU
+  tl.xcd = 0;
+  if (bB == 1 && cus % kXcds == 0 && a.nl <= kXcds && tl.gl <= cus / kXcds) {
+    tl.xcd = 1;
+    tl.grid = cus;
+  }
   const int nrows = 4 * tl.u;
   // LDS layout
   size_t off = 0;

@@ -206,12 +206,14 @@ def test_model_empty(ql):
     assert out["post"].shape == (0, 2, 5)
 
 
-@pytest.mark.parametrize("layers,B", [(3, 5), (3, 37), (7, 1), (6, 20)])
+@pytest.mark.parametrize("layers,B", [(3, 5), (3, 37), (7, 1), (2, 1), (6, 20)])
 def test_model_layer_wavefront(ql, orc, layers, B):
     """Layers sharing one width run several per launch (a wavefront); codes of
     every layer stay bit-exact and posteriors within 1e-4.  One batch row per
     tile (tagged exchange) and 16-row tiles (counters, ragged last slice);
-    more layers than fit one launch split into several launches."""
+    more layers than fit one launch split into several launches.  At one row,
+    up to 32 tiles per layer put each layer on an XCD of its own (7 layers of
+    16 tiles); 2 layers of 48 tiles spread over all XCDs."""
     from paper_1607_04683_amd.workloads import random_model
     w = random_model(40, 48, layers, states=64, seed=layers * 100 + B)
     x = np.random.default_rng(B).standard_normal((11, B, 40)).astype(np.float32)
