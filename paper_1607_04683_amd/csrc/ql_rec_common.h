@@ -21,6 +21,18 @@ struct RowParam {
   int32_t sum;      // code sum (0..255 domain)
   int32_t pad[3];
 };
+// Row params of a row of codes (zero point z, recovery factor iq, code sum
+// over K elements) as the products need them.
+__device__ __forceinline__ RowParam row_param(int32_t z, float iq, int32_t sum, int K) {
+  RowParam q;
+  q.z = z;
+  q.ztx = z + 128;
+  q.sigx = sum - 128 * K;
+  q.iqx = iq;
+  q.sum = sum;
+  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  return q;
+}
 
 // ---------------------------------------------------------------------------
 // Per-vector quantization (eq. 2) of RB consecutive rows by one wave.

@@ -5,15 +5,19 @@
 // tile for the whole sequence, keeps the 4u gate rows of W_h' it needs
 // resident in LDS, and keeps its cell state c in LDS.  Each step:
 //   1. prefetch its slice of the precomputed W_x x_t + b;
-//   2. wait for h_{t-1} of its batch rows and quantize it per vector (eq. 2)
-//      into LDS (redundantly in every unit tile of the batch slice);
+//   2. the codes of h_{t-1} of its batch rows, quantized per vector (eq. 2):
+//      one-row tiles quantize their row themselves; in batched tiles the
+//      first ceil(rows / 8) unit tiles of a batch slice quantize 8 rows each
+//      (one per wave) into the layer's output codes and signal a counter,
+//      and every unit tile of the slice loads the codes from there;
 //   3. Mult: signed 8-bit products against the resident W_h' slice
 //      (v_dot4 for one batch row, v_mfma_i32_16x16x64_i8 for 16+ rows);
 //   4. R(.) of eq. 1/3, + (W_x x + b), sigmoid/tanh gates, c and m update;
 //   5. with a projection: wait for m_t of the batch rows of a projection
 //      tile, quantize it per vector, W_r' product, recover h_t.
-// The workgroup whose unit tile is 0 also stores the codes of h_{t-1} (the
-// next layer's / output layer's input) so they are never recomputed.
+// Those codes are the layer's quantized output (the next layer's or the
+// output layer's input), so they are never recomputed: with one row per tile
+// the workgroup whose unit tile is 0 stores them.
 //
 // There is no grid barrier.  Values passed between workgroups inside the
 // launch (h_t, and m_t with a projection) are published as 64-bit words
@@ -40,6 +44,9 @@ namespace ql {
 // 8 wavefronts per workgroup (two per SIMD): more rows / gate quads in
 // flight per step, and one wave's memory wait overlaps another's work.
 constexpr int kRecThreads = 512;
+// arrival counters [kind][parity][slice], one 64-byte line each; kinds: 0 the
+// floats of h_t, 1 those of m_t, 2 the codes of h_t (batched tiles)
+constexpr int kRecCounterBytes = 3 * 2 * kMaxSlices * 64;
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -109,7 +116,7 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   auto counter = [&](int kind, int64_t par, int slice) {
     return cnt + ((kind * 2 + (int)par) * kMaxSlices + slice) * 16;
   };
-  char *xdata = static_cast<char *>(a.ws) + kHeaderBytes + kCounterBytes;
+  char *xdata = static_cast<char *>(a.ws) + kHeaderBytes + kRecCounterBytes;
   // counter mode: h_t in xhf [2][B][R], m_t in xmf [2][B][H] (slot t & 1)
   float *xhf = reinterpret_cast<float *>(xdata);
   float *xmf = xhf + 2 * B * R;
@@ -142,6 +149,11 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   const unsigned prod_h =
       NVB == 0 ? (unsigned)tl.nut : (unsigned)(((nb + tl.bB2 - 1) / tl.bB2) * tl.npt);
   const unsigned prod_m = (unsigned)tl.nut;
+  // batched tiles: the codes of h_{t-1} are made once, by the first Qn unit
+  // tiles of the slice (groups of 8 rows, one row per wave), straight into
+  // the layer's output codes; every tile of the slice then loads them
+  const int Qn = (nb + 7) / 8 < tl.nut ? (nb + 7) / 8 : tl.nut;
+  const int wave = tid >> 6, lane = tid & 63;
   if (tid == 0) s_abort = 0;
 
   // ---- prologue: resident W_h' slice, column params, initial c
@@ -197,14 +209,60 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
                                     });
       } else if (CNT) {
         const int64_t par = (t - 1) & 1;
-        if (!wait_count(counter(0, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod_h, flag)) s_abort = 1;
+        const int64_t hrow0 = (t - 1) * B + b0;
+        if (tu < Qn) {
+          if (!wait_count(counter(0, par, tb), (unsigned)(((t - 1) >> 1) + 1) * prod_h, flag))
+            s_abort = 1;
+          __syncthreads();
+          if (s_abort) return;
+          const float *prev = xhf + par * B * R;
+          const int owords = (int)(a.ld_out / 8);
+          for (int g = tu; g * 8 < nb; g += Qn) {
+            const int lb = g * 8 + wave;
+            if (lb >= nb) continue;
+            quant_rows<NVA, 1, kSrcCoherent>(prev + (b0 + lb) * R, R, 1, 1, 0u, (int)R,
+                                             xc + lb * tl.ldsX, tl.ldsX, tl.ldR, flag, rp + lb);
+            // the wave's own LDS writes are complete in program order
+            const int64_t row = hrow0 + lb;
+            for (int wd = lane; wd < owords; wd += kWave) {
+              uint64_t v = 0;
+              if (wd * 8 < tl.ldR) v = *reinterpret_cast<const uint64_t *>(xc + lb * tl.ldsX + wd * 8);
+              st_coherent64(reinterpret_cast<uint64_t *>(a.out_codes + row * a.ld_out) + wd, v);
+            }
+            if (lane == 0) {
+              st_coherent_i(&a.out_zero[row], rp[lb].z);
+              st_coherent(&a.out_inv_q[row], rp[lb].iqx);
+              st_coherent_i(&a.out_sums[row], rp[lb].sum);
+              if (a.tap_zero) a.tap_zero[row] = rp[lb].z;
+              if (a.tap_inv_q) a.tap_inv_q[row] = rp[lb].iqx;
+            }
+            if (a.tap_codes)
+              for (int k = lane; k < (int)R; k += kWave) a.tap_codes[row * R + k] = xc[lb * tl.ldsX + k];
+          }
+          // arrival once every wave's stores have completed
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          if (tid == 0)
+            __hip_atomic_fetch_add(counter(2, par, tb), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (t == T) break;  // the codes of h_{T-1} are the output's last rows
+        if (!wait_count(counter(2, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag)) s_abort = 1;
         __syncthreads();
         if (s_abort) return;
-        const float *prev = xhf + par * B * R;
-        ok = quant_tile<NVA, RBA, kSrcCoherent>(nb, rowsA, R, 0u, (int)R, xc, tl.ldsX, tl.ldR, flag,
-                                                rp, [&](int lb) -> const void * {
-                                                  return prev + (b0 + lb) * R;
-                                                });
+        const int rwords = tl.ldR / 8;
+        for (int idx = tid; idx < rowsA * rwords; idx += blockDim.x) {
+          const int lb = idx / rwords, wd = idx % rwords;
+          uint64_t v = 0;
+          if (lb < nb)
+            v = ld_coherent64(reinterpret_cast<const uint64_t *>(a.out_codes + (hrow0 + lb) * a.ld_out) + wd);
+          *reinterpret_cast<uint64_t *>(xc + lb * tl.ldsX + wd * 8) = v;
+        }
+        for (int lb = tid; lb < rowsA; lb += blockDim.x)
+          rp[lb] = lb < nb ? row_param(ld_coherent_i(&a.out_zero[hrow0 + lb]),
+                                       ld_coherent(&a.out_inv_q[hrow0 + lb]),
+                                       ld_coherent_i(&a.out_sums[hrow0 + lb]), (int)R)
+                           : row_param(0, 0.0f, 0, (int)R);
+        ok = true;
       } else {
         const uint64_t *prev = xh_mine + ((t + 1) & 1) * B * R;
         ok = quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, R, (uint32_t)t, (int)R, xc, tl.ldsX, tl.ldR,
@@ -216,7 +274,7 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       __syncthreads();
       if (s_abort) return;
       if (t == T) {
-        if (tu == 0) store_codes(a, tl, xc, rp, nb, (T - 1) * B + b0);
+        if (!CNT && tu == 0) store_codes(a, tl, xc, rp, nb, (T - 1) * B + b0);
         break;
       }
       // ---- 3. Mult against the resident slice
@@ -289,8 +347,9 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
           finish(pr, act(pr, 0), act(pr, 1), act(pr, 2), act(pr, 3));
         }
       }
-      // the codes of h_{t-1} become the layer's quantized output
-      if (t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
+      // the codes of h_{t-1} become the layer's quantized output (batched
+      // tiles: the designated quantizers stored them already)
+      if (!CNT && t > 0 && tu == 0) store_codes(a, tl, xc, rp, nb, (t - 1) * B + b0);
       if (CNT) arrive(counter(NVB == 0 ? 0 : 1, t & 1, tb));
     }
     if (t == T) break;
@@ -385,7 +444,7 @@ static int64_t exchange_words(int64_t B, int64_t H, int64_t P) {
   const int64_t R = P > 0 ? P : H;
   int64_t n = kMaxReplicas * replica_stride(2 * B * R);  // >= the float buffers of counter mode
   if (P > 0) n += kMaxReplicas * replica_stride(2 * B * H);
-  return kCounterBytes / 8 + n;
+  return kRecCounterBytes / 8 + n;
 }
 
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P) {
@@ -572,7 +631,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
     *unsupported = true;
     return hipSuccess;
   }
-  const int64_t n64 = kCounterBytes / 8 + tl.reph * tl.strideh + tl.repm * tl.stridem;
+  const int64_t n64 = kRecCounterBytes / 8 + tl.reph * tl.strideh + tl.repm * tl.stridem;
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(a.ws),
                      n64, 0);

@@ -63,30 +63,7 @@ struct StackTiling {
       off_rowx, off_bias, lds_bytes;
 };
 
-__device__ __forceinline__ void st_coherent64(uint64_t *p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_coherent64(const uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_coherent_i(int32_t *p, int32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int32_t ld_coherent_i(const int32_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
-// Row params of x codes as the products need them.
-__device__ __forceinline__ RowParam row_param(int32_t z, float iq, int32_t sum, int K) {
-  RowParam q;
-  q.z = z;
-  q.ztx = z + 128;
-  q.sigx = sum - 128 * K;
-  q.iqx = iq;
-  q.sum = sum;
-  q.pad[0] = q.pad[1] = q.pad[2] = 0;
-  return q;
-}
 
 // RBA: rows one wave quantizes together (2 for batched tiles, 1 at one row).
 template <int NVA, bool MFA, int RBA>
