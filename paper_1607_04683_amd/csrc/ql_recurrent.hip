@@ -187,8 +187,23 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   __syncthreads();
 
   const int pairs = nb * nu;
+  const int nthr = (int)blockDim.x, fullr = pairs / nthr;
+  // Without room to stage W_x x + b in LDS, each lane's values of the first
+  // kGxPre full rounds of pairs are loaded into registers at the top of the
+  // step, so their latency passes while h_{t-1} is awaited.
+  constexpr int kGxPre = 4;
+  float gxr[kGxPre][4];
   for (int64_t t = 0; t <= T; ++t) {
     const int64_t hcur = (t & 1) * B * R;  // h_t is published here with tag t+1
+    if (CNT && activeA && tl.tc == 0 && t < T) {
+#pragma unroll
+      for (int k = 0; k < kGxPre; ++k) {
+        const int pr = k * nthr + tid, lb = pr / nu, jj = pr % nu;
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg)
+          gxr[k][gg] = k < fullr ? a.gx[(t * B + b0 + lb) * 4 * H + gg * H + j0 + jj] : 0.0f;
+      }
+    }
     if (activeA) {
       // ---- 1. every tc steps, stage W_x x + b of the next tc steps in LDS
       if (tl.tc > 0 && t < T && t % tl.tc == 0) {
@@ -249,13 +264,23 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         if (!wait_count(counter(2, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag)) s_abort = 1;
         __syncthreads();
         if (s_abort) return;
-        const int rwords = tl.ldR / 8;
-        for (int idx = tid; idx < rowsA * rwords; idx += blockDim.x) {
-          const int lb = idx / rwords, wd = idx % rwords;
-          uint64_t v = 0;
-          if (lb < nb)
-            v = ld_coherent64(reinterpret_cast<const uint64_t *>(a.out_codes + (hrow0 + lb) * a.ld_out) + wd);
-          *reinterpret_cast<uint64_t *>(xc + lb * tl.ldsX + wd * 8) = v;
+        // kLdW words per thread in flight together, then parked in LDS
+        constexpr int kLdW = 8;
+        const int rwords = tl.ldR / 8, nwords = rowsA * rwords;
+        for (int base = 0; base < nwords; base += kLdW * (int)blockDim.x) {
+          uint64_t v[kLdW];
+#pragma unroll
+          for (int i = 0; i < kLdW; ++i) {
+            const int idx = base + i * (int)blockDim.x + tid, lb = idx / rwords, wd = idx % rwords;
+            v[i] = 0;
+            if (idx < nwords && lb < nb)
+              v[i] = ld_coherent64(reinterpret_cast<const uint64_t *>(a.out_codes + (hrow0 + lb) * a.ld_out) + wd);
+          }
+#pragma unroll
+          for (int i = 0; i < kLdW; ++i) {
+            const int idx = base + i * (int)blockDim.x + tid, lb = idx / rwords, wd = idx % rwords;
+            if (idx < nwords) *reinterpret_cast<uint64_t *>(xc + lb * tl.ldsX + wd * 8) = v[i];
+          }
         }
         for (int lb = tid; lb < rowsA; lb += blockDim.x)
           rp[lb] = lb < nb ? row_param(ld_coherent_i(&a.out_zero[hrow0 + lb]),
@@ -288,7 +313,12 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
       // activation of gate gg of pair pr (sigmoid for i, f, o; tanh(x) =
       // 2 sigmoid(2x) - 1 for g), with the raw accumulator tap
-      auto act = [&](int pr, int gg) {
+      // W_x x + b of gate gg of pair pr, from the LDS staging or global memory
+      auto gx_of = [&](int pr, int gg) {
+        const int lb = pr / nu, jj = pr % nu;
+        return gxt ? gxt[pr * 4 + gg] : a.gx[(t * B + b0 + lb) * 4 * H + gg * H + j0 + jj];
+      };
+      auto act_x = [&](int pr, int gg, float gxv) {
         const int lb = pr / nu, jj = pr % nu;
         const RowParam r = rp[lb];
         const int64_t b = b0 + lb, j = j0 + jj;
@@ -296,12 +326,12 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         const ColParam c = cp[n];
         const int32_t sv = S[lb * ldS + n];
         const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
-        const float gxv = gxt ? gxt[pr * 4 + gg] : a.gx[(t * B + b) * 4 * H + gg * H + j];
         const float av = gxv + yh;
         if (a.acc_h) a.acc_h[(t * B + b) * 4 * H + gg * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
         const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
         return gg == 2 ? 2.0f * sg - 1.0f : sg;
       };
+      auto act = [&](int pr, int gg) { return act_x(pr, gg, gx_of(pr, gg)); };
       // cell update and publication of pair pr
       auto finish = [&](int pr, float ig, float fg, float gv, float og) {
         const int lb = pr / nu, jj = pr % nu;
@@ -327,10 +357,22 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       // pairs one per lane in full rounds of the workgroup; the remainder
       // over four lanes per pair (lane g of a quad computes gate g) when that
       // fits, so no lane does much more than its share
-      const int nt = (int)blockDim.x, full = pairs / nt, remp = pairs % nt;
+      const int nt = nthr, full = fullr, remp = pairs % nt;
+      const bool pre = CNT && tl.tc == 0;
       for (int k = 0; k < full; ++k) {
         const int pr = k * nt + tid;
-        finish(pr, act(pr, 0), act(pr, 1), act(pr, 2), act(pr, 3));
+        if (pre && k < kGxPre) {
+          // the round's prefetched values, picked by selects (no indexed
+          // register array)
+          float gv4[4];
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg)
+            gv4[gg] = k == 0 ? gxr[0][gg] : k == 1 ? gxr[1][gg] : k == 2 ? gxr[2][gg] : gxr[3][gg];
+          finish(pr, act_x(pr, 0, gv4[0]), act_x(pr, 1, gv4[1]), act_x(pr, 2, gv4[2]),
+                 act_x(pr, 3, gv4[3]));
+        } else {
+          finish(pr, act(pr, 0), act(pr, 1), act(pr, 2), act(pr, 3));
+        }
       }
       if (remp > 0) {
         const int p0 = full * nt;
