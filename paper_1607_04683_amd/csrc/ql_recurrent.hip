@@ -45,8 +45,9 @@ namespace ql {
 // flight per step, and one wave's memory wait overlaps another's work.
 constexpr int kRecThreads = 512;
 // arrival counters [kind][parity][slice], one 64-byte line each; kinds: 0 the
-// floats of h_t, 1 those of m_t, 2 the codes of h_t (batched tiles)
-constexpr int kRecCounterBytes = 3 * 2 * kMaxSlices * 64;
+// floats of h_t, 1 those of m_t, 2 the codes of h_t, 3 the codes of m_t
+// (batched tiles)
+constexpr int kRecCounterBytes = 4 * 2 * kMaxSlices * 64;
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -62,6 +63,8 @@ struct RecTiling {
   int tc;           // steps of W_x x + b staged in LDS at a time (0: none)
   int64_t strideh, stridem;  // 64-bit words between replicas
   size_t off_w, off_x, off_s, off_c, off_col, off_row, off_gx, lds_bytes;
+  size_t off_mc;    // workspace bytes before the codes of m_t (batched tiles, projection)
+  size_t mc_zoff, mc_poff;  // from there: bytes to the zero points, between param arrays
 };
 
 // Store the codes of h_{t-1} (held in LDS) and their params as the layer's
@@ -404,14 +407,68 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       __syncthreads();  // LDS codes / params of phase 4 are no longer read
       bool ok;
       if (CNT) {
-        if (!wait_count(counter(1, t & 1, tbB), (unsigned)((t >> 1) + 1) * prod_m, flag)) s_abort = 1;
+        // the codes of m_t are made once per projection slice, by its first
+        // QnB tiles (8 rows each, one per wave), into a double buffer of the
+        // workspace; every projection tile of the slice loads them
+        const int QnB = (nb2 + 7) / 8 < tl.npt ? (nb2 + 7) / 8 : tl.npt;
+        const int64_t par = t & 1;
+        char *mbase = static_cast<char *>(a.ws) + tl.off_mc;
+        int8_t *mcodes = reinterpret_cast<int8_t *>(mbase) + par * B * tl.ldH;
+        const size_t zoff = tl.mc_zoff, poff = tl.mc_poff;
+        int32_t *mz = reinterpret_cast<int32_t *>(mbase + zoff) + par * B;
+        float *miq = reinterpret_cast<float *>(mbase + zoff + poff) + par * B;
+        int32_t *msum = reinterpret_cast<int32_t *>(mbase + zoff + 2 * poff) + par * B;
+        if (tp < QnB) {
+          if (!wait_count(counter(1, par, tbB), (unsigned)((t >> 1) + 1) * prod_m, flag)) s_abort = 1;
+          __syncthreads();
+          if (s_abort) return;
+          const float *mf = xmf + par * B * H;
+          const int mwords = tl.ldH / 8;
+          for (int g = tp; g * 8 < nb2; g += QnB) {
+            const int lb = g * 8 + wave;
+            if (lb >= nb2) continue;
+            quant_rows<NVB, 1, kSrcCoherent>(mf + (c0 + lb) * H, H, 1, 1, 0u, (int)H,
+                                             xc + lb * ldx2, ldx2, tl.ldH, flag, rp + lb);
+            const int64_t row = c0 + lb;
+            for (int wd = lane; wd < mwords; wd += kWave)
+              st_coherent64(reinterpret_cast<uint64_t *>(mcodes + row * tl.ldH) + wd,
+                            *reinterpret_cast<const uint64_t *>(xc + lb * ldx2 + wd * 8));
+            if (lane == 0) {
+              st_coherent_i(&mz[row], rp[lb].z);
+              st_coherent(&miq[row], rp[lb].iqx);
+              st_coherent_i(&msum[row], rp[lb].sum);
+            }
+          }
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          if (tid == 0)
+            __hip_atomic_fetch_add(counter(3, par, tb2), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (!wait_count(counter(3, par, tb2), (unsigned)((t >> 1) + 1) * QnB, flag)) s_abort = 1;
         __syncthreads();
         if (s_abort) return;
-        const float *mf = xmf + (t & 1) * B * H;
-        ok = quant_tile<NVB, RBB, kSrcCoherent>(nb2, rowsB, H, 0u, (int)H, xc, ldx2, tl.ldH, flag, rp,
-                                                [&](int lb) -> const void * {
-                                                  return mf + (c0 + lb) * H;
-                                                });
+        constexpr int kLdW = 8;
+        const int mwords = tl.ldH / 8, nwords = rowsB * mwords;
+        for (int base = 0; base < nwords; base += kLdW * (int)blockDim.x) {
+          uint64_t v[kLdW];
+#pragma unroll
+          for (int i = 0; i < kLdW; ++i) {
+            const int idx = base + i * (int)blockDim.x + tid, lb = idx / mwords, wd = idx % mwords;
+            v[i] = 0;
+            if (idx < nwords && lb < nb2)
+              v[i] = ld_coherent64(reinterpret_cast<const uint64_t *>(mcodes + (c0 + lb) * tl.ldH) + wd);
+          }
+#pragma unroll
+          for (int i = 0; i < kLdW; ++i) {
+            const int idx = base + i * (int)blockDim.x + tid, lb = idx / mwords, wd = idx % mwords;
+            if (idx < nwords) *reinterpret_cast<uint64_t *>(xc + lb * ldx2 + wd * 8) = v[i];
+          }
+        }
+        for (int lb = tid; lb < rowsB; lb += blockDim.x)
+          rp[lb] = lb < nb2 ? row_param(ld_coherent_i(&mz[c0 + lb]), ld_coherent(&miq[c0 + lb]),
+                                        ld_coherent_i(&msum[c0 + lb]), (int)H)
+                            : row_param(0, 0.0f, 0, (int)H);
+        ok = true;
       } else {
         ok = quant_tile<NVB, RBB, kSrcTagged>(nb2, rowsB, H, (uint32_t)(t + 1), (int)H, xc, ldx2,
                                               tl.ldH, flag, rp, [&](int lb) -> const void * {
@@ -489,8 +546,16 @@ static int64_t exchange_words(int64_t B, int64_t H, int64_t P) {
   return kRecCounterBytes / 8 + n;
 }
 
+// Codes of m_t made once per projection slice (batched tiles): [2][B][ldH]
+// bytes, then zero points, recovery factors and code sums, [2][B] each.
+static size_t mcode_bytes(int64_t B, int64_t H, int64_t P) {
+  if (P <= 0) return 0;
+  return align_up((size_t)2 * B * round_up(H, 64), 256) + 3 * align_up((size_t)2 * B * 4, 256);
+}
+
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P) {
-  return kHeaderBytes + align_up((size_t)exchange_words(B, H, P) * sizeof(uint64_t), 256);
+  return kHeaderBytes + align_up((size_t)exchange_words(B, H, P) * sizeof(uint64_t), 256) +
+         mcode_bytes(B, H, P);
 }
 
 static int replicas(int values_per_block, int consumers) {
@@ -581,7 +646,7 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
     tl.strideh = replica_stride(2 * B * a.R);
     tl.stridem = P > 0 ? replica_stride(2 * B * H) : 0;
   }
-  if (tl.nbt > kMaxSlices) return false;
+  if (tl.nbt > kMaxSlices || (P > 0 && tl.nbt2 > kMaxSlices)) return false;
   tl.grid = tl.nbt * tl.nut;
   if (P > 0 && tl.nbt2 * tl.npt > tl.grid) tl.grid = tl.nbt2 * tl.npt;
   if (tl.grid > G) return false;
@@ -679,6 +744,9 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
                      n64, 0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  tl.off_mc = kHeaderBytes + align_up((size_t)exchange_words(a.B, a.H, a.P) * sizeof(uint64_t), 256);
+  tl.mc_zoff = align_up((size_t)2 * a.B * tl.ldH, 256);
+  tl.mc_poff = align_up((size_t)2 * a.B * 4, 256);
   RecurrentArgs args = a;
   void *kargs[] = {&args, &tl};
   return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid), dim3(kRecThreads),
