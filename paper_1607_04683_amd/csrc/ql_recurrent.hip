@@ -94,6 +94,71 @@ __device__ __forceinline__ void store_codes(const RecurrentArgs &a, const RecTil
     }
 }
 
+// Quantizes one row of K <= 4 * blockDim floats (eq. 2) with the whole
+// workgroup: thread i takes elements 4i .. 4i+3 (device-coherent loads), the
+// min/max and the code sum are reduced within each wave and then across the
+// waves through red (16 + waves ints of LDS).  The four codes of a thread go
+// out as one device-coherent 32-bit store (device layout, zero from K up to
+// ldk), the row params to zp / iqp / sump with device-coherent stores, and,
+// when tap is not null, the codes also to tap[0, K) and the params to
+// tap_z / tap_iq.  Every thread calls it; it ends with a workgroup barrier.
+__device__ __forceinline__ void quant_row_wg(const float *src, int K, int ldk, int8_t *dst,
+                                             int32_t *zp, float *iqp, int32_t *sump, int *red,
+                                             int8_t *tap, int32_t *tap_z, float *tap_iq) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
+  const int k0 = 4 * tid;
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = k0 + e < K ? ld_coherent(src + k0 + e) : 0.0f;
+  int mm[2] = {0x7fffffff, 0x7fffffff};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int key = float_key(v[e]);
+    if (k0 + e < K) {
+      mm[0] = min(mm[0], key);
+      mm[1] = min(mm[1], ~key);
+    }
+  }
+  wave_min_n<2>(mm);
+  if (lane == 0) {
+    red[2 * wave] = mm[0];
+    red[2 * wave + 1] = mm[1];
+  }
+  __syncthreads();
+  int lo = red[0], hi = red[1];
+  for (int w = 1; w < nwave; ++w) {
+    lo = min(lo, red[2 * w]);
+    hi = min(hi, red[2 * w + 1]);
+  }
+  const QParams prm = make_qparams(key_float(lo), key_float(~hi));
+  int sum = 0;
+  uint32_t word = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool ok = k0 + e < K;
+    const int code = encode(v[e], prm.q, prm.z);
+    sum += ok ? code : 0;
+    word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
+    if (tap && ok) tap[k0 + e] = (int8_t)(code ^ 0x80);
+  }
+  for (int k = k0; k < ldk; k += 4 * (int)blockDim.x)
+    __hip_atomic_store(reinterpret_cast<uint32_t *>(dst + k), k == k0 ? word : 0u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  int s1[1] = {sum};
+  wave_add_n<1>(s1);
+  if (lane == 0) red[16 + wave] = s1[0];
+  __syncthreads();
+  if (tid == 0) {
+    int total = 0;
+    for (int w = 0; w < nwave; ++w) total += red[16 + w];
+    st_coherent_i(zp, prm.z);
+    st_coherent(iqp, prm.inv_q);
+    st_coherent_i(sump, total);
+    if (tap_z) *tap_z = prm.z;
+    if (tap_iq) *tap_iq = prm.inv_q;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // The persistent kernel.  NVA / NVB: values per lane of an h / m row (8 for
 // widths <= 512, 32 for <= 2048; NVB = 0 without projection); MFA / MFB: MFMA
@@ -110,6 +175,7 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_row);
   float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);  // [tc][pairs][4]
   __shared__ int s_abort;
+  __shared__ int s_red[32];
 
   const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
   int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
@@ -407,10 +473,11 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       __syncthreads();  // LDS codes / params of phase 4 are no longer read
       bool ok;
       if (CNT) {
-        // the codes of m_t are made once per projection slice, by its first
-        // QnB tiles (8 rows each, one per wave), into a double buffer of the
-        // workspace; every projection tile of the slice loads them
-        const int QnB = (nb2 + 7) / 8 < tl.npt ? (nb2 + 7) / 8 : tl.npt;
+        // the codes of m_t are made once per projection slice, its rows
+        // spread over its projection tiles (rows tp, tp + npt, ...; the whole
+        // workgroup per row), into a double buffer of the workspace; every
+        // projection tile of the slice loads them
+        const int QnB = nb2 < tl.npt ? nb2 : tl.npt;
         const int64_t par = t & 1;
         char *mbase = static_cast<char *>(a.ws) + tl.off_mc;
         int8_t *mcodes = reinterpret_cast<int8_t *>(mbase) + par * B * tl.ldH;
@@ -418,26 +485,15 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         int32_t *mz = reinterpret_cast<int32_t *>(mbase + zoff) + par * B;
         float *miq = reinterpret_cast<float *>(mbase + zoff + poff) + par * B;
         int32_t *msum = reinterpret_cast<int32_t *>(mbase + zoff + 2 * poff) + par * B;
-        if (tp < QnB) {
+        if (tp < nb2) {
           if (!wait_count(counter(1, par, tbB), (unsigned)((t >> 1) + 1) * prod_m, flag)) s_abort = 1;
           __syncthreads();
           if (s_abort) return;
           const float *mf = xmf + par * B * H;
-          const int mwords = tl.ldH / 8;
-          for (int g = tp; g * 8 < nb2; g += QnB) {
-            const int lb = g * 8 + wave;
-            if (lb >= nb2) continue;
-            quant_rows<NVB, 1, kSrcCoherent>(mf + (c0 + lb) * H, H, 1, 1, 0u, (int)H,
-                                             xc + lb * ldx2, ldx2, tl.ldH, flag, rp + lb);
+          for (int lb = tp; lb < nb2; lb += tl.npt) {
             const int64_t row = c0 + lb;
-            for (int wd = lane; wd < mwords; wd += kWave)
-              st_coherent64(reinterpret_cast<uint64_t *>(mcodes + row * tl.ldH) + wd,
-                            *reinterpret_cast<const uint64_t *>(xc + lb * ldx2 + wd * 8));
-            if (lane == 0) {
-              st_coherent_i(&mz[row], rp[lb].z);
-              st_coherent(&miq[row], rp[lb].iqx);
-              st_coherent_i(&msum[row], rp[lb].sum);
-            }
+            quant_row_wg(mf + row * H, (int)H, tl.ldH, mcodes + row * tl.ldH, &mz[row], &miq[row],
+                         &msum[row], s_red, nullptr, nullptr, nullptr);
           }
           __builtin_amdgcn_s_waitcnt(0);
           __syncthreads();
