@@ -48,6 +48,9 @@ constexpr int kRecThreads = 512;
 // floats of h_t, 1 those of m_t, 2 the codes of h_t, 3 the codes of m_t
 // (batched tiles)
 constexpr int kRecCounterBytes = 4 * 2 * kMaxSlices * 64;
+// W_r' fragments (16 bytes per lane each) a lane may hold for the projection:
+// up to 2 output tiles of 16 x up to 4 K steps of 64 bytes
+constexpr int kWrTiles = 2, kWrSteps = 4;
 
 struct RecTiling {
   int bB, u;        // phase A tile: batch rows x units
@@ -61,6 +64,7 @@ struct RecTiling {
   int ldsX;         // LDS row stride of activation codes
   int reph, repm;   // replicas of the published h / m double buffers
   int tc;           // steps of W_x x + b staged in LDS at a time (0: none)
+  int wres;         // projection: W_r' fragments resident in registers, K split over the waves
   int64_t strideh, stridem;  // 64-bit words between replicas
   size_t off_w, off_x, off_s, off_c, off_col, off_row, off_gx, lds_bytes;
   size_t off_mc;    // workspace bytes before the codes of m_t (batched tiles, projection)
@@ -255,6 +259,24 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   }
   __syncthreads();
 
+  // resident W_r' slice: fragment [tj][ks] of this wave covers output tile tj
+  // and K step ks of the wave's share of K (ldH / 8 bytes)
+  v4i wfr[kWrTiles][kWrSteps];
+  const int ksw = tl.ldH / 512, ntw = tl.p2 / 16, kwave = (tid >> 6) * (tl.ldH / 8);
+  if (NVB > 0 && MFB && activeB && tl.wres) {
+#pragma unroll
+    for (int tj = 0; tj < kWrTiles; ++tj)
+#pragma unroll
+      for (int ks = 0; ks < kWrSteps; ++ks) {
+        wfr[tj][ks] = v4i{};
+        if (tj < ntw && ks < ksw) {
+          const int wrow = tj * 16 + (tid & 15);
+          const int64_t rr = p0 + (wrow < np2 ? wrow : np2 - 1);
+          wfr[tj][ks] = *reinterpret_cast<const v4i *>(a.Wr.codes + rr * a.Wr.ld + kwave + ks * 64 +
+                                                       ((tid & 63) >> 4) * 16);
+        }
+      }
+  }
   const int pairs = nb * nu;
   const int nthr = (int)blockDim.x, fullr = pairs / nthr;
   // Without room to stage W_x x + b in LDS, each lane's values of the first
@@ -536,7 +558,35 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       if (s_abort) return;
       // W_r' rows p0 .. p0 + np2 - 1, read from global memory (L2 resident)
       const int8_t *wr = a.Wr.codes + p0 * a.Wr.ld;
-      if (MFB)
+      if (MFB && tl.wres) {
+        // this wave's share of K against the resident fragments; partial
+        // sums of wave w in S[(w * 16 + row) * p2 + col], then summed into
+        // slot 0 (integer sums: the order does not matter)
+        const int lane = tid & 63, wv = tid >> 6;
+        const int8_t *xr = xc + (lane & 15) * ldx2 + kwave + (lane >> 4) * 16;
+        v4i acc[kWrTiles] = {v4i{}, v4i{}};
+#pragma unroll
+        for (int ks = 0; ks < kWrSteps; ++ks) {
+          if (ks >= ksw) break;
+          const v4i av = *reinterpret_cast<const v4i *>(xr + ks * 64);
+#pragma unroll
+          for (int tj = 0; tj < kWrTiles; ++tj)
+            if (tj < ntw) acc[tj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, wfr[tj][ks], acc[tj], 0, 0, 0);
+        }
+#pragma unroll
+        for (int tj = 0; tj < kWrTiles; ++tj)
+          if (tj < ntw)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              S[(wv * 16 + (lane >> 4) * 4 + r) * tl.p2 + tj * 16 + (lane & 15)] = acc[tj][r];
+        __syncthreads();
+        const int nwv = (int)blockDim.x >> 6;
+        for (int idx = tid; idx < 16 * tl.p2; idx += blockDim.x) {
+          int sum = S[idx];
+          for (int w = 1; w < nwv; ++w) sum += S[w * 16 * tl.p2 + idx];
+          S[idx] = sum;
+        }
+      } else if (MFB)
         products_mfma(xc, ldx2, tl.bB2, wr, a.Wr.ld, tl.p2, np2, tl.ldH, S, tl.p2);
       else
         products_valu(xc, ldx2, nb2, wr, a.Wr.ld, tl.p2, np2, tl.ldH, S, tl.p2);
@@ -718,6 +768,15 @@ static bool plan(const RecurrentArgs &a, int cus, int lds_max, RecTiling *out) {
   if (P > 0) {
     const size_t sb2 = (size_t)tl.bB2 * tl.p2 * 4;
     sbytes = sbytes > sb2 ? sbytes : sb2;
+  }
+  // 16-row projection tiles whose W_r' slice fits kWrTiles x kWrSteps
+  // fragments per lane when K is split over the eight waves: the slice stays
+  // in registers and the waves' partial products are summed through LDS
+  tl.wres = P > 0 && tl.mfmaB && tl.bB2 == 16 && tl.p2 % 16 == 0 && tl.p2 / 16 <= kWrTiles &&
+            tl.ldH % 512 == 0 && tl.ldH / 512 <= kWrSteps;
+  if (tl.wres) {
+    const size_t sb3 = (size_t)(kRecThreads / 64) * 16 * tl.p2 * 4;
+    sbytes = sbytes > sb3 ? sbytes : sb3;
   }
   size_t off = 0;
   tl.off_w = off;

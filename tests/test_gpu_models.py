@@ -75,7 +75,8 @@ def test_lstm_layer_500_cells_T300_B1(ql, orc):
 @pytest.mark.parametrize("n_in,H,P,T,B", [(50, 37, 0, 13, 1), (50, 37, 0, 13, 3),
                                           (64, 40, 0, 9, 20), (33, 64, 24, 9, 2),
                                           (33, 64, 24, 9, 17), (33, 64, 24, 9, 45),
-                                          (40, 96, 32, 7, 100), (130, 129, 0, 5, 64)])
+                                          (40, 96, 32, 7, 100), (64, 512, 32, 6, 40),
+                                          (48, 1024, 48, 5, 24), (130, 129, 0, 5, 64)])
 def test_lstm_layer_shapes(ql, orc, n_in, H, P, T, B):
     g, o = _layer_case(ql, orc, n_in, H, P, T, B, seed=n_in + H + P + T + B)
     _assert_layer(g, o, P)
