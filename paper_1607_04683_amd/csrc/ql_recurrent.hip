@@ -279,6 +279,26 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
   }
   const int pairs = nb * nu;
   const int nthr = (int)blockDim.x, fullr = pairs / nthr;
+  // Batched tiles whose cell count divides the workgroup: a lane's cell is
+  // the same in every full round of pairs (rows lbL, lbL + dlb, ...), so the
+  // column params of its four gates, and whether they allow the 24-bit
+  // recovery, are read once here.
+  const bool cfix = CNT && activeA && nu > 0 && nthr % nu == 0;
+  const int jjL = cfix ? tid % nu : 0, lbL = cfix ? tid / nu : 0, dlb = cfix ? nthr / nu : 0;
+  int32_t fcol[4] = {0, 0, 0, 0}, fztw[4] = {0, 0, 0, 0};
+  float fiqw[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  bool fcf = cfix;
+  if (cfix) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const ColParam c = cp[g * tl.u + jjL];
+      fcol[g] = (int32_t)c.colterm;
+      fztw[g] = c.ztw;
+      fiqw[g] = c.iqw;
+      fcf = fcf && (uint32_t)(c.ztw + 127) <= 255u &&
+            (uint64_t)(c.colterm + (1 << 23)) < (uint64_t)(1 << 24);
+    }
+  }
   // Without room to stage W_x x + b in LDS, each lane's values of the first
   // kGxPre full rounds of pairs are loaded into registers at the top of the
   // step, so their latency passes while h_{t-1} is awaited.
@@ -402,13 +422,13 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       // ---- 4. recover, gates, cell update; publish h_t (or m_t)
       const int64_t mcur = (t & 1) * B * H;
       const float *gxt = tl.tc > 0 ? gxs + (t % tl.tc) * pairs * 4 : nullptr;
-      // activation of gate gg of pair pr (sigmoid for i, f, o; tanh(x) =
-      // 2 sigmoid(2x) - 1 for g), with the raw accumulator tap
       // W_x x + b of gate gg of pair pr, from the LDS staging or global memory
       auto gx_of = [&](int pr, int gg) {
         const int lb = pr / nu, jj = pr % nu;
         return gxt ? gxt[pr * 4 + gg] : a.gx[(t * B + b0 + lb) * 4 * H + gg * H + j0 + jj];
       };
+      // activation of gate gg of pair pr (sigmoid for i, f, o; tanh(x) =
+      // 2 sigmoid(2x) - 1 for g), with the raw accumulator tap
       auto act_x = [&](int pr, int gg, float gxv) {
         const int lb = pr / nu, jj = pr % nu;
         const RowParam r = rp[lb];
@@ -423,9 +443,8 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         return gg == 2 ? 2.0f * sg - 1.0f : sg;
       };
       auto act = [&](int pr, int gg) { return act_x(pr, gg, gx_of(pr, gg)); };
-      // cell update and publication of pair pr
-      auto finish = [&](int pr, float ig, float fg, float gv, float og) {
-        const int lb = pr / nu, jj = pr % nu;
+      // cell update and publication of pair (lb, jj)
+      auto finish_lj = [&](int lb, int jj, float ig, float fg, float gv, float og) {
         const int64_t b = b0 + lb, j = j0 + jj;
         const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
         cst[lb * tl.u + jj] = cn;
@@ -445,11 +464,44 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         }
         if (t == T - 1 && a.cT) a.cT[b * H + j] = cn;
       };
+      auto finish = [&](int pr, float ig, float fg, float gv, float og) {
+        finish_lj(pr / nu, pr % nu, ig, fg, gv, og);
+      };
       // pairs one per lane in full rounds of the workgroup; the remainder
       // over four lanes per pair (lane g of a quad computes gate g) when that
       // fits, so no lane does much more than its share
       const int nt = nthr, full = fullr, remp = pairs % nt;
       const bool pre = CNT && tl.tc == 0;
+      if (cfix && !a.acc_h) {
+        // fixed cell per lane: column params from registers, one decision
+        // per pair for the 24-bit recovery (the same values as recover())
+        for (int k = 0; k < full; ++k) {
+          const int pr = k * nt + tid, lb = lbL + k * dlb;
+          const RowParam r = rp[lb];
+          const bool fast = fcf && (uint32_t)(r.ztx + 127) <= 255u;
+          float av4[4];
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg) {
+            const float gxv = pre && k < kGxPre
+                                  ? (k == 0 ? gxr[0][gg] : k == 1 ? gxr[1][gg] : k == 2 ? gxr[2][gg] : gxr[3][gg])
+                                  : gx_of(pr, gg);
+            const int32_t sv = S[lb * ldS + gg * tl.u + jjL];
+            float yh;
+            if (fast) {
+              const uint32_t tt = (uint32_t)sv + (uint32_t)mul_i24(r.ztx, fcol[gg]) +
+                                  (uint32_t)mul_i24(fztw[gg], r.sigx);
+              yh = ((float)(int32_t)tt * fiqw[gg]) * r.iqx;
+            } else {
+              const ColParam c = cp[gg * tl.u + jjL];
+              yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
+            }
+            const float av = gxv + yh;
+            const float sg = sigmoid_cw(gg == 2 ? 2.0f * av : av);
+            av4[gg] = gg == 2 ? 2.0f * sg - 1.0f : sg;
+          }
+          finish_lj(lb, jjL, av4[0], av4[1], av4[2], av4[3]);
+        }
+      } else
       for (int k = 0; k < full; ++k) {
         const int pr = k * nt + tid;
         if (pre && k < kGxPre) {
