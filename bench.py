@@ -34,10 +34,10 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=4.487e9, read=3.011e9, written=1.476e9,
+TRAFFIC = dict(bytes=4.48e+09, read=3.004e+09, written=1.476e+09,
                sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
                         "ql_launch.h"),
-               sha256="2f6d8c8ad5c9cac8d698c863b04c5499f68554e312e51dfcd40149b5687fb2e6",
+               sha256="38989d930b3bd3acfcb74be7e60bb542bdb6057df8989c0da6e66bdc48270ff2",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 
