@@ -57,7 +57,15 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
   const int lane = threadIdx.x & 63;
   float v[RB][NV];
   if (MODE == kSrcTagged) {
+    // a word is re-read only until its tag has matched once (bit r*NV + i
+    // of `got`), so later polls touch only what is still missing
+    static_assert(RB * NV <= 32, "one bit per value of the lane");
     const uint64_t *base = static_cast<const uint64_t *>(src);
+    uint32_t got = 0;
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int i = 0; i < NV; ++i) v[r][i] = 0.0f;
     long it = 0;
     for (;;) {
       uint32_t bad = 0;
@@ -68,13 +76,16 @@ __device__ __forceinline__ bool quant_rows(const void *src, int64_t stride, int 
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int k = 4 * (c * kWave + lane) + e;
-            float x = 0.0f;
-            if (r < nvalid && k < K) {
+            const uint32_t bit = 1u << (r * NV + 4 * c + e);
+            if (r < nvalid && k < K && !(got & bit)) {
               const uint64_t w = ld_tagged(base + r * stride + k);
-              bad |= (uint32_t)(w >> 32) ^ tag;
-              x = __uint_as_float((uint32_t)w);
+              if ((uint32_t)(w >> 32) == tag) {
+                got |= bit;
+                v[r][4 * c + e] = __uint_as_float((uint32_t)w);
+              } else {
+                bad = 1;
+              }
             }
-            v[r][4 * c + e] = x;
           }
       if (!__any(bad != 0)) break;
       if (wait_expired(flag, it)) return false;
