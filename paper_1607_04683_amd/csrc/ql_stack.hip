@@ -65,6 +65,81 @@ struct StackTiling {
 
 
 
+// One row of K <= 512 published values (tagged words of step tag `tag`)
+// quantized per vector (eq. 2) by waves 0 and 1 together: wave w polls and
+// encodes half w of the row (lane l: elements 4 (w*64 + l) .. +3), and the
+// halves' min/max, then their code sums, meet in LDS slots xch[w*8 ..] (data,
+// then a flag holding the tag, released after the data).  The codes go to
+// dst (ldpad <= 512 bytes), the row params to *rp.  False if a wait expired.
+__device__ __forceinline__ bool quant_row_2w(const uint64_t *src, uint32_t tag, int K,
+                                             int8_t *dst, int ldpad, int *flag, RowParam *rp,
+                                             int *xch) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, o = 1 - w;
+  const int kb = 4 * (w * kWave + lane);
+  float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  uint32_t got = 0;
+  long it = 0;
+  for (;;) {
+    uint32_t bad = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (kb + e < K && !(got & (1u << e))) {
+        const uint64_t wd = ld_tagged(src + kb + e);
+        if ((uint32_t)(wd >> 32) == tag) {
+          got |= 1u << e;
+          v[e] = __uint_as_float((uint32_t)wd);
+        } else {
+          bad = 1;
+        }
+      }
+    if (!__any(bad != 0)) break;
+    if (wait_expired(flag, it)) return false;
+  }
+  int mm[2] = {0x7fffffff, 0x7fffffff};
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (kb + e < K) {
+      const int key = float_key(v[e]);
+      mm[0] = min(mm[0], key);
+      mm[1] = min(mm[1], ~key);
+    }
+  wave_min_n<2>(mm);
+  if (lane == 0) {
+    xch[w * 8 + 0] = mm[0];
+    xch[w * 8 + 1] = mm[1];
+    __hip_atomic_store(&xch[w * 8 + 2], (int)tag, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  it = 0;
+  while (__hip_atomic_load(&xch[o * 8 + 2], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != (int)tag)
+    if (wait_expired(flag, it)) return false;
+  const int lo = min(mm[0], xch[o * 8 + 0]), hi = min(mm[1], xch[o * 8 + 1]);
+  const QParams prm = make_qparams(key_float(lo), key_float(~hi));
+  int sum = 0;
+  uint32_t word = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool ok = kb + e < K;
+    const int code = encode(v[e], prm.q, prm.z);
+    sum += ok ? code : 0;
+    word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
+  }
+  if (kb < ldpad) reinterpret_cast<uint32_t *>(dst)[kb / 4] = word;
+  int s1[1] = {sum};
+  wave_add_n<1>(s1);
+  if (w == 1) {
+    if (lane == 0) {
+      xch[8 + 3] = s1[0];
+      __hip_atomic_store(&xch[8 + 4], (int)tag, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    return true;
+  }
+  it = 0;
+  while (__hip_atomic_load(&xch[8 + 4], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != (int)tag)
+    if (wait_expired(flag, it)) return false;
+  if (lane == 0) *rp = row_param(prm.z, prm.inv_q, s1[0] + xch[8 + 3], K);
+  return true;
+}
+
 // RBA: rows one wave quantizes together (2 for batched tiles, 1 at one row).
 template <int NVA, bool MFA, int RBA>
 __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTiling tl) {
@@ -82,6 +157,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   RowParam *rpx = reinterpret_cast<RowParam *>(smem + tl.off_rowx);
   float *bsl = reinterpret_cast<float *>(smem + tl.off_bias);
   __shared__ int s_abort;
+  __shared__ int s_xch[16];  // one-row tiles: the two quantizing waves' exchange
   constexpr bool CNT = MFA;  // batched tiles: counters + coherent data; else tagged words
 
   const int64_t T = a.T, B = a.B, H = a.H;
@@ -618,15 +694,15 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
   };
 
-  // Input side of step t for waves 1..: the codes of x_t straight into
+  // Input side of step t for waves 2..: the codes of x_t straight into
   // registers (plain input, or layer l-1's tagged words re-read until their
   // tags match), their products against the resident W_x' slice into Sx,
   // and the row params into rpx; no workgroup barrier inside.  False if a
   // wait expired.  One batch row; its ld of at most 512 codes is two 16-byte
   // chunks per lane of a 16-lane group.
   auto input_side_async = [&](int64_t t) -> bool {
-    const int gt = tid - kWave, grp = gt >> 4, gl = gt & 15;
-    const int ngrp = ((int)blockDim.x - kWave) >> 4;
+    const int gt = tid - 2 * kWave, grp = gt >> 4, gl = gt & 15;
+    const int ngrp = ((int)blockDim.x - 2 * kWave) >> 4;
     const int64_t xrow = t * B + b0;
     v4i xa[2] = {v4i{}, v4i{}};
     bool ok = true;
@@ -700,11 +776,12 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   };
 
   // Per step: the recurrent product and the gates (all waves); then, while
-  // h_t travels, wave 0 quantizes h_t into the other buffer of codes and the
-  // other waves share the codes of h_{t-1} and form the input side of step
-  // t+1.
+  // h_t travels, waves 0 and 1 quantize h_t into the other buffer of codes
+  // and the other waves share the codes of h_{t-1} and form the input side of
+  // step t+1.
   int8_t *const xhb[2] = {xh, reinterpret_cast<int8_t *>(smem + tl.off_xh2)};
   RowParam *const rphb[2] = {rph, reinterpret_cast<RowParam *>(smem + tl.off_rowh2)};
+  if (tid < 16) s_xch[tid] = 0;  // flags hold step tags, which start at 1
   if (T > 0 && !input_side(0)) return;
   if (!quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
                                        [&](int) -> const void * { return nullptr; }))
@@ -724,18 +801,15 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     gates(t, hcur);
     __syncthreads();  // Sx and Sh are free
 
-    // ---- 3. while h_t travels: its codes (wave 0); the share of the codes
+    // ---- 3. while h_t travels: its codes (waves 0, 1); the share of the codes
     // of h_{t-1} and the input side of step t+1 (the other waves)
-    if (wave == 0) {
+    if (wave < 2) {
       const uint64_t *cur = xht_mine + (t & 1) * B * H;
-      if (!quant_tile<NVA, RBA, kSrcTagged>(nb, rowsA, H, (uint32_t)(t + 1), (int)H,
-                                            xhb[(t + 1) & 1], tl.ldsX, tl.ldH, flag,
-                                            rphb[(t + 1) & 1], [&](int lb) -> const void * {
-                                              return cur + (b0 + lb) * H;
-                                            }))
+      if (!quant_row_2w(cur + b0 * H, (uint32_t)(t + 1), (int)H, xhb[(t + 1) & 1], tl.ldH, flag,
+                        rphb[(t + 1) & 1], s_xch))
         s_abort = 1;
     } else {
-      if (t > 0) share_prev(t, kWave, (int)blockDim.x - kWave);
+      if (t > 0) share_prev(t, 2 * kWave, (int)blockDim.x - 2 * kWave);
       if (t + 1 < T && !input_side_async(t + 1)) s_abort = 1;
     }
     __syncthreads();
