@@ -183,6 +183,81 @@ __device__ __forceinline__ bool quant_tile(int nvalid, int ntotal, int64_t strid
   return true;
 }
 
+// One row of K <= 512 published values (tagged words of step tag `tag`)
+// quantized per vector (eq. 2) by waves 0 and 1 together: wave w polls and
+// encodes half w of the row (lane l: elements 4 (w*64 + l) .. +3), and the
+// halves' min/max, then their code sums, meet in LDS slots xch[w*8 ..] (data,
+// then a flag holding the tag, released after the data).  The codes go to
+// dst (ldpad <= 512 bytes), the row params to *rp.  False if a wait expired.
+__device__ __forceinline__ bool quant_row_2w(const uint64_t *src, uint32_t tag, int K,
+                                             int8_t *dst, int ldpad, int *flag, RowParam *rp,
+                                             int *xch) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, o = 1 - w;
+  const int kb = 4 * (w * kWave + lane);
+  float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  uint32_t got = 0;
+  long it = 0;
+  for (;;) {
+    uint32_t bad = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (kb + e < K && !(got & (1u << e))) {
+        const uint64_t wd = ld_tagged(src + kb + e);
+        if ((uint32_t)(wd >> 32) == tag) {
+          got |= 1u << e;
+          v[e] = __uint_as_float((uint32_t)wd);
+        } else {
+          bad = 1;
+        }
+      }
+    if (!__any(bad != 0)) break;
+    if (wait_expired(flag, it)) return false;
+  }
+  int mm[2] = {0x7fffffff, 0x7fffffff};
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (kb + e < K) {
+      const int key = float_key(v[e]);
+      mm[0] = min(mm[0], key);
+      mm[1] = min(mm[1], ~key);
+    }
+  wave_min_n<2>(mm);
+  if (lane == 0) {
+    xch[w * 8 + 0] = mm[0];
+    xch[w * 8 + 1] = mm[1];
+    __hip_atomic_store(&xch[w * 8 + 2], (int)tag, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  it = 0;
+  while (__hip_atomic_load(&xch[o * 8 + 2], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != (int)tag)
+    if (wait_expired(flag, it)) return false;
+  const int lo = min(mm[0], xch[o * 8 + 0]), hi = min(mm[1], xch[o * 8 + 1]);
+  const QParams prm = make_qparams(key_float(lo), key_float(~hi));
+  int sum = 0;
+  uint32_t word = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool ok = kb + e < K;
+    const int code = encode(v[e], prm.q, prm.z);
+    sum += ok ? code : 0;
+    word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
+  }
+  if (kb < ldpad) reinterpret_cast<uint32_t *>(dst)[kb / 4] = word;
+  int s1[1] = {sum};
+  wave_add_n<1>(s1);
+  if (w == 1) {
+    if (lane == 0) {
+      xch[8 + 3] = s1[0];
+      __hip_atomic_store(&xch[8 + 4], (int)tag, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    return true;
+  }
+  it = 0;
+  while (__hip_atomic_load(&xch[8 + 4], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != (int)tag)
+    if (wait_expired(flag, it)) return false;
+  if (lane == 0) *rp = row_param(prm.z, prm.inv_q, s1[0] + xch[8 + 3], K);
+  return true;
+}
+
 // ---------------------------------------------------------------------------
 // Products S[lb][n] = sum_k x[lb][k] w[n][k] over K bytes (a multiple of 64).
 // ---------------------------------------------------------------------------
