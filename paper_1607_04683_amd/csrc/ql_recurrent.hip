@@ -103,12 +103,10 @@ __device__ __forceinline__ void store_codes(const RecurrentArgs &a, const RecTil
 // min/max and the code sum are reduced within each wave and then across the
 // waves through red (16 + waves ints of LDS).  The four codes of a thread go
 // out as one device-coherent 32-bit store (device layout, zero from K up to
-// ldk), the row params to zp / iqp / sump with device-coherent stores, and,
-// when tap is not null, the codes also to tap[0, K) and the params to
-// tap_z / tap_iq.  Every thread calls it; it ends with a workgroup barrier.
+// ldk), the row params to zp / iqp / sump with device-coherent stores.
+// Every thread calls it; it ends with a workgroup barrier.
 __device__ __forceinline__ void quant_row_wg(const float *src, int K, int ldk, int8_t *dst,
-                                             int32_t *zp, float *iqp, int32_t *sump, int *red,
-                                             int8_t *tap, int32_t *tap_z, float *tap_iq) {
+                                             int32_t *zp, float *iqp, int32_t *sump, int *red) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
   const int k0 = 4 * tid;
   float v[4];
@@ -143,7 +141,6 @@ __device__ __forceinline__ void quant_row_wg(const float *src, int K, int ldk, i
     const int code = encode(v[e], prm.q, prm.z);
     sum += ok ? code : 0;
     word |= (ok ? (uint32_t)((code ^ 0x80) & 0xff) : 0u) << (8 * e);
-    if (tap && ok) tap[k0 + e] = (int8_t)(code ^ 0x80);
   }
   for (int k = k0; k < ldk; k += 4 * (int)blockDim.x)
     __hip_atomic_store(reinterpret_cast<uint32_t *>(dst + k), k == k0 ? word : 0u, __ATOMIC_RELAXED,
@@ -158,8 +155,6 @@ __device__ __forceinline__ void quant_row_wg(const float *src, int K, int ldk, i
     st_coherent_i(zp, prm.z);
     st_coherent(iqp, prm.inv_q);
     st_coherent_i(sump, total);
-    if (tap_z) *tap_z = prm.z;
-    if (tap_iq) *tap_iq = prm.inv_q;
   }
 }
 
@@ -567,7 +562,7 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
           for (int lb = tp; lb < nb2; lb += tl.npt) {
             const int64_t row = c0 + lb;
             quant_row_wg(mf + row * H, (int)H, tl.ldH, mcodes + row * tl.ldH, &mz[row], &miq[row],
-                         &msum[row], s_red, nullptr, nullptr, nullptr);
+                         &msum[row], s_red);
           }
           __builtin_amdgcn_s_waitcnt(0);
           __syncthreads();

@@ -40,6 +40,7 @@ namespace ql {
 
 constexpr int kStackThreads = 512;
 constexpr int kXcds = 8;  // accelerator complex dies (XCDs) of the MI355X, each with its own L2
+constexpr int kXcdCus = 32;  // CUs of one XCD
 // Replicas of the tagged h words at one batch row (readers spread over them).
 constexpr int kMaxReph = 2;
 
@@ -786,9 +787,11 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.grid = a.nl * tl.gl;
   if (tl.grid > cus) return false;
   // one-row tiles: each layer on an XCD of its own when its tiles fit one
-  // (the h exchange then stays in that XCD's L2); the grid covers every CU
+  // (the h exchange then stays in that XCD's L2); the grid covers every CU.
+  // Only on the whole chip (all eight XCDs, XCC_IDs 0..7): a partition of it
+  // keeps the spread layout.
   tl.xcd = 0;
-  if (bB == 1 && cus % kXcds == 0 && a.nl <= kXcds && tl.gl <= cus / kXcds) {
+  if (bB == 1 && cus == kXcds * kXcdCus && a.nl <= kXcds && tl.gl <= kXcdCus) {
     tl.xcd = 1;
     tl.grid = cus;
   }
