@@ -14,7 +14,8 @@
  *     consistently with eq. 3;
  *   - layers that take and return float (Section 3.1, Fig. 1):
  *     y = F(R(Mult(Q(X), W')) + B), parameters quantized offline, inputs on
- *     the fly; weight matrices quantized independently per gate block
+ *     the fly; weight matrices quantized independently per gate block by
+ *     default, or per matrix, per sub-matrix of whole rows, or per row
  *     (Section 3.1, granularity paragraph);
  *   - the LSTM acoustic models of Section 4: stacked LSTM layers (optionally
  *     with a linear projection after each layer) and a quantized softmax
@@ -73,7 +74,12 @@ typedef enum { QL_ACT_PER_TENSOR = 0, QL_ACT_PER_ROW = 1 } ql_act_gran;
 
 /* One quantized matrix (Section 3.1): rows split into `nblocks` equal row
  * blocks, each quantized as an independent set (nblocks = 1: per matrix;
- * nblocks = 4: per LSTM gate i, f, g, o).  All arrays are device memory. */
+ * nblocks = 4: per LSTM gate i, f, g, o; more: the granularity paragraph's
+ * individually quantized sub-matrices, each a band of whole rows, down to
+ * nblocks = rows, one set per row).  Blocks are bands of rows so that every
+ * output of a product has one weight recovery factor over its whole sum.
+ * Every entry point accepts any nblocks dividing rows.  All arrays are device
+ * memory. */
 typedef struct {
   int8_t *codes;     /* [rows][ld], V' - 128 (see "Device code layout")    */
   int64_t rows, cols, ld;
@@ -121,7 +127,8 @@ typedef struct {
 /* ---- quantization (Section 3; eq. 2) ---------------------------------------
  * Quantizes src [rows][cols] (fp32, device) in nblocks row blocks into dst,
  * whose arrays the caller allocated (codes rows*ld bytes, ld = dst->ld).
- * dst->rows/cols/nblocks must match.  Offline step for weights. */
+ * dst->rows/cols/nblocks must match; nblocks <= 65535 (QL_EUNSUPPORTED
+ * beyond).  Offline step for weights. */
 size_t ql_quantize_workspace(int64_t rows, int64_t cols, int32_t nblocks);
 ql_status ql_quantize(const float *src, int64_t rows, int64_t cols, int32_t nblocks,
                       ql_qmatrix *dst, void *ws, size_t ws_bytes, void *stream);
@@ -218,6 +225,35 @@ size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B);
 ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T,
                                     int64_t B, float *post, const ql_model_taps *taps,
                                     void *ws, size_t ws_bytes, void *stream);
+
+/* ---- frontend fused into the input quantizer (Section 4) ------------------------
+ * The network's input at presented step t of utterance b is the concatenation of
+ * `stack` consecutive base frames skip*t, ..., skip*t + stack - 1 of that utterance
+ * (the paper stacks 8 frames of 40 log-mel energies, 7 of right context, and
+ * presents every third stacked frame: one network step per 30 ms).  frames
+ * [nframes][B][dim] fp32 (device, time-major).  The number of presented steps is
+ * T = ql_stacked_input_count(nframes, stack, skip) = (nframes - stack) / skip + 1
+ * when nframes >= stack, else 0 (trailing frames that do not complete a stack are
+ * not presented).  The stacked vectors are never written: each is gathered from
+ * the base frames while it is quantized, per vector, exactly as
+ * ql_quantize_activations quantizes the same vector. */
+int64_t ql_stacked_input_count(int64_t nframes, int32_t stack, int32_t skip);
+/* dst->rows must be T * B, dst->cols = stack * dim (QL_ESHAPE otherwise);
+ * codes and per-row zero point, recovery factor and code sum as in
+ * ql_quantize_activations.  stack, skip, dim > 0. */
+ql_status ql_quantize_stacked_frames(const float *frames, int64_t nframes, int64_t B, int64_t dim,
+                                     int32_t stack, int32_t skip, const ql_qact *dst,
+                                     void *stream);
+/* ql_acoustic_model_forward on the stacked inputs of frames [nframes][B][dim]:
+ * layers[0].in must equal stack * dim; post [T][B][S] with T as above.  Same bits
+ * as stacking on the host and calling ql_acoustic_model_forward. */
+size_t ql_acoustic_model_frames_workspace(const ql_model *M, int64_t nframes, int64_t B,
+                                          int32_t stack, int32_t skip);
+ql_status ql_acoustic_model_forward_frames(const ql_model *M, const float *frames,
+                                           int64_t nframes, int64_t B, int64_t dim,
+                                           int32_t stack, int32_t skip, float *post,
+                                           const ql_model_taps *taps, void *ws, size_t ws_bytes,
+                                           void *stream);
 
 /* ---- unquantized fp32 model (the float baseline of Section 5) -----------------
  * The same layers and model with fp32 weights and no quantization: products

@@ -2,8 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY: imported by tests/, the smoke check and the
 benchmark's CPU-baseline leg, never by the GPU library.  The arithmetic lives
-in qlstm_oracle.c; this file only builds it, marshals numpy arrays and packs
-the results.  Codes here are the paper's V' in 0..255 (uint8).
+in qlstm_oracle.c; this file builds it, marshals numpy arrays, packs the
+results and stacks the frontend's base frames (a plain gather, Section 4).  Codes here are the paper's V' in 0..255 (uint8).
 """
 from __future__ import annotations
 
@@ -241,15 +241,15 @@ class QLayer:
                      self.Wr.cstruct() if self.Wr is not None else empty, _p(self.bias))
 
 
-def quantize_layer(L: dict, gate_blocks: int = 4) -> QLayer:
-    """Float layer {'Wx','Wh','b','Wr'} -> quantized: W_x, W_h per gate block,
-    W_r per matrix (Section 3.1, granularity)."""
+def quantize_layer(L: dict, gate_blocks: int = 4, proj_blocks: int = 1) -> QLayer:
+    """Float layer {'Wx','Wh','b','Wr'} -> quantized: W_x, W_h in gate_blocks
+    row blocks (4: per gate), W_r in proj_blocks (Section 3.1, granularity)."""
     Wx, Wh = L["Wx"], L["Wh"]
     H = Wx.shape[0] // 4
     Wr = L.get("Wr")
     return QLayer(Wx.shape[1], H, 0 if Wr is None else Wr.shape[0],
                   quantize(Wx, gate_blocks), quantize(Wh, gate_blocks),
-                  None if Wr is None else quantize(Wr, 1),
+                  None if Wr is None else quantize(Wr, proj_blocks),
                   np.ascontiguousarray(L["b"], dtype=np.float32))
 
 
@@ -260,9 +260,11 @@ class QModel:
     by: np.ndarray
 
 
-def quantize_model(weights: dict, gate_blocks: int = 4) -> QModel:
-    return QModel([quantize_layer(L, gate_blocks) for L in weights["layers"]],
-                  quantize(weights["Wy"], 1), np.ascontiguousarray(weights["by"], np.float32))
+def quantize_model(weights: dict, gate_blocks: int = 4, proj_blocks: int = 1,
+                   out_blocks: int = 1) -> QModel:
+    return QModel([quantize_layer(L, gate_blocks, proj_blocks) for L in weights["layers"]],
+                  quantize(weights["Wy"], out_blocks),
+                  np.ascontiguousarray(weights["by"], np.float32))
 
 
 def _taps_arrays(T, B, H, P):
@@ -326,6 +328,36 @@ def acoustic_model_forward(Mq: QModel, feats, taps: bool = False):
                                                _p(acc_y), _p(logits)),
            "acoustic_model_forward")
     return out
+
+
+def stacked_input_count(nframes: int, stack: int = 8, skip: int = 3) -> int:
+    """Section 4 frontend: a stacked frame needs `stack` base frames (the first
+    plus stack-1 of right context); only every skip-th stacked frame, starting
+    with the first, is presented to the network."""
+    if nframes < stack:
+        return 0
+    return (nframes - stack) // skip + 1
+
+
+def stack_frames(frames, stack: int = 8, skip: int = 3) -> np.ndarray:
+    """Section 4 frontend: base frames [nframes][B][d] -> presented inputs
+    [T][B][stack*d], input t = base frames skip*t .. skip*t+stack-1 laid end to
+    end (plain loops: one copy per (t, b, j))."""
+    frames = np.asarray(frames, dtype=np.float32)
+    nframes, B, d = frames.shape
+    T = stacked_input_count(nframes, stack, skip)
+    out = np.empty((T, B, stack * d), np.float32)
+    for t in range(T):
+        for b in range(B):
+            for j in range(stack):
+                out[t, b, j * d:(j + 1) * d] = frames[skip * t + j, b, :]
+    return out
+
+
+def acoustic_model_forward_frames(Mq: QModel, frames, stack: int = 8, skip: int = 3,
+                                  taps: bool = False):
+    """The model on the presented inputs of base frames [nframes][B][d]."""
+    return acoustic_model_forward(Mq, stack_frames(frames, stack, skip), taps)
 
 
 # ---------------------------------------------------------------- fp32 model

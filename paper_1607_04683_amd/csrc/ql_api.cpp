@@ -80,7 +80,7 @@ ql_status check_layer(const ql_lstm_layer *L) {
   if (st != QL_OK) return st;
   if (L->Wx.rows != 4 * H || L->Wx.cols != L->in) return QL_ESHAPE;
   if (L->Wh.rows != 4 * H || L->Wh.cols != R) return QL_ESHAPE;
-  if (L->proj && (L->Wr.rows != L->proj || L->Wr.cols != H || L->Wr.nblocks != 1)) return QL_ESHAPE;
+  if (L->proj && (L->Wr.rows != L->proj || L->Wr.cols != H)) return QL_ESHAPE;
   if (H > kMaxK) return QL_EOVERFLOW;
   return QL_OK;
 }
@@ -178,6 +178,7 @@ ql_status ql_quantize(const float *src, int64_t rows, int64_t cols, int32_t nblo
   if (!dst || !dst->zero || !dst->inv_q) return QL_EINVAL;
   if (rows * cols > 0 && (!src || !dst->codes)) return QL_EINVAL;
   if (rows < 0 || cols < 0 || nblocks <= 0 || rows % nblocks != 0) return QL_ESHAPE;
+  if (nblocks > 65535) return QL_EUNSUPPORTED;  // one grid row of partial min/max per set
   if (dst->rows != rows || dst->cols != cols || dst->nblocks != nblocks) return QL_ESHAPE;
   if (dst->ld < cols || dst->ld % 64 != 0) return QL_ESHAPE;
   if (!ws || ws_bytes < ql_quantize_workspace(rows, cols, nblocks)) return QL_EWORKSPACE;
@@ -373,12 +374,32 @@ size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B) {
   return model_ws_bytes(M, T, B);
 }
 
-ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T, int64_t B,
-                                    float *post, const ql_model_taps *taps, void *ws,
-                                    size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+// Where the first layer's input comes from: a dense [T][B][in] array of
+// presented inputs, or the frontend's base frames [nframes][B][dim] stacked
+// `stack` at a time with every `skip`-th stack presented (Section 4).
+struct Frontend {
+  const float *x;
+  bool stacked;
+  int32_t dim, stack, skip;
+};
+
+hipError_t quantize_input(const Frontend &f, int64_t T, int64_t B, int64_t in, const ActBuf &dst,
+                          hipStream_t s) {
+  if (f.stacked)
+    return launch_quantize_stacked(f.x, B, f.dim, f.stack, f.skip, T, dst.codes, dst.ld,
+                                   dst.zero, dst.inv_q, dst.sums, s);
+  return launch_quantize_rows(f.x, in, T * B, in, dst.codes, dst.ld, dst.zero, dst.inv_q,
+                              dst.sums, s);
+}
+
+ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_t B, float *post,
+                        const ql_model_taps *taps, void *ws, size_t ws_bytes, void *stream) {
   if (!M || !M->layers || !M->by) return QL_EINVAL;
   if (M->nlayers <= 0 || T < 0 || B < 0) return QL_ESHAPE;
-  if (T * B > 0 && (!feats || !post)) return QL_EINVAL;
+  if (T * B > 0 && (!fe.x || !post)) return QL_EINVAL;
   for (int l = 0; l < M->nlayers; ++l) {
     ql_status st = check_layer(&M->layers[l]);
     if (st != QL_OK) return st;
@@ -406,9 +427,7 @@ ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64
   Carve c(ws);
   ModelWs mw = carve_model(c, *M, T, B);
 
-  if (launch_quantize_rows(feats, M->layers[0].in, MB, M->layers[0].in, mw.xin.codes, mw.xin.ld,
-                           mw.xin.zero, mw.xin.inv_q, mw.xin.sums, s) != hipSuccess)
-    return QL_EHIP;
+  if (quantize_input(fe, T, B, M->layers[0].in, mw.xin, s) != hipSuccess) return QL_EHIP;
   ActRows cur = mw.xin.rows();
   const bool stack = stackable(*M) && codes_taps_only(taps, M->nlayers);
   int per_launch = 1;
@@ -456,6 +475,62 @@ ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64
   return from_hip(launch_softmax_layer(cur, weight(M->Wy), MB, M->Wy.rows, K, M->by, post,
                                        taps ? taps->acc_y : nullptr,
                                        taps ? taps->logits : nullptr, mw.sws, s));
+}
+}  // namespace
+
+extern "C" {
+ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T, int64_t B,
+                                    float *post, const ql_model_taps *taps, void *ws,
+                                    size_t ws_bytes, void *stream) {
+  return model_forward(M, Frontend{feats, false, 0, 0, 0}, T, B, post, taps, ws, ws_bytes, stream);
+}
+
+int64_t ql_stacked_input_count(int64_t nframes, int32_t stack, int32_t skip) {
+  if (nframes < 0 || stack <= 0 || skip <= 0 || nframes < stack) return 0;
+  return (nframes - stack) / skip + 1;
+}
+
+namespace {
+ql_status check_frontend(int64_t nframes, int64_t B, int64_t dim, int32_t stack, int32_t skip,
+                         int64_t in) {
+  if (nframes < 0 || B < 0 || dim <= 0 || stack <= 0 || skip <= 0) return QL_ESHAPE;
+  if (dim * stack != in || in > INT32_MAX) return QL_ESHAPE;
+  return QL_OK;
+}
+}  // namespace
+
+ql_status ql_quantize_stacked_frames(const float *frames, int64_t nframes, int64_t B, int64_t dim,
+                                     int32_t stack, int32_t skip, const ql_qact *dst,
+                                     void *stream) {
+  if (!dst) return QL_EINVAL;
+  ql_status st = check_frontend(nframes, B, dim, stack, skip, dst->cols);
+  if (st != QL_OK) return st;
+  const int64_t T = ql_stacked_input_count(nframes, stack, skip);
+  if (dst->rows != T * B || dst->ld < round_up(dst->cols, 64) || dst->ld % 64) return QL_ESHAPE;
+  if (T * B == 0) return QL_OK;
+  if (!frames || !dst->codes || !dst->zero || !dst->inv_q || !dst->sums) return QL_EINVAL;
+  return from_hip(launch_quantize_stacked(frames, B, (int)dim, stack, skip, T, dst->codes,
+                                          dst->ld, dst->zero, dst->inv_q, dst->sums,
+                                          as_stream(stream)));
+}
+
+size_t ql_acoustic_model_frames_workspace(const ql_model *M, int64_t nframes, int64_t B,
+                                          int32_t stack, int32_t skip) {
+  return ql_acoustic_model_workspace(M, ql_stacked_input_count(nframes, stack, skip), B);
+}
+
+ql_status ql_acoustic_model_forward_frames(const ql_model *M, const float *frames,
+                                           int64_t nframes, int64_t B, int64_t dim,
+                                           int32_t stack, int32_t skip, float *post,
+                                           const ql_model_taps *taps, void *ws, size_t ws_bytes,
+                                           void *stream) {
+  if (!M || !M->layers) return QL_EINVAL;
+  if (M->nlayers <= 0) return QL_ESHAPE;
+  ql_status st = check_frontend(nframes, B, dim, stack, skip, M->layers[0].in);
+  if (st != QL_OK) return st;
+  const int64_t T = ql_stacked_input_count(nframes, stack, skip);
+  return model_forward(M, Frontend{frames, true, (int32_t)dim, stack, skip}, T, B, post, taps, ws,
+                       ws_bytes, stream);
 }
 
 size_t ql_lstm_recurrence_workspace(const ql_lstm_layer *L, int64_t T, int64_t B) {

@@ -16,6 +16,9 @@ hipError_t launch_quantize_rows(const float *X, int64_t ldx, int64_t m, int64_t 
                                 int64_t ld, int32_t *zero, float *inv_q, int32_t *sums,
                                 hipStream_t s);
 size_t set_quantize_ws(int nsets);
+hipError_t launch_quantize_stacked(const float *frames, int64_t B, int dim, int stack, int skip,
+                                   int64_t T, int8_t *codes, int64_t ld, int32_t *zero,
+                                   float *inv_q, int32_t *sums, hipStream_t s);
 hipError_t launch_set_quantize(const float *X, int64_t ldx, int64_t rows, int64_t cols,
                                int nsets, int8_t *codes, int64_t ld, double *range,
                                int32_t *zero, float *inv_q, int32_t *row_sums,

@@ -4,6 +4,9 @@
 //    are quantized on the fly).  One wavefront per vector: fused min/max
 //    wavefront reduction -> (R, Q, round(Q Vmin), Q^-1) -> packed codes and the
 //    code sum, in one pass over HBM (4 bytes read + 1 byte written per value).
+//  * k_quantize_stacked: the same quantizer reading the network's input straight
+//    from the frontend's base frames (Section 4: 8 consecutive frames stacked,
+//    every third stacked frame presented), so the stacked copy is never written.
 //  * k_set_*: quantization of larger sets (a weight matrix or one of its gate
 //    blocks; a whole activation tensor): partial min/max over many blocks,
 //    a finalize step, then the row encoder.
@@ -13,17 +16,65 @@
 
 namespace ql {
 
-// Encode row `row` of X (K values) with params (q, z) into codes[row][ld];
+// Row accessors of the on-the-fly quantizer: value i of one input vector.
+// A row of a dense [m][ldx] matrix.
+struct DenseRow {
+  const float *x;
+  __device__ bool vec4(int64_t K) const { return (K & 3) == 0 && (((uintptr_t)x) & 15) == 0; }
+  __device__ float4 load4(int64_t q) const { return reinterpret_cast<const float4 *>(x)[q]; }
+  __device__ float load1(int64_t i) const { return x[i]; }
+};
+// One presented input of the frontend (Section 4): `stack` consecutive base
+// frames of one utterance, `dim` values each, laid end to end.  f points at the
+// first of them; consecutive base frames of the utterance lie `fstride` floats
+// apart (B * dim in a time-major [frames][B][dim] array).  K = stack * dim < 2^31.
+struct StackedRow {
+  const float *f;
+  int dim;
+  int64_t fstride;
+  __device__ bool vec4(int64_t) const {
+    return (dim & 3) == 0 && (fstride & 3) == 0 && (((uintptr_t)f) & 15) == 0;
+  }
+  __device__ float4 load4(int64_t q) const {  // dim % 4 == 0: a float4 never straddles frames
+    const int i = 4 * (int)q, j = i / dim;
+    return *reinterpret_cast<const float4 *>(f + j * fstride + (i - j * dim));
+  }
+  __device__ float load1(int64_t i) const {
+    const int j = (int)i / dim;
+    return f[j * fstride + ((int)i - j * dim)];
+  }
+};
+
+// min and max of the K values of row x, reduced over the wave (every lane).
+template <class Row>
+__device__ __forceinline__ float2 row_minmax_wave(const Row &x, int64_t K, int lane) {
+  float lo = INFINITY, hi = -INFINITY;
+  if (x.vec4(K)) {
+    for (int64_t i = lane; i < K / 4; i += kWave) {
+      const float4 v = x.load4(i);
+      lo = fminf(fminf(lo, v.x), fminf(v.y, fminf(v.z, v.w)));
+      hi = fmaxf(fmaxf(hi, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
+    }
+  } else {
+    for (int64_t i = lane; i < K; i += kWave) {
+      const float v = x.load1(i);
+      lo = fminf(lo, v);
+      hi = fmaxf(hi, v);
+    }
+  }
+  return make_float2(wave_min(lo), wave_max(hi));
+}
+
+// Encode the K values of row x with params (q, z) into out[0, ld);
 // returns the code sum (0..255 domain) in every lane of the wave.
-__device__ __forceinline__ int encode_row_wave(const float *__restrict__ x, int64_t K,
-                                               int8_t *__restrict__ out, int64_t ld,
-                                               double q, int32_t z, int lane) {
+template <class Row>
+__device__ __forceinline__ int encode_row_wave(const Row &x, int64_t K, int8_t *__restrict__ out,
+                                               int64_t ld, double q, int32_t z, int lane) {
   int sum = 0;
-  if ((K & 3) == 0 && (((uintptr_t)x) & 15) == 0) {
-    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+  if (x.vec4(K)) {
     uint32_t *o4 = reinterpret_cast<uint32_t *>(out);
     for (int64_t i = lane; i < K / 4; i += kWave) {
-      const float4 v = x4[i];
+      const float4 v = x.load4(i);
       const int c0 = encode(v.x, q, z), c1 = encode(v.y, q, z), c2 = encode(v.z, q, z),
                 c3 = encode(v.w, q, z);
       sum += c0 + c1 + c2 + c3;
@@ -31,7 +82,7 @@ __device__ __forceinline__ int encode_row_wave(const float *__restrict__ x, int6
     }
   } else {
     for (int64_t i = lane; i < K; i += kWave) {
-      const int c = encode(x[i], q, z);
+      const int c = encode(x.load1(i), q, z);
       sum += c;
       out[i] = (int8_t)(c ^ 0x80);
     }
@@ -39,6 +90,24 @@ __device__ __forceinline__ int encode_row_wave(const float *__restrict__ x, int6
   // zero padding [K, ld) in the signed layout (V' - 128 = 0 contributes 0)
   for (int64_t i = K + lane; i < ld; i += kWave) out[i] = 0;
   return wave_sum(sum);
+}
+
+// One wave quantizes one vector: min/max, params, codes, code sum.
+template <class Row>
+__device__ __forceinline__ void quantize_row_wave(const Row &x, int64_t K, int64_t row,
+                                                  int8_t *__restrict__ codes, int64_t ld,
+                                                  int32_t *__restrict__ zero,
+                                                  float *__restrict__ inv_q,
+                                                  int32_t *__restrict__ sums, int lane) {
+  float2 mm = row_minmax_wave(x, K, lane);
+  if (K == 0) mm = make_float2(0.0f, 0.0f);
+  const QParams p = make_qparams(mm.x, mm.y);
+  const int s = encode_row_wave(x, K, codes + row * ld, ld, p.q, p.z, lane);
+  if (lane == 0) {
+    if (zero) zero[row] = p.z;
+    if (inv_q) inv_q[row] = p.inv_q;
+    if (sums) sums[row] = s;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_quantize_rows(const float *__restrict__ X, int64_t ldx,
@@ -50,31 +119,26 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float *__restrict__
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
   if (row >= m) return;
-  const float *x = X + row * ldx;
-  float lo = INFINITY, hi = -INFINITY;
-  if ((K & 3) == 0 && (((uintptr_t)x) & 15) == 0) {
-    const float4 *x4 = reinterpret_cast<const float4 *>(x);
-    for (int64_t i = lane; i < K / 4; i += kWave) {
-      const float4 v = x4[i];
-      lo = fminf(fminf(lo, v.x), fminf(v.y, fminf(v.z, v.w)));
-      hi = fmaxf(fmaxf(hi, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
-    }
-  } else {
-    for (int64_t i = lane; i < K; i += kWave) {
-      lo = fminf(lo, x[i]);
-      hi = fmaxf(hi, x[i]);
-    }
-  }
-  lo = wave_min(lo);
-  hi = wave_max(hi);
-  if (K == 0) lo = hi = 0.0f;
-  const QParams p = make_qparams(lo, hi);
-  const int s = encode_row_wave(x, K, codes + row * ld, ld, p.q, p.z, lane);
-  if (lane == 0) {
-    if (zero) zero[row] = p.z;
-    if (inv_q) inv_q[row] = p.inv_q;
-    if (sums) sums[row] = s;
-  }
+  quantize_row_wave(DenseRow{X + row * ldx}, K, row, codes, ld, zero, inv_q, sums, lane);
+}
+
+// Frontend fused into the input quantizer: presented input t of utterance b
+// (row t * B + b of the output) is base frames skip*t .. skip*t + stack - 1 of
+// that utterance, frames [nframes][B][dim]; the caller guarantees
+// skip * (T - 1) + stack <= nframes.
+__global__ __launch_bounds__(256) void k_quantize_stacked(const float *__restrict__ frames,
+                                                          int64_t B, int dim, int stack,
+                                                          int skip, int64_t m,
+                                                          int8_t *__restrict__ codes, int64_t ld,
+                                                          int32_t *__restrict__ zero,
+                                                          float *__restrict__ inv_q,
+                                                          int32_t *__restrict__ sums) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
+  if (row >= m) return;
+  const int64_t t = row / B, b = row - t * B;
+  const StackedRow x{frames + ((int64_t)skip * t * B + b) * dim, dim, B * (int64_t)dim};
+  quantize_row_wave(x, (int64_t)stack * dim, row, codes, ld, zero, inv_q, sums, lane);
 }
 
 // Partial min/max: set s = rows [s*rps, (s+1)*rps) of a [rows][cols] matrix
@@ -144,7 +208,8 @@ __global__ __launch_bounds__(256) void k_set_encode(
   const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int64_t s = row / rps;
-  const int sum = encode_row_wave(X + row * ldx, cols, codes + row * ld, ld, q[s], zero[s], lane);
+  const int sum =
+      encode_row_wave(DenseRow{X + row * ldx}, cols, codes + row * ld, ld, q[s], zero[s], lane);
   if (lane == 0) {
     if (row_sums) row_sums[row] = sum;
     if (row_zero) row_zero[row] = zero[s];
@@ -193,6 +258,16 @@ hipError_t launch_quantize_rows(const float *X, int64_t ldx, int64_t m, int64_t 
   if (m == 0) return hipSuccess;
   hipLaunchKernelGGL(k_quantize_rows, dim3(blocks_for(m, 4)), dim3(256), 0, s, X, ldx, m, K,
                      codes, ld, zero, inv_q, sums);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_stacked(const float *frames, int64_t B, int dim, int stack, int skip,
+                                   int64_t T, int8_t *codes, int64_t ld, int32_t *zero,
+                                   float *inv_q, int32_t *sums, hipStream_t s) {
+  const int64_t m = T * B;
+  if (m == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_quantize_stacked, dim3(blocks_for(m, 4)), dim3(256), 0, s, frames, B, dim,
+                     stack, skip, m, codes, ld, zero, inv_q, sums);
   return hipGetLastError();
 }
 

@@ -638,12 +638,13 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
       else
         products_valu(xc, ldx2, nb2, wr, a.Wr.ld, tl.p2, np2, tl.ldH, S, tl.p2);
       __syncthreads();
-      const int32_t ztw = a.Wr.zero[0] + 128;  // W_r is quantized per matrix
-      const float iqw = a.Wr.inv_q[0];
       for (int idx = tid; idx < nb2 * np2; idx += blockDim.x) {
         const int lb = idx / np2, pp = idx % np2;
         const int64_t b = c0 + lb, p = p0 + pp;
         const RowParam r = rp[lb];
+        const int blk = (int)p / (int)a.Wr.rows_per_block;  // W_r's row block of output p
+        const int32_t ztw = a.Wr.zero[blk] + 128;
+        const float iqw = a.Wr.inv_q[blk];
         const int32_t sigw = a.Wr.row_sums[p] - 128 * (int32_t)H;
         const int64_t colterm = (int64_t)sigw + H * (int64_t)ztw;
         const int32_t sv = S[lb * tl.p2 + pp];

@@ -31,7 +31,9 @@ EXPORTS = [
     "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_workspace",
     "ql_f32_lstm_layer_forward", "ql_f32_acoustic_model_workspace",
     "ql_f32_acoustic_model_forward", "ql_quantize_activations", "ql_lstm_stack_workspace",
-    "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch",
+    "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch", "ql_stacked_input_count",
+    "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
+    "ql_acoustic_model_forward_frames",
 ]
 
 
@@ -128,6 +130,13 @@ def load(path: str = LIB_PATH):
                                         C.POINTER(CQAct), vp, vp, sz, vp]
     L.ql_lstm_stack_layers_per_launch.argtypes = [C.POINTER(CLayer), i32, i64, i64]
     L.ql_lstm_stack_layers_per_launch.restype = i32
+    L.ql_stacked_input_count.argtypes = [i64, i32, i32]
+    L.ql_stacked_input_count.restype = i64
+    L.ql_quantize_stacked_frames.argtypes = [vp, i64, i64, i64, i32, i32, C.POINTER(CQAct), vp]
+    L.ql_acoustic_model_frames_workspace.argtypes = [C.POINTER(CModel), i64, i64, i32, i32]
+    L.ql_acoustic_model_frames_workspace.restype = sz
+    L.ql_acoustic_model_forward_frames.argtypes = [C.POINTER(CModel), vp, i64, i64, i64, i32,
+                                                   i32, vp, C.POINTER(CModelTaps), vp, sz, vp]
     L.ql_f32_lstm_layer_workspace.argtypes = [C.POINTER(CF32Layer), i64, i64]
     L.ql_f32_lstm_layer_workspace.restype = sz
     L.ql_f32_lstm_layer_forward.argtypes = [C.POINTER(CF32Layer), vp, i64, i64, vp, vp, vp, vp,
@@ -140,7 +149,8 @@ def load(path: str = LIB_PATH):
               "ql_lstm_layer_forward", "ql_acoustic_model_forward", "ql_workspace_status",
               "ql_gate_fn", "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_forward",
               "ql_f32_acoustic_model_forward", "ql_quantize_activations",
-              "ql_lstm_stack_forward"):
+              "ql_lstm_stack_forward", "ql_quantize_stacked_frames",
+              "ql_acoustic_model_forward_frames"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -296,15 +306,17 @@ class Layer:
                       self.Wr.cstruct() if self.Wr is not None else empty, self.bias.data_ptr())
 
 
-def quantize_layer(L: dict, device="cuda", gate_blocks: int = 4) -> Layer:
+def quantize_layer(L: dict, device="cuda", gate_blocks: int = 4, proj_blocks: int = 1) -> Layer:
     """Float layer {'Wx','Wh','b','Wr'} (numpy/tensors) -> quantized layer on the device:
-    W_x, W_h per gate block (i, f, g, o), W_r per matrix."""
+    W_x, W_h in gate_blocks row blocks (4: one per gate i, f, g, o; 4H: per row),
+    W_r in proj_blocks row blocks (1: per matrix)."""
     t = lambda a: torch.as_tensor(a, dtype=torch.float32).to(device).contiguous()
     Wx, Wh = t(L["Wx"]), t(L["Wh"])
     Wr = None if L.get("Wr") is None else t(L["Wr"])
     H = Wx.shape[0] // 4
     return Layer(Wx.shape[1], H, 0 if Wr is None else Wr.shape[0], quantize(Wx, gate_blocks),
-                 quantize(Wh, gate_blocks), None if Wr is None else quantize(Wr, 1), t(L["b"]))
+                 quantize(Wh, gate_blocks),
+                 None if Wr is None else quantize(Wr, proj_blocks), t(L["b"]))
 
 
 @dataclass
@@ -318,9 +330,13 @@ class Model:
         return CModel(len(self.layers), arr, self.Wy.cstruct(), self.by.data_ptr()), arr
 
 
-def quantize_model(weights: dict, device="cuda", gate_blocks: int = 4) -> Model:
-    return Model([quantize_layer(L, device, gate_blocks) for L in weights["layers"]],
-                 quantize(torch.as_tensor(weights["Wy"], dtype=torch.float32).to(device), 1),
+def quantize_model(weights: dict, device="cuda", gate_blocks: int = 4, proj_blocks: int = 1,
+                   out_blocks: int = 1) -> Model:
+    """Row blocks per matrix: gate_blocks for W_x / W_h, proj_blocks for W_r,
+    out_blocks for the softmax layer's W_y (Section 3.1, granularity)."""
+    return Model([quantize_layer(L, device, gate_blocks, proj_blocks) for L in weights["layers"]],
+                 quantize(torch.as_tensor(weights["Wy"], dtype=torch.float32).to(device),
+                          out_blocks),
                  torch.as_tensor(weights["by"], dtype=torch.float32).to(device).contiguous())
 
 
@@ -408,6 +424,25 @@ def lstm_recurrence(L: Layer, gx: torch.Tensor, h0=None, c0=None, taps=False,
     return res
 
 
+def _model_taps(M: Model, T: int, B: int, dev, taps, out: dict):
+    """Tap buffers of a model forward (None when taps is falsy)."""
+    if not taps:
+        return None
+    S = M.Wy.rows
+    lt = []
+    arr = (CTaps * len(M.layers))()
+    for i, L in enumerate(M.layers):
+        t, ct = _taps(T, B, L, dev, taps)
+        lt.append(t)
+        arr[i] = ct
+    full = taps is True or "acc_y" in taps
+    acc_y = torch.empty(T, B, S, dtype=torch.int32, device=dev) if full else None
+    logits = torch.empty(T, B, S, dtype=torch.float32, device=dev) if full else None
+    out.update(layers=lt, acc_y=acc_y, logits=logits, _keep=arr)
+    return CModelTaps(arr, None if acc_y is None else acc_y.data_ptr(),
+                      None if logits is None else logits.data_ptr())
+
+
 def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
                            workspace: Workspace | None = None, post: torch.Tensor | None = None,
                            check: bool = True):
@@ -417,32 +452,65 @@ def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
     dev = feats.device
     lib = load()
     cm, keep = M.cstruct()
-    S = M.Wy.rows
     if post is None:
-        post = torch.empty(T, B, S, dtype=torch.float32, device=dev)
+        post = torch.empty(T, B, M.Wy.rows, dtype=torch.float32, device=dev)
     nbytes = lib.ql_acoustic_model_workspace(C.byref(cm), T, B)
     ws = (workspace or Workspace()).get(nbytes, dev)
     out = dict(post=post)
-    mt = None
-    if taps:
-        lt = []
-        arr = (CTaps * len(M.layers))()
-        for i, L in enumerate(M.layers):
-            t, ct = _taps(T, B, L, dev, taps)
-            lt.append(t)
-            arr[i] = ct
-        full = taps is True or "acc_y" in taps
-        acc_y = torch.empty(T, B, S, dtype=torch.int32, device=dev) if full else None
-        logits = torch.empty(T, B, S, dtype=torch.float32, device=dev) if full else None
-        out.update(layers=lt, acc_y=acc_y, logits=logits)
-        mt = CModelTaps(arr, None if acc_y is None else acc_y.data_ptr(),
-                        None if logits is None else logits.data_ptr())
-        out["_keep"] = arr
+    mt = _model_taps(M, T, B, dev, taps, out)
     _check(lib.ql_acoustic_model_forward(C.byref(cm), _ptr(feats), T, B, _ptr(post),
                                          C.byref(mt) if mt is not None else None, _ptr(ws),
                                          ws.numel(), _stream()), "ql_acoustic_model_forward")
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward")
+    return out
+
+
+def stacked_input_count(nframes: int, stack: int = 8, skip: int = 3) -> int:
+    """Presented steps of nframes base frames (stack frames per input, every
+    skip-th stack presented)."""
+    return int(load().ql_stacked_input_count(nframes, stack, skip))
+
+
+def quantize_stacked_frames(frames: torch.Tensor, stack: int = 8, skip: int = 3,
+                            out: QAct | None = None) -> QAct:
+    """Base frames [nframes][B][dim] fp32 (device) -> per-vector codes of the
+    presented stacked inputs (T*B rows of stack*dim values)."""
+    frames = frames.contiguous()
+    nframes, B, dim = frames.shape
+    T = stacked_input_count(nframes, stack, skip)
+    q = out or QAct.empty(T * B, stack * dim, frames.device)
+    cq = q.cstruct()
+    _check(load().ql_quantize_stacked_frames(_ptr(frames), nframes, B, dim, stack, skip,
+                                             C.byref(cq), _stream()),
+           "ql_quantize_stacked_frames")
+    return q
+
+
+def acoustic_model_forward_frames(M: Model, frames: torch.Tensor, stack: int = 8, skip: int = 3,
+                                  taps: bool = False, workspace: Workspace | None = None,
+                                  post: torch.Tensor | None = None, check: bool = True):
+    """Base frames [nframes][B][dim] fp32 (device) -> dict(post [T][B][S][, taps]),
+    the frontend's stacking fused into the input quantizer."""
+    frames = frames.contiguous()
+    nframes, B, dim = frames.shape
+    dev = frames.device
+    lib = load()
+    T = stacked_input_count(nframes, stack, skip)
+    cm, keep = M.cstruct()
+    if post is None:
+        post = torch.empty(T, B, M.Wy.rows, dtype=torch.float32, device=dev)
+    nbytes = lib.ql_acoustic_model_frames_workspace(C.byref(cm), nframes, B, stack, skip)
+    ws = (workspace or Workspace()).get(nbytes, dev)
+    out = dict(post=post)
+    mt = _model_taps(M, T, B, dev, taps, out)
+    _check(lib.ql_acoustic_model_forward_frames(C.byref(cm), _ptr(frames), nframes, B, dim,
+                                                stack, skip, _ptr(post),
+                                                C.byref(mt) if mt is not None else None,
+                                                _ptr(ws), ws.numel(), _stream()),
+           "ql_acoustic_model_forward_frames")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward_frames")
     return out
 
 

@@ -158,6 +158,28 @@ def stacked_features(rng: np.random.Generator, T: int, B: int, frame_dim: int = 
     return out
 
 
+def base_frames(rng: np.random.Generator, T: int, B: int, frame_dim: int = 40, stack: int = 8,
+                skip: int = 3, utterances=None) -> np.ndarray:
+    """The base frames behind stacked_features, time-major [nbase][B][frame_dim]
+    fp32 with nbase = skip*(T-1)+stack: the same draws, in the same order, before
+    any stacking (the input of the fused frontend)."""
+    nbase = skip * (T - 1) + stack if T > 0 else 0
+    keep = list(range(B)) if utterances is None else list(utterances)
+    out = np.empty((nbase, len(keep), frame_dim), dtype=np.float32)
+    slot = {b: k for k, b in enumerate(keep)}
+    for b in range(B):
+        base = rng.standard_normal((nbase, frame_dim))
+        if b in slot:
+            out[:, slot[b], :] = base.astype(np.float32)
+    return out
+
+
+def frames(w: Workload, utterances=None) -> np.ndarray:
+    _, rng = model_weights(w)
+    m = w.model
+    return base_frames(rng, w.T, w.B, m.frame_dim, m.stack, m.skip, utterances)
+
+
 def features(w: Workload, utterances=None) -> np.ndarray:
     _, rng = model_weights(w)
     m = w.model

@@ -102,8 +102,8 @@ def test_layer_argument_errors(ql):
     assert f(bad) == ql.QL_ESHAPE
     bad = ql.CLayer(IN, H, 3, qm(4 * H, IN, 64, 4), qm(4 * H, 3, 64, 4), qm(3, H, 64, 1), None)
     assert f(bad) == ql.QL_EINVAL          # null bias
-    bad = ql.CLayer(IN, H, 3, qm(4 * H, IN, 64, 4), qm(4 * H, 3, 64, 4), qm(3, H, 64, 3), FAKE)
-    assert f(bad) == ql.QL_ESHAPE          # W_r must be one block
+    bad = ql.CLayer(IN, H, 3, qm(4 * H, IN, 64, 4), qm(4 * H, 3, 64, 4), qm(3, H, 64, 2), FAKE)
+    assert f(bad) == ql.QL_ESHAPE          # W_r rows % nblocks
 
 
 def test_model_argument_errors(ql):
@@ -181,3 +181,33 @@ def test_activation_and_stack_argument_errors(ql):
                                         qm(4 * H + 4, H + 1, 64, 4), empty, FAKE))
     assert f(layers=bad) == ql.QL_ESHAPE   # widths differ
     assert lib.ql_lstm_stack_forward(arr, 2, None, T, B, outs, None, FAKE, need, None) == ql.QL_EINVAL
+
+
+def test_frontend_argument_errors(ql):
+    """Stacked-frame entry points: presented-step count and argument checks."""
+    lib = ql.load()
+    cnt = lib.ql_stacked_input_count
+    assert [cnt(n, 8, 3) for n in (0, 7, 8, 10, 11, 14, 308)] == [0, 0, 1, 1, 2, 3, 101]
+    assert cnt(5, 0, 3) == 0 and cnt(5, 1, 0) == 0 and cnt(-1, 8, 3) == 0
+    T = cnt(20, 8, 3)  # 5 presented steps
+    q = ql.CQAct(FAKE, T * 2, 320, 320, FAKE, FAKE, FAKE)
+    f = lambda frames=FAKE, n=20, B=2, dim=40, st=8, sk=3, qq=q: lib.ql_quantize_stacked_frames(
+        frames, n, B, dim, st, sk, C.byref(qq), None)
+    assert f(dim=41) == ql.QL_ESHAPE                                   # stack*dim != cols
+    assert f(n=23) == ql.QL_ESHAPE                                     # 6 steps, 5 rows given
+    assert f(sk=0) == ql.QL_ESHAPE and f(st=0) == ql.QL_ESHAPE
+    assert f(qq=ql.CQAct(FAKE, T * 2, 320, 300, FAKE, FAKE, FAKE)) == ql.QL_ESHAPE  # ld
+    assert f(frames=None) == ql.QL_EINVAL
+    assert lib.ql_quantize_stacked_frames(FAKE, 20, 2, 40, 8, 3, None, None) == ql.QL_EINVAL
+    assert f(n=7, qq=ql.CQAct(FAKE, 0, 320, 320, FAKE, FAKE, FAKE)) == ql.QL_OK  # nothing to do
+    H, IN = 8, 320
+    empty = ql.CQMatrix(None, 0, 0, 0, 1, None, None, None, None)
+    L0 = ql.CLayer(IN, H, 0, qm(4 * H, IN, 320, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    arr = (ql.CLayer * 1)(L0)
+    m = ql.CModel(1, arr, qm(16, H, 64, 1), FAKE)
+    need = lib.ql_acoustic_model_frames_workspace(C.byref(m), 20, 2, 8, 3)
+    assert need == lib.ql_acoustic_model_workspace(C.byref(m), T, 2) > 0
+    g = lambda dim=40, wsb=need: lib.ql_acoustic_model_forward_frames(
+        C.byref(m), FAKE, 20, 2, dim, 8, 3, FAKE, None, FAKE, wsb, None)
+    assert g(dim=20) == ql.QL_ESHAPE                                   # 8*20 != layers[0].in
+    assert g(wsb=need - 1) == ql.QL_EWORKSPACE
