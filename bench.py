@@ -96,23 +96,52 @@ def model_on_device(ql, workload, torch):
     return w, M, x
 
 
-def time_model(ql, torch, M, x, steps, warmup):
-    """ms per forward pass (events + wall clock), posteriors preallocated."""
-    T, B, _ = x.shape
+def time_model(ql, torch, M, x, steps, warmup, frames=False):
+    """ms per forward pass (events + wall clock), posteriors preallocated.
+    frames: x holds base frames [nframes][B][dim]; the frontend's stacking runs
+    inside the input quantizer."""
+    if frames:
+        T, B = ql.stacked_input_count(x.shape[0]), x.shape[1]
+        fwd = ql.acoustic_model_forward_frames
+    else:
+        T, B, _ = x.shape
+        fwd = ql.acoustic_model_forward
     ws = ql.Workspace()
     post = torch.empty(T, B, M.Wy.rows, dtype=torch.float32, device="cuda")
     for _ in range(warmup):
-        ql.acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+        fwd(M, x, workspace=ws, post=post, check=False)
     ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "warmup")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     with Timer(torch) as tm:
         for _ in range(steps):
-            ql.acoustic_model_forward(M, x, workspace=ws, post=post, check=False)
+            fwd(M, x, workspace=ws, post=post, check=False)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3
     ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "timed steps")
     return tm.ms / steps, wall / steps
+
+
+def table1_sweep(ql, torch, wl, steps, warmup):
+    """The ten architectures of Table 1 (4-5 layers of 300-500 cells; 5 x 500
+    with projections of 100-400 units) with synthetic weights and an 8192-way
+    softmax, streaming one utterance of T = 500 presented frames."""
+    import numpy as np
+    out = []
+    T = 500
+    x = torch.from_numpy(wl.stacked_features(np.random.Generator(np.random.PCG64(0)), T, 1)).cuda()
+    for (layers, hidden, proj) in ((4, 300, 0), (5, 300, 0), (4, 400, 0), (5, 400, 0),
+                                   (4, 500, 0), (5, 500, 0), (5, 500, 100), (5, 500, 200),
+                                   (5, 500, 300), (5, 500, 400)):
+        w = wl.random_model(320, hidden, layers, proj=proj, states=8192, seed=0)
+        M = ql.quantize_model(w, device="cuda")
+        ms, _ = time_model(ql, torch, M, x, steps, warmup)
+        out.append(dict(arch=f"{layers}x{hidden}" + (f" P{proj}" if proj else ""),
+                        ms_per_step=round(ms, 3), frames_per_s=round(T / (ms * 1e-3), 1),
+                        us_per_frame=round(ms * 1e3 / T, 2),
+                        wavefront_layers=ql.stack_layers_per_launch(M, T, 1)))
+        del M
+    return out
 
 
 def recurrence_kernel(ql, torch, M, x, reps):
@@ -333,6 +362,14 @@ def main():
 
     extra = {}
     if not args.quick:
+        fr64 = torch.from_numpy(wl.frames(W64)).cuda()
+        msf, _ = time_model(ql, torch, M64, fr64, max(3, args.steps // 2), args.warmup,
+                            frames=True)
+        extra["frontend_fused"] = dict(
+            workload=W64.name + ", fed 40-dim base frames (8 stacked, every 3rd presented)",
+            ms_per_step=round(msf, 3), frames_per_s=round(frames / (msf * 1e-3), 1))
+        log(f"fused frontend: {extra['frontend_fused']}")
+        del fr64
         W1 = wl.LSTM5x500_S8192_T500_B1
         log(f"setup {W1.name}")
         _, M1, x1 = model_on_device(ql, W1, torch)
@@ -364,6 +401,8 @@ def main():
             batch1=dict(ms_per_step=round(f1, 3), frames_per_s=round(W1.T / (f1 * 1e-3), 1),
                         int8_speedup=round(f1 / ms1, 3)))
         log(f"fp32 model: {extra['fp32_model']}")
+        extra["table1_b1"] = table1_sweep(ql, torch, wl, max(3, args.steps // 4), args.warmup)
+        log(f"Table 1 architectures, batch 1: {extra['table1_b1']}")
         W5 = wl.LSTMP4x2048P512_S16384_T800_B256
         log(f"setup {W5.name}")
         _, M5, x5 = model_on_device(ql, W5, torch)
