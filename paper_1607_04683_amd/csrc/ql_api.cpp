@@ -307,6 +307,52 @@ bool codes_taps_only(const ql_model_taps *taps, int nlayers) {
   return true;
 }
 
+// Layers that all have a projection, at one batch row, run as the projection
+// wavefront (ql_pstack.hip) when at least two of them share a launch.
+bool pstack_shapes(const ql_lstm_layer *layers, int n, int64_t B) {
+  if (B != 1 || n < 2) return false;
+  for (int l = 0; l < n; ++l) {
+    const ql_lstm_layer &L = layers[l];
+    if (L.proj <= 0 || L.hidden > 512 || L.proj > 512 || L.in > 512) return false;
+  }
+  return true;
+}
+PStackArgs pstack_shape_args(const ql_lstm_layer *layers, int n, int64_t T) {
+  PStackArgs a{};
+  a.nl = n < kMaxStack ? n : kMaxStack;
+  a.T = T;
+  for (int k = 0; k < a.nl; ++k) {
+    a.L[k].in = layers[k].in;
+    a.L[k].H = layers[k].hidden;
+    a.L[k].P = layers[k].proj;
+  }
+  return a;
+}
+int pstack_per_launch(const ql_lstm_layer *layers, int n, int64_t T, int64_t B) {
+  if (!pstack_shapes(layers, n, B)) return 1;
+  return pstack_layers_per_launch(pstack_shape_args(layers, n, T));
+}
+PStackLayer pstack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf &out,
+                         const ql_lstm_taps *t) {
+  PStackLayer s{};
+  s.Wx = weight(L.Wx);
+  s.Wh = weight(L.Wh);
+  s.Wr = weight(L.Wr);
+  s.bias = L.bias;
+  s.in = L.in;
+  s.H = L.hidden;
+  s.P = L.proj;
+  s.xin = xin;
+  s.out = OutRows{out.codes, out.ld, out.zero, out.inv_q, out.sums};
+  s.h = nullptr;
+  if (t) {
+    s.tap_codes = t->h_codes;
+    s.tap_zero = t->h_zero;
+    s.tap_inv_q = t->h_inv_q;
+  }
+  return s;
+}
+
 // Workspace of a model forward: exchange scratch first (it holds the timeout
 // flag), then the input codes, W_x x + b, one code buffer per layer, h.
 struct ModelWs {
@@ -331,12 +377,20 @@ ModelWs carve_model(Carve &c, const ql_model &M, int64_t T, int64_t B) {
     const size_t st = stack_ws(M.nlayers < kMaxStack ? M.nlayers : kMaxStack, T, B, maxH);
     rec = rec > st ? rec : st;
   }
+  const bool pst = pstack_shapes(M.layers, M.nlayers, B);
+  if (pst) {
+    int64_t hs[kMaxStack], ps[kMaxStack];
+    const int nl = M.nlayers < kMaxStack ? M.nlayers : kMaxStack;
+    for (int k = 0; k < nl; ++k) hs[k] = maxH, ps[k] = maxP;
+    const size_t st = pstack_ws(hs, ps, nl, T);
+    rec = rec > st ? rec : st;
+  }
   ModelWs w{};
   w.rec = c.take<char>(rec);
   w.xin = take_act(c, MB, M.layers[0].in);
   w.gx = c.take<float>((size_t)(MB * 4 * maxH));
   // one output code buffer per layer (two alternate when layers run one by one)
-  const int nbuf = stackable(M) ? (M.nlayers < 16 ? M.nlayers : 16) : 2;
+  const int nbuf = stackable(M) || pst ? (M.nlayers < 16 ? M.nlayers : 16) : 2;
   for (int i = 0; i < nbuf; ++i) w.out[i] = take_act(c, MB, maxR);
   w.hf = c.take<float>((size_t)(MB * maxR));
   w.sws = c.take<char>(softmax_ws(MB, M.Wy.rows));
@@ -430,10 +484,14 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
   if (quantize_input(fe, T, B, M->layers[0].in, mw.xin, s) != hipSuccess) return QL_EHIP;
   ActRows cur = mw.xin.rows();
   const bool stack = stackable(*M) && codes_taps_only(taps, M->nlayers);
+  const bool pst = !stack && pstack_shapes(M->layers, M->nlayers, B) &&
+                   codes_taps_only(taps, M->nlayers);
   int per_launch = 1;
   if (stack) {
     const int64_t in1 = M->nlayers > 1 ? M->layers[1].in : M->layers[0].in;
     per_launch = stack_layers_per_launch(M->nlayers, T, B, maxH, M->layers[0].in, in1);
+  } else if (pst) {
+    per_launch = pstack_per_launch(M->layers, M->nlayers, T, B);
   }
   for (int l = 0; l < M->nlayers;) {
     const int left = M->nlayers - l;
@@ -459,11 +517,27 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
       l += n;
       continue;
     }
+    if (pst && n >= 2) {
+      PStackArgs pa{};
+      pa.nl = n;
+      pa.T = T;
+      pa.ws = mw.rec;
+      for (int k = 0; k < n; ++k) {
+        const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l + k] : nullptr;
+        pa.L[k] = pstack_layer(M->layers[l + k], k == 0 ? cur : ActRows{}, mw.out[l + k], lt);
+      }
+      bool unsupported = false;
+      if (launch_pstack(pa, s, &unsupported) != hipSuccess) return QL_EHIP;
+      if (unsupported) return QL_EUNSUPPORTED;
+      cur = mw.out[l + n - 1].rows();
+      l += n;
+      continue;
+    }
     const ql_lstm_layer &L = M->layers[l];
     LayerWs w;
     w.rec = mw.rec;
     w.gx = mw.gx;
-    w.hout = mw.out[stack ? l : (l & 1)];
+    w.hout = mw.out[stack || pst ? l : (l & 1)];
     w.hout.ld = round_up(layer_width(L), 64);
     const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l] : nullptr;
     st = run_layer(L, cur, T, B, nullptr, nullptr, mw.hf, nullptr, nullptr, w, lt, s);
@@ -726,6 +800,7 @@ size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T
 int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, int64_t T,
                                         int64_t B) {
   if (!layers || n < 2 || T < 0 || B < 0) return 1;
+  if (pstack_shapes(layers, n, B)) return pstack_per_launch(layers, n, T, B);
   const int64_t H = layers[0].hidden;
   for (int k = 0; k < n; ++k)
     if (layers[k].proj != 0 || layers[k].hidden != H || (k > 0 && layers[k].in != H)) return 1;

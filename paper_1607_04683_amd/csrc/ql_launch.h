@@ -126,6 +126,29 @@ struct StackArgs {
   void *ws;                // stack_ws bytes; timeout flag cleared by the caller
 };
 size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H);
+// ---- stacked layers with a projection, one batch row (ql_pstack.hip)
+struct PStackLayer {
+  WeightMat Wx, Wh, Wr;    // [4H][in], [4H][P], [P][H]
+  const float *bias;       // [4H]
+  int64_t in, H, P;        // input width (layer k > 0: P of layer k-1), cells, projection
+  ActRows xin;             // the launch's first layer only: codes of every x_t
+  OutRows out;             // [T] rows of codes of h_t + params
+  float *h;                // [T][P] fp32 (nullable)
+  int8_t *tap_codes;       // optional taps: [T][P] codes (ld = P), zero, inv_q
+  int32_t *tap_zero;
+  float *tap_inv_q;
+};
+struct PStackArgs {
+  int nl;                  // layers in this launch (1 .. kMaxStack)
+  int64_t T;               // frames (batch 1)
+  PStackLayer L[kMaxStack];
+  void *ws;                // pstack_ws bytes; timeout flag cleared by the caller
+};
+size_t pstack_ws(const int64_t *H, const int64_t *P, int nl, int64_t T);
+hipError_t launch_pstack(const PStackArgs &a, hipStream_t s, bool *unsupported);
+// How many of a.nl layers fit one launch (1: none; use the one-layer path).
+int pstack_layers_per_launch(const PStackArgs &a);
+
 hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported);
 // How many layers of such a stack fit one launch (1: none, use the one-layer path).
 int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0, int64_t in1);

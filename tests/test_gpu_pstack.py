@@ -1,0 +1,88 @@
+"""Stacked projection layers at one batch row in one wavefront launch (the
+5 x 500 / P models of Section 4 streamed frame by frame): codes of every
+layer's h_t bit-exact and posteriors within 1e-4 of the oracle, and the same
+bits as the one-layer-per-launch path."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def ql():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_1607_04683_amd import qlstm
+    qlstm.load()
+    return qlstm
+
+
+def u8(t):
+    return t.cpu().numpy().view(np.uint8) ^ 0x80
+
+
+def _weights(n_in, dims, states, seed):
+    """Layers of different widths: dims = [(H, P), ...], layer k's input = P of k-1."""
+    from paper_1607_04683_amd.workloads import random_model
+    layers = []
+    width = n_in
+    for k, (H, P) in enumerate(dims):
+        layers.append(random_model(width, H, 1, proj=P, seed=seed + k)["layers"][0])
+        width = P
+    rng = np.random.default_rng(seed + 99)
+    return {"layers": layers,
+            "Wy": rng.uniform(-0.08, 0.08, (states, width)).astype(np.float32),
+            "by": rng.uniform(-0.08, 0.08, states).astype(np.float32)}
+
+
+def _case(ql, orc, w, T, seed, gate_blocks=4, proj_blocks=1):
+    x = np.random.default_rng(seed).standard_normal((T, 1, w["layers"][0]["Wx"].shape[1]))
+    x = x.astype(np.float32)
+    Mg = ql.quantize_model(w, gate_blocks=gate_blocks, proj_blocks=proj_blocks)
+    g = ql.acoustic_model_forward(Mg, torch.from_numpy(x).cuda(), taps=("h_codes",))
+    o = orc.acoustic_model_forward(orc.quantize_model(w, gate_blocks, proj_blocks), x, taps=True)
+    for l in range(len(w["layers"])):
+        assert np.array_equal(u8(g["layers"][l]["h_codes"]), o["layers"][l]["h_codes"]), l
+    err = np.max(np.abs(g["post"].cpu().numpy() - o["post"])) if T else 0.0
+    assert err <= TOL, err
+    return Mg, x, g
+
+
+@pytest.mark.parametrize("dims,T", [
+    ([(500, 100)] * 5, 60),                     # Table 1 shapes
+    ([(500, 400)] * 5, 30),
+    ([(64, 24), (40, 30), (64, 5)], 25),        # mixed widths; 5 outputs over 4 tiles
+    ([(48, 16)] * 9, 12),                       # two launches (at most 8 layers in one)
+    ([(500, 200)] * 2, 1),                      # one frame
+])
+def test_projection_wavefront(ql, orc, dims, T):
+    w = _weights(320, dims, 300, seed=len(dims) * 10 + T)
+    Mg, x, g = _case(ql, orc, w, T, seed=T)
+    assert ql.stack_layers_per_launch(Mg, T, 1) >= 2
+
+
+def test_projection_wavefront_row_blocks(ql, orc):
+    w = _weights(320, [(100, 40)] * 3, 200, seed=3)
+    _case(ql, orc, w, 20, seed=4, gate_blocks=400, proj_blocks=40)
+
+
+def test_projection_wavefront_equals_one_layer_path(ql):
+    """Accumulator taps keep the model on the one-layer-per-launch path: its
+    posteriors and codes equal the wavefront's bit for bit."""
+    w = _weights(320, [(500, 200)] * 5, 8192, seed=7)
+    x = torch.from_numpy(np.random.default_rng(9).standard_normal((50, 1, 320)).astype(np.float32))
+    Mg = ql.quantize_model(w)
+    a = ql.acoustic_model_forward(Mg, x.cuda(), taps=("h_codes",))
+    b = ql.acoustic_model_forward(Mg, x.cuda(), taps=True)
+    assert torch.equal(a["post"], b["post"])
+    for l in range(5):
+        assert torch.equal(a["layers"][l]["h_codes"], b["layers"][l]["h_codes"])
+
+
+def test_projection_wavefront_empty(ql):
+    w = _weights(16, [(24, 8)] * 2, 10, seed=1)
+    Mg = ql.quantize_model(w)
+    g = ql.acoustic_model_forward(Mg, torch.zeros(0, 1, 16, device="cuda"))
+    assert g["post"].shape == (0, 1, 10)
