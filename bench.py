@@ -65,7 +65,7 @@ def parse():
                     help="frames of the batch-64 workload the CPU oracle is timed on")
     ap.add_argument("--profile-target", default=None,
                     choices=["stack_b64", "stack_b1", "recurrence_b64", "recurrence_b1",
-                             "gemm8192", "lstmp_b256", "copy"],
+                             "gemm8192", "lstmp_b256", "pstack_b1", "table1", "copy"],
                     help="run only one piece (for hardware-counter passes) and exit")
     return ap.parse_args()
 
@@ -136,10 +136,15 @@ def table1_sweep(ql, torch, wl, steps, warmup):
         w = wl.random_model(320, hidden, layers, proj=proj, states=8192, seed=0)
         M = ql.quantize_model(w, device="cuda")
         ms, _ = time_model(ql, torch, M, x, steps, warmup)
+        # weight codes a frame streams through the layers (decode-style bytes)
+        wbytes = sum(4 * L.hidden * (L.n_in + L.width) + L.proj * L.hidden for L in M.layers)
+        us = ms * 1e3 / T
         out.append(dict(arch=f"{layers}x{hidden}" + (f" P{proj}" if proj else ""),
                         ms_per_step=round(ms, 3), frames_per_s=round(T / (ms * 1e-3), 1),
-                        us_per_frame=round(ms * 1e3 / T, 2),
-                        wavefront_layers=ql.stack_layers_per_launch(M, T, 1)))
+                        us_per_frame=round(us, 2),
+                        wavefront_layers=ql.stack_layers_per_launch(M, T, 1),
+                        weight_bytes_per_frame=wbytes,
+                        weight_frac_of_hbm=round(wbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)))
         del M
     return out
 
@@ -304,6 +309,18 @@ def profile_target(ql, torch, target, reps):
         _, M, x = model_on_device(ql, W, torch)
         out = recurrence_kernel(ql, torch, M, x, reps)
         out["workload"] = W.name
+    elif target == "pstack_b1":
+        import numpy as np
+        T = 500
+        w = wl.random_model(320, 500, 5, proj=200, states=8192, seed=0)
+        M = ql.quantize_model(w, device="cuda")
+        x = torch.from_numpy(wl.stacked_features(np.random.Generator(np.random.PCG64(0)), T,
+                                                 1)).cuda()
+        ms, _ = time_model(ql, torch, M, x, 5, 2)
+        out = dict(workload="5xLSTM500 P200 + softmax8192, T500 B1", ms_per_step=round(ms, 3),
+                   us_per_frame=round(ms * 1e3 / T, 2))
+    elif target == "table1":
+        out = dict(table1_b1=table1_sweep(ql, torch, wl, 5, 2))
     elif target == "gemm8192":
         out = gemm_sweep(ql, torch, 8192, reps)
     elif target == "lstmp_b256":

@@ -13,10 +13,9 @@
 //   3. quantizes m_t (per vector) from the tagged words of all the layer's
 //      tiles and forms its rows of the projection h_t = recover(W_r' m'_t),
 //      which it publishes;
-//   4. off the critical path, while the other tiles finish h_t: takes x_{t+1}
-//      (the launch's first layer reads its codes, a later layer quantizes layer
-//      l-1's published h_{t+1} itself: one vector, one quantization, the same
-//      codes layer l-1 makes of it) and forms the input-side product.
+// and, beside step 1 on two other waves, takes x_t: the launch's first layer
+// reads its codes, a later layer quantizes layer l-1's published h_t itself
+// (one vector, one quantization: the same codes layer l-1 makes of it).
 // Every value exchanged goes into a full-length [T] buffer of 64-bit tagged
 // words (step tag + fp32 value), so no slot is ever reused inside a launch and
 // a layer may run any number of frames ahead of the next.  Every wait is
@@ -26,8 +25,9 @@
 // most 32 tiles, the launch has one workgroup per CU; each reads its XCC_ID and
 // takes the next free slot of its XCD, playing tile `slot` of layer `XCC_ID`.
 // A layer's tiles then share one L2, and m_t, read only by the own layer, goes
-// out with plain stores that stay in that L2.  h_t is also read by the next
-// layer (another XCD) and always goes out with device-coherent stores.
+// out with plain stores that stay in that L2.  h_t goes out twice: with plain
+// stores for the own layer's tiles, and with device-coherent stores into a
+// second buffer for the next layer (another XCD).
 // Otherwise workgroup i plays tile i % G of layer i / G.
 #include "ql_device.h"
 #include "ql_exchange.h"
@@ -116,12 +116,14 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
   RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_rp);  // [0] x, [1] h, [2] m
   const int ldsX = tl.ldXmax, ldsH = tl.ldHmax, ldsP = tl.ldPmax;
 
-  // tagged words of layer k: m [T][H], then h [T][P]
+  // tagged words of layer k: m [T][H], h for the next layer [T][P], then (XCD
+  // layout) h for the own layer [T][P]
   auto mwords = [&](int k) { return reinterpret_cast<uint64_t *>(wsb + tl.layer_off[k]); };
   auto hwords = [&](int k) {
     return reinterpret_cast<uint64_t *>(wsb + tl.layer_off[k]) + T * a.L[k].H;
   };
   uint64_t *mw = mwords(l), *hw = hwords(l);
+  uint64_t *hown = tl.xcd ? hw + T * P : hw;
 
   // ---- prologue: weight slices, column params, bias, c = 0
   for (int idx = tid; idx < nrows * (ldX / 16); idx += blockDim.x) {
@@ -158,24 +160,6 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
   for (int i = tid; i < 16; i += blockDim.x) xch_x[i] = xch_h[i] = xch_m[i] = 0;
   __syncthreads();
 
-  // Codes of x_t into xc, row params into rp[0], then the input-side product.
-  auto input_side = [&](int64_t t) -> bool {
-    if (l == 0) {
-      const int8_t *src = Ly.xin.codes + t * Ly.xin.ld;
-      for (int k = tid; k < ldX / 4; k += blockDim.x)
-        reinterpret_cast<uint32_t *>(xc)[k] = reinterpret_cast<const uint32_t *>(src)[k];
-      if (tid == 0) rp[0] = row_param(Ly.xin.zero[t], Ly.xin.inv_q[t], Ly.xin.sums[t], (int)IN);
-    } else if (tid < 2 * kWave) {
-      if (!quant_row_2w(hwords(l - 1) + t * IN, (uint32_t)(t + 1), (int)IN, xc, ldX, flag, &rp[0],
-                        xch_x))
-        s_abort = 1;
-    }
-    __syncthreads();
-    if (s_abort) return false;
-    products_valu(xc, ldsX, 1, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
-    return true;
-  };
-
   // Codes of row t of this layer's h (quantized here, in hc) to the layer's
   // output rows; this tile's share of the code words, tile 0 the row params.
   auto store_out = [&](int64_t t) {
@@ -197,20 +181,35 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
         Ly.tap_codes[t * P + k] = hc[k];
   };
 
-  if (!input_side(0)) return;
   for (int64_t t = 0; t < T; ++t) {
-    // 1. codes of h_{t-1}: an all-zero h_{-1} quantizes to Q = 1, zero point 0,
-    //    codes V' = 0 (stored -128), which makes W_h h exactly 0
-    if (t == 0) {
-      for (int k = tid; k < ldP; k += blockDim.x) hc[k] = k < P ? (int8_t)-128 : (int8_t)0;
-      if (tid == 0) rp[1] = row_param(0, 1.0f, 0, (int)P);
-    } else if (tid < 2 * kWave) {
-      if (!quant_row_2w(hw + (t - 1) * P, (uint32_t)t, (int)P, hc, ldP, flag, &rp[1], xch_h))
+    // 1. codes of h_{t-1} (waves 0, 1) and of x_t (waves 2, 3 for a later
+    //    layer, which quantizes layer l-1's h_t; waves 4.. copy the input codes
+    //    for the first layer) side by side.  An all-zero h_{-1} quantizes to
+    //    Q = 1, zero point 0, codes V' = 0 (stored -128): W_h h is exactly 0.
+    if (tid < 2 * kWave) {
+      if (t == 0) {
+        for (int k = tid; k < ldP; k += 2 * kWave) hc[k] = k < P ? (int8_t)-128 : (int8_t)0;
+        if (tid == 0) rp[1] = row_param(0, 1.0f, 0, (int)P);
+      } else if (!quant_row_2w(hown + (t - 1) * P, (uint32_t)t, (int)P, hc, ldP, flag, &rp[1],
+                               xch_h)) {
         s_abort = 1;
+      }
+    } else if (l > 0) {
+      if (tid < 4 * kWave &&
+          !quant_row_2w(hwords(l - 1) + t * IN, (uint32_t)(t + 1), (int)IN, xc, ldX, flag, &rp[0],
+                        xch_x, 2))
+        s_abort = 1;
+    } else {
+      const int8_t *src = Ly.xin.codes + t * Ly.xin.ld;
+      for (int k = tid - 2 * kWave; k < ldX / 4; k += (int)blockDim.x - 2 * kWave)
+        reinterpret_cast<uint32_t *>(xc)[k] = reinterpret_cast<const uint32_t *>(src)[k];
+      if (tid == 2 * kWave)
+        rp[0] = row_param(Ly.xin.zero[t], Ly.xin.inv_q[t], Ly.xin.sums[t], (int)IN);
     }
     __syncthreads();
     if (s_abort) return;
     products_valu(hc, ldsP, 1, wh, ldsP, nrows, nrows, ldP, Sh, nrows);
+    products_valu(xc, ldsX, 1, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
     __syncthreads();
 
     // 2. gates: lane 4 jj + gt computes gate gt of cell jj (i, f, g, o)
@@ -248,17 +247,16 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
       const RowParam rm = rp[2];
       const ColParam cr = cpr[tid];
       const float hv = recover(Sr[tid], cr.colterm, cr.ztw, rm.ztx, rm.sigx, cr.iqw, rm.iqx);
+      if (tl.xcd) publish_local(&hown[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       publish(&hw[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       if (Ly.h) Ly.h[t * P + p0 + tid] = hv;
     }
-
-    // 4. next frame's input side while the other tiles finish h_t
-    if (t + 1 < T && !input_side(t + 1)) return;
-    __syncthreads();
+    // the next step's first phase writes only hc, xc, rp[0], rp[1]: none of
+    // them is read after the last barrier
   }
   // codes of the last h
   if (tid < 2 * kWave) {
-    if (!quant_row_2w(hw + (T - 1) * P, (uint32_t)T, (int)P, hc, ldP, flag, &rp[1], xch_h))
+    if (!quant_row_2w(hown + (T - 1) * P, (uint32_t)T, (int)P, hc, ldP, flag, &rp[1], xch_h))
       s_abort = 1;
   }
   __syncthreads();
@@ -319,7 +317,7 @@ static bool plan_pstack(const PStackArgs &a, int cus, int lds_max, PStackTiling 
   size_t woff = kHeaderBytes + kPSlotBytes;
   for (int l = 0; l < a.nl; ++l) {
     tl.layer_off[l] = woff;
-    woff += align_up((size_t)a.T * (a.L[l].H + a.L[l].P) * 8, 256);
+    woff += align_up((size_t)a.T * (a.L[l].H + 2 * a.L[l].P) * 8, 256);
   }
   *out = tl;
   return true;
@@ -327,7 +325,7 @@ static bool plan_pstack(const PStackArgs &a, int cus, int lds_max, PStackTiling 
 
 size_t pstack_ws(const int64_t *H, const int64_t *P, int nl, int64_t T) {
   size_t n = kHeaderBytes + kPSlotBytes;
-  for (int l = 0; l < nl; ++l) n += align_up((size_t)T * (H[l] + P[l]) * 8, 256);
+  for (int l = 0; l < nl; ++l) n += align_up((size_t)T * (H[l] + 2 * P[l]) * 8, 256);
   return n;
 }
 
@@ -366,7 +364,7 @@ hipError_t launch_pstack(const PStackArgs &a, hipStream_t s, bool *unsupported) 
   }
   // slot counters and every tagged word start at 0 (tags count from 1)
   const size_t used = tl.layer_off[a.nl - 1] +
-                      align_up((size_t)a.T * (a.L[a.nl - 1].H + a.L[a.nl - 1].P) * 8, 256);
+                      align_up((size_t)a.T * (a.L[a.nl - 1].H + 2 * a.L[a.nl - 1].P) * 8, 256);
   e = clear_exchange(a.ws, (int64_t)((used - kHeaderBytes) / 8), s);
   if (e != hipSuccess) return e;
   PStackArgs args = a;

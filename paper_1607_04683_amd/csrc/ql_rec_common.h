@@ -184,15 +184,15 @@ __device__ __forceinline__ bool quant_tile(int nvalid, int ntotal, int64_t strid
 }
 
 // One row of K <= 512 published values (tagged words of step tag `tag`)
-// quantized per vector (eq. 2) by waves 0 and 1 together: wave w polls and
-// encodes half w of the row (lane l: elements 4 (w*64 + l) .. +3), and the
+// quantized per vector (eq. 2) by waves w0 and w0 + 1 together: wave w polls
+// and encodes half w of the row (lane l: elements 4 (w*64 + l) .. +3), and the
 // halves' min/max, then their code sums, meet in LDS slots xch[w*8 ..] (data,
 // then a flag holding the tag, released after the data).  The codes go to
 // dst (ldpad <= 512 bytes), the row params to *rp.  False if a wait expired.
 __device__ __forceinline__ bool quant_row_2w(const uint64_t *src, uint32_t tag, int K,
                                              int8_t *dst, int ldpad, int *flag, RowParam *rp,
-                                             int *xch) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, o = 1 - w;
+                                             int *xch, int w0 = 0) {
+  const int lane = threadIdx.x & 63, w = (int)(threadIdx.x >> 6) - w0, o = 1 - w;
   const int kb = 4 * (w * kWave + lane);
   float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   uint32_t got = 0;
