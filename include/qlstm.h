@@ -199,8 +199,8 @@ size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T
 /* How many of the first n layers one launch holds on the current device (the
  * grouping ql_acoustic_model_forward uses); 1 when they cannot share one.
  * Layers that all have a projection (H, P, in <= 512) share launches at batch 1:
- * ql_acoustic_model_forward runs them as a wavefront too, while this entry
- * point and ql_lstm_stack_forward take layers without a projection only. */
+ * ql_acoustic_model_forward runs them as a wavefront too (ql_lstm_stack_forward
+ * takes layers without a projection only). */
 int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, int64_t T,
                                         int64_t B);
 ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,
