@@ -34,10 +34,10 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=4.471e+09, read=2.995e+09, written=1.476e+09,
+TRAFFIC = dict(bytes=4.474e+09, read=2.998e+09, written=1.476e+09,
                sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
                         "ql_launch.h"),
-               sha256="21d23c0e426de2a2c1821b0b9484a0ad5ec024e7a9ad75c6d74f2c76ed2c73cf",
+               sha256="da863718f6d64ad4df4edd88b86ce981047cc2a05551368d16f246af5ad89a35",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 
