@@ -187,20 +187,22 @@ ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const
                                   void *stream);
 
 /* ---- several stacked layers in one launch (Section 4) ---------------------------
- * n layers without projection and of one width H <= 512 (layer k > 0 takes
- * layer k-1's output), run as one persistent launch in which layer k works on
- * frame t while layer k-1 is already on a later frame.  Input: the per-vector
- * codes of x_t (x->rows = T*B, x->cols = layers[0].in).  Output: the codes of
- * every h_t of every layer, h_codes[k] (rows = T*B, cols = H, ld a multiple of
- * 64), and h_last [T][B][H] fp32 of the last layer (nullable); zero initial
- * state.  QL_EUNSUPPORTED when the n layers do not fit one launch.  Same
- * results, bit for bit, as n calls of the one-layer path. */
+ * n layers (layer k > 0 takes layer k-1's output), run as one persistent launch
+ * in which layer k works on frame t while layer k-1 is already on a later frame:
+ * either layers without projection and of one width H <= 512, or (batch 1 only)
+ * layers that all have a projection, with H, P and in <= 512.  Input: the
+ * per-vector codes of x_t (x->rows = T*B, x->cols = layers[0].in).  Output: the
+ * codes of every h_t of every layer, h_codes[k] (rows = T*B, cols = R = P or H,
+ * ld a multiple of 64), and h_last [T][B][R] fp32 of the last layer (nullable);
+ * zero initial state.  QL_EUNSUPPORTED when the n layers do not fit one launch
+ * (or projection layers at B > 1).  Same results, bit for bit, as n calls of the
+ * one-layer path. */
 size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B);
 /* How many of the first n layers one launch holds on the current device (the
  * grouping ql_acoustic_model_forward uses); 1 when they cannot share one.
  * Layers that all have a projection (H, P, in <= 512) share launches at batch 1:
- * ql_acoustic_model_forward runs them as a wavefront too (ql_lstm_stack_forward
- * takes layers without a projection only). */
+ * ql_acoustic_model_forward and ql_lstm_stack_forward run them as a wavefront
+ * too. */
 int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, int64_t T,
                                         int64_t B);
 ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,

@@ -794,6 +794,11 @@ ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const
 
 size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B) {
   if (!layers || n < 1 || n > kMaxStack || T < 0 || B < 0) return 0;
+  if (layers[0].proj > 0) {  // the projection wavefront (batch 1)
+    int64_t hs[kMaxStack], ps[kMaxStack];
+    for (int k = 0; k < n; ++k) hs[k] = layers[k].hidden, ps[k] = layers[k].proj;
+    return align_up(pstack_ws(hs, ps, n, T), 256);
+  }
   return align_up(stack_ws(n, T, B, layers[0].hidden), 256);
 }
 
@@ -813,13 +818,19 @@ ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql
   if (!layers || !x || !h_codes) return QL_EINVAL;
   if (n < 1 || n > kMaxStack || T < 0 || B < 0) return QL_ESHAPE;
   const int64_t H = layers[0].hidden;
+  const bool proj = layers[0].proj > 0;
   for (int k = 0; k < n; ++k) {
     const ql_status st = check_layer(&layers[k]);
     if (st != QL_OK) return st;
-    if (layers[k].proj != 0 || layers[k].hidden != H) return QL_ESHAPE;
-    if (k > 0 && layers[k].in != H) return QL_ESHAPE;
+    if (proj) {  // every layer projected, each taking the previous one's P outputs
+      if (layers[k].proj <= 0 || (k > 0 && layers[k].in != layers[k - 1].proj)) return QL_ESHAPE;
+    } else {
+      if (layers[k].proj != 0 || layers[k].hidden != H) return QL_ESHAPE;
+      if (k > 0 && layers[k].in != H) return QL_ESHAPE;
+    }
+    const int64_t R = layer_width(layers[k]);
     const ql_qact &o = h_codes[k];
-    if (o.rows != T * B || o.cols != H || o.ld < round_up(H, 64) || o.ld % 64) return QL_ESHAPE;
+    if (o.rows != T * B || o.cols != R || o.ld < round_up(R, 64) || o.ld % 64) return QL_ESHAPE;
     if (T * B > 0 && (!o.codes || !o.zero || !o.inv_q || !o.sums)) return QL_EINVAL;
   }
   if (x->rows != T * B || x->cols != layers[0].in || x->ld < round_up(x->cols, 64) || x->ld % 64)
@@ -830,6 +841,22 @@ ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql
   hipStream_t s = as_stream(stream);
   if (reset_recurrent_flag(ws, s) != hipSuccess) return QL_EHIP;
   if (T == 0 || B == 0) return QL_OK;
+  if (proj) {
+    if (B != 1) return QL_EUNSUPPORTED;  // batched projection layers: one layer per call
+    PStackArgs pa{};
+    pa.nl = n;
+    pa.T = T;
+    pa.ws = ws;
+    for (int k = 0; k < n; ++k) {
+      const ActRows xin = k == 0 ? ActRows{x->codes, x->ld, x->zero, x->inv_q, x->sums} : ActRows{};
+      ActBuf out{h_codes[k].codes, h_codes[k].ld, h_codes[k].zero, h_codes[k].sums, h_codes[k].inv_q};
+      pa.L[k] = pstack_layer(layers[k], xin, out, nullptr);
+      if (k == n - 1) pa.L[k].h = h_last;
+    }
+    bool unsupported = false;
+    if (launch_pstack(pa, s, &unsupported) != hipSuccess) return QL_EHIP;
+    return unsupported ? QL_EUNSUPPORTED : QL_OK;
+  }
   StackArgs sa{};
   sa.nl = n;
   sa.T = T;

@@ -649,16 +649,16 @@ def quantize_activations(X: torch.Tensor, out: QAct | None = None) -> QAct:
 def lstm_stack_forward(layers: list, x: QAct, T: int, B: int, want_h: bool = False,
                        outs: list | None = None, workspace: Workspace | None = None,
                        check: bool = True):
-    """n stacked layers (no projection, one width) in one launch from input
-    codes x (T*B rows) -> dict(codes=[QAct per layer], h=[T][B][H] of the last)."""
+    """n stacked layers (no projection and one width, or all projected at
+    B = 1) in one launch from input codes x (T*B rows) -> dict(codes=[QAct per
+    layer], h=[T][B][R] of the last)."""
     lib = load()
     n = len(layers)
-    H = layers[0].hidden
     dev = x.codes.device
     arr = (CLayer * n)(*[L.cstruct() for L in layers])
-    outs = outs or [QAct.empty(T * B, H, dev) for _ in range(n)]
+    outs = outs or [QAct.empty(T * B, L.width, dev) for L in layers]
     oarr = (CQAct * n)(*[o.cstruct() for o in outs])
-    h = torch.empty(T, B, H, dtype=torch.float32, device=dev) if want_h else None
+    h = torch.empty(T, B, layers[-1].width, dtype=torch.float32, device=dev) if want_h else None
     nbytes = lib.ql_lstm_stack_workspace(arr, n, T, B)
     ws = (workspace or Workspace()).get(nbytes, dev)
     cx = x.cstruct()

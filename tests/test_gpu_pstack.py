@@ -86,3 +86,28 @@ def test_projection_wavefront_empty(ql):
     Mg = ql.quantize_model(w)
     g = ql.acoustic_model_forward(Mg, torch.zeros(0, 1, 16, device="cuda"))
     assert g["post"].shape == (0, 1, 10)
+
+
+def test_lstm_stack_forward_entry_projection(ql, orc):
+    """ql_lstm_stack_forward with projection layers at batch 1: every layer's
+    codes and row params and the last layer's fp32 h equal the oracle's
+    layer-by-layer evaluation."""
+    T = 13
+    w = _weights(40, [(48, 20), (36, 28), (48, 12)], 10, seed=5)
+    x = np.random.default_rng(2).standard_normal((T, 1, 40)).astype(np.float32)
+    layers = [ql.quantize_layer(L) for L in w["layers"]]
+    xq = ql.quantize_activations(torch.from_numpy(x.reshape(T, 40)).cuda())
+    g = ql.lstm_stack_forward(layers, xq, T, 1, want_h=True)
+    cur = x
+    for k, (L, P) in enumerate(zip(w["layers"], (20, 28, 12))):
+        o = orc.lstm_layer_forward(orc.quantize_layer(L), cur, taps=True)
+        got = u8(g["codes"][k].codes)[:, :P].reshape(T, 1, P)
+        assert np.array_equal(got, o["h_codes"]), f"layer {k}"
+        assert np.array_equal(g["codes"][k].zero.cpu().numpy().reshape(T, 1), o["h_zero"])
+        assert np.array_equal(g["codes"][k].inv_q.cpu().numpy().reshape(T, 1), o["h_inv_q"])
+        cur = o["h"]
+    assert np.array_equal(g["h"].cpu().numpy(), cur)
+    # batched projection layers are not taken by this entry point
+    xb = ql.quantize_activations(torch.zeros(T * 2, 40, device="cuda"))
+    with pytest.raises(ql.QLError):
+        ql.lstm_stack_forward(layers, xb, T, 2)
