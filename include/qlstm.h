@@ -302,7 +302,9 @@ ql_status ql_f32_acoustic_model_forward(const ql_f32_model *M, const float *feat
 ql_status ql_workspace_status(const void *ws, void *stream);
 const char *ql_status_str(ql_status s);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
- * 2 = tanh) -- the exact functions the LSTM kernels use. */
+ * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,
+ * defined for d in [1, 2^126) and equal there to IEEE division) -- the exact
+ * functions the LSTM kernels use. */
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream);
 
 #ifdef __cplusplus

@@ -885,7 +885,7 @@ ql_status ql_workspace_status(const void *ws, void *stream) {
 
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {
   if (n > 0 && (!x || !y)) return QL_EINVAL;
-  if (fn < 0 || fn > 2) return QL_EINVAL;
+  if (fn < 0 || fn > 3) return QL_EINVAL;
   if (n < 0) return QL_ESHAPE;
   return from_hip(launch_gate_fn(fn, x, y, n, as_stream(stream)));
 }

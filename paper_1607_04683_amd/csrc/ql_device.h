@@ -47,7 +47,20 @@ __device__ __forceinline__ float exp_cw(float x) {
   const float scale = __int_as_float(((int)n + 127) << 23);
   return p * scale;
 }
-__device__ __forceinline__ float sigmoid_cw(float x) { return 1.0f / (1.0f + exp_cw(-x)); }
+// 1 / d for d in [1, 2^126) (every denominator 1 + e^-x of the gate
+// functions), correctly rounded: v_rcp_f32 refined by two Newton steps whose
+// residual and update are each one fused multiply-add (Markstein's reciprocal,
+// IBM J. Res. Dev. 34(1), 1990).  Equal bit for bit to IEEE division 1.0f / d
+// (checked over every float in [1, 6.1e37]), in 5 instructions instead of the
+// 11 of the general division sequence.
+__device__ __forceinline__ float recip_ge1(float d) {
+  float r = __builtin_amdgcn_rcpf(d);
+  float e = __builtin_fmaf(-d, r, 1.0f);
+  r = __builtin_fmaf(e, r, r);
+  e = __builtin_fmaf(-d, r, 1.0f);
+  return __builtin_fmaf(e, r, r);
+}
+__device__ __forceinline__ float sigmoid_cw(float x) { return recip_ge1(1.0f + exp_cw(-x)); }
 __device__ __forceinline__ float tanh_cw(float x) { return 2.0f * sigmoid_cw(2.0f * x) - 1.0f; }
 
 // ---------------------------------------------------------------------------

@@ -246,7 +246,7 @@ __global__ void k_gate_fn(int fn, const float *__restrict__ x, float *__restrict
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const float v = x[i];
-  y[i] = fn == 0 ? exp_cw(v) : fn == 1 ? sigmoid_cw(v) : tanh_cw(v);
+  y[i] = fn == 0 ? exp_cw(v) : fn == 1 ? sigmoid_cw(v) : fn == 2 ? tanh_cw(v) : recip_ge1(v);
 }
 
 // ---------------------------------------------------------------- launchers

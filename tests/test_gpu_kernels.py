@@ -34,6 +34,23 @@ def test_gate_functions_bit_exact(ql, orc):
         assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), fn
 
 
+def test_gate_reciprocal_equals_ieee_division(ql):
+    """The reciprocal inside sigmoid (v_rcp_f32 + two Newton steps) against
+    IEEE fp32 division 1 / d on the CPU: every mantissa at the bottom, middle
+    and top binades of the gate denominators 1 + e^-x (x clamped to 87, so
+    d <= 1 + e^87 < 6.1e37), and the whole top range up to 6.1e37."""
+    mant = np.arange(1 << 23, dtype=np.uint32)
+    top = np.float32(6.1e37).view(np.uint32)
+    chunks = [(np.uint32(e + 127) << np.uint32(23)) | mant for e in (0, 1, 2, 23, 24, 60, 100)]
+    chunks.append(np.arange(np.uint32(125 + 127) << np.uint32(23), top + 1, dtype=np.uint32))
+    for bits in chunks:
+        d = bits.view(np.float32)
+        got = ql.gate_fn(3, torch.from_numpy(d).cuda()).cpu().numpy()
+        want = np.float32(1.0) / d
+        bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+        assert bad.size == 0, (d[bad[:4]], got[bad[:4]], want[bad[:4]])
+
+
 @pytest.mark.parametrize("rows,cols,nblocks", [(2000, 320, 4), (2000, 500, 4), (256, 128, 1),
                                                (8192, 512, 1), (37, 5, 1), (64, 1, 4),
                                                (12, 130, 3)])
