@@ -183,8 +183,8 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
 
   for (int64_t t = 0; t < T; ++t) {
     // 1. codes of h_{t-1} (waves 0, 1) and of x_t (waves 2, 3 for a later
-    //    layer, which quantizes layer l-1's h_t; waves 4.. copy the input codes
-    //    for the first layer) side by side.  An all-zero h_{-1} quantizes to
+    //    layer, which quantizes layer l-1's h_t; waves 2 .. 7 copy the input
+    //    codes for the first layer) side by side.  An all-zero h_{-1} quantizes to
     //    Q = 1, zero point 0, codes V' = 0 (stored -128): W_h h is exactly 0.
     if (tid < 2 * kWave) {
       if (t == 0) {
