@@ -111,3 +111,20 @@ def test_lstm_stack_forward_entry_projection(ql, orc):
     xb = ql.quantize_activations(torch.zeros(T * 2, 40, device="cuda"))
     with pytest.raises(ql.QLError):
         ql.lstm_stack_forward(layers, xb, T, 2)
+
+
+@pytest.mark.parametrize("P", [100, 400])
+def test_projection_wavefront_table1_full_size(ql, orc, P):
+    """The bench's Table 1 configuration: 5 x 500 cells with P projections and
+    an 8192-way softmax, one utterance of T = 500 presented frames (seed 0)."""
+    from paper_1607_04683_amd.workloads import random_model, stacked_features
+    T = 500
+    w = random_model(320, 500, 5, proj=P, states=8192, seed=0)
+    x = stacked_features(np.random.Generator(np.random.PCG64(0)), T, 1)
+    Mg = ql.quantize_model(w)
+    assert ql.stack_layers_per_launch(Mg, T, 1) == 5
+    g = ql.acoustic_model_forward(Mg, torch.from_numpy(x).cuda(), taps=("h_codes",))
+    o = orc.acoustic_model_forward(orc.quantize_model(w), x, taps=True)
+    for l in range(5):
+        assert np.array_equal(u8(g["layers"][l]["h_codes"]), o["layers"][l]["h_codes"]), l
+    assert np.max(np.abs(g["post"].cpu().numpy() - o["post"])) <= TOL
