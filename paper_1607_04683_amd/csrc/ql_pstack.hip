@@ -7,7 +7,8 @@
 // in LDS) and v rows of the layer's projection W_r' (also resident).  Per
 // frame t it
 //   1. quantizes h_{t-1} (eq. 2, per vector) from the layer's tagged words and
-//      forms the recurrent product W_h' h'_{t-1} for its gate rows;
+//      forms the recurrent product W_h' h'_{t-1} for its gate rows (MFMA, the
+//      vector as row 0 of a 16-row block);
 //   2. recovers both products (eq. 1 / eq. 3), (W_x x + b) + W_h h, runs the
 //      gates and the cell update, and publishes its cells of m_t;
 //   3. quantizes m_t (per vector) from the tagged words of all the layer's
@@ -158,6 +159,10 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
   for (int j = tid; j < u; j += blockDim.x) cst[j] = 0.0f;
   if (tid == 0) s_abort = 0;
   for (int i = tid; i < 16; i += blockDim.x) xch_x[i] = xch_h[i] = xch_m[i] = 0;
+  // the codes of x_t and h_{t-1} are row 0 of 16-row blocks whose other rows
+  // stay zero, so the gate-row products run on MFMA (rows 1..15 give 0)
+  for (int k = tid; k < 16 * ldsX; k += blockDim.x) xc[k] = 0;
+  for (int k = tid; k < 16 * ldsP; k += blockDim.x) hc[k] = 0;
   __syncthreads();
 
   // Codes of row t of this layer's h (quantized here, in hc) to the layer's
@@ -208,8 +213,8 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
     }
     __syncthreads();
     if (s_abort) return;
-    products_valu(hc, ldsP, 1, wh, ldsP, nrows, nrows, ldP, Sh, nrows);
-    products_valu(xc, ldsX, 1, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
+    products_mfma(hc, ldsP, 16, wh, ldsP, nrows, nrows, ldP, Sh, nrows);
+    products_mfma(xc, ldsX, 16, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
     __syncthreads();
 
     // 2. gates: lane 4 jj + gt computes gate gt of cell jj (i, f, g, o)
@@ -281,6 +286,7 @@ static bool plan_pstack(const PStackArgs &a, int cus, int lds_max, PStackTiling 
   const int share = cus / a.nl;
   if (share < 1) return false;
   tl.u = (int)std::max<int64_t>(20, (maxH + share - 1) / share);
+  tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows in whole 16-row MFMA tiles
   tl.G = (int)((maxH + tl.u - 1) / tl.u);
   tl.v = (int)((maxP + tl.G - 1) / tl.G);
   if (4 * tl.u > kPThreads || tl.v > kPThreads) return false;
@@ -297,11 +303,11 @@ static bool plan_pstack(const PStackArgs &a, int cus, int lds_max, PStackTiling 
   tl.off_wx = take((size_t)nrows * tl.ldXmax);
   tl.off_wh = take((size_t)nrows * tl.ldPmax);
   tl.off_wr = take((size_t)tl.v * tl.ldHmax);
-  tl.off_xc = take(tl.ldXmax);
-  tl.off_hc = take(tl.ldPmax);
+  tl.off_xc = take((size_t)16 * tl.ldXmax);
+  tl.off_hc = take((size_t)16 * tl.ldPmax);
   tl.off_mc = take(tl.ldHmax);
-  tl.off_sx = take((size_t)nrows * 4);
-  tl.off_sh = take((size_t)nrows * 4);
+  tl.off_sx = take((size_t)16 * nrows * 4);
+  tl.off_sh = take((size_t)16 * nrows * 4);
   tl.off_sr = take((size_t)tl.v * 4);
   tl.off_cpx = take((size_t)nrows * sizeof(ColParam));
   tl.off_cph = take((size_t)nrows * sizeof(ColParam));
