@@ -230,6 +230,11 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     bsl[r] = Ly.bias[n];
   }
   for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) cst[idx] = 0.0f;
+  if constexpr (!MFA) {  // rows 1..15 of the one-row code blocks stay zero
+    int8_t *xh2 = reinterpret_cast<int8_t *>(smem + tl.off_xh2);
+    for (int k = tid; k < 16 * tl.ldsX; k += blockDim.x) xh[k] = xh2[k] = 0;
+    for (int k = tid; k < 16 * tl.ldsXx; k += blockDim.x) xx[k] = 0;
+  }
   __syncthreads();
 
   // Counter mode: the codes of x_t (the input, or layer l-1's h_t) are loaded
@@ -570,7 +575,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
     __syncthreads();
 
-    products_valu(xx, tl.ldsXx, nb, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
+    products_mfma(xx, tl.ldsXx, 16, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
     __syncthreads();
     return true;
   };
@@ -720,7 +725,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     rph = rphb[t & 1];
 
     // ---- 1. the recurrent product (the input side's is already in Sx)
-    products_valu(xh, tl.ldsX, nb, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+    products_mfma(xh, tl.ldsX, 16, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
     __syncthreads();
 
     // ---- 2. recover, gates, cell; publish h_t
@@ -777,7 +782,7 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
     if (nut < 1) return false;
     tl.u = (int)((H + nut - 1) / nut);
   }
-  if (tl.mfma) tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16
+  tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16 (MFMA tiles)
   tl.nut = (int)((H + tl.u - 1) / tl.u);
   // the x-code prefetch holds 4 words of 8 codes per thread
   if (tl.ldH > 512 || (size_t)(tl.mfma ? bB : 0) * (tl.ldXmax / 8) > 4 * (size_t)kStackThreads)
@@ -805,12 +810,16 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   };
   tl.off_wh = take((size_t)nrows * tl.ldsW);
   tl.off_wx = take((size_t)nrows * tl.ldsWx);
-  tl.off_xh = take((size_t)tl.bB * tl.ldsX);
-  tl.off_xx = take((size_t)tl.bB * tl.ldsXx);
-  // the codes of x_t are consumed (their product formed) before the
-  // recurrent product is written, so Sh may share their space
-  tl.off_sh = (size_t)nrows * 4 <= (size_t)tl.ldsXx ? tl.off_xx : take((size_t)tl.bB * nrows * 4);
-  tl.off_sx = take((size_t)tl.bB * nrows * 4);
+  // one-row tiles keep their row of codes as row 0 of a 16-row block whose
+  // other rows stay zero, so their products run on MFMA too
+  const int rowsB = tl.mfma ? tl.bB : 16;
+  tl.off_xh = take((size_t)rowsB * tl.ldsX);
+  tl.off_xx = take((size_t)rowsB * tl.ldsXx);
+  // batched tiles: the codes of x_t are consumed (their product formed)
+  // before the recurrent product is written, so Sh may share their space
+  tl.off_sh = tl.mfma && (size_t)nrows * 4 <= (size_t)tl.ldsXx ? tl.off_xx
+                                                               : take((size_t)rowsB * nrows * 4);
+  tl.off_sx = take((size_t)rowsB * nrows * 4);
   tl.off_c = take((size_t)tl.bB * tl.u * 4);
   tl.off_colh = take((size_t)nrows * sizeof(ColParam));
   tl.off_colx = take((size_t)nrows * sizeof(ColParam));
@@ -818,7 +827,7 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   tl.off_rowx = take((size_t)tl.bB * sizeof(RowParam));
   tl.off_bias = take((size_t)nrows * 4);
   // one-row tiles make the codes of h_t while h_{t-1}'s are still being shared
-  tl.off_xh2 = tl.mfma ? tl.off_xh : take((size_t)tl.bB * tl.ldsX);
+  tl.off_xh2 = tl.mfma ? tl.off_xh : take((size_t)rowsB * tl.ldsX);
   tl.off_rowh2 = tl.mfma ? tl.off_rowh : take((size_t)tl.bB * sizeof(RowParam));
   tl.lds_bytes = off;
   if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
