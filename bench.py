@@ -34,10 +34,10 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=4.471e+09, read=2.995e+09, written=1.476e+09,
+TRAFFIC = dict(bytes=4.474e+09, read=2.998e+09, written=1.476e+09,
                sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
                         "ql_launch.h"),
-               sha256="02ced77456b0c20edb0117b89c7ef9a8005a869d6ccbd68c837b8a769f5f5996",
+               sha256="e64a7c10121af3fd3d1efc72feb2dc3842363e46398ad3d30bad269725d3c532",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 

@@ -782,6 +782,14 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
     if (nut < 1) return false;
     tl.u = (int)((H + nut - 1) / nut);
   }
+  // one row with MFMA products: tiles of at least 16 cells over up to a whole
+  // XCD per layer (five 500-cell layers: 32 tiles of 16 cells 4.39 us a frame,
+  // 25 of 20 4.47, 21 of 24 4.44, 42 of 12 4.77; five 300-cell layers: 19 of
+  // 16 4.04, 25 of 12 4.08)
+  if (bB == 1) {
+    const int64_t u16 = std::max<int64_t>(16, (H + kXcdCus - 1) / kXcdCus);
+    if ((H + u16 - 1) / u16 <= cus / a.nl) tl.u = (int)u16;
+  }
   tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16 (MFMA tiles)
   tl.nut = (int)((H + tl.u - 1) / tl.u);
   // the x-code prefetch holds 4 words of 8 codes per thread
