@@ -108,7 +108,9 @@ typedef struct {
 
 /* Optional diagnostic outputs of one LSTM layer (every pointer nullable,
  * device memory).  acc_* are the raw 8-bit-domain accumulators
- * sum_k W'[n][k] x'[k] of eq. 1 before zero-point terms and recovery. */
+ * sum_k W'[n][k] x'[k] of eq. 1 before zero-point terms and recovery (gate
+ * row n = g H + j, gates i, f, g, o).  Every kernel that runs the layer fills
+ * every tap it is given, the layer wavefronts included. */
 typedef struct {
   int32_t *acc_x;   /* [T][B][4H] input products                              */
   int32_t *acc_h;   /* [T][B][4H] recurrent products (h_{t-1})                */
@@ -116,7 +118,18 @@ typedef struct {
   int8_t *h_codes;  /* [T][B][R]  codes of h_t (device code layout, ld = R)   */
   int32_t *h_zero;  /* [T][B]     zero point of h_t                           */
   float *h_inv_q;   /* [T][B]     recovery factor of h_t                      */
+  float *h;         /* [T][B][R]  fp32 h_t; honoured by the model and stack
+                       forwards (the one-layer entry points return h anyway)  */
 } ql_lstm_taps;
+
+/* Recurrent state of one layer at a chunk boundary of a stream (Section 4:
+ * the network runs on a live utterance, one frame per 30 ms): h [B][R] and
+ * c [B][H] fp32, device memory.  Both pointers nullable (zeros in, not
+ * written out). */
+typedef struct {
+  float *h;
+  float *c;
+} ql_lstm_state;
 
 typedef struct {
   const ql_lstm_taps *layers; /* host array [nlayers] or NULL                 */
@@ -193,10 +206,12 @@ ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const
  * layers that all have a projection, with H, P and in <= 512.  Input: the
  * per-vector codes of x_t (x->rows = T*B, x->cols = layers[0].in).  Output: the
  * codes of every h_t of every layer, h_codes[k] (rows = T*B, cols = R = P or H,
- * ld a multiple of 64), and h_last [T][B][R] fp32 of the last layer (nullable);
- * zero initial state.  QL_EUNSUPPORTED when the n layers do not fit one launch
- * (or projection layers at B > 1).  Same results, bit for bit, as n calls of the
- * one-layer path. */
+ * ld a multiple of 64), and h_last [T][B][R] fp32 of the last layer (nullable).
+ * state_in / state_out (host arrays of n descriptors, or NULL): each layer's
+ * initial state (NULL or null pointers: zeros) and final state; in and out
+ * must not overlap.  taps: host array of n, or NULL.  QL_EUNSUPPORTED when the
+ * n layers do not fit one launch (or projection layers at B > 1).  Same
+ * results, bit for bit, as n calls of the one-layer path. */
 size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B);
 /* How many of the first n layers one launch holds on the current device (the
  * grouping ql_acoustic_model_forward uses); 1 when they cannot share one.
@@ -207,7 +222,9 @@ int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, 
                                         int64_t B);
 ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,
                                 int64_t T, int64_t B, const ql_qact *h_codes, float *h_last,
-                                void *ws, size_t ws_bytes, void *stream);
+                                const ql_lstm_state *state_in, const ql_lstm_state *state_out,
+                                const ql_lstm_taps *taps, void *ws, size_t ws_bytes,
+                                void *stream);
 
 /* ---- the recurrence of one layer alone (Section 4) ------------------------------
  * Given the input pre-activations gx [T][B][4H] fp32 = R(Mult(Q(x_t), W_x')) + b
@@ -230,6 +247,17 @@ size_t ql_acoustic_model_workspace(const ql_model *M, int64_t T, int64_t B);
 ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T,
                                     int64_t B, float *post, const ql_model_taps *taps,
                                     void *ws, size_t ws_bytes, void *stream);
+/* The same for one chunk of a stream (Section 4: a live utterance evaluated
+ * as its frames arrive): state_in / state_out are host arrays of nlayers
+ * per-layer states (either NULL: zeros in / nothing out); they must not
+ * overlap.  Calls chained through state_out -> state_in give, bit for bit,
+ * the posteriors of one call over the whole utterance.  Workspace as
+ * ql_acoustic_model_workspace. */
+ql_status ql_acoustic_model_forward_stream(const ql_model *M, const float *feats, int64_t T,
+                                           int64_t B, const ql_lstm_state *state_in,
+                                           const ql_lstm_state *state_out, float *post,
+                                           const ql_model_taps *taps, void *ws, size_t ws_bytes,
+                                           void *stream);
 
 /* ---- frontend fused into the input quantizer (Section 4) ------------------------
  * The network's input at presented step t of utterance b is the concatenation of

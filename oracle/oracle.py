@@ -65,7 +65,7 @@ class Model(C.Structure):
 class Taps(C.Structure):
     _fields_ = [("acc_x", C.c_void_p), ("acc_h", C.c_void_p), ("acc_r", C.c_void_p),
                 ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p),
-                ("c", C.c_void_p)]
+                ("c", C.c_void_p), ("h", C.c_void_p)]
 
 
 class LayerF32(C.Structure):
@@ -272,9 +272,10 @@ def _taps_arrays(T, B, H, P):
     t = dict(acc_x=np.empty((T, B, 4 * H), np.int32), acc_h=np.empty((T, B, 4 * H), np.int32),
              acc_r=np.empty((T, B, P), np.int32) if P else None,
              h_codes=np.empty((T, B, RD), np.uint8), h_zero=np.empty((T, B), np.int32),
-             h_inv_q=np.empty((T, B), np.float32), c=np.empty((T, B, H), np.float32))
+             h_inv_q=np.empty((T, B), np.float32), c=np.empty((T, B, H), np.float32),
+             h=np.empty((T, B, RD), np.float32))
     ts = Taps(*[_p(t[k]) for k in ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero",
-                                   "h_inv_q", "c")])
+                                   "h_inv_q", "c", "h")])
     return t, ts
 
 

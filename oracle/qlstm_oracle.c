@@ -342,6 +342,7 @@ int oracle_lstm_layer_forward(const orc_layer *L, const float *x, int64_t T,
       memcpy(h + row * RD, hn, sizeof(float) * (size_t)RD);
       memcpy(hprev, hn, sizeof(float) * (size_t)RD);
       if (taps && taps->c) memcpy(taps->c + row * H, cprev, sizeof(float) * (size_t)H);
+      if (taps && taps->h) memcpy(taps->h + row * RD, hn, sizeof(float) * (size_t)RD);
       if (taps && (taps->h_codes || taps->h_zero || taps->h_inv_q)) {
         orc_qparams pn;
         oracle_quantize_set(hn, RD, hc, &pn, NULL);

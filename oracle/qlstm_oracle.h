@@ -78,6 +78,7 @@ typedef struct {
   int32_t *h_zero;  /* [T][B]     zero point round(Q vmin) of h_t            */
   float *h_inv_q;   /* [T][B]     recovery factor of h_t                     */
   float *c;         /* [T][B][H]  cell state after step t                    */
+  float *h;         /* [T][B][R]  the layer's fp32 output h_t                */
 } orc_layer_taps;
 
 /* ---- scalar pieces ------------------------------------------------------ */

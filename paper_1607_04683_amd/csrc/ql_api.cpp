@@ -298,14 +298,12 @@ bool stackable(const ql_model &M) {
   }
   return true;
 }
-bool codes_taps_only(const ql_model_taps *taps, int nlayers) {
-  if (!taps || !taps->layers) return true;
-  for (int l = 0; l < nlayers; ++l) {
-    const ql_lstm_taps &t = taps->layers[l];
-    if (t.acc_x || t.acc_h || t.acc_r) return false;
-  }
-  return true;
-}
+// Initial / final state of layer l of a call (host arrays of per-layer
+// descriptors, each nullable).
+const float *st_h(const ql_lstm_state *s, int l) { return s ? s[l].h : nullptr; }
+const float *st_c(const ql_lstm_state *s, int l) { return s ? s[l].c : nullptr; }
+float *st_hout(const ql_lstm_state *s, int l) { return s ? s[l].h : nullptr; }
+float *st_cout(const ql_lstm_state *s, int l) { return s ? s[l].c : nullptr; }
 
 // Layers that all have a projection, at one batch row, run as the projection
 // wavefront (ql_pstack.hip) when at least two of them share a launch.
@@ -333,7 +331,8 @@ int pstack_per_launch(const ql_lstm_layer *layers, int n, int64_t T, int64_t B) 
   return pstack_layers_per_launch(pstack_shape_args(layers, n, T));
 }
 PStackLayer pstack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf &out,
-                         const ql_lstm_taps *t) {
+                         const ql_lstm_taps *t, const ql_lstm_state *s0, const ql_lstm_state *s1,
+                         int l) {
   PStackLayer s{};
   s.Wx = weight(L.Wx);
   s.Wh = weight(L.Wh);
@@ -349,7 +348,15 @@ PStackLayer pstack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBu
     s.tap_codes = t->h_codes;
     s.tap_zero = t->h_zero;
     s.tap_inv_q = t->h_inv_q;
+    s.acc_x = t->acc_x;
+    s.acc_h = t->acc_h;
+    s.acc_r = t->acc_r;
+    s.h = t->h;
   }
+  s.h0 = st_h(s0, l);
+  s.c0 = st_c(s0, l);
+  s.hT = st_hout(s1, l);
+  s.cT = st_cout(s1, l);
   return s;
 }
 
@@ -398,7 +405,8 @@ ModelWs carve_model(Carve &c, const ql_model &M, int64_t T, int64_t B) {
 }
 
 StackLayer stack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf &out,
-                       const ql_lstm_taps *t) {
+                       const ql_lstm_taps *t, const ql_lstm_state *s0, const ql_lstm_state *s1,
+                       int l) {
   StackLayer s{};
   s.Wx = weight(L.Wx);
   s.Wh = weight(L.Wh);
@@ -411,7 +419,14 @@ StackLayer stack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf 
     s.tap_codes = t->h_codes;
     s.tap_zero = t->h_zero;
     s.tap_inv_q = t->h_inv_q;
+    s.acc_x = t->acc_x;
+    s.acc_h = t->acc_h;
+    s.h = t->h;
   }
+  s.h0 = st_h(s0, l);
+  s.c0 = st_c(s0, l);
+  s.hT = st_hout(s1, l);
+  s.cT = st_cout(s1, l);
   return s;
 }
 
@@ -450,6 +465,7 @@ hipError_t quantize_input(const Frontend &f, int64_t T, int64_t B, int64_t in, c
 }
 
 ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_t B, float *post,
+                        const ql_lstm_state *s0, const ql_lstm_state *s1,
                         const ql_model_taps *taps, void *ws, size_t ws_bytes, void *stream) {
   if (!M || !M->layers || !M->by) return QL_EINVAL;
   if (M->nlayers <= 0 || T < 0 || B < 0) return QL_ESHAPE;
@@ -483,9 +499,8 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
 
   if (quantize_input(fe, T, B, M->layers[0].in, mw.xin, s) != hipSuccess) return QL_EHIP;
   ActRows cur = mw.xin.rows();
-  const bool stack = stackable(*M) && codes_taps_only(taps, M->nlayers);
-  const bool pst = !stack && pstack_shapes(M->layers, M->nlayers, B) &&
-                   codes_taps_only(taps, M->nlayers);
+  const bool stack = stackable(*M);
+  const bool pst = !stack && pstack_shapes(M->layers, M->nlayers, B);
   int per_launch = 1;
   if (stack) {
     const int64_t in1 = M->nlayers > 1 ? M->layers[1].in : M->layers[0].in;
@@ -508,7 +523,7 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
       for (int k = 0; k < n; ++k) {
         const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l + k] : nullptr;
         const ActRows xin = k == 0 ? cur : mw.out[l + k - 1].rows();
-        sa.L[k] = stack_layer(M->layers[l + k], xin, mw.out[l + k], lt);
+        sa.L[k] = stack_layer(M->layers[l + k], xin, mw.out[l + k], lt, s0, s1, l + k);
       }
       bool unsupported = false;
       if (launch_stack(sa, s, &unsupported) != hipSuccess) return QL_EHIP;
@@ -524,7 +539,8 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
       pa.ws = mw.rec;
       for (int k = 0; k < n; ++k) {
         const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l + k] : nullptr;
-        pa.L[k] = pstack_layer(M->layers[l + k], k == 0 ? cur : ActRows{}, mw.out[l + k], lt);
+        pa.L[k] = pstack_layer(M->layers[l + k], k == 0 ? cur : ActRows{}, mw.out[l + k], lt, s0,
+                               s1, l + k);
       }
       bool unsupported = false;
       if (launch_pstack(pa, s, &unsupported) != hipSuccess) return QL_EHIP;
@@ -540,7 +556,8 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
     w.hout = mw.out[stack || pst ? l : (l & 1)];
     w.hout.ld = round_up(layer_width(L), 64);
     const ql_lstm_taps *lt = taps && taps->layers ? &taps->layers[l] : nullptr;
-    st = run_layer(L, cur, T, B, nullptr, nullptr, mw.hf, nullptr, nullptr, w, lt, s);
+    st = run_layer(L, cur, T, B, st_h(s0, l), st_c(s0, l), lt && lt->h ? lt->h : mw.hf,
+                   st_hout(s1, l), st_cout(s1, l), w, lt, s);
     if (st != QL_OK) return st;
     cur = w.hout.rows();
     ++l;
@@ -556,7 +573,17 @@ extern "C" {
 ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64_t T, int64_t B,
                                     float *post, const ql_model_taps *taps, void *ws,
                                     size_t ws_bytes, void *stream) {
-  return model_forward(M, Frontend{feats, false, 0, 0, 0}, T, B, post, taps, ws, ws_bytes, stream);
+  return model_forward(M, Frontend{feats, false, 0, 0, 0}, T, B, post, nullptr, nullptr, taps, ws,
+                       ws_bytes, stream);
+}
+
+ql_status ql_acoustic_model_forward_stream(const ql_model *M, const float *feats, int64_t T,
+                                           int64_t B, const ql_lstm_state *state_in,
+                                           const ql_lstm_state *state_out, float *post,
+                                           const ql_model_taps *taps, void *ws, size_t ws_bytes,
+                                           void *stream) {
+  return model_forward(M, Frontend{feats, false, 0, 0, 0}, T, B, post, state_in, state_out, taps,
+                       ws, ws_bytes, stream);
 }
 
 int64_t ql_stacked_input_count(int64_t nframes, int32_t stack, int32_t skip) {
@@ -603,8 +630,8 @@ ql_status ql_acoustic_model_forward_frames(const ql_model *M, const float *frame
   ql_status st = check_frontend(nframes, B, dim, stack, skip, M->layers[0].in);
   if (st != QL_OK) return st;
   const int64_t T = ql_stacked_input_count(nframes, stack, skip);
-  return model_forward(M, Frontend{frames, true, (int32_t)dim, stack, skip}, T, B, post, taps, ws,
-                       ws_bytes, stream);
+  return model_forward(M, Frontend{frames, true, (int32_t)dim, stack, skip}, T, B, post, nullptr,
+                       nullptr, taps, ws, ws_bytes, stream);
 }
 
 size_t ql_lstm_recurrence_workspace(const ql_lstm_layer *L, int64_t T, int64_t B) {
@@ -792,6 +819,15 @@ ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const
                                        dst->inv_q, dst->sums, as_stream(stream)));
 }
 
+namespace {
+// The last layer's h went to its tap when one was given: h_last gets a copy.
+ql_status copy_last_h(float *h_last, const float *written, int64_t count, hipStream_t s) {
+  if (!h_last || written == h_last || count == 0) return QL_OK;
+  return from_hip(hipMemcpyAsync(h_last, written, (size_t)count * sizeof(float),
+                                 hipMemcpyDeviceToDevice, s));
+}
+}  // namespace
+
 size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B) {
   if (!layers || n < 1 || n > kMaxStack || T < 0 || B < 0) return 0;
   if (layers[0].proj > 0) {  // the projection wavefront (batch 1)
@@ -814,7 +850,9 @@ int32_t ql_lstm_stack_layers_per_launch(const ql_lstm_layer *layers, int32_t n, 
 
 ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql_qact *x,
                                 int64_t T, int64_t B, const ql_qact *h_codes, float *h_last,
-                                void *ws, size_t ws_bytes, void *stream) {
+                                const ql_lstm_state *state_in, const ql_lstm_state *state_out,
+                                const ql_lstm_taps *taps, void *ws, size_t ws_bytes,
+                                void *stream) {
   if (!layers || !x || !h_codes) return QL_EINVAL;
   if (n < 1 || n > kMaxStack || T < 0 || B < 0) return QL_ESHAPE;
   const int64_t H = layers[0].hidden;
@@ -850,12 +888,14 @@ ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql
     for (int k = 0; k < n; ++k) {
       const ActRows xin = k == 0 ? ActRows{x->codes, x->ld, x->zero, x->inv_q, x->sums} : ActRows{};
       ActBuf out{h_codes[k].codes, h_codes[k].ld, h_codes[k].zero, h_codes[k].sums, h_codes[k].inv_q};
-      pa.L[k] = pstack_layer(layers[k], xin, out, nullptr);
-      if (k == n - 1) pa.L[k].h = h_last;
+      pa.L[k] = pstack_layer(layers[k], xin, out, taps ? &taps[k] : nullptr, state_in,
+                             state_out, k);
+      if (k == n - 1 && h_last && !pa.L[k].h) pa.L[k].h = h_last;
     }
     bool unsupported = false;
     if (launch_pstack(pa, s, &unsupported) != hipSuccess) return QL_EHIP;
-    return unsupported ? QL_EUNSUPPORTED : QL_OK;
+    if (unsupported) return QL_EUNSUPPORTED;
+    return copy_last_h(h_last, pa.L[n - 1].h, T * B * layers[n - 1].proj, s);
   }
   StackArgs sa{};
   sa.nl = n;
@@ -868,12 +908,14 @@ ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql
                                : ActRows{h_codes[k - 1].codes, h_codes[k - 1].ld, h_codes[k - 1].zero,
                                          h_codes[k - 1].inv_q, h_codes[k - 1].sums};
     ActBuf out{h_codes[k].codes, h_codes[k].ld, h_codes[k].zero, h_codes[k].sums, h_codes[k].inv_q};
-    sa.L[k] = stack_layer(layers[k], xin, out, nullptr);
-    if (k == n - 1) sa.L[k].h = h_last;
+    sa.L[k] = stack_layer(layers[k], xin, out, taps ? &taps[k] : nullptr, state_in, state_out,
+                          k);
+    if (k == n - 1 && h_last && !sa.L[k].h) sa.L[k].h = h_last;
   }
   bool unsupported = false;
   if (launch_stack(sa, s, &unsupported) != hipSuccess) return QL_EHIP;
-  return unsupported ? QL_EUNSUPPORTED : QL_OK;
+  if (unsupported) return QL_EUNSUPPORTED;
+  return copy_last_h(h_last, sa.L[n - 1].h, T * B * H, s);
 }
 
 ql_status ql_workspace_status(const void *ws, void *stream) {

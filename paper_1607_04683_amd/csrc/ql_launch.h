@@ -118,6 +118,9 @@ struct StackLayer {
   int8_t *tap_codes;       // optional taps: [T][B][H] codes (ld = H), zero, inv_q
   int32_t *tap_zero;
   float *tap_inv_q;
+  int32_t *acc_x, *acc_h;  // optional taps: [T][B][4H] raw input / recurrent sums
+  const float *h0, *c0;    // [B][H] initial state (nullable = zeros)
+  float *hT, *cT;          // [B][H] final state (nullable)
 };
 struct StackArgs {
   int nl;                  // layers in this launch (2 .. kMaxStack)
@@ -137,6 +140,10 @@ struct PStackLayer {
   int8_t *tap_codes;       // optional taps: [T][P] codes (ld = P), zero, inv_q
   int32_t *tap_zero;
   float *tap_inv_q;
+  int32_t *acc_x, *acc_h;  // optional taps: [T][4H] raw input / recurrent sums
+  int32_t *acc_r;          // optional tap: [T][P] raw projection sums
+  const float *h0, *c0;    // [P], [H] initial state (nullable = zeros)
+  float *hT, *cT;          // [P], [H] final state (nullable)
 };
 struct PStackArgs {
   int nl;                  // layers in this launch (1 .. kMaxStack)

@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
   }
   for (int r = tid; r < v; r += blockDim.x)
     cpr[r] = col_param(Ly.Wr, nv > 0 ? p0 + (r < nv ? r : 0) : 0, H);
-  for (int j = tid; j < u; j += blockDim.x) cst[j] = 0.0f;
+  for (int j = tid; j < u; j += blockDim.x) cst[j] = Ly.c0 && j < nu ? Ly.c0[j0 + j] : 0.0f;
   if (tid == 0) s_abort = 0;
   for (int i = tid; i < 16; i += blockDim.x) xch_x[i] = xch_h[i] = xch_m[i] = 0;
   // the codes of x_t and h_{t-1} are row 0 of 16-row blocks whose other rows
@@ -192,7 +192,11 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
     //    codes for the first layer) side by side.  An all-zero h_{-1} quantizes to
     //    Q = 1, zero point 0, codes V' = 0 (stored -128): W_h h is exactly 0.
     if (tid < 2 * kWave) {
-      if (t == 0) {
+      if (t == 0 && Ly.h0) {
+        // h_{-1} = h0 (plain floats), quantized per vector by wave 0
+        if (tid < kWave)
+          quant_rows<8, 1, kSrcPlain>(Ly.h0, P, 1, 1, 0u, (int)P, hc, ldsP, ldP, flag, &rp[1]);
+      } else if (t == 0) {
         for (int k = tid; k < ldP; k += 2 * kWave) hc[k] = k < P ? (int8_t)-128 : (int8_t)0;
         if (tid == 0) rp[1] = row_param(0, 1.0f, 0, (int)P);
       } else if (!quant_row_2w(hown + (t - 1) * P, (uint32_t)t, (int)P, hc, ldP, flag, &rp[1],
@@ -216,6 +220,14 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
     products_mfma(hc, ldsP, 16, wh, ldsP, nrows, nrows, ldP, Sh, nrows);
     products_mfma(xc, ldsX, 16, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
     __syncthreads();
+    if (Ly.acc_x || Ly.acc_h)  // sums of step t (row 0 of S) to the taps [T][4H], 0..255 domain
+      for (int n = tid; n < nrows; n += blockDim.x) {
+        const int gt = n / u, jj = n % u;
+        if (jj >= nu) continue;
+        const int64_t o = (t * 4 + gt) * H + j0 + jj;
+        if (Ly.acc_x) Ly.acc_x[o] = acc_u8(Sx[n], cpx[n].sigw, rp[0].sigx, IN);
+        if (Ly.acc_h) Ly.acc_h[o] = acc_u8(Sh[n], cph[n].sigw, rp[1].sigx, P);
+      }
 
     // 2. gates: lane 4 jj + gt computes gate gt of cell jj (i, f, g, o)
     if (tid < 4 * u) {
@@ -234,6 +246,7 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
         const float m = og * tanh_cw(cn);
         if (tl.xcd) publish_local(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
         else publish(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
+        if (Ly.cT && t == T - 1) Ly.cT[j0 + jj] = cn;
       }
     }
     // the output codes of h_{t-1} (in hc) leave while m_t travels
@@ -255,6 +268,8 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
       if (tl.xcd) publish_local(&hown[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       publish(&hw[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       if (Ly.h) Ly.h[t * P + p0 + tid] = hv;
+      if (Ly.acc_r) Ly.acc_r[t * P + p0 + tid] = acc_u8(Sr[tid], cr.sigw, rm.sigx, H);
+      if (Ly.hT && t == T - 1) Ly.hT[p0 + tid] = hv;
     }
     // the next step's first phase writes only hc, xc, rp[0], rp[1]: none of
     // them is read after the last barrier

@@ -229,13 +229,29 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     }
     bsl[r] = Ly.bias[n];
   }
-  for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) cst[idx] = 0.0f;
+  for (int idx = tid; idx < tl.bB * tl.u; idx += blockDim.x) {
+    const int lb = idx / tl.u, jj = idx % tl.u;
+    cst[idx] = Ly.c0 && lb < nb && jj < nu ? Ly.c0[(b0 + lb) * H + j0 + jj] : 0.0f;
+  }
   if constexpr (!MFA) {  // rows 1..15 of the one-row code blocks stay zero
     int8_t *xh2 = reinterpret_cast<int8_t *>(smem + tl.off_xh2);
     for (int k = tid; k < 16 * tl.ldsX; k += blockDim.x) xh[k] = xh2[k] = 0;
     for (int k = tid; k < 16 * tl.ldsXx; k += blockDim.x) xx[k] = 0;
   }
   __syncthreads();
+
+  // Sums of step t (signed-code sums S[lb][n], gate-major n = g u + jj) to a
+  // tap [T][B][4H] in the 0..255 code domain; only when the caller asked.
+  auto tap_acc = [&](int32_t *dst, const int32_t *S, const ColParam *cp, const RowParam *rp,
+                     int64_t K, int64_t t) {
+    for (int idx = tid; idx < nb * nrows; idx += blockDim.x) {
+      const int lb = idx / nrows, n = idx % nrows, g = n / tl.u, jj = n % tl.u;
+      if (jj < nu)
+        dst[((t * B + b0 + lb) * 4 + g) * H + j0 + jj] = acc_u8(S[idx], cp[n].sigw, rp[lb].sigx, K);
+    }
+  };
+  // Initial state h_{-1}: rows of h0 (plain floats), or zeros.
+  auto h0_row = [&](int lb) -> const void * { return Ly.h0 ? Ly.h0 + (b0 + lb) * H : nullptr; };
 
   // Counter mode: the codes of x_t (the input, or layer l-1's h_t) are loaded
   // into registers before h_{t-1} is quantized, and parked in LDS afterwards
@@ -266,8 +282,9 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   // place in Sx (float bits) for rows [0, nr), off the recurrence's critical
   // path.  (One-row tiles recover it in the gates: there the gates are not
   // the long pole and the extra pass would delay the next step.)
-  auto x_preact = [&](int nr) {
+  auto x_preact = [&](int64_t t, int nr) {
     __syncthreads();  // Sx complete
+    if (Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);  // each lane reads its own sums first
     for (int idx = tid; idx < nr * nrows; idx += blockDim.x) {
       const int lb = idx / nrows, n = idx % nrows;
       const RowParam rx = rpx[lb];
@@ -310,6 +327,10 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         else publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
       }
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
+      if (t == T - 1) {
+        if (Ly.hT) Ly.hT[b * H + j] = m;
+        if (Ly.cT) Ly.cT[b * H + j] = cn;
+      }
     };
     const int full = pairs / nt, rem = pairs % nt;
     for (int k = 0; k < full; ++k) {
@@ -421,6 +442,10 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       for (int c2 = 0; c2 < tl.reph; ++c2)
         publish(&xht[c2 * tl.strideh + hcur + p.poff], (uint32_t)(t + 1), m);
       if (Ly.h) Ly.h[t * B * H + p.poff] = m;
+      if (t == T - 1) {
+        if (Ly.hT) Ly.hT[p.poff] = m;
+        if (Ly.cT) Ly.cT[p.poff] = cn;
+      }
     };
     auto row_fast = [](const RowParam &rh) { return (uint32_t)(rh.ztx + 127) <= 255u; };
     auto gates_b = [&](int64_t t, int64_t hcur) {
@@ -478,7 +503,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         rpx[tid] = tid < nb ? row_param(xpz, xpq, xps, (int)IN) : row_param(0, 0.0f, 0, (int)IN);
       __syncthreads();
       products_mfma(xx, tl.ldsXx, tl.bB, wx, tl.ldsWx, nrows, nrows, ldXl, Sx, nrows);
-      x_preact(nb);
+      x_preact(t, nb);
 
       // ---- 2. codes of h_{t-1}
       if (t > 0 && !wait_count(ctr(l, par, tb), (unsigned)(((t - 1) >> 1) + 1) * Qn, flag))
@@ -504,9 +529,9 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         }
       }
       if (t == 0) {
-        // h_{-1} = 0: every tile quantizes the zero rows itself
+        // h_{-1} (h0, or zeros): every tile quantizes those rows itself
         quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
-                                        [&](int) -> const void * { return nullptr; });
+                                        h0_row);
       } else {
 #pragma unroll
         for (int i = 0; i < kXPre; ++i) {
@@ -521,6 +546,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       // ---- 3. the recurrent product against the resident W_h' slice
       products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
       __syncthreads();
+      if (Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
 
       // ---- 4. recover, gates, cell; publish h_t
       gates_b(t, hcur);
@@ -715,7 +741,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   if (tid < 16) s_xch[tid] = 0;  // flags hold step tags, which start at 1
   if (T > 0 && !input_side(0)) return;
   if (!quant_tile<NVA, RBA, kSrcPlain>(nb, rowsA, H, 0u, (int)H, xh, tl.ldsX, tl.ldH, flag, rph,
-                                       [&](int) -> const void * { return nullptr; }))
+                                       h0_row))
     return;
   __syncthreads();
   const int wave = tid >> 6;
@@ -727,6 +753,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     // ---- 1. the recurrent product (the input side's is already in Sx)
     products_mfma(xh, tl.ldsX, 16, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
     __syncthreads();
+    if (Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);
+    if (Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
 
     // ---- 2. recover, gates, cell; publish h_t
     gates(t, hcur);
@@ -757,12 +785,13 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
 static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, StackTiling *out) {
   StackTiling tl{};
   const int64_t B = a.B, H = a.H;
-  // workgroups per layer: at one batch row, half of the CUs' share (25 tiles
-  // of 20 cells for five 500-cell layers): the per-step exchange costs less
-  // with fewer readers than the extra cells per tile cost (measured with every
-  // layer on an XCD of its own: 20, 25, 28 and 32 tiles give 5.05, 4.88,
-  // 4.97 and 4.97 us per frame; spread over all XCDs, 40%, 50%, 60% and 100%
-  // of the share gave 5.80, 5.59, 5.68 and 6.54)
+  // workgroups per layer: at one row per tile, half of the CUs' share: the
+  // per-step exchange costs less with fewer readers than the extra cells per
+  // tile cost (with dot-product gate rows, every layer on an XCD of its own:
+  // 20, 25, 28 and 32 tiles gave 5.05, 4.88, 4.97 and 4.97 us per frame;
+  // spread over all XCDs, 40%, 50%, 60% and 100% of the share gave 5.80,
+  // 5.59, 5.68 and 6.54).  With MFMA gate rows a single batch row takes the
+  // 16-cell tiling below instead.
   const int G = bB == 1 ? cus / a.nl / 2 : cus / a.nl;
   tl.ldH = (int)round_up(H, 64);
   int64_t maxin = 0;
@@ -785,10 +814,12 @@ static bool plan_stack_bb(const StackArgs &a, int cus, int lds_max, int bB, Stac
   // one row with MFMA products: tiles of at least 16 cells over up to a whole
   // XCD per layer (five 500-cell layers: 32 tiles of 16 cells 4.39 us a frame,
   // 25 of 20 4.47, 21 of 24 4.44, 42 of 12 4.77; five 300-cell layers: 19 of
-  // 16 4.04, 25 of 12 4.08)
+  // 16 4.04, 25 of 12 4.08), when every batch row's tiles still fit the
+  // layer's share of the CUs (otherwise the half-share tiling above stands,
+  // so that at 2..15 rows no layer drops out of the launch)
   if (bB == 1) {
     const int64_t u16 = std::max<int64_t>(16, (H + kXcdCus - 1) / kXcdCus);
-    if ((H + u16 - 1) / u16 <= cus / a.nl) tl.u = (int)u16;
+    if (tl.nbt * ((H + u16 - 1) / u16) <= cus / a.nl) tl.u = (int)u16;
   }
   tl.u = (tl.u + 3) / 4 * 4;  // 4u gate rows a multiple of 16 (MFMA tiles)
   tl.nut = (int)((H + tl.u - 1) / tl.u);

@@ -33,7 +33,7 @@ EXPORTS = [
     "ql_f32_acoustic_model_forward", "ql_quantize_activations", "ql_lstm_stack_workspace",
     "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch", "ql_stacked_input_count",
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
-    "ql_acoustic_model_forward_frames",
+    "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
 ]
 
 
@@ -61,7 +61,12 @@ class CModel(C.Structure):
 
 class CTaps(C.Structure):
     _fields_ = [("acc_x", C.c_void_p), ("acc_h", C.c_void_p), ("acc_r", C.c_void_p),
-                ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p)]
+                ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p),
+                ("h", C.c_void_p)]
+
+
+class CState(C.Structure):
+    _fields_ = [("h", C.c_void_p), ("c", C.c_void_p)]
 
 
 class CQAct(C.Structure):
@@ -127,7 +132,11 @@ def load(path: str = LIB_PATH):
     L.ql_lstm_stack_workspace.argtypes = [C.POINTER(CLayer), i32, i64, i64]
     L.ql_lstm_stack_workspace.restype = sz
     L.ql_lstm_stack_forward.argtypes = [C.POINTER(CLayer), i32, C.POINTER(CQAct), i64, i64,
-                                        C.POINTER(CQAct), vp, vp, sz, vp]
+                                        C.POINTER(CQAct), vp, C.POINTER(CState),
+                                        C.POINTER(CState), C.POINTER(CTaps), vp, sz, vp]
+    L.ql_acoustic_model_forward_stream.argtypes = [C.POINTER(CModel), vp, i64, i64,
+                                                   C.POINTER(CState), C.POINTER(CState), vp,
+                                                   C.POINTER(CModelTaps), vp, sz, vp]
     L.ql_lstm_stack_layers_per_launch.argtypes = [C.POINTER(CLayer), i32, i64, i64]
     L.ql_lstm_stack_layers_per_launch.restype = i32
     L.ql_stacked_input_count.argtypes = [i64, i32, i32]
@@ -150,7 +159,7 @@ def load(path: str = LIB_PATH):
               "ql_gate_fn", "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_forward",
               "ql_f32_acoustic_model_forward", "ql_quantize_activations",
               "ql_lstm_stack_forward", "ql_quantize_stacked_frames",
-              "ql_acoustic_model_forward_frames"):
+              "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -340,21 +349,25 @@ def quantize_model(weights: dict, device="cuda", gate_blocks: int = 4, proj_bloc
                  torch.as_tensor(weights["by"], dtype=torch.float32).to(device).contiguous())
 
 
-TAP_NAMES = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q")
+TAP_NAMES = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q", "h")
 
 
-def _taps(T, B, L: Layer, device, which=True):
-    """Allocate the requested taps (True = all, or a collection of names)."""
+def _taps(T, B, L: Layer, device, which=True, layer_h=True):
+    """Allocate the requested taps (True = all, or a collection of names);
+    layer_h=False leaves out the fp32 h tap (the one-layer calls return h)."""
     H, P, R = L.hidden, L.proj, L.width
     want = set(TAP_NAMES) if which is True else set(which)
+    if not layer_h:
+        want.discard("h")
     z = lambda name, *s, dt: torch.empty(*s, dtype=dt, device=device) if name in want else None
     t = dict(acc_x=z("acc_x", T, B, 4 * H, dt=torch.int32),
              acc_h=z("acc_h", T, B, 4 * H, dt=torch.int32),
              acc_r=z("acc_r", T, B, P, dt=torch.int32) if P else None,
              h_codes=z("h_codes", T, B, R, dt=torch.int8), h_zero=z("h_zero", T, B, dt=torch.int32),
-             h_inv_q=z("h_inv_q", T, B, dt=torch.float32))
-    c = CTaps(*[None if t[k] is None else t[k].data_ptr()
-                for k in ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q")])
+             h_inv_q=z("h_inv_q", T, B, dt=torch.float32), h=z("h", T, B, R, dt=torch.float32))
+    c = CTaps(*[None if t[k] is None else t[k].data_ptr() for k in TAP_NAMES])
+    if not layer_h:
+        del t["h"]  # the caller's own h output keeps its name
     return t, c
 
 
@@ -386,7 +399,7 @@ def lstm_layer_forward(L: Layer, x: torch.Tensor, h0=None, c0=None, taps: bool =
     out = dict(h=h, hT=hT, cT=cT)
     tp = None
     if taps:
-        t, ct = _taps(T, B, L, dev, taps)
+        t, ct = _taps(T, B, L, dev, taps, layer_h=False)
         out.update(t)
         tp = C.byref(ct)
     _check(lib.ql_lstm_layer_forward(C.byref(cl), _ptr(x), T, B, _ptr(h0), _ptr(c0), _ptr(h),
@@ -413,7 +426,7 @@ def lstm_recurrence(L: Layer, gx: torch.Tensor, h0=None, c0=None, taps=False,
     res = dict(h=h)
     tp = None
     if taps:
-        t, ct = _taps(T, B, L, dev, taps)
+        t, ct = _taps(T, B, L, dev, taps, layer_h=False)
         res.update(t)
         tp = C.byref(ct)
     _check(lib.ql_lstm_recurrence(C.byref(cl), _ptr(gx), T, B, _ptr(h0), _ptr(c0), _ptr(h),
@@ -443,10 +456,25 @@ def _model_taps(M: Model, T: int, B: int, dev, taps, out: dict):
                       None if logits is None else logits.data_ptr())
 
 
+def _state_array(states):
+    """Host array of per-layer ql_lstm_state from [(h, c), ...] (tensors or None)."""
+    if states is None:
+        return None
+    return (CState * len(states))(*[CState(_ptr(h), _ptr(c)) for h, c in states])
+
+
+def empty_state(M: Model, B: int, device="cuda"):
+    """Per-layer (h [B][R], c [B][H]) fp32 buffers for a stream's state."""
+    return [(torch.empty(B, L.width, dtype=torch.float32, device=device),
+             torch.empty(B, L.hidden, dtype=torch.float32, device=device)) for L in M.layers]
+
+
 def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
                            workspace: Workspace | None = None, post: torch.Tensor | None = None,
-                           check: bool = True):
-    """feats [T][B][in] fp32 (device) -> dict(post [T][B][S][, taps])."""
+                           check: bool = True, state_in=None, state_out=None):
+    """feats [T][B][in] fp32 (device) -> dict(post [T][B][S][, taps]).
+    state_in / state_out: per-layer [(h, c)] of a stream (ql_acoustic_model_forward_stream);
+    they must not share memory."""
     feats = feats.contiguous()
     T, B, _ = feats.shape
     dev = feats.device
@@ -458,9 +486,17 @@ def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
     ws = (workspace or Workspace()).get(nbytes, dev)
     out = dict(post=post)
     mt = _model_taps(M, T, B, dev, taps, out)
-    _check(lib.ql_acoustic_model_forward(C.byref(cm), _ptr(feats), T, B, _ptr(post),
-                                         C.byref(mt) if mt is not None else None, _ptr(ws),
-                                         ws.numel(), _stream()), "ql_acoustic_model_forward")
+    mtp = C.byref(mt) if mt is not None else None
+    if state_in is None and state_out is None:
+        _check(lib.ql_acoustic_model_forward(C.byref(cm), _ptr(feats), T, B, _ptr(post), mtp,
+                                             _ptr(ws), ws.numel(), _stream()),
+               "ql_acoustic_model_forward")
+    else:
+        si, so = _state_array(state_in), _state_array(state_out)
+        _check(lib.ql_acoustic_model_forward_stream(C.byref(cm), _ptr(feats), T, B, si, so,
+                                                    _ptr(post), mtp, _ptr(ws), ws.numel(),
+                                                    _stream()),
+               "ql_acoustic_model_forward_stream")
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward")
     return out
@@ -648,10 +684,11 @@ def quantize_activations(X: torch.Tensor, out: QAct | None = None) -> QAct:
 
 def lstm_stack_forward(layers: list, x: QAct, T: int, B: int, want_h: bool = False,
                        outs: list | None = None, workspace: Workspace | None = None,
-                       check: bool = True):
+                       check: bool = True, taps=False, state_in=None, state_out=None):
     """n stacked layers (no projection and one width, or all projected at
     B = 1) in one launch from input codes x (T*B rows) -> dict(codes=[QAct per
-    layer], h=[T][B][R] of the last)."""
+    layer], h=[T][B][R] of the last[, layers=per-layer taps]).  state_in /
+    state_out: per-layer [(h, c)] (must not share memory)."""
     lib = load()
     n = len(layers)
     dev = x.codes.device
@@ -662,11 +699,22 @@ def lstm_stack_forward(layers: list, x: QAct, T: int, B: int, want_h: bool = Fal
     nbytes = lib.ql_lstm_stack_workspace(arr, n, T, B)
     ws = (workspace or Workspace()).get(nbytes, dev)
     cx = x.cstruct()
-    _check(lib.ql_lstm_stack_forward(arr, n, C.byref(cx), T, B, oarr, _ptr(h), _ptr(ws),
-                                     ws.numel(), _stream()), "ql_lstm_stack_forward")
+    res = dict(codes=outs, h=h)
+    tarr = None
+    if taps:
+        lt = []
+        tarr = (CTaps * n)()
+        for i, L in enumerate(layers):
+            t, ct = _taps(T, B, L, dev, taps)
+            lt.append(t)
+            tarr[i] = ct
+        res["layers"] = lt
+    _check(lib.ql_lstm_stack_forward(arr, n, C.byref(cx), T, B, oarr, _ptr(h),
+                                     _state_array(state_in), _state_array(state_out), tarr,
+                                     _ptr(ws), ws.numel(), _stream()), "ql_lstm_stack_forward")
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_lstm_stack_forward")
-    return dict(codes=outs, h=h)
+    return res
 
 
 def stack_layers_per_launch(M: Model, T: int, B: int) -> int:

@@ -174,13 +174,14 @@ def test_activation_and_stack_argument_errors(ql):
     need = lib.ql_lstm_stack_workspace(arr, 2, T, B)
     assert need > 0
     f = lambda layers=arr, xx=x, wsb=need: lib.ql_lstm_stack_forward(
-        layers, 2, C.byref(xx), T, B, outs, None, FAKE, wsb, None)
+        layers, 2, C.byref(xx), T, B, outs, None, None, None, None, FAKE, wsb, None)
     assert f(wsb=need - 1) == ql.QL_EWORKSPACE
     assert f(xx=ql.CQAct(FAKE, T * B + 1, IN, 64, FAKE, FAKE, FAKE)) == ql.QL_ESHAPE
     bad = (ql.CLayer * 2)(L0, ql.CLayer(H, H + 1, 0, qm(4 * H + 4, H, 64, 4),
                                         qm(4 * H + 4, H + 1, 64, 4), empty, FAKE))
     assert f(layers=bad) == ql.QL_ESHAPE   # widths differ
-    assert lib.ql_lstm_stack_forward(arr, 2, None, T, B, outs, None, FAKE, need, None) == ql.QL_EINVAL
+    assert lib.ql_lstm_stack_forward(arr, 2, None, T, B, outs, None, None, None, None, FAKE, need,
+                                     None) == ql.QL_EINVAL
 
 
 def test_frontend_argument_errors(ql):

@@ -7,6 +7,7 @@ posteriors (a different summation order in the softmax) to 1e-4 absolute."""
 import numpy as np
 import pytest
 import torch
+from model_parity import assert_model_taps
 
 pytestmark = pytest.mark.gpu
 
@@ -109,17 +110,14 @@ def test_lstm_layer_empty(ql):
 
 
 def _model_case(ql, orc, weights, feats, utts=None, taps=("h_codes",)):
+    """GPU forward of the whole batch; the oracle on the sampled utterances
+    (per-vector quantization makes them independent of their batch-mates);
+    every requested tap compared element by element."""
     Mg = ql.quantize_model(weights)
     g = ql.acoustic_model_forward(Mg, torch.from_numpy(feats).cuda(), taps=taps)
-    sel = slice(None) if utts is None else list(utts)
-    fo = feats if utts is None else np.ascontiguousarray(feats[:, sel])
+    fo = feats if utts is None else np.ascontiguousarray(feats[:, list(utts)])
     o = orc.acoustic_model_forward(orc.quantize_model(weights), fo, taps=True)
-    for l, lt in enumerate(g["layers"]):
-        got = u8(lt["h_codes"])[:, sel]
-        assert np.array_equal(got, o["layers"][l]["h_codes"]), f"layer {l} codes"
-    post = np_(g["post"])[:, sel]
-    err = np.max(np.abs(post - o["post"]))
-    assert err <= TOL, err
+    assert_model_taps(g, o, utts, names=ql.TAP_NAMES if taps is True else taps)
     return g, o
 
 
@@ -152,25 +150,40 @@ def test_model_softmax_large_tiles_ragged_states(ql, orc):
 
 
 def test_model_5x500_softmax8192_T500_B1(ql, orc):
-    """Five 500-cell layers + 8192-way quantized softmax, T=500, batch 1."""
+    """Five 500-cell layers + 8192-way quantized softmax, T=500, batch 1, on the
+    one-row layer wavefront (all five layers in one launch): every layer's
+    input and recurrent int32 sums, codes, row params and fp32 h, the softmax
+    sums and logits bit-exact, posteriors within 1e-4."""
     from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T500_B1 as W_, model_weights, features
-    _model_case(ql, orc, model_weights(W_)[0], features(W_))
+    w = model_weights(W_)[0]
+    assert ql.stack_layers_per_launch(ql.quantize_model(w), W_.T, W_.B) == 5
+    _model_case(ql, orc, w, features(W_), taps=True)
+
+
+# Ten of the 64 utterances: the first row of each of the four 8-row quantizing
+# workgroups in both 32-row batch slices, plus rows 45 and 63 (a wave other
+# than the first of its workgroup; the last row).
+B64_UTTS = [0, 8, 16, 24, 32, 40, 45, 48, 56, 63]
 
 
 def test_model_5x500_softmax8192_T1000_B64_sampled(ql, orc):
-    """Batch 64 x T=1000 on the GPU; the oracle recomputes two utterances
-    (per-vector quantization makes utterances independent)."""
+    """Batch 64 x T=1000 on the batched layer wavefront (the benchmarked
+    kernel); the oracle recomputes ten utterances (per-vector quantization
+    makes utterances independent), and every tap of theirs is compared."""
     from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T1000_B64 as W_, model_weights, features
-    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[0, 45])
+    w = model_weights(W_)[0]
+    assert ql.stack_layers_per_launch(ql.quantize_model(w), W_.T, W_.B) == 5
+    _model_case(ql, orc, w, features(W_), utts=B64_UTTS, taps=True)
 
 
 def test_model_4xlstmp2048_softmax16384_T800_B256_sampled(ql, orc):
     """4 x LSTMP(2048 cells, P=512), 640-dim input, 16384-way softmax, batch 256
     x T=800 on the GPU; the oracle recomputes four whole utterances (the first
-    and the last among them)."""
+    and the last among them); input, recurrent and projection sums, codes, h,
+    softmax sums and logits bit-exact."""
     from paper_1607_04683_amd.workloads import (LSTMP4x2048P512_S16384_T800_B256 as W_,
                                                 model_weights, features)
-    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[0, 77, 131, 255])
+    _model_case(ql, orc, model_weights(W_)[0], features(W_), utts=[0, 77, 131, 255], taps=True)
 
 
 def test_model_batch_invariance_and_determinism(ql):
@@ -208,43 +221,106 @@ def test_model_empty(ql):
     assert out["post"].shape == (0, 2, 5)
 
 
-@pytest.mark.parametrize("layers,B", [(3, 5), (3, 37), (7, 1), (2, 1), (6, 20)])
+@pytest.mark.parametrize("layers,B", [(3, 5), (3, 37), (7, 1), (2, 1), (6, 20), (2, 12)])
 def test_model_layer_wavefront(ql, orc, layers, B):
-    """Layers sharing one width run several per launch (a wavefront); codes of
-    every layer stay bit-exact and posteriors within 1e-4.  One batch row per
-    tile (tagged exchange) and 16-row tiles (counters, ragged last slice);
-    more layers than fit one launch split into several launches.  At one row,
-    up to 32 tiles per layer put each layer on an XCD of its own (7 layers of
-    16 tiles); 2 layers of 48 tiles spread over all XCDs."""
+    """Layers sharing one width run several per launch (a wavefront); every
+    tap of every layer (input and recurrent sums, codes, row params, fp32 h)
+    stays bit-exact and posteriors within 1e-4.  One batch row per tile
+    (tagged exchange) and 16-row tiles (counters, ragged last slice); more
+    layers than fit one launch split into several launches.  At one row, tiles
+    of 16 cells (3 per 48-cell layer) put each layer's tiles on an XCD of its
+    own while a layer's B x 3 tiles fit one (32 CUs); 2 layers at B = 12 have
+    36 tiles each and take the spread layout over all XCDs."""
     from paper_1607_04683_amd.workloads import random_model
     w = random_model(40, 48, layers, states=64, seed=layers * 100 + B)
     x = np.random.default_rng(B).standard_normal((11, B, 40)).astype(np.float32)
-    g, _ = _model_case(ql, orc, w, x, taps=("h_codes", "h_zero", "h_inv_q"))
-    # the one-layer-per-launch path (forced by accumulator taps) gives the same bits
     M = ql.quantize_model(w)
-    one = ql.acoustic_model_forward(M, torch.from_numpy(x).cuda(), taps=True)
-    assert torch.equal(one["post"], g["post"])
-    for l in range(layers):
-        assert torch.equal(one["layers"][l]["h_codes"], g["layers"][l]["h_codes"])
-        assert torch.equal(one["layers"][l]["h_zero"], g["layers"][l]["h_zero"])
+    assert ql.stack_layers_per_launch(M, 11, B) >= 2
+    _model_case(ql, orc, w, x, taps=True)
 
 
 @pytest.mark.parametrize("B", [1, 20])
 def test_lstm_stack_forward_entry(ql, orc, B):
-    """ql_lstm_stack_forward on the per-vector codes of x: every layer's codes
-    and the last layer's h equal the oracle's layer-by-layer evaluation."""
+    """ql_lstm_stack_forward on the per-vector codes of x, from a given initial
+    state (h0, c0 per layer): every layer's codes, sums, fp32 h and final
+    state equal the oracle's layer-by-layer evaluation."""
     from paper_1607_04683_amd.workloads import random_model
-    n, T = 3, 9
-    w = random_model(40, 48, n, seed=7 + B)
-    x = np.random.default_rng(B + 3).standard_normal((T, B, 40)).astype(np.float32)
+    n, T, H = 3, 9, 48
+    w = random_model(40, H, n, seed=7 + B)
+    rng = np.random.default_rng(B + 3)
+    x = rng.standard_normal((T, B, 40)).astype(np.float32)
+    h0 = [(np.tanh(rng.standard_normal((B, H))) * 0.7).astype(np.float32) for _ in range(n)]
+    c0 = [rng.standard_normal((B, H)).astype(np.float32) for _ in range(n)]
     layers = [ql.quantize_layer(L) for L in w["layers"]]
     xq = ql.quantize_activations(torch.from_numpy(x.reshape(T * B, 40)).cuda())
-    g = ql.lstm_stack_forward(layers, xq, T, B, want_h=True)
+    s_in = [(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()) for a, b in zip(h0, c0)]
+    s_out = [(torch.empty(B, H, device="cuda"), torch.empty(B, H, device="cuda")) for _ in range(n)]
+    g = ql.lstm_stack_forward(layers, xq, T, B, want_h=True, taps=True, state_in=s_in,
+                              state_out=s_out)
     cur = x
     for k in range(n):
-        o = orc.lstm_layer_forward(orc.quantize_layer(w["layers"][k]), cur, taps=True)
-        got = u8(g["codes"][k].codes)[:, :48].reshape(T, B, 48)
+        o = orc.lstm_layer_forward(orc.quantize_layer(w["layers"][k]), cur, h0[k], c0[k], taps=True)
+        got = u8(g["codes"][k].codes)[:, :H].reshape(T, B, H)
         assert np.array_equal(got, o["h_codes"]), f"layer {k}"
         assert np.array_equal(np_(g["codes"][k].zero).reshape(T, B), o["h_zero"])
+        for name in ("acc_x", "acc_h", "h_codes", "h_zero", "h_inv_q", "h"):
+            got = np_(g["layers"][k][name])
+            if name == "h_codes":
+                got = got.view(np.uint8) ^ 0x80
+            assert np.array_equal(got, o[name]), f"layer {k} {name}"
+        assert np.array_equal(np_(s_out[k][0]), o["hT"]), f"layer {k} hT"
+        assert np.array_equal(np_(s_out[k][1]), o["cT"]), f"layer {k} cT"
         cur = o["h"]
     assert np.array_equal(np_(g["h"]), cur)
+
+
+def _stream(ql, M, x, cuts):
+    """The forward of x [T][B][in] cut at frames `cuts`, chained through each
+    chunk's final state (two state buffers used in turn)."""
+    B = x.shape[1]
+    bufs = [ql.empty_state(M, B), ql.empty_state(M, B)]
+    state, posts, codes = None, [], []
+    bounds = [0, *cuts, x.shape[0]]
+    for i, (a, b) in enumerate(zip(bounds[:-1], bounds[1:])):
+        out = bufs[i & 1]
+        g = ql.acoustic_model_forward(M, x[a:b].contiguous(), taps=("h_codes",), state_in=state,
+                                      state_out=out)
+        posts.append(g["post"])
+        codes.append([lt["h_codes"] for lt in g["layers"]])
+        state = out
+    return torch.cat(posts), [torch.cat([c[l] for c in codes]) for l in range(len(M.layers))]
+
+
+@pytest.mark.parametrize("layers,H,P,B,cuts", [
+    (3, 48, 0, 1, [1, 7, 8]),       # one-row wavefront, one-frame chunk
+    (3, 48, 0, 20, [5, 11]),        # batched wavefront (counters)
+    (3, 48, 16, 1, [4, 13]),        # projection wavefront
+    (1, 40, 0, 3, [6]),             # one layer per launch
+    (2, 40, 24, 5, [3, 9]),         # batched projection layers, one per launch
+])
+def test_model_stream_chunks_equal_one_call(ql, layers, H, P, B, cuts):
+    """A stream cut into chunks and chained through (hT, cT) -> (h0, c0) gives
+    the posteriors and codes of one call over the whole stream, bit for bit,
+    on every path the model forward takes."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(40, H, layers, proj=P, states=64, seed=layers * 10 + B + P)
+    M = ql.quantize_model(w)
+    x = torch.from_numpy(np.random.default_rng(B).standard_normal((17, B, 40)).astype(np.float32)).cuda()
+    full = ql.acoustic_model_forward(M, x, taps=("h_codes",))
+    post, codes = _stream(ql, M, x, cuts)
+    assert torch.equal(post, full["post"])
+    for l in range(layers):
+        assert torch.equal(codes[l], full["layers"][l]["h_codes"]), l
+
+
+def test_model_5x500_stream_chunks_T500_B1(ql):
+    """The 5 x 500 + softmax 8192 model at batch 1 (T = 500) fed as a live
+    stream in chunks of 1 to 250 frames: bit-identical to one call."""
+    from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T500_B1 as W_, model_weights, features
+    M = ql.quantize_model(model_weights(W_)[0])
+    x = torch.from_numpy(features(W_)).cuda()
+    full = ql.acoustic_model_forward(M, x, taps=("h_codes",))
+    post, codes = _stream(ql, M, x, [1, 100, 250])
+    assert torch.equal(post, full["post"])
+    for l in range(5):
+        assert torch.equal(codes[l], full["layers"][l]["h_codes"]), l

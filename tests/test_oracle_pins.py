@@ -327,6 +327,54 @@ def test_float_lstm_matches_torch(orc, proj):
     assert np.max(np.abs(o["cT"] - cT)) < 2e-6
 
 
+@pytest.mark.parametrize("proj", [0, 12])
+def test_float_lstm_with_initial_state_matches_torch(orc, proj):
+    """The same from a nonzero (h0, c0), and its final state (hT, cT)."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(24, 20, 1, proj=proj, seed=4)
+    L = w["layers"][0]
+    rng = np.random.default_rng(14)
+    R = proj if proj else 20
+    x = rng.standard_normal((17, 3, 24)).astype(np.float32)
+    h0 = (np.tanh(rng.standard_normal((3, R))) * 0.8).astype(np.float32)
+    c0 = rng.standard_normal((3, 20)).astype(np.float32)
+    o = orc.lstm_layer_forward_f32(L, x, h0, c0)
+    ref, hT, cT = _torch_lstm(L, x, h0, c0)
+    assert np.max(np.abs(o["h"] - ref)) < 2e-6
+    assert np.max(np.abs(o["hT"] - hT)) < 2e-6
+    assert np.max(np.abs(o["cT"] - cT)) < 2e-6
+    # the initial state is used: zeros give a different first step
+    z = orc.lstm_layer_forward_f32(L, x[:1])
+    assert np.max(np.abs(z["h"][0] - o["h"][0])) > 1e-3
+
+
+@pytest.mark.parametrize("proj", [0, 8])
+def test_float_model_matches_torch_composition(orc, proj):
+    """The unquantized acoustic model (the float baseline of Section 5):
+    stacked layers, each fed the previous layer's h, then W_y h + b_y and a
+    softmax, against torch in fp64 (chained nn.LSTM layers, nn.functional
+    linear and softmax).  A dropped b_y, a layer fed the wrong input or a
+    softmax over the wrong axis each fail it."""
+    import torch
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(16, 24, 3, proj=proj, states=37, seed=9 + proj)
+    # a b_y large enough to move the posteriors far beyond the tolerance
+    w["by"] = np.random.default_rng(2).uniform(-2, 2, 37).astype(np.float32)
+    x = np.random.default_rng(15).standard_normal((11, 4, 16)).astype(np.float32)
+    o = orc.acoustic_model_forward_f32(w, x)
+    cur = x
+    for L in w["layers"]:
+        cur = _torch_lstm(L, cur)[0]
+    with torch.no_grad():
+        lg = torch.nn.functional.linear(torch.from_numpy(cur),
+                                        torch.from_numpy(w["Wy"].astype(np.float64)),
+                                        torch.from_numpy(w["by"].astype(np.float64)))
+        ref = torch.softmax(lg, dim=-1).numpy()
+    assert o["post"].shape == (11, 4, 37)
+    assert np.max(np.abs(o["post"] - ref)) < 2e-6
+    assert np.max(np.abs(o["post"].astype(np.float64).sum(-1) - 1.0)) < 1e-6
+
+
 def _recovered(orc, codes, z, iq):
     codes = np.atleast_2d(codes)
     q = orc.QMatrix(codes, np.zeros(codes.shape[0]), np.atleast_1d(np.int32(z)),
