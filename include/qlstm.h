@@ -67,7 +67,8 @@ typedef enum {
   QL_EWORKSPACE = -4,   /* workspace null or smaller than the query returned        */
   QL_EHIP = -5,         /* HIP runtime error                                        */
   QL_EUNSUPPORTED = -6, /* shape outside what the kernels implement                 */
-  QL_ETIMEOUT = -7      /* a persistent kernel's bounded inter-block wait expired   */
+  QL_ETIMEOUT = -7,     /* a persistent kernel's bounded inter-block wait expired   */
+  QL_ESCRATCH = -8      /* needs more than the static scratch of the no-alloc call  */
 } ql_status;
 
 typedef enum { QL_ACT_PER_TENSOR = 0, QL_ACT_PER_ROW = 1 } ql_act_gran;
@@ -258,6 +259,29 @@ ql_status ql_acoustic_model_forward_stream(const ql_model *M, const float *feats
                                            const ql_lstm_state *state_out, float *post,
                                            const ql_model_taps *taps, void *ws, size_t ws_bytes,
                                            void *stream);
+
+/* ---- the stream step for callers that cannot allocate -------------------------
+ * For callers that must not allocate device memory or hand over a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The same computation as ql_acoustic_model_forward_stream
+ * (without taps), on a scratch buffer the library holds in a static device
+ * array of QL_NOALLOC_SCRATCH_BYTES per GPU (resolved once per device on the
+ * first call there and kept until the process ends).  Calls whose
+ * ql_acoustic_model_workspace(M, T, B) exceeds it return QL_ESCRATCH before
+ * anything is enqueued (the 5 x 500 model with an 8192-way softmax fits chunks
+ * of up to about 1700 frames at batch 1).  Every call on one GPU uses that
+ * GPU's one scratch array: calls that overlap in time on one GPU (other
+ * streams, other threads) race and give undefined results; calls ordered on
+ * one stream are safe (each clears what it needs).  timed_out (device int32,
+ * nullable) receives 1 if a persistent kernel's bounded wait expired (the
+ * outputs are then undefined), else 0, in stream order.  Allocates nothing:
+ * no hipMalloc, no hipFree, no allocating library call. */
+#define QL_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+ql_status ql_acoustic_model_forward_stream_noalloc(const ql_model *M, const float *feats,
+                                                   int64_t T, int64_t B,
+                                                   const ql_lstm_state *state_in,
+                                                   const ql_lstm_state *state_out, float *post,
+                                                   int32_t *timed_out, void *stream);
 
 /* ---- frontend fused into the input quantizer (Section 4) ------------------------
  * The network's input at presented step t of utterance b is the concatenation of

@@ -12,7 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libqlstm.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
-SOURCES = ["ql_quantize.hip", "ql_gemm.hip", "ql_recurrent.hip", "ql_stack.hip", "ql_pstack.hip", "ql_f32.hip", "ql_api.cpp"]
+SOURCES = ["ql_quantize.hip", "ql_gemm.hip", "ql_recurrent.hip", "ql_stack.hip", "ql_pstack.hip",
+           "ql_f32.hip", "ql_api.cpp", "ql_scratch.hip"]
 HEADERS = ["ql_device.h", "ql_exchange.h", "ql_launch.h", "ql_rec_common.h"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -163,6 +163,7 @@ const char *ql_status_str(ql_status s) {
     case QL_EHIP: return "HIP runtime error";
     case QL_EUNSUPPORTED: return "shape not supported by the kernels";
     case QL_ETIMEOUT: return "persistent kernel wait timed out";
+    case QL_ESCRATCH: return "call needs more than the no-alloc entry point's static scratch";
   }
   return "unknown status";
 }

@@ -20,7 +20,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqlstm.so")
 
 QL_OK, QL_EINVAL, QL_ESHAPE, QL_EOVERFLOW, QL_EWORKSPACE, QL_EHIP, QL_EUNSUPPORTED, \
-    QL_ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
+    QL_ETIMEOUT, QL_ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7, -8
+NOALLOC_SCRATCH_BYTES = 32 << 20  # QL_NOALLOC_SCRATCH_BYTES
 QL_ACT_PER_TENSOR, QL_ACT_PER_ROW = 0, 1
 
 EXPORTS = [
@@ -34,6 +35,7 @@ EXPORTS = [
     "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch", "ql_stacked_input_count",
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
     "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
+    "ql_acoustic_model_forward_stream_noalloc",
 ]
 
 
@@ -137,6 +139,9 @@ def load(path: str = LIB_PATH):
     L.ql_acoustic_model_forward_stream.argtypes = [C.POINTER(CModel), vp, i64, i64,
                                                    C.POINTER(CState), C.POINTER(CState), vp,
                                                    C.POINTER(CModelTaps), vp, sz, vp]
+    L.ql_acoustic_model_forward_stream_noalloc.argtypes = [C.POINTER(CModel), vp, i64, i64,
+                                                           C.POINTER(CState), C.POINTER(CState),
+                                                           vp, vp, vp]
     L.ql_lstm_stack_layers_per_launch.argtypes = [C.POINTER(CLayer), i32, i64, i64]
     L.ql_lstm_stack_layers_per_launch.restype = i32
     L.ql_stacked_input_count.argtypes = [i64, i32, i32]
@@ -159,7 +164,8 @@ def load(path: str = LIB_PATH):
               "ql_gate_fn", "ql_lstm_recurrence", "ql_f32_matmul", "ql_f32_lstm_layer_forward",
               "ql_f32_acoustic_model_forward", "ql_quantize_activations",
               "ql_lstm_stack_forward", "ql_quantize_stacked_frames",
-              "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream"):
+              "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
+              "ql_acoustic_model_forward_stream_noalloc"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -500,6 +506,21 @@ def acoustic_model_forward(M: Model, feats: torch.Tensor, taps: bool = False,
     if check:
         _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_acoustic_model_forward")
     return out
+
+
+def acoustic_model_forward_stream_noalloc(M: Model, feats: torch.Tensor, post: torch.Tensor,
+                                          state_in=None, state_out=None, timed_out=None):
+    """One chunk of a stream on the library's static scratch
+    (ql_acoustic_model_forward_stream_noalloc): post [T][B][S] and the optional
+    timed_out (int32 device tensor of one element) are the caller's; nothing
+    is allocated here or in the library."""
+    feats = feats.contiguous()
+    T, B, _ = feats.shape
+    cm, keep = M.cstruct()
+    _check(load().ql_acoustic_model_forward_stream_noalloc(
+        C.byref(cm), _ptr(feats), T, B, _state_array(state_in), _state_array(state_out),
+        _ptr(post), _ptr(timed_out), _stream()), "ql_acoustic_model_forward_stream_noalloc")
+    return post
 
 
 def stacked_input_count(nframes: int, stack: int = 8, skip: int = 3) -> int:
