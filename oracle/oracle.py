@@ -65,7 +65,8 @@ class Model(C.Structure):
 class Taps(C.Structure):
     _fields_ = [("acc_x", C.c_void_p), ("acc_h", C.c_void_p), ("acc_r", C.c_void_p),
                 ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p),
-                ("c", C.c_void_p), ("h", C.c_void_p)]
+                ("c", C.c_void_p), ("h", C.c_void_p), ("preact", C.c_void_p),
+                ("gates", C.c_void_p), ("m", C.c_void_p)]
 
 
 class LayerF32(C.Structure):
@@ -75,6 +76,11 @@ class LayerF32(C.Structure):
 
 
 class ModelF32(C.Structure):
+    _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(LayerF32)), ("S", C.c_int64),
+                ("Wy", C.c_void_p), ("by", C.c_void_p)]
+
+
+class TrainModel(C.Structure):
     _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(LayerF32)), ("S", C.c_int64),
                 ("Wy", C.c_void_p), ("by", C.c_void_p)]
 
@@ -100,12 +106,19 @@ def _declare(L):
     L.oracle_acoustic_model_forward.argtypes = [C.POINTER(Model), vp, i64, i64, vp,
                                                 C.POINTER(Taps), vp, vp]
     L.oracle_lstm_layer_forward_f32.argtypes = [C.POINTER(LayerF32), vp, i64, i64, vp, vp,
-                                                vp, vp, vp]
+                                                vp, vp, vp, C.POINTER(Taps)]
+    L.oracle_lstm_layer_backward.argtypes = [C.POINTER(LayerF32), vp, i64, i64, vp, vp, vp, vp,
+                                             vp, vp, vp, vp, vp, vp]
+    L.oracle_output_backward.argtypes = [vp, i64, i64, vp, vp, vp, i64, C.POINTER(C.c_double),
+                                         vp, vp, vp]
+    L.oracle_train_step.argtypes = [C.POINTER(TrainModel), vp, vp, i64, i64, C.c_float, i32,
+                                    i32, i32, C.POINTER(C.c_double), C.POINTER(TrainModel)]
     L.oracle_acoustic_model_forward_f32.argtypes = [C.POINTER(ModelF32), vp, i64, i64, vp]
     for f in ("oracle_quantize", "oracle_dequantize", "oracle_quantized_matmul",
               "oracle_gemm_u8", "oracle_lstm_layer_forward",
               "oracle_acoustic_model_forward", "oracle_lstm_layer_forward_f32",
-              "oracle_acoustic_model_forward_f32"):
+              "oracle_acoustic_model_forward_f32", "oracle_lstm_layer_backward",
+              "oracle_output_backward", "oracle_train_step"):
         getattr(L, f).restype = i32
 
 
@@ -273,9 +286,10 @@ def _taps_arrays(T, B, H, P):
              acc_r=np.empty((T, B, P), np.int32) if P else None,
              h_codes=np.empty((T, B, RD), np.uint8), h_zero=np.empty((T, B), np.int32),
              h_inv_q=np.empty((T, B), np.float32), c=np.empty((T, B, H), np.float32),
-             h=np.empty((T, B, RD), np.float32))
+             h=np.empty((T, B, RD), np.float32), preact=np.empty((T, B, 4 * H), np.float32),
+             gates=np.empty((T, B, 4 * H), np.float32), m=np.empty((T, B, H), np.float32))
     ts = Taps(*[_p(t[k]) for k in ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero",
-                                   "h_inv_q", "c", "h")])
+                                   "h_inv_q", "c", "h", "preact", "gates", "m")])
     return t, ts
 
 
@@ -366,7 +380,8 @@ def _f32(a):
     return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
 
 
-def lstm_layer_forward_f32(L: dict, x, h0=None, c0=None):
+def lstm_layer_forward_f32(L: dict, x, h0=None, c0=None, taps: bool = False):
+    """The unquantized layer -> dict(h, hT, cT[, c, m, gates, h taps])."""
     x = _f32(x)
     T, B, n_in = x.shape
     Wx, Wh, b, Wr = _f32(L["Wx"]), _f32(L["Wh"]), _f32(L["b"]), _f32(L.get("Wr"))
@@ -378,9 +393,17 @@ def lstm_layer_forward_f32(L: dict, x, h0=None, c0=None):
     hT = np.empty((B, RD), np.float32)
     cT = np.empty((B, H), np.float32)
     h0, c0 = _f32(h0), _f32(c0)
+    out = dict(h=h, hT=hT, cT=cT)
+    tp = None
+    if taps:
+        t, ts = _taps_arrays(T, B, H, P)
+        out.update({k: t[k] for k in ("c", "m", "gates")})
+        ts.h = None
+        tp = C.byref(ts)
+        out["_keep"] = t
     _check(lib().oracle_lstm_layer_forward_f32(C.byref(ls), _p(x), T, B, _p(h0), _p(c0),
-                                               _p(h), _p(hT), _p(cT)), "lstm_f32")
-    return dict(h=h, hT=hT, cT=cT)
+                                               _p(h), _p(hT), _p(cT), tp), "lstm_f32")
+    return out
 
 
 def acoustic_model_forward_f32(weights: dict, feats):
@@ -401,3 +424,61 @@ def acoustic_model_forward_f32(weights: dict, feats):
     _check(lib().oracle_acoustic_model_forward_f32(C.byref(m), _p(feats), T, B, _p(post)),
            "model_f32")
     return dict(post=post)
+
+
+# ------------------------------------------------- quantization aware training
+def _train_struct(weights: dict):
+    """Host fp32 copies of a model's parameters and the C struct over them."""
+    keep, ls = [], []
+    for L in weights["layers"]:
+        Wx, Wh, b = (np.array(L[k], dtype=np.float32, copy=True) for k in ("Wx", "Wh", "b"))
+        Wr = None if L.get("Wr") is None else np.array(L["Wr"], dtype=np.float32, copy=True)
+        keep.append(dict(Wx=Wx, Wh=Wh, b=b, Wr=Wr))
+        H = Wx.shape[0] // 4
+        ls.append(LayerF32(Wx.shape[1], H, 0 if Wr is None else Wr.shape[0], _p(Wx), _p(Wh),
+                           _p(Wr), _p(b)))
+    Wy = np.array(weights["Wy"], dtype=np.float32, copy=True)
+    by = np.array(weights["by"], dtype=np.float32, copy=True)
+    arr = (LayerF32 * len(ls))(*ls)
+    st = TrainModel(len(ls), arr, Wy.shape[0], _p(Wy), _p(by))
+    return dict(layers=keep, Wy=Wy, by=by), st, arr
+
+
+def train_step(weights: dict, feats, targets, lr: float, gate_blocks: int = 4,
+               quantize_layers: bool = True, quantize_output: bool = True):
+    """Algorithm 1 on one mini-batch -> (updated weights, gradients, loss).
+    weights is not modified."""
+    feats = _f32(feats)
+    T, B, _ = feats.shape
+    targets = np.ascontiguousarray(targets, dtype=np.int32)
+    assert targets.shape == (T, B)
+    new, st, keep1 = _train_struct(weights)
+    zeros = {"layers": [dict(Wx=np.zeros_like(L["Wx"]), Wh=np.zeros_like(L["Wh"]),
+                             b=np.zeros_like(L["b"]),
+                             Wr=None if L["Wr"] is None else np.zeros_like(L["Wr"]))
+                        for L in new["layers"]],
+             "Wy": np.zeros_like(new["Wy"]), "by": np.zeros_like(new["by"])}
+    grads, gst, keep2 = _train_struct(zeros)
+    loss = C.c_double()
+    _check(lib().oracle_train_step(C.byref(st), _p(feats), _p(targets), T, B, float(lr),
+                                   gate_blocks, int(quantize_layers), int(quantize_output),
+                                   C.byref(loss), C.byref(gst)), "train_step")
+    return new, grads, float(loss.value)
+
+
+def lstm_layer_backward(L: dict, x, gates, c, m, h, dy):
+    """Float BPTT of one layer at the given forward activations -> dict of
+    gradients (Wx, Wh, Wr, b) and dx."""
+    x, gates, c, m, h, dy = (_f32(a) for a in (x, gates, c, m, h, dy))
+    T, B, n_in = x.shape
+    Wx, Wh, b, Wr = _f32(L["Wx"]), _f32(L["Wh"]), _f32(L["b"]), _f32(L.get("Wr"))
+    H = Wx.shape[0] // 4
+    P = 0 if Wr is None else Wr.shape[0]
+    ls = LayerF32(n_in, H, P, _p(Wx), _p(Wh), _p(Wr), _p(b))
+    out = dict(Wx=np.empty_like(Wx), Wh=np.empty_like(Wh), b=np.empty_like(b),
+               Wr=None if Wr is None else np.empty_like(Wr), dx=np.empty_like(x))
+    _check(lib().oracle_lstm_layer_backward(C.byref(ls), _p(x), T, B, _p(gates), _p(c), _p(m),
+                                            _p(h), _p(dy), _p(out["Wx"]), _p(out["Wh"]),
+                                            _p(out["Wr"]), _p(out["b"]), _p(out["dx"])),
+           "lstm_layer_backward")
+    return out

@@ -330,7 +330,16 @@ int oracle_lstm_layer_forward(const orc_layer *L, const float *x, int64_t T,
         const float c = (fg * cprev[j]) + (ig * gg);
         cprev[j] = c;
         m[j] = og * oracle_tanhf(c);
+        if (taps && taps->preact) {
+          float *pa = taps->preact + row * 4 * H;
+          pa[j] = ai, pa[H + j] = af, pa[2 * H + j] = ag, pa[3 * H + j] = ao;
+        }
+        if (taps && taps->gates) {
+          float *ga = taps->gates + row * 4 * H;
+          ga[j] = ig, ga[H + j] = fg, ga[2 * H + j] = gg, ga[3 * H + j] = og;
+        }
       }
+      if (taps && taps->m) memcpy(taps->m + row * H, m, sizeof(float) * (size_t)H);
       if (P) { /* linear projection: h = R(Mult(Q(m), Wr')) */
         orc_qparams pm;
         oracle_quantize_set(m, H, mc, &pm, NULL);
@@ -439,7 +448,8 @@ static void flinear_vec(const float *W, int64_t N, int64_t K, const float *x,
 
 int oracle_lstm_layer_forward_f32(const orc_layer_f32 *L, const float *x,
                                   int64_t T, int64_t B, const float *h0,
-                                  const float *c0, float *h, float *hT, float *cT) {
+                                  const float *c0, float *h, float *hT, float *cT,
+                                  const orc_layer_taps *taps) {
   const int64_t H = L->hidden, P = L->proj, IN = L->in;
   const int64_t RD = P ? P : H;
   if (T < 0 || B < 0 || H <= 0 || IN <= 0 || P < 0 || !L->Wx || !L->Wh || !L->bias ||
@@ -467,6 +477,10 @@ int oracle_lstm_layer_forward_f32(const orc_layer_f32 *L, const float *x,
         const float c = (fg * cprev[j]) + (ig * gg);
         cprev[j] = c;
         m[j] = og * oracle_tanhf(c);
+        if (taps && taps->gates) {
+          float *ga = taps->gates + row * 4 * H;
+          ga[j] = ig, ga[H + j] = fg, ga[2 * H + j] = gg, ga[3 * H + j] = og;
+        }
       }
       if (P)
         flinear_vec(L->Wr, P, H, m, hn);
@@ -474,6 +488,9 @@ int oracle_lstm_layer_forward_f32(const orc_layer_f32 *L, const float *x,
         memcpy(hn, m, sizeof(float) * (size_t)H);
       memcpy(h + row * RD, hn, sizeof(float) * (size_t)RD);
       memcpy(hprev, hn, sizeof(float) * (size_t)RD);
+      if (taps && taps->c) memcpy(taps->c + row * H, cprev, sizeof(float) * (size_t)H);
+      if (taps && taps->m) memcpy(taps->m + row * H, m, sizeof(float) * (size_t)H);
+      if (taps && taps->h) memcpy(taps->h + row * RD, hn, sizeof(float) * (size_t)RD);
     }
     if (hT) memcpy(hT + b * RD, hprev, sizeof(float) * (size_t)RD);
     if (cT) memcpy(cT + b * H, cprev, sizeof(float) * (size_t)H);
@@ -498,7 +515,7 @@ int oracle_acoustic_model_forward_f32(const orc_model_f32 *M, const float *feats
     if (L->in != width) return -2;
     const int64_t RD = L->proj ? L->proj : L->hidden;
     float *hl = (float *)malloc(sizeof(float) * (size_t)(T * B * RD > 0 ? T * B * RD : 1));
-    int rc = oracle_lstm_layer_forward_f32(L, x, T, B, NULL, NULL, hl, NULL, NULL);
+    int rc = oracle_lstm_layer_forward_f32(L, x, T, B, NULL, NULL, hl, NULL, NULL, NULL);
     free(prev);
     if (rc) {
       free(hl);
@@ -523,4 +540,327 @@ int oracle_acoustic_model_forward_f32(const orc_model_f32 *M, const float *feats
   }
   free(prev);
   return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Quantization aware training (Section 3.2, Algorithm 1)                    */
+/*                                                                           */
+/* The forward pass runs in quantized form (infer-and-recover: the inference */
+/* path above, on freshly quantized copies of the float parameters); the     */
+/* error, the gradients and the update are ordinary floating-point           */
+/* backpropagation with the float parameters, evaluated at the activations   */
+/* the quantized forward pass produced.  Quantization itself is not          */
+/* differentiated.  Float arithmetic of the backward pass is done in fp64.   */
+/* ------------------------------------------------------------------------ */
+
+/* LSTM backward through time, one layer (gate order i, f, g, o; c = f c + i g;
+ * m = o tanh(c); h = m, or h = Wr m with a projection; zero initial state). */
+int oracle_lstm_layer_backward(const orc_layer_f32 *L, const float *x, int64_t T, int64_t B,
+                               const float *gates, const float *c, const float *m,
+                               const float *h, const float *dy, float *dWx, float *dWh,
+                               float *dWr, float *db, float *dx) {
+  const int64_t H = L->hidden, P = L->proj, IN = L->in;
+  const int64_t RD = P ? P : H, G = 4 * H, N = T * B;
+  if (T < 0 || B < 0 || H <= 0 || IN <= 0 || P < 0 || !L->Wx || !L->Wh || (P && !L->Wr))
+    return -2;
+  if (N > 0 && (!x || !gates || !c || !m || !h || !dy)) return -2;
+  /* dC/da for every step: the serial part, one utterance at a time */
+  double *da = (double *)calloc((size_t)(N * G > 0 ? N * G : 1), sizeof(double));
+  double *dh_all = (double *)calloc((size_t)(N * RD > 0 ? N * RD : 1), sizeof(double));
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t b = 0; b < B; ++b) {
+    double *dh_next = (double *)calloc((size_t)RD, sizeof(double)); /* via W_h from step t+1 */
+    double *dc_next = (double *)calloc((size_t)H, sizeof(double));  /* via f from step t+1 */
+    double *dm = (double *)malloc(sizeof(double) * (size_t)H);
+    for (int64_t t = T - 1; t >= 0; --t) {
+      const int64_t row = t * B + b;
+      double *dh = dh_all + row * RD;
+      for (int64_t k = 0; k < RD; ++k) dh[k] = (double)dy[row * RD + k] + dh_next[k];
+      if (P) { /* h = Wr m: dC/dm = Wr^T dC/dh */
+        for (int64_t j = 0; j < H; ++j) {
+          double s = 0.0;
+          for (int64_t p = 0; p < P; ++p) s += (double)L->Wr[p * H + j] * dh[p];
+          dm[j] = s;
+        }
+      } else {
+        for (int64_t j = 0; j < H; ++j) dm[j] = dh[j];
+      }
+      const float *gt = gates + row * G;
+      double *dat = da + row * G;
+      for (int64_t j = 0; j < H; ++j) {
+        const double ig = gt[j], fg = gt[H + j], gg = gt[2 * H + j], og = gt[3 * H + j];
+        const double ct = c[row * H + j];
+        const double cp = t > 0 ? (double)c[(row - B) * H + j] : 0.0;
+        const double tc = tanh(ct);
+        const double d_o = dm[j] * tc;
+        const double d_c = dm[j] * og * (1.0 - tc * tc) + dc_next[j];
+        const double d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cp;
+        dc_next[j] = d_c * fg;
+        dat[j] = d_i * ig * (1.0 - ig);         /* sigmoid' = s (1 - s) */
+        dat[H + j] = d_f * fg * (1.0 - fg);
+        dat[2 * H + j] = d_g * (1.0 - gg * gg); /* tanh' = 1 - tanh^2 */
+        dat[3 * H + j] = d_o * og * (1.0 - og);
+      }
+      /* to h_{t-1} through W_h */
+      for (int64_t k = 0; k < RD; ++k) {
+        double s = 0.0;
+        for (int64_t n = 0; n < G; ++n) s += (double)L->Wh[n * RD + k] * dat[n];
+        dh_next[k] = s;
+      }
+    }
+    free(dh_next);
+    free(dc_next);
+    free(dm);
+  }
+  /* gradients of the parameters: sums over all T*B frames */
+#pragma omp parallel for schedule(static)
+  for (int64_t n = 0; n < G; ++n) {
+    double sb = 0.0;
+    for (int64_t r = 0; r < N; ++r) sb += da[r * G + n];
+    if (db) db[n] = (float)sb;
+    if (dWx)
+      for (int64_t i = 0; i < IN; ++i) {
+        double s = 0.0;
+        for (int64_t r = 0; r < N; ++r) s += da[r * G + n] * (double)x[r * IN + i];
+        dWx[n * IN + i] = (float)s;
+      }
+    if (dWh)
+      for (int64_t k = 0; k < RD; ++k) {
+        double s = 0.0; /* h_{t-1} = 0 at t = 0 */
+        for (int64_t r = B; r < N; ++r) s += da[r * G + n] * (double)h[(r - B) * RD + k];
+        dWh[n * RD + k] = (float)s;
+      }
+  }
+  if (P && dWr) {
+#pragma omp parallel for schedule(static)
+    for (int64_t p = 0; p < P; ++p)
+      for (int64_t j = 0; j < H; ++j) {
+        double s = 0.0;
+        for (int64_t r = 0; r < N; ++r) s += dh_all[r * RD + p] * (double)m[r * H + j];
+        dWr[p * H + j] = (float)s;
+      }
+  }
+  if (dx) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < N; ++r)
+      for (int64_t i = 0; i < IN; ++i) {
+        double s = 0.0;
+        for (int64_t n = 0; n < G; ++n) s += (double)L->Wx[n * IN + i] * da[r * G + n];
+        dx[r * IN + i] = (float)s;
+      }
+  }
+  free(da);
+  free(dh_all);
+  return 0;
+}
+
+/* C = -(1/N) sum_r log p_r[target_r]; dC/dz = (p - onehot) / N for the
+ * softmax of z = Wy hL + by. */
+int oracle_output_backward(const float *Wy, int64_t S, int64_t R, const float *hL,
+                           const float *post, const int32_t *targets, int64_t N,
+                           double *loss, float *dWy, float *dby, float *dhL) {
+  if (S <= 0 || R <= 0 || N < 0 || !Wy) return -2;
+  for (int64_t r = 0; r < N; ++r)
+    if (targets[r] < 0 || targets[r] >= S) return -2;
+  double *dz = (double *)malloc(sizeof(double) * (size_t)(N * S > 0 ? N * S : 1));
+  double l = 0.0;
+  for (int64_t r = 0; r < N; ++r) {
+    l -= log((double)post[r * S + targets[r]]);
+    for (int64_t s = 0; s < S; ++s)
+      dz[r * S + s] = ((double)post[r * S + s] - (s == targets[r] ? 1.0 : 0.0)) / (double)N;
+  }
+  if (loss) *loss = N > 0 ? l / (double)N : 0.0;
+#pragma omp parallel for schedule(static)
+  for (int64_t s = 0; s < S; ++s) {
+    double sb = 0.0;
+    for (int64_t r = 0; r < N; ++r) sb += dz[r * S + s];
+    if (dby) dby[s] = (float)sb;
+    if (dWy)
+      for (int64_t k = 0; k < R; ++k) {
+        double sw = 0.0;
+        for (int64_t r = 0; r < N; ++r) sw += dz[r * S + s] * (double)hL[r * R + k];
+        dWy[s * R + k] = (float)sw;
+      }
+  }
+  if (dhL) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < N; ++r)
+      for (int64_t k = 0; k < R; ++k) {
+        double sh = 0.0;
+        for (int64_t s = 0; s < S; ++s) sh += (double)Wy[s * R + k] * dz[r * S + s];
+        dhL[r * R + k] = (float)sh;
+      }
+  }
+  free(dz);
+  return 0;
+}
+
+/* One quantized copy of a float matrix (w^q of Algorithm 1). */
+typedef struct {
+  uint8_t *codes;
+  int32_t *zero;
+  float *inv_q;
+  orc_qmat q;
+} orc_qcopy;
+static void qcopy_make(orc_qcopy *c, const float *W, int64_t rows, int64_t cols, int32_t nb) {
+  c->codes = (uint8_t *)malloc((size_t)(rows * cols > 0 ? rows * cols : 1));
+  c->zero = (int32_t *)malloc(sizeof(int32_t) * (size_t)nb);
+  c->inv_q = (float *)malloc(sizeof(float) * (size_t)nb);
+  oracle_quantize(W, rows, cols, nb, c->codes, NULL, c->zero, c->inv_q, NULL);
+  c->q.rows = rows;
+  c->q.cols = cols;
+  c->q.nblocks = nb;
+  c->q.codes = c->codes;
+  c->q.zero = c->zero;
+  c->q.inv_q = c->inv_q;
+}
+static void qcopy_free(orc_qcopy *c) {
+  free(c->codes);
+  free(c->zero);
+  free(c->inv_q);
+}
+
+int oracle_train_step(const orc_train_model *M, const float *feats, const int32_t *targets,
+                      int64_t T, int64_t B, float lr, int32_t gate_blocks,
+                      int32_t quantize_layers, int32_t quantize_output, double *loss,
+                      const orc_train_model *grads) {
+  if (!M || M->nlayers <= 0 || !M->layers || !M->Wy || !M->by || M->S <= 0) return -2;
+  if (T < 0 || B < 0 || gate_blocks <= 0 || (quantize_output && !quantize_layers)) return -2;
+  if (!grads || !grads->layers || !grads->Wy || !grads->by) return -2;
+  const int32_t NL = M->nlayers;
+  const int64_t N = T * B, S = M->S;
+  int64_t width = M->layers[0].in;
+  for (int32_t l = 0; l < NL; ++l) {
+    const orc_train_layer *L = &M->layers[l];
+    if (L->in != width || (4 * L->hidden) % gate_blocks != 0) return -2;
+    width = L->proj ? L->proj : L->hidden;
+  }
+  const int64_t RL = width;
+
+  /* 1. w^q <- quantize(w) */
+  orc_qcopy *qx = (orc_qcopy *)calloc((size_t)NL, sizeof(orc_qcopy));
+  orc_qcopy *qh = (orc_qcopy *)calloc((size_t)NL, sizeof(orc_qcopy));
+  orc_qcopy *qr = (orc_qcopy *)calloc((size_t)NL, sizeof(orc_qcopy));
+  orc_qcopy qy;
+  memset(&qy, 0, sizeof(qy));
+  if (quantize_layers)
+    for (int32_t l = 0; l < NL; ++l) {
+      const orc_train_layer *L = &M->layers[l];
+      const int64_t RD = L->proj ? L->proj : L->hidden;
+      qcopy_make(&qx[l], L->Wx, 4 * L->hidden, L->in, gate_blocks);
+      qcopy_make(&qh[l], L->Wh, 4 * L->hidden, RD, gate_blocks);
+      if (L->proj) qcopy_make(&qr[l], L->Wr, L->proj, L->hidden, 1);
+    }
+  if (quantize_output) qcopy_make(&qy, M->Wy, S, RL, 1);
+
+  /* 2. a_k <- infer-and-recover(a_{k-1}, w^q, b), keeping what the backward
+   *    pass needs: every layer's input, gates, c, m and h */
+  float **xin = (float **)calloc((size_t)NL + 1, sizeof(float *));
+  float **gat = (float **)calloc((size_t)NL, sizeof(float *));
+  float **cst = (float **)calloc((size_t)NL, sizeof(float *));
+  float **mo = (float **)calloc((size_t)NL, sizeof(float *));
+  xin[0] = (float *)feats;
+  int rc = 0;
+  for (int32_t l = 0; l < NL && rc == 0; ++l) {
+    const orc_train_layer *L = &M->layers[l];
+    const int64_t H = L->hidden, RD = L->proj ? L->proj : H;
+    xin[l + 1] = (float *)malloc(sizeof(float) * (size_t)(N * RD > 0 ? N * RD : 1));
+    gat[l] = (float *)malloc(sizeof(float) * (size_t)(N * 4 * H > 0 ? N * 4 * H : 1));
+    cst[l] = (float *)malloc(sizeof(float) * (size_t)(N * H > 0 ? N * H : 1));
+    mo[l] = (float *)malloc(sizeof(float) * (size_t)(N * H > 0 ? N * H : 1));
+    orc_layer_taps tp;
+    memset(&tp, 0, sizeof(tp));
+    tp.gates = gat[l];
+    tp.c = cst[l];
+    tp.m = mo[l];
+    if (quantize_layers) {
+      orc_layer ql;
+      ql.in = L->in;
+      ql.hidden = H;
+      ql.proj = L->proj;
+      ql.Wx = qx[l].q;
+      ql.Wh = qh[l].q;
+      if (L->proj) ql.Wr = qr[l].q;
+      else memset(&ql.Wr, 0, sizeof(ql.Wr));
+      ql.bias = L->bias;
+      rc = oracle_lstm_layer_forward(&ql, xin[l], T, B, NULL, NULL, xin[l + 1], NULL, NULL, &tp);
+    } else {
+      orc_layer_f32 fl = {L->in, H, L->proj, L->Wx, L->Wh, L->Wr, L->bias};
+      rc = oracle_lstm_layer_forward_f32(&fl, xin[l], T, B, NULL, NULL, xin[l + 1], NULL, NULL,
+                                         &tp);
+    }
+  }
+  float *post = (float *)malloc(sizeof(float) * (size_t)(N * S > 0 ? N * S : 1));
+  float *dh = (float *)malloc(sizeof(float) * (size_t)(N * RL > 0 ? N * RL : 1));
+  if (rc == 0) {
+    const float *hL = xin[NL];
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < N; ++r) {
+      float *lg = (float *)malloc(sizeof(float) * (size_t)S);
+      if (quantize_output) { /* 'quant-all': the output layer quantized too */
+        uint8_t *hc = (uint8_t *)malloc((size_t)RL);
+        orc_qparams p;
+        oracle_quantize_set(hL + r * RL, RL, hc, &p, NULL);
+        qlinear_vec(&qy.q, hc, p.z, p.inv_q, lg, NULL);
+        free(hc);
+      } else { /* 'quant': a float output layer */
+        flinear_vec(M->Wy, S, RL, hL + r * RL, lg);
+      }
+      for (int64_t s = 0; s < S; ++s) lg[s] = lg[s] + M->by[s];
+      softmax_row(lg, S, post + r * S);
+      free(lg);
+    }
+    /* 3. output error, then the layers from the top (float parameters) */
+    double l = 0.0;
+    rc = oracle_output_backward(M->Wy, S, RL, hL, post, targets, N, &l,
+                                grads->Wy, grads->by, dh);
+    if (loss) *loss = l;
+  }
+  for (int32_t l = NL - 1; l >= 0 && rc == 0; --l) {
+    const orc_train_layer *L = &M->layers[l];
+    const orc_layer_f32 fl = {L->in, L->hidden, L->proj, L->Wx, L->Wh, L->Wr, L->bias};
+    float *dx = l > 0 ? (float *)malloc(sizeof(float) * (size_t)(N * L->in > 0 ? N * L->in : 1))
+                      : NULL;
+    const orc_train_layer *g = &grads->layers[l];
+    rc = oracle_lstm_layer_backward(&fl, xin[l], T, B, gat[l], cst[l], mo[l], xin[l + 1], dh,
+                                    g->Wx, g->Wh, g->Wr, g->bias, dx);
+    free(dh);
+    dh = dx;
+  }
+  free(dh);
+  /* 4. w <- w - lr dC/dw (fp32): every weight and bias */
+  if (rc == 0) {
+    for (int32_t l = 0; l < NL; ++l) {
+      const orc_train_layer *L = &M->layers[l], *g = &grads->layers[l];
+      const int64_t H = L->hidden, RD = L->proj ? L->proj : H;
+      for (int64_t i = 0; i < 4 * H * L->in; ++i) L->Wx[i] = L->Wx[i] - lr * g->Wx[i];
+      for (int64_t i = 0; i < 4 * H * RD; ++i) L->Wh[i] = L->Wh[i] - lr * g->Wh[i];
+      for (int64_t i = 0; i < 4 * H; ++i) L->bias[i] = L->bias[i] - lr * g->bias[i];
+      if (L->proj)
+        for (int64_t i = 0; i < L->proj * H; ++i) L->Wr[i] = L->Wr[i] - lr * g->Wr[i];
+    }
+    for (int64_t i = 0; i < S * RL; ++i) M->Wy[i] = M->Wy[i] - lr * grads->Wy[i];
+    for (int64_t i = 0; i < S; ++i) M->by[i] = M->by[i] - lr * grads->by[i];
+  }
+  for (int32_t l = 0; l < NL; ++l) {
+    if (quantize_layers) {
+      qcopy_free(&qx[l]);
+      qcopy_free(&qh[l]);
+      if (M->layers[l].proj) qcopy_free(&qr[l]);
+    }
+    free(xin[l + 1]);
+    free(gat[l]);
+    free(cst[l]);
+    free(mo[l]);
+  }
+  if (quantize_output) qcopy_free(&qy);
+  free(qx);
+  free(qh);
+  free(qr);
+  free(xin);
+  free(gat);
+  free(cst);
+  free(mo);
+  free(post);
+  return rc;
 }

@@ -79,6 +79,9 @@ typedef struct {
   float *h_inv_q;   /* [T][B]     recovery factor of h_t                     */
   float *c;         /* [T][B][H]  cell state after step t                    */
   float *h;         /* [T][B][R]  the layer's fp32 output h_t                */
+  float *preact;    /* [T][B][4H] gate pre-activations (Wx x + b) + Wh h     */
+  float *gates;     /* [T][B][4H] i, f, g, o after their activation functions */
+  float *m;         /* [T][B][H]  cell output o tanh(c) (before a projection) */
 } orc_layer_taps;
 
 /* ---- scalar pieces ------------------------------------------------------ */
@@ -139,9 +142,56 @@ typedef struct {
 } orc_model_f32;
 int oracle_lstm_layer_forward_f32(const orc_layer_f32 *L, const float *x,
                                   int64_t T, int64_t B, const float *h0,
-                                  const float *c0, float *h, float *hT, float *cT);
+                                  const float *c0, float *h, float *hT, float *cT,
+                                  const orc_layer_taps *taps);
 int oracle_acoustic_model_forward_f32(const orc_model_f32 *M, const float *feats,
                                       int64_t T, int64_t B, float *post);
+
+/* ---- quantization aware training (Section 3.2, Algorithm 1) ------------ */
+/* Float master parameters of an acoustic model (fp32, host, updated in
+ * place by the training step); the same layout holds gradients. */
+typedef struct {
+  int64_t in, hidden, proj;
+  float *Wx, *Wh, *Wr, *bias; /* [4H][in], [4H][R], [P][H], [4H] */
+} orc_train_layer;
+typedef struct {
+  int32_t nlayers;
+  const orc_train_layer *layers;
+  int64_t S;
+  float *Wy, *by; /* [S][R_last], [S] */
+} orc_train_model;
+
+/* Backward pass through time of one LSTM layer in floating point, with the
+ * float weights of L, given what its forward pass produced: the layer input
+ * x [T][B][in], gates [T][B][4H] (after activation), c [T][B][H], m
+ * [T][B][H] (o tanh c), h [T][B][R], zero initial state, and dC/dh dy
+ * [T][B][R].  Writes dC/dWx, dC/dWh, dC/dWr (P > 0), dC/db and dC/dx
+ * [T][B][in] (each nullable). */
+int oracle_lstm_layer_backward(const orc_layer_f32 *L, const float *x, int64_t T, int64_t B,
+                               const float *gates, const float *c, const float *m,
+                               const float *h, const float *dy, float *dWx, float *dWh,
+                               float *dWr, float *db, float *dx);
+/* Frame-level cross-entropy of N frames of posteriors post [N][S] against
+ * targets [N], averaged over the frames; its gradient through the output
+ * layer z = Wy hL + by (Wy [S][R] float) to dC/dWy, dC/dby and dC/dhL
+ * [N][R]. */
+int oracle_output_backward(const float *Wy, int64_t S, int64_t R, const float *hL,
+                           const float *post, const int32_t *targets, int64_t N,
+                           double *loss, float *dWy, float *dby, float *dhL);
+/* One training step (Algorithm 1) on a mini-batch feats [T][B][in] with
+ * frame targets [T][B]: the parameters are quantized (W_x, W_h in gate_blocks
+ * row blocks, W_r and W_y per matrix) and the forward pass runs in quantized
+ * form (quantize_layers = 1; the inference path of this oracle) or in float
+ * (0), with the output layer quantized (quantize_output = 1, 'quant-all') or
+ * float (0, 'quant'); the loss and the backward pass are float, with the
+ * float parameters, at the forward pass's activations; every weight and bias
+ * is then moved by -lr times its gradient.  loss (nullable) receives the
+ * mini-batch loss, grads (required; the shapes of M) the gradients.
+ * quantize_output = 1 needs quantize_layers = 1. */
+int oracle_train_step(const orc_train_model *M, const float *feats, const int32_t *targets,
+                      int64_t T, int64_t B, float lr, int32_t gate_blocks,
+                      int32_t quantize_layers, int32_t quantize_output, double *loss,
+                      const orc_train_model *grads);
 
 #ifdef __cplusplus
 }
