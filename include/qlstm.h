@@ -121,6 +121,9 @@ typedef struct {
   float *h_inv_q;   /* [T][B]     recovery factor of h_t                      */
   float *h;         /* [T][B][R]  fp32 h_t; honoured by the model and stack
                        forwards (the one-layer entry points return h anyway)  */
+  float *gates;     /* [T][B][4H] i, f, g, o after their activation functions */
+  float *c;         /* [T][B][H]  cell state c_t                              */
+  float *m;         /* [T][B][H]  cell output o tanh(c_t) (before a projection) */
 } ql_lstm_taps;
 
 /* Recurrent state of one layer at a chunk boundary of a stream (Section 4:
@@ -345,6 +348,43 @@ size_t ql_f32_acoustic_model_workspace(const ql_f32_model *M, int64_t T, int64_t
 ql_status ql_f32_acoustic_model_forward(const ql_f32_model *M, const float *feats, int64_t T,
                                         int64_t B, float *post, void *ws, size_t ws_bytes,
                                         void *stream);
+
+/* ---- quantization-aware training step (Section 3.2, Algorithm 1) ---------------
+ * Float master parameters of an acoustic model (device fp32, row-major, the
+ * layouts of ql_f32_layer / ql_f32_model), updated in place by the step. */
+typedef struct {
+  int64_t in, hidden, proj;  /* proj must be 0 (QL_EUNSUPPORTED otherwise)     */
+  float *Wx, *Wh, *Wr, *bias; /* [4H][in], [4H][H], unused, [4H]               */
+} ql_train_layer;
+typedef struct {
+  int32_t nlayers;
+  const ql_train_layer *layers; /* host array of nlayers descriptors            */
+  int64_t states;
+  float *Wy, *by;               /* [states][H_last], [states]                    */
+} ql_train_model;
+/* One training step on a mini-batch feats [T][B][in] (fp32, device) with frame
+ * targets [T][B] (int32 state indices, device), as Algorithm 1 lays it out:
+ *   1. the parameters are quantized (W_x and W_h in gate_blocks row blocks,
+ *      4 = per gate; the output layer's W_y per matrix);
+ *   2. the forward pass runs in quantized form, the inference path of this
+ *      library (ql_acoustic_model_forward, bit for bit), its activations kept;
+ *      quantize_output = 1 quantizes the output layer too ('quant-all'),
+ *      0 keeps it float ('quant', Section 5);
+ *   3. the loss is frame-level cross-entropy of the posteriors, averaged over
+ *      the T*B frames (*loss, device float, nullable);
+ *   4. the backward pass is floating point, with the float parameters,
+ *      evaluated at the quantized forward pass's activations (quantization is
+ *      not differentiated); grads (required; device arrays of the shapes of M)
+ *      receives every gradient;
+ *   5. every weight and bias moves by -lr times its gradient (fp32).
+ * Layers without projection, hidden <= 512.  Zero initial state per
+ * utterance.  Workspace from ql_train_step_workspace. */
+size_t ql_train_step_workspace(const ql_train_model *M, int64_t T, int64_t B,
+                               int32_t gate_blocks);
+ql_status ql_train_step(const ql_train_model *M, const float *feats, const int32_t *targets,
+                        int64_t T, int64_t B, float lr, int32_t gate_blocks,
+                        int32_t quantize_output, float *loss, const ql_train_model *grads,
+                        void *ws, size_t ws_bytes, void *stream);
 
 /* ---- misc -------------------------------------------------------------------- */
 /* Synchronizes `stream`, then reports QL_ETIMEOUT if a persistent kernel of the

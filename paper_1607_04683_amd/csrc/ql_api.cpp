@@ -129,6 +129,9 @@ RecurrentArgs rec_args(const ql_lstm_layer &L, int64_t T, int64_t B, const float
     a.tap_codes = taps->h_codes;
     a.tap_zero = taps->h_zero;
     a.tap_inv_q = taps->h_inv_q;
+    a.tap_gates = taps->gates;
+    a.tap_c = taps->c;
+    a.tap_m = taps->m;
   }
   a.ws = rec;
   return a;
@@ -353,6 +356,9 @@ PStackLayer pstack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBu
     s.acc_h = t->acc_h;
     s.acc_r = t->acc_r;
     s.h = t->h;
+    s.tap_gates = t->gates;
+    s.tap_c = t->c;
+    s.tap_m = t->m;
   }
   s.h0 = st_h(s0, l);
   s.c0 = st_c(s0, l);
@@ -423,6 +429,9 @@ StackLayer stack_layer(const ql_lstm_layer &L, const ActRows &xin, const ActBuf 
     s.acc_x = t->acc_x;
     s.acc_h = t->acc_h;
     s.h = t->h;
+    s.tap_gates = t->gates;
+    s.tap_c = t->c;
+    s.tap_m = t->m;
   }
   s.h0 = st_h(s0, l);
   s.c0 = st_c(s0, l);
@@ -467,7 +476,8 @@ hipError_t quantize_input(const Frontend &f, int64_t T, int64_t B, int64_t in, c
 
 ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_t B, float *post,
                         const ql_lstm_state *s0, const ql_lstm_state *s1,
-                        const ql_model_taps *taps, void *ws, size_t ws_bytes, void *stream) {
+                        const ql_model_taps *taps, void *ws, size_t ws_bytes, void *stream,
+                        bool output_layer = true) {
   if (!M || !M->layers || !M->by) return QL_EINVAL;
   if (M->nlayers <= 0 || T < 0 || B < 0) return QL_ESHAPE;
   if (T * B > 0 && (!fe.x || !post)) return QL_EINVAL;
@@ -477,9 +487,12 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
     const int64_t want_in = l == 0 ? M->layers[0].in : layer_width(M->layers[l - 1]);
     if (M->layers[l].in != want_in) return QL_ESHAPE;
   }
-  ql_status st = check_qmatrix(&M->Wy, true);
-  if (st != QL_OK) return st;
-  if (M->Wy.cols != layer_width(M->layers[M->nlayers - 1])) return QL_ESHAPE;
+  ql_status st = QL_OK;
+  if (output_layer) {
+    st = check_qmatrix(&M->Wy, true);
+    if (st != QL_OK) return st;
+    if (M->Wy.cols != layer_width(M->layers[M->nlayers - 1])) return QL_ESHAPE;
+  }
   if (!ws || ws_bytes < ql_acoustic_model_workspace(M, T, B)) return QL_EWORKSPACE;
   hipStream_t s = as_stream(stream);
   // the timeout flag sits at the start of the workspace in every forward call
@@ -563,6 +576,7 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
     cur = w.hout.rows();
     ++l;
   }
+  if (!output_layer) return QL_OK;
   const int64_t K = layer_width(M->layers[M->nlayers - 1]);
   return from_hip(launch_softmax_layer(cur, weight(M->Wy), MB, M->Wy.rows, K, M->by, post,
                                        taps ? taps->acc_y : nullptr,
@@ -931,6 +945,288 @@ ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stre
   if (fn < 0 || fn > 3) return QL_EINVAL;
   if (n < 0) return QL_ESHAPE;
   return from_hip(launch_gate_fn(fn, x, y, n, as_stream(stream)));
+}
+
+}  // extern "C"
+
+// ------------------------------------------------ quantization-aware training
+namespace {
+
+// Workspace of a training step, carved in a fixed order.  The exchange
+// region at the head serves the forward pass, then the backward pass (its
+// first bytes hold the timeout flag of both).
+struct TrainWs {
+  void *xch;
+  size_t xch_bytes;
+  struct QCopy {
+    int8_t *codes;
+    double *range;
+    int32_t *zero;
+    float *inv_q;
+    int32_t *row_sums;
+  } qx[kMaxStack > 16 ? kMaxStack : 16], qh[16], qy;
+  void *qws;                          // set-quantizer scratch
+  float *gates[16], *c[16], *h[16];   // forward activations per layer
+  float *post;                        // posteriors, then dC/dz
+  float *row_loss;
+  float *dy, *dx, *da;                // dC/dh of the current layer, of its input, dC/da
+  float *part;                        // split-K partial products
+  float *cpart;                       // column-sum partials
+};
+
+constexpr int kMaxTrainLayers = 16;
+
+int64_t train_width_max(const ql_train_model &M, int64_t *maxH, int64_t *maxIn) {
+  int64_t mh = 0, mi = 0;
+  for (int l = 0; l < M.nlayers; ++l) {
+    mh = std::max<int64_t>(mh, M.layers[l].hidden);
+    mi = std::max<int64_t>(mi, M.layers[l].in);
+  }
+  *maxH = mh;
+  *maxIn = mi;
+  return mh;
+}
+
+// K split of a gradient product with an M x N result: enough workgroups for
+// the chip when the result is small and K is long.
+int grad_splits(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  const int64_t by_k = std::max<int64_t>(1, K / 1024);
+  return (int)std::max<int64_t>(1, std::min<int64_t>({512 / std::max<int64_t>(tiles, 1), by_k, 64}));
+}
+
+size_t grad_part_floats(const ql_train_model &M, int64_t T, int64_t B) {
+  const int64_t N = T * B;
+  size_t mx = 0;
+  auto need = [&](int64_t m, int64_t n, int64_t k) {
+    const int sp = grad_splits(m, n, k);
+    if (sp > 1) mx = std::max(mx, (size_t)sp * (size_t)(m * n));
+  };
+  for (int l = 0; l < M.nlayers; ++l) {
+    const int64_t H = M.layers[l].hidden;
+    need(4 * H, M.layers[l].in, N);
+    need(4 * H, H, N > B ? N - B : 0);
+  }
+  need(M.states, M.layers[M.nlayers - 1].hidden, N);
+  return mx;
+}
+
+// A model of the quantized copies in w (descriptor arrays owned by the caller).
+void train_qmodel(const ql_train_model &M, const TrainWs &w, int32_t gb, bool qout,
+                  ql_lstm_layer *layers, ql_model *qm) {
+  for (int l = 0; l < M.nlayers; ++l) {
+    const ql_train_layer &L = M.layers[l];
+    const int64_t H = L.hidden;
+    ql_lstm_layer q{};
+    q.in = L.in;
+    q.hidden = H;
+    q.proj = 0;
+    q.Wx = ql_qmatrix{w.qx[l].codes, 4 * H, L.in, round_up(L.in, 64), gb, w.qx[l].range,
+                      w.qx[l].zero, w.qx[l].inv_q, w.qx[l].row_sums};
+    q.Wh = ql_qmatrix{w.qh[l].codes, 4 * H, H, round_up(H, 64), gb, w.qh[l].range,
+                      w.qh[l].zero, w.qh[l].inv_q, w.qh[l].row_sums};
+    q.bias = L.bias;
+    layers[l] = q;
+  }
+  qm->nlayers = M.nlayers;
+  qm->layers = layers;
+  const int64_t HL = M.layers[M.nlayers - 1].hidden;
+  qm->Wy = qout ? ql_qmatrix{w.qy.codes, M.states, HL, round_up(HL, 64), 1, w.qy.range,
+                             w.qy.zero, w.qy.inv_q, w.qy.row_sums}
+                : ql_qmatrix{nullptr, 0, HL, round_up(HL, 64), 1, nullptr, nullptr, nullptr, nullptr};
+  qm->by = M.by;
+}
+
+TrainWs carve_train(Carve &c, const ql_train_model &M, int64_t T, int64_t B, int32_t gb,
+                    bool qout) {
+  TrainWs w{};
+  const int64_t N = T * B;
+  int64_t maxH = 0, maxIn = 0;
+  train_width_max(M, &maxH, &maxIn);
+  // exchange region: the forward pass's whole workspace, or the backward's
+  // counters, whichever is larger
+  ql_lstm_layer layers[kMaxTrainLayers];
+  ql_model qm{};
+  train_qmodel(M, w, gb, qout, layers, &qm);
+  if (!qout) qm.Wy.rows = 0;
+  w.xch_bytes = std::max(model_ws_bytes(&qm, T, B), bptt_ws(T, B));
+  w.xch = c.take<char>(w.xch_bytes);
+  auto qcopy = [&](TrainWs::QCopy &q, int64_t rows, int64_t cols, int nb) {
+    q.codes = c.take<int8_t>((size_t)(rows * round_up(cols, 64)));
+    q.range = c.take<double>((size_t)nb);
+    q.zero = c.take<int32_t>((size_t)nb);
+    q.inv_q = c.take<float>((size_t)nb);
+    q.row_sums = c.take<int32_t>((size_t)rows);
+  };
+  for (int l = 0; l < M.nlayers; ++l) {
+    const int64_t H = M.layers[l].hidden;
+    qcopy(w.qx[l], 4 * H, M.layers[l].in, gb);
+    qcopy(w.qh[l], 4 * H, H, gb);
+  }
+  const int64_t HL = M.layers[M.nlayers - 1].hidden;
+  if (qout) qcopy(w.qy, M.states, HL, 1);
+  w.qws = c.take<char>(set_quantize_ws(gb));
+  for (int l = 0; l < M.nlayers; ++l) {
+    const int64_t H = M.layers[l].hidden;
+    w.gates[l] = c.take<float>((size_t)(N * 4 * H));
+    w.c[l] = c.take<float>((size_t)(N * H));
+    w.h[l] = c.take<float>((size_t)(N * H));
+  }
+  w.post = c.take<float>((size_t)(N * M.states));
+  w.row_loss = c.take<float>((size_t)std::max<int64_t>(N, 1) + 1);
+  w.dy = c.take<float>((size_t)(N * std::max(maxH, maxIn)));
+  w.dx = c.take<float>((size_t)(N * std::max(maxH, maxIn)));
+  w.da = c.take<float>((size_t)(N * 4 * maxH));
+  w.part = c.take<float>(grad_part_floats(M, T, B));
+  w.cpart = c.take<float>(colsum_ws(std::max<int64_t>(4 * maxH, M.states)) / sizeof(float));
+  return w;
+}
+
+ql_status check_train_model(const ql_train_model *M, int32_t gb, bool need_ptrs) {
+  if (!M || !M->layers || M->nlayers <= 0) return QL_EINVAL;
+  if (M->nlayers > kMaxTrainLayers || M->states <= 0 || gb <= 0) return QL_ESHAPE;
+  if (need_ptrs && (!M->Wy || !M->by)) return QL_EINVAL;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_train_layer &L = M->layers[l];
+    if (L.proj != 0) return QL_EUNSUPPORTED;
+    if (L.in <= 0 || L.hidden <= 0) return QL_ESHAPE;
+    if (L.hidden > 512) return QL_EUNSUPPORTED;
+    if (l > 0 && L.in != M->layers[l - 1].hidden) return QL_ESHAPE;
+    if ((4 * L.hidden) % gb != 0) return QL_ESHAPE;
+    if (L.in > kMaxK || gb > 65535) return QL_EOVERFLOW;
+    if (need_ptrs && (!L.Wx || !L.Wh || !L.bias)) return QL_EINVAL;
+  }
+  return QL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ql_train_step_workspace(const ql_train_model *M, int64_t T, int64_t B,
+                               int32_t gate_blocks) {
+  if (check_train_model(M, gate_blocks, false) != QL_OK || T < 0 || B < 0) return 0;
+  Carve c(nullptr);
+  carve_train(c, *M, T, B, gate_blocks, true);
+  return c.off;
+}
+
+ql_status ql_train_step(const ql_train_model *M, const float *feats, const int32_t *targets,
+                        int64_t T, int64_t B, float lr, int32_t gate_blocks,
+                        int32_t quantize_output, float *loss, const ql_train_model *grads,
+                        void *ws, size_t ws_bytes, void *stream) {
+  ql_status st = check_train_model(M, gate_blocks, true);
+  if (st != QL_OK) return st;
+  if (T < 0 || B < 0) return QL_ESHAPE;
+  if (quantize_output != 0 && quantize_output != 1) return QL_EINVAL;
+  if (!grads || !grads->layers || grads->nlayers != M->nlayers || grads->states != M->states ||
+      !grads->Wy || !grads->by)
+    return QL_EINVAL;
+  for (int l = 0; l < M->nlayers; ++l) {
+    const ql_train_layer &g = grads->layers[l], &L = M->layers[l];
+    if (!g.Wx || !g.Wh || !g.bias) return QL_EINVAL;
+    if (g.in != L.in || g.hidden != L.hidden || g.proj != 0) return QL_ESHAPE;
+  }
+  if (T * B > 0 && (!feats || !targets)) return QL_EINVAL;
+  if (!ws || ws_bytes < ql_train_step_workspace(M, T, B, gate_blocks)) return QL_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  const bool qout = quantize_output == 1;
+  Carve c(ws);
+  TrainWs w = carve_train(c, *M, T, B, gate_blocks, qout);
+  if (reset_recurrent_flag(w.xch, s) != hipSuccess) return QL_EHIP;
+  const int64_t N = T * B, S = M->states, NL = M->nlayers;
+  const int64_t HL = M->layers[NL - 1].hidden;
+
+  // 1. w^q <- quantize(w)
+  for (int l = 0; l < NL; ++l) {
+    const ql_train_layer &L = M->layers[l];
+    const int64_t H = L.hidden;
+    if (launch_set_quantize(L.Wx, L.in, 4 * H, L.in, gate_blocks, w.qx[l].codes,
+                            round_up(L.in, 64), w.qx[l].range, w.qx[l].zero, w.qx[l].inv_q,
+                            w.qx[l].row_sums, nullptr, nullptr, w.qws, s) != hipSuccess ||
+        launch_set_quantize(L.Wh, H, 4 * H, H, gate_blocks, w.qh[l].codes, round_up(H, 64),
+                            w.qh[l].range, w.qh[l].zero, w.qh[l].inv_q, w.qh[l].row_sums,
+                            nullptr, nullptr, w.qws, s) != hipSuccess)
+      return QL_EHIP;
+  }
+  if (qout && launch_set_quantize(M->Wy, HL, S, HL, 1, w.qy.codes, round_up(HL, 64), w.qy.range,
+                                  w.qy.zero, w.qy.inv_q, w.qy.row_sums, nullptr, nullptr, w.qws,
+                                  s) != hipSuccess)
+    return QL_EHIP;
+
+  // 2. the quantized forward pass (the inference path), its activations kept
+  ql_lstm_layer layers[kMaxTrainLayers];
+  ql_model qm{};
+  train_qmodel(*M, w, gate_blocks, qout, layers, &qm);
+  ql_lstm_taps lt[kMaxTrainLayers];
+  for (int l = 0; l < NL; ++l) {
+    lt[l] = ql_lstm_taps{};
+    lt[l].gates = w.gates[l];
+    lt[l].c = w.c[l];
+    lt[l].h = w.h[l];
+  }
+  const ql_model_taps mt{lt, nullptr, nullptr};
+  if (N > 0) {
+    st = model_forward(&qm, Frontend{feats, false, 0, 0, 0}, T, B, w.post, nullptr, nullptr, &mt,
+                       w.xch, w.xch_bytes, stream, qout);
+    if (st != QL_OK) return st;
+    if (!qout) {  // 'quant': float output layer on the quantized layers' h
+      if (launch_sgemm(w.h[NL - 1], HL, M->Wy, HL, N, S, HL, M->by, w.post, S, s) != hipSuccess ||
+          launch_softmax_rows(w.post, N, S, s) != hipSuccess)
+        return QL_EHIP;
+    }
+  }
+
+  // 3. loss and output error; gradients of the output layer; dC/dh of the top layer
+  if (launch_xent_grad(w.post, targets, N, S, w.row_loss, loss, s) != hipSuccess) return QL_EHIP;
+  auto gemm_grad = [&](const float *A, int64_t lda, const float *Bm, int64_t ldb, int64_t m,
+                       int64_t n, int64_t k, float *C) {
+    return launch_sgemm_ex(true, true, A, lda, Bm, ldb, m, n, k, nullptr, C, n,
+                           grad_splits(m, n, k), w.part, s);
+  };
+  if (gemm_grad(w.post, S, w.h[NL - 1], HL, S, HL, N, grads->Wy) != hipSuccess ||
+      launch_colsum(w.post, N, S, grads->by, w.cpart, s) != hipSuccess ||
+      launch_sgemm_ex(false, true, w.post, S, M->Wy, HL, N, HL, S, nullptr, w.dy, HL, 1, nullptr,
+                      s) != hipSuccess)
+    return QL_EHIP;
+
+  // 4. the layers from the top: BPTT, then the gradient products
+  float *dy = w.dy, *dx = w.dx;
+  for (int l = (int)NL - 1; l >= 0; --l) {
+    const ql_train_layer &L = M->layers[l];
+    const ql_train_layer &g = grads->layers[l];
+    const int64_t H = L.hidden, IN = L.in;
+    const float *xin = l == 0 ? feats : w.h[l - 1];
+    BpttArgs ba{T, B, H, L.Wh, dy, w.gates[l], w.c[l], w.da, w.xch};
+    bool unsupported = false;
+    if (launch_bptt(ba, s, &unsupported) != hipSuccess) return QL_EHIP;
+    if (unsupported) return QL_EUNSUPPORTED;
+    if (gemm_grad(w.da, 4 * H, xin, IN, 4 * H, IN, N, g.Wx) != hipSuccess ||
+        gemm_grad(w.da + B * 4 * H, 4 * H, w.h[l], H, 4 * H, H, N > B ? N - B : 0, g.Wh) !=
+            hipSuccess ||
+        launch_colsum(w.da, N, 4 * H, g.bias, w.cpart, s) != hipSuccess)
+      return QL_EHIP;
+    if (l > 0) {
+      if (launch_sgemm_ex(false, true, w.da, 4 * H, L.Wx, IN, N, IN, 4 * H, nullptr, dx, IN, 1,
+                          nullptr, s) != hipSuccess)
+        return QL_EHIP;
+      std::swap(dy, dx);
+    }
+  }
+
+  // 5. w <- w - lr dC/dw
+  for (int l = 0; l < NL; ++l) {
+    const ql_train_layer &L = M->layers[l], &g = grads->layers[l];
+    const int64_t H = L.hidden;
+    if (launch_sgd(L.Wx, g.Wx, 4 * H * L.in, lr, s) != hipSuccess ||
+        launch_sgd(L.Wh, g.Wh, 4 * H * H, lr, s) != hipSuccess ||
+        launch_sgd(L.bias, g.bias, 4 * H, lr, s) != hipSuccess)
+      return QL_EHIP;
+  }
+  if (launch_sgd(M->Wy, grads->Wy, S * HL, lr, s) != hipSuccess ||
+      launch_sgd(M->by, grads->by, S, lr, s) != hipSuccess)
+    return QL_EHIP;
+  return QL_OK;
 }
 
 }  // extern "C"

@@ -23,51 +23,83 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 // ---------------------------------------------------------------------------
-// GEMM  C[m][n] = sum_k A[m][k] B[n][k] (+ bias[n]), A [M][lda], B [N][ldb].
+// GEMM  C[m][n] = sum_k A(m, k) B(n, k) (+ bias[n]).  An operand is stored
+// either row-major [rows][ld] with k contiguous (A(m, k) = A[m*lda + k]) or,
+// transposed (TA / TB), [K][ld] with its rows contiguous (A(m, k) =
+// A[k*lda + m]); the training step's gradient products need both.
 // 128x128 tiles, 2x2 waves of 64x64 (2x2 blocks of 32x32 MFMA), K in steps
 // of 32 floats through two register-staged LDS stages; LDS rows hold 33
-// floats so the column reads of 32 consecutive rows use 32 banks.
+// floats so the column reads of 32 consecutive rows use 32 banks.  A grid
+// with gridDim.y > 1 splits K: split s sums k in [s*klen, (s+1)*klen) into
+// C + s*split_stride (partial sums, no bias), reduced afterwards in split
+// order.
 // ---------------------------------------------------------------------------
 constexpr int kFB = 128, kFK = 32, kFLD = kFK + 1, kFThreads = 256;
 constexpr size_t kFStage = (size_t)2 * kFB * kFLD;  // floats per stage (A and B)
 
-__device__ __forceinline__ void f_load(const float *X, int64_t ld, int64_t nrows, int64_t K,
+// rows r0.., k in [k0, kend): 128 x 32 elements, 4 vectors of 4 per thread
+template <bool TR>
+__device__ __forceinline__ void f_load(const float *X, int64_t ld, int64_t nrows, int64_t kend,
                                        int64_t r0, int64_t k0, bool vec, v4f (&st)[4]) {
-  const int tid = threadIdx.x, kc = tid & 7;
+  const int tid = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t gr = r0 + i * 32 + (tid >> 3), gk = k0 + 4 * kc;
     v4f x = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (gr < nrows) {
-      const float *p = X + gr * ld + gk;
-      if (vec && gk + 3 < K) {
-        x = *reinterpret_cast<const v4f *>(p);
-      } else {
+    if constexpr (!TR) {  // 4 consecutive k of row gr
+      const int64_t gr = r0 + i * 32 + (tid >> 3), gk = k0 + 4 * (tid & 7);
+      if (gr < nrows) {
+        const float *p = X + gr * ld + gk;
+        if (vec && gk + 3 < kend) {
+          x = *reinterpret_cast<const v4f *>(p);
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (gk + e < K) x[e] = p[e];
+          for (int e = 0; e < 4; ++e)
+            if (gk + e < kend) x[e] = p[e];
+        }
+      }
+    } else {  // 4 consecutive rows at one k
+      const int64_t gk = k0 + (tid >> 3), gr = r0 + 4 * ((tid & 7) + 8 * i);
+      if (gk < kend) {
+        const float *p = X + gk * ld + gr;
+        if (vec && gr + 3 < nrows) {
+          x = *reinterpret_cast<const v4f *>(p);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (gr + e < nrows) x[e] = p[e];
+        }
       }
     }
     st[i] = x;
   }
 }
 
+template <bool TR>
 __device__ __forceinline__ void f_store(float *lds, const v4f (&st)[4]) {
-  const int tid = threadIdx.x, kc = tid & 7;
+  const int tid = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) lds[(i * 32 + (tid >> 3)) * kFLD + 4 * kc + e] = st[i][e];
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (!TR)
+        lds[(i * 32 + (tid >> 3)) * kFLD + 4 * (tid & 7) + e] = st[i][e];
+      else
+        lds[(4 * ((tid & 7) + 8 * i) + e) * kFLD + (tid >> 3)] = st[i][e];
+    }
 }
 
+template <bool TA, bool TB>
 __global__ __launch_bounds__(kFThreads) void k_sgemm(const float *__restrict__ A, int64_t lda,
                                                      const float *__restrict__ Bm, int64_t ldb,
                                                      int64_t M, int64_t N, int64_t K,
                                                      const float *__restrict__ bias,
-                                                     float *__restrict__ C, int64_t ldc) {
+                                                     float *__restrict__ C, int64_t ldc,
+                                                     int64_t klen, int64_t split_stride) {
   extern __shared__ __attribute__((aligned(16))) float fsm[];
   const int ntn = (int)((N + kFB - 1) / kFB);
   const int64_t m0 = (int64_t)(blockIdx.x / ntn) * kFB, n0 = (int64_t)(blockIdx.x % ntn) * kFB;
+  const int64_t kbeg = (int64_t)blockIdx.y * klen, kend = std::min<int64_t>(K, kbeg + klen);
+  if (gridDim.y > 1) C += (int64_t)blockIdx.y * split_stride;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave >> 1, wn = wave & 1;
   const bool va = (lda & 3) == 0 && (reinterpret_cast<uintptr_t>(A) & 15) == 0;
   const bool vb = (ldb & 3) == 0 && (reinterpret_cast<uintptr_t>(Bm) & 15) == 0;
@@ -76,20 +108,20 @@ __global__ __launch_bounds__(kFThreads) void k_sgemm(const float *__restrict__ A
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v16f{};
-  const int nk = (int)((K + kFK - 1) / kFK);
+  const int nk = kend > kbeg ? (int)((kend - kbeg + kFK - 1) / kFK) : 0;
   v4f sa[4], sb[4];
   if (nk > 0) {
-    f_load(A, lda, M, K, m0, 0, va, sa);
-    f_load(Bm, ldb, N, K, n0, 0, vb, sb);
-    f_store(fsm, sa);
-    f_store(fsm + kFB * kFLD, sb);
+    f_load<TA>(A, lda, M, kend, m0, kbeg, va, sa);
+    f_load<TB>(Bm, ldb, N, kend, n0, kbeg, vb, sb);
+    f_store<TA>(fsm, sa);
+    f_store<TB>(fsm + kFB * kFLD, sb);
   }
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const bool more = kt + 1 < nk;
     if (more) {
-      f_load(A, lda, M, K, m0, (int64_t)(kt + 1) * kFK, va, sa);
-      f_load(Bm, ldb, N, K, n0, (int64_t)(kt + 1) * kFK, vb, sb);
+      f_load<TA>(A, lda, M, kend, m0, kbeg + (int64_t)(kt + 1) * kFK, va, sa);
+      f_load<TB>(Bm, ldb, N, kend, n0, kbeg + (int64_t)(kt + 1) * kFK, vb, sb);
     }
     const float *as = fsm + (kt & 1) * kFStage, *bs = as + kFB * kFLD;
 #pragma unroll 4
@@ -108,8 +140,8 @@ __global__ __launch_bounds__(kFThreads) void k_sgemm(const float *__restrict__ A
     }
     if (more) {
       float *nb = fsm + ((kt + 1) & 1) * kFStage;
-      f_store(nb, sa);
-      f_store(nb + kFB * kFLD, sb);
+      f_store<TA>(nb, sa);
+      f_store<TB>(nb + kFB * kFLD, sb);
     }
     __syncthreads();
   }
@@ -120,7 +152,7 @@ __global__ __launch_bounds__(kFThreads) void k_sgemm(const float *__restrict__ A
     for (int j = 0; j < 2; ++j) {
       const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
       if (n >= N) continue;
-      const float bn = bias ? bias[n] : 0.0f;
+      const float bn = bias && gridDim.y == 1 ? bias[n] : 0.0f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t m = m0 + wm * 64 + i * 32 + ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3);
@@ -129,22 +161,65 @@ __global__ __launch_bounds__(kFThreads) void k_sgemm(const float *__restrict__ A
     }
 }
 
+// C[m][n] = sum_s part[s][m][n] over the splits in order (+ bias[n]).
+__global__ void k_sum_splits(const float *part, int splits, int64_t M, int64_t N,
+                             const float *bias, float *C, int64_t ldc) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M * N) return;
+  const int64_t m = i / N, n = i % N;
+  float v = part[i];
+  for (int sp = 1; sp < splits; ++sp) v += part[(int64_t)sp * M * N + i];
+  C[m * ldc + n] = bias ? v + bias[n] : v;
+}
+
+template <bool TA, bool TB>
+static hipError_t sgemm_set_attr() {
+  static bool attr_set = false;
+  if (attr_set) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_sgemm<TA, TB>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)(2 * kFStage * sizeof(float)));
+  if (e == hipSuccess) attr_set = true;
+  return e;
+}
+
+hipError_t launch_sgemm_ex(bool ta, bool tb, const float *A, int64_t lda, const float *B,
+                           int64_t ldb, int64_t M, int64_t N, int64_t K, const float *bias,
+                           float *C, int64_t ldc, int splits, float *part, hipStream_t s) {
+  if (M == 0 || N == 0) return hipSuccess;
+  const size_t lds = 2 * kFStage * sizeof(float);
+  hipError_t e = ta ? (tb ? sgemm_set_attr<true, true>() : sgemm_set_attr<true, false>())
+                    : (tb ? sgemm_set_attr<false, true>() : sgemm_set_attr<false, false>());
+  if (e != hipSuccess) return e;
+  const int64_t tiles = ((M + kFB - 1) / kFB) * ((N + kFB - 1) / kFB);
+  if (splits < 1 || !part) splits = 1;
+  const int64_t klen = splits > 1 ? round_up((K + splits - 1) / splits, kFK) : std::max<int64_t>(K, 1);
+  if (splits > 1) splits = (int)((K + klen - 1) / klen);
+  float *out = splits > 1 ? part : C;
+  const int64_t ldo = splits > 1 ? N : ldc;
+  const dim3 grid((unsigned)tiles, (unsigned)splits);
+  const float *biasp = splits > 1 ? nullptr : bias;
+  const int64_t stride = M * N;
+#define QL_SGEMM(TA_, TB_)                                                                    \
+  hipLaunchKernelGGL((k_sgemm<TA_, TB_>), grid, dim3(kFThreads), lds, s, A, lda, B, ldb, M, N, \
+                     K, biasp, out, ldo, klen, stride)
+  if (ta && tb) QL_SGEMM(true, true);
+  else if (ta) QL_SGEMM(true, false);
+  else if (tb) QL_SGEMM(false, true);
+  else QL_SGEMM(false, false);
+#undef QL_SGEMM
+  e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t n = M * N;
+  hipLaunchKernelGGL(k_sum_splits, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     (const float *)part, splits, M, N, bias, C, ldc);
+  return hipGetLastError();
+}
+
 hipError_t launch_sgemm(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M,
                         int64_t N, int64_t K, const float *bias, float *C, int64_t ldc,
                         hipStream_t s) {
-  if (M == 0 || N == 0) return hipSuccess;
-  const size_t lds = 2 * kFStage * sizeof(float);
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_sgemm),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t tiles = ((M + kFB - 1) / kFB) * ((N + kFB - 1) / kFB);
-  hipLaunchKernelGGL(k_sgemm, dim3((unsigned)tiles), dim3(kFThreads), lds, s, A, lda, B, ldb, M, N,
-                     K, bias, C, ldc);
-  return hipGetLastError();
+  return launch_sgemm_ex(false, false, A, lda, B, ldb, M, N, K, bias, C, ldc, 1, nullptr, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -84,6 +84,9 @@ struct RecurrentArgs {
   int8_t *tap_codes;         // [T][B][R] (ld = R)
   int32_t *tap_zero;         // [T][B]
   float *tap_inv_q;          // [T][B]
+  float *tap_gates;          // [T][B][4H] activated gates i, f, g, o
+  float *tap_c;              // [T][B][H] cell state
+  float *tap_m;              // [T][B][H] cell output o tanh(c)
   // scratch
   void *ws;
 };
@@ -119,6 +122,8 @@ struct StackLayer {
   int32_t *tap_zero;
   float *tap_inv_q;
   int32_t *acc_x, *acc_h;  // optional taps: [T][B][4H] raw input / recurrent sums
+  float *tap_gates;        // optional taps: [T][B][4H] activated gates, [T][B][H] c and
+  float *tap_c, *tap_m;    // m (= h without a projection)
   const float *h0, *c0;    // [B][H] initial state (nullable = zeros)
   float *hT, *cT;          // [B][H] final state (nullable)
 };
@@ -142,6 +147,8 @@ struct PStackLayer {
   float *tap_inv_q;
   int32_t *acc_x, *acc_h;  // optional taps: [T][4H] raw input / recurrent sums
   int32_t *acc_r;          // optional tap: [T][P] raw projection sums
+  float *tap_gates;        // optional taps: [T][4H] activated gates, [T][H] c and m
+  float *tap_c, *tap_m;
   const float *h0, *c0;    // [P], [H] initial state (nullable = zeros)
   float *hT, *cT;          // [P], [H] final state (nullable)
 };
@@ -165,6 +172,12 @@ int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0,
 hipError_t launch_sgemm(const float *A, int64_t lda, const float *B, int64_t ldb, int64_t M,
                         int64_t N, int64_t K, const float *bias, float *C, int64_t ldc,
                         hipStream_t s);
+// The same with either operand transposed: A(m, k) = A[k*lda + m] when ta,
+// B(n, k) = B[k*ldb + n] when tb.  splits > 1 (with part: splits*M*N floats)
+// splits K over more workgroups and sums the partial products in order.
+hipError_t launch_sgemm_ex(bool ta, bool tb, const float *A, int64_t lda, const float *B,
+                           int64_t ldb, int64_t M, int64_t N, int64_t K, const float *bias,
+                           float *C, int64_t ldc, int splits, float *part, hipStream_t s);
 // In-place softmax of each of `rows` rows of S floats.
 hipError_t launch_softmax_rows(float *x, int64_t rows, int64_t S, hipStream_t s);
 struct F32RecArgs {
@@ -179,5 +192,29 @@ struct F32RecArgs {
 };
 size_t recurrent_f32_ws(int64_t B, int64_t H, int64_t P);
 hipError_t launch_recurrent_f32(const F32RecArgs &a, hipStream_t s, bool *unsupported);
+
+// ---- quantization-aware training step (ql_train.hip)
+// Cross-entropy of the posteriors post [N][S] against targets [N]: dC/dz =
+// (p - onehot) / N written over post, -log p[target] per row into row_loss,
+// their mean into *loss (nullable).
+hipError_t launch_xent_grad(float *post, const int32_t *targets, int64_t N, int64_t S,
+                            float *row_loss, float *loss, hipStream_t s);
+// out[n] = sum_m X[m][n] (fixed order); part: colsum_ws(N) bytes.
+size_t colsum_ws(int64_t N);
+hipError_t launch_colsum(const float *X, int64_t M, int64_t N, float *out, float *part,
+                         hipStream_t s);
+// w <- w - lr g
+hipError_t launch_sgd(float *w, const float *g, int64_t n, float lr, hipStream_t s);
+// Backpropagation through time of one layer without projection: da [T][B][4H]
+// = dC/d(gate pre-activations) from dy [T][B][H] = dC/dh (from above) and the
+// forward pass's gates [T][B][4H] and c [T][B][H], with W_h [4H][H] fp32.
+struct BpttArgs {
+  int64_t T, B, H;
+  const float *Wh, *dy, *gates, *c;
+  float *da;
+  void *ws;  // bptt_ws bytes; timeout flag cleared by the caller
+};
+size_t bptt_ws(int64_t T, int64_t B);
+hipError_t launch_bptt(const BpttArgs &a, hipStream_t s, bool *unsupported);
 
 }  // namespace ql

@@ -240,10 +240,13 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
       const float act = gt == 2 ? 2.0f * sg - 1.0f : sg;
       const float ig = quad_bcast<0>(act), fg = quad_bcast<1>(act);
       const float gv = quad_bcast<2>(act), og = quad_bcast<3>(act);
+      if (Ly.tap_gates && jj < nu) Ly.tap_gates[(t * 4 + gt) * H + j0 + jj] = act;
       if (gt == 0 && jj < nu) {
         const float cn = (fg * cst[jj]) + (ig * gv);
         cst[jj] = cn;
         const float m = og * tanh_cw(cn);
+        if (Ly.tap_c) Ly.tap_c[t * H + j0 + jj] = cn;
+        if (Ly.tap_m) Ly.tap_m[t * H + j0 + jj] = m;
         if (tl.xcd) publish_local(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
         else publish(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
         if (Ly.cT && t == T - 1) Ly.cT[j0 + jj] = cn;

@@ -444,6 +444,12 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
         const float cn = (fg * cst[lb * tl.u + jj]) + (ig * gv);
         cst[lb * tl.u + jj] = cn;
         const float m = og * tanh_cw(cn);
+        if (a.tap_gates) {
+          float *gp = a.tap_gates + (t * B + b) * 4 * H + j;
+          gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
+        }
+        if (a.tap_c) a.tap_c[(t * B + b) * H + j] = cn;
+        if (a.tap_m) a.tap_m[(t * B + b) * H + j] = m;
         if (NVB == 0) {
           if (CNT)
             st_coherent(&xhf[hcur + b * R + j], m);

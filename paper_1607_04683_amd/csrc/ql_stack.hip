@@ -327,6 +327,12 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         else publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
       }
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
+      if (Ly.tap_gates) {
+        float *gp = Ly.tap_gates + (t * B + b) * 4 * H + j;
+        gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
+      }
+      if (Ly.tap_c) Ly.tap_c[(t * B + b) * H + j] = cn;
+      if (Ly.tap_m) Ly.tap_m[(t * B + b) * H + j] = m;
       if (t == T - 1) {
         if (Ly.hT) Ly.hT[b * H + j] = m;
         if (Ly.cT) Ly.cT[b * H + j] = cn;
@@ -442,6 +448,12 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       for (int c2 = 0; c2 < tl.reph; ++c2)
         publish(&xht[c2 * tl.strideh + hcur + p.poff], (uint32_t)(t + 1), m);
       if (Ly.h) Ly.h[t * B * H + p.poff] = m;
+      if (Ly.tap_gates) {
+        float *gp = Ly.tap_gates + (t * B + b0 + p.lb) * 4 * H + j0 + p.jj;
+        gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
+      }
+      if (Ly.tap_c) Ly.tap_c[t * B * H + p.poff] = cn;
+      if (Ly.tap_m) Ly.tap_m[t * B * H + p.poff] = m;
       if (t == T - 1) {
         if (Ly.hT) Ly.hT[p.poff] = m;
         if (Ly.cT) Ly.cT[p.poff] = cn;

@@ -35,7 +35,7 @@ EXPORTS = [
     "ql_lstm_stack_forward", "ql_lstm_stack_layers_per_launch", "ql_stacked_input_count",
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
     "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
-    "ql_acoustic_model_forward_stream_noalloc",
+    "ql_acoustic_model_forward_stream_noalloc", "ql_train_step_workspace", "ql_train_step",
 ]
 
 
@@ -64,7 +64,7 @@ class CModel(C.Structure):
 class CTaps(C.Structure):
     _fields_ = [("acc_x", C.c_void_p), ("acc_h", C.c_void_p), ("acc_r", C.c_void_p),
                 ("h_codes", C.c_void_p), ("h_zero", C.c_void_p), ("h_inv_q", C.c_void_p),
-                ("h", C.c_void_p)]
+                ("h", C.c_void_p), ("gates", C.c_void_p), ("c", C.c_void_p), ("m", C.c_void_p)]
 
 
 class CState(C.Structure):
@@ -84,6 +84,16 @@ class CF32Layer(C.Structure):
 
 class CF32Model(C.Structure):
     _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(CF32Layer)), ("states", C.c_int64),
+                ("Wy", C.c_void_p), ("by", C.c_void_p)]
+
+
+class CTrainLayer(C.Structure):
+    _fields_ = [("in_", C.c_int64), ("hidden", C.c_int64), ("proj", C.c_int64),
+                ("Wx", C.c_void_p), ("Wh", C.c_void_p), ("Wr", C.c_void_p), ("bias", C.c_void_p)]
+
+
+class CTrainModel(C.Structure):
+    _fields_ = [("nlayers", C.c_int32), ("layers", C.POINTER(CTrainLayer)), ("states", C.c_int64),
                 ("Wy", C.c_void_p), ("by", C.c_void_p)]
 
 
@@ -139,6 +149,10 @@ def load(path: str = LIB_PATH):
     L.ql_acoustic_model_forward_stream.argtypes = [C.POINTER(CModel), vp, i64, i64,
                                                    C.POINTER(CState), C.POINTER(CState), vp,
                                                    C.POINTER(CModelTaps), vp, sz, vp]
+    L.ql_train_step_workspace.argtypes = [C.POINTER(CTrainModel), i64, i64, i32]
+    L.ql_train_step_workspace.restype = sz
+    L.ql_train_step.argtypes = [C.POINTER(CTrainModel), vp, vp, i64, i64, C.c_float, i32, i32,
+                                vp, C.POINTER(CTrainModel), vp, sz, vp]
     L.ql_acoustic_model_forward_stream_noalloc.argtypes = [C.POINTER(CModel), vp, i64, i64,
                                                            C.POINTER(CState), C.POINTER(CState),
                                                            vp, vp, vp]
@@ -165,7 +179,7 @@ def load(path: str = LIB_PATH):
               "ql_f32_acoustic_model_forward", "ql_quantize_activations",
               "ql_lstm_stack_forward", "ql_quantize_stacked_frames",
               "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
-              "ql_acoustic_model_forward_stream_noalloc"):
+              "ql_acoustic_model_forward_stream_noalloc", "ql_train_step"):
         getattr(L, f).restype = i32
     _lib = L
     return L
@@ -355,7 +369,7 @@ def quantize_model(weights: dict, device="cuda", gate_blocks: int = 4, proj_bloc
                  torch.as_tensor(weights["by"], dtype=torch.float32).to(device).contiguous())
 
 
-TAP_NAMES = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q", "h")
+TAP_NAMES = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q", "h", "gates", "c", "m")
 
 
 def _taps(T, B, L: Layer, device, which=True, layer_h=True):
@@ -370,7 +384,9 @@ def _taps(T, B, L: Layer, device, which=True, layer_h=True):
              acc_h=z("acc_h", T, B, 4 * H, dt=torch.int32),
              acc_r=z("acc_r", T, B, P, dt=torch.int32) if P else None,
              h_codes=z("h_codes", T, B, R, dt=torch.int8), h_zero=z("h_zero", T, B, dt=torch.int32),
-             h_inv_q=z("h_inv_q", T, B, dt=torch.float32), h=z("h", T, B, R, dt=torch.float32))
+             h_inv_q=z("h_inv_q", T, B, dt=torch.float32), h=z("h", T, B, R, dt=torch.float32),
+             gates=z("gates", T, B, 4 * H, dt=torch.float32), c=z("c", T, B, H, dt=torch.float32),
+             m=z("m", T, B, H, dt=torch.float32))
     c = CTaps(*[None if t[k] is None else t[k].data_ptr() for k in TAP_NAMES])
     if not layer_h:
         del t["h"]  # the caller's own h output keeps its name
@@ -743,3 +759,45 @@ def stack_layers_per_launch(M: Model, T: int, B: int) -> int:
     forward then runs one layer per launch)."""
     arr = (CLayer * len(M.layers))(*[L.cstruct() for L in M.layers])
     return int(load().ql_lstm_stack_layers_per_launch(arr, len(M.layers), T, B))
+
+
+# ------------------------------------------- quantization-aware training step
+def train_params(weights: dict, device="cuda") -> dict:
+    """Device fp32 copies of a model's float parameters (layers without
+    projection): {'layers': [{'Wx','Wh','b'}], 'Wy', 'by'}."""
+    t = lambda a: torch.as_tensor(a, dtype=torch.float32).to(device).contiguous().clone()
+    return {"layers": [{k: t(L[k]) for k in ("Wx", "Wh", "b")} for L in weights["layers"]],
+            "Wy": t(weights["Wy"]), "by": t(weights["by"])}
+
+
+def _train_struct(P: dict):
+    arr = (CTrainLayer * len(P["layers"]))(*[
+        CTrainLayer(L["Wx"].shape[1], L["Wx"].shape[0] // 4, 0, _ptr(L["Wx"]), _ptr(L["Wh"]),
+                    None, _ptr(L["b"])) for L in P["layers"]])
+    return CTrainModel(len(P["layers"]), arr, P["Wy"].shape[0], _ptr(P["Wy"]), _ptr(P["by"])), arr
+
+
+def train_step(P: dict, feats: torch.Tensor, targets: torch.Tensor, lr: float,
+               gate_blocks: int = 4, quantize_output: bool = True, grads: dict | None = None,
+               workspace: Workspace | None = None, check: bool = True):
+    """One quantization-aware SGD step (ql_train_step) on device parameters P
+    (updated in place) -> (loss tensor [1], grads dict of P's shapes)."""
+    feats = feats.contiguous()
+    targets = targets.to(torch.int32).contiguous()
+    T, B, _ = feats.shape
+    dev = feats.device
+    lib = load()
+    if grads is None:
+        grads = {"layers": [{k: torch.empty_like(v) for k, v in L.items()} for L in P["layers"]],
+                 "Wy": torch.empty_like(P["Wy"]), "by": torch.empty_like(P["by"])}
+    cm, keep1 = _train_struct(P)
+    cg, keep2 = _train_struct(grads)
+    ws = (workspace or Workspace()).get(lib.ql_train_step_workspace(C.byref(cm), T, B,
+                                                                    gate_blocks), dev)
+    loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    _check(lib.ql_train_step(C.byref(cm), _ptr(feats), _ptr(targets), T, B, float(lr), gate_blocks,
+                             int(bool(quantize_output)), _ptr(loss), C.byref(cg), _ptr(ws),
+                             ws.numel(), _stream()), "ql_train_step")
+    if check:
+        _check(lib.ql_workspace_status(_ptr(ws), _stream()), "ql_train_step")
+    return loss, grads

@@ -2,15 +2,16 @@
 oracle's (helpers for the GPU parity tests; no test of its own).
 
 Codes, zero points, recovery factors and int32 accumulators are compared bit
-for bit; the fp32 h_t of every layer too (every float operation on the
-recurrent chain is elementwise and reproduced exactly); logits bit for bit
+for bit; the fp32 h_t, gates, c_t and cell output of every layer too (every
+float operation on the recurrent chain is elementwise and reproduced
+exactly); logits bit for bit
 (the softmax layer's recovery is elementwise as well); posteriors within
 1e-4 absolute (the GPU's softmax sums in a different order)."""
 import numpy as np
 import torch
 
 TOL = 1e-4
-LAYER_TAPS = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q", "h")
+LAYER_TAPS = ("acc_x", "acc_h", "acc_r", "h_codes", "h_zero", "h_inv_q", "h", "gates", "c", "m")
 
 
 def rows_of(t, utts):
