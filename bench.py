@@ -28,6 +28,7 @@ if ROOT not in sys.path:
 METRIC = "quantized LSTM AM frames/sec at batch 1 and 64; int8 GEMM TOPS vs MFMA peak"
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
+FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 
 # HBM bytes per launch of the dominant kernel (the wavefront launch over the
 # first layers of the 5x500 model at batch 64, T = 1000), from two rocprofv3
@@ -65,7 +66,8 @@ def parse():
                     help="frames of the batch-64 workload the CPU oracle is timed on")
     ap.add_argument("--profile-target", default=None,
                     choices=["stack_b64", "stack_b1", "recurrence_b64", "recurrence_b1",
-                             "gemm8192", "lstmp_b256", "pstack_b1", "table1", "copy"],
+                             "gemm8192", "lstmp_b256", "lstmp_rec", "pstack_b1", "table1",
+                             "qat_b64", "copy"],
                     help="run only one piece (for hardware-counter passes) and exit")
     return ap.parse_args()
 
@@ -242,8 +244,78 @@ def stack_kernel(ql, torch, M, x, n, reps):
            + n * rows * (H + 12)               # codes + params written by every layer
            + (n - 1) * rows * (H + 12))        # read again by the next layer
     avg = sum(ms) / len(ms)
-    return dict(avg_ms=avg, min_ms=min(ms), alg_bytes=alg, layers=n,
+    ops = 2 * T * B * w_step                   # every 8-bit multiply-accumulate, both products
+    return dict(avg_ms=avg, min_ms=min(ms), alg_bytes=alg, layers=n, int8_ops=ops,
                 us_per_frame=avg * 1e3 / T, weight_bytes_per_frame=w_step)
+
+
+def lstmp_recurrence_kernel(ql, torch, M, x, reps):
+    """One persistent-recurrence launch of the LSTMP model's second layer (its
+    real pre-activations): per-step time against the bandwidth floor of
+    streaming W_h' and W_r' (decode-style) and the int8 MFMA peak."""
+    T, B, _ = x.shape
+    L1, L2 = M.layers[0], M.layers[1]
+    h1 = ql.lstm_layer_forward(L1, x)["h"]
+    gx, _ = ql.quantized_matmul(L2.Wx, h1.reshape(T * B, -1), ql.QL_ACT_PER_ROW, L2.bias)
+    gx = gx.reshape(T, B, -1)
+    del h1
+    ws = ql.Workspace()
+    out = {"h": torch.empty(T, B, L2.width, dtype=torch.float32, device="cuda")}
+    ql.lstm_recurrence(L2, gx, workspace=ws, out=out, check=False)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        with Timer(torch) as tm:
+            ql.lstm_recurrence(L2, gx, workspace=ws, out=out, check=False)
+        ms.append(tm.ms)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "lstmp recurrence")
+    H, P = L2.hidden, L2.proj
+    w_bytes = 4 * H * P + P * H                # W_h' and W_r' codes per step
+    ops = 2 * B * (4 * H * P + P * H)          # per step
+    avg = sum(ms) / len(ms)
+    us = avg * 1e3 / T
+    return dict(kernel="k_recurrent (LSTMP 2048/512 layer 2, B=256, T=800)",
+                avg_ms=round(avg, 3), us_per_step=round(us, 2),
+                weight_bytes_per_step=w_bytes,
+                weight_frac_of_hbm=round(w_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 5),
+                int8_ops_per_step=ops,
+                mfma_frac=round(ops / (us * 1e-6) / 1e12 / INT8_PEAK_TOPS, 5))
+
+
+def qat_step(ql, torch, W, steps, warmup):
+    """The quantization-aware training step (Section 3.2, Algorithm 1) on the
+    5 x 500 + 8192 model: a mini-batch of B utterances x T frames with
+    synthetic frame targets; parameters updated in place every step."""
+    from paper_1607_04683_amd import workloads as wl
+    w, _ = wl.model_weights(W)
+    P = ql.train_params(w)
+    x = torch.from_numpy(wl.features(W)).cuda()
+    y = torch.from_numpy(wl.frame_targets(W)).cuda()
+    ws = ql.Workspace()
+    g = None
+    for _ in range(warmup):
+        _, g = ql.train_step(P, x, y, 0.1, grads=g, workspace=ws, check=False)
+    torch.cuda.synchronize()
+    with Timer(torch) as tm:
+        for _ in range(steps):
+            loss, g = ql.train_step(P, x, y, 0.1, grads=g, workspace=ws, check=False)
+    ql._check(ql.load().ql_workspace_status(ql._ptr(ws.buf), ql._stream()), "train steps")
+    ms = tm.ms / steps
+    T, B = W.T, W.B
+    N = T * B
+    m = W.model
+    # fp32 flops of the gradient products (2 per multiply-add): the output
+    # layer's dW_y and dh_L, every layer's dW_x, dW_h and (but the first) dx
+    fl = 2 * N * m.states * m.hidden * 2
+    for l, (i, h, _) in enumerate(m.layer_dims()):
+        fl += 2 * N * 4 * h * i + 2 * N * 4 * h * h + (2 * N * 4 * h * i if l > 0 else 0)
+    return dict(workload=W.name + ", quantization-aware SGD step, synthetic frame targets",
+                ms_per_step=round(ms, 3), frames_per_s=round(N / (ms * 1e-3), 1),
+                loss=round(float(loss.item()), 4),
+                grad_product_tflop=round(fl / 1e12, 3),
+                grad_product_tflops_over_step=round(fl / (ms * 1e-3) / 1e12, 2),
+                note="the step's whole time against the fp32 flops of its gradient products "
+                     "(a lower bound on their MFMA rate; fp32 peak 157.3 TF/s)")
 
 
 def gemm_sweep(ql, torch, n, reps):
@@ -264,6 +336,64 @@ def gemm_sweep(ql, torch, n, reps):
     return dict(n=n, ms=ms, tops=tops, frac_of_peak=tops / INT8_PEAK_TOPS)
 
 
+def _cpu_name():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baselines_all(threads):
+    """The oracle on every workload (bounded samples), with `threads` OpenMP
+    threads and, for the three smallest, one thread as well."""
+    import numpy as np
+
+    from oracle import oracle
+    from paper_1607_04683_amd import workloads as wl
+    oracle.lib()
+    out = []
+
+    def run(name, fn, unit, scale, sample, nthreads):
+        oracle.set_threads(nthreads)
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        out.append(dict(workload=name, value=round(scale / dt, 2), unit=unit, cores=nthreads,
+                        kind="oracle", sample=f"{sample}, {dt:.2f} s"))
+
+    W0 = wl.QMATMUL_16x128x256
+    Wm, Xm = wl.qmatmul_operands(W0)
+    q = oracle.quantize(Wm, 1)
+    reps = 2000
+    for n in (threads, 1):
+        run(W0.name, lambda: [oracle.quantized_matmul(q, Xm, act_gran=0) for _ in range(reps)],
+            "qmatmul/s", reps, f"{reps} calls", n)
+    for W, Tcap1 in ((wl.LSTM1x500_T300_B1, 300), (wl.LSTM5x500_S8192_T500_B1, 100)):
+        w, _ = wl.model_weights(W)
+        x = wl.features(W)
+        x1 = np.ascontiguousarray(x[:Tcap1])
+        if W.model.states:
+            Mq = oracle.quantize_model(w)
+            f = lambda xx, Mq=Mq: oracle.acoustic_model_forward(Mq, xx)
+        else:
+            Lq = oracle.quantize_layer(w["layers"][0])
+            f = lambda xx, Lq=Lq: oracle.lstm_layer_forward(Lq, xx)
+        run(W.name, lambda: f(x), "frames/s", x.shape[0], f"{x.shape[0]} frames", threads)
+        run(W.name, lambda: f(x1), "frames/s", x1.shape[0], f"first {x1.shape[0]} frames", 1)
+    W5 = wl.LSTMP4x2048P512_S16384_T800_B256
+    w5, _ = wl.model_weights(W5)
+    Mq5 = oracle.quantize_model(w5)
+    nu, T5 = 32, 50
+    x5 = np.ascontiguousarray(wl.features(W5, utterances=list(range(nu)))[:T5])
+    run(W5.name, lambda: oracle.acoustic_model_forward(Mq5, x5), "frames/s", nu * T5,
+        f"{nu} utterances x {T5} frames", threads)
+    oracle.set_threads(threads)
+    return out
+
+
 def cpu_baseline(workload, frames):
     """The oracle (untuned) on a bounded sample of the same workload: the first
     `frames` frames of the first utterances (utterances are independent)."""
@@ -282,14 +412,7 @@ def cpu_baseline(workload, frames):
     oracle.acoustic_model_forward(Mq, np.ascontiguousarray(x))
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
-    cpu = "unknown"
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
+    cpu = _cpu_name()
     return dict(value=T * n_utt / dt, unit="frames/s", cores=cores, kind="oracle",
                 sample=f"{n_utt} utterances x {T} frames of the batch-64 workload "
                        f"({T * n_utt} frames, {dt:.1f} s, {cpu})")
@@ -328,6 +451,12 @@ def profile_target(ql, torch, target, reps):
         _, M, x = model_on_device(ql, W, torch)
         ms, _ = time_model(ql, torch, M, x, 2, 1)
         out = dict(workload=W.name, ms_per_step=round(ms, 3))
+    elif target == "lstmp_rec":
+        W = wl.LSTMP4x2048P512_S16384_T800_B256
+        _, M, x = model_on_device(ql, W, torch)
+        out = lstmp_recurrence_kernel(ql, torch, M, x, reps)
+    elif target == "qat_b64":
+        out = qat_step(ql, torch, wl.LSTM5x500_S8192_T1000_B64, 2, 1)
     else:  # a plain device copy of 1 GiB: calibrates the byte counters
         n = 1 << 28
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -375,7 +504,10 @@ def main():
                     achieved=round(achieved, 2), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 5), traffic=measured_traffic(),
                     traffic_unit="bytes per launch", traffic_source=TRAFFIC["summary"],
-                    avg_launch_ms=round(rec["avg_ms"], 4), alg_bytes=rec["alg_bytes"])
+                    avg_launch_ms=round(rec["avg_ms"], 4), alg_bytes=rec["alg_bytes"],
+                    int8_ops=rec["int8_ops"],
+                    mfma_frac=round(rec["int8_ops"] / (rec["avg_ms"] * 1e-3) / 1e12 /
+                                    INT8_PEAK_TOPS, 5))
 
     extra = {}
     if not args.quick:
@@ -425,13 +557,19 @@ def main():
         _, M5, x5 = model_on_device(ql, W5, torch)
         ms5, _ = time_model(ql, torch, M5, x5, 3, 1)
         extra["lstmp_b256"] = dict(workload=W5.name, ms_per_step=round(ms5, 3),
-                                   frames_per_s=round(W5.T * W5.B / (ms5 * 1e-3), 1))
+                                   frames_per_s=round(W5.T * W5.B / (ms5 * 1e-3), 1),
+                                   recurrence=lstmp_recurrence_kernel(ql, torch, M5, x5, 3))
         log(f"LSTMP batch 256: {extra['lstmp_b256']}")
         del M5, x5
+        torch.cuda.empty_cache()
+        extra["qat_b64"] = qat_step(ql, torch, W64, 3, 1)
+        log(f"quantization-aware training step: {extra['qat_b64']}")
         torch.cuda.empty_cache()
         extra["gemm_sweep"] = [gemm_sweep(ql, torch, n, reps=10) for n in wl.GEMM_SWEEP]
         for g in extra["gemm_sweep"]:
             g.update({k: round(v, 4) for k, v in g.items() if isinstance(v, float)})
+            g["note"] = ("row sums of the code operands computed on the host before timing "
+                         "(an O(n^2) pass outside the timed region)")
         log(f"GEMM sweep: {extra['gemm_sweep']}")
 
     cpu = None
@@ -440,6 +578,9 @@ def main():
         cpu = cpu_baseline(W64, args.cpu_frames)
         cpu["value"] = round(cpu["value"], 2)
         log(f"cpu baseline: {cpu}")
+        if not args.quick:
+            extra["cpu_baselines"] = cpu_baselines_all(cpu["cores"])
+            log(f"cpu baselines: {extra['cpu_baselines']}")
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "frames/s", "n_gpus": 1,

@@ -122,6 +122,16 @@ def _declare(L):
         getattr(L, f).restype = i32
 
 
+def set_threads(n: int) -> None:
+    """OpenMP threads the oracle runs on (omp_set_num_threads of its runtime)."""
+    lib().omp_set_num_threads(int(n))
+
+
+def threads() -> int:
+    lib().omp_get_max_threads.restype = C.c_int
+    return int(lib().omp_get_max_threads())
+
+
 def _p(a):
     return None if a is None else a.ctypes.data
 

@@ -63,6 +63,9 @@ __device__ __forceinline__ ColParam col_param(const WeightMat &W, int64_t n, int
   return c;
 }
 
+// TP: the launch writes sums, gate or cell taps or a final state (the variant
+// without them carries none of their per-step code).
+template <bool TP>
 __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_abort;
@@ -220,7 +223,7 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
     products_mfma(hc, ldsP, 16, wh, ldsP, nrows, nrows, ldP, Sh, nrows);
     products_mfma(xc, ldsX, 16, wx, ldsX, nrows, nrows, ldX, Sx, nrows);
     __syncthreads();
-    if (Ly.acc_x || Ly.acc_h)  // sums of step t (row 0 of S) to the taps [T][4H], 0..255 domain
+    if (TP && (Ly.acc_x || Ly.acc_h))  // sums of step t (row 0 of S) to the taps [T][4H], 0..255 domain
       for (int n = tid; n < nrows; n += blockDim.x) {
         const int gt = n / u, jj = n % u;
         if (jj >= nu) continue;
@@ -240,16 +243,18 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
       const float act = gt == 2 ? 2.0f * sg - 1.0f : sg;
       const float ig = quad_bcast<0>(act), fg = quad_bcast<1>(act);
       const float gv = quad_bcast<2>(act), og = quad_bcast<3>(act);
-      if (Ly.tap_gates && jj < nu) Ly.tap_gates[(t * 4 + gt) * H + j0 + jj] = act;
+      if (TP && Ly.tap_gates && jj < nu) Ly.tap_gates[(t * 4 + gt) * H + j0 + jj] = act;
       if (gt == 0 && jj < nu) {
         const float cn = (fg * cst[jj]) + (ig * gv);
         cst[jj] = cn;
         const float m = og * tanh_cw(cn);
-        if (Ly.tap_c) Ly.tap_c[t * H + j0 + jj] = cn;
-        if (Ly.tap_m) Ly.tap_m[t * H + j0 + jj] = m;
         if (tl.xcd) publish_local(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
         else publish(&mw[t * H + j0 + jj], (uint32_t)(t + 1), m);
-        if (Ly.cT && t == T - 1) Ly.cT[j0 + jj] = cn;
+        if constexpr (TP) {
+          if (Ly.tap_c) Ly.tap_c[t * H + j0 + jj] = cn;
+          if (Ly.tap_m) Ly.tap_m[t * H + j0 + jj] = m;
+          if (Ly.cT && t == T - 1) Ly.cT[j0 + jj] = cn;
+        }
       }
     }
     // the output codes of h_{t-1} (in hc) leave while m_t travels
@@ -271,8 +276,10 @@ __global__ __launch_bounds__(kPThreads) void k_pstack(PStackArgs a, PStackTiling
       if (tl.xcd) publish_local(&hown[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       publish(&hw[t * P + p0 + tid], (uint32_t)(t + 1), hv);
       if (Ly.h) Ly.h[t * P + p0 + tid] = hv;
-      if (Ly.acc_r) Ly.acc_r[t * P + p0 + tid] = acc_u8(Sr[tid], cr.sigw, rm.sigx, H);
-      if (Ly.hT && t == T - 1) Ly.hT[p0 + tid] = hv;
+      if constexpr (TP) {
+        if (Ly.acc_r) Ly.acc_r[t * P + p0 + tid] = acc_u8(Sr[tid], cr.sigw, rm.sigx, H);
+        if (Ly.hT && t == T - 1) Ly.hT[p0 + tid] = hv;
+      }
     }
     // the next step's first phase writes only hc, xc, rp[0], rp[1]: none of
     // them is read after the last barrier
@@ -376,11 +383,17 @@ hipError_t launch_pstack(const PStackArgs &a, hipStream_t s, bool *unsupported) 
     *unsupported = true;
     return hipSuccess;
   }
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_pstack),
+  bool tp = false;  // any tap or final state asked for
+  for (int l = 0; l < a.nl; ++l) {
+    const PStackLayer &L = a.L[l];
+    tp = tp || L.acc_x || L.acc_h || L.acc_r || L.tap_gates || L.tap_c || L.tap_m || L.hT || L.cT;
+  }
+  auto kern = tp ? k_pstack<true> : k_pstack<false>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)tl.lds_bytes);
   if (e != hipSuccess) return e;
   int per_cu = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_pstack, kPThreads, tl.lds_bytes);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kPThreads, tl.lds_bytes);
   if (e != hipSuccess) return e;
   if (per_cu * cus < tl.grid) {
     *unsupported = true;
@@ -393,7 +406,7 @@ hipError_t launch_pstack(const PStackArgs &a, hipStream_t s, bool *unsupported) 
   if (e != hipSuccess) return e;
   PStackArgs args = a;
   void *kargs[] = {&args, &tl};
-  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(k_pstack), dim3(tl.grid),
+  return hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(tl.grid),
                                     dim3(kPThreads), kargs, (unsigned)tl.lds_bytes, s);
 }
 

@@ -67,7 +67,9 @@ struct StackTiling {
 
 
 // RBA: rows one wave quantizes together (2 for batched tiles, 1 at one row).
-template <int NVA, bool MFA, int RBA>
+// TP: the launch writes sums, gate or cell taps or a final state (the
+// variant without them carries none of their per-step code).
+template <int NVA, bool MFA, int RBA, bool TP>
 __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTiling tl) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int8_t *wh = reinterpret_cast<int8_t *>(smem + tl.off_wh);
@@ -284,7 +286,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
   // the long pole and the extra pass would delay the next step.)
   auto x_preact = [&](int64_t t, int nr) {
     __syncthreads();  // Sx complete
-    if (Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);  // each lane reads its own sums first
+    if (TP && Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);  // each lane reads its own sums first
     for (int idx = tid; idx < nr * nrows; idx += blockDim.x) {
       const int lb = idx / nrows, n = idx % nrows;
       const RowParam rx = rpx[lb];
@@ -327,15 +329,17 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
         else publish(&xht[c2 * tl.strideh + hcur + b * H + j], (uint32_t)(t + 1), m);
       }
       if (Ly.h) Ly.h[(t * B + b) * H + j] = m;
-      if (Ly.tap_gates) {
-        float *gp = Ly.tap_gates + (t * B + b) * 4 * H + j;
-        gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
-      }
-      if (Ly.tap_c) Ly.tap_c[(t * B + b) * H + j] = cn;
-      if (Ly.tap_m) Ly.tap_m[(t * B + b) * H + j] = m;
-      if (t == T - 1) {
-        if (Ly.hT) Ly.hT[b * H + j] = m;
-        if (Ly.cT) Ly.cT[b * H + j] = cn;
+      if constexpr (TP) {
+        if (Ly.tap_gates) {
+          float *gp = Ly.tap_gates + (t * B + b) * 4 * H + j;
+          gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
+        }
+        if (Ly.tap_c) Ly.tap_c[(t * B + b) * H + j] = cn;
+        if (Ly.tap_m) Ly.tap_m[(t * B + b) * H + j] = m;
+        if (t == T - 1) {
+          if (Ly.hT) Ly.hT[b * H + j] = m;
+          if (Ly.cT) Ly.cT[b * H + j] = cn;
+        }
       }
     };
     const int full = pairs / nt, rem = pairs % nt;
@@ -448,15 +452,17 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       for (int c2 = 0; c2 < tl.reph; ++c2)
         publish(&xht[c2 * tl.strideh + hcur + p.poff], (uint32_t)(t + 1), m);
       if (Ly.h) Ly.h[t * B * H + p.poff] = m;
-      if (Ly.tap_gates) {
-        float *gp = Ly.tap_gates + (t * B + b0 + p.lb) * 4 * H + j0 + p.jj;
-        gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
-      }
-      if (Ly.tap_c) Ly.tap_c[t * B * H + p.poff] = cn;
-      if (Ly.tap_m) Ly.tap_m[t * B * H + p.poff] = m;
-      if (t == T - 1) {
-        if (Ly.hT) Ly.hT[p.poff] = m;
-        if (Ly.cT) Ly.cT[p.poff] = cn;
+      if constexpr (TP) {
+        if (Ly.tap_gates) {
+          float *gp = Ly.tap_gates + (t * B + b0 + p.lb) * 4 * H + j0 + p.jj;
+          gp[0] = ig, gp[H] = fg, gp[2 * H] = gv, gp[3 * H] = og;
+        }
+        if (Ly.tap_c) Ly.tap_c[t * B * H + p.poff] = cn;
+        if (Ly.tap_m) Ly.tap_m[t * B * H + p.poff] = m;
+        if (t == T - 1) {
+          if (Ly.hT) Ly.hT[p.poff] = m;
+          if (Ly.cT) Ly.cT[p.poff] = cn;
+        }
       }
     };
     auto row_fast = [](const RowParam &rh) { return (uint32_t)(rh.ztx + 127) <= 255u; };
@@ -558,7 +564,7 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       // ---- 3. the recurrent product against the resident W_h' slice
       products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
       __syncthreads();
-      if (Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
+      if (TP && Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
 
       // ---- 4. recover, gates, cell; publish h_t
       gates_b(t, hcur);
@@ -765,8 +771,8 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     // ---- 1. the recurrent product (the input side's is already in Sx)
     products_mfma(xh, tl.ldsX, 16, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
     __syncthreads();
-    if (Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);
-    if (Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
+    if (TP && Ly.acc_x) tap_acc(Ly.acc_x, Sx, cpx, rpx, IN, t);
+    if (TP && Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
 
     // ---- 2. recover, gates, cell; publish h_t
     gates(t, hcur);
@@ -942,7 +948,13 @@ hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported) {
     *unsupported = true;
     return hipSuccess;
   }
-  StackKernel kern = tl.bB == 1 ? k_stack<8, false, 1> : k_stack<8, true, 2>;
+  bool tp = false;  // any tap or final state asked for
+  for (int l = 0; l < a.nl; ++l) {
+    const StackLayer &L = a.L[l];
+    tp = tp || L.acc_x || L.acc_h || L.tap_gates || L.tap_c || L.tap_m || L.hT || L.cT;
+  }
+  StackKernel kern = tl.bB == 1 ? (tp ? k_stack<8, false, 1, true> : k_stack<8, false, 1, false>)
+                                : (tp ? k_stack<8, true, 2, true> : k_stack<8, true, 2, false>);
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)tl.lds_bytes);
   if (e != hipSuccess) return e;

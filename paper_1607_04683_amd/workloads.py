@@ -186,6 +186,15 @@ def features(w: Workload, utterances=None) -> np.ndarray:
     return stacked_features(rng, w.T, w.B, m.frame_dim, m.stack, m.skip, utterances)
 
 
+def frame_targets(w: Workload, seed: int = 1) -> np.ndarray:
+    """Synthetic frame-level state targets [T][B] (int32, uniform over the
+    output states) for a training mini-batch of workload w: the paper's
+    alignments need its transcribed data, and a training step's work does not
+    depend on the label values."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.integers(0, w.model.states, size=(w.T, w.B)).astype(np.int32)
+
+
 def qmatmul_operands(w: Workload = QMATMUL_16x128x256):
     """(W [rows][cols], X [m][cols]) fp32: W ~ N(0, 0.1), X ~ U[-1, 1]."""
     e = w.extra
