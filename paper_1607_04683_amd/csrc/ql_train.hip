@@ -117,28 +117,37 @@ hipError_t launch_sgd(float *w, const float *g, int64_t n, float lr, hipStream_t
 //   dc_t   = dh_t o (1 - tanh^2 c_t) + f_{t+1} dc_{t+1}
 //   da_t   = (dc_t g i (1 - i), dc_t c_{t-1} f (1 - f), dc_t i (1 - g^2),
 //             dh_t tanh(c_t) o (1 - o))            (dC/d pre-activation)
-// A tile owns (bB batch rows) x (u cells): the 4u rows of W_h^T it needs
-// (columns j of W_h) stay in LDS for the launch.  Per step it waits until
-// every tile of its batch slice has published da_{t+1} (device-coherent
-// stores, then an arrival on the slice's counter of that step), stages those
-// rows' da_{t+1} through LDS in chunks, forms W_h^T da_{t+1} for its cells
-// (each (row, cell) pair's sum split over several lanes, the partial sums
-// added in a fixed order), runs the cell's backward step and publishes its
-// part of da_t.  Counters are per step, so nothing is reused in a launch.
+// A tile owns (bB <= 16 batch rows) x (u <= 16 cells).  Per step it waits
+// until every tile of its batch slice has published da_{t+1} (device-coherent
+// stores, then an arrival on the slice's counter of that step) and forms
+// W_h^T da_{t+1} for its (row, cell) pairs on fp32 MFMA (one 16 x 16 block,
+// K = 4H split over the eight waves, 256 k each): the W_h columns of its
+// cells stay in LDS for the launch (transposed, one padded row of k per
+// cell), and the da values go from memory straight into registers, lane
+// (row r, group q) reading 16 consecutive k of row r per 64-k block and the
+// same 16 k of its cell's W_h column from LDS; an MFMA then sums
+// k = base + 16 q + j over q for one j, so A and B take the same order of k.  The waves' partial blocks are
+// added in wave order (the result does not depend on timing); then the
+// cell's backward step and its part of da_t.  Counters are per step, so
+// nothing is reused in a launch.
 // ---------------------------------------------------------------------------
 constexpr int kBpttThreads = 512;
+constexpr int kBpttWaves = kBpttThreads / 64;
+constexpr int kBpttKBlocks = 4;  // 64-k blocks per wave: 8 x 4 x 64 = 2048 >= 4H
+
+constexpr int kBpttLdw = kBpttWaves * kBpttKBlocks * 64 + 4;  // padded row of W_h^T (floats)
 
 struct BpttTiling {
-  int bB, u, nbt, nut, grid, chunk, ns;  // ns lanes per (row, cell) pair
-  int ldw, ldc;                          // LDS row strides (floats) of W_h^T and the da chunk
-  size_t off_w, off_d, off_p, off_dc, lds_bytes;
+  int bB, u, nbt, nut, grid;
+  size_t off_w, off_p, off_dc, lds_bytes;
 };
+
+typedef float v4f_t __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl) {
   extern __shared__ __attribute__((aligned(16))) float bsm[];
-  float *wT = bsm + tl.off_w / 4;    // [u][ldw]: W_h[n][j0 + jj] at wT[jj * ldw + n]
-  float *dS = bsm + tl.off_d / 4;    // [bB][ldc]: staged da_{t+1} chunk
-  float *part = bsm + tl.off_p / 4;  // [ns][bB * u]
+  float *wT = bsm + tl.off_w / 4;    // [16 cells][kBpttLdw]: W_h[k][j0 + c] at wT[c * ldw + k]
+  float *part = bsm + tl.off_p / 4;  // [waves][16 rows][16 cells] partial blocks
   float *dcn = bsm + tl.off_dc / 4;  // [bB * u]: dC/dc carried to the step before
   __shared__ int s_abort;
   const int tid = threadIdx.x;
@@ -152,55 +161,81 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
   const int nb = (int)std::min<int64_t>(tl.bB, B - b0);
   const int nu = (int)std::min<int64_t>(tl.u, H - j0);
   const int npr = tl.bB * tl.u;  // pair p = lb * u + jj
+  const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
 
-  for (int idx = tid; idx < tl.u * G4; idx += blockDim.x) {
-    const int jj = idx / (int)G4;
-    const int64_t n = idx % G4;
-    wT[jj * tl.ldw + n] = jj < nu ? a.Wh[n * H + j0 + jj] : 0.0f;
+  // k of element j of block kb of this lane (rows / cells fr, group fq)
+  auto kof = [&](int kb, int j) {
+    return (int64_t)wave * (64 * kBpttKBlocks) + kb * 64 + fq * 16 + j;
+  };
+  // the W_h column block of the tile's cells, transposed into LDS (zeros past
+  // the cells and past 4H)
+  for (int idx = tid; idx < 16 * kBpttWaves * kBpttKBlocks * 64; idx += blockDim.x) {
+    const int c = idx / (kBpttWaves * kBpttKBlocks * 64);
+    const int64_t k = idx % (kBpttWaves * kBpttKBlocks * 64);
+    wT[c * kBpttLdw + k] = c < nu && k < G4 ? a.Wh[k * H + j0 + c] : 0.0f;
   }
-  for (int p = tid; p < npr; p += blockDim.x) dcn[p] = 0.0f;
+  for (int q = tid; q < npr; q += blockDim.x) dcn[q] = 0.0f;
   if (tid == 0) s_abort = 0;
   __syncthreads();
 
-  const int p = tid % npr, q = tid / npr;  // this lane: pair p, share q of each chunk
-  const bool dot_lane = q < tl.ns;
-  const int lb = p / tl.u, jj = p % tl.u;
+  const int lb = tid / tl.u, jj = tid % tl.u;  // cell lanes: pair (row lb, cell jj)
+  const bool cell_lane = tid < npr && lb < nb && jj < nu;
+  // this lane's cell operands of a step (the forward pass's gates, c_t,
+  // c_{t-1} and dC/dh from above): loaded a step ahead, while the stores of
+  // the current step complete
+  float ig = 0.0f, fg = 0.0f, gg = 0.0f, og = 0.0f, ct = 0.0f, cp = 0.0f, dyv = 0.0f;
+  auto load_cell = [&](int64_t t) {
+    if (!cell_lane || t < 0) return;
+    const int64_t row = t * B + b0 + lb, j = j0 + jj;
+    const float *gt = a.gates + row * G4;
+    ig = gt[j], fg = gt[H + j], gg = gt[2 * H + j], og = gt[3 * H + j];
+    ct = a.c[row * H + j];
+    cp = t > 0 ? a.c[(row - B) * H + j] : 0.0f;
+    dyv = a.dy[row * H + j];
+  };
+  load_cell(T - 1);
   for (int64_t t = T - 1; t >= 0; --t) {
     // ---- W_h^T da_{t+1} for this tile's (row, cell) pairs
-    float acc = 0.0f;
+    v4f_t acc = v4f_t{0.0f, 0.0f, 0.0f, 0.0f};
     if (t + 1 < T) {
       if (!wait_count(counter(t + 1, tb), (unsigned)tl.nut, flag)) s_abort = 1;
       __syncthreads();
       if (s_abort) return;
-      const float *src = a.da + ((t + 1) * B + b0) * G4;
-      for (int64_t c0 = 0; c0 < G4; c0 += tl.chunk) {
-        const int cl = (int)std::min<int64_t>(tl.chunk, G4 - c0);
-        for (int idx = tid; idx < nb * cl; idx += blockDim.x) {
-          const int r = idx / cl, nn = idx % cl;
-          dS[r * tl.ldc + nn] = ld_coherent(src + r * G4 + c0 + nn);
+      // 16 consecutive k of row fr per block, as 8-byte words, all in flight
+      const float *src = a.da + ((t + 1) * B + b0 + fr) * G4;
+      uint64_t dv[kBpttKBlocks][8];
+#pragma unroll
+      for (int kb = 0; kb < kBpttKBlocks; ++kb)
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const int64_t k = kof(kb, 2 * w);
+          dv[kb][w] = fr < nb && k < G4
+                          ? ld_coherent64(reinterpret_cast<const uint64_t *>(src + k))
+                          : 0;
         }
-        __syncthreads();
-        if (dot_lane && lb < nb) {
-          const float *w = wT + jj * tl.ldw + c0;
-          const float *d = dS + lb * tl.ldc;
-          for (int nn = q; nn < cl; nn += tl.ns) acc += w[nn] * d[nn];
+#pragma unroll
+      for (int kb = 0; kb < kBpttKBlocks; ++kb) {
+        const v4f_t *wr = reinterpret_cast<const v4f_t *>(wT + fr * kBpttLdw + kof(kb, 0));
+        const v4f_t w4[4] = {wr[0], wr[1], wr[2], wr[3]};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const uint32_t bits = (uint32_t)(dv[kb][j / 2] >> (32 * (j & 1)));
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bits), w4[j / 4][j % 4], acc,
+                                                     0, 0, 0);
         }
-        __syncthreads();
       }
     }
-    if (dot_lane) part[q * npr + p] = acc;
+    // partial blocks to LDS: part[wave][row][cell]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[(wave * 16 + 4 * fq + i) * 16 + fr] = acc[i];
     __syncthreads();
 
     // ---- the cell's backward step and da_t
-    if (tid < npr && lb < nb && jj < nu) {
+    if (cell_lane) {
       float dhrec = 0.0f;
-      for (int k = 0; k < tl.ns; ++k) dhrec += part[k * npr + tid];
+      for (int w = 0; w < kBpttWaves; ++w) dhrec += part[(w * 16 + lb) * 16 + jj];
       const int64_t row = t * B + b0 + lb, j = j0 + jj;
-      const float *gt = a.gates + row * G4;
-      const float ig = gt[j], fg = gt[H + j], gg = gt[2 * H + j], og = gt[3 * H + j];
-      const float ct = a.c[row * H + j];
-      const float cp = t > 0 ? a.c[(row - B) * H + j] : 0.0f;
-      const float dh = a.dy[row * H + j] + dhrec;
+      const float dh = dyv + dhrec;
       const float tc = tanh_cw(ct);
       const float d_o = dh * tc;
       const float d_c = dh * og * (1.0f - tc * tc) + dcn[tid];
@@ -212,39 +247,33 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
       st_coherent(dst + 2 * H, d_g * (1.0f - gg * gg));
       st_coherent(dst + 3 * H, d_o * og * (1.0f - og));
     }
+    load_cell(t - 1);
     if (t > 0) arrive(counter(t, tb));  // (no tile waits on step 0's arrivals)
+    else __syncthreads();               // part is rewritten only by a next launch
   }
 }
 
 static bool plan_bptt(const BpttArgs &a, int cus, int lds_max, BpttTiling *out) {
   BpttTiling tl{};
-  const int64_t G4 = 4 * a.H;
+  // K = 4H in registers: eight waves of four 64-k blocks
+  if (4 * a.H > (int64_t)kBpttWaves * kBpttKBlocks * 64) return false;
   tl.bB = (int)std::min<int64_t>(a.B, 16);
   tl.nbt = (int)((a.B + tl.bB - 1) / tl.bB);
-  if (tl.nbt > cus) return false;
-  tl.ldw = (int)G4 + 1;
-  // W_h^T rows in LDS: at most 96 KB of them
-  const int umax = (int)std::min<int64_t>(kBpttThreads / tl.bB, (96 * 1024) / (4 * tl.ldw));
-  if (umax < 1) return false;
-  const int nut0 = std::max(1, cus / tl.nbt);
-  tl.u = (int)std::min<int64_t>(umax, std::max<int64_t>(1, (a.H + nut0 - 1) / nut0));
+  // 16 cells per tile (one MFMA column block): every tile of a slice reads all
+  // of the slice's da_{t+1}, so fewer, wider tiles move fewer bytes a step
+  tl.u = (int)std::min<int64_t>(16, a.H);
   tl.nut = (int)((a.H + tl.u - 1) / tl.u);
   tl.grid = tl.nbt * tl.nut;
   if (tl.grid > cus) return false;
-  const int npr = tl.bB * tl.u;
-  tl.ns = std::max(1, kBpttThreads / npr);
-  tl.chunk = (int)std::min<int64_t>(G4, std::max<int64_t>(64, (16 * 1024) / tl.bB));
-  tl.ldc = tl.chunk + 1;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 16);
     return o;
   };
-  tl.off_w = take((size_t)tl.u * tl.ldw * 4);
-  tl.off_d = take((size_t)tl.bB * tl.ldc * 4);
-  tl.off_p = take((size_t)tl.ns * npr * 4);
-  tl.off_dc = take((size_t)npr * 4);
+  tl.off_w = take((size_t)16 * kBpttLdw * 4);
+  tl.off_p = take((size_t)kBpttWaves * 256 * 4);
+  tl.off_dc = take((size_t)tl.bB * tl.u * 4);
   tl.lds_bytes = off;
   if ((int64_t)tl.lds_bytes + 64 > lds_max) return false;
   *out = tl;
