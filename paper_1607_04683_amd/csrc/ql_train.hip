@@ -130,6 +130,12 @@ hipError_t launch_sgd(float *w, const float *g, int64_t n, float lr, hipStream_t
 // added in wave order (the result does not depend on timing); then the
 // cell's backward step and its part of da_t.  Counters are per step, so
 // nothing is reused in a launch.
+// On the whole chip (8 XCDs of 32 CUs) with at most 8 batch slices of at most
+// 32 tiles, every CU gets a workgroup, which reads its XCC_ID and takes the
+// next free slot of its XCD: tile `slot` of slice `XCC_ID`.  A slice's tiles
+// then share one L2 for the da_{t+1} they all read.  da_t still goes out with
+// device-coherent stores: the gradient products launched after this kernel
+// read it from every XCD.
 // ---------------------------------------------------------------------------
 constexpr int kBpttThreads = 512;
 constexpr int kBpttWaves = kBpttThreads / 64;
@@ -137,8 +143,11 @@ constexpr int kBpttKBlocks = 4;  // 64-k blocks per wave: 8 x 4 x 64 = 2048 >= 4
 
 constexpr int kBpttLdw = kBpttWaves * kBpttKBlocks * 64 + 4;  // padded row of W_h^T (floats)
 
+constexpr int kBpttXcds = 8, kBpttXcdCus = 32;
+constexpr int kBpttSlotBytes = kBpttXcds * 64;  // per-XCD slot counters after the header
+
 struct BpttTiling {
-  int bB, u, nbt, nut, grid;
+  int bB, u, nbt, nut, grid, xcd;
   size_t off_w, off_p, off_dc, lds_bytes;
 };
 
@@ -153,10 +162,28 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
   const int tid = threadIdx.x;
   const int64_t T = a.T, B = a.B, H = a.H, G4 = 4 * a.H;
   int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
-  unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+  unsigned *cnt0 = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes +
+                                                kBpttSlotBytes);
   auto counter = [&](int64_t t, int tb) { return cnt0 + (t * tl.nbt + tb) * 16; };
 
-  const int tb = blockIdx.x / tl.nut, tu = blockIdx.x % tl.nut;
+  int blk = (int)blockIdx.x;
+  if (tl.xcd) {
+    __shared__ int s_role;
+    if (tid == 0) {
+      const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
+      s_role = -1;
+      if (xcc < tl.nbt) {
+        const unsigned k = __hip_atomic_fetch_add(slots + xcc * 16, 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        if (k < (unsigned)tl.nut) s_role = xcc * tl.nut + (int)k;
+      }
+    }
+    __syncthreads();
+    if (s_role < 0) return;
+    blk = s_role;
+  }
+  const int tb = blk / tl.nut, tu = blk % tl.nut;
   const int64_t b0 = (int64_t)tb * tl.bB, j0 = (int64_t)tu * tl.u;
   const int nb = (int)std::min<int64_t>(tl.bB, B - b0);
   const int nu = (int)std::min<int64_t>(tl.u, H - j0);
@@ -242,10 +269,12 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
       const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cp;
       dcn[tid] = d_c * fg;
       float *dst = a.da + row * G4 + j;
-      st_coherent(dst, d_i * ig * (1.0f - ig));
-      st_coherent(dst + H, d_f * fg * (1.0f - fg));
-      st_coherent(dst + 2 * H, d_g * (1.0f - gg * gg));
-      st_coherent(dst + 3 * H, d_o * og * (1.0f - og));
+      const float v0 = d_i * ig * (1.0f - ig), v1 = d_f * fg * (1.0f - fg);
+      const float v2 = d_g * (1.0f - gg * gg), v3 = d_o * og * (1.0f - og);
+      st_coherent(dst, v0);
+      st_coherent(dst + H, v1);
+      st_coherent(dst + 2 * H, v2);
+      st_coherent(dst + 3 * H, v3);
     }
     load_cell(t - 1);
     if (t > 0) arrive(counter(t, tb));  // (no tile waits on step 0's arrivals)
@@ -257,13 +286,23 @@ static bool plan_bptt(const BpttArgs &a, int cus, int lds_max, BpttTiling *out) 
   BpttTiling tl{};
   // K = 4H in registers: eight waves of four 64-k blocks
   if (4 * a.H > (int64_t)kBpttWaves * kBpttKBlocks * 64) return false;
-  tl.bB = (int)std::min<int64_t>(a.B, 16);
-  tl.nbt = (int)((a.B + tl.bB - 1) / tl.bB);
   // 16 cells per tile (one MFMA column block): every tile of a slice reads all
   // of the slice's da_{t+1}, so fewer, wider tiles move fewer bytes a step
   tl.u = (int)std::min<int64_t>(16, a.H);
   tl.nut = (int)((a.H + tl.u - 1) / tl.u);
-  tl.grid = tl.nbt * tl.nut;
+  // a slice per XCD when the chip is whole and a slice's tiles fit one XCD
+  // (the batch spread over all eight), else slices of 16 rows
+  tl.xcd = 0;
+  if (cus == kBpttXcds * kBpttXcdCus && tl.nut <= kBpttXcdCus) {
+    tl.bB = (int)std::min<int64_t>(16, (a.B + kBpttXcds - 1) / kBpttXcds);
+    tl.nbt = (int)((a.B + tl.bB - 1) / tl.bB);
+    tl.xcd = tl.nbt <= kBpttXcds;
+  }
+  if (!tl.xcd) {
+    tl.bB = (int)std::min<int64_t>(a.B, 16);
+    tl.nbt = (int)((a.B + tl.bB - 1) / tl.bB);
+  }
+  tl.grid = tl.xcd ? cus : tl.nbt * tl.nut;
   if (tl.grid > cus) return false;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -281,8 +320,10 @@ static bool plan_bptt(const BpttArgs &a, int cus, int lds_max, BpttTiling *out) 
 }
 
 size_t bptt_ws(int64_t T, int64_t B) {
-  // per-step, per-slice arrival counters (64 bytes each) after the header
-  return kHeaderBytes + (size_t)std::max<int64_t>(T, 1) * (size_t)((B + 15) / 16) * 64;
+  // per-XCD slot counters, then per-step, per-slice arrival counters (64
+  // bytes each; at most max(8, B / 16 rounded up) slices) after the header
+  const int64_t slices = std::max<int64_t>(8, (B + 15) / 16);
+  return kHeaderBytes + kBpttSlotBytes + (size_t)std::max<int64_t>(T, 1) * (size_t)slices * 64;
 }
 
 hipError_t launch_bptt(const BpttArgs &a, hipStream_t s, bool *unsupported) {
