@@ -213,7 +213,7 @@ ql_status ql_quantize_activations(const float *X, int64_t m, int64_t cols, const
  * ld a multiple of 64), and h_last [T][B][R] fp32 of the last layer (nullable).
  * state_in / state_out (host arrays of n descriptors, or NULL): each layer's
  * initial state (NULL or null pointers: zeros) and final state; in and out
- * must not overlap.  taps: host array of n, or NULL.  QL_EUNSUPPORTED when the
+ * must not overlap (QL_EINVAL).  taps: host array of n, or NULL.  QL_EUNSUPPORTED when the
  * n layers do not fit one launch (or projection layers at B > 1).  Same
  * results, bit for bit, as n calls of the one-layer path. */
 size_t ql_lstm_stack_workspace(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B);
@@ -254,7 +254,7 @@ ql_status ql_acoustic_model_forward(const ql_model *M, const float *feats, int64
 /* The same for one chunk of a stream (Section 4: a live utterance evaluated
  * as its frames arrive): state_in / state_out are host arrays of nlayers
  * per-layer states (either NULL: zeros in / nothing out); they must not
- * overlap.  Calls chained through state_out -> state_in give, bit for bit,
+ * overlap (QL_EINVAL).  Calls chained through state_out -> state_in give, bit for bit,
  * the posteriors of one call over the whole utterance.  Workspace as
  * ql_acoustic_model_workspace. */
 ql_status ql_acoustic_model_forward_stream(const ql_model *M, const float *feats, int64_t T,
@@ -377,8 +377,12 @@ typedef struct {
  *      not differentiated); grads (required; device arrays of the shapes of M)
  *      receives every gradient;
  *   5. every weight and bias moves by -lr times its gradient (fp32).
- * Layers without projection, hidden <= 512.  Zero initial state per
- * utterance.  Workspace from ql_train_step_workspace. */
+ * Layers without projection, hidden <= 512 (QL_EUNSUPPORTED otherwise).  Zero
+ * initial state per utterance.  Workspace from ql_train_step_workspace (0 for
+ * an invalid model).  QL_EINVAL: a null pointer (feats / targets may be null
+ * when T*B = 0), quantize_output not 0 or 1, lr not finite, grads not of the
+ * model's layer count and states; QL_ESHAPE: widths that do not chain, 4H not
+ * a multiple of gate_blocks, grads of other shapes, T or B < 0. */
 size_t ql_train_step_workspace(const ql_train_model *M, int64_t T, int64_t B,
                                int32_t gate_blocks);
 ql_status ql_train_step(const ql_train_model *M, const float *feats, const int32_t *targets,

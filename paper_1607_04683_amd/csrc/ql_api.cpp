@@ -4,6 +4,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+#include <cstring>
+
 #include "ql_launch.h"
 
 using namespace ql;
@@ -69,6 +72,44 @@ ActBuf take_act(Carve &c, int64_t m, int64_t cols) {
 }
 
 int64_t layer_width(const ql_lstm_layer &L) { return L.proj ? L.proj : L.hidden; }
+
+// The int a C caller passed for an enum argument.  C lets an enum carry any
+// int; in C++ only its enumerators' range is a valid value, so the argument
+// is read through its bytes, never as the enum.
+template <class E>
+int enum_arg(const E &e) {
+  static_assert(sizeof(E) == sizeof(int), "C enums are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+
+// True when a buffer of the initial states (per layer h [B][R], c [B][H])
+// shares a byte with a buffer of the final states: the kernels read the one
+// and write the other within a launch.
+bool states_overlap(const ql_lstm_layer *layers, int n, int64_t B, const ql_lstm_state *in,
+                    const ql_lstm_state *out) {
+  if (!in || !out || B <= 0) return false;
+  auto span = [&](const ql_lstm_state &st, int l, bool cell, uintptr_t *lo, uintptr_t *hi) {
+    const float *p = cell ? st.c : st.h;
+    if (!p) return false;
+    const int64_t w = cell ? layers[l].hidden : layer_width(layers[l]);
+    *lo = reinterpret_cast<uintptr_t>(p);
+    *hi = *lo + static_cast<uintptr_t>(B * w) * sizeof(float);
+    return true;
+  };
+  for (int a = 0; a < n; ++a)
+    for (int ca = 0; ca < 2; ++ca) {
+      uintptr_t alo, ahi;
+      if (!span(in[a], a, ca == 1, &alo, &ahi)) continue;
+      for (int b = 0; b < n; ++b)
+        for (int cb = 0; cb < 2; ++cb) {
+          uintptr_t blo, bhi;
+          if (span(out[b], b, cb == 1, &blo, &bhi) && alo < bhi && blo < ahi) return true;
+        }
+    }
+  return false;
+}
 
 ql_status check_layer(const ql_lstm_layer *L) {
   if (!L || !L->bias) return QL_EINVAL;
@@ -157,7 +198,7 @@ ql_status run_layer(const ql_lstm_layer &L, const ActRows &xin, int64_t T, int64
 extern "C" {
 
 const char *ql_status_str(ql_status s) {
-  switch (s) {
+  switch (enum_arg(s)) {
     case QL_OK: return "ok";
     case QL_EINVAL: return "invalid argument";
     case QL_ESHAPE: return "inconsistent shapes";
@@ -215,7 +256,8 @@ ql_status ql_quantized_matmul(const ql_qmatrix *W, const float *X, int64_t m, ql
   ql_status st = check_qmatrix(W, true);
   if (st != QL_OK) return st;
   if (m > 0 && (!X || !Y)) return QL_EINVAL;
-  if (gran != QL_ACT_PER_TENSOR && gran != QL_ACT_PER_ROW) return QL_EINVAL;
+  const int g = enum_arg(gran);
+  if (g != QL_ACT_PER_TENSOR && g != QL_ACT_PER_ROW) return QL_EINVAL;
   if (m < 0) return QL_ESHAPE;
   if (!ws || ws_bytes < ql_quantized_matmul_workspace(m, W->rows, W->cols)) return QL_EWORKSPACE;
   hipStream_t s = as_stream(stream);
@@ -223,7 +265,7 @@ ql_status ql_quantized_matmul(const ql_qmatrix *W, const float *X, int64_t m, ql
   ActBuf x = take_act(c, m, W->cols);
   void *qws = c.take<char>(set_quantize_ws(1));
   hipError_t e;
-  if (gran == QL_ACT_PER_ROW)
+  if (g == QL_ACT_PER_ROW)
     e = launch_quantize_rows(X, W->cols, m, W->cols, x.codes, x.ld, x.zero, x.inv_q, x.sums, s);
   else
     e = launch_set_quantize(X, W->cols, m, W->cols, 1, x.codes, x.ld, nullptr, nullptr, nullptr,
@@ -487,6 +529,7 @@ ql_status model_forward(const ql_model *M, const Frontend &fe, int64_t T, int64_
     const int64_t want_in = l == 0 ? M->layers[0].in : layer_width(M->layers[l - 1]);
     if (M->layers[l].in != want_in) return QL_ESHAPE;
   }
+  if (states_overlap(M->layers, M->nlayers, B, s0, s1)) return QL_EINVAL;
   ql_status st = QL_OK;
   if (output_layer) {
     st = check_qmatrix(&M->Wy, true);
@@ -889,6 +932,7 @@ ql_status ql_lstm_stack_forward(const ql_lstm_layer *layers, int32_t n, const ql
   if (x->rows != T * B || x->cols != layers[0].in || x->ld < round_up(x->cols, 64) || x->ld % 64)
     return QL_ESHAPE;
   if (T * B > 0 && (!x->codes || !x->zero || !x->inv_q || !x->sums)) return QL_EINVAL;
+  if (states_overlap(layers, n, B, state_in, state_out)) return QL_EINVAL;
   if (!ws || ws_bytes < ql_lstm_stack_workspace(layers, n, T, B)) return QL_EWORKSPACE;
   if (n == 1) return QL_EUNSUPPORTED;  // one layer: ql_lstm_layer_forward
   hipStream_t s = as_stream(stream);
@@ -1119,6 +1163,7 @@ ql_status ql_train_step(const ql_train_model *M, const float *feats, const int32
   if (st != QL_OK) return st;
   if (T < 0 || B < 0) return QL_ESHAPE;
   if (quantize_output != 0 && quantize_output != 1) return QL_EINVAL;
+  if (!std::isfinite(lr)) return QL_EINVAL;
   if (!grads || !grads->layers || grads->nlayers != M->nlayers || grads->states != M->states ||
       !grads->Wy || !grads->by)
     return QL_EINVAL;

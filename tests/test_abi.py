@@ -212,3 +212,79 @@ def test_frontend_argument_errors(ql):
         C.byref(m), FAKE, 20, 2, dim, 8, 3, FAKE, None, FAKE, wsb, None)
     assert g(dim=20) == ql.QL_ESHAPE                                   # 8*20 != layers[0].in
     assert g(wsb=need - 1) == ql.QL_EWORKSPACE
+
+
+def test_train_step_argument_errors(ql):
+    """ql_train_step (Section 3.2, Algorithm 1): every documented error."""
+    lib = ql.load()
+    TL, TM = ql.CTrainLayer, ql.CTrainModel
+
+    def model(*layers, states=10):
+        arr = (TL * len(layers))(*layers)
+        return TM(len(layers), arr, states, FAKE, FAKE), arr
+
+    M, _keep = model(TL(16, 8, 0, FAKE, FAKE, None, FAKE), TL(8, 8, 0, FAKE, FAKE, None, FAKE))
+    G, _keepg = model(TL(16, 8, 0, FAKE, FAKE, None, FAKE), TL(8, 8, 0, FAKE, FAKE, None, FAKE))
+    need = lib.ql_train_step_workspace(C.byref(M), 5, 2, 4)
+    assert need > 0
+    assert lib.ql_train_step_workspace(C.byref(M), 5, 2, 3) == 0        # 4H % 3
+
+    def step(m=M, g=G, T=5, lr=0.1, qout=1, wsb=need, feats=FAKE, gb=4):
+        return lib.ql_train_step(C.byref(m) if m is not None else None, feats, FAKE, T, 2, lr, gb,
+                                 qout, None, C.byref(g) if g is not None else None, FAKE, wsb,
+                                 None)
+
+    assert step(m=None) == ql.QL_EINVAL
+    assert step(g=None) == ql.QL_EINVAL
+    assert step(qout=2) == ql.QL_EINVAL
+    assert step(lr=float("nan")) == ql.QL_EINVAL
+    assert step(lr=float("inf")) == ql.QL_EINVAL
+    assert step(feats=None) == ql.QL_EINVAL
+    assert step(T=-1) == ql.QL_ESHAPE
+    assert step(gb=3) == ql.QL_ESHAPE
+    assert step(wsb=need - 1) == ql.QL_EWORKSPACE
+    G2, _k2 = model(TL(16, 8, 0, FAKE, FAKE, None, FAKE), TL(8, 7, 0, FAKE, FAKE, None, FAKE))
+    assert step(g=G2) == ql.QL_ESHAPE                                   # gradient shapes
+    G3, _k3 = model(TL(16, 8, 0, FAKE, FAKE, None, FAKE), TL(8, 8, 0, FAKE, FAKE, None, FAKE),
+                    states=11)
+    assert step(g=G3) == ql.QL_EINVAL                                   # states differ
+    MP, _kp = model(TL(16, 8, 4, FAKE, FAKE, FAKE, FAKE))
+    assert lib.ql_train_step_workspace(C.byref(MP), 5, 2, 4) == 0
+    assert step(m=MP) == ql.QL_EUNSUPPORTED                             # projection
+    MW, _kw = model(TL(16, 513, 0, FAKE, FAKE, None, FAKE))
+    assert step(m=MW) == ql.QL_EUNSUPPORTED                             # H > 512
+    MC, _kc = model(TL(16, 8, 0, FAKE, FAKE, None, FAKE), TL(9, 8, 0, FAKE, FAKE, None, FAKE))
+    assert step(m=MC) == ql.QL_ESHAPE                                   # widths do not chain
+
+
+def test_stream_state_in_and_out_must_not_overlap(ql):
+    """The stream entry points reject initial and final states that share
+    memory (the kernels read the one while writing the other)."""
+    lib = ql.load()
+    H, IN, S, T, B = 8, 16, 10, 3, 2
+    empty = ql.CQMatrix(None, 0, 0, 0, 1, None, None, None, None)
+    L0 = ql.CLayer(IN, H, 0, qm(4 * H, IN, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    L1 = ql.CLayer(H, H, 0, qm(4 * H, H, 64, 4), qm(4 * H, H, 64, 4), empty, FAKE)
+    arr = (ql.CLayer * 2)(L0, L1)
+    m = ql.CModel(2, arr, qm(S, H, 64, 1), FAKE)
+    need = lib.ql_acoustic_model_workspace(C.byref(m), T, B)
+    base = 0x100000
+    s_in = (ql.CState * 2)(ql.CState(base, base + 0x1000), ql.CState(base + 0x2000, base + 0x3000))
+
+    def call(s_out):
+        return lib.ql_acoustic_model_forward_stream(C.byref(m), FAKE, T, B, s_in, s_out, FAKE,
+                                                    None, FAKE, need, None)
+
+    # layer 1's c out starts inside layer 0's h in (B * H floats = 64 bytes from base)
+    overl = (ql.CState * 2)(ql.CState(base + 0x5000, base + 0x6000),
+                            ql.CState(base + 0x7000, base + 60))
+    assert call(overl) == ql.QL_EINVAL
+    same = (ql.CState * 2)(ql.CState(base + 0x5000, base + 0x6000),
+                           ql.CState(base + 0x2000, None))
+    assert call(same) == ql.QL_EINVAL
+    outs = (ql.CQAct * 2)(ql.CQAct(FAKE, T * B, H, 64, FAKE, FAKE, FAKE),
+                          ql.CQAct(FAKE, T * B, H, 64, FAKE, FAKE, FAKE))
+    x = ql.CQAct(FAKE, T * B, IN, 64, FAKE, FAKE, FAKE)
+    sneed = lib.ql_lstm_stack_workspace(arr, 2, T, B)
+    assert lib.ql_lstm_stack_forward(arr, 2, C.byref(x), T, B, outs, None, s_in, same, None, FAKE,
+                                     sneed, None) == ql.QL_EINVAL
