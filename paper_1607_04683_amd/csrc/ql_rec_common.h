@@ -342,4 +342,58 @@ __device__ __forceinline__ void products_mfma(const int8_t *x, int ldx, int nb, 
   }
 }
 
+// Fragments of 16-row block `blk` of a weight slice in LDS (rows of ldw
+// bytes, K codes) as the B operand of v_mfma_i32_16x16x64_i8: lane l holds row
+// l % 16, bytes 16 (l / 16) .. +15 of every 64-byte chunk of K; chunks past K
+// are zero.  Loaded once and kept in registers across a launch.
+__device__ __forceinline__ void load_wfrag(v4i (&b)[8], const int8_t *w, int ldw, int blk, int K) {
+  const int lane = threadIdx.x & 63;
+  const int8_t *wr = w + (blk * 16 + (lane & 15)) * ldw + (lane >> 4) * 16;
+#pragma unroll
+  for (int c = 0; c < 8; ++c)
+    b[c] = c * 64 < K ? *reinterpret_cast<const v4i *>(wr + c * 64) : v4i{};
+}
+
+// The products of every 16-row block of x (nb rows, a multiple of 16, in LDS)
+// against the register fragments b of weight block blk (K <= 512 codes):
+// S[row][blk * 16 + col].  One wave; two row blocks go through the MFMA
+// pipeline side by side.
+__device__ __forceinline__ void products_mfma_reg(const int8_t *x, int ldx, int nb,
+                                                  const v4i (&b)[8], int blk, int K, int32_t *S,
+                                                  int ldS) {
+  const int lane = threadIdx.x & 63;
+  const int mt = nb / 16;
+  auto put = [&](int ti, const v4i &acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      S[(ti * 16 + (lane >> 4) * 4 + r) * ldS + blk * 16 + (lane & 15)] = acc[r];
+  };
+  int ti = 0;
+  for (; ti + 1 < mt; ti += 2) {
+    const int8_t *x0 = x + (ti * 16 + (lane & 15)) * ldx + (lane >> 4) * 16;
+    const int8_t *x1 = x0 + 16 * ldx;
+    v4i acc0 = v4i{}, acc1 = v4i{};
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      if (c * 64 < K) {
+        const v4i a0 = *reinterpret_cast<const v4i *>(x0 + c * 64);
+        const v4i a1 = *reinterpret_cast<const v4i *>(x1 + c * 64);
+        acc0 = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0, b[c], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1, b[c], acc1, 0, 0, 0);
+      }
+    put(ti, acc0);
+    put(ti + 1, acc1);
+  }
+  if (ti < mt) {
+    const int8_t *x0 = x + (ti * 16 + (lane & 15)) * ldx + (lane >> 4) * 16;
+    v4i acc = v4i{};
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      if (c * 64 < K)
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(*reinterpret_cast<const v4i *>(x0 + c * 64),
+                                                   b[c], acc, 0, 0, 0);
+    put(ti, acc);
+  }
+}
+
 }  // namespace ql

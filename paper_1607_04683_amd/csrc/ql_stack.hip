@@ -382,6 +382,15 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
     const int hwords = tl.ldH / 8;
     uint64_t hpre[kXPre];
 
+    // With at most one 16-row block of gate rows per wave, wave w keeps the
+    // fragments of block w of W_h' in registers for the launch: the recurrent
+    // product (on the critical path) then reads only the activation
+    // fragments from LDS.
+    const int wave = tid >> 6, nblk = nrows / 16;
+    const bool wreg = nblk <= kStackThreads / 64;
+    v4i fh[8];
+    if (wreg && wave < nblk) load_wfrag(fh, wh, tl.ldsW, wave, tl.ldH);
+
     // Gate work of this lane, fixed for the launch: pair (row, cell) number
     // tid of every full round of nt pairs, then in the remainder one pair
     // over lpp lanes (gates g0 .. g0 + ng - 1 on this lane).  Index
@@ -562,7 +571,10 @@ __global__ __launch_bounds__(kStackThreads) void k_stack(StackArgs a, StackTilin
       __syncthreads();
 
       // ---- 3. the recurrent product against the resident W_h' slice
-      products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+      if (!wreg)
+        products_mfma(xh, tl.ldsX, tl.bB, wh, tl.ldsW, nrows, nrows, tl.ldH, Sh, nrows);
+      else if (wave < nblk)
+        products_mfma_reg(xh, tl.ldsX, tl.bB, fh, wave, tl.ldH, Sh, nrows);
       __syncthreads();
       if (TP && Ly.acc_h) tap_acc(Ly.acc_h, Sh, cph, rph, H, t);
 
