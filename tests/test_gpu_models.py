@@ -149,6 +149,26 @@ def test_model_softmax_large_tiles_ragged_states(ql, orc):
     assert np.max(np.abs(p.sum(-1) - 1.0)) < 1e-5
 
 
+@pytest.mark.parametrize("H,S", [(40, 300), (130, 8200)])
+def test_model_softmax_long_runs_ragged(ql, orc, H, S):
+    """33020 frames (260 x 127, a ragged last block of rows) with K of one
+    64-byte step (H = 40) or three (H = 130) and a ragged last block of states
+    (300, 8200).  Logits and accumulators bit-exact and posteriors to 1e-4 on
+    sampled utterances; the launch without taps writes the same posteriors."""
+    from paper_1607_04683_amd.workloads import random_model
+    w = random_model(24, H, 1, states=S, seed=43 + H)
+    x = np.random.default_rng(3).standard_normal((260, 127, 24)).astype(np.float32)
+    utts = [0, 64, 126]
+    g, o = _model_case(ql, orc, w, x, utts=utts, taps=True)
+    assert np.array_equal(np_(g["acc_y"])[:, utts], o["acc_y"])
+    assert np.array_equal(np_(g["logits"])[:, utts], o["logits"])
+    p = np_(g["post"][:, :16]).astype(np.float64)
+    assert np.max(np.abs(p.sum(-1) - 1.0)) < 1e-5
+    # the same posteriors without taps (the launch that writes no logits)
+    post = ql.acoustic_model_forward(ql.quantize_model(w), torch.from_numpy(x).cuda())["post"]
+    assert torch.equal(post, g["post"])
+
+
 def test_model_5x500_softmax8192_T500_B1(ql, orc):
     """Five 500-cell layers + 8192-way quantized softmax, T=500, batch 1, on the
     one-row layer wavefront (all five layers in one launch): every layer's
