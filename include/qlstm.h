@@ -397,6 +397,13 @@ ql_status ql_train_step(const ql_train_model *M, const float *feats, const int32
  * undefined), else QL_OK. */
 ql_status ql_workspace_status(const void *ws, void *stream);
 const char *ql_status_str(ql_status s);
+/* Test hook for the timeout path: calls made after it bound every inter-
+ * workgroup wait of their persistent kernels to `polls` re-reads (0 restores
+ * the default bound), so a wait that is not met at once expires, every
+ * workgroup leaves at its next wait, and ql_workspace_status reports
+ * QL_ETIMEOUT (the outputs are then undefined).  Process-wide; QL_EINVAL for
+ * a negative count. */
+ql_status ql_debug_set_wait_bound(int32_t polls);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
  * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,
  * defined for d in [1, 2^126) and equal there to IEEE division) -- the exact

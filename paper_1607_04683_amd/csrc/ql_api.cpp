@@ -984,6 +984,12 @@ ql_status ql_workspace_status(const void *ws, void *stream) {
   return to ? QL_ETIMEOUT : QL_OK;
 }
 
+ql_status ql_debug_set_wait_bound(int32_t polls) {
+  if (polls < 0) return QL_EINVAL;
+  set_wait_bound(polls);
+  return QL_OK;
+}
+
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {
   if (n > 0 && (!x || !y)) return QL_EINVAL;
   if (fn < 0 || fn > 3) return QL_EINVAL;

@@ -19,6 +19,8 @@ namespace ql {
 constexpr long kSpinLimit = 1l << 22;
 constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
 constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
+// The next word bounds every wait of the launch to that many re-reads (0:
+// kSpinLimit); the API writes it with the flag at the start of every call.
 constexpr int kMaxSlices = 256;    // arrival counters per kind and parity
 constexpr int kCounterBytes = 2 * 2 * kMaxSlices * 64;  // one 64-byte line per counter
 
@@ -62,8 +64,15 @@ __device__ __forceinline__ void st_coherent_i(int32_t *p, int32_t v) {
 __device__ __forceinline__ int32_t ld_coherent_i(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Bounded-wait bookkeeping: true when the wait must be abandoned.
+// Bounded-wait bookkeeping: true when the wait must be abandoned.  Called
+// once per failed poll with `it` zero before the first; a bound other than
+// the default (the header word after the flag) is read at the first call and
+// counted into `it`, so a wait that succeeds at once reads nothing.
 __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
+  if (it == 0) {
+    const int bound = __hip_atomic_load(flag + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (bound > 0 && bound < kSpinLimit) it = kSpinLimit - bound;
+  }
   if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
     return true;
   if (it > kSpinLimit) {

@@ -93,8 +93,10 @@ struct RecurrentArgs {
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P);
 // returns hipSuccess, or an error; *unsupported set if shapes do not fit.
 hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsupported);
-// Clears the timeout flag (once per API call, before the first layer).
+// Clears the timeout flag (once per API call, before the first layer) and
+// writes the bound of the call's waits (set_wait_bound; 0 = the default).
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s);
+void set_wait_bound(int polls);
 // Reads the timeout flag a persistent launch left in its workspace (syncs s).
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
 // Zeroes the n64 64-bit words after the workspace header (counters first).

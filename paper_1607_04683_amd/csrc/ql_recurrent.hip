@@ -32,6 +32,7 @@
 // the buffer is cleared before every launch.  Every wait is bounded: on expiry
 // a flag in the workspace is raised, and all workgroups leave at their next
 // wait, so the grid always drains.
+#include <atomic>
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
@@ -670,10 +671,14 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
 }
 
 // Clears the arrival counters and the exchange buffers (n64 64-bit words
-// after the header); the timeout flag only when asked (once per API call).
-__global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
+// after the header); the timeout flag only when asked (once per API call),
+// writing the bound of the call's waits beside it.
+__global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag, int bound) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0 && with_flag) hdr[kHdrFlag] = 0u;
+  if (i == 0 && with_flag) {
+    hdr[kHdrFlag] = 0u;
+    hdr[kHdrFlag + 1] = (unsigned)bound;
+  }
   uint64_t *x = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(hdr) + kHeaderBytes);
   for (int64_t k = i; k < n64; k += (int64_t)gridDim.x * blockDim.x) x[k] = 0;
 }
@@ -681,13 +686,18 @@ __global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
 hipError_t clear_exchange(void *ws, int64_t n64, hipStream_t s) {
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(ws), n64,
-                     0);
+                     0, 0);
   return hipGetLastError();
 }
 
+// Bound of every wait of the calls made from now on (0: the default); a
+// test hook that forces the timeout path without a kernel that hangs.
+static std::atomic<int> g_wait_bound{0};
+void set_wait_bound(int polls) { g_wait_bound.store(polls < 0 ? 0 : polls); }
+
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s) {
   hipLaunchKernelGGL(k_clear_exchange, dim3(1), dim3(64), 0, s, static_cast<unsigned *>(ws),
-                     (int64_t)0, 1);
+                     (int64_t)0, 1, g_wait_bound.load());
   return hipGetLastError();
 }
 
@@ -910,7 +920,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
   const int64_t n64 = kRecCounterBytes / 8 + tl.reph * tl.strideh + tl.repm * tl.stridem;
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(a.ws),
-                     n64, 0);
+                     n64, 0, 0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   tl.off_mc = kHeaderBytes + align_up((size_t)exchange_words(a.B, a.H, a.P) * sizeof(uint64_t), 256);

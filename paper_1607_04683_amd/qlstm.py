@@ -36,6 +36,7 @@ EXPORTS = [
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
     "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
     "ql_acoustic_model_forward_stream_noalloc", "ql_train_step_workspace", "ql_train_step",
+    "ql_debug_set_wait_bound",
 ]
 
 
@@ -139,6 +140,7 @@ def load(path: str = LIB_PATH):
                                      C.POINTER(CQAct), C.POINTER(CTaps), vp, sz, vp]
     L.ql_workspace_status.argtypes = [vp, vp]
     L.ql_gate_fn.argtypes = [i32, vp, vp, i64, vp]
+    L.ql_debug_set_wait_bound.argtypes = [i32]
     L.ql_f32_matmul.argtypes = [vp, i64, i64, vp, i64, vp, vp, vp]
     L.ql_quantize_activations.argtypes = [vp, i64, i64, C.POINTER(CQAct), vp]
     L.ql_lstm_stack_workspace.argtypes = [C.POINTER(CLayer), i32, i64, i64]
@@ -179,7 +181,8 @@ def load(path: str = LIB_PATH):
               "ql_f32_acoustic_model_forward", "ql_quantize_activations",
               "ql_lstm_stack_forward", "ql_quantize_stacked_frames",
               "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
-              "ql_acoustic_model_forward_stream_noalloc", "ql_train_step"):
+              "ql_acoustic_model_forward_stream_noalloc", "ql_train_step",
+              "ql_debug_set_wait_bound"):
         getattr(L, f).restype = i32
     _lib = L
     return L

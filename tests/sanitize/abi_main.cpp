@@ -65,6 +65,12 @@ ql_qact qact(int64_t rows, int64_t cols) {
   return a;
 }
 
+void wait_bound_hook() {
+  EXPECT(ql_debug_set_wait_bound(-1), QL_EINVAL);
+  EXPECT(ql_debug_set_wait_bound(5), QL_OK);
+  EXPECT(ql_debug_set_wait_bound(0), QL_OK);
+}
+
 void status_strings() {
   for (int s = -8; s <= 0; ++s) EXPECT(ql_status_str(static_cast<ql_status>(s)) != nullptr, 1);
   EXPECT(ql_status_str(static_cast<ql_status>(-100)) != nullptr, 1);
@@ -266,6 +272,7 @@ void training() {
 
 int main() {
   status_strings();
+  wait_bound_hook();
   quantize_and_products();
   layers_and_models();
   fp32_model();

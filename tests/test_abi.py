@@ -288,3 +288,9 @@ def test_stream_state_in_and_out_must_not_overlap(ql):
     sneed = lib.ql_lstm_stack_workspace(arr, 2, T, B)
     assert lib.ql_lstm_stack_forward(arr, 2, C.byref(x), T, B, outs, None, s_in, same, None, FAKE,
                                      sneed, None) == ql.QL_EINVAL
+
+
+def test_wait_bound_hook_arguments(ql):
+    lib = ql.load()
+    assert lib.ql_debug_set_wait_bound(-1) == ql.QL_EINVAL
+    assert lib.ql_debug_set_wait_bound(0) == ql.QL_OK
