@@ -252,6 +252,15 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
         }
       }
     }
+    // An XDL result needs a pass-count-dependent number of wait states before
+    // an LDS store may read it, and nothing checks that in hardware.  The
+    // compiler's spacing was found missing here (the stores of acc[0..1] two
+    // instructions after the last MFMA, on the path that falls through from
+    // the products): those rows then took a value from before the final
+    // pass, at random.  The statement below reads and writes acc, so it sits
+    // between the last MFMA and the stores whatever the schedule, and gives
+    // 24 wait states (a 16-pass XDL result needs at most 19).
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acc));
     // partial blocks to LDS: part[wave][row][cell]
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[(wave * 16 + 4 * fq + i) * 16 + fr] = acc[i];

@@ -88,6 +88,22 @@ def test_train_step_5x500_softmax8192_B64(ql, orc):
     _compare(ql, orc, w, x, y, lr=1.0)
 
 
+@pytest.mark.parametrize("H,B", [(500, 64), (128, 64), (48, 20)])
+def test_train_step_repeats_bit_for_bit(ql, H, B):
+    """The same step on the same inputs gives the same gradients, bit for bit,
+    every time: the backward recurrence and the products sum in fixed orders,
+    so a difference means some value was read before it was final.  At 500
+    cells and batch 64 every CU of the chip holds a backward tile."""
+    w, x, y = _case(40, H, 1, 96, 12, B, seed=H + B)
+    x, y = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    _, ref = ql.train_step(ql.train_params(w), x, y, 1.0)
+    for _ in range(4):
+        _, g = ql.train_step(ql.train_params(w), x, y, 1.0)
+        for k in ("Wx", "Wh", "b"):
+            assert torch.equal(g["layers"][0][k], ref["layers"][0][k]), k
+        assert torch.equal(g["Wy"], ref["Wy"]) and torch.equal(g["by"], ref["by"])
+
+
 def test_train_steps_lower_the_loss(ql, orc):
     """Repeated quantization-aware steps on one mini-batch (targets a function
     of the current frame) lower its loss at every step, as the oracle's
