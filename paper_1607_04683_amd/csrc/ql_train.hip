@@ -208,8 +208,8 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
   const int lb = tid / tl.u, jj = tid % tl.u;  // cell lanes: pair (row lb, cell jj)
   const bool cell_lane = tid < npr && lb < nb && jj < nu;
   // this lane's cell operands of a step (the forward pass's gates, c_t,
-  // c_{t-1} and dC/dh from above): loaded a step ahead, while the stores of
-  // the current step complete
+  // c_{t-1} and dC/dh from above): loaded a step ahead, right after the
+  // step's arrival
   float ig = 0.0f, fg = 0.0f, gg = 0.0f, og = 0.0f, ct = 0.0f, cp = 0.0f, dyv = 0.0f;
   auto load_cell = [&](int64_t t) {
     if (!cell_lane || t < 0) return;
@@ -228,18 +228,22 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
       if (!wait_count(counter(t + 1, tb), (unsigned)tl.nut, flag)) s_abort = 1;
       __syncthreads();
       if (s_abort) return;
-      // 16 consecutive k of row fr per block, as 8-byte words, all in flight
-      const float *src = a.da + ((t + 1) * B + b0 + fr) * G4;
+      // 16 consecutive k of row fr per block, as 8-byte words, all in flight,
+      // issued block by block so that each block's products wait only for its
+      // own loads.  Every lane loads: a row past the slice reads the slice's
+      // row 0 (its products land in output rows nobody reads), and k past 4H
+      // reads k = 0 (a finite value, times the zero columns of W_h^T in LDS).
+      const float *src = a.da + ((t + 1) * B + b0 + (fr < nb ? fr : 0)) * G4;
       uint64_t dv[kBpttKBlocks][8];
 #pragma unroll
-      for (int kb = 0; kb < kBpttKBlocks; ++kb)
+      for (int kb = 0; kb < kBpttKBlocks; ++kb) {
 #pragma unroll
         for (int w = 0; w < 8; ++w) {
           const int64_t k = kof(kb, 2 * w);
-          dv[kb][w] = fr < nb && k < G4
-                          ? ld_coherent64(reinterpret_cast<const uint64_t *>(src + k))
-                          : 0;
+          dv[kb][w] = ld_coherent64(reinterpret_cast<const uint64_t *>(src + (k < G4 ? k : 0)));
         }
+        __builtin_amdgcn_sched_barrier(0);  // issue order: block by block
+      }
 #pragma unroll
       for (int kb = 0; kb < kBpttKBlocks; ++kb) {
         const v4f_t *wr = reinterpret_cast<const v4f_t *>(wT + fr * kBpttLdw + kof(kb, 0));
@@ -285,9 +289,11 @@ __global__ __launch_bounds__(kBpttThreads) void k_bptt(BpttArgs a, BpttTiling tl
       st_coherent(dst + 2 * H, v2);
       st_coherent(dst + 3 * H, v3);
     }
-    load_cell(t - 1);
     if (t > 0) arrive(counter(t, tb));  // (no tile waits on step 0's arrivals)
     else __syncthreads();               // part is rewritten only by a next launch
+    // the next step's cell operands, issued after the arrival so that its
+    // wait for the stores of da_t does not also wait for these loads
+    load_cell(t - 1);
   }
 }
 
