@@ -56,8 +56,19 @@ __global__ __launch_bounds__(256) void k_colsum_part(const float *X, int64_t M, 
   if (n >= N) return;
   const int64_t m0 = (int64_t)blockIdx.y * rows_per_chunk;
   const int64_t m1 = std::min<int64_t>(M, m0 + rows_per_chunk);
+  // eight rows loaded before they are added (in row order), so eight loads
+  // are in flight per thread
+  constexpr int kU = 8;
   float s = 0.0f;
-  for (int64_t m = m0; m < m1; ++m) s += X[m * N + n];
+  int64_t m = m0;
+  for (; m + kU <= m1; m += kU) {
+    float v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) v[u] = X[(m + u) * N + n];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) s += v[u];
+  }
+  for (; m < m1; ++m) s += X[m * N + n];
   part[(int64_t)blockIdx.y * N + n] = s;
 }
 __global__ __launch_bounds__(256) void k_colsum_final(const float *part, int chunks, int64_t N,
