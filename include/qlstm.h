@@ -399,10 +399,11 @@ ql_status ql_workspace_status(const void *ws, void *stream);
 const char *ql_status_str(ql_status s);
 /* Test hook for the timeout path: calls made after it bound every inter-
  * workgroup wait of their persistent kernels to `polls` re-reads (0 restores
- * the default bound), so a wait that is not met at once expires, every
+ * the default bound), so a wait that is not met within them expires, every
  * workgroup leaves at its next wait, and ql_workspace_status reports
- * QL_ETIMEOUT (the outputs are then undefined).  Process-wide; QL_EINVAL for
- * a negative count. */
+ * QL_ETIMEOUT (the outputs are then undefined).  Applies to every device of
+ * the process (none: nothing to do); QL_EINVAL for a negative count, QL_EHIP
+ * if a device could not be set. */
 ql_status ql_debug_set_wait_bound(int32_t polls);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
  * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,

@@ -986,8 +986,7 @@ ql_status ql_workspace_status(const void *ws, void *stream) {
 
 ql_status ql_debug_set_wait_bound(int32_t polls) {
   if (polls < 0) return QL_EINVAL;
-  set_wait_bound(polls);
-  return QL_OK;
+  return set_wait_bound(polls) == hipSuccess ? QL_OK : QL_EHIP;
 }
 
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {

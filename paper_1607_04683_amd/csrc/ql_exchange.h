@@ -19,8 +19,6 @@ namespace ql {
 constexpr long kSpinLimit = 1l << 22;
 constexpr int kHeaderBytes = 256;  // timeout flag at byte 64
 constexpr int kHdrFlag = 16;       // 32-bit word index of the timeout flag
-// The next word bounds every wait of the launch to that many re-reads (0:
-// kSpinLimit); the API writes it with the flag at the start of every call.
 constexpr int kMaxSlices = 256;    // arrival counters per kind and parity
 constexpr int kCounterBytes = 2 * 2 * kMaxSlices * 64;  // one 64-byte line per counter
 
@@ -64,15 +62,16 @@ __device__ __forceinline__ void st_coherent_i(int32_t *p, int32_t v) {
 __device__ __forceinline__ int32_t ld_coherent_i(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Re-reads counted at the start of every wait of this code object's kernels:
+// 0, or kSpinLimit - n to bound each wait to n re-reads.  A test hook sets it
+// from the host (set_wait_bound_here); every source file that includes this
+// header has its own copy.  Constant memory: read with scalar loads.
+static __constant__ long g_wait_it0 = 0;
+
 // Bounded-wait bookkeeping: true when the wait must be abandoned.  Called
-// once per failed poll with `it` zero before the first; a bound other than
-// the default (the header word after the flag) is read at the first call and
-// counted into `it`, so a wait that succeeds at once reads nothing.
+// once per failed poll with `it` zero before the first.
 __device__ __forceinline__ bool wait_expired(int *flag, long &it) {
-  if (it == 0) {
-    const int bound = __hip_atomic_load(flag + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (bound > 0 && bound < kSpinLimit) it = kSpinLimit - bound;
-  }
+  if (it == 0) it = g_wait_it0;
   if ((++it & 63) == 0 && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
     return true;
   if (it > kSpinLimit) {
@@ -100,6 +99,13 @@ __device__ __forceinline__ bool wait_count(const unsigned *cnt, unsigned target,
   while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target)
     if (wait_expired(flag, it)) return false;
   return true;
+}
+
+// Host side: this source file's bound, on the current device (polls = 0:
+// the default).
+static inline hipError_t set_wait_bound_here(int polls) {
+  const long v = polls > 0 && polls < kSpinLimit ? kSpinLimit - polls : 0;
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_wait_it0), &v, sizeof v);
 }
 
 }  // namespace ql

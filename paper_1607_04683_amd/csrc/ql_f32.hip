@@ -592,4 +592,6 @@ hipError_t launch_recurrent_f32(const F32RecArgs &a, hipStream_t s, bool *unsupp
                                     dim3(kF32Threads), kargs, (unsigned)tl.lds_bytes, s);
 }
 
+hipError_t set_wait_bound_f32(int polls) { return set_wait_bound_here(polls); }
+
 }  // namespace ql

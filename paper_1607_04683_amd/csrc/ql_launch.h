@@ -93,10 +93,16 @@ struct RecurrentArgs {
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P);
 // returns hipSuccess, or an error; *unsupported set if shapes do not fit.
 hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsupported);
-// Clears the timeout flag (once per API call, before the first layer) and
-// writes the bound of the call's waits (set_wait_bound; 0 = the default).
+// Clears the timeout flag (once per API call, before the first layer).
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s);
-void set_wait_bound(int polls);
+// Bounds every wait of the persistent kernels to `polls` re-reads (0: the
+// default), on every device; one setter per source file with such kernels.
+hipError_t set_wait_bound(int polls);
+hipError_t set_wait_bound_recurrent(int polls);
+hipError_t set_wait_bound_stack(int polls);
+hipError_t set_wait_bound_pstack(int polls);
+hipError_t set_wait_bound_f32(int polls);
+hipError_t set_wait_bound_train(int polls);
 // Reads the timeout flag a persistent launch left in its workspace (syncs s).
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
 // Zeroes the n64 64-bit words after the workspace header (counters first).

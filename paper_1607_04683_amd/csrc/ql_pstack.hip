@@ -422,4 +422,6 @@ int pstack_layers_per_launch(const PStackArgs &a) {
   return 1;
 }
 
+hipError_t set_wait_bound_pstack(int polls) { return set_wait_bound_here(polls); }
+
 }  // namespace ql

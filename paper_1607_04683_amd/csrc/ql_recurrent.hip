@@ -32,7 +32,6 @@
 // the buffer is cleared before every launch.  Every wait is bounded: on expiry
 // a flag in the workspace is raised, and all workgroups leave at their next
 // wait, so the grid always drains.
-#include <atomic>
 #include "ql_device.h"
 #include "ql_exchange.h"
 #include "ql_launch.h"
@@ -671,14 +670,10 @@ __global__ __launch_bounds__(kRecThreads) void k_recurrent(RecurrentArgs a, RecT
 }
 
 // Clears the arrival counters and the exchange buffers (n64 64-bit words
-// after the header); the timeout flag only when asked (once per API call),
-// writing the bound of the call's waits beside it.
-__global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag, int bound) {
+// after the header); the timeout flag only when asked (once per API call).
+__global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0 && with_flag) {
-    hdr[kHdrFlag] = 0u;
-    hdr[kHdrFlag + 1] = (unsigned)bound;
-  }
+  if (i == 0 && with_flag) hdr[kHdrFlag] = 0u;
   uint64_t *x = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(hdr) + kHeaderBytes);
   for (int64_t k = i; k < n64; k += (int64_t)gridDim.x * blockDim.x) x[k] = 0;
 }
@@ -686,19 +681,38 @@ __global__ void k_clear_exchange(unsigned *hdr, int64_t n64, int with_flag, int 
 hipError_t clear_exchange(void *ws, int64_t n64, hipStream_t s) {
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(ws), n64,
-                     0, 0);
+                     0);
   return hipGetLastError();
 }
 
-// Bound of every wait of the calls made from now on (0: the default); a
-// test hook that forces the timeout path without a kernel that hangs.
-static std::atomic<int> g_wait_bound{0};
-void set_wait_bound(int polls) { g_wait_bound.store(polls < 0 ? 0 : polls); }
-
 hipError_t reset_recurrent_flag(void *ws, hipStream_t s) {
   hipLaunchKernelGGL(k_clear_exchange, dim3(1), dim3(64), 0, s, static_cast<unsigned *>(ws),
-                     (int64_t)0, 1, g_wait_bound.load());
+                     (int64_t)0, 1);
   return hipGetLastError();
+}
+
+hipError_t set_wait_bound_recurrent(int polls) { return set_wait_bound_here(polls); }
+
+// The bound of every wait of the persistent kernels, on every device (a test
+// hook that forces the timeout path without a kernel that hangs); without a
+// device there is nothing to bound.
+hipError_t set_wait_bound(int polls) {
+  int n = 0, cur = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return hipSuccess;
+  }
+  hipError_t e = hipGetDevice(&cur);
+  for (int d = 0; d < n && e == hipSuccess; ++d) {
+    e = hipSetDevice(d);
+    if (e == hipSuccess) e = set_wait_bound_recurrent(polls);
+    if (e == hipSuccess) e = set_wait_bound_stack(polls);
+    if (e == hipSuccess) e = set_wait_bound_pstack(polls);
+    if (e == hipSuccess) e = set_wait_bound_f32(polls);
+    if (e == hipSuccess) e = set_wait_bound_train(polls);
+  }
+  const hipError_t r = hipSetDevice(cur);
+  return e != hipSuccess ? e : r;
 }
 
 // ------------------------------------------------------------------ host side
@@ -920,7 +934,7 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
   const int64_t n64 = kRecCounterBytes / 8 + tl.reph * tl.strideh + tl.repm * tl.stridem;
   const unsigned zb = (unsigned)std::min<int64_t>(1024, (n64 + 255) / 256 + 1);
   hipLaunchKernelGGL(k_clear_exchange, dim3(zb), dim3(256), 0, s, static_cast<unsigned *>(a.ws),
-                     n64, 0, 0);
+                     n64, 0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   tl.off_mc = kHeaderBytes + align_up((size_t)exchange_words(a.B, a.H, a.P) * sizeof(uint64_t), 256);

@@ -1009,4 +1009,6 @@ int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0,
   return 1;
 }
 
+hipError_t set_wait_bound_stack(int polls) { return set_wait_bound_here(polls); }
+
 }  // namespace ql

@@ -384,4 +384,6 @@ hipError_t launch_bptt(const BpttArgs &a, hipStream_t s, bool *unsupported) {
                                     dim3(kBpttThreads), kargs, (unsigned)tl.lds_bytes, s);
 }
 
+hipError_t set_wait_bound_train(int polls) { return set_wait_bound_here(polls); }
+
 }  // namespace ql
