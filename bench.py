@@ -35,10 +35,10 @@ FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=4.473e+09, read=2.998e+09, written=1.476e+09,
+TRAFFIC = dict(bytes=4.47e+09, read=2.994e+09, written=1.476e+09,
                sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
                         "ql_launch.h"),
-               sha256="ca431dde8a0d5ebfb158c28cfc5286431cef480fc3c4266d332fbaa8623048bc",
+               sha256="3f64d75e66db12695e28ef7e92486c916181ee91003d4bfa0bb09adcf6410fa9",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
 
