@@ -402,8 +402,9 @@ const char *ql_status_str(ql_status s);
  * the default bound), so a wait that is not met within them expires, every
  * workgroup leaves at its next wait, and ql_workspace_status reports
  * QL_ETIMEOUT (the outputs are then undefined).  Applies to every device of
- * the process (none: nothing to do); QL_EINVAL for a negative count, QL_EHIP
- * if a device could not be set. */
+ * the process (none: nothing to do) and must not overlap a call of this
+ * library in flight; QL_EINVAL for a negative count, QL_EHIP if a device
+ * could not be set. */
 ql_status ql_debug_set_wait_bound(int32_t polls);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
  * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,
