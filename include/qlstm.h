@@ -406,6 +406,11 @@ const char *ql_status_str(ql_status s);
  * library in flight; QL_EINVAL for a negative count, QL_EHIP if a device
  * could not be set. */
 ql_status ql_debug_set_wait_bound(int32_t polls);
+/* Test hook: which layout the recurrence of layer L runs in at batch B on the
+ * current device -- 1: one persistent launch over the whole chip with each
+ * XCD holding an eighth of the batch (layers with a projection, batch 16 to
+ * 256, 256 CUs), 0: any other path; -1 for an invalid layer or B < 0. */
+int32_t ql_debug_recurrence_layout(const ql_lstm_layer *L, int64_t B);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
  * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,
  * defined for d in [1, 2^126) and equal there to IEEE division) -- the exact

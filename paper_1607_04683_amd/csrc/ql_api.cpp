@@ -989,6 +989,15 @@ ql_status ql_debug_set_wait_bound(int32_t polls) {
   return set_wait_bound(polls) == hipSuccess ? QL_OK : QL_EHIP;
 }
 
+int32_t ql_debug_recurrence_layout(const ql_lstm_layer *L, int64_t B) {
+  if (check_layer(L) != QL_OK || B < 0) return -1;
+  ActBuf out{};
+  out.ld = round_up(layer_width(*L), 64);
+  RecurrentArgs a = rec_args(*L, 1, B, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                             out, nullptr, nullptr);
+  return recurrent_layout(a);
+}
+
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {
   if (n > 0 && (!x || !y)) return QL_EINVAL;
   if (fn < 0 || fn > 3) return QL_EINVAL;

@@ -91,6 +91,14 @@ struct RecurrentArgs {
   void *ws;
 };
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P);
+// Batched layers with a projection on the whole chip (ql_xrec.hip): each XCD
+// runs the layer for an eighth of the batch.  *done false when the shapes or
+// the device do not fit that layout (nothing launched).
+size_t xrec_ws(int64_t B, int64_t H, int64_t P);
+hipError_t launch_xrec(const RecurrentArgs &a, int cus, int lds_max, hipStream_t s, bool *done);
+// 1 when launch_recurrent would run `a` in the XCD-local layout on the current
+// device, else 0.
+int recurrent_layout(const RecurrentArgs &a);
 // returns hipSuccess, or an error; *unsupported set if shapes do not fit.
 hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsupported);
 // Clears the timeout flag (once per API call, before the first layer).
@@ -103,6 +111,7 @@ hipError_t set_wait_bound_stack(int polls);
 hipError_t set_wait_bound_pstack(int polls);
 hipError_t set_wait_bound_f32(int polls);
 hipError_t set_wait_bound_train(int polls);
+hipError_t set_wait_bound_xrec(int polls);
 // Reads the timeout flag a persistent launch left in its workspace (syncs s).
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
 // Zeroes the n64 64-bit words after the workspace header (counters first).

@@ -710,6 +710,7 @@ hipError_t set_wait_bound(int polls) {
     if (e == hipSuccess) e = set_wait_bound_pstack(polls);
     if (e == hipSuccess) e = set_wait_bound_f32(polls);
     if (e == hipSuccess) e = set_wait_bound_train(polls);
+    if (e == hipSuccess) e = set_wait_bound_xrec(polls);
   }
   const hipError_t r = hipSetDevice(cur);
   return e != hipSuccess ? e : r;
@@ -738,8 +739,10 @@ static size_t mcode_bytes(int64_t B, int64_t H, int64_t P) {
 }
 
 size_t recurrent_ws(int64_t B, int64_t H, int64_t P) {
-  return kHeaderBytes + align_up((size_t)exchange_words(B, H, P) * sizeof(uint64_t), 256) +
-         mcode_bytes(B, H, P);
+  const size_t spread = kHeaderBytes +
+                        align_up((size_t)exchange_words(B, H, P) * sizeof(uint64_t), 256) +
+                        mcode_bytes(B, H, P);
+  return std::max(spread, xrec_ws(B, H, P));
 }
 
 static int replicas(int values_per_block, int consumers) {
@@ -910,6 +913,10 @@ hipError_t launch_recurrent(const RecurrentArgs &a, hipStream_t s, bool *unsuppo
   }
   int lds_max = 0;
   const int cus = device_cus(&lds_max);
+  // batched layers with a projection on the whole chip: the XCD-local layout
+  bool done = false;
+  hipError_t ex = launch_xrec(a, cus, lds_max, s, &done);
+  if (ex != hipSuccess || done) return ex;
   RecTiling tl;
   if (!plan(a, cus, lds_max, &tl)) {
     *unsupported = true;

@@ -1,0 +1,807 @@
+// ql_xrec.hip -- a quantized LSTM layer with a projection (Section 4, the
+// LSTMP layer: m_t = o tanh(c_t), h_t = W_r m_t) at batch 16 .. 256, one
+// persistent launch over the whole chip laid out by XCD.
+//
+// The batch rows of a layer are independent of one another, so the batch is
+// split over the eight XCDs: XCD x owns rows [x rows, (x + 1) rows) of the
+// batch for the whole sequence, and its 32 workgroups (one per CU; each reads
+// its XCC_ID and takes the next free slot s of its XCD) never exchange a value
+// with another XCD.  Every hand-off of a step then stays in that XCD's L2:
+// values go out with plain stores and are read with device-coherent loads,
+// which find them there.  Slot s plays two tiles:
+//   * a unit tile: cells [s u, (s + 1) u) of every row of the XCD.  Its 4u
+//     gate rows of W_h' stay in registers as MFMA fragments for the launch,
+//     four cells (their 16 gate rows, gates i f g o of a cell adjacent) per
+//     fragment block, so an MFMA result gives a lane the four gates of one
+//     (cell, row) pair and c stays in that lane's registers;
+//   * a projection tile: outputs [o pw, (o + 1) pw) of row group g (half of
+//     the XCD's rows), with (g, o) = (s / 16, s % 16); its rows of W_r' stay
+//     in registers too, K split over the eight waves.
+// A step t, for the XCD's rows:
+//   1. the codes of h_{t-1} (quantized per vector, eq. 2) and their row
+//      params, from the projection tiles (E4 below); at t = 0 every tile
+//      quantizes h_0 itself;
+//   2. Mult against W_h', R(.) of eq. 1 / eq. 3, + (W_x x + b) (the hoisted
+//      input product, staged through LDS), gates, c and m;
+//   3. E1: per-row min/max of m over the tile's cells, published; every tile
+//      reads all of them and forms the quantizer params of every row of m;
+//   4. E2: each unit tile encodes its own cells of m (eq. 2) and publishes the
+//      codes with their per-row code sums; each projection tile reads the
+//      codes of its rows;
+//   5. Mult against W_r' and R(.) give h_t; E3: per-row min/max of h_t over
+//      the tile's outputs, published; the row group's tiles read them and
+//      form the params of h_t;
+//   6. E4: each projection tile encodes its outputs of h_t and publishes the
+//      codes, code sums and (output group 0) the row's zero point and
+//      recovery factor; they are the layer's quantized output too.
+// Every value a step needs from another tile of the XCD is one of these four
+// hand-offs, each a single round trip through L2.  Exchanged words are 64-bit
+// (step tag << 32 | 32-bit payload) in a double buffer indexed by step
+// parity; a consumer re-reads the words it needs until every tag matches.
+// A buffer half is reused two steps later, and a tile can only reach that
+// point after every tile of its XCD has read the step in between (each hand-off
+// needs the previous one from every tile of the XCD), so nothing is
+// overwritten before it is read.  Every wait is bounded: on expiry a flag in
+// the workspace is raised and every workgroup leaves at its next wait.
+// The arithmetic (quantizer, recovery, gate functions, their operand order)
+// is that of the other recurrent kernels, so the results are bit-identical.
+#include "ql_device.h"
+#include "ql_exchange.h"
+#include "ql_launch.h"
+#include "ql_rec_common.h"
+
+#include <algorithm>
+
+namespace ql {
+
+constexpr int kXrecThreads = 512;
+constexpr int kXrecWaves = kXrecThreads / 64;
+constexpr int kXrecXcds = 8;     // XCDs of the MI355X, each with its own L2
+constexpr int kXrecSlots = 32;   // CUs (workgroups) of one XCD
+constexpr int kXrecGroups = 2;   // projection row groups per XCD
+constexpr int kXrecOuts = 16;    // projection output groups per row group
+constexpr int kXrecOutBlocks = 2;  // 16-output MFMA blocks of a projection tile (pw <= 32)
+constexpr int kXrecSlotBytes = kXrecXcds * 64;  // slot counters after the header
+// batches below this keep the spread layout of k_recurrent
+constexpr int64_t kXrecMinBatch = 16;
+
+struct XrecTiling {
+  int rows;      // batch rows per XCD (the last XCDs may hold fewer)
+  int bX;        // rows padded to MFMA tiles: 16 * NT
+  int u;         // cells per unit tile: 32 * NBW
+  int pw;        // outputs per projection tile: 16 or 32
+  int rg;        // rows per projection row group: bX / 2
+  int ldR, ldH;  // padded widths of the codes of h (K of W_h') and of m (K of W_r')
+  int ksw;       // 64-byte K chunks of W_r' per wave
+  int64_t pwords, xwords;  // exchange words per parity and per XCD
+  // word offsets inside one parity of an XCD's exchange
+  int64_t o_e1, o_e2c, o_e2s, o_e3, o_e4c, o_e4s, o_e4p;
+  size_t off_xc, off_gx, off_cp, off_rp, off_mp, off_pm, off_mcs, off_mc, off_red, off_rpp,
+      off_hp, off_hcs, off_sum, off_par, lds_bytes;
+};
+
+// Quantizer params of a row as the encoder needs them.
+struct XParam {
+  double q;
+  int32_t z;
+  float inv_q;
+};
+
+// A 64-bit exchange word with a plain store (no cache-policy bits): it stays
+// in the L2 of the producer's XCD, where the consumers' device-coherent loads
+// find it.  A wavefront-scope atomic store is exactly that instruction, and
+// the compiler counts it among the outstanding memory operations.
+__device__ __forceinline__ void put_word(uint64_t *p, uint32_t tag, uint32_t v) {
+  __hip_atomic_store(p, ((uint64_t)tag << 32) | (uint64_t)v, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+// Waits until every vector memory operation of the wave has completed (gfx9
+// encoding: only the vector-memory count limited).
+__device__ __forceinline__ void wait_vmcnt0() {
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+}
+
+// Re-reads the words addr(i), i < N, whose bit is set in `need` until each
+// carries `tag`; the payloads go to v.  A word is read again only while its
+// tag has not matched.  False if the wait expired.
+template <int N, class AddrFn>
+__device__ __forceinline__ bool poll_words(uint32_t need, uint32_t tag, uint32_t (&v)[N],
+                                           AddrFn addr, int *flag) {
+  static_assert(N < 32, "one bit per word");
+  uint32_t got = ~need & ((1u << N) - 1);
+  long it = 0;
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (!((got >> i) & 1u)) {
+        const uint64_t w = ld_tagged(addr(i));
+        if ((uint32_t)(w >> 32) == tag) {
+          got |= 1u << i;
+          v[i] = (uint32_t)w;
+        }
+      }
+    if (!__any(got != (1u << N) - 1)) return true;
+    if (wait_expired(flag, it)) return false;
+  }
+}
+
+// The same for wider sets of words whose payloads go to LDS: each payload is
+// stored at dst(i, th) as soon as its tag matches, so no word is held in
+// registers between rounds.  Source and destination addresses are recomputed
+// every round from an opaque thread id th (nothing per word stays live).  The
+// loads of a round are all issued before any of them is examined.
+template <int N, class SrcFn, class DstFn>
+__device__ __forceinline__ bool poll_to_lds(uint32_t need, uint32_t tag, SrcFn src, DstFn dst,
+                                            int *flag) {
+  static_assert(N < 32, "one bit per word");
+  constexpr uint32_t all = (1u << N) - 1;
+  uint32_t got = ~need & all;
+  long it = 0;
+  for (;;) {
+    int th = (int)threadIdx.x;
+    asm volatile("" : "+v"(th));
+    uint64_t w[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) w[i] = ((got >> i) & 1u) ? 0 : ld_tagged(src(i, th));
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (!((got >> i) & 1u) && (uint32_t)(w[i] >> 32) == tag) {
+        got |= 1u << i;
+        *dst(i, th) = (uint32_t)w[i];
+      }
+    if (!__any(got != all)) return true;
+    if (wait_expired(flag, it)) return false;
+  }
+}
+
+// Reductions over aligned groups of 8 or 16 lanes (DPP): every lane of the
+// group ends with the group's result.
+template <class Op>
+__device__ __forceinline__ int red8(int v, Op op) {
+  v = op(v, __builtin_amdgcn_mov_dpp(v, 0xb1, 0xf, 0xf, false));   // quad_perm [1,0,3,2]
+  v = op(v, __builtin_amdgcn_mov_dpp(v, 0x4e, 0xf, 0xf, false));   // quad_perm [2,3,0,1]
+  return op(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xf, 0xf, false));  // row_half_mirror
+}
+template <class Op>
+__device__ __forceinline__ int red16(int v, Op op) {
+  v = red8(v, op);
+  return op(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xf, 0xf, false));  // row_mirror
+}
+// Over aligned groups of W = 16, 32 or 64 lanes.
+template <class Op>
+__device__ __forceinline__ int red_w(int v, int W, Op op) {
+  v = red16(v, op);
+  if (W == 16) return v;
+  const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+  const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+  if (W == 64) return op(op(r0, r1), op(r2, r3));
+  return (threadIdx.x & 32) ? op(r2, r3) : op(r0, r1);
+}
+struct MinI {
+  __device__ int operator()(int a, int b) const { return min(a, b); }
+};
+struct AddI {
+  __device__ int operator()(int a, int b) const { return a + b; }
+};
+
+// NBW: fragment blocks (four cells each) per wave, u = 32 NBW cells a unit
+// tile; NT: 16-row MFMA tiles of the XCD's rows; TP: the launch writes taps.
+template <int NBW, int NT, bool TP>
+__global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTiling tl) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  int8_t *xc = reinterpret_cast<int8_t *>(smem + tl.off_xc);     // [bX][ldR + 16] codes of h_{t-1}
+  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);      // [bX][4][u + 1] W_x x + b
+  ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_cp); // [u][4] gate rows of W_h'
+  RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_rp); // [bX] rows of h_{t-1}
+  XParam *mp = reinterpret_cast<XParam *>(smem + tl.off_mp);     // [bX] quantizer of m_t
+  int *pm = reinterpret_cast<int *>(smem + tl.off_pm);           // [bX][32][2] m min/max parts
+  uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + tl.off_mcs); // [bX][u] codes of m_t (own cells)
+  int8_t *mc = reinterpret_cast<int8_t *>(smem + tl.off_mc);     // [rg][ldH + 16] codes of m_t
+  int32_t *red = reinterpret_cast<int32_t *>(smem + tl.off_red); // [waves][pw][rg] partial sums
+  RowParam *rpp = reinterpret_cast<RowParam *>(smem + tl.off_rpp); // [rg] rows of m_t
+  XParam *hp = reinterpret_cast<XParam *>(smem + tl.off_hp);     // [rg] quantizer of h_t
+  uint8_t *hcs = reinterpret_cast<uint8_t *>(smem + tl.off_hcs); // [rg][pw] codes of h_t
+  int *ssum = reinterpret_cast<int *>(smem + tl.off_sum);         // code sums of polled words
+  int *spar = reinterpret_cast<int *>(smem + tl.off_par);         // [bX][2] z, 1/Q of h_{t-1}
+  __shared__ int s_abort, s_role;
+
+  constexpr int bX = 16 * NT, u = 32 * NBW, uw = u / 4;  // uw: code words of a row per unit tile
+  const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
+  int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
+  unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
+
+  if (threadIdx.x == 0) {
+    const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
+    s_role = -1;
+    s_abort = 0;
+    if (xcc < kXrecXcds) {
+      const unsigned k = __hip_atomic_fetch_add(slots + xcc * 16, 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      if (k < (unsigned)kXrecSlots) s_role = xcc * kXrecSlots + (int)k;
+    }
+  }
+  __syncthreads();
+  if (s_role < 0) return;
+  const int x = s_role / kXrecSlots, s = s_role % kXrecSlots;
+  const int64_t xb0 = (int64_t)x * tl.rows;  // the XCD's first batch row
+  const int nbx = (int)std::min<int64_t>(tl.rows, B - xb0);
+  if (nbx <= 0) return;  // no rows: the whole XCD leaves
+  const int64_t j0 = (int64_t)s * u;
+  const int ldR = tl.ldR, ldH = tl.ldH, ldsX = ldR + 16, ldsM = ldH + 16, pw = tl.pw, rg = tl.rg;
+  const int g = s / kXrecOuts, o = s % kXrecOuts;
+  const int prow0 = g * rg;  // the row group's first row (XCD-local)
+  const int nrg = std::max(0, std::min(rg, nbx - prow0));
+  const int64_t p0 = (int64_t)o * pw;
+
+  uint64_t *X = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes +
+                                             kXrecSlotBytes) + (int64_t)x * tl.xwords;
+  auto E = [&](int64_t t) { return X + (t & 1) * tl.pwords; };
+
+  // ---- prologue: W_h' and W_r' fragments, column params, c_0
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
+  // W_h' block b of wave w (cells 4 (w NBW + b) .. +3): lane row fr is gate
+  // fr & 3 of cell fr >> 2; 16 bytes 16 fq of each 64-byte chunk of K
+  v4i wh[NBW][8];
+#pragma unroll
+  for (int b = 0; b < NBW; ++b) {
+    const int jj = 4 * (wave * NBW + b) + (fr >> 2);
+    const bool ok = j0 + jj < H;
+    const int8_t *src = a.Wh.codes + ((int64_t)(fr & 3) * H + j0 + jj) * a.Wh.ld + 16 * fq;
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      wh[b][c] = ok && c * 64 < ldR ? *reinterpret_cast<const v4i *>(src + c * 64) : v4i{};
+  }
+  // W_r' output block nb of the tile: lane row fr is output p0 + 16 nb + fr;
+  // this wave's K chunks wave * ksw + ks
+  v4i wr[kXrecOutBlocks][4];
+#pragma unroll
+  for (int nb = 0; nb < kXrecOutBlocks; ++nb)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int64_t p = p0 + 16 * nb + fr;
+      const int c = wave * tl.ksw + ks;
+      wr[nb][ks] = v4i{};
+      if (16 * nb < pw && ks < tl.ksw && p < P && c * 64 < ldH)
+        wr[nb][ks] = *reinterpret_cast<const v4i *>(a.Wr.codes + p * a.Wr.ld + c * 64 + 16 * fq);
+    }
+  for (int r = tid; r < 4 * u; r += kXrecThreads) {
+    const int jj = r >> 2, gate = r & 3;
+    const int64_t n = (int64_t)gate * H + std::min<int64_t>(j0 + jj, H - 1);
+    const int64_t blk = n / a.Wh.rows_per_block;
+    ColParam c;
+    c.ztw = a.Wh.zero[blk] + 128;
+    c.sigw = a.Wh.row_sums[n] - 128 * (int32_t)R;
+    c.colterm = (int64_t)c.sigw + R * (int64_t)c.ztw;
+    c.iqw = a.Wh.inv_q[blk];
+    c.pad = 0;
+    cp[r] = c;
+  }
+  // the lane's (cell, row) pairs: block b, row tile tt -> cell
+  // 4 (wave NBW + b) + fq, row 16 tt + fr
+  float cst[NBW][NT];
+#pragma unroll
+  for (int b = 0; b < NBW; ++b)
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+      const int64_t j = j0 + 4 * (wave * NBW + b) + fq, lb = 16 * tt + fr;
+      cst[b][tt] = a.c0 && j < H && lb < nbx ? a.c0[(xb0 + lb) * H + j] : 0.0f;
+    }
+  // the projection lane (row tid / pw, output tid % pw): column params of its
+  // W_r' row
+  int32_t r_ztw = 0, r_sigw = 0;
+  int64_t r_colterm = 0;
+  float r_iqw = 0.0f;
+  {
+    const int64_t pc = std::min<int64_t>(p0 + tid % pw, P - 1);
+    const int64_t blk = pc / a.Wr.rows_per_block;
+    r_ztw = a.Wr.zero[blk] + 128;
+    r_sigw = a.Wr.row_sums[pc] - 128 * (int32_t)H;
+    r_colterm = (int64_t)r_sigw + H * (int64_t)r_ztw;
+    r_iqw = a.Wr.inv_q[blk];
+  }
+  __syncthreads();
+
+  for (int64_t t = 0;; ++t) {
+    // per-thread indices re-derived every step from an opaque thread id, so
+    // that the compiler keeps no per-thread offsets alive across the loop
+    int tid = (int)threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
+    auto jjOf = [&](int b) { return 4 * (wave * NBW + b) + fq; };
+    auto rowOf = [&](int tt) { return 16 * tt + fr; };
+    const int lr = tid / pw, pp = tid % pw;
+    const int64_t pout = p0 + pp;
+    const bool plane = lr < rg;
+    // ---- W_x x + b of step t straight into LDS, [row][gate][u] with rows
+    // 4u + 4 floats apart: one 16-byte load per lane, one row (4 gates x u
+    // cells) per wave instruction (u = 32: the first 32 lanes)
+    if (t < T && (u == 64 || lane < 32)) {
+      const int gate = lane / uw, c4 = lane % uw;
+      const int64_t jc = j0 + 4 * c4 < H ? j0 + 4 * c4 : 0;  // past H: any cell in bounds
+      for (int row = wave; row < nbx; row += kXrecWaves)
+        __builtin_amdgcn_global_load_lds(a.gx + ((t * B + xb0 + row) * 4 * H + gate * H + jc),
+                                         (lds_ptr)(gxs + row * (4 * u + 4)), 16, 0, 0);
+    }
+    // ---- 1. the codes of h_{t-1} and their row params
+    if (t == 0) {
+      if (!quant_tile<8, 2, kSrcPlain>(nbx, bX, R, 0u, (int)R, xc, ldsX, ldR, flag, rp,
+                                       [&](int lb) -> const void * {
+                                         return a.h0 ? a.h0 + (xb0 + lb) * R : nullptr;
+                                       }))
+        s_abort = 1;
+    } else {
+      // E4 of step t - 1: code words into xc; per (row, output group) the code
+      // sum, and the row's z and 1/Q, into LDS
+      const uint64_t *e4 = E(t - 1);
+      const int cwr = ldR / 4;    // code words of a row
+      constexpr int CW = bX / 4;  // >= bX * ldR / 4 / threads for ldR <= 512
+      uint32_t need = 0;
+#pragma unroll
+      for (int k = 0; k < CW; ++k)
+        if (k * kXrecThreads + tid < nbx * cwr) need |= 1u << k;
+      if (tid < nbx * kXrecOuts) need |= 1u << CW;  // sum of (row tid / 16, group tid % 16)
+      if (tid < nbx * 2) need |= 1u << (CW + 1);    // z (even tid) or 1/Q of row tid / 2
+      if (!poll_to_lds<CW + 2>(
+              need, (uint32_t)t,
+              [&](int i, int th) -> const uint64_t * {
+                if (i < CW) {
+                  const int idx = i * kXrecThreads + th, row = idx / cwr, wd = idx % cwr;
+                  return e4 + tl.o_e4c + (int64_t)row * (kXrecOuts * pw / 4) + wd;
+                }
+                return e4 + (i == CW ? tl.o_e4s : tl.o_e4p) + th;
+              },
+              [&](int i, int th) -> uint32_t * {
+                if (i < CW) {
+                  const int idx = i * kXrecThreads + th, row = idx / cwr, wd = idx % cwr;
+                  return reinterpret_cast<uint32_t *>(xc + row * ldsX + 4 * wd);
+                }
+                return reinterpret_cast<uint32_t *>(i == CW ? ssum + th : spar + th);
+              },
+              flag))
+        s_abort = 1;
+    }
+    wait_vmcnt0();  // the direct loads of W_x x + b have landed in LDS
+    __syncthreads();
+    if (s_abort) return;
+    if (t > 0 && tid < nbx) {
+      // the row's code sum over the output groups, in group order
+      int total = 0;
+      for (int og = 0; og < kXrecOuts; ++og) total += ssum[tid * kXrecOuts + og];
+      rp[tid] = row_param(spar[2 * tid], __int_as_float(spar[2 * tid + 1]), total, (int)R);
+      if (s == 0) a.out_sums[(t - 1) * B + xb0 + tid] = total;
+    }
+    if (t == T) break;  // step T only collects the last step's code sums
+
+    // ---- 2. Mult against the resident W_h' fragments: block b, row tile tt
+    v4i acc[NBW][NT];
+#pragma unroll
+    for (int b = 0; b < NBW; ++b)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) acc[b][tt] = v4i{};
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      if (c * 64 >= ldR) break;
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const v4i bx = *reinterpret_cast<const v4i *>(xc + rowOf(tt) * ldsX + c * 64 + 16 * fq);
+#pragma unroll
+        for (int b = 0; b < NBW; ++b)
+          acc[b][tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wh[b][c], bx, acc[b][tt], 0, 0, 0);
+      }
+    }
+    // the MFMA results are read by ordinary instructions below: at least 19
+    // wait states after the last pass, which the hardware does not check
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acc[0][0]));
+    __syncthreads();  // the row params of h_{t-1} are in LDS
+
+    // ---- recover (eq. 1 / eq. 3), + W_x x + b, gates, c and m
+    float mv[NBW][NT];
+#pragma unroll
+    for (int b = 0; b < NBW; ++b)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const int jj = jjOf(b), lb = rowOf(tt);
+        const int64_t j = j0 + jj, brow = xb0 + lb;
+        const RowParam r = rp[lb];
+        float gv[4];
+#pragma unroll
+        for (int gate = 0; gate < 4; ++gate) {
+          const ColParam c = cp[jj * 4 + gate];
+          const int32_t sv = acc[b][tt][gate];
+          const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
+          const float av = gxs[lb * (4 * u + 4) + gate * u + jj] + yh;
+          const float sg = sigmoid_cw(gate == 2 ? 2.0f * av : av);
+          gv[gate] = gate == 2 ? 2.0f * sg - 1.0f : sg;
+          if (TP && a.acc_h && j < H && lb < nbx)
+            a.acc_h[(t * B + brow) * 4 * H + gate * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
+        }
+        const float cn = (gv[1] * cst[b][tt]) + (gv[0] * gv[2]);
+        cst[b][tt] = cn;
+        const float m = gv[3] * tanh_cw(cn);
+        mv[b][tt] = m;
+        if (j < H && lb < nbx) {
+          if (TP) {
+            if (a.tap_gates) {
+              float *gp = a.tap_gates + (t * B + brow) * 4 * H + j;
+              gp[0] = gv[0], gp[H] = gv[1], gp[2 * H] = gv[2], gp[3 * H] = gv[3];
+            }
+            if (a.tap_c) a.tap_c[(t * B + brow) * H + j] = cn;
+            if (a.tap_m) a.tap_m[(t * B + brow) * H + j] = m;
+          }
+          if (t == T - 1 && a.cT) a.cT[brow * H + j] = cn;
+        }
+      }
+
+    // ---- 3. E1: min/max of m per row over the tile's cells
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+      int lo = 0x7fffffff, hi = 0x7fffffff;
+#pragma unroll
+      for (int b = 0; b < NBW; ++b)
+        if (j0 + jjOf(b) < H) {
+          const int key = float_key(mv[b][tt]);
+          lo = min(lo, key);
+          hi = min(hi, ~key);
+        }
+      int *d = pm + (rowOf(tt) * 32 + wave * 4 + fq) * 2;
+      d[0] = lo;
+      d[1] = hi;
+    }
+    __syncthreads();
+    uint64_t *e = E(t);
+    const uint32_t tag = (uint32_t)(t + 1);
+    {
+      // 16 lanes per row, two of the row's 32 (wave, lane group) parts each
+      const int row = tid >> 4, j = tid & 15;
+      int lo = 0x7fffffff, hi = 0x7fffffff;
+      if (row < bX) {
+        const int *q = pm + (row * 32 + 2 * j) * 2;
+        lo = min(q[0], q[2]);
+        hi = min(q[1], q[3]);
+      }
+      lo = red16(lo, MinI{});
+      hi = red16(hi, MinI{});
+      if (row < nbx && j == 0) {
+        put_word(e + tl.o_e1 + (row * kXrecSlots + s) * 2, tag, (uint32_t)lo);
+        put_word(e + tl.o_e1 + (row * kXrecSlots + s) * 2 + 1, tag, (uint32_t)hi);
+      }
+    }
+    // every row's params from the 32 tiles' parts: 16 lanes per row, two
+    // tiles' (min, max) words each
+    {
+      const int row = tid >> 4, j = tid & 15;
+      uint32_t v[4];
+      const uint32_t need = row < nbx ? 0xfu : 0u;
+      const bool ok = poll_words<4>(need, tag, v, [&](int i) -> const uint64_t * {
+        return e + tl.o_e1 + (row * kXrecSlots + 2 * j + (i >> 1)) * 2 + (i & 1);
+      }, flag);
+      if (!ok) s_abort = 1;
+      int lo = need ? min((int)v[0], (int)v[2]) : 0x7fffffff;
+      int hi = need ? min((int)v[1], (int)v[3]) : 0x7fffffff;
+      lo = red16(lo, MinI{});
+      hi = red16(hi, MinI{});
+      if (row < nbx && j == 0 && ok) {
+        const QParams prm = make_qparams(key_float(lo), key_float(~hi));
+        XParam xp;
+        xp.q = prm.q;
+        xp.z = prm.z;
+        xp.inv_q = prm.inv_q;
+        mp[row] = xp;
+      }
+    }
+    __syncthreads();
+    if (s_abort) return;
+
+    // ---- 4. E2: the tile's cells of m encoded (eq. 2), with per-row code sums
+#pragma unroll
+    for (int b = 0; b < NBW; ++b)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const int jj = jjOf(b), lb = rowOf(tt);
+        if (lb < nbx) {
+          int code = 128;  // device byte 0: cells past H add nothing to a product
+          if (j0 + jj < H) code = encode(mv[b][tt], mp[lb].q, mp[lb].z);
+          mcs[lb * u + jj] = (uint8_t)(code ^ 0x80);
+        }
+      }
+    __syncthreads();
+    {
+      // uw lanes per row (8 or 16, aligned), one word of four codes each
+      const int row = tid / uw, wd = tid % uw;
+      int sum = 0;
+      if (row < nbx) {
+        const uint32_t word = *reinterpret_cast<const uint32_t *>(mcs + row * u + 4 * wd);
+        put_word(e + tl.o_e2c + (int64_t)row * (kXrecSlots * uw) + s * uw + wd, tag, word);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (j0 + 4 * wd + k < H) sum += (int)((word >> (8 * k)) & 0xffu) ^ 0x80;
+      }
+      sum = uw == 16 ? red16(sum, AddI{}) : red8(sum, AddI{});
+      if (row < nbx && wd == 0) put_word(e + tl.o_e2s + row * kXrecSlots + s, tag, (uint32_t)sum);
+    }
+
+    // ---- 5. the projection tile: the codes of m_t of its rows, Mult against
+    // W_r', recovery of h_t
+    float hv = 0.0f;
+    if (nrg > 0) {
+      const int cwm = ldH / 4;  // code words of a row of m
+      constexpr int CW = bX / kXrecGroups;  // >= rg * ldH / 4 / threads for ldH <= 2048
+      uint32_t need = 0;
+#pragma unroll
+      for (int k = 0; k < CW; ++k)
+        if (k * kXrecThreads + tid < nrg * cwm) need |= 1u << k;
+      if (tid < nrg * kXrecSlots) need |= 1u << CW;  // sum of (row tid / 32, tile tid % 32)
+      if (!poll_to_lds<CW + 1>(
+              need, tag,
+              [&](int i, int th) -> const uint64_t * {
+                if (i < CW) {
+                  const int idx = i * kXrecThreads + th, row = idx / cwm, wd = idx % cwm;
+                  return e + tl.o_e2c + (int64_t)(prow0 + row) * (kXrecSlots * uw) + wd;
+                }
+                return e + tl.o_e2s + prow0 * kXrecSlots + th;
+              },
+              [&](int i, int th) -> uint32_t * {
+                if (i < CW) {
+                  const int idx = i * kXrecThreads + th, row = idx / cwm, wd = idx % cwm;
+                  return reinterpret_cast<uint32_t *>(mc + row * ldsM + 4 * wd);
+                }
+                return reinterpret_cast<uint32_t *>(ssum + th);
+              },
+              flag))
+        s_abort = 1;
+      __syncthreads();
+      if (s_abort) return;
+      if (tid < nrg) {
+        int sum = 0;
+        for (int k = 0; k < kXrecSlots; ++k) sum += ssum[tid * kXrecSlots + k];
+        const XParam xp = mp[prow0 + tid];
+        rpp[tid] = row_param(xp.z, xp.inv_q, sum, (int)H);
+      }
+      __syncthreads();
+      // this wave's K chunks against every output block; rows past the group
+      // read zeros
+      v4i accp[kXrecOutBlocks] = {v4i{}, v4i{}};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c = wave * tl.ksw + ks;
+        if (ks >= tl.ksw || c * 64 >= ldH) break;
+        const v4i bm = fr < nrg ? *reinterpret_cast<const v4i *>(mc + fr * ldsM + c * 64 + 16 * fq)
+                                : v4i{};
+#pragma unroll
+        for (int nb = 0; nb < kXrecOutBlocks; ++nb)
+          if (16 * nb < pw) accp[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wr[nb][ks], bm, accp[nb], 0, 0, 0);
+      }
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(accp[0]));
+      if (fr < rg)
+#pragma unroll
+        for (int nb = 0; nb < kXrecOutBlocks; ++nb)
+          if (16 * nb < pw)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              red[(wave * pw + 16 * nb + 4 * fq + r) * rg + fr] = accp[nb][r];
+      __syncthreads();
+      const bool valid = plane && lr < nrg && pout < P;
+      if (plane) {
+        int32_t sv = 0;
+        for (int w = 0; w < kXrecWaves; ++w) sv += red[(w * pw + pp) * rg + lr];
+        const RowParam r = rpp[lr < nrg ? lr : 0];
+        hv = recover(sv, r_colterm, r_ztw, r.ztx, r.sigx, r_iqw, r.iqx);
+        if (valid) {
+          const int64_t brow = xb0 + prow0 + lr;
+          a.h[(t * B + brow) * P + pout] = hv;
+          if (t == T - 1 && a.hT) a.hT[brow * P + pout] = hv;
+          if (TP && a.acc_r) a.acc_r[(t * B + brow) * P + pout] = acc_u8(sv, r_sigw, r.sigx, H);
+        }
+      }
+      // E3: min/max of h_t per row over the tile's outputs
+      int lo = 0x7fffffff, hi = 0x7fffffff;
+      if (valid) {
+        const int key = float_key(hv);
+        lo = key;
+        hi = ~key;
+      }
+      lo = red_w(lo, pw, MinI{});
+      hi = red_w(hi, pw, MinI{});
+      if (plane && lr < nrg && pp == 0) {
+        put_word(e + tl.o_e3 + ((prow0 + lr) * kXrecOuts + o) * 2, tag, (uint32_t)lo);
+        put_word(e + tl.o_e3 + ((prow0 + lr) * kXrecOuts + o) * 2 + 1, tag, (uint32_t)hi);
+      }
+      // ---- 6. the row group's params of h_t (16 lanes per row, one output
+      // group's words each), then E4
+      {
+        const int row = tid >> 4, og = tid & 15;
+        uint32_t w2[2];
+        const uint32_t need3 = row < nrg ? 3u : 0u;
+        const bool ok3 = poll_words<2>(need3, tag, w2, [&](int i) -> const uint64_t * {
+          return e + tl.o_e3 + ((prow0 + row) * kXrecOuts + og) * 2 + i;
+        }, flag);
+        if (!ok3) s_abort = 1;
+        const int l2 = red16(need3 ? (int)w2[0] : 0x7fffffff, MinI{});
+        const int h2 = red16(need3 ? (int)w2[1] : 0x7fffffff, MinI{});
+        if (row < nrg && og == 0 && ok3) {
+          const QParams prm = make_qparams(key_float(l2), key_float(~h2));
+          XParam xp;
+          xp.q = prm.q;
+          xp.z = prm.z;
+          xp.inv_q = prm.inv_q;
+          hp[row] = xp;
+        }
+      }
+      __syncthreads();
+      if (s_abort) return;
+      int code = 0;
+      if (plane && lr < nrg) {
+        const XParam xp = hp[lr];
+        code = valid ? encode(hv, xp.q, xp.z) : 128;  // outputs past P: device byte 0
+        hcs[lr * pw + pp] = (uint8_t)(code ^ 0x80);
+        const int64_t orow = t * B + xb0 + prow0 + lr;
+        if (TP && a.tap_codes && valid) a.tap_codes[orow * R + pout] = (int8_t)(code ^ 0x80);
+        if (pp == 0 && o == 0) {
+          a.out_zero[orow] = xp.z;
+          a.out_inv_q[orow] = xp.inv_q;
+          if (TP && a.tap_zero) a.tap_zero[orow] = xp.z;
+          if (TP && a.tap_inv_q) a.tap_inv_q[orow] = xp.inv_q;
+        }
+      }
+      const int csum = red_w(valid ? code : 0, pw, AddI{});
+      if (plane && lr < nrg && pp == 0) {
+        const int row = prow0 + lr;
+        put_word(e + tl.o_e4s + row * kXrecOuts + o, tag, (uint32_t)csum);
+        if (o == 0) {
+          put_word(e + tl.o_e4p + row * 2, tag, (uint32_t)hp[lr].z);
+          put_word(e + tl.o_e4p + row * 2 + 1, tag, __float_as_uint(hp[lr].inv_q));
+        }
+      }
+      __syncthreads();
+      {
+        const int pw4 = pw / 4, row = tid / pw4, wd = tid % pw4;
+        if (row < nrg) {
+          const uint32_t word = *reinterpret_cast<const uint32_t *>(hcs + row * pw + 4 * wd);
+          put_word(e + tl.o_e4c + (int64_t)(prow0 + row) * (kXrecOuts * pw4) + o * pw4 + wd, tag, word);
+          const int64_t orow = t * B + xb0 + prow0 + row, k = p0 + 4 * wd;
+          if (k < a.ld_out) *reinterpret_cast<uint32_t *>(a.out_codes + orow * a.ld_out + k) = word;
+        }
+        // the output rows' padding past the last group (wider layouts only)
+        if (o == kXrecOuts - 1)
+          for (int idx = tid; idx < nrg * (int)((a.ld_out - kXrecOuts * pw) / 4); idx += kXrecThreads) {
+            const int nw = (int)((a.ld_out - kXrecOuts * pw) / 4), row = idx / nw, wd = idx % nw;
+            *reinterpret_cast<uint32_t *>(a.out_codes + (t * B + xb0 + prow0 + row) * a.ld_out +
+                                          kXrecOuts * pw + 4 * wd) = 0u;
+          }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ host side
+// One parity of an XCD's exchange, in 64-bit words:
+//   E1  [rows][32 tiles][2]   min / max keys of m_t
+//   E2c [rows][32 tiles][u/4] codes of m_t, E2s [rows][32 tiles] their sums
+//   E3  [rows][16 groups][2]  min / max keys of h_t
+//   E4c [rows][4 pw]          codes of h_t, E4s [rows][16 groups] their sums,
+//   E4p [rows][2]             zero point and recovery factor of h_t
+static bool plan_xrec(const RecurrentArgs &a, int cus, int lds_max, XrecTiling *out) {
+  const int64_t B = a.B, H = a.H, P = a.P;
+  if (P <= 0 || a.R != P || cus != kXrecXcds * kXrecSlots) return false;
+  if (B < kXrecMinBatch || B > kXrecXcds * 32 || H > 2048 || H % 4 || P > 512) return false;
+  XrecTiling tl{};
+  tl.rows = (int)((B + kXrecXcds - 1) / kXrecXcds);
+  tl.bX = tl.rows <= 16 ? 16 : 32;
+  tl.u = H <= 1024 ? 32 : 64;
+  tl.pw = P <= 256 ? 16 : 32;
+  tl.rg = tl.bX / kXrecGroups;
+  tl.ldR = (int)round_up(P, 64);
+  tl.ldH = (int)round_up(H, 64);
+  tl.ksw = (tl.ldH / 64 + kXrecWaves - 1) / kXrecWaves;
+  if (tl.ksw > 4 || tl.u * kXrecSlots < H) return false;
+  if (a.Wh.ld < tl.ldR || a.Wr.ld < tl.ldH) return false;
+  if (a.ld_out < tl.ldR || a.ld_out % 4) return false;
+  const int64_t rows = tl.bX, uw = tl.u / 4;
+  int64_t w = 0;
+  tl.o_e1 = w;
+  w += rows * kXrecSlots * 2;
+  tl.o_e2c = w;
+  w += rows * kXrecSlots * uw;
+  tl.o_e2s = w;
+  w += rows * kXrecSlots;
+  tl.o_e3 = w;
+  w += rows * kXrecOuts * 2;
+  tl.o_e4c = w;
+  w += rows * kXrecOuts * tl.pw / 4;
+  tl.o_e4s = w;
+  w += rows * kXrecOuts;
+  tl.o_e4p = w;
+  w += rows * 2;
+  tl.pwords = round_up(w, 32);  // parities 256 bytes apart
+  tl.xwords = 2 * tl.pwords;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 16);
+    return at;
+  };
+  tl.off_xc = take((size_t)tl.bX * (tl.ldR + 16));
+  tl.off_gx = take((size_t)tl.bX * (4 * tl.u + 4) * 4);
+  tl.off_cp = take((size_t)4 * tl.u * sizeof(ColParam));
+  tl.off_rp = take((size_t)tl.bX * sizeof(RowParam));
+  tl.off_mp = take((size_t)tl.bX * sizeof(XParam));
+  tl.off_pm = take((size_t)tl.bX * 32 * 2 * 4);
+  tl.off_mcs = take((size_t)tl.bX * tl.u);
+  tl.off_mc = take((size_t)tl.rg * (tl.ldH + 16));
+  tl.off_red = take((size_t)kXrecWaves * tl.pw * tl.rg * 4);
+  tl.off_rpp = take((size_t)tl.rg * sizeof(RowParam));
+  tl.off_hp = take((size_t)tl.rg * sizeof(XParam));
+  tl.off_hcs = take((size_t)tl.rg * tl.pw);
+  tl.off_sum = take((size_t)std::max(tl.bX * kXrecOuts, tl.rg * kXrecSlots) * 4);
+  tl.off_par = take((size_t)tl.bX * 2 * 4);
+  tl.lds_bytes = off;
+  if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
+  *out = tl;
+  return true;
+}
+
+size_t xrec_ws(int64_t B, int64_t H, int64_t P) {
+  if (P <= 0) return 0;
+  const int64_t rows = 32, uw = 16, pw = 32;  // the largest tiling
+  const int64_t w = rows * kXrecSlots * (2 + uw + 1) + rows * kXrecOuts * 3 + rows * kXrecOuts * pw / 4 + rows * 2;
+  return kHeaderBytes + kXrecSlotBytes + (size_t)kXrecXcds * 2 * round_up(w, 32) * 8;
+}
+
+using XrecKernel = void (*)(RecurrentArgs, XrecTiling);
+
+static XrecKernel pick_xrec(const XrecTiling &tl, bool taps) {
+  const int nbw = tl.u / 32, nt = tl.bX / 16;
+  if (taps) {
+    if (nbw == 1) return nt == 1 ? k_xrec<1, 1, true> : k_xrec<1, 2, true>;
+    return nt == 1 ? k_xrec<2, 1, true> : k_xrec<2, 2, true>;
+  }
+  if (nbw == 1) return nt == 1 ? k_xrec<1, 1, false> : k_xrec<1, 2, false>;
+  return nt == 1 ? k_xrec<2, 1, false> : k_xrec<2, 2, false>;
+}
+
+bool xrec_applies(const RecurrentArgs &a, int cus, int lds_max) {
+  XrecTiling tl;
+  return plan_xrec(a, cus, lds_max, &tl);
+}
+
+int recurrent_layout(const RecurrentArgs &a) {
+  int dev = 0, cus = 0, lds_max = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return xrec_applies(a, cus, lds_max) ? 1 : 0;
+}
+
+hipError_t launch_xrec(const RecurrentArgs &a, int cus, int lds_max, hipStream_t s, bool *done) {
+  *done = false;
+  XrecTiling tl;
+  if (!plan_xrec(a, cus, lds_max, &tl)) return hipSuccess;
+  const bool taps = a.acc_h || a.acc_r || a.tap_codes || a.tap_zero || a.tap_inv_q ||
+                    a.tap_gates || a.tap_c || a.tap_m;
+  XrecKernel kern = pick_xrec(tl, taps);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)tl.lds_bytes);
+  if (e != hipSuccess) return e;
+  int per_cu = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kXrecThreads, tl.lds_bytes);
+  if (e != hipSuccess) return e;
+  if (per_cu < 1) return hipSuccess;  // leave it to the spread layout
+  e = clear_exchange(a.ws, kXrecSlotBytes / 8 + kXrecXcds * tl.xwords, s);
+  if (e != hipSuccess) return e;
+  RecurrentArgs args = a;
+  void *kargs[] = {&args, &tl};
+  e = hipLaunchCooperativeKernel(reinterpret_cast<void *>(kern), dim3(cus), dim3(kXrecThreads),
+                                 kargs, (unsigned)tl.lds_bytes, s);
+  if (e == hipSuccess) *done = true;
+  return e;
+}
+
+hipError_t set_wait_bound_xrec(int polls) { return set_wait_bound_here(polls); }
+
+}  // namespace ql

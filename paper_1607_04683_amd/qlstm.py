@@ -36,7 +36,7 @@ EXPORTS = [
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
     "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
     "ql_acoustic_model_forward_stream_noalloc", "ql_train_step_workspace", "ql_train_step",
-    "ql_debug_set_wait_bound",
+    "ql_debug_set_wait_bound", "ql_debug_recurrence_layout",
 ]
 
 
@@ -141,6 +141,8 @@ def load(path: str = LIB_PATH):
     L.ql_workspace_status.argtypes = [vp, vp]
     L.ql_gate_fn.argtypes = [i32, vp, vp, i64, vp]
     L.ql_debug_set_wait_bound.argtypes = [i32]
+    L.ql_debug_recurrence_layout.argtypes = [C.POINTER(CLayer), i64]
+    L.ql_debug_recurrence_layout.restype = i32
     L.ql_f32_matmul.argtypes = [vp, i64, i64, vp, i64, vp, vp, vp]
     L.ql_quantize_activations.argtypes = [vp, i64, i64, C.POINTER(CQAct), vp]
     L.ql_lstm_stack_workspace.argtypes = [C.POINTER(CLayer), i32, i64, i64]
@@ -762,6 +764,13 @@ def stack_layers_per_launch(M: Model, T: int, B: int) -> int:
     forward then runs one layer per launch)."""
     arr = (CLayer * len(M.layers))(*[L.cstruct() for L in M.layers])
     return int(load().ql_lstm_stack_layers_per_launch(arr, len(M.layers), T, B))
+
+
+def recurrence_layout(L: Layer, B: int) -> int:
+    """1 when L's recurrence at batch B runs with each XCD holding an eighth of
+    the batch (layers with a projection on the whole chip), else 0."""
+    c = L.cstruct()
+    return int(load().ql_debug_recurrence_layout(C.byref(c), B))
 
 
 # ------------------------------------------- quantization-aware training step

@@ -6,7 +6,7 @@ next wait (so the launch drains and the kernel ends normally), and the call
 reports QL_ETIMEOUT.  The next call with the default bound gives the same
 results, bit for bit, as a call made before.  Covers each persistent kernel:
 the batched and the one-row layer wavefronts, the one-layer recurrence with a
-projection, the fp32 recurrence, the training step's backward recurrence and
+projection (XCD-local and spread layouts), the fp32 recurrence, the training step's backward recurrence and
 the allocation-free entry point."""
 import numpy as np
 import pytest
@@ -61,10 +61,13 @@ def test_layer_wavefront_times_out_and_recovers(ql, B):
     assert torch.equal(ql.acoustic_model_forward(M, x)["post"], ref)
 
 
-def test_projection_recurrence_times_out_and_recovers(ql):
+@pytest.mark.parametrize("H,B,layout", [(64, 20, 1), (42, 20, 0), (64, 5, 0)])
+def test_projection_recurrence_times_out_and_recovers(ql, H, B, layout):
+    """The XCD-local layout (batch 20) and the spread one (42 cells; batch 5)."""
     from paper_1607_04683_amd.workloads import random_model
-    L = ql.quantize_layer(random_model(24, 64, 1, proj=24, seed=3)["layers"][0])
-    x = torch.randn(9, 20, 24, device="cuda")
+    L = ql.quantize_layer(random_model(24, H, 1, proj=24, seed=3)["layers"][0])
+    assert ql.recurrence_layout(L, B) == layout
+    x = torch.randn(9, B, 24, device="cuda")
     ref = ql.lstm_layer_forward(L, x)["h"]
     _times_out(ql, lambda: ql.lstm_layer_forward(L, x))
     assert torch.equal(ql.lstm_layer_forward(L, x)["h"], ref)
