@@ -29,10 +29,10 @@ constexpr int kWave = 64;
 // one fused multiply-add; the result scaled by 2^n through its exponent
 // field.  x is clamped to [-87, 87] so results and 1 / (1 + e^x) are normal.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float exp_cw(float x) {
-  if (x != x) return x;
-  x = x > 87.0f ? 87.0f : x;
-  x = x < -87.0f ? -87.0f : x;
+__device__ __forceinline__ float exp_cw(float x_in) {
+  // the clamp as one median-of-three; a NaN input is passed through by the
+  // select at the end (no branch)
+  const float x = __builtin_amdgcn_fmed3f(x_in, -87.0f, 87.0f);
   const float n = floorf(__builtin_fmaf(x, 1.44269504088896340736f, 0.5f));
   float r = __builtin_fmaf(-n, 0.693145751953125f, x);
   r = __builtin_fmaf(-n, 1.42860682030941723212e-6f, r);
@@ -45,7 +45,7 @@ __device__ __forceinline__ float exp_cw(float x) {
   p = __builtin_fmaf(p, r, 1.0f);
   p = __builtin_fmaf(p, r, 1.0f);
   const float scale = __int_as_float(((int)n + 127) << 23);
-  return p * scale;
+  return x_in != x_in ? x_in : p * scale;
 }
 // 1 / d for d in [1, 2^126) (every denominator 1 + e^-x of the gate
 // functions), correctly rounded: v_rcp_f32 refined by two Newton steps whose

@@ -51,6 +51,7 @@
 #include "ql_rec_common.h"
 
 #include <algorithm>
+#include <cstddef>
 
 namespace ql {
 
@@ -77,7 +78,7 @@ struct XrecTiling {
   // word offsets inside one parity of an XCD's exchange
   int64_t o_e1, o_e2c, o_e2s, o_e3, o_e4c, o_e4s, o_e4p;
   size_t off_xc, off_gx, off_cp, off_rp, off_mp, off_pm, off_mcs, off_mc, off_red, off_rpp,
-      off_hp, off_hcs, off_sum, off_par, lds_bytes;
+      off_hp, off_hcs, off_sum, off_par, off_cf, lds_bytes;
 };
 
 // Quantizer params of a row as the encoder needs them.
@@ -189,32 +190,67 @@ struct AddI {
 
 // NBW: fragment blocks (four cells each) per wave, u = 32 NBW cells a unit
 // tile; NT: 16-row MFMA tiles of the XCD's rows; TP: the launch writes taps.
-template <int NBW, int NT, bool TP>
-__global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTiling tl) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  int8_t *xc = reinterpret_cast<int8_t *>(smem + tl.off_xc);     // [bX][ldR + 16] codes of h_{t-1}
-  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);      // [bX][4][u + 1] W_x x + b
-  ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_cp); // [u][4] gate rows of W_h'
-  RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_rp); // [bX] rows of h_{t-1}
-  XParam *mp = reinterpret_cast<XParam *>(smem + tl.off_mp);     // [bX] quantizer of m_t
-  int *pm = reinterpret_cast<int *>(smem + tl.off_pm);           // [bX][32][2] m min/max parts
-  uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + tl.off_mcs); // [bX][u] codes of m_t (own cells)
-  int8_t *mc = reinterpret_cast<int8_t *>(smem + tl.off_mc);     // [rg][ldH + 16] codes of m_t
-  int32_t *red = reinterpret_cast<int32_t *>(smem + tl.off_red); // [waves][pw][rg] partial sums
-  RowParam *rpp = reinterpret_cast<RowParam *>(smem + tl.off_rpp); // [rg] rows of m_t
-  XParam *hp = reinterpret_cast<XParam *>(smem + tl.off_hp);     // [rg] quantizer of h_t
-  uint8_t *hcs = reinterpret_cast<uint8_t *>(smem + tl.off_hcs); // [rg][pw] codes of h_t
-  int *ssum = reinterpret_cast<int *>(smem + tl.off_sum);         // code sums of polled words
-  int *spar = reinterpret_cast<int *>(smem + tl.off_par);         // [bX][2] z, 1/Q of h_{t-1}
-  __shared__ int s_abort, s_role;
+// Everything a workgroup derives from the launch arguments and its role:
+// LDS arrays, sizes, its rows, cells, projection tile and exchange area.  The
+// kernel states it once for the prologue and again at the top of every step,
+// reading the arguments through a pointer the compiler cannot follow across
+// steps, so none of these values has to stay live across the loop (they are
+// cheap scalar work; kept live, they overflow the scalar registers).
+#define XREC_DERIVED(a, tl, role)                                                              \
+  int8_t *xc = reinterpret_cast<int8_t *>(smem + tl.off_xc);      /* [bX][ldR+16] h codes */ \
+  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);       /* [bX][4][u] W_x x + b */ \
+  ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_cp);  /* [u][4] W_h' rows     */ \
+  int4 *ctm = reinterpret_cast<int4 *>(smem + tl.off_cf);         /* [u] colterm, 4 gates */ \
+  int4 *czt = ctm + tl.u;                                         /* [u] shifted zeros    */ \
+  float4 *ciq = reinterpret_cast<float4 *>(czt + tl.u);           /* [u] 1/Q              */ \
+  RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_rp);  /* [bX] rows of h_{t-1} */ \
+  XParam *mp = reinterpret_cast<XParam *>(smem + tl.off_mp);      /* [bX] quantizer of m  */ \
+  int *pm = reinterpret_cast<int *>(smem + tl.off_pm);            /* [bX][32][2] m parts  */ \
+  uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + tl.off_mcs);  /* [bX][u] own m codes  */ \
+  int8_t *mc = reinterpret_cast<int8_t *>(smem + tl.off_mc);      /* [rg][ldH+16] m codes */ \
+  int32_t *red = reinterpret_cast<int32_t *>(smem + tl.off_red);  /* [waves][pw][rg] sums */ \
+  RowParam *rpp = reinterpret_cast<RowParam *>(smem + tl.off_rpp); /* [rg] rows of m      */ \
+  XParam *hp = reinterpret_cast<XParam *>(smem + tl.off_hp);      /* [rg] quantizer of h  */ \
+  uint8_t *hcs = reinterpret_cast<uint8_t *>(smem + tl.off_hcs);  /* [rg][pw] h codes     */ \
+  int *ssum = reinterpret_cast<int *>(smem + tl.off_sum);         /* polled code sums     */ \
+  int *spar = reinterpret_cast<int *>(smem + tl.off_par);         /* [bX][2] z, 1/Q of h  */ \
+  const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;                                   \
+  int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;                                        \
+  const int x = (role) / kXrecSlots, s = (role) % kXrecSlots;                                  \
+  const int64_t xb0 = (int64_t)x * tl.rows; /* the XCD's first batch row */                    \
+  const int nbx = (int)std::min<int64_t>((int64_t)tl.rows, B - xb0);                                 \
+  const int64_t j0 = (int64_t)s * u;                                                           \
+  const int ldR = tl.ldR, ldH = tl.ldH, ldsX = ldR + 16, ldsM = ldH + 16, pw = tl.pw;          \
+  const int rg = tl.rg;                                                                        \
+  const int g = s / kXrecOuts, o = s % kXrecOuts;                                              \
+  const int prow0 = g * rg; /* the row group's first row (XCD-local) */                        \
+  const int nrg = std::max(0, std::min(rg, nbx - prow0));                                      \
+  const int64_t p0 = (int64_t)o * pw;                                                          \
+  uint64_t *X = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes +        \
+                                             kXrecSlotBytes) + (int64_t)x * tl.xwords;         \
+  auto E = [&](int64_t tt_) { return X + (tt_ & 1) * tl.pwords; };                             \
+  (void)xc, (void)gxs, (void)cp, (void)ctm, (void)czt, (void)ciq, (void)rp, (void)mp, (void)pm, \
+      (void)mcs, (void)mc, (void)red, (void)rpp, (void)hp, (void)hcs, (void)ssum, (void)spar,   \
+      (void)T, (void)P, (void)R, (void)flag, (void)nbx, (void)ldsX, (void)ldsM, (void)nrg,     \
+      (void)p0, (void)E, (void)g
 
+// The kernel's arguments as laid out in its argument segment.
+struct XrecKArgs {
+  RecurrentArgs a;
+  XrecTiling tl;
+};
+typedef const __attribute__((address_space(4))) XrecKArgs *KArgPtr;
+
+template <int NBW, int NT, bool TP>
+__global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecTiling tiling) {
+  static_assert(offsetof(XrecKArgs, tl) == sizeof(RecurrentArgs), "argument layout");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ int s_abort, s_role;
   constexpr int bX = 16 * NT, u = 32 * NBW, uw = u / 4;  // uw: code words of a row per unit tile
-  const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;
-  int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;
-  unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
 
   if (threadIdx.x == 0) {
     const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
+    unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(args.ws) + kHeaderBytes);
     s_role = -1;
     s_abort = 0;
     if (xcc < kXrecXcds) {
@@ -224,21 +260,12 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
     }
   }
   __syncthreads();
-  if (s_role < 0) return;
-  const int x = s_role / kXrecSlots, s = s_role % kXrecSlots;
-  const int64_t xb0 = (int64_t)x * tl.rows;  // the XCD's first batch row
-  const int nbx = (int)std::min<int64_t>(tl.rows, B - xb0);
+  const int role = __builtin_amdgcn_readfirstlane(s_role);
+  if (role < 0) return;
+  const RecurrentArgs &a = args;
+  const XrecTiling &tl = tiling;
+  XREC_DERIVED(a, tl, role);
   if (nbx <= 0) return;  // no rows: the whole XCD leaves
-  const int64_t j0 = (int64_t)s * u;
-  const int ldR = tl.ldR, ldH = tl.ldH, ldsX = ldR + 16, ldsM = ldH + 16, pw = tl.pw, rg = tl.rg;
-  const int g = s / kXrecOuts, o = s % kXrecOuts;
-  const int prow0 = g * rg;  // the row group's first row (XCD-local)
-  const int nrg = std::max(0, std::min(rg, nbx - prow0));
-  const int64_t p0 = (int64_t)o * pw;
-
-  uint64_t *X = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes +
-                                             kXrecSlotBytes) + (int64_t)x * tl.xwords;
-  auto E = [&](int64_t t) { return X + (t & 1) * tl.pwords; };
 
   // ---- prologue: W_h' and W_r' fragments, column params, c_0
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
@@ -278,6 +305,9 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
     c.iqw = a.Wh.inv_q[blk];
     c.pad = 0;
     cp[r] = c;
+    reinterpret_cast<int *>(ctm + jj)[gate] = (int32_t)c.colterm;
+    reinterpret_cast<int *>(czt + jj)[gate] = c.ztw;
+    reinterpret_cast<float *>(ciq + jj)[gate] = c.iqw;
   }
   // the lane's (cell, row) pairs: block b, row tile tt -> cell
   // 4 (wave NBW + b) + fq, row 16 tt + fr
@@ -303,10 +333,30 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
     r_iqw = a.Wr.inv_q[blk];
   }
   __syncthreads();
+  // blocks b whose four gate rows of this lane's cell allow the 24-bit recovery
+  int cfm = 0;
+#pragma unroll
+  for (int b = 0; b < NBW; ++b) {
+    bool f = true;
+#pragma unroll
+    for (int gate = 0; gate < 4; ++gate) {
+      const ColParam c = cp[(4 * (wave * NBW + b) + fq) * 4 + gate];
+      f = f && fast_col(c.ztw, c.colterm);
+    }
+    cfm |= f ? 1 << b : 0;
+  }
 
+  // the arguments where the launch put them (the kernel argument segment,
+  // constant memory: scalar loads)
+  KArgPtr kp = (KArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
   for (int64_t t = 0;; ++t) {
-    // per-thread indices re-derived every step from an opaque thread id, so
-    // that the compiler keeps no per-thread offsets alive across the loop
+    // the launch's scalars and the per-thread indices re-derived every step
+    // (an opaque argument pointer, an opaque thread id), so that the compiler
+    // keeps none of them alive across the loop
+    asm volatile("" : "+s"(kp));
+    auto &a = kp->a;
+    auto &tl = kp->tl;
+    XREC_DERIVED(a, tl, role);
     int tid = (int)threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
@@ -366,12 +416,14 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
     wait_vmcnt0();  // the direct loads of W_x x + b have landed in LDS
     __syncthreads();
     if (s_abort) return;
-    if (t > 0 && tid < nbx) {
-      // the row's code sum over the output groups, in group order
-      int total = 0;
-      for (int og = 0; og < kXrecOuts; ++og) total += ssum[tid * kXrecOuts + og];
-      rp[tid] = row_param(spar[2 * tid], __int_as_float(spar[2 * tid + 1]), total, (int)R);
-      if (s == 0) a.out_sums[(t - 1) * B + xb0 + tid] = total;
+    if (t > 0) {
+      // the row's code sum over its 16 output groups: 16 lanes per row
+      const int row = tid >> 4, og = tid & 15;
+      const int total = red16(row < nbx ? ssum[row * kXrecOuts + og] : 0, AddI{});
+      if (row < nbx && og == 0) {
+        rp[row] = row_param(spar[2 * row], __int_as_float(spar[2 * row + 1]), total, (int)R);
+        if (s == 0) a.out_sums[(t - 1) * B + xb0 + row] = total;
+      }
     }
     if (t == T) break;  // step T only collects the last step's code sums
 
@@ -406,17 +458,34 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
         const int jj = jjOf(b), lb = rowOf(tt);
         const int64_t j = j0 + jj, brow = xb0 + lb;
         const RowParam r = rp[lb];
+        // recovery: the 24-bit form straight through; where a zero point or
+        // column term rules it out (rare), the exact form, in a branch the
+        // wave takes only then
+        const int4 ct = ctm[jj], cz = czt[jj];
+        const float4 ci = ciq[jj];
+        float yh[4];
+        yh[0] = recover_fast(acc[b][tt][0], ct.x, cz.x, r.ztx, r.sigx, ci.x, r.iqx);
+        yh[1] = recover_fast(acc[b][tt][1], ct.y, cz.y, r.ztx, r.sigx, ci.y, r.iqx);
+        yh[2] = recover_fast(acc[b][tt][2], ct.z, cz.z, r.ztx, r.sigx, ci.z, r.iqx);
+        yh[3] = recover_fast(acc[b][tt][3], ct.w, cz.w, r.ztx, r.sigx, ci.w, r.iqx);
+        const bool fast = ((cfm >> b) & 1) && fast_row(r.ztx);
+        if (__any(!fast)) {
+          if (!fast)
+#pragma unroll
+            for (int gate = 0; gate < 4; ++gate) {
+              const ColParam c = cp[jj * 4 + gate];
+              yh[gate] = recover(acc[b][tt][gate], c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
+            }
+        }
         float gv[4];
 #pragma unroll
         for (int gate = 0; gate < 4; ++gate) {
-          const ColParam c = cp[jj * 4 + gate];
-          const int32_t sv = acc[b][tt][gate];
-          const float yh = recover(sv, c.colterm, c.ztw, r.ztx, r.sigx, c.iqw, r.iqx);
-          const float av = gxs[lb * (4 * u + 4) + gate * u + jj] + yh;
+          const float av = gxs[lb * (4 * u + 4) + gate * u + jj] + yh[gate];
           const float sg = sigmoid_cw(gate == 2 ? 2.0f * av : av);
           gv[gate] = gate == 2 ? 2.0f * sg - 1.0f : sg;
           if (TP && a.acc_h && j < H && lb < nbx)
-            a.acc_h[(t * B + brow) * 4 * H + gate * H + j] = acc_u8(sv, c.sigw, r.sigx, R);
+            a.acc_h[(t * B + brow) * 4 * H + gate * H + j] =
+                acc_u8(acc[b][tt][gate], cp[jj * 4 + gate].sigw, r.sigx, R);
         }
         const float cn = (gv[1] * cst[b][tt]) + (gv[0] * gv[2]);
         cst[b][tt] = cn;
@@ -554,11 +623,17 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
         s_abort = 1;
       __syncthreads();
       if (s_abort) return;
-      if (tid < nrg) {
-        int sum = 0;
-        for (int k = 0; k < kXrecSlots; ++k) sum += ssum[tid * kXrecSlots + k];
-        const XParam xp = mp[prow0 + tid];
-        rpp[tid] = row_param(xp.z, xp.inv_q, sum, (int)H);
+      {
+        // the row's code sum over the 32 unit tiles: 16 lanes per row, two each
+        const int row = tid >> 4, j = tid & 15;
+        const int sum = red16(row < nrg ? ssum[row * kXrecSlots + 2 * j] +
+                                              ssum[row * kXrecSlots + 2 * j + 1]
+                                        : 0,
+                              AddI{});
+        if (row < nrg && j == 0) {
+          const XParam xp = mp[prow0 + row];
+          rpp[row] = row_param(xp.z, xp.inv_q, sum, (int)H);
+        }
       }
       __syncthreads();
       // this wave's K chunks against every output block; rows past the group
@@ -585,8 +660,12 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTili
       __syncthreads();
       const bool valid = plane && lr < nrg && pout < P;
       if (plane) {
+        int32_t pv[kXrecWaves];
+#pragma unroll
+        for (int w = 0; w < kXrecWaves; ++w) pv[w] = red[(w * pw + pp) * rg + lr];
         int32_t sv = 0;
-        for (int w = 0; w < kXrecWaves; ++w) sv += red[(w * pw + pp) * rg + lr];
+#pragma unroll
+        for (int w = 0; w < kXrecWaves; ++w) sv += pv[w];
         const RowParam r = rpp[lr < nrg ? lr : 0];
         hv = recover(sv, r_colterm, r_ztw, r.ztx, r.sigx, r_iqw, r.iqx);
         if (valid) {
@@ -737,6 +816,7 @@ static bool plan_xrec(const RecurrentArgs &a, int cus, int lds_max, XrecTiling *
   tl.off_hcs = take((size_t)tl.rg * tl.pw);
   tl.off_sum = take((size_t)std::max(tl.bX * kXrecOuts, tl.rg * kXrecSlots) * 4);
   tl.off_par = take((size_t)tl.bX * 2 * 4);
+  tl.off_cf = take((size_t)3 * tl.u * 16);
   tl.lds_bytes = off;
   if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
   *out = tl;
