@@ -385,29 +385,27 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
     } else {
       // E4 of step t - 1: code words into xc; per (row, output group) the code
       // sum, and the row's z and 1/Q, into LDS
+      // word i of a thread: row 4 i + th / 128, word th % 128 of it (a row
+      // has at most 128), no division; the bases once per step
       const uint64_t *e4 = E(t - 1);
-      const int cwr = ldR / 4;    // code words of a row
-      constexpr int CW = bX / 4;  // >= bX * ldR / 4 / threads for ldR <= 512
+      const uint64_t *e4c = e4 + tl.o_e4c, *e4s = e4 + tl.o_e4s, *e4p = e4 + tl.o_e4p;
+      const int cwr = ldR / 4, rs4 = 4 * (kXrecOuts * pw / 4), ls4 = 4 * ldsX;
+      constexpr int CW = bX / 4;
       uint32_t need = 0;
 #pragma unroll
       for (int k = 0; k < CW; ++k)
-        if (k * kXrecThreads + tid < nbx * cwr) need |= 1u << k;
+        if (4 * k + (tid >> 7) < nbx && (tid & 127) < cwr) need |= 1u << k;
       if (tid < nbx * kXrecOuts) need |= 1u << CW;  // sum of (row tid / 16, group tid % 16)
       if (tid < nbx * 2) need |= 1u << (CW + 1);    // z (even tid) or 1/Q of row tid / 2
       if (!poll_to_lds<CW + 2>(
               need, (uint32_t)t,
               [&](int i, int th) -> const uint64_t * {
-                if (i < CW) {
-                  const int idx = i * kXrecThreads + th, row = idx / cwr, wd = idx % cwr;
-                  return e4 + tl.o_e4c + (int64_t)row * (kXrecOuts * pw / 4) + wd;
-                }
-                return e4 + (i == CW ? tl.o_e4s : tl.o_e4p) + th;
+                if (i < CW) return e4c + i * rs4 + (th >> 7) * (rs4 / 4) + (th & 127);
+                return (i == CW ? e4s : e4p) + th;
               },
               [&](int i, int th) -> uint32_t * {
-                if (i < CW) {
-                  const int idx = i * kXrecThreads + th, row = idx / cwr, wd = idx % cwr;
-                  return reinterpret_cast<uint32_t *>(xc + row * ldsX + 4 * wd);
-                }
+                if (i < CW)
+                  return reinterpret_cast<uint32_t *>(xc + i * ls4 + (th >> 7) * ldsX + 4 * (th & 127));
                 return reinterpret_cast<uint32_t *>(i == CW ? ssum + th : spar + th);
               },
               flag))
@@ -544,9 +542,9 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       const int row = tid >> 4, j = tid & 15;
       uint32_t v[4];
       const uint32_t need = row < nbx ? 0xfu : 0u;
-      const bool ok = poll_words<4>(need, tag, v, [&](int i) -> const uint64_t * {
-        return e + tl.o_e1 + (row * kXrecSlots + 2 * j + (i >> 1)) * 2 + (i & 1);
-      }, flag);
+      const uint64_t *e1 = e + tl.o_e1 + (row * kXrecSlots + 2 * j) * 2;  // 4 consecutive words
+      const bool ok = poll_words<4>(need, tag, v, [&](int i) -> const uint64_t * { return e1 + i; },
+                                    flag);
       if (!ok) s_abort = 1;
       int lo = need ? min((int)v[0], (int)v[2]) : 0x7fffffff;
       int hi = need ? min((int)v[1], (int)v[3]) : 0x7fffffff;
@@ -596,28 +594,24 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
     // W_r', recovery of h_t
     float hv = 0.0f;
     if (nrg > 0) {
+      // word i of a thread: row i of the group, word th of it (a row has at
+      // most 512), no division; the bases once per step
       const int cwm = ldH / 4;  // code words of a row of m
-      constexpr int CW = bX / kXrecGroups;  // >= rg * ldH / 4 / threads for ldH <= 2048
+      constexpr int CW = bX / kXrecGroups;
+      const uint64_t *e2c = e + tl.o_e2c + (int64_t)prow0 * (kXrecSlots * uw);
+      const uint64_t *e2s = e + tl.o_e2s + prow0 * kXrecSlots;
       uint32_t need = 0;
 #pragma unroll
       for (int k = 0; k < CW; ++k)
-        if (k * kXrecThreads + tid < nrg * cwm) need |= 1u << k;
+        if (k < nrg && tid < cwm) need |= 1u << k;
       if (tid < nrg * kXrecSlots) need |= 1u << CW;  // sum of (row tid / 32, tile tid % 32)
       if (!poll_to_lds<CW + 1>(
               need, tag,
               [&](int i, int th) -> const uint64_t * {
-                if (i < CW) {
-                  const int idx = i * kXrecThreads + th, row = idx / cwm, wd = idx % cwm;
-                  return e + tl.o_e2c + (int64_t)(prow0 + row) * (kXrecSlots * uw) + wd;
-                }
-                return e + tl.o_e2s + prow0 * kXrecSlots + th;
+                return i < CW ? e2c + i * (kXrecSlots * uw) + th : e2s + th;
               },
               [&](int i, int th) -> uint32_t * {
-                if (i < CW) {
-                  const int idx = i * kXrecThreads + th, row = idx / cwm, wd = idx % cwm;
-                  return reinterpret_cast<uint32_t *>(mc + row * ldsM + 4 * wd);
-                }
-                return reinterpret_cast<uint32_t *>(ssum + th);
+                return reinterpret_cast<uint32_t *>(i < CW ? mc + i * ldsM + 4 * th : (int8_t *)(ssum + th));
               },
               flag))
         s_abort = 1;
@@ -694,9 +688,9 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
         const int row = tid >> 4, og = tid & 15;
         uint32_t w2[2];
         const uint32_t need3 = row < nrg ? 3u : 0u;
-        const bool ok3 = poll_words<2>(need3, tag, w2, [&](int i) -> const uint64_t * {
-          return e + tl.o_e3 + ((prow0 + row) * kXrecOuts + og) * 2 + i;
-        }, flag);
+        const uint64_t *e3 = e + tl.o_e3 + ((prow0 + row) * kXrecOuts + og) * 2;
+        const bool ok3 = poll_words<2>(need3, tag, w2, [&](int i) -> const uint64_t * { return e3 + i; },
+                                       flag);
         if (!ok3) s_abort = 1;
         const int l2 = red16(need3 ? (int)w2[0] : 0x7fffffff, MinI{});
         const int h2 = red16(need3 ? (int)w2[1] : 0x7fffffff, MinI{});
