@@ -70,15 +70,10 @@ struct XrecTiling {
   int rows;      // batch rows per XCD (the last XCDs may hold fewer)
   int bX;        // rows padded to MFMA tiles: 16 * NT
   int u;         // cells per unit tile: 32 * NBW
-  int pw;        // outputs per projection tile: 16 or 32
-  int rg;        // rows per projection row group: bX / 2
   int ldR, ldH;  // padded widths of the codes of h (K of W_h') and of m (K of W_r')
   int ksw;       // 64-byte K chunks of W_r' per wave
-  int64_t pwords, xwords;  // exchange words per parity and per XCD
-  // word offsets inside one parity of an XCD's exchange
-  int64_t o_e1, o_e2c, o_e2s, o_e3, o_e4c, o_e4s, o_e4p;
-  size_t off_xc, off_gx, off_cp, off_rp, off_mp, off_pm, off_mcs, off_mc, off_red, off_rpp,
-      off_hp, off_hcs, off_sum, off_par, off_cf, lds_bytes;
+  size_t lds_bytes;  // (host) dynamic LDS of the instance
+  int64_t xwords;    // (host) exchange words per XCD
 };
 
 // Quantizer params of a row as the encoder needs them.
@@ -86,6 +81,55 @@ struct XParam {
   double q;
   int32_t z;
   float inv_q;
+};
+
+// Widths the layout is sized for: h up to 512 values (16 projection tiles of
+// 32 outputs), m up to 2048.
+constexpr int kXrecMaxR = 512, kXrecMaxH = 2048, kXrecMaxPw = 32;
+constexpr size_t xal16(size_t n) { return (n + 15) / 16 * 16; }
+
+// The LDS and exchange layout of an instance, fixed at compile time (the
+// widths of a layer only bound the loops): every offset is an immediate.
+template <int NBW, int NT>
+struct XLay {
+  static constexpr int bX = 16 * NT, u = 32 * NBW, uw = u / 4, rg = bX / kXrecGroups;
+  static constexpr int ldsX = kXrecMaxR + 16;    // row stride of the codes of h
+  static constexpr int ldsM = kXrecMaxH + 16;    // row stride of the codes of m
+  static constexpr int gxr = 4 * u + 4;          // row stride (floats) of W_x x + b
+  static constexpr int e4rw = kXrecOuts * kXrecMaxPw / 4;  // code words of a row of h
+  static constexpr int nsum = bX * kXrecOuts > rg * kXrecSlots ? bX * kXrecOuts : rg * kXrecSlots;
+  // LDS byte offsets
+  static constexpr size_t xc = 0;                                               // [bX][ldsX]
+  static constexpr size_t gx = xal16(xc + (size_t)bX * ldsX);                   // [2][bX][gxr]
+  static constexpr size_t cp = xal16(gx + (size_t)2 * bX * gxr * 4);            // [u][4]
+  static constexpr size_t cf = xal16(cp + (size_t)4 * u * sizeof(ColParam));    // 3 x [u] x 16
+  static constexpr size_t rp = xal16(cf + (size_t)3 * u * 16);                  // [bX]
+  static constexpr size_t mp = xal16(rp + (size_t)bX * sizeof(RowParam));       // [bX]
+  static constexpr size_t pm = xal16(mp + (size_t)bX * sizeof(XParam));         // [bX][32][2]
+  static constexpr size_t mcs = xal16(pm + (size_t)bX * 32 * 2 * 4);            // [bX][u]
+  static constexpr size_t mc = xal16(mcs + (size_t)bX * u);                     // [rg][ldsM]
+  static constexpr size_t red = xal16(mc + (size_t)rg * ldsM);                  // [waves][pw][rg]
+  static constexpr size_t rpp = xal16(red + (size_t)kXrecWaves * kXrecMaxPw * rg * 4);
+  static constexpr size_t hp = xal16(rpp + (size_t)rg * sizeof(RowParam));      // [rg]
+  static constexpr size_t hcs = xal16(hp + (size_t)rg * sizeof(XParam));        // [rg][pw]
+  static constexpr size_t sum = xal16(hcs + (size_t)rg * kXrecMaxPw);           // [nsum]
+  static constexpr size_t par = xal16(sum + (size_t)nsum * 4);                  // [bX][2]
+  static constexpr size_t bytes = xal16(par + (size_t)bX * 2 * 4);
+  // exchange word offsets inside one parity of an XCD's area:
+  //   E1  [bX][32 tiles][2]   min / max keys of m_t
+  //   E2c [bX][32 tiles][uw]  codes of m_t, E2s [bX][32 tiles] their sums
+  //   E3  [bX][16 groups][2]  min / max keys of h_t
+  //   E4c [bX][e4rw]          codes of h_t, E4s [bX][16 groups] their sums,
+  //   E4p [bX][2]             zero point and recovery factor of h_t
+  static constexpr int64_t e1 = 0;
+  static constexpr int64_t e2c = e1 + (int64_t)bX * kXrecSlots * 2;
+  static constexpr int64_t e2s = e2c + (int64_t)bX * kXrecSlots * uw;
+  static constexpr int64_t e3 = e2s + (int64_t)bX * kXrecSlots;
+  static constexpr int64_t e4c = e3 + (int64_t)bX * kXrecOuts * 2;
+  static constexpr int64_t e4s = e4c + (int64_t)bX * e4rw;
+  static constexpr int64_t e4p = e4s + (int64_t)bX * kXrecOuts;
+  static constexpr int64_t pwords = (e4p + (int64_t)bX * 2 + 31) / 32 * 32;  // parities 256 B apart
+  static constexpr int64_t xwords = 2 * pwords;
 };
 
 // A 64-bit exchange word with a plain store (no cache-policy bits): it stays
@@ -190,49 +234,30 @@ struct AddI {
 
 // NBW: fragment blocks (four cells each) per wave, u = 32 NBW cells a unit
 // tile; NT: 16-row MFMA tiles of the XCD's rows; TP: the launch writes taps.
-// Everything a workgroup derives from the launch arguments and its role:
-// LDS arrays, sizes, its rows, cells, projection tile and exchange area.  The
-// kernel states it once for the prologue and again at the top of every step,
-// reading the arguments through a pointer the compiler cannot follow across
-// steps, so none of these values has to stay live across the loop (they are
-// cheap scalar work; kept live, they overflow the scalar registers).
-#define XREC_DERIVED(a, tl, role)                                                              \
-  int8_t *xc = reinterpret_cast<int8_t *>(smem + tl.off_xc);      /* [bX][ldR+16] h codes */ \
-  float *gxs = reinterpret_cast<float *>(smem + tl.off_gx);       /* [bX][4][u] W_x x + b */ \
-  ColParam *cp = reinterpret_cast<ColParam *>(smem + tl.off_cp);  /* [u][4] W_h' rows     */ \
-  int4 *ctm = reinterpret_cast<int4 *>(smem + tl.off_cf);         /* [u] colterm, 4 gates */ \
-  int4 *czt = ctm + tl.u;                                         /* [u] shifted zeros    */ \
-  float4 *ciq = reinterpret_cast<float4 *>(czt + tl.u);           /* [u] 1/Q              */ \
-  RowParam *rp = reinterpret_cast<RowParam *>(smem + tl.off_rp);  /* [bX] rows of h_{t-1} */ \
-  XParam *mp = reinterpret_cast<XParam *>(smem + tl.off_mp);      /* [bX] quantizer of m  */ \
-  int *pm = reinterpret_cast<int *>(smem + tl.off_pm);            /* [bX][32][2] m parts  */ \
-  uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + tl.off_mcs);  /* [bX][u] own m codes  */ \
-  int8_t *mc = reinterpret_cast<int8_t *>(smem + tl.off_mc);      /* [rg][ldH+16] m codes */ \
-  int32_t *red = reinterpret_cast<int32_t *>(smem + tl.off_red);  /* [waves][pw][rg] sums */ \
-  RowParam *rpp = reinterpret_cast<RowParam *>(smem + tl.off_rpp); /* [rg] rows of m      */ \
-  XParam *hp = reinterpret_cast<XParam *>(smem + tl.off_hp);      /* [rg] quantizer of h  */ \
-  uint8_t *hcs = reinterpret_cast<uint8_t *>(smem + tl.off_hcs);  /* [rg][pw] h codes     */ \
-  int *ssum = reinterpret_cast<int *>(smem + tl.off_sum);         /* polled code sums     */ \
-  int *spar = reinterpret_cast<int *>(smem + tl.off_par);         /* [bX][2] z, 1/Q of h  */ \
+// What a workgroup derives from the launch's scalars and its role: its rows,
+// cells, projection tile and exchange area.  The kernel states it once for
+// the prologue and again at the top of every step, reading the arguments
+// through a pointer the compiler cannot follow across steps, so that none of
+// these values (nor anything computed from them) stays live across the loop:
+// kept live, they overflow the scalar registers.
+#define XREC_SCALARS(a, tl, role)                                                               \
   const int64_t T = a.T, B = a.B, H = a.H, P = a.P, R = a.R;                                   \
   int *flag = reinterpret_cast<int *>(a.ws) + kHdrFlag;                                        \
   const int x = (role) / kXrecSlots, s = (role) % kXrecSlots;                                  \
   const int64_t xb0 = (int64_t)x * tl.rows; /* the XCD's first batch row */                    \
-  const int nbx = (int)std::min<int64_t>((int64_t)tl.rows, B - xb0);                                 \
+  const int nbx = (int)std::min<int64_t>((int64_t)tl.rows, B - xb0);                           \
   const int64_t j0 = (int64_t)s * u;                                                           \
-  const int ldR = tl.ldR, ldH = tl.ldH, ldsX = ldR + 16, ldsM = ldH + 16, pw = tl.pw;          \
-  const int rg = tl.rg;                                                                        \
+  const int ldR = tl.ldR, ldH = tl.ldH;                                                        \
+  constexpr int pw = kXrecMaxPw; /* outputs per projection tile */                             \
   const int g = s / kXrecOuts, o = s % kXrecOuts;                                              \
   const int prow0 = g * rg; /* the row group's first row (XCD-local) */                        \
   const int nrg = std::max(0, std::min(rg, nbx - prow0));                                      \
   const int64_t p0 = (int64_t)o * pw;                                                          \
   uint64_t *X = reinterpret_cast<uint64_t *>(static_cast<char *>(a.ws) + kHeaderBytes +        \
-                                             kXrecSlotBytes) + (int64_t)x * tl.xwords;         \
-  auto E = [&](int64_t tt_) { return X + (tt_ & 1) * tl.pwords; };                             \
-  (void)xc, (void)gxs, (void)cp, (void)ctm, (void)czt, (void)ciq, (void)rp, (void)mp, (void)pm, \
-      (void)mcs, (void)mc, (void)red, (void)rpp, (void)hp, (void)hcs, (void)ssum, (void)spar,   \
-      (void)T, (void)P, (void)R, (void)flag, (void)nbx, (void)ldsX, (void)ldsM, (void)nrg,     \
-      (void)p0, (void)E, (void)g
+                                             kXrecSlotBytes) + (int64_t)x * L::xwords;         \
+  auto E = [&](int64_t tt_) { return X + (tt_ & 1) * L::pwords; };                             \
+  (void)T, (void)P, (void)R, (void)flag, (void)nbx, (void)ldR, (void)ldH, (void)nrg, (void)p0, \
+      (void)E, (void)g, (void)o
 
 // The kernel's arguments as laid out in its argument segment.
 struct XrecKArgs {
@@ -242,15 +267,16 @@ struct XrecKArgs {
 typedef const __attribute__((address_space(4))) XrecKArgs *KArgPtr;
 
 template <int NBW, int NT, bool TP>
-__global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecTiling tiling) {
+__global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs a, XrecTiling tl) {
   static_assert(offsetof(XrecKArgs, tl) == sizeof(RecurrentArgs), "argument layout");
+  using L = XLay<NBW, NT>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_abort, s_role;
   constexpr int bX = 16 * NT, u = 32 * NBW, uw = u / 4;  // uw: code words of a row per unit tile
 
   if (threadIdx.x == 0) {
     const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
-    unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(args.ws) + kHeaderBytes);
+    unsigned *slots = reinterpret_cast<unsigned *>(static_cast<char *>(a.ws) + kHeaderBytes);
     s_role = -1;
     s_abort = 0;
     if (xcc < kXrecXcds) {
@@ -262,9 +288,28 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
   __syncthreads();
   const int role = __builtin_amdgcn_readfirstlane(s_role);
   if (role < 0) return;
-  const RecurrentArgs &a = args;
-  const XrecTiling &tl = tiling;
-  XREC_DERIVED(a, tl, role);
+  int8_t *xc = reinterpret_cast<int8_t *>(smem + L::xc);        // codes of h_{t-1}
+  float *gxs = reinterpret_cast<float *>(smem + L::gx);         // W_x x + b, [row][gate][u]
+  ColParam *cp = reinterpret_cast<ColParam *>(smem + L::cp);    // [u][4] gate rows of W_h'
+  // the same for the 24-bit recovery, four gates of a cell per vector:
+  // low 32 bits of colterm, shifted zero point, 1/Q
+  int4 *ctm = reinterpret_cast<int4 *>(smem + L::cf);
+  int4 *czt = ctm + u;
+  float4 *ciq = reinterpret_cast<float4 *>(czt + u);
+  RowParam *rp = reinterpret_cast<RowParam *>(smem + L::rp);   // rows of h_{t-1}
+  XParam *mp = reinterpret_cast<XParam *>(smem + L::mp);       // quantizer of each row of m_t
+  int *pm = reinterpret_cast<int *>(smem + L::pm);             // min/max parts of m_t
+  uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + L::mcs);   // own cells' codes of m_t
+  int8_t *mc = reinterpret_cast<int8_t *>(smem + L::mc);       // the row group's codes of m_t
+  int32_t *red = reinterpret_cast<int32_t *>(smem + L::red);   // the waves' partial products
+  RowParam *rpp = reinterpret_cast<RowParam *>(smem + L::rpp); // the row group's rows of m_t
+  XParam *hp = reinterpret_cast<XParam *>(smem + L::hp);       // quantizer of h_t
+  uint8_t *hcs = reinterpret_cast<uint8_t *>(smem + L::hcs);   // own outputs' codes of h_t
+  int *ssum = reinterpret_cast<int *>(smem + L::sum);          // code sums of polled words
+  int *spar = reinterpret_cast<int *>(smem + L::par);          // z, 1/Q of h_{t-1}
+  constexpr int ldsX = L::ldsX, ldsM = L::ldsM;
+  constexpr int rg = L::rg;
+  XREC_SCALARS(a, tl, role);
   if (nbx <= 0) return;  // no rows: the whole XCD leaves
 
   // ---- prologue: W_h' and W_r' fragments, column params, c_0
@@ -346,8 +391,8 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
     cfm |= f ? 1 << b : 0;
   }
 
-  // the arguments where the launch put them (the kernel argument segment,
-  // constant memory: scalar loads)
+  // the arguments where the launch put them (the kernel argument segment:
+  // scalar loads)
   KArgPtr kp = (KArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
   for (int64_t t = 0;; ++t) {
     // the launch's scalars and the per-thread indices re-derived every step
@@ -356,7 +401,7 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
     asm volatile("" : "+s"(kp));
     auto &a = kp->a;
     auto &tl = kp->tl;
-    XREC_DERIVED(a, tl, role);
+    XREC_SCALARS(a, tl, role);
     int tid = (int)threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
@@ -365,16 +410,25 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
     const int lr = tid / pw, pp = tid % pw;
     const int64_t pout = p0 + pp;
     const bool plane = lr < rg;
-    // ---- W_x x + b of step t straight into LDS, [row][gate][u] with rows
-    // 4u + 4 floats apart: one 16-byte load per lane, one row (4 gates x u
-    // cells) per wave instruction (u = 32: the first 32 lanes)
-    if (t < T && (u == 64 || lane < 32)) {
-      const int gate = lane / uw, c4 = lane % uw;
-      const int64_t jc = j0 + 4 * c4 < H ? j0 + 4 * c4 : 0;  // past H: any cell in bounds
-      for (int row = wave; row < nbx; row += kXrecWaves)
-        __builtin_amdgcn_global_load_lds(a.gx + ((t * B + xb0 + row) * 4 * H + gate * H + jc),
-                                         (lds_ptr)(gxs + row * (4 * u + 4)), 16, 0, 0);
-    }
+    // ---- W_x x + b of step tt straight into LDS buffer tt & 1, [row][gate][u]
+    // with rows 4u + 4 floats apart: one 16-byte load per lane, one row (4
+    // gates x u cells) per wave instruction (u = 32: the first 32 lanes).
+    // Step t + 1's is issued as soon as step t's codes of h_{t-1} are in:
+    // loads complete in order, so issued at the top of a step it would hold
+    // up that step's first poll.  (Issued later in the step, before a poll
+    // or before the gates, it measured slower: its latency, about 2 us under
+    // this load, then falls on that phase.)
+    auto load_gx = [&](int64_t tt) {
+      if (tt < T && (u == 64 || lane < 32)) {
+        const int gate = lane / uw, c4 = lane % uw;
+        const int64_t jc = j0 + 4 * c4 < H ? j0 + 4 * c4 : 0;  // past H: any cell in bounds
+        float *buf = gxs + (tt & 1) * (bX * L::gxr);
+        for (int row = wave; row < nbx; row += kXrecWaves)
+          __builtin_amdgcn_global_load_lds(a.gx + ((tt * B + xb0 + row) * 4 * H + gate * H + jc),
+                                           (lds_ptr)(buf + row * L::gxr), 16, 0, 0);
+      }
+    };
+    if (t == 0) load_gx(0);
     // ---- 1. the codes of h_{t-1} and their row params
     if (t == 0) {
       if (!quant_tile<8, 2, kSrcPlain>(nbx, bX, R, 0u, (int)R, xc, ldsX, ldR, flag, rp,
@@ -388,8 +442,9 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       // word i of a thread: row 4 i + th / 128, word th % 128 of it (a row
       // has at most 128), no division; the bases once per step
       const uint64_t *e4 = E(t - 1);
-      const uint64_t *e4c = e4 + tl.o_e4c, *e4s = e4 + tl.o_e4s, *e4p = e4 + tl.o_e4p;
-      const int cwr = ldR / 4, rs4 = 4 * (kXrecOuts * pw / 4), ls4 = 4 * ldsX;
+      const uint64_t *e4c = e4 + L::e4c, *e4s = e4 + L::e4s, *e4p = e4 + L::e4p;
+      const int cwr = ldR / 4;
+      constexpr int rs4 = 4 * L::e4rw, ls4 = 4 * ldsX;
       constexpr int CW = bX / 4;
       uint32_t need = 0;
 #pragma unroll
@@ -424,6 +479,8 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       }
     }
     if (t == T) break;  // step T only collects the last step's code sums
+    // W_x x + b of the next step, into the other buffer
+    load_gx(t + 1);
 
     // ---- 2. Mult against the resident W_h' fragments: block b, row tile tt
     v4i acc[NBW][NT];
@@ -478,7 +535,7 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
         float gv[4];
 #pragma unroll
         for (int gate = 0; gate < 4; ++gate) {
-          const float av = gxs[lb * (4 * u + 4) + gate * u + jj] + yh[gate];
+          const float av = gxs[(t & 1) * (bX * L::gxr) + lb * L::gxr + gate * u + jj] + yh[gate];
           const float sg = sigmoid_cw(gate == 2 ? 2.0f * av : av);
           gv[gate] = gate == 2 ? 2.0f * sg - 1.0f : sg;
           if (TP && a.acc_h && j < H && lb < nbx)
@@ -532,8 +589,8 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       lo = red16(lo, MinI{});
       hi = red16(hi, MinI{});
       if (row < nbx && j == 0) {
-        put_word(e + tl.o_e1 + (row * kXrecSlots + s) * 2, tag, (uint32_t)lo);
-        put_word(e + tl.o_e1 + (row * kXrecSlots + s) * 2 + 1, tag, (uint32_t)hi);
+        put_word(e + L::e1 + (row * kXrecSlots + s) * 2, tag, (uint32_t)lo);
+        put_word(e + L::e1 + (row * kXrecSlots + s) * 2 + 1, tag, (uint32_t)hi);
       }
     }
     // every row's params from the 32 tiles' parts: 16 lanes per row, two
@@ -542,7 +599,7 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       const int row = tid >> 4, j = tid & 15;
       uint32_t v[4];
       const uint32_t need = row < nbx ? 0xfu : 0u;
-      const uint64_t *e1 = e + tl.o_e1 + (row * kXrecSlots + 2 * j) * 2;  // 4 consecutive words
+      const uint64_t *e1 = e + L::e1 + (row * kXrecSlots + 2 * j) * 2;  // 4 consecutive words
       const bool ok = poll_words<4>(need, tag, v, [&](int i) -> const uint64_t * { return e1 + i; },
                                     flag);
       if (!ok) s_abort = 1;
@@ -581,13 +638,13 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       int sum = 0;
       if (row < nbx) {
         const uint32_t word = *reinterpret_cast<const uint32_t *>(mcs + row * u + 4 * wd);
-        put_word(e + tl.o_e2c + (int64_t)row * (kXrecSlots * uw) + s * uw + wd, tag, word);
+        put_word(e + L::e2c + (int64_t)row * (kXrecSlots * uw) + s * uw + wd, tag, word);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           if (j0 + 4 * wd + k < H) sum += (int)((word >> (8 * k)) & 0xffu) ^ 0x80;
       }
       sum = uw == 16 ? red16(sum, AddI{}) : red8(sum, AddI{});
-      if (row < nbx && wd == 0) put_word(e + tl.o_e2s + row * kXrecSlots + s, tag, (uint32_t)sum);
+      if (row < nbx && wd == 0) put_word(e + L::e2s + row * kXrecSlots + s, tag, (uint32_t)sum);
     }
 
     // ---- 5. the projection tile: the codes of m_t of its rows, Mult against
@@ -598,8 +655,8 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       // most 512), no division; the bases once per step
       const int cwm = ldH / 4;  // code words of a row of m
       constexpr int CW = bX / kXrecGroups;
-      const uint64_t *e2c = e + tl.o_e2c + (int64_t)prow0 * (kXrecSlots * uw);
-      const uint64_t *e2s = e + tl.o_e2s + prow0 * kXrecSlots;
+      const uint64_t *e2c = e + L::e2c + (int64_t)prow0 * (kXrecSlots * uw);
+      const uint64_t *e2s = e + L::e2s + prow0 * kXrecSlots;
       uint32_t need = 0;
 #pragma unroll
       for (int k = 0; k < CW; ++k)
@@ -679,8 +736,8 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       lo = red_w(lo, pw, MinI{});
       hi = red_w(hi, pw, MinI{});
       if (plane && lr < nrg && pp == 0) {
-        put_word(e + tl.o_e3 + ((prow0 + lr) * kXrecOuts + o) * 2, tag, (uint32_t)lo);
-        put_word(e + tl.o_e3 + ((prow0 + lr) * kXrecOuts + o) * 2 + 1, tag, (uint32_t)hi);
+        put_word(e + L::e3 + ((prow0 + lr) * kXrecOuts + o) * 2, tag, (uint32_t)lo);
+        put_word(e + L::e3 + ((prow0 + lr) * kXrecOuts + o) * 2 + 1, tag, (uint32_t)hi);
       }
       // ---- 6. the row group's params of h_t (16 lanes per row, one output
       // group's words each), then E4
@@ -688,7 +745,7 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
         const int row = tid >> 4, og = tid & 15;
         uint32_t w2[2];
         const uint32_t need3 = row < nrg ? 3u : 0u;
-        const uint64_t *e3 = e + tl.o_e3 + ((prow0 + row) * kXrecOuts + og) * 2;
+        const uint64_t *e3 = e + L::e3 + ((prow0 + row) * kXrecOuts + og) * 2;
         const bool ok3 = poll_words<2>(need3, tag, w2, [&](int i) -> const uint64_t * { return e3 + i; },
                                        flag);
         if (!ok3) s_abort = 1;
@@ -722,10 +779,10 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
       const int csum = red_w(valid ? code : 0, pw, AddI{});
       if (plane && lr < nrg && pp == 0) {
         const int row = prow0 + lr;
-        put_word(e + tl.o_e4s + row * kXrecOuts + o, tag, (uint32_t)csum);
+        put_word(e + L::e4s + row * kXrecOuts + o, tag, (uint32_t)csum);
         if (o == 0) {
-          put_word(e + tl.o_e4p + row * 2, tag, (uint32_t)hp[lr].z);
-          put_word(e + tl.o_e4p + row * 2 + 1, tag, __float_as_uint(hp[lr].inv_q));
+          put_word(e + L::e4p + row * 2, tag, (uint32_t)hp[lr].z);
+          put_word(e + L::e4p + row * 2 + 1, tag, __float_as_uint(hp[lr].inv_q));
         }
       }
       __syncthreads();
@@ -733,7 +790,7 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
         const int pw4 = pw / 4, row = tid / pw4, wd = tid % pw4;
         if (row < nrg) {
           const uint32_t word = *reinterpret_cast<const uint32_t *>(hcs + row * pw + 4 * wd);
-          put_word(e + tl.o_e4c + (int64_t)(prow0 + row) * (kXrecOuts * pw4) + o * pw4 + wd, tag, word);
+          put_word(e + L::e4c + (int64_t)(prow0 + row) * L::e4rw + o * pw4 + wd, tag, word);
           const int64_t orow = t * B + xb0 + prow0 + row, k = p0 + 4 * wd;
           if (k < a.ld_out) *reinterpret_cast<uint32_t *>(a.out_codes + orow * a.ld_out + k) = word;
         }
@@ -750,68 +807,26 @@ __global__ __launch_bounds__(kXrecThreads) void k_xrec(RecurrentArgs args, XrecT
 }
 
 // ------------------------------------------------------------------ host side
-// One parity of an XCD's exchange, in 64-bit words:
-//   E1  [rows][32 tiles][2]   min / max keys of m_t
-//   E2c [rows][32 tiles][u/4] codes of m_t, E2s [rows][32 tiles] their sums
-//   E3  [rows][16 groups][2]  min / max keys of h_t
-//   E4c [rows][4 pw]          codes of h_t, E4s [rows][16 groups] their sums,
-//   E4p [rows][2]             zero point and recovery factor of h_t
 static bool plan_xrec(const RecurrentArgs &a, int cus, int lds_max, XrecTiling *out) {
   const int64_t B = a.B, H = a.H, P = a.P;
   if (P <= 0 || a.R != P || cus != kXrecXcds * kXrecSlots) return false;
-  if (B < kXrecMinBatch || B > kXrecXcds * 32 || H > 2048 || H % 4 || P > 512) return false;
+  if (B < kXrecMinBatch || B > kXrecXcds * 32 || H > kXrecMaxH || H % 4 || P > kXrecMaxR)
+    return false;
   XrecTiling tl{};
   tl.rows = (int)((B + kXrecXcds - 1) / kXrecXcds);
   tl.bX = tl.rows <= 16 ? 16 : 32;
   tl.u = H <= 1024 ? 32 : 64;
-  tl.pw = P <= 256 ? 16 : 32;
-  tl.rg = tl.bX / kXrecGroups;
   tl.ldR = (int)round_up(P, 64);
   tl.ldH = (int)round_up(H, 64);
   tl.ksw = (tl.ldH / 64 + kXrecWaves - 1) / kXrecWaves;
   if (tl.ksw > 4 || tl.u * kXrecSlots < H) return false;
   if (a.Wh.ld < tl.ldR || a.Wr.ld < tl.ldH) return false;
   if (a.ld_out < tl.ldR || a.ld_out % 4) return false;
-  const int64_t rows = tl.bX, uw = tl.u / 4;
-  int64_t w = 0;
-  tl.o_e1 = w;
-  w += rows * kXrecSlots * 2;
-  tl.o_e2c = w;
-  w += rows * kXrecSlots * uw;
-  tl.o_e2s = w;
-  w += rows * kXrecSlots;
-  tl.o_e3 = w;
-  w += rows * kXrecOuts * 2;
-  tl.o_e4c = w;
-  w += rows * kXrecOuts * tl.pw / 4;
-  tl.o_e4s = w;
-  w += rows * kXrecOuts;
-  tl.o_e4p = w;
-  w += rows * 2;
-  tl.pwords = round_up(w, 32);  // parities 256 bytes apart
-  tl.xwords = 2 * tl.pwords;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t at = off;
-    off = align_up(off + bytes, 16);
-    return at;
-  };
-  tl.off_xc = take((size_t)tl.bX * (tl.ldR + 16));
-  tl.off_gx = take((size_t)tl.bX * (4 * tl.u + 4) * 4);
-  tl.off_cp = take((size_t)4 * tl.u * sizeof(ColParam));
-  tl.off_rp = take((size_t)tl.bX * sizeof(RowParam));
-  tl.off_mp = take((size_t)tl.bX * sizeof(XParam));
-  tl.off_pm = take((size_t)tl.bX * 32 * 2 * 4);
-  tl.off_mcs = take((size_t)tl.bX * tl.u);
-  tl.off_mc = take((size_t)tl.rg * (tl.ldH + 16));
-  tl.off_red = take((size_t)kXrecWaves * tl.pw * tl.rg * 4);
-  tl.off_rpp = take((size_t)tl.rg * sizeof(RowParam));
-  tl.off_hp = take((size_t)tl.rg * sizeof(XParam));
-  tl.off_hcs = take((size_t)tl.rg * tl.pw);
-  tl.off_sum = take((size_t)std::max(tl.bX * kXrecOuts, tl.rg * kXrecSlots) * 4);
-  tl.off_par = take((size_t)tl.bX * 2 * 4);
-  tl.off_cf = take((size_t)3 * tl.u * 16);
-  tl.lds_bytes = off;
+  const int nbw = tl.u / 32, nt = tl.bX / 16;
+  tl.lds_bytes = nbw == 1 ? (nt == 1 ? XLay<1, 1>::bytes : XLay<1, 2>::bytes)
+                          : (nt == 1 ? XLay<2, 1>::bytes : XLay<2, 2>::bytes);
+  tl.xwords = nbw == 1 ? (nt == 1 ? XLay<1, 1>::xwords : XLay<1, 2>::xwords)
+                       : (nt == 1 ? XLay<2, 1>::xwords : XLay<2, 2>::xwords);
   if (tl.lds_bytes + 64 > (size_t)lds_max) return false;
   *out = tl;
   return true;
@@ -819,9 +834,7 @@ static bool plan_xrec(const RecurrentArgs &a, int cus, int lds_max, XrecTiling *
 
 size_t xrec_ws(int64_t B, int64_t H, int64_t P) {
   if (P <= 0) return 0;
-  const int64_t rows = 32, uw = 16, pw = 32;  // the largest tiling
-  const int64_t w = rows * kXrecSlots * (2 + uw + 1) + rows * kXrecOuts * 3 + rows * kXrecOuts * pw / 4 + rows * 2;
-  return kHeaderBytes + kXrecSlotBytes + (size_t)kXrecXcds * 2 * round_up(w, 32) * 8;
+  return kHeaderBytes + kXrecSlotBytes + (size_t)kXrecXcds * XLay<2, 2>::xwords * 8;  // the largest
 }
 
 using XrecKernel = void (*)(RecurrentArgs, XrecTiling);
