@@ -274,7 +274,7 @@ def lstmp_recurrence_kernel(ql, torch, M, x, reps):
     ops = 2 * B * (4 * H * P + P * H)          # per step
     avg = sum(ms) / len(ms)
     us = avg * 1e3 / T
-    return dict(kernel="k_recurrent (LSTMP 2048/512 layer 2, B=256, T=800)",
+    return dict(kernel="k_xrec (LSTMP 2048/512 layer 2, B=256, T=800; an eighth of the batch per XCD)",
                 avg_ms=round(avg, 3), us_per_step=round(us, 2),
                 weight_bytes_per_step=w_bytes,
                 weight_frac_of_hbm=round(w_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 5),
