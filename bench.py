@@ -36,8 +36,8 @@ FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
 TRAFFIC = dict(bytes=4.47e+09, read=2.994e+09, written=1.476e+09,
-               sources=("ql_stack.hip", "ql_rec_common.h", "ql_device.h", "ql_exchange.h",
-                        "ql_launch.h"),
+               sources=("ql_stack.hip", "ql_xstack.hip", "ql_xcd.h", "ql_rec_common.h",
+                        "ql_device.h", "ql_exchange.h", "ql_launch.h"),
                sha256="3f64d75e66db12695e28ef7e92486c916181ee91003d4bfa0bb09adcf6410fa9",
                summary="profiles/k_stack_5x500_B64_T1000_counters.md")
 
@@ -500,7 +500,7 @@ def main():
     achieved = rec["alg_bytes"] / (rec["avg_ms"] * 1e-3) / 1e9
     log(f"wavefront kernel ({nst} layers): {rec['avg_ms']:.3f} ms/launch, "
         f"{rec['us_per_frame']:.2f} us/frame, {achieved:.1f} GB/s algorithmic")
-    roofline = dict(bound="hbm", kernel=f"k_stack ({nst} 500-cell layers, B=64, T=1000)",
+    roofline = dict(bound="hbm", kernel=f"k_xstack ({nst} 500-cell layers, B=64, T=1000; one XCD per layer)",
                     achieved=round(achieved, 2), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 5), traffic=measured_traffic(),
                     traffic_unit="bytes per launch", traffic_source=TRAFFIC["summary"],

@@ -411,6 +411,13 @@ ql_status ql_debug_set_wait_bound(int32_t polls);
  * XCD holding an eighth of the batch (layers with a projection, batch 16 to
  * 256, 256 CUs), 0: any other path; -1 for an invalid layer or B < 0. */
 int32_t ql_debug_recurrence_layout(const ql_lstm_layer *L, int64_t B);
+/* Test hook: which layout the first wavefront launch over the n stacked
+ * layers (no projection) runs in for T frames at batch B on the current
+ * device -- 1: one persistent launch over the whole chip with one XCD per
+ * layer (batch 16 to 64, 2 to 8 layers, widths up to 512, 256 CUs), 0: any
+ * other path (including none); -1 for an invalid layer, n < 1, T < 0 or
+ * B < 0.  The layers are read, never written. */
+int32_t ql_debug_stack_layout(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B);
 /* Elementwise gate functions on device arrays (fn 0 = e^x, 1 = sigmoid,
  * 2 = tanh, 3 = the reciprocal 1 / d that sigmoid applies to d = 1 + e^-x,
  * defined for d in [1, 2^126) and equal there to IEEE division) -- the exact

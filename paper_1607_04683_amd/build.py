@@ -13,8 +13,8 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libqlstm.so")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 SOURCES = ["ql_quantize.hip", "ql_gemm.hip", "ql_recurrent.hip", "ql_stack.hip", "ql_pstack.hip",
-           "ql_f32.hip", "ql_train.hip", "ql_xrec.hip", "ql_api.cpp", "ql_scratch.hip"]
-HEADERS = ["ql_device.h", "ql_exchange.h", "ql_launch.h", "ql_rec_common.h"]
+           "ql_f32.hip", "ql_train.hip", "ql_xrec.hip", "ql_xstack.hip", "ql_api.cpp", "ql_scratch.hip"]
+HEADERS = ["ql_device.h", "ql_exchange.h", "ql_launch.h", "ql_rec_common.h", "ql_xcd.h"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -998,6 +998,29 @@ int32_t ql_debug_recurrence_layout(const ql_lstm_layer *L, int64_t B) {
   return recurrent_layout(a);
 }
 
+int32_t ql_debug_stack_layout(const ql_lstm_layer *layers, int32_t n, int64_t T, int64_t B) {
+  if (!layers || n < 1 || T < 0 || B < 0) return -1;
+  for (int k = 0; k < n; ++k)
+    if (check_layer(&layers[k]) != QL_OK) return -1;
+  const int per = ql_lstm_stack_layers_per_launch(layers, n, T, B);
+  if (per < 2 || layers[0].proj != 0) return 0;
+  // the first launch of the model forward's split into nearly equal launches
+  const int launches = (n + per - 1) / per;
+  const int nl = (n + launches - 1) / launches;
+  if (nl < 2) return 0;
+  StackArgs sa{};
+  sa.nl = nl;
+  sa.T = T;
+  sa.B = B;
+  sa.H = layers[0].hidden;
+  for (int k = 0; k < nl; ++k) {
+    ActBuf out{};
+    out.ld = round_up(layer_width(layers[k]), 64);
+    sa.L[k] = stack_layer(layers[k], ActRows{}, out, nullptr, nullptr, nullptr, k);
+  }
+  return stack_layout(sa);
+}
+
 ql_status ql_gate_fn(int32_t fn, const float *x, float *y, int64_t n, void *stream) {
   if (n > 0 && (!x || !y)) return QL_EINVAL;
   if (fn < 0 || fn > 3) return QL_EINVAL;

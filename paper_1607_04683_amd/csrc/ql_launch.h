@@ -112,6 +112,7 @@ hipError_t set_wait_bound_pstack(int polls);
 hipError_t set_wait_bound_f32(int polls);
 hipError_t set_wait_bound_train(int polls);
 hipError_t set_wait_bound_xrec(int polls);
+hipError_t set_wait_bound_xstack(int polls);
 // Reads the timeout flag a persistent launch left in its workspace (syncs s).
 hipError_t recurrent_timed_out(const void *ws, hipStream_t s, bool *timed_out);
 // Zeroes the n64 64-bit words after the workspace header (counters first).
@@ -181,6 +182,15 @@ hipError_t launch_pstack(const PStackArgs &a, hipStream_t s, bool *unsupported);
 int pstack_layers_per_launch(const PStackArgs &a);
 
 hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported);
+// Batch 16 to 64 on the whole chip (ql_xstack.hip): one XCD per layer.  *done
+// false when the shapes or the device do not fit that layout (nothing
+// launched).
+size_t xstack_ws(int nl);
+bool xstack_applies(const StackArgs &a, int cus, int lds_max);
+hipError_t launch_xstack(const StackArgs &a, int cus, int lds_max, bool taps, hipStream_t s,
+                         bool *done);
+// 1 when launch_stack would run a in that layout on the current device, else 0.
+int stack_layout(const StackArgs &a);
 // How many layers of such a stack fit one launch (1: none, use the one-layer path).
 int stack_layers_per_launch(int n, int64_t T, int64_t B, int64_t H, int64_t in0, int64_t in1);
 

@@ -711,6 +711,7 @@ hipError_t set_wait_bound(int polls) {
     if (e == hipSuccess) e = set_wait_bound_f32(polls);
     if (e == hipSuccess) e = set_wait_bound_train(polls);
     if (e == hipSuccess) e = set_wait_bound_xrec(polls);
+    if (e == hipSuccess) e = set_wait_bound_xstack(polls);
   }
   const hipError_t r = hipSetDevice(cur);
   return e != hipSuccess ? e : r;

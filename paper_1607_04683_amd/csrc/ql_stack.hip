@@ -937,10 +937,21 @@ size_t stack_ws(int nl, int64_t T, int64_t B, int64_t H) {
   } else {
     per = align_up(align_up((size_t)2 * B * H * 8, 256), 256);
   }
-  return kHeaderBytes + (size_t)nl * kStackCounterBytes + (size_t)nl * per;
+  return std::max(kHeaderBytes + (size_t)nl * kStackCounterBytes + (size_t)nl * per, xstack_ws(nl));
 }
 
 using StackKernel = void (*)(StackArgs, StackTiling);
+
+int stack_layout(const StackArgs &a) {
+  int dev = 0, cus = 0, lds_max = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return xstack_applies(a, cus, lds_max) ? 1 : 0;
+}
 
 hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported) {
   *unsupported = false;
@@ -955,15 +966,19 @@ hipError_t launch_stack(const StackArgs &a, hipStream_t s, bool *unsupported) {
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  StackTiling tl;
-  if (!plan_stack(a, cus, lds_max, &tl)) {
-    *unsupported = true;
-    return hipSuccess;
-  }
   bool tp = false;  // any tap or final state asked for
   for (int l = 0; l < a.nl; ++l) {
     const StackLayer &L = a.L[l];
     tp = tp || L.acc_x || L.acc_h || L.tap_gates || L.tap_c || L.tap_m || L.hT || L.cT;
+  }
+  // batch 16 to 64 on the whole chip: one XCD per layer
+  bool done = false;
+  e = launch_xstack(a, cus, lds_max, tp, s, &done);
+  if (e != hipSuccess || done) return e;
+  StackTiling tl;
+  if (!plan_stack(a, cus, lds_max, &tl)) {
+    *unsupported = true;
+    return hipSuccess;
   }
   StackKernel kern = tl.bB == 1 ? (tp ? k_stack<8, false, 1, true> : k_stack<8, false, 1, false>)
                                 : (tp ? k_stack<8, true, 2, true> : k_stack<8, true, 2, false>);

@@ -36,7 +36,7 @@ EXPORTS = [
     "ql_quantize_stacked_frames", "ql_acoustic_model_frames_workspace",
     "ql_acoustic_model_forward_frames", "ql_acoustic_model_forward_stream",
     "ql_acoustic_model_forward_stream_noalloc", "ql_train_step_workspace", "ql_train_step",
-    "ql_debug_set_wait_bound", "ql_debug_recurrence_layout",
+    "ql_debug_set_wait_bound", "ql_debug_recurrence_layout", "ql_debug_stack_layout",
 ]
 
 
@@ -143,6 +143,8 @@ def load(path: str = LIB_PATH):
     L.ql_debug_set_wait_bound.argtypes = [i32]
     L.ql_debug_recurrence_layout.argtypes = [C.POINTER(CLayer), i64]
     L.ql_debug_recurrence_layout.restype = i32
+    L.ql_debug_stack_layout.argtypes = [C.POINTER(CLayer), i32, i64, i64]
+    L.ql_debug_stack_layout.restype = i32
     L.ql_f32_matmul.argtypes = [vp, i64, i64, vp, i64, vp, vp, vp]
     L.ql_quantize_activations.argtypes = [vp, i64, i64, C.POINTER(CQAct), vp]
     L.ql_lstm_stack_workspace.argtypes = [C.POINTER(CLayer), i32, i64, i64]
@@ -771,6 +773,13 @@ def recurrence_layout(L: Layer, B: int) -> int:
     the batch (layers with a projection on the whole chip), else 0."""
     c = L.cstruct()
     return int(load().ql_debug_recurrence_layout(C.byref(c), B))
+
+
+def stack_layout(M: Model, T: int, B: int) -> int:
+    """1 when the first wavefront launch over M's layers runs with one XCD per
+    layer (batch 16 to 64 on the whole chip), else 0."""
+    arr = (CLayer * len(M.layers))(*[L.cstruct() for L in M.layers])
+    return int(load().ql_debug_stack_layout(arr, len(M.layers), T, B))
 
 
 # ------------------------------------------- quantization-aware training step
