@@ -89,6 +89,34 @@ __device__ __forceinline__ bool poll_to_lds(uint32_t need, uint32_t tag, SrcFn s
   }
 }
 
+// The first round of poll_to_lds issued ahead of other work: the words
+// whose bit is set in `need` are loaded into w; poll_to_lds_finish examines
+// them later (and polls on for those whose tag had not matched).
+template <int N, class SrcFn>
+__device__ __forceinline__ void poll_to_lds_issue(uint32_t need, SrcFn src, uint64_t (&w)[N]) {
+  int th = (int)threadIdx.x;
+  asm volatile("" : "+v"(th));
+#pragma unroll
+  for (int i = 0; i < N; ++i) w[i] = ((need >> i) & 1u) ? ld_tagged(src(i, th)) : 0;
+}
+template <int N, class SrcFn, class DstFn>
+__device__ __forceinline__ bool poll_to_lds_finish(uint32_t need, uint32_t tag, const uint64_t (&w)[N],
+                                                   SrcFn src, DstFn dst, int *flag) {
+  // every load of the round has landed, on every path (they are the wave's
+  // youngest memory operations, so this waits for nothing more)
+  wait_vmcnt0();
+  int th = (int)threadIdx.x;
+  asm volatile("" : "+v"(th));
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    if (((need >> i) & 1u) && (uint32_t)(w[i] >> 32) == tag) {
+      need &= ~(1u << i);
+      *dst(i, th) = (uint32_t)w[i];
+    }
+  if (!__any(need != 0)) return true;
+  return poll_to_lds<N>(need, tag, src, dst, flag);
+}
+
 // Reductions over aligned groups of 8 or 16 lanes (DPP): every lane of the
 // group ends with the group's result.
 template <class Op>

@@ -67,15 +67,16 @@ template <int NT>
 struct XsLay {
   static constexpr int bX = 16 * NT, u = kXsCells, uw = u / 4;
   static constexpr int ldsX = kXsMaxW + 16;  // row stride of the codes of x and of h
-  static constexpr size_t xx = 0;                                              // [bX][ldsX]
-  static constexpr size_t xh = xal16(xx + (size_t)bX * ldsX);                  // [bX][ldsX]
+  static constexpr size_t xxb = (size_t)bX * ldsX;                             // one x buffer
+  static constexpr size_t xx = 0;                                              // 2 x [bX][ldsX]
+  static constexpr size_t xh = xal16(xx + 2 * xxb);                            // [bX][ldsX]
   static constexpr size_t cph = xal16(xh + (size_t)bX * ldsX);                 // [u][4]
   static constexpr size_t cpx = xal16(cph + (size_t)4 * u * sizeof(ColParam)); // [u][4]
   static constexpr size_t cf = xal16(cpx + (size_t)4 * u * sizeof(ColParam));  // 6 x [u] x 16
   static constexpr size_t bias = xal16(cf + (size_t)6 * u * 16);               // [u] float4
   static constexpr size_t rph = xal16(bias + (size_t)u * 16);                  // [bX]
-  static constexpr size_t rpx = xal16(rph + (size_t)bX * sizeof(RowParam));    // [bX]
-  static constexpr size_t hp = xal16(rpx + (size_t)bX * sizeof(RowParam));     // [bX]
+  static constexpr size_t rpx = xal16(rph + (size_t)bX * sizeof(RowParam));    // 2 x [bX]
+  static constexpr size_t hp = xal16(rpx + (size_t)2 * bX * sizeof(RowParam)); // [bX]
   static constexpr size_t pm = xal16(hp + (size_t)bX * sizeof(XParam));        // [bX][32][2]
   static constexpr size_t mcs = xal16(pm + (size_t)bX * 32 * 2 * 4);           // [bX][u]
   static constexpr size_t sum = xal16(mcs + (size_t)bX * u);                   // [bX][16]
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
   __syncthreads();
   const int role = __builtin_amdgcn_readfirstlane(s_role);
   if (role < 0) return;
-  int8_t *xx = reinterpret_cast<int8_t *>(smem + L::xx);          // codes of x_t
+  int8_t *xx = reinterpret_cast<int8_t *>(smem + L::xx);          // codes of x_t, by step parity
   int8_t *xh = reinterpret_cast<int8_t *>(smem + L::xh);          // codes of h_{t-1}
   ColParam *cph = reinterpret_cast<ColParam *>(smem + L::cph);    // [u][4] W_h' rows
   ColParam *cpx = reinterpret_cast<ColParam *>(smem + L::cpx);    // [u][4] W_x' rows
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
   float4 *ciqx = reinterpret_cast<float4 *>(cztx + u);
   float4 *bias4 = reinterpret_cast<float4 *>(smem + L::bias);      // [u] gates i f g o
   RowParam *rph = reinterpret_cast<RowParam *>(smem + L::rph);    // rows of h_{t-1}
-  RowParam *rpx = reinterpret_cast<RowParam *>(smem + L::rpx);    // rows of x_t
+  RowParam *rpx = reinterpret_cast<RowParam *>(smem + L::rpx);    // rows of x_t, by step parity
   XParam *hp = reinterpret_cast<XParam *>(smem + L::hp);          // quantizer of each row of h_t
   int *pm = reinterpret_cast<int *>(smem + L::pm);                // min/max parts of h_t
   uint8_t *mcs = reinterpret_cast<uint8_t *>(smem + L::mcs);      // own cells' codes of h_t
@@ -289,11 +290,14 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
       xs = ld_coherent_i(xsp + o);
     }
   };
-  auto park_x = [&]() {
+  // into the LDS buffer of step parity par
+  auto park_x = [&](int par) {
+    int8_t *xd = xx + par * L::xxb;
 #pragma unroll
     for (int i = 0; i < bX / 8; ++i)
-      if ((xmask >> i) & 1u) *reinterpret_cast<uint64_t *>(xx + (8 * i + xr0) * ldsX + 8 * xwd) = xv[i];
-    if (threadIdx.x < bX) rpx[threadIdx.x] = xmeta ? row_param(xz, xq, xs, xin_k) : row_param(0, 0.0f, 0, xin_k);
+      if ((xmask >> i) & 1u) *reinterpret_cast<uint64_t *>(xd + (8 * i + xr0) * ldsX + 8 * xwd) = xv[i];
+    if (threadIdx.x < bX)
+      rpx[par * bX + threadIdx.x] = xmeta ? row_param(xz, xq, xs, xin_k) : row_param(0, 0.0f, 0, xin_k);
   };
   // This tile's part of the layer's quantized output of step tx (codes of
   // its cells, from the codes of h_tx in LDS; tile 0 also the rows' z, 1/Q
@@ -337,7 +341,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
   // x_0 goes to LDS, x_1 into registers
   wait_vmcnt0();
   load_x(0, 0u);
-  park_x();
+  park_x(0);
   if (T > 1) load_x(1, 0u);
   __syncthreads();
   for (int64_t t = 0;; ++t) {
@@ -351,11 +355,31 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
     const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
     const int jjL = 4 * wave + fq;  // the lane's cell (tile-local)
     const int64_t jL = j0 + jjL;
-    // the arrival count of x_{t+2}, read now so that it is in hand when its
-    // loads are issued (step 6)
-    unsigned seen = 0;
-    if (l > 0 && t + 2 < T)
-      seen = __hip_atomic_load(ctr(l - 1, (t + 2) & 1, g), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // ---- 0. the first round of the poll for the codes of h_{t-1} (E2 of step
+    // t-1), issued now and examined after step 1: word i of a thread is row
+    // 4 i + tid / 128, word tid % 128 (a row has at most 128); sums of (row
+    // tid / 16, tile tid % 16)
+    constexpr int CW = bX / 4;
+    constexpr int rs4 = 4 * kXsTiles * uw, ls4 = 4 * ldsX;
+    const uint64_t *e2 = E(t - 1);
+    const uint64_t *e2c = e2 + L::e2c, *e2s = e2 + L::e2s;
+    auto e2src = [&](int i, int th) -> const uint64_t * {
+      return i < CW ? e2c + i * rs4 + (th >> 7) * (rs4 / 4) + (th & 127) : e2s + th;
+    };
+    auto e2dst = [&](int i, int th) -> uint32_t * {
+      return reinterpret_cast<uint32_t *>(i < CW ? xh + i * ls4 + (th >> 7) * ldsX + 4 * (th & 127)
+                                                 : (int8_t *)(ssum + th));
+    };
+    uint32_t need = 0;
+    uint64_t w2[CW + 1];
+    if (t > 0) {
+      const int cw = ldH / 4;
+#pragma unroll
+      for (int k = 0; k < CW; ++k)
+        if (4 * k + (tid >> 7) < nb && (tid & 127) < cw) need |= 1u << k;
+      if (tid < nb * kXsTiles) need |= 1u << CW;
+      poll_to_lds_issue<CW + 1>(need, e2src, w2);
+    }
 
     // ---- 1. W_x' x_t, recovered (eq. 1 / eq. 3) plus the bias, as the
     // hoisted input product forms it.  x_t has been in LDS since the step
@@ -366,6 +390,8 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
     // hold, which adds exactly nothing to an integer sum.
     float xb[NT][4];
     if (t < T) {
+      const int8_t *xxt = xx + (t & 1) * L::xxb;
+      const RowParam *rpxt = rpx + (t & 1) * bX;
       v4i accx[NT];
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt) accx[tt] = v4i{};
@@ -374,7 +400,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt)
           accx[tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
-              wx[c], *reinterpret_cast<const v4i *>(xx + (16 * tt + fr) * ldsX + c * 64 + 16 * fq),
+              wx[c], *reinterpret_cast<const v4i *>(xxt + (16 * tt + fr) * ldsX + c * 64 + 16 * fq),
               accx[tt], 0, 0, 0);
       // the MFMA results are read by ordinary instructions below: at least 19
       // wait states after the last pass, which the hardware does not check
@@ -384,7 +410,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt) {
         const int lb = 16 * tt + fr;
-        const RowParam rx = rpx[lb];
+        const RowParam rx = rpxt[lb];
         float yx[4];
         yx[0] = recover_fast(accx[tt][0], cthx.x, czx.x, rx.ztx, rx.sigx, cix.x, rx.iqx);
         yx[1] = recover_fast(accx[tt][1], cthx.y, czx.y, rx.ztx, rx.sigx, cix.y, rx.iqx);
@@ -419,30 +445,15 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
                                        }))
         s_abort = 1;
     } else {
-      // E2 of step t-1: word i of a thread is row 4 i + tid / 128, word
-      // tid % 128 (a row has at most 128); sums of (row tid / 16, tile tid % 16)
-      const uint64_t *e2 = E(t - 1);
-      const uint64_t *e2c = e2 + L::e2c, *e2s = e2 + L::e2s;
-      const int cw = ldH / 4;
-      constexpr int CW = bX / 4;
-      constexpr int rs4 = 4 * kXsTiles * uw, ls4 = 4 * ldsX;
-      uint32_t need = 0;
-#pragma unroll
-      for (int k = 0; k < CW; ++k)
-        if (4 * k + (tid >> 7) < nb && (tid & 127) < cw) need |= 1u << k;
-      if (tid < nb * kXsTiles) need |= 1u << CW;
-      if (!poll_to_lds<CW + 1>(
-              need, (uint32_t)t,
-              [&](int i, int th) -> const uint64_t * {
-                return i < CW ? e2c + i * rs4 + (th >> 7) * (rs4 / 4) + (th & 127) : e2s + th;
-              },
-              [&](int i, int th) -> uint32_t * {
-                return reinterpret_cast<uint32_t *>(
-                    i < CW ? xh + i * ls4 + (th >> 7) * ldsX + 4 * (th & 127) : (int8_t *)(ssum + th));
-              },
-              flag))
-        s_abort = 1;
+      if (!poll_to_lds_finish<CW + 1>(need, (uint32_t)t, w2, e2src, e2dst, flag)) s_abort = 1;
     }
+    // (on both paths: nothing of the step's first round stays in flight)
+    wait_vmcnt0();
+    // the arrival count of x_{t+2}, read now so that it is in hand when its
+    // loads are issued (step 8)
+    unsigned seen = 0;
+    if (l > 0 && t + 2 < T)
+      seen = __hip_atomic_load(ctr(l - 1, (t + 2) & 1, g), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (s_abort) return;
     if (t > 0) {
@@ -598,14 +609,8 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
     __syncthreads();
     if (s_abort) return;
 
-    // ---- 6. x_{t+1} (loaded a step ago) into LDS for the next step; the
-    // loads of x_{t+2} issued, to land during the step after; then the
-    // arrival that tells layer l+1 step t-1 is out (issued last: nothing
-    // below waits for it before the next step's poll)
-    if (t + 1 < T) park_x();
-    if (t + 2 < T) load_x(t + 2, seen);
-    if (t > 0 && tid == 0)
-      __hip_atomic_fetch_add(ctr(l, (t - 1) & 1, g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // ---- 6. x_{t+1} (loaded a step ago) into the LDS buffer of the next step
+    if (t + 1 < T) park_x((int)((t + 1) & 1));
 
     // ---- 7. E2: the tile's cells of h_t encoded (eq. 2), with per-row sums
 #pragma unroll
@@ -632,6 +637,11 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
       sum = red8(sum, AddI{});
       if (row < nb && wd == 0) put_word(e + L::e2s + row * kXsTiles + ct, tag, (uint32_t)sum);
     }
+    // ---- 8. the loads of x_{t+2} issued, to land during the next step; then
+    // the arrival that tells layer l+1 step t-1 is out
+    if (t + 2 < T) load_x(t + 2, seen);
+    if (t > 0 && tid == 0)
+      __hip_atomic_fetch_add(ctr(l, (t - 1) & 1, g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
