@@ -35,11 +35,11 @@ FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=4.47e+09, read=2.994e+09, written=1.476e+09,
+TRAFFIC = dict(bytes=3.412e+08, read=1.675e+08, written=1.737e+08,
                sources=("ql_stack.hip", "ql_xstack.hip", "ql_xcd.h", "ql_rec_common.h",
                         "ql_device.h", "ql_exchange.h", "ql_launch.h"),
-               sha256="3f64d75e66db12695e28ef7e92486c916181ee91003d4bfa0bb09adcf6410fa9",
-               summary="profiles/k_stack_5x500_B64_T1000_counters.md")
+               sha256="72ea34a74b76964b069b4fb5ec649c88189504905761a65f9b8b5fe5be26c004",
+               summary="profiles/k_xstack_5x500_B64_T1000_counters.md")
 
 
 def measured_traffic():
