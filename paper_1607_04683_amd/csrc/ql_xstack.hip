@@ -303,39 +303,60 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
   // its cells, from the codes of h_tx in LDS; tile 0 also the rows' z, 1/Q
   // and code sums from their row params), with device-coherent stores, for
   // layer l+1 on another XCD; taps of the codes.
+  // What publish_out needs on every step, held in vector registers like the
+  // above: this thread's word of 4 codes (row tid / 8, word tid % 8 of the
+  // tile's 32 cells) and, in tile 0, its row's params.
+  const int orw = tid0 >> 3, oww = tid0 & 7;
+  const bool ocode = orw < nb && j0 + 4 * oww < ldH;
+  const int oxh = orw * ldsX + (int)j0 + 4 * oww;
+  uint32_t *ocp = reinterpret_cast<uint32_t *>(Ly.out.codes + (b0 + orw) * Ly.out.ld + j0) + oww;
+  int64_t ostep = B * Ly.out.ld / 4;  // 4-byte words from frame t to t + 1
+  asm volatile("" : "+v"(ostep));
+  const bool ometa = ct == 0 && tid0 < nb;
+  int32_t *ozp = Ly.out.zero + b0 + tid0;
+  float *oqp = Ly.out.inv_q + b0 + tid0;
+  int32_t *osp = Ly.out.sums + b0 + tid0;
+  // (the last tile zeroes the rows' padding up to the output's stride; taps)
+  const bool orare = (ct == kXsTiles - 1 && Ly.out.ld > ldH) || Ly.tap_codes || Ly.tap_zero ||
+                     Ly.tap_inv_q;
+  // This tile's part of the layer's quantized output of step tx (codes of
+  // its cells, from the codes of h_tx in LDS; tile 0 also the rows' z, 1/Q
+  // and code sums from their row params), with device-coherent stores, for
+  // layer l+1 on another XCD; taps of the codes.
   auto publish_out = [&](int64_t tx) {
-    auto &a = kp->a;
-    auto &tl = kp->tl;
-    XS_SCALARS(a, tl, role);
-    const int tid = threadIdx.x;
-    const int64_t orow0 = tx * B + b0;
-    if (ct == 0 && tid < nb) {
-      const RowParam r = rph[tid];
-      st_coherent_i(&Ly.out.zero[orow0 + tid], r.z);
-      st_coherent(&Ly.out.inv_q[orow0 + tid], r.iqx);
-      st_coherent_i(&Ly.out.sums[orow0 + tid], r.sum);
-      if (Ly.tap_zero) Ly.tap_zero[orow0 + tid] = r.z;
-      if (Ly.tap_inv_q) Ly.tap_inv_q[orow0 + tid] = r.iqx;
+    if (ometa) {
+      const RowParam r = rph[threadIdx.x];
+      const int64_t o = tx * xB;
+      st_coherent_i(ozp + o, r.z);
+      st_coherent(oqp + o, r.iqx);
+      st_coherent_i(osp + o, r.sum);
     }
-    // 8 words of 4 codes per row; the last tile also zeroes the row's
-    // padding up to the output's stride
-    const int orow = tid >> 3, w = tid & 7;
-    if (orow < nb && j0 + 4 * w < ldH) {
-      const uint32_t v = *reinterpret_cast<const uint32_t *>(xh + orow * ldsX + j0 + 4 * w);
-      __hip_atomic_store(reinterpret_cast<uint32_t *>(Ly.out.codes + (orow0 + orow) * Ly.out.ld + j0) + w,
-                         v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (ocode)
+      __hip_atomic_store(ocp + tx * ostep, *reinterpret_cast<const uint32_t *>(xh + oxh),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (orare) {
+      auto &a = kp->a;
+      auto &tl = kp->tl;
+      XS_SCALARS(a, tl, role);
+      const int tid = threadIdx.x;
+      const int64_t orow0 = tx * B + b0;
+      if (ct == 0 && tid < nb) {
+        const RowParam r = rph[tid];
+        if (Ly.tap_zero) Ly.tap_zero[orow0 + tid] = r.z;
+        if (Ly.tap_inv_q) Ly.tap_inv_q[orow0 + tid] = r.iqx;
+      }
+      if (ct == kXsTiles - 1)
+        for (int idx = tid; idx < nb * (int)((Ly.out.ld - ldH) / 4); idx += kXsThreads) {
+          const int nw = (int)((Ly.out.ld - ldH) / 4), r2 = idx / nw, w2 = idx % nw;
+          __hip_atomic_store(reinterpret_cast<uint32_t *>(Ly.out.codes + (orow0 + r2) * Ly.out.ld + ldH) + w2,
+                             0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      if (Ly.tap_codes)
+        for (int idx = tid; idx < nb * u; idx += kXsThreads) {
+          const int r2 = idx / u, k = idx % u;
+          if (j0 + k < H) Ly.tap_codes[(orow0 + r2) * H + j0 + k] = xh[r2 * ldsX + j0 + k];
+        }
     }
-    if (ct == kXsTiles - 1)
-      for (int idx = tid; idx < nb * (int)((Ly.out.ld - ldH) / 4); idx += kXsThreads) {
-        const int nw = (int)((Ly.out.ld - ldH) / 4), r2 = idx / nw, w2 = idx % nw;
-        __hip_atomic_store(reinterpret_cast<uint32_t *>(Ly.out.codes + (orow0 + r2) * Ly.out.ld + ldH) + w2,
-                           0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    if (Ly.tap_codes)
-      for (int idx = tid; idx < nb * u; idx += kXsThreads) {
-        const int r2 = idx / u, k = idx % u;
-        if (j0 + k < H) Ly.tap_codes[(orow0 + r2) * H + j0 + k] = xh[r2 * ldsX + j0 + k];
-      }
   };
   // the weight fragments have landed before the loop (no wait for them in it);
   // x_0 goes to LDS, x_1 into registers
@@ -586,11 +607,27 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
       // every row's params from the 16 tiles' parts: 16 lanes per row, one
       // tile's (min, max) words each
       const int row = tid >> 4, j = tid & 15;
-      uint32_t v[2];
+      uint32_t v[2] = {0u, 0u};
       const uint32_t need = row < nb ? 3u : 0u;
       const uint64_t *e1 = e + L::e1 + (row * kXsTiles + j) * 2;
-      const bool ok = poll_words<2>(need, tag, v, [&](int i) -> const uint64_t * { return e1 + i; },
-                                    flag);
+      uint64_t w1[2] = {0, 0};
+      if (need) {
+        w1[0] = ld_tagged(e1);
+        w1[1] = ld_tagged(e1 + 1);
+      }
+      // ---- 6. x_{t+1} (loaded a step ago) into the LDS buffer of the next
+      // step, while these loads are in flight
+      if (t + 1 < T) park_x((int)((t + 1) & 1));
+      uint32_t left = need;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (((left >> i) & 1u) && (uint32_t)(w1[i] >> 32) == tag) {
+          v[i] = (uint32_t)w1[i];
+          left &= ~(1u << i);
+        }
+      bool ok = true;
+      if (__any(left != 0))
+        ok = poll_words<2>(left, tag, v, [&](int i) -> const uint64_t * { return e1 + i; }, flag);
       if (!ok) s_abort = 1;
       int lo = red16(need ? (int)v[0] : 0x7fffffff, MinI{});
       int hi = red16(need ? (int)v[1] : 0x7fffffff, MinI{});
@@ -608,9 +645,6 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (s_abort) return;
-
-    // ---- 6. x_{t+1} (loaded a step ago) into the LDS buffer of the next step
-    if (t + 1 < T) park_x((int)((t + 1) & 1));
 
     // ---- 7. E2: the tile's cells of h_t encoded (eq. 2), with per-row sums
 #pragma unroll
