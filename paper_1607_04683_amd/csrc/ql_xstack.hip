@@ -97,10 +97,11 @@ struct XsKArgs {
 };
 typedef const __attribute__((address_space(4))) XsKArgs *XsKArgPtr;
 
-// What a workgroup derives from the launch's scalars and its role.  The
-// kernel states it once for the prologue and again at the top of every
-// step, reading the arguments through a pointer the compiler cannot follow
-// across steps, so that none of these values stays live across the loop.
+// What a workgroup derives from the launch's scalars and its role: stated
+// once for the kernel, and again (through the kernel-argument pointer) on the
+// rare output path of the step.  What the step needs on every step (the x
+// and output addresses) is held in vector registers instead, so that no
+// scalar reload sits on the step's chain.
 #define XS_SCALARS(a, tl, role)                                                                 \
   const int l = (role) / kXsSlots, s = (role) % kXsSlots;                                      \
   const int g = s / kXsTiles, ct = s % kXsTiles;                                               \
@@ -358,6 +359,8 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
         }
     }
   };
+  float *hout = Ly.h;
+  asm volatile("" : "+v"(hout));
   // the weight fragments have landed before the loop (no wait for them in it);
   // x_0 goes to LDS, x_1 into registers
   wait_vmcnt0();
@@ -366,11 +369,6 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
   if (T > 1) load_x(1, 0u);
   __syncthreads();
   for (int64_t t = 0;; ++t) {
-    // the launch's scalars and the per-thread indices re-derived every step
-    asm volatile("" : "+s"(kp));
-    auto &a = kp->a;
-    auto &tl = kp->tl;
-    XS_SCALARS(a, tl, role);
     int tid = (int)threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, wave = tid >> 6, fr = lane & 15, fq = lane >> 4;
@@ -477,17 +475,18 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
       seen = __hip_atomic_load(ctr(l - 1, (t + 2) & 1, g), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (s_abort) return;
-    if (t > 0) {
-      // the row params of h_{t-1}: the quantizer of step t-1 and the row's
-      // code sum over the 16 tiles
+    // the row params of h_{t-1}: the quantizer of step t-1 and the row's code
+    // sum over the 16 tiles (formed while the MFMAs of step 3 run)
+    auto build_rph = [&]() {
       const int row = tid >> 4, og = tid & 15;
       const int total = red16(row < nb ? ssum[row * kXsTiles + og] : 0, AddI{});
       if (row < nb && og == 0) {
         const XParam xp = hp[row];
         rph[row] = row_param(xp.z, xp.inv_q, total, (int)H);
       }
-    }
+    };
     if (t == T) {
+      build_rph();
       // the last step's output, and the arrival once its stores have completed
       __syncthreads();
       publish_out(t - 1);
@@ -509,6 +508,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
         acch[tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
             wh[c], *reinterpret_cast<const v4i *>(xh + (16 * tt + fr) * ldsX + c * 64 + 16 * fq),
             acch[tt], 0, 0, 0);
+    if (t > 0) build_rph();
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acch[0]), "+v"(acch[NT - 1]));
     __syncthreads();  // the row params of h_{t-1} are in LDS
     // this tile's part of the layer's quantized output of step t-1, across
@@ -549,7 +549,7 @@ __global__ __launch_bounds__(kXsThreads) void k_xstack(StackArgs a, XsTiling tl)
         const float m = gv[3] * tanh_cw(cn);
         hv[tt] = m;
         if (jL < H && lb < nb) {
-          if (Ly.h) Ly.h[(t * B + brow) * H + jL] = m;
+          if (hout) hout[(t * B + brow) * H + jL] = m;
           if (TP) {
             if (Ly.acc_h)
 #pragma unroll
