@@ -35,10 +35,10 @@ FP32_PEAK_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 # --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain
 # 1 GiB copy; valid only for the kernel sources with this digest (any edit
 # makes it stale -> null).
-TRAFFIC = dict(bytes=3.412e+08, read=1.675e+08, written=1.737e+08,
+TRAFFIC = dict(bytes=3.4146e+08, read=1.6776e+08, written=1.7371e+08,
                sources=("ql_stack.hip", "ql_xstack.hip", "ql_xcd.h", "ql_rec_common.h",
                         "ql_device.h", "ql_exchange.h", "ql_launch.h"),
-               sha256="72ea34a74b76964b069b4fb5ec649c88189504905761a65f9b8b5fe5be26c004",
+               sha256="0dec05fd50f7ed0487cf1bb21fa55bb7691a9dbcff5dba8e0caaf48345ffe611",
                summary="profiles/k_xstack_5x500_B64_T1000_counters.md")
 
 
