@@ -193,6 +193,7 @@ def test_model_5x500_softmax8192_T1000_B64_sampled(ql, orc):
     from paper_1607_04683_amd.workloads import LSTM5x500_S8192_T1000_B64 as W_, model_weights, features
     w = model_weights(W_)[0]
     assert ql.stack_layers_per_launch(ql.quantize_model(w), W_.T, W_.B) == 5
+    assert ql.stack_layout(ql.quantize_model(w), W_.T, W_.B) == 1  # one XCD per layer
     _model_case(ql, orc, w, features(W_), utts=B64_UTTS, taps=True)
 
 
