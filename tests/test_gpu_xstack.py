@@ -6,8 +6,8 @@ and each layer's quantized output crosses to the next XCD.  Every tap of
 every layer (input and recurrent sums, codes, row params, fp32 h, gates, c)
 is compared with the oracle bit for bit on ragged shapes: the smallest and
 largest batch, odd batches (the second row group one row short), cell counts
-that leave tiles without cells, the widest input and cell count, and the
-most layers one launch holds."""
+that leave tiles without cells, the widest input and cell count, the most
+layers one launch holds, and sequences of one and two frames."""
 import numpy as np
 import pytest
 import torch
@@ -32,6 +32,8 @@ CASES = [
     (2, 512, 512, 4, 64),    # the widest input and cell count at full batch
     (3, 320, 500, 4, 64),    # the 5 x 500 model's widths
     (4, 70, 36, 7, 47),      # 36 cells: one full tile and one with 4 cells
+    (3, 40, 48, 1, 20),      # one frame: x_1 never loaded, the last output at once
+    (2, 24, 64, 2, 64),      # two frames: x_2 never loaded
 ]
 
 
